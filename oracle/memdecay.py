@@ -1,0 +1,294 @@
+"""Plain CPU oracle of MemDecay's observation step (Sec. III, Alg. 1).
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the package entry's smoke
+check and the benchmark's CPU-baseline leg may import this module.  The
+device path never calls it and shares no code with it.
+
+Arithmetic is float64 throughout.  Keys arrive as bfloat16 bits and are
+widened exactly; queries arrive as float32 and are widened exactly; the
+region tables arrive as float32 and are widened exactly.  Sessions are
+independent, and each one is a list of pages in logical (insertion) order.
+A page has a serial number (opening order, never reused) and its member
+token slots.  The one decode step of ``Session.step`` takes the paper's
+steps in the paper's order:
+
+  append   the step's new token joins the tail page, or opens a page
+  O2/O3    attention of the decode query against every cached key, per
+           layer and query head, softmax over the cached tokens, averaged
+           over heads and layers: the attention mass A_i   (Sec. III-C)
+  O4       EWMA of the importance a_i                      (Eq. 2)
+  O5       refresh clock: t_ref_i <- t when A_i >= tau     (Eq. 3)
+  O6       retention score s_i                              (Eq. 4)
+  O7       page score S_p, mean over live members           (Eq. 5)
+  O8       when |K_t| > B: evict non-pinned pages in ascending S_p until
+           the budget holds                                 (Sec. III-D, Alg. 1)
+  O9       drop the evicted pages
+
+Readings where the paper leaves a choice (listed with their reasons in the
+design notes of the repository):
+  * one observation per decode step and a window of one query (k = 1, W = 1);
+  * the mass averages over all L*Hq query heads; query head h reads KV head
+    h // (Hq/Hkv); scale 1/sqrt(d); no mask over the cached tokens; the new
+    token attends to itself;
+  * a new token starts with a = 0 and its own observation applies at once;
+  * refresh compares this step's raw A_i with tau = tau_scale / |K_t|, where
+    |K_t| counts the cached tokens after the append and before eviction;
+  * pinned tokens (region in the pin mask) still get EWMA and refresh but
+    score +inf; a page with any pinned member is pinned (+inf);
+  * |p| in the page mean is the number of live members;
+  * ties in S_p go to the smaller serial (the older page first);
+  * if the pinned tokens alone exceed B, every unpinned page is evicted and
+    the session is flagged infeasible.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+
+def widen_bf16(bits) -> np.ndarray:
+    """bfloat16 bit patterns (uint16) -> float32 values, exactly."""
+    b = np.asarray(bits, dtype=np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def softmax(x: np.ndarray) -> np.ndarray:
+    """Textbook softmax of a 1-D float64 vector (shifted by its maximum)."""
+    e = np.exp(x - np.max(x))
+    return e / np.sum(e)
+
+
+@dataclass
+class Page:
+    serial: int
+    slots: List[int]
+
+
+@dataclass
+class StepRecord:
+    """What one observation step produced, in the session's logical order
+    (tokens are listed page by page, as the pages stood after the append)."""
+    t: int
+    n: int                       # |K_t| after the append, before eviction
+    tau: float
+    page_serial: np.ndarray      # [m] serials of the pages scored
+    page_size: np.ndarray        # [m] live members per page
+    page_pinned: np.ndarray      # [m] bool
+    page_score: np.ndarray       # [m] S_p (+inf for pinned pages)
+    abar: np.ndarray             # [n] attention mass A_i
+    a: np.ndarray                # [n] importance after the EWMA
+    t_ref: np.ndarray            # [n] refresh clock after this step
+    region: np.ndarray           # [n]
+    score: np.ndarray            # [n] s_i (+inf for pinned tokens)
+    evicted: np.ndarray          # serials evicted this step, ascending
+    n_after: int
+    infeasible: bool
+
+
+class Session:
+    """One agent session's cache and MemDecay state."""
+
+    def __init__(self, *, L: int, Hq: int, Hkv: int, d: int, P: int,
+                 b: Sequence[float], lam: Sequence[float], alpha: float,
+                 rho: float, tau_scale: float, pinned_mask: int, budget: int,
+                 clock: int, region, keys_bits, t_ins=None, t_ref=None, a=None,
+                 page_sizes: Optional[Sequence[int]] = None,
+                 page_serials: Optional[Sequence[int]] = None,
+                 next_serial: Optional[int] = None, capacity: Optional[int] = None):
+        if Hq % Hkv:
+            raise ValueError("query heads must be a multiple of KV heads")
+        self.L, self.Hq, self.Hkv, self.d, self.P = L, Hq, Hkv, d, P
+        self.G = Hq // Hkv
+        self.b = np.asarray(b, dtype=np.float64)
+        self.lam = np.asarray(lam, dtype=np.float64)
+        self.alpha, self.rho, self.tau_scale = float(alpha), float(rho), float(tau_scale)
+        self.pinned_mask = int(pinned_mask)
+        self.budget = int(budget)
+        self.t = int(clock)
+
+        region = np.asarray(region, dtype=np.int64)
+        n = region.shape[0]
+        cap = n if capacity is None else max(int(capacity), n)
+        # Slot store: slot j holds one token's state; keys layer-major
+        # [L][Hkv][slot][d] as float32 (bf16 values are exact in float32).
+        self.region = np.zeros(cap, dtype=np.int64)
+        self.t_ins = np.zeros(cap, dtype=np.int64)
+        self.t_ref = np.zeros(cap, dtype=np.int64)
+        self.a = np.zeros(cap, dtype=np.float64)
+        self.keys = np.zeros((L, Hkv, cap, d), dtype=np.float32)
+        self.n_slots = n
+        self.region[:n] = region
+        self.t_ins[:n] = np.arange(n) if t_ins is None else np.asarray(t_ins)
+        self.t_ref[:n] = self.t_ins[:n] if t_ref is None else np.asarray(t_ref)
+        if a is not None:
+            self.a[:n] = np.asarray(a, dtype=np.float64)
+        kb = np.asarray(keys_bits, dtype=np.uint16).reshape(n, L, Hkv, d)
+        self.keys[:, :, :n, :] = widen_bf16(kb).transpose(1, 2, 0, 3)
+
+        if page_sizes is None:
+            page_sizes = [min(P, n - i) for i in range(0, n, P)]
+        if sum(page_sizes) != n or any(not 1 <= s <= P for s in page_sizes):
+            raise ValueError("page sizes must be in [1, P] and cover the tokens")
+        if page_serials is None:
+            page_serials = list(range(len(page_sizes)))
+        self.pages: List[Page] = []
+        pos = 0
+        for ser, sz in zip(page_serials, page_sizes):
+            self.pages.append(Page(int(ser), list(range(pos, pos + sz))))
+            pos += sz
+        self.next_serial = (max(page_serials) + 1 if page_serials else 0) \
+            if next_serial is None else int(next_serial)
+
+    # ------------------------------------------------------------ helpers
+    def live(self) -> np.ndarray:
+        """Slot ids of the cached tokens in logical order."""
+        if not self.pages:
+            return np.zeros(0, dtype=np.int64)
+        return np.concatenate([np.asarray(p.slots, dtype=np.int64) for p in self.pages])
+
+    def n_tokens(self) -> int:
+        return sum(len(p.slots) for p in self.pages)
+
+    def is_pinned_region(self, r) -> np.ndarray:
+        return ((self.pinned_mask >> np.asarray(r, dtype=np.int64)) & 1).astype(bool)
+
+    def _grow(self, need: int):
+        cap = self.region.shape[0]
+        if need <= cap:
+            return
+        new = max(need, 2 * cap)
+        for name in ("region", "t_ins", "t_ref"):
+            arr = getattr(self, name)
+            setattr(self, name, np.concatenate([arr, np.zeros(new - cap, dtype=arr.dtype)]))
+        self.a = np.concatenate([self.a, np.zeros(new - cap)])
+        k = np.zeros((self.L, self.Hkv, new, self.d), dtype=np.float32)
+        k[:, :, :cap, :] = self.keys
+        self.keys = k
+
+    # ------------------------------------------------------------ steps
+    def append(self, key_bits, region: int):
+        """The decode engine caches the step's token (Fig. 1 'append KV')."""
+        j = self.n_slots
+        self._grow(j + 1)
+        self.n_slots += 1
+        self.region[j] = int(region)
+        self.t_ins[j] = self.t
+        self.t_ref[j] = self.t
+        self.a[j] = 0.0
+        self.keys[:, :, j, :] = widen_bf16(key_bits).reshape(self.L, self.Hkv, self.d)
+        if self.pages and len(self.pages[-1].slots) < self.P:
+            self.pages[-1].slots.append(j)
+        else:
+            self.pages.append(Page(self.next_serial, [j]))
+            self.next_serial += 1
+
+    def attention_mass(self, q, live: np.ndarray) -> np.ndarray:
+        """A_i: softmax attention of the decode query, averaged over the L*Hq
+        query heads (Sec. III-C, window of one query)."""
+        q = np.asarray(q, dtype=np.float32).astype(np.float64).reshape(self.L, self.Hq, self.d)
+        n = live.shape[0]
+        mass = np.zeros(n, dtype=np.float64)
+        inv_sqrt_d = 1.0 / math.sqrt(self.d)
+        for l in range(self.L):
+            for kv in range(self.Hkv):
+                k = self.keys[l, kv][live].astype(np.float64)          # [n][d]
+                heads = range(kv * self.G, (kv + 1) * self.G)
+                x = (k @ q[l, kv * self.G:(kv + 1) * self.G].T) * inv_sqrt_d   # [n][G]
+                for j, h in enumerate(heads):
+                    mass += softmax(x[:, j])
+        return mass / (self.L * self.Hq)
+
+    def step(self, q, new_key_bits=None, new_region: Optional[int] = None) -> StepRecord:
+        """One observation step at the next clock value (Alg. 1)."""
+        self.t += 1
+        t = self.t
+        if new_key_bits is not None:
+            self.append(new_key_bits, new_region)
+        live = self.live()
+        n = live.shape[0]
+        m = len(self.pages)
+        empty = np.zeros(0)
+        if n == 0:
+            return StepRecord(t, 0, math.inf, np.zeros(0, np.int64), np.zeros(0, np.int64),
+                              np.zeros(0, bool), empty, empty, empty, np.zeros(0, np.int64),
+                              np.zeros(0, np.int64), empty, np.zeros(0, np.int64), 0, False)
+
+        # O2-O3: attention mass.
+        abar = self.attention_mass(q, live)
+        # O4: EWMA over every cached token, pinned included (Eq. 2).
+        self.a[live] = self.rho * self.a[live] + (1.0 - self.rho) * abar
+        # O5: refresh clock (Eq. 3), threshold scaled to the uniform level.
+        tau = self.tau_scale / n
+        refreshed = live[abar >= tau]
+        self.t_ref[refreshed] = t
+        # O6: retention score (Eq. 4); pinned tokens bypass scoring.
+        r = self.region[live]
+        dt = (t - self.t_ref[live]).astype(np.float64)
+        score = self.b[r] * np.exp(-self.lam[r] * dt) + self.alpha * self.a[live]
+        pinned_tok = self.is_pinned_region(r)
+        score = np.where(pinned_tok, np.inf, score)
+        # O7: page score (Eq. 5), mean over the page's live members.
+        sizes = np.array([len(p.slots) for p in self.pages], dtype=np.int64)
+        serials = np.array([p.serial for p in self.pages], dtype=np.int64)
+        bounds = np.concatenate([[0], np.cumsum(sizes)])
+        page_pinned = np.zeros(m, dtype=bool)
+        page_score = np.zeros(m, dtype=np.float64)
+        for i in range(m):
+            seg = slice(bounds[i], bounds[i + 1])
+            page_pinned[i] = bool(np.any(pinned_tok[seg]))
+            page_score[i] = np.inf if page_pinned[i] else float(np.sum(score[seg])) / sizes[i]
+        # O8: budget-aware page eviction (Alg. 1, min-heap order).
+        evicted, n_after, infeasible = select_pages(page_score, serials, sizes,
+                                                    page_pinned, n, self.budget)
+        # O9: drop the evicted pages (irreversible, Sec. III-E).
+        if evicted.size:
+            gone = set(int(x) for x in evicted)
+            self.pages = [p for p in self.pages if p.serial not in gone]
+        return StepRecord(t, n, tau, serials, sizes, page_pinned, page_score, abar,
+                          self.a[live].copy(), self.t_ref[live].copy(), r.copy(), score,
+                          evicted, n_after, infeasible)
+
+    # ------------------------------------------------------------ views
+    def state(self):
+        """Per-page view: list of (serial, region[], t_ins[], t_ref[], a[])."""
+        out = []
+        for p in self.pages:
+            s = np.asarray(p.slots, dtype=np.int64)
+            out.append((p.serial, self.region[s].copy(), self.t_ins[s].copy(),
+                        self.t_ref[s].copy(), self.a[s].copy()))
+        return out
+
+
+def select_pages(page_score, serials, sizes, pinned, n: int, budget: int):
+    """Greedy page eviction (Alg. 1): while |K| > B, evict the non-pinned page
+    of smallest (S_p, serial).  Returns (evicted serials ascending, n after,
+    infeasible flag)."""
+    evicted = []
+    if n > budget:
+        cand = [i for i in range(len(serials)) if not pinned[i]]
+        cand.sort(key=lambda i: (page_score[i], serials[i]))
+        for i in cand:
+            if n <= budget:
+                break
+            evicted.append(int(serials[i]))
+            n -= int(sizes[i])
+    infeasible = n > budget
+    return np.array(sorted(evicted), dtype=np.int64), n, infeasible
+
+
+def session_from_workload(w, session: int, *, region, keys_bits, b, lam, budget,
+                          alpha=None, rho=None, tau_scale=None, capacity=None) -> Session:
+    """A session at the start of decoding: prefix token i has t_ins = t_ref = i,
+    importance 0, and the clock stands at n0 (so decode step k runs at
+    t = n0 + k)."""
+    n0 = int(np.asarray(region).shape[0])
+    return Session(L=w.L, Hq=w.Hq, Hkv=w.Hkv, d=w.d, P=w.P, b=b, lam=lam,
+                   alpha=w.alpha if alpha is None else alpha,
+                   rho=w.rho if rho is None else rho,
+                   tau_scale=w.tau_scale if tau_scale is None else tau_scale,
+                   pinned_mask=w.pinned_mask, budget=budget, clock=n0,
+                   region=region, keys_bits=keys_bits,
+                   capacity=capacity if capacity is not None else n0 + w.steps)
