@@ -1,0 +1,214 @@
+/*
+ * memdecay.h — C ABI of the MemDecay retention hot path on one AMD Instinct
+ * MI355X (gfx950).
+ *
+ * MemDecay ("Region-Aware KV Cache Eviction for Efficient LLM Agent
+ * Inference", Sec. III) keeps, for every cached token i of an agent
+ * session, a region label r(i), an insertion step, an attention importance
+ * a_i (Eq. 2) and a refresh clock t_ref_i (Eq. 3).  At each observation
+ * step it scores tokens with s_i = b_r exp(-lambda_r (t - t_ref_i)) + alpha
+ * a_i (Eq. 4), averages scores per page (Eq. 5) and, when the session holds
+ * more than its budget B, evicts non-pinned pages in ascending page score
+ * until the budget holds (Sec. III-D, Alg. 1).  This library runs one such
+ * step per call sequence
+ *
+ *     md_observe_step  ->  md_score_pages  ->  md_select_evict  ->  md_compact
+ *
+ * over a batch of independent sessions whose keys live in a paged bf16 pool.
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ *  * All array arguments are DEVICE pointers into memory the caller owns
+ *    (allocated with hipMalloc or by a framework on the same device).  The
+ *    library never frees them.  Only md_init's struct arguments and the
+ *    host_out of md_read_device_status are host pointers.
+ *  * Every call enqueues work on the stream given to md_init and returns
+ *    without synchronising, except md_init (which validates the region tables
+ *    on the host) and md_read_device_status.
+ *  * Negative return values are errors detected on the host before anything
+ *    was enqueued; the session state is unchanged.  Conditions only the
+ *    device can see (free list empty, non-finite query) set bits in a device
+ *    status word read by md_read_device_status.
+ *  * A handle is not thread-safe; calls on one handle must be serialised.
+ *  * Physical page ids handed out by the free list depend on scheduling; all
+ *    scores, selections and logical page orders are deterministic.
+ *
+ * Layouts (S = max_sessions, NP = n_phys_pages, P = page_size, MP = max_pages)
+ *  k_pool       uint16 bf16 bits [NP][L][Hkv][P][d]   keys of each physical page
+ *  region       uint8  [NP][P]   region code of each slot
+ *  t_ins, t_ref int32  [NP][P]   insertion step, refresh clock of each slot
+ *  importance   float  [NP][P]   a_i of each slot
+ *  page_table   int32  [S][MP]   physical page ids in logical order
+ *  page_serial  int32  [S][MP]   opening serial of each listed page (ascending)
+ *  n_pages, n_tokens, clock, next_serial, budget   int32 [S]
+ *  free_list    int32  [NP]      stack of free physical ids; free_count int32 [1]
+ * Every page of a session except the last holds exactly P live tokens; the
+ * last holds n_tokens - (n_pages - 1) * P.  Region codes follow the paper's
+ * label list: system 0, plan 1, user 2, tool_in 3, tool_out 4, retrieval 5,
+ * scratchpad 6.
+ */
+#ifndef MEMDECAY_H
+#define MEMDECAY_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MD_ABI_VERSION 1
+
+typedef int32_t md_status;
+
+enum {
+    MD_OK = 0,
+    MD_E_INVALID = -1,      /* null or misaligned pointer, bad value            */
+    MD_E_UNSUPPORTED = -2,  /* shape outside what the kernels are built for     */
+    MD_E_STEP = -3,         /* step did not advance by exactly one              */
+    MD_E_HIP = -4,          /* a HIP runtime call failed                        */
+    MD_E_STATE = -5,        /* call out of order (e.g. select before score)     */
+    MD_E_NOMEM = -6         /* scratch allocation failed in md_init             */
+};
+
+/* Bits of the device status word. */
+#define MD_DEV_CAPACITY   0x1   /* free list empty or page table full at append */
+#define MD_DEV_NONFINITE  0x2   /* NaN or infinity in a decode query            */
+#define MD_DEV_BAD_EVICT  0x4   /* md_compact got a serial the session lacks    */
+#define MD_DEV_CORRUPT    0x8   /* a session's counters, page table or region   */
+                                /* codes are out of range; the session is      */
+                                /* skipped for the step                         */
+
+typedef struct md_config {
+    int32_t n_layers;           /* L                                              */
+    int32_t n_q_heads;          /* Hq, a multiple of Hkv, Hq/Hkv <= 16            */
+    int32_t n_kv_heads;         /* Hkv                                            */
+    int32_t head_dim;           /* d; must be 128                                 */
+    int32_t page_size;          /* P; 16 or 64                                    */
+    int32_t max_sessions;       /* S, 1..1024                                     */
+    int32_t max_pages;          /* MP, page-table capacity per session            */
+    int32_t n_phys_pages;       /* NP, pages in the pool                          */
+    int32_t n_regions;          /* number of region codes, 1..32 (7 in the paper) */
+    uint32_t pinned_region_mask;/* bit r set => region r is pinned (Sec. III-A)   */
+    float rho;                  /* EWMA smoothing, 0 <= rho < 1 (Eq. 2)           */
+    float alpha;                /* attention weight, alpha >= 0 (Eq. 4)           */
+    float tau_scale;            /* tau = tau_scale / |K_t| (Eq. 3's scaled form)  */
+    int32_t reserved;           /* must be 0                                      */
+} md_config;
+
+/* Region priors (Sec. III-B): b_r >= 0 and lambda_r >= 0 per session and
+ * region, float32 device arrays [S][n_regions].  Read at every step. */
+typedef struct md_region_params {
+    const float* base_priority;  /* b      */
+    const float* decay_rate;     /* lambda */
+} md_region_params;
+
+typedef struct md_cache_view {
+    uint16_t* k_pool;
+    uint8_t*  region;
+    int32_t*  t_ins;
+    int32_t*  t_ref;
+    float*    importance;
+    int32_t*  page_table;
+    int32_t*  page_serial;
+    int32_t*  n_pages;
+    int32_t*  n_tokens;
+    int32_t*  clock;
+    int32_t*  next_serial;
+    int32_t*  budget;
+    int32_t*  free_list;
+    int32_t*  free_count;
+} md_cache_view;
+
+typedef struct md_handle_s* md_handle;
+
+/* Library ABI version (MD_ABI_VERSION of the build). */
+int32_t md_abi_version(void);
+
+/* Text for a status code (static storage; never NULL). */
+const char* md_status_str(md_status s);
+
+/*
+ * md_init — validate the configuration and buffers, allocate the library's
+ * own scratch (attention logits of one step, softmax statistics, page scores,
+ * work lists; sized from cfg), and bind everything to `stream` (a
+ * hipStream_t; NULL = the null stream) on the current device.
+ * Copies the region tables to the host once to check b >= 0, lambda >= 0 and
+ * finiteness (Sec. III-B).  On success *out holds a new handle; on failure
+ * *out is NULL and nothing is allocated.
+ */
+md_status md_init(const md_config* cfg, const md_region_params* rp,
+                  const md_cache_view* cv, void* stream, md_handle* out);
+
+/*
+ * md_observe_step — one observation step (Alg. 1, first two lines, with one
+ * observation per decode step and a window of one query):
+ *   append: each session's clock advances, t <- t + 1.  If new_k is not NULL
+ *     the step's token joins the session's last page, or a page popped from
+ *     the free list when the last page is full, with region new_region[s],
+ *     t_ins = t_ref = t, a = 0 (Fig. 1, the decode engine's append).
+ *   attention mass: for every cached token i, A_i = (1 / (L Hq)) sum over
+ *     layers l and query heads h of softmax_i(q_{l,h} . k_{l,h/G,i} / sqrt(d)),
+ *     the softmax running over the session's cached tokens (Sec. III-C).
+ *   EWMA (Eq. 2): a_i <- rho a_i + (1 - rho) A_i for every cached token.
+ *   refresh (Eq. 3): t_ref_i <- t when A_i >= tau_scale / |K_t|, |K_t| the
+ *     session's token count after the append.
+ * q:          float32 [S][L][Hq][d] decode queries (device).
+ * new_k:      bf16 bits [S][L][Hkv][d] keys of the appended tokens, or NULL.
+ * new_region: uint8 [S] region codes of the appended tokens; required with new_k.
+ * abar_out:   optional float32 [NP][P]; receives A_i at each live slot.
+ * step:       any value on the first call, then exactly the previous + 1
+ *             (MD_E_STEP otherwise, nothing enqueued).
+ */
+md_status md_observe_step(md_handle h, int32_t step, const float* q,
+                          const uint16_t* new_k, const uint8_t* new_region,
+                          float* abar_out);
+
+/*
+ * md_score_pages — retention scores and page scores (Alg. 1, lines 3-4):
+ *   s_i = b_{r(i)} exp(-lambda_{r(i)} (t - t_ref_i)) + alpha a_i    (Eq. 4)
+ *   S_p = (1/|p|) sum_{i in p} s_i over the page's live tokens      (Eq. 5)
+ * Pinned tokens bypass scoring (+INFINITY); a page with any pinned member
+ * is pinned and scores +INFINITY.
+ * page_score:  optional float32 [S][MP], logical page order.
+ * token_score: optional float32 [NP][P] at each live slot.
+ * The library keeps its own copy of the page scores for md_select_evict.
+ * Requires md_observe_step since the last md_compact (MD_E_STATE otherwise).
+ */
+md_status md_score_pages(md_handle h, float* page_score, float* token_score);
+
+/*
+ * md_select_evict — budget-aware page eviction (Alg. 1, lines 5-8): when a
+ * session holds n > B tokens (B = budget[s]), the shortest prefix of its
+ * non-pinned pages in ascending (S_p, serial) order whose removal leaves
+ * n <= B.  If even all non-pinned pages are not enough, all of them are
+ * selected and infeasible[s] = 1 (the pinned set alone exceeds B).
+ * evict_serial: int32 [S][MP]; row s receives evict_count[s] serials, ascending.
+ * evict_count:  int32 [S].   infeasible: uint8 [S].
+ * Mutates no session state; may be called again.  Requires md_score_pages
+ * since the last md_observe_step.
+ */
+md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_count,
+                          uint8_t* infeasible);
+
+/*
+ * md_compact — apply an eviction (Sec. III-E: irreversible): remove the
+ * listed pages from each session's page table and serial list keeping the
+ * order of the rest, update n_pages / n_tokens, and push the freed physical
+ * ids onto the free list.  evict_serial / evict_count have md_select_evict's
+ * layout and are normally its output; serials a session does not hold set
+ * MD_DEV_BAD_EVICT and are ignored.
+ */
+md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* evict_count);
+
+/* Synchronise the stream and copy the device status word to *host_out, then
+ * clear it.  Returns MD_E_HIP if the stream reports an error. */
+md_status md_read_device_status(md_handle h, int32_t* host_out);
+
+/* Release the scratch and the handle (synchronises the stream first). */
+md_status md_destroy(md_handle h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MEMDECAY_H */

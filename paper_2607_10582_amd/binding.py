@@ -1,0 +1,149 @@
+"""ctypes binding of libmemdecay.so: the C ABI's entry points under the same
+names, argument marshalling only.  Every step of the retention path runs in
+the library's HIP kernels; there is no fallback.  If the library is missing
+the first call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libmemdecay.so")
+
+MD_OK = 0
+MD_E_INVALID = -1
+MD_E_UNSUPPORTED = -2
+MD_E_STEP = -3
+MD_E_HIP = -4
+MD_E_STATE = -5
+MD_E_NOMEM = -6
+
+MD_DEV_CAPACITY = 0x1
+MD_DEV_NONFINITE = 0x2
+MD_DEV_BAD_EVICT = 0x4
+MD_DEV_CORRUPT = 0x8
+
+EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_observe_step",
+           "md_score_pages", "md_select_evict", "md_compact", "md_read_device_status",
+           "md_destroy")
+
+
+class md_config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("max_sessions", ctypes.c_int32),
+                ("max_pages", ctypes.c_int32), ("n_phys_pages", ctypes.c_int32),
+                ("n_regions", ctypes.c_int32), ("pinned_region_mask", ctypes.c_uint32),
+                ("rho", ctypes.c_float), ("alpha", ctypes.c_float),
+                ("tau_scale", ctypes.c_float), ("reserved", ctypes.c_int32)]
+
+
+class md_region_params(ctypes.Structure):
+    _fields_ = [("base_priority", ctypes.c_void_p), ("decay_rate", ctypes.c_void_p)]
+
+
+class md_cache_view(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "k_pool", "region", "t_ins", "t_ref", "importance", "page_table", "page_serial",
+        "n_pages", "n_tokens", "clock", "next_serial", "budget", "free_list", "free_count")]
+
+
+class MemDecayError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} failed: {status} ({md_status_str(status)})")
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libmemdecay.so (built by paper_2607_10582_amd.build)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it first "
+                           "(python -m paper_2607_10582_amd.build)")
+    lib = ctypes.CDLL(path)
+    vp, i32 = ctypes.c_void_p, ctypes.c_int32
+    lib.md_abi_version.restype = i32
+    lib.md_abi_version.argtypes = []
+    lib.md_status_str.restype = ctypes.c_char_p
+    lib.md_status_str.argtypes = [i32]
+    lib.md_init.restype = i32
+    lib.md_init.argtypes = [ctypes.POINTER(md_config), ctypes.POINTER(md_region_params),
+                            ctypes.POINTER(md_cache_view), vp, ctypes.POINTER(vp)]
+    lib.md_observe_step.restype = i32
+    lib.md_observe_step.argtypes = [vp, i32, vp, vp, vp, vp]
+    lib.md_score_pages.restype = i32
+    lib.md_score_pages.argtypes = [vp, vp, vp]
+    lib.md_select_evict.restype = i32
+    lib.md_select_evict.argtypes = [vp, vp, vp, vp]
+    lib.md_compact.restype = i32
+    lib.md_compact.argtypes = [vp, vp, vp]
+    lib.md_read_device_status.restype = i32
+    lib.md_read_device_status.argtypes = [vp, ctypes.POINTER(i32)]
+    lib.md_destroy.restype = i32
+    lib.md_destroy.argtypes = [vp]
+    _lib = lib
+    return lib
+
+
+def _check(fn: str, st: int) -> int:
+    if st < 0:
+        raise MemDecayError(fn, st)
+    return st
+
+
+def md_abi_version() -> int:
+    return load_library().md_abi_version()
+
+
+def md_status_str(status: int) -> str:
+    return load_library().md_status_str(status).decode()
+
+
+def md_init_raw(cfg: md_config, rp: md_region_params, cv: md_cache_view, stream: int):
+    """Returns (status, handle or None) without raising."""
+    h = ctypes.c_void_p()
+    st = load_library().md_init(ctypes.byref(cfg), ctypes.byref(rp), ctypes.byref(cv),
+                                ctypes.c_void_p(stream), ctypes.byref(h))
+    return st, (h.value if st == MD_OK else None)
+
+
+def md_init(cfg: md_config, rp: md_region_params, cv: md_cache_view, stream: int) -> int:
+    st, h = md_init_raw(cfg, rp, cv, stream)
+    _check("md_init", st)
+    return h
+
+
+def md_observe_step(h: int, step: int, q: int, new_k: int | None, new_region: int | None,
+                    abar_out: int | None = None) -> int:
+    return _check("md_observe_step", load_library().md_observe_step(
+        h, step, q, new_k or None, new_region or None, abar_out or None))
+
+
+def md_score_pages(h: int, page_score: int | None, token_score: int | None = None) -> int:
+    return _check("md_score_pages", load_library().md_score_pages(
+        h, page_score or None, token_score or None))
+
+
+def md_select_evict(h: int, evict_serial: int, evict_count: int, infeasible: int) -> int:
+    return _check("md_select_evict", load_library().md_select_evict(
+        h, evict_serial, evict_count, infeasible))
+
+
+def md_compact(h: int, evict_serial: int, evict_count: int) -> int:
+    return _check("md_compact", load_library().md_compact(h, evict_serial, evict_count))
+
+
+def md_read_device_status(h: int) -> int:
+    out = ctypes.c_int32(0)
+    _check("md_read_device_status", load_library().md_read_device_status(h, ctypes.byref(out)))
+    return out.value
+
+
+def md_destroy(h: int) -> int:
+    return _check("md_destroy", load_library().md_destroy(h))

@@ -1,0 +1,173 @@
+"""Caller-side buffers and a thin driver for the MemDecay C ABI.
+
+``PagedCache`` owns (through PyTorch) every device buffer of the library's
+cache view: the paged bf16 key pool, the per-slot side arrays (region,
+insertion step, refresh clock, importance), the page tables, the per-session
+counters and the free list.  ``MemDecay`` binds a cache to a library handle
+and calls the entry points in order.  PyTorch only allocates memory, places
+the initial prompt into the pool (the decode engine's prefill, not part of
+the retention step) and provides the stream; every step of the path runs in
+the library's kernels.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import binding as B
+
+
+class PagedCache:
+    """Device buffers of one batch of sessions (layouts as in memdecay.h)."""
+
+    def __init__(self, *, L: int, Hq: int, Hkv: int, d: int, P: int, S: int,
+                 max_pages: int, n_phys: int, device="cuda"):
+        self.L, self.Hq, self.Hkv, self.d, self.P = L, Hq, Hkv, d, P
+        self.S, self.max_pages, self.n_phys = S, max_pages, n_phys
+        self.device = torch.device(device)
+        dev = self.device
+        i32 = dict(dtype=torch.int32, device=dev)
+        # Slots past a session's token count are never used, so the pool is
+        # left uninitialised.
+        self.k_pool = torch.empty((n_phys, L, Hkv, P, d), dtype=torch.bfloat16, device=dev)
+        self.region = torch.zeros((n_phys, P), dtype=torch.uint8, device=dev)
+        self.t_ins = torch.zeros((n_phys, P), **i32)
+        self.t_ref = torch.zeros((n_phys, P), **i32)
+        self.importance = torch.zeros((n_phys, P), dtype=torch.float32, device=dev)
+        self.page_table = torch.full((S, max_pages), -1, **i32)
+        self.page_serial = torch.full((S, max_pages), -1, **i32)
+        self.n_pages = torch.zeros(S, **i32)
+        self.n_tokens = torch.zeros(S, **i32)
+        self.clock = torch.zeros(S, **i32)
+        self.next_serial = torch.zeros(S, **i32)
+        self.budget = torch.zeros(S, **i32)
+        self.free_list = torch.zeros(n_phys, **i32)
+        self.free_count = torch.zeros(1, **i32)
+
+    def view(self) -> B.md_cache_view:
+        v = B.md_cache_view()
+        for name in ("k_pool", "region", "t_ins", "t_ref", "importance", "page_table",
+                     "page_serial", "n_pages", "n_tokens", "clock", "next_serial", "budget",
+                     "free_list", "free_count"):
+            setattr(v, name, getattr(self, name).data_ptr())
+        return v
+
+    def load_session(self, s: int, keys: torch.Tensor, region, page_ids: Sequence[int],
+                     budget: int, clock: int, t_ins=None):
+        """Place a session's prompt: keys bf16 [n][L][Hkv][d] (device), region
+        codes [n], physical page ids in logical order (ceil(n / P) of them).
+        Token i gets t_ins = t_ref = t_ins[i] (default i) and importance 0."""
+        P = self.P
+        n = int(keys.shape[0])
+        m = (n + P - 1) // P
+        if len(page_ids) != m or m > self.max_pages:
+            raise ValueError("need ceil(n / P) page ids within max_pages")
+        ids = torch.as_tensor(np.asarray(page_ids, dtype=np.int64), device=self.device)
+        pad = m * P - n
+        k = keys.to(self.device, torch.bfloat16)
+        if pad:
+            k = torch.cat([k, torch.zeros((pad,) + tuple(k.shape[1:]), dtype=k.dtype, device=k.device)])
+        # [m][P][L][Hkv][d] -> [m][L][Hkv][P][d]
+        self.k_pool.index_copy_(0, ids, k.view(m, P, self.L, self.Hkv, self.d).permute(0, 2, 3, 1, 4))
+        reg = torch.as_tensor(np.asarray(region, dtype=np.uint8), device=self.device)
+        t0 = torch.arange(n, dtype=torch.int32, device=self.device) if t_ins is None else \
+            torch.as_tensor(np.asarray(t_ins, dtype=np.int32), device=self.device)
+        flat = (ids.view(-1, 1) * P + torch.arange(P, device=self.device).view(1, -1)).view(-1)[:n]
+        self.region.view(-1)[flat] = reg
+        self.t_ins.view(-1)[flat] = t0
+        self.t_ref.view(-1)[flat] = t0
+        self.importance.view(-1)[flat] = 0.0
+        self.page_table[s, :m] = ids.to(torch.int32)
+        self.page_table[s, m:] = -1
+        self.page_serial[s, :m] = torch.arange(m, dtype=torch.int32, device=self.device)
+        self.page_serial[s, m:] = -1
+        self.n_pages[s] = m
+        self.n_tokens[s] = n
+        self.clock[s] = clock
+        self.next_serial[s] = m
+        self.budget[s] = budget
+
+    def set_free_pages(self, ids: Sequence[int]):
+        """The free list: ids pop from the end."""
+        ids = np.ascontiguousarray(ids, dtype=np.int32)
+        self.free_list.zero_()
+        if ids.size:
+            self.free_list[: ids.size] = torch.as_tensor(ids, device=self.device)
+        self.free_count[0] = int(ids.size)
+
+
+class MemDecay:
+    """A library handle bound to a PagedCache, with the step's output buffers."""
+
+    def __init__(self, cache: PagedCache, base_priority: torch.Tensor, decay_rate: torch.Tensor, *,
+                 rho: float, alpha: float, tau_scale: float, pinned_mask: int,
+                 n_regions: int = 7, stream: Optional[torch.cuda.Stream] = None):
+        self.cache = cache
+        dev = cache.device
+        self.b = base_priority.to(dev, torch.float32).contiguous()
+        self.lam = decay_rate.to(dev, torch.float32).contiguous()
+        cfg = B.md_config(n_layers=cache.L, n_q_heads=cache.Hq, n_kv_heads=cache.Hkv,
+                          head_dim=cache.d, page_size=cache.P, max_sessions=cache.S,
+                          max_pages=cache.max_pages, n_phys_pages=cache.n_phys,
+                          n_regions=n_regions, pinned_region_mask=pinned_mask, rho=rho,
+                          alpha=alpha, tau_scale=tau_scale, reserved=0)
+        rp = B.md_region_params(base_priority=self.b.data_ptr(), decay_rate=self.lam.data_ptr())
+        self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
+        self._cfg, self._rp, self._cv = cfg, rp, cache.view()
+        self.handle = B.md_init(cfg, rp, self._cv, self.stream.cuda_stream)
+        S, MP = cache.S, cache.max_pages
+        self.page_score = torch.zeros((S, MP), dtype=torch.float32, device=dev)
+        self.evict_serial = torch.zeros((S, MP), dtype=torch.int32, device=dev)
+        self.evict_count = torch.zeros(S, dtype=torch.int32, device=dev)
+        self.infeasible = torch.zeros(S, dtype=torch.uint8, device=dev)
+
+    # ---- the four calls of one step
+    def observe(self, step: int, q: torch.Tensor, new_k: Optional[torch.Tensor] = None,
+                new_region: Optional[torch.Tensor] = None, abar_out: Optional[torch.Tensor] = None):
+        B.md_observe_step(self.handle, step, _ptr(q, torch.float32),
+                          None if new_k is None else _ptr(new_k, torch.bfloat16),
+                          None if new_region is None else _ptr(new_region, torch.uint8),
+                          None if abar_out is None else _ptr(abar_out, torch.float32))
+
+    def score(self, token_score: Optional[torch.Tensor] = None, page_score: bool = True):
+        B.md_score_pages(self.handle, self.page_score.data_ptr() if page_score else None,
+                         None if token_score is None else _ptr(token_score, torch.float32))
+
+    def select(self):
+        B.md_select_evict(self.handle, self.evict_serial.data_ptr(), self.evict_count.data_ptr(),
+                          self.infeasible.data_ptr())
+
+    def compact(self, evict_serial: Optional[torch.Tensor] = None,
+                evict_count: Optional[torch.Tensor] = None):
+        es = self.evict_serial if evict_serial is None else evict_serial
+        ec = self.evict_count if evict_count is None else evict_count
+        B.md_compact(self.handle, _ptr(es, torch.int32), _ptr(ec, torch.int32))
+
+    def step(self, step: int, q, new_k=None, new_region=None):
+        self.observe(step, q, new_k, new_region)
+        self.score()
+        self.select()
+        self.compact()
+
+    def device_status(self) -> int:
+        return B.md_read_device_status(self.handle)
+
+    def close(self):
+        if self.handle is not None:
+            B.md_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _ptr(t: torch.Tensor, dtype) -> int:
+    if t.dtype != dtype or not t.is_contiguous():
+        raise ValueError(f"expected a contiguous {dtype} tensor, got {t.dtype}")
+    return t.data_ptr()

@@ -1,0 +1,267 @@
+// C-ABI layer of the MemDecay retention step: argument validation (all on the
+// host, before anything is enqueued), the handle, the scratch, and the order
+// of kernel launches on the caller's stream.
+
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "md_internal.h"
+
+namespace {
+
+enum Phase { kNone = 0, kObserved = 1, kScored = 2, kCompacted = 3 };
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+}  // namespace
+
+struct md_handle_s {
+    md::Dims dm;
+    md::View v;
+    md::Scratch sc;
+    hipStream_t stream;
+    int device;
+    void* scratch;
+    int logits_blocks;
+    int mass_blocks;
+    int score_blocks;
+    bool have_step;
+    int32_t last_step;
+    Phase phase;
+};
+
+extern "C" {
+
+int32_t md_abi_version(void) { return MD_ABI_VERSION; }
+
+const char* md_status_str(md_status s) {
+    switch (s) {
+        case MD_OK: return "ok";
+        case MD_E_INVALID: return "invalid argument (null or misaligned pointer, or a value out of range)";
+        case MD_E_UNSUPPORTED: return "unsupported shape (head_dim must be 128, page_size 16 or 64, "
+                                      "Hq/Hkv <= 16, L*Hq <= 1024, sessions <= 1024, pages per session <= 8192)";
+        case MD_E_STEP: return "step must advance by exactly one per md_observe_step";
+        case MD_E_HIP: return "HIP runtime call failed";
+        case MD_E_STATE: return "call out of order (score needs an observe, select needs a score, "
+                                "and neither may follow a compact before the next observe)";
+        case MD_E_NOMEM: return "could not allocate the library scratch";
+        default: return "unknown status";
+    }
+}
+
+static md_status validate_config(const md_config* c) {
+    if (c == nullptr) return MD_E_INVALID;
+    if (c->reserved != 0) return MD_E_INVALID;
+    if (c->n_layers < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1) return MD_E_INVALID;
+    if (c->n_q_heads % c->n_kv_heads != 0) return MD_E_INVALID;
+    if (c->max_sessions < 1 || c->max_pages < 1 || c->n_phys_pages < 1) return MD_E_INVALID;
+    if (c->n_regions < 1 || c->n_regions > 32) return MD_E_INVALID;
+    if (c->n_regions < 32 && (c->pinned_region_mask >> c->n_regions) != 0) return MD_E_INVALID;
+    if (!(c->rho >= 0.0f && c->rho < 1.0f)) return MD_E_INVALID;
+    if (!(c->alpha >= 0.0f) || !isfinite(c->alpha)) return MD_E_INVALID;
+    if (!(c->tau_scale >= 0.0f) || !isfinite(c->tau_scale)) return MD_E_INVALID;
+    if (c->head_dim != md::kHeadDim) return MD_E_UNSUPPORTED;
+    if (c->page_size != 16 && c->page_size != 64) return MD_E_UNSUPPORTED;
+    if (c->n_q_heads / c->n_kv_heads > 16) return MD_E_UNSUPPORTED;
+    if ((int64_t)c->n_layers * c->n_q_heads > md::kMaxRows) return MD_E_UNSUPPORTED;
+    if (c->max_sessions > md::kMaxSessions) return MD_E_UNSUPPORTED;
+    if (c->max_pages > md::kMaxPages) return MD_E_UNSUPPORTED;
+    // token and element counts must stay within int32 where kernels index with int
+    if ((int64_t)c->max_pages * c->page_size > (int64_t)1 << 30) return MD_E_UNSUPPORTED;
+    if ((int64_t)c->n_phys_pages * c->page_size > (int64_t)1 << 30) return MD_E_UNSUPPORTED;
+    return MD_OK;
+}
+
+static md_status validate_view(const md_cache_view* v) {
+    if (v == nullptr) return MD_E_INVALID;
+    const void* ptrs[] = {v->k_pool, v->region, v->t_ins, v->t_ref, v->importance,
+                          v->page_table, v->page_serial, v->n_pages, v->n_tokens, v->clock,
+                          v->next_serial, v->budget, v->free_list, v->free_count};
+    for (const void* p : ptrs)
+        if (p == nullptr) return MD_E_INVALID;
+    if (!aligned(v->k_pool, 16)) return MD_E_INVALID;
+    const void* words[] = {v->t_ins, v->t_ref, v->importance, v->page_table, v->page_serial,
+                           v->n_pages, v->n_tokens, v->clock, v->next_serial, v->budget,
+                           v->free_list, v->free_count};
+    for (const void* p : words)
+        if (!aligned(p, 4)) return MD_E_INVALID;
+    return MD_OK;
+}
+
+md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cache_view* cv,
+                  void* stream, md_handle* out) {
+    if (out == nullptr) return MD_E_INVALID;
+    *out = nullptr;
+    md_status st = validate_config(cfg);
+    if (st != MD_OK) return st;
+    st = validate_view(cv);
+    if (st != MD_OK) return st;
+    if (rp == nullptr || rp->base_priority == nullptr || rp->decay_rate == nullptr) return MD_E_INVALID;
+    if (!aligned(rp->base_priority, 4) || !aligned(rp->decay_rate, 4)) return MD_E_INVALID;
+
+    md::Dims dm{};
+    dm.L = cfg->n_layers;
+    dm.Hq = cfg->n_q_heads;
+    dm.Hkv = cfg->n_kv_heads;
+    dm.G = dm.Hq / dm.Hkv;
+    dm.P = cfg->page_size;
+    dm.Pshift = dm.P == 16 ? 4 : 6;
+    dm.S = cfg->max_sessions;
+    dm.MP = cfg->max_pages;
+    dm.NP = cfg->n_phys_pages;
+    dm.R = dm.L * dm.Hq;
+    dm.LHkv = dm.L * dm.Hkv;
+    dm.n_regions = cfg->n_regions;
+    dm.max_chunks = (int)(((int64_t)dm.MP * dm.P + md::kChunk - 1) / md::kChunk);
+    dm.pin_mask = cfg->pinned_region_mask;
+    dm.rho = cfg->rho;
+    dm.alpha = cfg->alpha;
+    dm.tau_scale = cfg->tau_scale;
+
+    // ---- from here on the HIP runtime is used
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return MD_E_HIP;
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return MD_E_HIP;
+    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) return MD_E_UNSUPPORTED;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+
+    // Region priors: b_r >= 0, lambda_r >= 0, finite (Sec. III-B).
+    const size_t nrp = (size_t)dm.S * dm.n_regions;
+    std::vector<float> hb(nrp), hl(nrp);
+    if (hipMemcpyAsync(hb.data(), rp->base_priority, nrp * sizeof(float), hipMemcpyDeviceToHost, hs) != hipSuccess ||
+        hipMemcpyAsync(hl.data(), rp->decay_rate, nrp * sizeof(float), hipMemcpyDeviceToHost, hs) != hipSuccess ||
+        hipStreamSynchronize(hs) != hipSuccess)
+        return MD_E_HIP;
+    for (size_t i = 0; i < nrp; ++i)
+        if (!(hb[i] >= 0.0f) || !isfinite(hb[i]) || !(hl[i] >= 0.0f) || !isfinite(hl[i])) return MD_E_INVALID;
+
+    md_handle_s* h = new (std::nothrow) md_handle_s();
+    if (h == nullptr) return MD_E_NOMEM;
+    h->dm = dm;
+    h->v.k_pool = cv->k_pool;
+    h->v.region = cv->region;
+    h->v.t_ins = cv->t_ins;
+    h->v.t_ref = cv->t_ref;
+    h->v.imp = cv->importance;
+    h->v.page_table = cv->page_table;
+    h->v.page_serial = cv->page_serial;
+    h->v.n_pages = cv->n_pages;
+    h->v.n_tokens = cv->n_tokens;
+    h->v.clock = cv->clock;
+    h->v.next_serial = cv->next_serial;
+    h->v.budget = cv->budget;
+    h->v.free_list = cv->free_list;
+    h->v.free_count = cv->free_count;
+    h->v.b = rp->base_priority;
+    h->v.lam = rp->decay_rate;
+    h->stream = hs;
+    h->device = dev;
+
+    const size_t bytes = md::scratch_bytes(dm);
+    if (hipMalloc(&h->scratch, bytes) != hipSuccess) {
+        delete h;
+        return MD_E_NOMEM;
+    }
+    md::scratch_carve(dm, h->scratch, &h->sc);
+    // counters and status start at zero; work lists empty until the first append
+    if (hipMemsetAsync(h->sc.done, 0, 2 * sizeof(int32_t), hs) != hipSuccess ||
+        hipMemsetAsync(h->sc.item_prefix, 0, (size_t)(dm.S + 1) * sizeof(int32_t), hs) != hipSuccess ||
+        hipMemsetAsync(h->sc.tile_prefix, 0, (size_t)(dm.S + 1) * sizeof(int32_t), hs) != hipSuccess ||
+        hipMemsetAsync(h->sc.valid, 0, (size_t)(dm.S + 1) * sizeof(int32_t), hs) != hipSuccess ||
+        hipStreamSynchronize(hs) != hipSuccess) {
+        (void)hipFree(h->scratch);
+        delete h;
+        return MD_E_HIP;
+    }
+    const int n_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
+    h->logits_blocks = 2 * n_cu;
+    h->mass_blocks = 4 * n_cu;
+    h->score_blocks = 2 * n_cu;
+    h->have_step = false;
+    h->last_step = 0;
+    h->phase = kNone;
+    *out = h;
+    return MD_OK;
+}
+
+md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint16_t* new_k,
+                          const uint8_t* new_region, float* abar_out) {
+    if (h == nullptr || q == nullptr || !aligned(q, 16)) return MD_E_INVALID;
+    if (new_k != nullptr && (new_region == nullptr || !aligned(new_k, 16))) return MD_E_INVALID;
+    if (abar_out != nullptr && !aligned(abar_out, 4)) return MD_E_INVALID;
+    if (h->have_step && step != h->last_step + 1) return MD_E_STEP;
+    if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    hipError_t e = md::launch_append(h->dm, h->v, h->sc, new_k, new_region, h->stream);
+    if (e == hipSuccess) e = md::launch_logits(h->dm, h->v, h->sc, q, h->logits_blocks, h->stream);
+    if (e == hipSuccess) e = md::launch_rowstats(h->dm, h->sc, h->stream);
+    if (e == hipSuccess) e = md::launch_mass(h->dm, h->v, h->sc, abar_out, h->mass_blocks, h->stream);
+    if (e != hipSuccess) return MD_E_HIP;
+    h->have_step = true;
+    h->last_step = step;
+    h->phase = kObserved;
+    return MD_OK;
+}
+
+md_status md_score_pages(md_handle h, float* page_score, float* token_score) {
+    if (h == nullptr) return MD_E_INVALID;
+    if ((page_score != nullptr && !aligned(page_score, 4)) ||
+        (token_score != nullptr && !aligned(token_score, 4)))
+        return MD_E_INVALID;
+    if (h->phase != kObserved && h->phase != kScored) return MD_E_STATE;
+    if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    if (md::launch_score(h->dm, h->v, h->sc, page_score, token_score, h->score_blocks, h->stream) != hipSuccess)
+        return MD_E_HIP;
+    h->phase = kScored;
+    return MD_OK;
+}
+
+md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_count, uint8_t* infeasible) {
+    if (h == nullptr || evict_serial == nullptr || evict_count == nullptr || infeasible == nullptr)
+        return MD_E_INVALID;
+    if (!aligned(evict_serial, 4) || !aligned(evict_count, 4)) return MD_E_INVALID;
+    if (h->phase != kScored) return MD_E_STATE;
+    if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    if (md::launch_select(h->dm, h->v, h->sc, evict_serial, evict_count, infeasible, h->stream) != hipSuccess)
+        return MD_E_HIP;
+    return MD_OK;
+}
+
+md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* evict_count) {
+    if (h == nullptr || evict_serial == nullptr || evict_count == nullptr) return MD_E_INVALID;
+    if (!aligned(evict_serial, 4) || !aligned(evict_count, 4)) return MD_E_INVALID;
+    if (h->phase == kNone) return MD_E_STATE;
+    if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    if (md::launch_compact(h->dm, h->v, h->sc, evict_serial, evict_count, h->stream) != hipSuccess)
+        return MD_E_HIP;
+    h->phase = kCompacted;
+    return MD_OK;
+}
+
+md_status md_read_device_status(md_handle h, int32_t* host_out) {
+    if (h == nullptr || host_out == nullptr) return MD_E_INVALID;
+    if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    int32_t v = 0;
+    if (hipMemcpyAsync(&v, h->sc.status, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream) != hipSuccess ||
+        hipMemsetAsync(h->sc.status, 0, sizeof(int32_t), h->stream) != hipSuccess ||
+        hipStreamSynchronize(h->stream) != hipSuccess)
+        return MD_E_HIP;
+    *host_out = v;
+    return MD_OK;
+}
+
+md_status md_destroy(md_handle h) {
+    if (h == nullptr) return MD_E_INVALID;
+    md_status st = MD_OK;
+    if (hipSetDevice(h->device) != hipSuccess || hipStreamSynchronize(h->stream) != hipSuccess) st = MD_E_HIP;
+    if (hipFree(h->scratch) != hipSuccess) st = MD_E_HIP;
+    delete h;
+    return st;
+}
+
+}  // extern "C"

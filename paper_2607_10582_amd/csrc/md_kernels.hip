@@ -1,0 +1,829 @@
+// gfx950 kernels of the MemDecay observation step.
+//
+// One step over a batch of sessions runs seven kernels on the caller's stream:
+//   k_append    one block per session: clock, append into the tail page or a
+//               page popped from the free list, copy of the new key rows; the
+//               last block to finish builds the step's work lists.
+//   k_logits    HOT: every cached token's logits q.k/sqrt(d) for all query heads
+//               (Sec. III-C), one 128-token chunk of one (layer, KV head) per
+//               wave, on MFMA; chunk softmax statistics; logits spilled for
+//               the normalisation pass.
+//   k_rowstats  per (session, layer, query head): softmax max and 1/sum over
+//               the chunk statistics, in a fixed order.
+//   k_mass      per token: attention mass A_i, EWMA (Eq. 2), refresh (Eq. 3).
+//   k_score     per token: retention score (Eq. 4); per page: mean (Eq. 5).
+//   k_select    one block per session: weighted radix select of the pages to
+//               evict (Sec. III-D, Alg. 1).
+//   k_compact   one block per session: page-table compaction, free-list push.
+// Every reduction is in a fixed order; no float atomics are used.
+
+#include <math.h>
+
+#include "md_internal.h"
+
+namespace md {
+
+typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// log2(e) / sqrt(128): logits are kept in base 2 so that 2^(x - m) is the
+// softmax numerator exp(q.k/sqrt(d) - m').
+constexpr float kLogitScale = (float)(1.4426950408889634074 / 11.313708498984760390);
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+__device__ __forceinline__ int load_agent(const int32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Exclusive prefix of one int per thread across the whole block (any multiple
+// of 64 threads up to 1024).  lds needs 17 ints.  Contains __syncthreads.
+__device__ int block_exclusive_scan(int v, int* lds, int* total) {
+    const int lane = lane_id(), wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    int incl = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(incl, o);
+        if (lane >= o) incl += t;
+    }
+    if (lane == 63) lds[wid] = incl;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int acc = 0;
+        for (int w = 0; w < nw; ++w) {
+            const int t = lds[w];
+            lds[w] = acc;
+            acc += t;
+        }
+        lds[16] = acc;
+    }
+    __syncthreads();
+    const int res = lds[wid] + incl - v;
+    *total = lds[16];
+    __syncthreads();
+    return res;
+}
+
+// Largest s in [0, S) with pref[s] <= x, given pref[0] <= x < pref[S].
+__device__ __forceinline__ int find_session(const int* pref, int S, int x) {
+    int lo = 0, hi = S;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (pref[mid] <= x) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ bool counters_ok(int np, int nt, const Dims& dm) {
+    if (np < 0 || np > dm.MP) return false;
+    if (np == 0) return nt == 0;
+    return nt > (np - 1) * dm.P && nt <= np * dm.P;
+}
+
+// ---------------------------------------------------------------- append
+
+__global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
+                                                const uint16_t* __restrict__ new_k,
+                                                const uint8_t* __restrict__ new_region) {
+    const int s = blockIdx.x;
+    __shared__ int sh_phys, sh_slot, sh_last;
+    __shared__ int lds[17];
+    if (threadIdx.x == 0) {
+        const int t = v.clock[s] + 1;
+        v.clock[s] = t;
+        int phys = -1, slot = 0;
+        const int np = v.n_pages[s], nt = v.n_tokens[s];
+        if (new_k != nullptr && counters_ok(np, nt, dm)) {
+            const size_t row = (size_t)s * dm.MP;
+            if (np > 0 && nt < np * dm.P) {
+                const int p = v.page_table[row + np - 1];
+                if (p >= 0 && p < dm.NP) {
+                    phys = p;
+                    slot = nt - (np - 1) * dm.P;
+                } else {
+                    atomicOr(sc.status, kDevCorrupt);
+                }
+            } else if (np < dm.MP) {
+                const int old = atomicSub(v.free_count, 1);
+                if (old > 0 && old <= dm.NP) {
+                    const int p = v.free_list[old - 1];
+                    if (p >= 0 && p < dm.NP) {
+                        phys = p;
+                        slot = 0;
+                        v.page_table[row + np] = p;
+                        v.page_serial[row + np] = v.next_serial[s];
+                        v.next_serial[s] += 1;
+                        v.n_pages[s] = np + 1;
+                    } else {
+                        atomicOr(sc.status, kDevCorrupt);
+                    }
+                } else {
+                    atomicAdd(v.free_count, 1);
+                    atomicOr(sc.status, MD_DEV_CAPACITY);
+                }
+            } else {
+                atomicOr(sc.status, MD_DEV_CAPACITY);
+            }
+            if (phys >= 0) {
+                v.n_tokens[s] = nt + 1;
+                const size_t si = (size_t)phys * dm.P + slot;
+                v.region[si] = new_region[s];
+                v.t_ins[si] = t;
+                v.t_ref[si] = t;
+                v.imp[si] = 0.0f;
+            }
+        }
+        sh_phys = phys;
+        sh_slot = slot;
+    }
+    __syncthreads();
+    const int phys = sh_phys;
+    if (phys >= 0) {
+        // L*Hkv rows of d bf16 = 16 pieces of 16 bytes per row.
+        const int slot = sh_slot;
+        const u32x4* src = reinterpret_cast<const u32x4*>(new_k + (size_t)s * dm.LHkv * kHeadDim);
+        for (int i = threadIdx.x; i < dm.LHkv * 16; i += blockDim.x) {
+            const int r = i >> 4, part = i & 15;
+            u32x4* dst = reinterpret_cast<u32x4*>(
+                v.k_pool + (((size_t)phys * dm.LHkv + r) * dm.P + slot) * kHeadDim);
+            dst[part] = src[i];
+        }
+    }
+
+    // The last block to finish lays out the step's work lists.
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) sh_last = (atomicAdd(sc.done, 1) == (int)gridDim.x - 1);
+    __syncthreads();
+    if (!sh_last) return;
+    __threadfence();
+    int it[4], ti[4];
+    int my_items = 0, my_tiles = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int s2 = threadIdx.x * 4 + k;
+        it[k] = ti[k] = 0;
+        if (s2 < dm.S) {
+            const int np = load_agent(v.n_pages + s2);
+            const int nt = load_agent(v.n_tokens + s2);
+            const bool ok = counters_ok(np, nt, dm);
+            if (!ok) atomicOr(sc.status, kDevCorrupt);
+            const int ch = ok ? (np * dm.P + kChunk - 1) / kChunk : 0;
+            sc.chunks[s2] = ch;
+            sc.valid[s2] = ok ? 1 : 0;
+            it[k] = ch * dm.LHkv;
+            ti[k] = ok ? (nt + kTile - 1) / kTile : 0;
+        }
+        my_items += it[k];
+        my_tiles += ti[k];
+    }
+    int tot_i, tot_t;
+    int ex_i = block_exclusive_scan(my_items, lds, &tot_i);
+    int ex_t = block_exclusive_scan(my_tiles, lds, &tot_t);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int s2 = threadIdx.x * 4 + k;
+        if (s2 < dm.S) {
+            sc.item_prefix[s2] = ex_i;
+            sc.tile_prefix[s2] = ex_t;
+        }
+        ex_i += it[k];
+        ex_t += ti[k];
+    }
+    if (threadIdx.x == 0) {
+        sc.item_prefix[dm.S] = tot_i;
+        sc.tile_prefix[dm.S] = tot_t;
+        *sc.done = 0;
+    }
+}
+
+hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
+                         const uint16_t* new_k, const uint8_t* new_region, hipStream_t st) {
+    hipLaunchKernelGGL(k_append, dim3(dm.S), dim3(256), 0, st, dm, v, sc, new_k, new_region);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- logits
+
+// Split a float32 into three bfloat16 terms with x == hi + mid + lo exactly:
+// hi and mid truncate (the differences are exact by Sterbenz's lemma), and
+// what is left has at most 8 significant bits, so lo holds it exactly.
+__device__ __forceinline__ void split3(float x, uint32_t& hi, uint32_t& mid, uint32_t& lo) {
+    const uint32_t u = __float_as_uint(x);
+    const uint32_t h = u & 0xFFFF0000u;
+    const float r1 = x - __uint_as_float(h);
+    const uint32_t m = __float_as_uint(r1) & 0xFFFF0000u;
+    const float r2 = r1 - __uint_as_float(m);
+    hi = h >> 16;
+    mid = m >> 16;
+    lo = __float_as_uint(r2) >> 16;
+}
+
+// One wave: logits of one 128-token chunk of one (session, layer, KV head)
+// for the G query heads of the group, as eight 16x16x32 bf16 MFMA row tiles:
+// A = 16 tokens x 32 dims of K (bf16, straight from the pool), B = 32 dims x
+// 16 columns holding the G heads' query terms (hi, mid, lo accumulate into
+// the same C), C = 16 tokens x 16 heads in float32.
+// Lane layout (16x16x32): A/B lane l holds row/column l & 15 and the eight
+// consecutive k = 8 (l >> 4) .. +7; C lane l holds column l & 15, rows
+// 4 (l >> 4) .. +3.
+__global__ void __launch_bounds__(256) k_logits(Dims dm, View v, Scratch sc,
+                                                const float* __restrict__ q) {
+    __shared__ int s_pref[kMaxSessions + 1];
+    const int S = dm.S;
+    for (int i = threadIdx.x; i <= S; i += blockDim.x) s_pref[i] = sc.item_prefix[i];
+    __syncthreads();
+    const int total = s_pref[S];
+    const int lane = lane_id();
+    const int n_waves = gridDim.x * (blockDim.x >> 6);
+    const int gw = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+    const int per = (total + n_waves - 1) / n_waves;
+    int it = gw * per;
+    const int end = min(total, it + per);
+    if (it >= end) return;
+
+    int s = find_session(s_pref, S, it);
+    int nch = (s_pref[s + 1] - s_pref[s]) / dm.LHkv;
+    int local = it - s_pref[s];
+    int lkv = local / nch;
+    int c = local - lkv * nch;
+
+    const int h = lane & 15;         // MFMA column = query head within the group
+    const int g = lane >> 4;         // k-group of A/B, row quad of C
+    u32x4 bq[4][3];
+    int cur_row = -1;
+
+    for (; it < end; ++it) {
+        const int l = lkv / dm.Hkv;
+        const int kv = lkv - l * dm.Hkv;
+        const int row_id = s * dm.LHkv + lkv;
+        if (row_id != cur_row) {
+            cur_row = row_id;
+            bool bad = false;
+            const float* qh = q + (((size_t)s * dm.L + l) * dm.Hq + kv * dm.G + h) * kHeadDim;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                float xs[8];
+                if (h < dm.G) {
+                    const f32x4* p = reinterpret_cast<const f32x4*>(qh + 32 * j + 8 * g);
+                    const f32x4 u0 = p[0], u1 = p[1];
+                    xs[0] = u0.x; xs[1] = u0.y; xs[2] = u0.z; xs[3] = u0.w;
+                    xs[4] = u1.x; xs[5] = u1.y; xs[6] = u1.z; xs[7] = u1.w;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) xs[e] = 0.0f;
+                }
+                uint32_t hi[8], mi[8], lo[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    bad |= !isfinite(xs[e]);
+                    split3(xs[e], hi[e], mi[e], lo[e]);
+                }
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    bq[j][0][w] = hi[2 * w] | (hi[2 * w + 1] << 16);
+                    bq[j][1][w] = mi[2 * w] | (mi[2 * w + 1] << 16);
+                    bq[j][2][w] = lo[2 * w] | (lo[2 * w + 1] << 16);
+                }
+            }
+            if (bad) atomicOr(sc.status, MD_DEV_NONFINITE);
+        }
+
+        const int nt = v.n_tokens[s];
+        const int* ptab = v.page_table + (size_t)s * dm.MP;
+        const int tok0 = c * kChunk;
+        int phys_t[8], sub_t[8];
+        bool tv[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int tok = tok0 + 16 * t;
+            tv[t] = tok < nt;
+            phys_t[t] = 0;
+            sub_t[t] = 0;
+            if (tv[t]) {
+                const int pg = tok >> dm.Pshift;
+                const int p = ptab[pg];
+                if ((unsigned)p < (unsigned)dm.NP) {
+                    phys_t[t] = p;
+                    sub_t[t] = tok - (pg << dm.Pshift);
+                } else {
+                    tv[t] = false;
+                    if (lane == 0) atomicOr(sc.status, kDevCorrupt);
+                }
+            }
+        }
+        u32x4 a[8][4];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            if (tv[t]) {
+                const u32x4* rowp = reinterpret_cast<const u32x4*>(
+                    v.k_pool + (((size_t)phys_t[t] * dm.LHkv + lkv) * dm.P + sub_t[t] + h) * kHeadDim);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) a[t][j] = rowp[4 * j + g];
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) a[t][j] = u32x4{0u, 0u, 0u, 0u};
+            }
+        }
+        f32x4 acc[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int p = 0; p < 3; ++p) {
+#pragma unroll
+                for (int t = 0; t < 8; ++t) {
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8, a[t][j]), __builtin_bit_cast(bf16x8, bq[j][p]),
+                        acc[t], 0, 0, 0);
+                }
+            }
+        }
+
+        // Base-2 logits; tokens past the session's count are masked out.
+        float m = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int tok = tok0 + 16 * t + 4 * g + i;
+                const float x = (tv[t] && tok < nt) ? acc[t][i] * kLogitScale : -INFINITY;
+                acc[t][i] = x;
+                m = fmaxf(m, x);
+            }
+        }
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        float lsum = 0.0f;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) lsum += exp2f(acc[t][i] - m);
+        }
+        lsum += __shfl_xor(lsum, 16);
+        lsum += __shfl_xor(lsum, 32);
+
+        if (h < dm.G) {
+            const int row = l * dm.Hq + kv * dm.G + h;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                if (tv[t]) {
+                    f32x4* dst = reinterpret_cast<f32x4*>(
+                        sc.logits + ((size_t)phys_t[t] * dm.R + row) * dm.P + sub_t[t] + 4 * g);
+                    *dst = acc[t];
+                }
+            }
+            if (g == 0)
+                sc.cstats[((size_t)s * dm.R + row) * dm.max_chunks + c] = make_float2(m, lsum);
+        }
+
+        // next item
+        if (++c == nch) {
+            c = 0;
+            if (++lkv == dm.LHkv) {
+                lkv = 0;
+                do { ++s; } while (s < S && s_pref[s + 1] == s_pref[s]);
+                if (s < S) nch = (s_pref[s + 1] - s_pref[s]) / dm.LHkv;
+            }
+        }
+    }
+}
+
+hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q,
+                         int n_blocks, hipStream_t st) {
+    hipLaunchKernelGGL(k_logits, dim3(n_blocks), dim3(256), 0, st, dm, v, sc, q);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- row statistics
+
+__global__ void __launch_bounds__(256) k_rowstats(Dims dm, Scratch sc) {
+    const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = lane_id();
+    if (w >= dm.S * dm.R) return;
+    const int s = w / dm.R, row = w - s * dm.R;
+    const int nch = sc.chunks[s];
+    if (nch == 0) return;
+    const float2* cs = sc.cstats + ((size_t)s * dm.R + row) * dm.max_chunks;
+    float m = -INFINITY;
+    for (int c = lane; c < nch; c += 64) m = fmaxf(m, cs[c].x);
+    m = wave_max(m);
+    float l = 0.0f;
+    for (int c = lane; c < nch; c += 64) {
+        const float2 st = cs[c];
+        l += st.y * exp2f(st.x - m);
+    }
+    l = wave_sum(l);
+    if (lane == 0) sc.rstats[(size_t)s * dm.R + row] = make_float2(m, 1.0f / l);
+}
+
+hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st) {
+    const int waves = dm.S * dm.R;
+    hipLaunchKernelGGL(k_rowstats, dim3((waves + 3) / 4), dim3(256), 0, st, dm, sc);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- mass, EWMA, refresh
+
+// One block per 64-token tile at a time: 4 row groups x 64 tokens; each
+// thread sums its rows' softmax weights 2^(x - M) / Lambda, the four partials
+// add in a fixed order.
+__global__ void __launch_bounds__(256) k_mass(Dims dm, View v, Scratch sc, float* abar_out) {
+    __shared__ int s_pref[kMaxSessions + 1];
+    __shared__ float2 s_rs[kMaxRows];
+    __shared__ float s_part[4][kTile];
+    const int S = dm.S;
+    for (int i = threadIdx.x; i <= S; i += blockDim.x) s_pref[i] = sc.tile_prefix[i];
+    __syncthreads();
+    const int total = s_pref[S];
+    const int tl = threadIdx.x & 63, rg = threadIdx.x >> 6;
+    const float one_m_rho = 1.0f - dm.rho;
+    int cur = -1;
+    for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
+        const int s = find_session(s_pref, S, tile);
+        if (s != cur) {
+            __syncthreads();
+            for (int i = threadIdx.x; i < dm.R; i += blockDim.x) s_rs[i] = sc.rstats[(size_t)s * dm.R + i];
+            __syncthreads();
+            cur = s;
+        }
+        const int nt = v.n_tokens[s];
+        const int tok = (tile - s_pref[s]) * kTile + tl;
+        bool valid = tok < nt;
+        int phys = 0, slot = 0;
+        float acc = 0.0f;
+        if (valid) {
+            const int pg = tok >> dm.Pshift;
+            slot = tok - (pg << dm.Pshift);
+            phys = v.page_table[(size_t)s * dm.MP + pg];
+            if ((unsigned)phys >= (unsigned)dm.NP) {
+                valid = false;
+                atomicOr(sc.status, kDevCorrupt);
+            } else {
+                const float* lp = sc.logits + (size_t)phys * dm.R * dm.P + slot;
+#pragma unroll 8
+                for (int row = rg; row < dm.R; row += 4) {
+                    const float2 rs = s_rs[row];
+                    acc += exp2f(lp[(size_t)row * dm.P] - rs.x) * rs.y;
+                }
+            }
+        }
+        s_part[rg][tl] = acc;
+        __syncthreads();
+        if (rg == 0 && valid) {
+            const float abar =
+                (((s_part[0][tl] + s_part[1][tl]) + s_part[2][tl]) + s_part[3][tl]) / (float)dm.R;
+            const size_t si = (size_t)phys * dm.P + slot;
+            const float a = v.imp[si];
+            v.imp[si] = fmaf(dm.rho, a, one_m_rho * abar);
+            if (abar >= dm.tau_scale / (float)nt) v.t_ref[si] = v.clock[s];
+            if (abar_out != nullptr) abar_out[si] = abar;
+        }
+        __syncthreads();
+    }
+}
+
+hipError_t launch_mass(const Dims& dm, const View& v, const Scratch& sc, float* abar_out,
+                       int n_blocks, hipStream_t st) {
+    hipLaunchKernelGGL(k_mass, dim3(n_blocks), dim3(256), 0, st, dm, v, sc, abar_out);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- scores
+
+// One wave per 64-token tile (4 pages of 16 or one page of 64); a page's
+// members are P consecutive lanes, reduced with a butterfly; lane 0 of the
+// page writes its score.
+__global__ void __launch_bounds__(256) k_score(Dims dm, View v, Scratch sc, float* page_score,
+                                               float* token_score) {
+    __shared__ int s_pref[kMaxSessions + 1];
+    const int S = dm.S;
+    for (int i = threadIdx.x; i <= S; i += blockDim.x) s_pref[i] = sc.tile_prefix[i];
+    __syncthreads();
+    const int total = s_pref[S];
+    const int lane = lane_id();
+    const int n_waves = gridDim.x * (blockDim.x >> 6);
+    const int gw = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+    for (int tile = gw; tile < total; tile += n_waves) {
+        const int s = find_session(s_pref, S, tile);
+        const int nt = v.n_tokens[s];
+        const int t = v.clock[s];
+        const int tok = (tile - s_pref[s]) * kTile + lane;
+        const int pg = tok >> dm.Pshift;
+        bool valid = tok < nt;
+        bool pin = false;
+        float sc_i = 0.0f;
+        if (valid) {
+            const int phys = v.page_table[(size_t)s * dm.MP + pg];
+            if ((unsigned)phys >= (unsigned)dm.NP) {
+                valid = false;
+                atomicOr(sc.status, kDevCorrupt);
+            } else {
+                const size_t si = (size_t)phys * dm.P + (tok - (pg << dm.Pshift));
+                int r = v.region[si];
+                if (r >= dm.n_regions) {
+                    atomicOr(sc.status, kDevCorrupt);
+                    r = dm.n_regions - 1;
+                }
+                pin = (dm.pin_mask >> r) & 1u;
+                if (pin) {
+                    sc_i = INFINITY;
+                } else {
+                    const size_t ri = (size_t)s * dm.n_regions + r;
+                    const float dt = (float)(t - v.t_ref[si]);
+                    sc_i = v.b[ri] * expf(-v.lam[ri] * dt) + dm.alpha * v.imp[si];
+                }
+                if (token_score != nullptr) token_score[si] = sc_i;
+            }
+        }
+        float sum = (valid && !pin) ? sc_i : 0.0f;
+        int cnt = valid ? 1 : 0;
+        int anyp = pin ? 1 : 0;
+        for (int o = 1; o < dm.P; o <<= 1) {
+            sum += __shfl_xor(sum, o);
+            cnt += __shfl_xor(cnt, o);
+            anyp |= __shfl_xor(anyp, o);
+        }
+        if ((lane & (dm.P - 1)) == 0 && cnt > 0) {
+            const float ps = anyp ? INFINITY : sum / (float)cnt;
+            sc.pscore[(size_t)s * dm.MP + pg] = ps;
+            if (page_score != nullptr) page_score[(size_t)s * dm.MP + pg] = ps;
+        }
+    }
+}
+
+hipError_t launch_score(const Dims& dm, const View& v, const Scratch& sc, float* page_score,
+                        float* token_score, int n_blocks, hipStream_t st) {
+    hipLaunchKernelGGL(k_score, dim3(n_blocks), dim3(256), 0, st, dm, v, sc, page_score, token_score);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- select
+
+// Radix select over the float bit patterns of the page scores (non-negative,
+// so the unsigned order of the bits is the numeric order), weighted by each
+// page's live token count: the threshold key T is where the ascending
+// cumulative weight first reaches need = n - B.  Pages with key < T go; pages
+// with key == T go in serial order until the need is met.  Pinned pages
+// (+inf) never enter.  Each thread owns a contiguous run of page indices, so
+// per-thread runs in thread order are the serial order.
+__global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch sc,
+                                                        int32_t* ev_serial, int32_t* ev_count,
+                                                        uint8_t* infeasible) {
+    const int s = blockIdx.x;
+    __shared__ int lds[17];
+    __shared__ int hist[256];
+    __shared__ int sh_digit, sh_before;
+    const int tid = threadIdx.x;
+    const int np = v.n_pages[s], nt = v.n_tokens[s], B = v.budget[s];
+    const int need = nt - B;
+    if (!sc.valid[s] || need <= 0 || np == 0) {
+        if (tid == 0) {
+            ev_count[s] = 0;
+            infeasible[s] = 0;
+        }
+        return;
+    }
+    const uint32_t kInf = 0x7F800000u;
+    const float* ps = sc.pscore + (size_t)s * dm.MP;
+    const int* ser = v.page_serial + (size_t)s * dm.MP;
+    const int tailw = nt - (np - 1) * dm.P;
+    const int per = (np + kSelThreads - 1) / kSelThreads;
+    const int i0 = min(np, tid * per), i1 = min(np, i0 + per);
+    uint32_t key[kPerThread];
+    int wt[kPerThread];
+    int wsum = 0;
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+        const int i = i0 + k;
+        key[k] = kInf;
+        wt[k] = 0;
+        if (i < i1) {
+            key[k] = __float_as_uint(ps[i]);
+            wt[k] = (i == np - 1) ? tailw : dm.P;
+            if (key[k] < kInf) wsum += wt[k];
+        }
+    }
+    int total;
+    block_exclusive_scan(wsum, lds, &total);
+    const bool infeas = total < need;
+    uint32_t T = 0;
+    int rem = need;
+    if (!infeas) {
+        uint32_t prefix = 0, pmask = 0;
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            if (tid < 256) hist[tid] = 0;
+            __syncthreads();
+#pragma unroll
+            for (int k = 0; k < kPerThread; ++k) {
+                if (key[k] < kInf && (key[k] & pmask) == prefix)
+                    atomicAdd(&hist[(key[k] >> shift) & 255u], wt[k]);
+            }
+            __syncthreads();
+            // inclusive scan of the 256 bins by the first four waves; every
+            // thread of the block reaches both barriers
+            int hv = 0, incl = 0;
+            if (tid < 256) {
+                const int lane = lane_id();
+                hv = hist[tid];
+                incl = hv;
+#pragma unroll
+                for (int o = 1; o < 64; o <<= 1) {
+                    const int t2 = __shfl_up(incl, o);
+                    if (lane >= o) incl += t2;
+                }
+                if (lane == 63) lds[tid >> 6] = incl;
+            }
+            __syncthreads();
+            if (tid < 256) {
+                const int wid = tid >> 6;
+                for (int w = 0; w < wid; ++w) incl += lds[w];
+                const int excl = incl - hv;
+                if (excl < rem && rem <= incl) {
+                    sh_digit = tid;
+                    sh_before = excl;
+                }
+            }
+            __syncthreads();
+            prefix |= (uint32_t)sh_digit << shift;
+            pmask |= 0xFFu << shift;
+            rem -= sh_before;
+            __syncthreads();
+        }
+        T = prefix;
+    }
+    // weights of the key == T pages before this thread's run
+    int teq = 0;
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k)
+        if (!infeas && key[k] == T) teq += wt[k];
+    int dummy;
+    int run = block_exclusive_scan(teq, lds, &dummy);
+    bool ev[kPerThread];
+    int my_ev = 0;
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+        bool e = false;
+        if (i0 + k < i1 && key[k] < kInf) {
+            if (infeas) {
+                e = true;
+            } else if (key[k] < T) {
+                e = true;
+            } else if (key[k] == T) {
+                e = run < rem;
+                run += wt[k];
+            }
+        }
+        ev[k] = e;
+        my_ev += e ? 1 : 0;
+    }
+    int n_ev;
+    int pos = block_exclusive_scan(my_ev, lds, &n_ev);
+    int32_t* out = ev_serial + (size_t)s * dm.MP;
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k)
+        if (ev[k]) out[pos++] = ser[i0 + k];
+    if (tid == 0) {
+        ev_count[s] = n_ev;
+        infeasible[s] = infeas ? 1 : 0;
+    }
+}
+
+hipError_t launch_select(const Dims& dm, const View& v, const Scratch& sc, int32_t* ev_serial,
+                         int32_t* ev_count, uint8_t* infeasible, hipStream_t st) {
+    hipLaunchKernelGGL(k_select, dim3(dm.S), dim3(kSelThreads), 0, st, dm, v, sc, ev_serial,
+                       ev_count, infeasible);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- compact
+
+__global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratch sc,
+                                                         const int32_t* __restrict__ ev_serial,
+                                                         const int32_t* __restrict__ ev_count) {
+    const int s = blockIdx.x;
+    __shared__ int lds[17];
+    __shared__ int sh_base;
+    const int tid = threadIdx.x;
+    const int cnt = ev_count[s];
+    const int np = v.n_pages[s], nt = v.n_tokens[s];
+    if (!sc.valid[s] || cnt <= 0 || np == 0) return;
+    const int* evs = ev_serial + (size_t)s * dm.MP;
+    int* ptab = v.page_table + (size_t)s * dm.MP;
+    int* pser = v.page_serial + (size_t)s * dm.MP;
+    const int per = (np + kSelThreads - 1) / kSelThreads;
+    const int i0 = min(np, tid * per), i1 = min(np, i0 + per);
+    int ph[kPerThread], se[kPerThread];
+    bool keep[kPerThread];
+    int n_keep = 0, n_gone = 0;
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+        const int i = i0 + k;
+        keep[k] = false;
+        ph[k] = se[k] = 0;
+        if (i < i1) {
+            ph[k] = ptab[i];
+            se[k] = pser[i];
+            int lo = 0, hi = min(cnt, dm.MP);
+            while (lo < hi) {  // serials in the list ascend
+                const int mid = (lo + hi) >> 1;
+                if (evs[mid] < se[k]) lo = mid + 1; else hi = mid;
+            }
+            const bool gone = lo < min(cnt, dm.MP) && evs[lo] == se[k];
+            keep[k] = !gone;
+            n_keep += gone ? 0 : 1;
+            n_gone += gone ? 1 : 0;
+        }
+    }
+    int kept_total, gone_total;
+    int kpos = block_exclusive_scan(n_keep, lds, &kept_total);
+    int gpos = block_exclusive_scan(n_gone, lds, &gone_total);
+    if (tid == 0) {
+        if (gone_total != cnt) atomicOr(sc.status, MD_DEV_BAD_EVICT);
+        sh_base = gone_total > 0 ? atomicAdd(v.free_count, gone_total) : 0;
+        if (sh_base < 0 || sh_base + gone_total > dm.NP) atomicOr(sc.status, kDevCorrupt);
+    }
+    __syncthreads();  // every read of the old table is done before any write
+    const int base = sh_base;
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+        if (i0 + k < i1) {
+            if (keep[k]) {
+                ptab[kpos] = ph[k];
+                pser[kpos] = se[k];
+                ++kpos;
+            } else {
+                if (base + gpos >= 0 && base + gpos < dm.NP) v.free_list[base + gpos] = ph[k];
+                ++gpos;
+            }
+        }
+    }
+    // The thread owning the last page knows whether it survived; all pages
+    // but the last are full, so the token count follows from that.
+    if (i1 == np && i1 > i0) {
+        const int k_last = np - 1 - i0;
+        bool last_kept = false;
+#pragma unroll
+        for (int k = 0; k < kPerThread; ++k)
+            if (k == k_last) last_kept = keep[k];
+        v.n_pages[s] = kept_total;
+        v.n_tokens[s] = last_kept ? nt - gone_total * dm.P : kept_total * dm.P;
+    }
+}
+
+hipError_t launch_compact(const Dims& dm, const View& v, const Scratch& sc,
+                          const int32_t* ev_serial, const int32_t* ev_count, hipStream_t st) {
+    hipLaunchKernelGGL(k_compact, dim3(dm.S), dim3(kSelThreads), 0, st, dm, v, sc, ev_serial, ev_count);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- scratch layout
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t scratch_bytes(const Dims& dm) {
+    size_t n = 0;
+    n += align256((size_t)dm.NP * dm.R * dm.P * sizeof(float));
+    n += align256((size_t)dm.S * dm.R * dm.max_chunks * sizeof(float2));
+    n += align256((size_t)dm.S * dm.R * sizeof(float2));
+    n += align256((size_t)dm.S * dm.MP * sizeof(float));
+    n += 4 * align256((size_t)(dm.S + 1) * sizeof(int32_t));
+    n += align256(2 * sizeof(int32_t));
+    return n;
+}
+
+void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
+    char* p = static_cast<char*>(base);
+    auto take = [&](size_t bytes) {
+        char* r = p;
+        p += align256(bytes);
+        return r;
+    };
+    sc->logits = reinterpret_cast<float*>(take((size_t)dm.NP * dm.R * dm.P * sizeof(float)));
+    sc->cstats = reinterpret_cast<float2*>(take((size_t)dm.S * dm.R * dm.max_chunks * sizeof(float2)));
+    sc->rstats = reinterpret_cast<float2*>(take((size_t)dm.S * dm.R * sizeof(float2)));
+    sc->pscore = reinterpret_cast<float*>(take((size_t)dm.S * dm.MP * sizeof(float)));
+    sc->item_prefix = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
+    sc->tile_prefix = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
+    sc->chunks = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
+    sc->valid = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
+    int32_t* words = reinterpret_cast<int32_t*>(take(2 * sizeof(int32_t)));
+    sc->done = words;
+    sc->status = words + 1;
+}
+
+}  // namespace md

@@ -183,3 +183,41 @@ def torch_append_keys(w: Workload, step: int, device):
     g.manual_seed(_torch_seed(w, 0, "kapp", step))
     x = torch.randn((w.S, w.L, w.Hkv, w.d), generator=g, device=device, dtype=torch.float32)
     return x.to(torch.bfloat16)
+
+
+# ---------------------------------------------------------------- planted structure
+
+def planted_tokens(w: Workload, session: int, n0: int, count: int) -> np.ndarray:
+    """Seeded subset of prefix positions (outside the system span) that get
+    keys along a fixed direction, so that attention concentrates on them."""
+    g = rng(w, session, "perm", 1)
+    lo = min(w.system_len, n0 - 1)
+    return np.sort(g.choice(np.arange(lo, n0), size=min(count, n0 - lo), replace=False))
+
+
+def planted_direction(w: Workload, session: int) -> np.ndarray:
+    """Unit float32 directions [L][Hkv][d], one per (layer, KV head)."""
+    u = rng(w, session, "perm", 2).standard_normal((w.L, w.Hkv, w.d))
+    u /= np.linalg.norm(u, axis=-1, keepdims=True)
+    return u.astype(np.float32)
+
+
+def planted_keys(w: Workload, session: int, keys_bits: np.ndarray, tokens: np.ndarray,
+                 strength) -> np.ndarray:
+    """Replace the keys of ``tokens`` by strength * direction (+ the token's
+    own key as noise); ``strength`` is a scalar or one value per token."""
+    u = planted_direction(w, session)
+    k = bf16_bits_to_f32(keys_bits).copy()
+    st = np.broadcast_to(np.asarray(strength, dtype=np.float32), (len(tokens),))
+    k[tokens] = 0.25 * k[tokens] + st[:, None, None, None] * u[None]
+    return f32_to_bf16_bits(k)
+
+
+def planted_query(w: Workload, session: int, q: np.ndarray, gain: float) -> np.ndarray:
+    """Add gain * sqrt(d) * direction of each head's KV group to a query."""
+    u = planted_direction(w, session)
+    G = w.Hq // w.Hkv
+    qq = q.astype(np.float32).copy()
+    for h in range(w.Hq):
+        qq[:, h, :] += np.float32(gain * np.sqrt(w.d)) * u[:, h // G, :]
+    return qq

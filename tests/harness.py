@@ -1,0 +1,300 @@
+"""Drive the device path (through the C ABI) and the CPU oracle on the same
+seeded inputs, one decode step at a time, and compare them.
+
+Comparison rules
+----------------
+* Attention mass, importance, token scores and page scores: within
+  REL = 1e-5 relative (float32 accumulation on the device, float64 in the
+  oracle), with an absolute floor ABS for values that underflow in float32.
+* Refresh clocks: equal, except for tokens whose oracle mass lies within
+  REL * tau of tau: either decision is correct there (excused, counted).
+* Evicted page serials: equal, except for pages whose oracle page score lies
+  within REL of the oracle's eviction threshold (the largest evicted score),
+  or pages holding an excused token: there several answers are correct.  The
+  device's own selection must in any case be the ascending-(score, serial)
+  prefix of its own scores that meets the budget (checked here, in the test).
+* After a comparison the oracle's discrete decisions are carried to the
+  device when an excusal let them differ: the oracle's refresh clock is
+  written over the device's for excused tokens, and md_compact applies the
+  oracle's eviction list.  Data only flows from the oracle to the device.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2607_10582_amd.cache import MemDecay, PagedCache
+from synth import configs as C
+from synth import generator as g
+
+REL = 1e-5
+ABS = 1e-30
+
+
+def f32(x) -> float:
+    return float(np.float32(x))
+
+
+def bits_to_torch(bits: np.ndarray, device) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(device).view(torch.bfloat16)
+
+
+def torch_to_bits(t: torch.Tensor) -> np.ndarray:
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def rel_err(got: np.ndarray, ref: np.ndarray) -> np.ndarray:
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    return np.abs(got - ref) / np.maximum(np.abs(ref), ABS / REL)
+
+
+def check_selection_prefix(scores, serials, sizes, pinned, n, budget, P, evicted, infeasible):
+    """Selection invariants on one side's own scores (no oracle involved)."""
+    ev = set(int(x) for x in evicted)
+    cand = [i for i in range(len(serials)) if not pinned[i]]
+    assert all(int(serials[i]) in ev for i in cand) if infeasible else True
+    assert not any(int(serials[i]) in ev for i in range(len(serials)) if pinned[i])
+    removed = sum(int(sizes[i]) for i in range(len(serials)) if int(serials[i]) in ev)
+    if not infeasible:
+        assert n - removed <= budget
+        if ev:
+            assert n - removed > budget - P
+            order = sorted(cand, key=lambda i: (float(scores[i]), int(serials[i])))
+            k = len(ev)
+            assert set(int(serials[i]) for i in order[:k]) == ev
+    else:
+        assert n - removed > budget
+
+
+@dataclass
+class Stats:
+    steps: int = 0
+    tokens: int = 0
+    max_rel: Dict[str, float] = field(default_factory=lambda: {"abar": 0.0, "a": 0.0, "score": 0.0,
+                                                               "page": 0.0})
+    tau_excused: int = 0
+    tie_excused: int = 0
+    evicted_pages: int = 0
+
+    def bump(self, key, arr):
+        if arr.size:
+            self.max_rel[key] = max(self.max_rel[key], float(np.max(arr)))
+
+
+class Pair:
+    """One workload on the device and in the oracle (for ``oracle_sessions``)."""
+
+    def __init__(self, w: C.Workload, *, device="cuda", backend="numpy",
+                 oracle_sessions: Optional[List[int]] = None, n0s=None, budgets=None,
+                 regions=None, planted: int = 0, planted_strength=3.0, query_gain=0.0,
+                 pinned_mask=None, alpha=None, n_phys_extra: int = 0, max_pages=None,
+                 steps=None):
+        self.w = w
+        self.dev = torch.device(device)
+        self.backend = backend
+        self.steps = w.steps if steps is None else steps
+        self.n0s = g.prefix_lengths(w) if n0s is None else np.asarray(n0s, np.int64)
+        S = len(self.n0s)
+        assert S == w.S
+        self.B = g.budgets(w, self.n0s) if budgets is None else np.asarray(budgets, np.int64)
+        self.b, self.lam = g.region_priors(w)
+        self.pinned_mask = w.pinned_mask if pinned_mask is None else pinned_mask
+        self.alpha = w.alpha if alpha is None else alpha
+        self.oracle_sessions = list(range(S)) if oracle_sessions is None else list(oracle_sessions)
+        self.query_gain = query_gain
+        self.planted = planted
+        P = w.P
+        w_steps = C.with_overrides(w, steps=self.steps)
+        n_phys = g.pages_needed(w_steps, self.n0s) + n_phys_extra
+        mp = max(int(np.max((self.n0s + self.steps + P - 1) // P)) + 1, 1) if max_pages is None else max_pages
+        self.cache = PagedCache(L=w.L, Hq=w.Hq, Hkv=w.Hkv, d=w.d, P=P, S=S, max_pages=mp,
+                                n_phys=n_phys, device=self.dev)
+        perm = g.page_permutation(w, n_phys)
+        pos = 0
+        self.oracles: Dict[int, oracle.Session] = {}
+        for s in range(S):
+            n0 = int(self.n0s[s])
+            reg = g.region_spans(w, s, n0) if regions is None else np.asarray(regions[s], np.uint8)
+            m = (n0 + P - 1) // P
+            ids = perm[pos:pos + m]
+            pos += m
+            if backend == "numpy":
+                kb = g.k_prefix(w, s, n0)
+                if planted:
+                    toks = g.planted_tokens(w, s, n0, planted)
+                    kb = g.planted_keys(w, s, kb, toks, planted_strength)
+                kt = bits_to_torch(kb, self.dev)
+            else:
+                kt = g.torch_keys(w, s, n0, self.dev)
+                kb = torch_to_bits(kt) if s in self.oracle_sessions else None
+            if n0:
+                self.cache.load_session(s, kt.view(n0, w.L, w.Hkv, w.d), reg, ids,
+                                        budget=int(self.B[s]), clock=n0)
+            else:
+                self.cache.budget[s] = int(self.B[s])
+                self.cache.clock[s] = 0
+            del kt
+            if s in self.oracle_sessions:
+                self.oracles[s] = oracle.Session(
+                    L=w.L, Hq=w.Hq, Hkv=w.Hkv, d=w.d, P=P, b=self.b[s], lam=self.lam[s],
+                    alpha=f32(self.alpha), rho=f32(w.rho), tau_scale=f32(w.tau_scale),
+                    pinned_mask=self.pinned_mask, budget=int(self.B[s]), clock=n0, region=reg,
+                    keys_bits=kb if n0 else np.zeros((0, w.L, w.Hkv, w.d), np.uint16),
+                    capacity=n0 + self.steps)
+        self.cache.set_free_pages(perm[pos:][::-1])
+        self.md = MemDecay(self.cache, torch.from_numpy(self.b), torch.from_numpy(self.lam),
+                           rho=f32(w.rho), alpha=f32(self.alpha), tau_scale=f32(w.tau_scale),
+                           pinned_mask=self.pinned_mask)
+        n_slots = n_phys * P
+        self.abar = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
+        self.tscore = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
+        self.stats = Stats()
+        self.k = 0
+
+    # -------------------------------------------------------------- inputs
+    def inputs(self, k: int):
+        w, S = self.w, self.w.S
+        reg = np.full(S, g.append_region(w, k), dtype=np.uint8)
+        if self.backend == "numpy":
+            q = np.stack([g.q_step(w, s, k) for s in range(S)])
+            if self.query_gain:
+                q = np.stack([g.planted_query(w, s, q[s], self.query_gain) for s in range(S)])
+            nk = np.stack([g.k_append(w, s, k) for s in range(S)])
+            qt = torch.from_numpy(q).to(self.dev)
+            nkt = bits_to_torch(nk, self.dev)
+            qo = {s: q[s] for s in self.oracle_sessions}
+            nko = {s: nk[s] for s in self.oracle_sessions}
+        else:
+            qt = g.torch_queries(w, k, self.dev)
+            nkt = g.torch_append_keys(w, k, self.dev)
+            qo = {s: qt[s].cpu().numpy() for s in self.oracle_sessions}
+            nb = torch_to_bits(nkt)
+            nko = {s: nb[s] for s in self.oracle_sessions}
+        return qt, nkt, torch.from_numpy(reg).to(self.dev), qo, nko, reg
+
+    # -------------------------------------------------------------- one step
+    def step(self, compare: bool = True):
+        self.k += 1
+        k = self.k
+        w, P, S = self.w, self.w.P, self.w.S
+        qt, nkt, regt, qo, nko, reg = self.inputs(k)
+        md = self.md
+        md.observe(k, qt, nkt, regt, abar_out=self.abar)
+        md.score(token_score=self.tscore)
+        md.select()
+        torch.cuda.synchronize(self.dev)
+        c = self.cache
+        host = {name: getattr(c, name).cpu().numpy() for name in
+                ("page_table", "page_serial", "n_pages", "n_tokens", "importance", "t_ref")}
+        abar = self.abar.cpu().numpy()
+        tsc = self.tscore.cpu().numpy()
+        psc = md.page_score.cpu().numpy()
+        ev_ser = md.evict_serial.cpu().numpy()
+        ev_cnt = md.evict_count.cpu().numpy()
+        infeas = md.infeasible.cpu().numpy()
+        final_ser = ev_ser.copy()
+        final_cnt = ev_cnt.copy()
+        tref_fix = []
+        for s in self.oracle_sessions:
+            rec = self.oracles[s].step(qo[s], nko[s], int(reg[s]))
+            if not compare:
+                continue
+            npg, nt = int(host["n_pages"][s]), int(host["n_tokens"][s])
+            assert nt == rec.n, (k, s, nt, rec.n)
+            ptab = host["page_table"][s, :npg].astype(np.int64)
+            pser = host["page_serial"][s, :npg]
+            assert pser.tolist() == rec.page_serial.tolist(), (k, s)
+            slots = (ptab[:, None] * P + np.arange(P)[None, :]).reshape(-1)[:nt]
+            st = self.stats
+            st.tokens += nt
+            # attention mass and importance
+            e = rel_err(abar[slots], rec.abar)
+            st.bump("abar", e)
+            assert np.all(e <= REL), (k, s, "abar", float(e.max()), int(np.argmax(e)))
+            e = rel_err(host["importance"].reshape(-1)[slots], rec.a)
+            st.bump("a", e)
+            assert np.all(e <= REL), (k, s, "a", float(e.max()))
+            # refresh decisions
+            band = np.abs(rec.abar - rec.tau) <= REL * rec.tau
+            tref_g = host["t_ref"].reshape(-1)[slots]
+            mism = tref_g != rec.t_ref
+            assert not np.any(mism & ~band), (k, s, "t_ref", np.flatnonzero(mism & ~band)[:5])
+            exc = mism & band
+            st.tau_excused += int(exc.sum())
+            if exc.any():
+                tref_fix.append((slots[exc], rec.t_ref[exc]))
+            # token scores
+            gs = tsc[slots]
+            pin = np.isinf(rec.score)
+            assert np.array_equal(np.isinf(gs), pin), (k, s, "pinned tokens")
+            ok = ~pin & ~exc
+            e = rel_err(gs[ok], rec.score[ok])
+            st.bump("score", e)
+            assert np.all(e <= REL), (k, s, "score", float(e.max()) if e.size else 0)
+            # page scores
+            gp = psc[s, :npg]
+            assert np.array_equal(np.isinf(gp), rec.page_pinned), (k, s, "pinned pages")
+            page_of = np.repeat(np.arange(npg), rec.page_size)
+            exc_pages = np.zeros(npg, bool)
+            exc_pages[page_of[exc]] = True
+            okp = ~rec.page_pinned & ~exc_pages
+            e = rel_err(gp[okp], rec.page_score[okp])
+            st.bump("page", e)
+            assert np.all(e <= REL), (k, s, "page score", float(e.max()) if e.size else 0)
+            # eviction
+            g_ev = ev_ser[s, :ev_cnt[s]]
+            assert np.all(np.diff(g_ev) > 0), (k, s, "evicted serials ascend")
+            assert bool(infeas[s]) == rec.infeasible, (k, s, "infeasible")
+            check_selection_prefix(gp, pser, rec.page_size, np.isinf(gp), nt, int(self.B[s]), P,
+                                   g_ev, bool(infeas[s]))
+            if g_ev.tolist() != rec.evicted.tolist():
+                diff = set(g_ev.tolist()) ^ set(rec.evicted.tolist())
+                thr = max((rec.page_score[i] for i in range(npg)
+                           if rec.page_serial[i] in set(rec.evicted.tolist())), default=0.0)
+                for ser_ in diff:
+                    i = int(np.flatnonzero(rec.page_serial == ser_)[0])
+                    near = abs(rec.page_score[i] - thr) <= REL * max(thr, ABS)
+                    assert near or exc_pages[i], (k, s, "eviction differs outside the tie band",
+                                                  ser_, rec.page_score[i], thr)
+                st.tie_excused += len(diff)
+            st.evicted_pages += len(rec.evicted)
+            final_ser[s, :] = 0
+            final_ser[s, :len(rec.evicted)] = rec.evicted
+            final_cnt[s] = len(rec.evicted)
+        for slots_, vals in tref_fix:
+            c.t_ref.view(-1)[torch.from_numpy(slots_).to(self.dev)] = \
+                torch.from_numpy(vals.astype(np.int32)).to(self.dev)
+        md.compact(torch.from_numpy(final_ser).to(self.dev), torch.from_numpy(final_cnt).to(self.dev))
+        torch.cuda.synchronize(self.dev)
+        if compare:
+            n_pages = c.n_pages.cpu().numpy()
+            n_tokens = c.n_tokens.cpu().numpy()
+            pser = c.page_serial.cpu().numpy()
+            for s in self.oracle_sessions:
+                o = self.oracles[s]
+                assert int(n_tokens[s]) == o.n_tokens(), (k, s, "n after compaction")
+                assert pser[s, :n_pages[s]].tolist() == [p.serial for p in o.pages], (k, s)
+        self.stats.steps += 1
+        return self.stats
+
+    def device_status(self) -> int:
+        return self.md.device_status()
+
+    def free_pages_consistent(self) -> bool:
+        """Live pages plus free pages account for every physical page."""
+        c = self.cache
+        npg = c.n_pages.cpu().numpy()
+        live = np.concatenate([c.page_table[s, :npg[s]].cpu().numpy() for s in range(c.S)] +
+                              [np.zeros(0, np.int32)])
+        fc = int(c.free_count.item())
+        free = c.free_list[:fc].cpu().numpy()
+        allp = np.concatenate([live, free])
+        return allp.size == c.n_phys and np.unique(allp).size == c.n_phys
+
+    def close(self):
+        self.md.close()

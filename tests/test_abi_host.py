@@ -1,0 +1,145 @@
+"""The C ABI on the host (no GPU needed): the library loads, exports every
+entry point include/memdecay.h declares, its ctypes mirror matches the
+header's struct layout, and argument validation rejects bad calls before
+any HIP call or launch."""
+import ctypes
+import os
+import re
+import subprocess
+import tempfile
+
+import pytest
+
+from paper_2607_10582_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "memdecay.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2607_10582_amd.build import build
+        build()
+    return B.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:md_status|int32_t|const char\*)\s+(md_[a-z_]+)\s*\(",
+                                 text, flags=re.M)))
+
+
+def test_header_declares_the_entry_points():
+    assert declared_functions() == sorted(B.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    nm = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True, text=True)
+    syms = set(l.split()[-1] for l in nm.stdout.splitlines() if l.strip())
+    for f in declared_functions():
+        assert f in syms, f
+        assert hasattr(lib, f)
+
+
+def test_abi_version_and_status_strings(lib):
+    assert B.md_abi_version() == 1
+    for st in (0, -1, -2, -3, -4, -5, -6):
+        assert B.md_status_str(st)
+    assert B.md_status_str(12345) == "unknown status"
+
+
+def test_struct_layout_matches_the_header(lib):
+    src = r'''
+    #include <stdio.h>
+    #include <stddef.h>
+    #include "memdecay.h"
+    int main(void) {
+      printf("%zu %zu %zu %zu %zu\n", sizeof(md_config), offsetof(md_config, rho),
+             offsetof(md_config, reserved), sizeof(md_region_params), sizeof(md_cache_view));
+      printf("%zu %zu\n", offsetof(md_cache_view, importance), offsetof(md_cache_view, free_count));
+      return 0; }
+    '''
+    with tempfile.TemporaryDirectory() as d:
+        c = os.path.join(d, "layout.c")
+        exe = os.path.join(d, "layout")
+        open(c, "w").write(src)
+        subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), c, "-o", exe], check=True)
+        out = subprocess.run([exe], capture_output=True, text=True, check=True).stdout.split()
+    got = [ctypes.sizeof(B.md_config), B.md_config.rho.offset, B.md_config.reserved.offset,
+           ctypes.sizeof(B.md_region_params), ctypes.sizeof(B.md_cache_view),
+           B.md_cache_view.importance.offset, B.md_cache_view.free_count.offset]
+    assert [int(x) for x in out] == got
+
+
+def good_config(**kw):
+    c = dict(n_layers=28, n_q_heads=12, n_kv_heads=2, head_dim=128, page_size=16,
+             max_sessions=16, max_pages=2100, n_phys_pages=40000, n_regions=7,
+             pinned_region_mask=1, rho=0.9, alpha=1.0, tau_scale=2.0, reserved=0)
+    c.update(kw)
+    return B.md_config(**c)
+
+
+def fake_view(**kw):
+    v = B.md_cache_view()
+    for i, (name, _) in enumerate(B.md_cache_view._fields_):
+        setattr(v, name, 0x10000 * (i + 1))
+    for k, val in kw.items():
+        setattr(v, k, val)
+    return v
+
+
+def fake_rp():
+    return B.md_region_params(base_priority=0x900000, decay_rate=0x910000)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(head_dim=64), B.MD_E_UNSUPPORTED),
+    (dict(page_size=32), B.MD_E_UNSUPPORTED),
+    (dict(page_size=0), B.MD_E_UNSUPPORTED),
+    (dict(n_q_heads=13), B.MD_E_INVALID),
+    (dict(n_q_heads=34, n_kv_heads=2), B.MD_E_UNSUPPORTED),
+    (dict(n_layers=100, n_q_heads=12), B.MD_E_UNSUPPORTED),
+    (dict(max_sessions=0), B.MD_E_INVALID),
+    (dict(max_sessions=1025), B.MD_E_UNSUPPORTED),
+    (dict(max_pages=8193), B.MD_E_UNSUPPORTED),
+    (dict(n_phys_pages=0), B.MD_E_INVALID),
+    (dict(n_regions=0), B.MD_E_INVALID),
+    (dict(n_regions=33), B.MD_E_INVALID),
+    (dict(pinned_region_mask=1 << 7), B.MD_E_INVALID),
+    (dict(rho=1.0), B.MD_E_INVALID),
+    (dict(rho=-0.1), B.MD_E_INVALID),
+    (dict(rho=float("nan")), B.MD_E_INVALID),
+    (dict(alpha=-1.0), B.MD_E_INVALID),
+    (dict(alpha=float("inf")), B.MD_E_INVALID),
+    (dict(tau_scale=-2.0), B.MD_E_INVALID),
+    (dict(reserved=1), B.MD_E_INVALID),
+])
+def test_init_rejects_bad_configs_on_the_host(lib, kw, expect):
+    st, h = B.md_init_raw(good_config(**kw), fake_rp(), fake_view(), 0)
+    assert st == expect and h is None
+
+
+@pytest.mark.parametrize("field", [f for f, _ in B.md_cache_view._fields_])
+def test_init_rejects_null_buffers(lib, field):
+    st, h = B.md_init_raw(good_config(), fake_rp(), fake_view(**{field: 0}), 0)
+    assert st == B.MD_E_INVALID
+
+
+def test_init_rejects_misaligned_buffers(lib):
+    assert B.md_init_raw(good_config(), fake_rp(), fake_view(k_pool=0x10008), 0)[0] == B.MD_E_INVALID
+    assert B.md_init_raw(good_config(), fake_rp(), fake_view(t_ref=0x10002), 0)[0] == B.MD_E_INVALID
+    rp = B.md_region_params(base_priority=0, decay_rate=0x910000)
+    assert B.md_init_raw(good_config(), rp, fake_view(), 0)[0] == B.MD_E_INVALID
+
+
+def test_calls_reject_a_null_handle(lib):
+    L = lib
+    assert L.md_observe_step(None, 1, 0x1000, None, None, None) == B.MD_E_INVALID
+    assert L.md_score_pages(None, None, None) == B.MD_E_INVALID
+    assert L.md_select_evict(None, 0x1000, 0x1000, 0x1000) == B.MD_E_INVALID
+    assert L.md_compact(None, 0x1000, 0x1000) == B.MD_E_INVALID
+    assert L.md_destroy(None) == B.MD_E_INVALID
+    out = ctypes.c_int32()
+    assert L.md_read_device_status(None, ctypes.byref(out)) == B.MD_E_INVALID
+    assert L.md_init(None, None, None, None, None) == B.MD_E_INVALID

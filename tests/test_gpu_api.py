@@ -1,0 +1,127 @@
+"""C-ABI behaviour on the device: call order, step numbering, device status
+bits (capacity, non-finite queries), and re-binding a saved cache."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_10582_amd import binding as B
+from synth import configs as C
+
+from harness import Pair
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a ROCm device")
+    B.load_library()
+
+
+def small_pair(**kw):
+    return Pair(C.with_overrides(C.get("small"), steps=8), **kw)
+
+
+def test_call_order_and_step_numbering():
+    p = small_pair(oracle_sessions=[])
+    md = p.md
+    q, nk, reg, *_ = p.inputs(1)
+    with pytest.raises(B.MemDecayError) as e:
+        md.score()
+    assert e.value.status == B.MD_E_STATE
+    with pytest.raises(B.MemDecayError) as e:
+        md.select()
+    assert e.value.status == B.MD_E_STATE
+    md.observe(5, q, nk, reg)
+    with pytest.raises(B.MemDecayError) as e:
+        md.observe(7, q, nk, reg)                 # must be 6
+    assert e.value.status == B.MD_E_STEP
+    with pytest.raises(B.MemDecayError) as e:
+        md.select()                               # needs a score first
+    assert e.value.status == B.MD_E_STATE
+    md.score()
+    md.select()
+    md.select()                                   # idempotent
+    md.compact()
+    with pytest.raises(B.MemDecayError) as e:
+        md.select()
+    assert e.value.status == B.MD_E_STATE
+    md.observe(6, q, nk, reg)
+    torch.cuda.synchronize()
+    assert md.device_status() == 0
+    p.close()
+
+
+def test_free_list_exhaustion_sets_capacity():
+    # 448 prompt tokens fill 28 pages exactly, so the first append needs a
+    # page from the (empty) free list: nothing is appended, the bit is set.
+    p = small_pair(oracle_sessions=[], n0s=[448], budgets=[448])
+    c = p.cache
+    c.free_count.zero_()
+    for k in range(1, 3):
+        q, nk, reg, *_ = p.inputs(k)
+        p.md.observe(k, q, nk, reg)
+        p.md.score()
+    torch.cuda.synchronize()
+    assert int(c.n_tokens[0].item()) == 448 and int(c.n_pages[0].item()) == 28
+    assert p.md.device_status() == B.MD_DEV_CAPACITY
+    assert int(c.free_count.item()) == 0
+    assert int(c.clock[0].item()) == 448 + 2
+    p.close()
+
+
+def test_nonfinite_query_sets_status():
+    p = small_pair(oracle_sessions=[])
+    q, nk, reg, *_ = p.inputs(1)
+    q[0, 0, 3, 17] = float("nan")
+    p.md.observe(1, q, nk, reg)
+    torch.cuda.synchronize()
+    assert p.md.device_status() & B.MD_DEV_NONFINITE
+    assert p.md.device_status() == 0              # reading clears the word
+    p.close()
+
+
+def test_bad_eviction_serial_sets_status():
+    p = small_pair(oracle_sessions=[])
+    q, nk, reg, *_ = p.inputs(1)
+    p.md.observe(1, q, nk, reg)
+    p.md.score()
+    ev = torch.zeros_like(p.md.evict_serial)
+    ev[0, 0] = 9999
+    cnt = torch.ones_like(p.md.evict_count)
+    n_before = int(p.cache.n_pages[0].item())
+    p.md.compact(ev, cnt)
+    torch.cuda.synchronize()
+    assert p.md.device_status() == B.MD_DEV_BAD_EVICT
+    assert int(p.cache.n_pages[0].item()) == n_before
+    p.close()
+
+
+def test_state_lives_in_caller_buffers():
+    # Snapshot every caller-owned buffer mid-run, run on, restore into a new
+    # handle, run the same steps again: identical results.
+    w = C.with_overrides(C.get("small"), steps=12)
+    p = Pair(w, oracle_sessions=[])
+    for _ in range(4):
+        p.step(compare=False)
+    names = ("k_pool", "region", "t_ins", "t_ref", "importance", "page_table", "page_serial",
+             "n_pages", "n_tokens", "clock", "next_serial", "budget", "free_list", "free_count")
+    snap = {n: getattr(p.cache, n).clone() for n in names}
+    first = []
+    for _ in range(4):
+        p.step(compare=False)
+        m = int(p.cache.n_pages[0].item())
+        first.append(p.md.page_score[0, :m].clone())
+    for n in names:
+        getattr(p.cache, n).copy_(snap[n])
+    p.md.close()
+    from paper_2607_10582_amd.cache import MemDecay
+    p.md = MemDecay(p.cache, torch.from_numpy(p.b), torch.from_numpy(p.lam), rho=0.9,
+                    alpha=1.0, tau_scale=2.0, pinned_mask=1)
+    p.k = 4
+    for i in range(4):
+        p.step(compare=False)
+        m = int(p.cache.n_pages[0].item())
+        assert torch.equal(p.md.page_score[0, :m].view(torch.int32), first[i].view(torch.int32))
+    p.close()
