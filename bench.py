@@ -1,0 +1,279 @@
+#!/usr/bin/env python3
+"""Benchmark of MemDecay's per-decode-step retention path on one MI355X.
+
+A step is the whole path over one batch: md_observe_step (append, attention
+mass, EWMA, refresh), md_score_pages (token and page scores), md_select_evict
+(budgeted page selection) and md_compact (page-table compaction).  All inputs
+(the paged key cache, every step's queries and appended keys) are resident in
+HBM before timing starts.  The default workload is 16 sessions of 32,768
+cached tokens with Qwen2.5-1.5B's attention shape (28 layers, 12 query / 2 KV
+heads, d = 128), 16-token pages and a 25 % budget.  The warm-up steps include
+the first step's bulk eviction (32,768 -> 8,192 tokens per session); the
+timed steps are the steady state that follows.
+
+Printed on stdout: one JSON line.  value = tokens scored per second (the
+sum over sessions and timed steps of the cached tokens scored, divided by
+the wall time of the timed steps); roofline = the attention-logits kernel's
+algorithmic bytes per launch over its event-timed average duration, against
+MI355X's 8 TB/s; cpu_baseline = the CPU oracle on one session of the same
+workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "cached tokens scored+evicted per second per decode step; achieved HBM GB/s vs peak"
+PEAK_HBM_GBS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2607_10582_amd", "csrc", "md_kernels.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def describe(w, n0s) -> str:
+    n = f"{int(n0s[0])}" if len(set(n0s.tolist())) == 1 else f"U[{w.n0_range[0]},{w.n0_range[1]}]"
+    return (f"{w.name}: {w.S} sessions x {n} cached tokens, {w.L} layers, {w.Hq}/{w.Hkv} heads, "
+            f"d {w.d}, pages of {w.P}, budget {int(w.budget_frac * 100)}%")
+
+
+def setup(w, steps_total, dev):
+    import torch
+    from paper_2607_10582_amd.cache import MemDecay, PagedCache
+    from synth import configs as C
+    from synth import generator as g
+
+    n0s = g.prefix_lengths(w)
+    B = g.budgets(w, n0s)
+    b, lam = g.region_priors(w)
+    ws = C.with_overrides(w, steps=max(steps_total, 1))
+    n_phys = g.pages_needed(ws, n0s)
+    max_pages = int(np.max((n0s + steps_total + w.P - 1) // w.P)) + 1
+    cache = PagedCache(L=w.L, Hq=w.Hq, Hkv=w.Hkv, d=w.d, P=w.P, S=w.S, max_pages=max_pages,
+                       n_phys=n_phys, device=dev)
+    perm = g.page_permutation(w, n_phys)
+    pos = 0
+    for s in range(w.S):
+        n0 = int(n0s[s])
+        m = (n0 + w.P - 1) // w.P
+        keys = g.torch_keys(w, s, n0, dev)
+        cache.load_session(s, keys, g.region_spans(w, s, n0), perm[pos:pos + m],
+                           budget=int(B[s]), clock=n0)
+        pos += m
+        del keys
+    cache.set_free_pages(perm[pos:][::-1])
+    md = MemDecay(cache, torch.from_numpy(b), torch.from_numpy(lam), rho=w.rho, alpha=w.alpha,
+                  tau_scale=w.tau_scale, pinned_mask=w.pinned_mask)
+    inputs = []
+    for k in range(1, steps_total + 1):
+        q = g.torch_queries(w, k, dev)
+        nk = g.torch_append_keys(w, k, dev)
+        reg = torch.full((w.S,), g.append_region(w, k), dtype=torch.uint8, device=dev)
+        inputs.append((q, nk, reg))
+    torch.cuda.synchronize(dev)
+    return n0s, B, cache, md, inputs
+
+
+def cpu_baseline(w, n0s, B, budget_s: float, max_steps: int):
+    """The CPU oracle, as it stands, on session 0 of the workload: step 1 (the
+    bulk eviction) untimed, then steady steps timed until ``budget_s``."""
+    import torch
+    import oracle
+    from synth import generator as g
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([1] + [int(i.get("num_threads", 1)) for i in threadpool_info()])
+    except Exception:
+        threads = 1
+    b, lam = g.region_priors(w)
+    n0 = int(n0s[0])
+    dev = torch.device("cuda:0")
+    kb = g.torch_keys(w, 0, n0, dev).view(torch.int16).cpu().numpy().view(np.uint16)
+    sess = oracle.session_from_workload(w, 0, region=g.region_spans(w, 0, n0), keys_bits=kb,
+                                        b=b[0], lam=lam[0], budget=int(B[0]),
+                                        capacity=n0 + max_steps)
+    del kb
+
+    def inputs(k):
+        q = g.torch_queries(w, k, dev)[0].cpu().numpy()
+        nk = g.torch_append_keys(w, k, dev)[0].view(torch.int16).cpu().numpy().view(np.uint16)
+        return q, nk, g.append_region(w, k)
+
+    sess.step(*inputs(1))
+    scored = 0
+    steps = 0
+    elapsed = 0.0
+    k = 2
+    while elapsed < budget_s and k <= max_steps:
+        q, nk, r = inputs(k)
+        t0 = time.perf_counter()
+        rec = sess.step(q, nk, r)
+        elapsed += time.perf_counter() - t0
+        scored += rec.n
+        steps += 1
+        k += 1
+    return {"value": scored / elapsed, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"session 0 of {w.S} ({w.name}), {steps} steady decode steps (steps 2-{k - 1}, "
+                      f"after the bulk eviction), {scored} token-steps in {elapsed:.1f} s, numpy float64",
+            "seconds_per_step": elapsed / max(steps, 1)}
+
+
+def load_traffic(workload: str, avg_launch_bytes: float):
+    """Counter-measured HBM bytes per launch of the logits kernel, if a
+    profile of the current kernel source exists."""
+    path = os.path.join(ROOT, "profiles", f"k_logits_{workload}_pmc.json")
+    if not os.path.exists(path):
+        return None, None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None, "stale"
+    return d.get("hbm_bytes_per_launch"), path
+
+
+def calibrate_copy(mib: int):
+    """A plain device copy of known size, for scaling the FETCH_SIZE /
+    WRITE_SIZE counters."""
+    import torch
+    n = mib * (1 << 20)
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copied {n} bytes 5 times")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="long32k")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the retention path shards over sessions with no "
+              f"exchange, and this build measures the one-GPU share (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
+
+    import torch
+    from paper_2607_10582_amd import binding
+    from synth import configs as C
+
+    binding.load_library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = C.get(args.workload)
+    W, K = args.warmup, args.steps
+    if W + K > w.steps:
+        log(f"note: {W + K} steps asked, the workload defines {w.steps} decode steps")
+    t_setup = time.perf_counter()
+    n0s, B, cache, md, inputs = setup(w, W + K, dev)
+    log(f"setup {time.perf_counter() - t_setup:.1f} s: {describe(w, n0s)}")
+
+    for k in range(1, W + 1):
+        q, nk, reg = inputs[k - 1]
+        md.step(k, q, nk, reg)
+    torch.cuda.synchronize(dev)
+    c0 = md.counters()
+    md.profile(("logits",))
+    stream = md.stream
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for k in range(W + 1, W + K + 1):
+        q, nk, reg = inputs[k - 1]
+        md.step(k, q, nk, reg)
+    ev1.record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    logits_ms, launches = md.profile_read("logits")
+    md.profile(())
+    c1 = md.counters()
+    status = md.device_status()
+    if status != 0:
+        log(f"device status {status:#x}")
+        sys.exit(1)
+
+    scored = c1[0] - c0[0]
+    evicted_tokens = c1[3] - c0[3]
+    evicted_pages = c1[2] - c0[2]
+    kb = w.k_bytes_per_token
+    q_bytes = w.S * w.L * w.Hq * w.d * 4
+    logits_bytes = scored * kb + K * q_bytes              # algorithmic, over the timed launches
+    avg_launch_s = logits_ms / 1e3 / max(launches, 1)
+    per_launch_bytes = logits_bytes / max(launches, 1)
+    achieved = per_launch_bytes / avg_launch_s / 1e9
+    traffic, traffic_src = load_traffic(w.name, per_launch_bytes)
+    # whole step: K + per-token state (region 1, a 4+4, t_ref 4+4) + per-page
+    # score and page-table entry + the queries
+    step_bytes = scored * (kb + 17) + scored // w.P * 8 + K * q_bytes
+
+    line = {
+        "metric": METRIC,
+        "value": scored / wall,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": wall * 1e3 / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": describe(w, n0s), "sessions": w.S,
+                   "cached_tokens_per_session": int(n0s[0]) if w.n0 else "ragged",
+                   "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.d,
+                   "page_size": w.P, "budget_frac": w.budget_frac, "parallelism": "none"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
+                     "kernel": "k_logits", "launches": launches,
+                     "avg_launch_us": avg_launch_s * 1e6,
+                     "algorithmic_bytes_per_launch": per_launch_bytes},
+        "tokens_scored_per_step": scored / K,
+        "tokens_evicted_per_step": evicted_tokens / K,
+        "pages_evicted": evicted_pages,
+        "gpu_event_ms_per_step": gpu_ms / K,
+        "step_algorithmic_gbs": step_bytes / wall / 1e9,
+        "step_frac_of_peak": step_bytes / wall / 1e9 / PEAK_HBM_GBS,
+    }
+    md.close()
+    del cache, inputs
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, n0s, B, args.cpu_seconds, w.steps)
+    else:
+        line["cpu_baseline"] = None
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -204,6 +204,25 @@ md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* ev
  * clear it.  Returns MD_E_HIP if the stream reports an error. */
 md_status md_read_device_status(md_handle h, int32_t* host_out);
 
+/* Kernel ids for md_profile_enable / md_profile_read. */
+enum {
+    MD_K_APPEND = 0, MD_K_LOGITS = 1, MD_K_ROWSTATS = 2, MD_K_MASS = 3,
+    MD_K_SCORE = 4, MD_K_SELECT = 5, MD_K_COMPACT = 6, MD_K_COUNT = 7
+};
+
+/* Diagnostics.  md_profile_enable: from now on, bracket every launch of the
+ * kernels whose bit (1 << id) is set in kernel_mask with a pair of hipEvents
+ * on the handle's stream (0 turns timing off).  md_profile_read: synchronise,
+ * return the summed duration in milliseconds and the number of timed launches
+ * of kernel `kernel` since the last read, and reset them. */
+md_status md_profile_enable(md_handle h, uint32_t kernel_mask);
+md_status md_profile_read(md_handle h, int32_t kernel, double* total_ms, int64_t* launches);
+
+/* Device-side running totals since md_init, read after synchronising:
+ * out[0] tokens scored (sum over steps and sessions of |K_t|), out[1] steps
+ * observed, out[2] pages evicted, out[3] tokens evicted. */
+md_status md_read_counters(md_handle h, int64_t* out);
+
 /* Release the scratch and the handle (synchronises the stream first). */
 md_status md_destroy(md_handle h);
 

@@ -26,7 +26,11 @@ MD_DEV_CORRUPT = 0x8
 
 EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_observe_step",
            "md_score_pages", "md_select_evict", "md_compact", "md_read_device_status",
-           "md_destroy")
+           "md_profile_enable", "md_profile_read", "md_read_counters", "md_destroy")
+
+# kernel ids of md_profile_enable / md_profile_read
+KERNELS = ("append", "logits", "rowstats", "mass", "score", "select", "compact")
+MD_K_APPEND, MD_K_LOGITS, MD_K_ROWSTATS, MD_K_MASS, MD_K_SCORE, MD_K_SELECT, MD_K_COMPACT = range(7)
 
 
 class md_config(ctypes.Structure):
@@ -85,6 +89,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.md_compact.argtypes = [vp, vp, vp]
     lib.md_read_device_status.restype = i32
     lib.md_read_device_status.argtypes = [vp, ctypes.POINTER(i32)]
+    lib.md_profile_enable.restype = i32
+    lib.md_profile_enable.argtypes = [vp, ctypes.c_uint32]
+    lib.md_profile_read.restype = i32
+    lib.md_profile_read.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_double),
+                                    ctypes.POINTER(ctypes.c_int64)]
+    lib.md_read_counters.restype = i32
+    lib.md_read_counters.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
     lib.md_destroy.restype = i32
     lib.md_destroy.argtypes = [vp]
     _lib = lib
@@ -143,6 +154,26 @@ def md_read_device_status(h: int) -> int:
     out = ctypes.c_int32(0)
     _check("md_read_device_status", load_library().md_read_device_status(h, ctypes.byref(out)))
     return out.value
+
+
+def md_profile_enable(h: int, kernel_mask: int) -> int:
+    return _check("md_profile_enable", load_library().md_profile_enable(h, kernel_mask))
+
+
+def md_profile_read(h: int, kernel: int):
+    """(total milliseconds, launches) of ``kernel`` since the last read."""
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_int64(0)
+    _check("md_profile_read", load_library().md_profile_read(h, kernel, ctypes.byref(ms),
+                                                             ctypes.byref(n)))
+    return ms.value, n.value
+
+
+def md_read_counters(h: int):
+    """(tokens scored, steps observed, pages evicted, tokens evicted) since md_init."""
+    out = (ctypes.c_int64 * 4)()
+    _check("md_read_counters", load_library().md_read_counters(h, out))
+    return tuple(int(x) for x in out)
 
 
 def md_destroy(h: int) -> int:

@@ -155,6 +155,19 @@ class MemDecay:
     def device_status(self) -> int:
         return B.md_read_device_status(self.handle)
 
+    def profile(self, kernels=("logits",)):
+        """Time the named kernels with events from now on (() turns it off)."""
+        mask = 0
+        for k in kernels:
+            mask |= 1 << B.KERNELS.index(k)
+        B.md_profile_enable(self.handle, mask)
+
+    def profile_read(self, kernel: str):
+        return B.md_profile_read(self.handle, B.KERNELS.index(kernel))
+
+    def counters(self):
+        return B.md_read_counters(self.handle)
+
     def close(self):
         if self.handle is not None:
             B.md_destroy(self.handle)

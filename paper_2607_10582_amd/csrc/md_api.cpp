@@ -20,6 +20,10 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 }  // namespace
 
+struct Timed {
+    hipEvent_t start, stop;
+};
+
 struct md_handle_s {
     md::Dims dm;
     md::View v;
@@ -33,7 +37,48 @@ struct md_handle_s {
     bool have_step;
     int32_t last_step;
     Phase phase;
+    uint32_t profile_mask;
+    std::vector<Timed> pending[MD_K_COUNT];   // launches not yet read back
+    std::vector<Timed> spare;                  // recycled event pairs
 };
+
+namespace {
+
+// Launch through `fn`, bracketed by an event pair when kernel `id` is timed.
+template <typename F>
+hipError_t timed_launch(md_handle_s* h, int id, F&& fn) {
+    if (!(h->profile_mask & (1u << id))) return fn();
+    Timed t;
+    if (!h->spare.empty()) {
+        t = h->spare.back();
+        h->spare.pop_back();
+    } else {
+        if (hipEventCreate(&t.start) != hipSuccess) return hipErrorOutOfMemory;
+        if (hipEventCreate(&t.stop) != hipSuccess) {
+            (void)hipEventDestroy(t.start);
+            return hipErrorOutOfMemory;
+        }
+    }
+    hipError_t e = hipEventRecord(t.start, h->stream);
+    if (e == hipSuccess) e = fn();
+    if (e == hipSuccess) e = hipEventRecord(t.stop, h->stream);
+    if (e == hipSuccess) h->pending[id].push_back(t); else h->spare.push_back(t);
+    return e;
+}
+
+void release_events(md_handle_s* h) {
+    for (auto& v : h->pending) {
+        for (auto& t : v) h->spare.push_back(t);
+        v.clear();
+    }
+    for (auto& t : h->spare) {
+        (void)hipEventDestroy(t.start);
+        (void)hipEventDestroy(t.stop);
+    }
+    h->spare.clear();
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -171,6 +216,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     md::scratch_carve(dm, h->scratch, &h->sc);
     // counters and status start at zero; work lists empty until the first append
     if (hipMemsetAsync(h->sc.done, 0, 2 * sizeof(int32_t), hs) != hipSuccess ||
+        hipMemsetAsync(h->sc.counters, 0, 4 * sizeof(unsigned long long), hs) != hipSuccess ||
         hipMemsetAsync(h->sc.item_prefix, 0, (size_t)(dm.S + 1) * sizeof(int32_t), hs) != hipSuccess ||
         hipMemsetAsync(h->sc.tile_prefix, 0, (size_t)(dm.S + 1) * sizeof(int32_t), hs) != hipSuccess ||
         hipMemsetAsync(h->sc.valid, 0, (size_t)(dm.S + 1) * sizeof(int32_t), hs) != hipSuccess ||
@@ -186,6 +232,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     h->have_step = false;
     h->last_step = 0;
     h->phase = kNone;
+    h->profile_mask = 0;
     *out = h;
     return MD_OK;
 }
@@ -197,10 +244,14 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     if (abar_out != nullptr && !aligned(abar_out, 4)) return MD_E_INVALID;
     if (h->have_step && step != h->last_step + 1) return MD_E_STEP;
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
-    hipError_t e = md::launch_append(h->dm, h->v, h->sc, new_k, new_region, h->stream);
-    if (e == hipSuccess) e = md::launch_logits(h->dm, h->v, h->sc, q, h->logits_blocks, h->stream);
-    if (e == hipSuccess) e = md::launch_rowstats(h->dm, h->sc, h->stream);
-    if (e == hipSuccess) e = md::launch_mass(h->dm, h->v, h->sc, abar_out, h->mass_blocks, h->stream);
+    hipError_t e = timed_launch(h, MD_K_APPEND, [&] {
+        return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, h->stream); });
+    if (e == hipSuccess) e = timed_launch(h, MD_K_LOGITS, [&] {
+        return md::launch_logits(h->dm, h->v, h->sc, q, h->logits_blocks, h->stream); });
+    if (e == hipSuccess) e = timed_launch(h, MD_K_ROWSTATS, [&] {
+        return md::launch_rowstats(h->dm, h->sc, h->stream); });
+    if (e == hipSuccess) e = timed_launch(h, MD_K_MASS, [&] {
+        return md::launch_mass(h->dm, h->v, h->sc, abar_out, h->mass_blocks, h->stream); });
     if (e != hipSuccess) return MD_E_HIP;
     h->have_step = true;
     h->last_step = step;
@@ -215,7 +266,9 @@ md_status md_score_pages(md_handle h, float* page_score, float* token_score) {
         return MD_E_INVALID;
     if (h->phase != kObserved && h->phase != kScored) return MD_E_STATE;
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
-    if (md::launch_score(h->dm, h->v, h->sc, page_score, token_score, h->score_blocks, h->stream) != hipSuccess)
+    if (timed_launch(h, MD_K_SCORE, [&] {
+            return md::launch_score(h->dm, h->v, h->sc, page_score, token_score, h->score_blocks,
+                                    h->stream); }) != hipSuccess)
         return MD_E_HIP;
     h->phase = kScored;
     return MD_OK;
@@ -227,7 +280,9 @@ md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_cou
     if (!aligned(evict_serial, 4) || !aligned(evict_count, 4)) return MD_E_INVALID;
     if (h->phase != kScored) return MD_E_STATE;
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
-    if (md::launch_select(h->dm, h->v, h->sc, evict_serial, evict_count, infeasible, h->stream) != hipSuccess)
+    if (timed_launch(h, MD_K_SELECT, [&] {
+            return md::launch_select(h->dm, h->v, h->sc, evict_serial, evict_count, infeasible,
+                                     h->stream); }) != hipSuccess)
         return MD_E_HIP;
     return MD_OK;
 }
@@ -237,7 +292,9 @@ md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* ev
     if (!aligned(evict_serial, 4) || !aligned(evict_count, 4)) return MD_E_INVALID;
     if (h->phase == kNone) return MD_E_STATE;
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
-    if (md::launch_compact(h->dm, h->v, h->sc, evict_serial, evict_count, h->stream) != hipSuccess)
+    if (timed_launch(h, MD_K_COMPACT, [&] {
+            return md::launch_compact(h->dm, h->v, h->sc, evict_serial, evict_count, h->stream); }) !=
+        hipSuccess)
         return MD_E_HIP;
     h->phase = kCompacted;
     return MD_OK;
@@ -255,10 +312,47 @@ md_status md_read_device_status(md_handle h, int32_t* host_out) {
     return MD_OK;
 }
 
+md_status md_profile_enable(md_handle h, uint32_t kernel_mask) {
+    if (h == nullptr || (kernel_mask >> MD_K_COUNT) != 0) return MD_E_INVALID;
+    h->profile_mask = kernel_mask;
+    return MD_OK;
+}
+
+md_status md_profile_read(md_handle h, int32_t kernel, double* total_ms, int64_t* launches) {
+    if (h == nullptr || total_ms == nullptr || launches == nullptr || kernel < 0 || kernel >= MD_K_COUNT)
+        return MD_E_INVALID;
+    if (hipSetDevice(h->device) != hipSuccess || hipStreamSynchronize(h->stream) != hipSuccess)
+        return MD_E_HIP;
+    double sum = 0.0;
+    md_status st = MD_OK;
+    for (auto& t : h->pending[kernel]) {
+        float ms = 0.0f;
+        if (hipEventElapsedTime(&ms, t.start, t.stop) != hipSuccess) st = MD_E_HIP;
+        sum += ms;
+        h->spare.push_back(t);
+    }
+    *launches = (int64_t)h->pending[kernel].size();
+    h->pending[kernel].clear();
+    *total_ms = sum;
+    return st;
+}
+
+md_status md_read_counters(md_handle h, int64_t* out) {
+    if (h == nullptr || out == nullptr) return MD_E_INVALID;
+    if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    unsigned long long v[4] = {0, 0, 0, 0};
+    if (hipMemcpyAsync(v, h->sc.counters, sizeof(v), hipMemcpyDeviceToHost, h->stream) != hipSuccess ||
+        hipStreamSynchronize(h->stream) != hipSuccess)
+        return MD_E_HIP;
+    for (int i = 0; i < 4; ++i) out[i] = (int64_t)v[i];
+    return MD_OK;
+}
+
 md_status md_destroy(md_handle h) {
     if (h == nullptr) return MD_E_INVALID;
     md_status st = MD_OK;
     if (hipSetDevice(h->device) != hipSuccess || hipStreamSynchronize(h->stream) != hipSuccess) st = MD_E_HIP;
+    release_events(h);
     if (hipFree(h->scratch) != hipSuccess) st = MD_E_HIP;
     delete h;
     return st;

@@ -56,6 +56,7 @@ struct Scratch {
     int32_t* valid;        // [S] 1 when the session's counters are consistent
     int32_t* done;         // [1] completion counter of the append kernel
     int32_t* status;       // [1] device status word
+    unsigned long long* counters;  // [4] tokens scored, steps, pages evicted, tokens evicted
 };
 
 size_t scratch_bytes(const Dims& dm);

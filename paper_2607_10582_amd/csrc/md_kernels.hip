@@ -171,7 +171,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     if (!sh_last) return;
     __threadfence();
     int it[4], ti[4];
-    int my_items = 0, my_tiles = 0;
+    int my_items = 0, my_tiles = 0, my_tokens = 0;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int s2 = threadIdx.x * 4 + k;
@@ -186,13 +186,15 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             sc.valid[s2] = ok ? 1 : 0;
             it[k] = ch * dm.LHkv;
             ti[k] = ok ? (nt + kTile - 1) / kTile : 0;
+            my_tokens += ok ? nt : 0;
         }
         my_items += it[k];
         my_tiles += ti[k];
     }
-    int tot_i, tot_t;
+    int tot_i, tot_t, tot_n;
     int ex_i = block_exclusive_scan(my_items, lds, &tot_i);
     int ex_t = block_exclusive_scan(my_tiles, lds, &tot_t);
+    block_exclusive_scan(my_tokens, lds, &tot_n);
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int s2 = threadIdx.x * 4 + k;
@@ -207,6 +209,8 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         sc.item_prefix[dm.S] = tot_i;
         sc.tile_prefix[dm.S] = tot_t;
         *sc.done = 0;
+        atomicAdd(&sc.counters[0], (unsigned long long)tot_n);
+        atomicAdd(&sc.counters[1], 1ull);
     }
 }
 
@@ -780,8 +784,11 @@ __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratc
 #pragma unroll
         for (int k = 0; k < kPerThread; ++k)
             if (k == k_last) last_kept = keep[k];
+        const int nt_new = last_kept ? nt - gone_total * dm.P : kept_total * dm.P;
         v.n_pages[s] = kept_total;
-        v.n_tokens[s] = last_kept ? nt - gone_total * dm.P : kept_total * dm.P;
+        v.n_tokens[s] = nt_new;
+        atomicAdd(&sc.counters[2], (unsigned long long)gone_total);
+        atomicAdd(&sc.counters[3], (unsigned long long)(nt - nt_new));
     }
 }
 
@@ -803,6 +810,7 @@ size_t scratch_bytes(const Dims& dm) {
     n += align256((size_t)dm.S * dm.MP * sizeof(float));
     n += 4 * align256((size_t)(dm.S + 1) * sizeof(int32_t));
     n += align256(2 * sizeof(int32_t));
+    n += align256(4 * sizeof(unsigned long long));
     return n;
 }
 
@@ -824,6 +832,7 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
     int32_t* words = reinterpret_cast<int32_t*>(take(2 * sizeof(int32_t)));
     sc->done = words;
     sc->status = words + 1;
+    sc->counters = reinterpret_cast<unsigned long long*>(take(4 * sizeof(unsigned long long)));
 }
 
 }  // namespace md
