@@ -226,7 +226,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
         return MD_E_HIP;
     }
     const int n_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
-    h->logits_blocks = 2 * n_cu;
+    h->logits_blocks = 3 * n_cu;
     h->mass_blocks = 4 * n_cu;
     h->score_blocks = 2 * n_cu;
     h->have_step = false;

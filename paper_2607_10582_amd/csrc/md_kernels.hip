@@ -33,6 +33,11 @@ constexpr float kLogitScale = (float)(1.4426950408889634074 / 11.313708498984760
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
+// 2^x on the transcendental unit (v_exp_f32, about 1 ulp).  Results below
+// 2^-126 come out as zero or denormal; softmax weights that small are
+// negligible next to the row maximum's weight of 1.
+__device__ __forceinline__ float hw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
@@ -93,8 +98,25 @@ __device__ __forceinline__ bool counters_ok(int np, int nt, const Dims& dm) {
     return nt > (np - 1) * dm.P && nt <= np * dm.P;
 }
 
+// Split a float32 into three bfloat16 terms with x == hi + mid + lo exactly:
+// hi and mid truncate (the differences are exact by Sterbenz's lemma), and
+// what is left has at most 8 significant bits, so lo holds it exactly.
+__device__ __forceinline__ void split3(float x, uint32_t& hi, uint32_t& mid, uint32_t& lo) {
+    const uint32_t u = __float_as_uint(x);
+    const uint32_t h = u & 0xFFFF0000u;
+    const float r1 = x - __uint_as_float(h);
+    const uint32_t m = __float_as_uint(r1) & 0xFFFF0000u;
+    const float r2 = r1 - __uint_as_float(m);
+    hi = h >> 16;
+    mid = m >> 16;
+    lo = __float_as_uint(r2) >> 16;
+}
+
+
 // ---------------------------------------------------------------- append
 
+// One block per session: the append.  The last block to finish lays out the
+// step's work lists.
 __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                                                 const uint16_t* __restrict__ new_k,
                                                 const uint8_t* __restrict__ new_region) {
@@ -222,194 +244,269 @@ hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
 
 // ---------------------------------------------------------------- logits
 
-// Split a float32 into three bfloat16 terms with x == hi + mid + lo exactly:
-// hi and mid truncate (the differences are exact by Sterbenz's lemma), and
-// what is left has at most 8 significant bits, so lo holds it exactly.
-__device__ __forceinline__ void split3(float x, uint32_t& hi, uint32_t& mid, uint32_t& lo) {
-    const uint32_t u = __float_as_uint(x);
-    const uint32_t h = u & 0xFFFF0000u;
-    const float r1 = x - __uint_as_float(h);
-    const uint32_t m = __float_as_uint(r1) & 0xFFFF0000u;
-    const float r2 = r1 - __uint_as_float(m);
-    hi = h >> 16;
-    mid = m >> 16;
-    lo = __float_as_uint(r2) >> 16;
+// Position of an attention work item: chunk c (128 tokens) of row (s, lkv),
+// lkv = layer * Hkv + KV head.  Items are ordered session, row, chunk.
+struct Cursor {
+    int s, lkv, c, nch;
+};
+
+// Wave-uniform value kept in a scalar register.
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// find_session with every LDS read made wave-uniform.
+__device__ __forceinline__ int find_session_uni(const int* pref, int S, int x) {
+    int lo = 0, hi = S;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (uni(pref[mid]) <= x) lo = mid; else hi = mid;
+    }
+    return lo;
 }
 
-// One wave: logits of one 128-token chunk of one (session, layer, KV head)
-// for the G query heads of the group, as eight 16x16x32 bf16 MFMA row tiles:
-// A = 16 tokens x 32 dims of K (bf16, straight from the pool), B = 32 dims x
-// 16 columns holding the G heads' query terms (hi, mid, lo accumulate into
-// the same C), C = 16 tokens x 16 heads in float32.
-// Lane layout (16x16x32): A/B lane l holds row/column l & 15 and the eight
-// consecutive k = 8 (l >> 4) .. +7; C lane l holds column l & 15, rows
-// 4 (l >> 4) .. +3.
-__global__ void __launch_bounds__(256) k_logits(Dims dm, View v, Scratch sc,
-                                                const float* __restrict__ q) {
-    __shared__ int s_pref[kMaxSessions + 1];
-    const int S = dm.S;
-    for (int i = threadIdx.x; i <= S; i += blockDim.x) s_pref[i] = sc.item_prefix[i];
-    __syncthreads();
-    const int total = s_pref[S];
-    const int lane = lane_id();
-    const int n_waves = gridDim.x * (blockDim.x >> 6);
-    const int gw = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-    const int per = (total + n_waves - 1) / n_waves;
-    int it = gw * per;
-    const int end = min(total, it + per);
-    if (it >= end) return;
-
-    int s = find_session(s_pref, S, it);
-    int nch = (s_pref[s + 1] - s_pref[s]) / dm.LHkv;
-    int local = it - s_pref[s];
-    int lkv = local / nch;
-    int c = local - lkv * nch;
-
-    const int h = lane & 15;         // MFMA column = query head within the group
-    const int g = lane >> 4;         // k-group of A/B, row quad of C
-    u32x4 bq[4][3];
-    int cur_row = -1;
-
-    for (; it < end; ++it) {
-        const int l = lkv / dm.Hkv;
-        const int kv = lkv - l * dm.Hkv;
-        const int row_id = s * dm.LHkv + lkv;
-        if (row_id != cur_row) {
-            cur_row = row_id;
-            bool bad = false;
-            const float* qh = q + (((size_t)s * dm.L + l) * dm.Hq + kv * dm.G + h) * kHeadDim;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                float xs[8];
-                if (h < dm.G) {
-                    const f32x4* p = reinterpret_cast<const f32x4*>(qh + 32 * j + 8 * g);
-                    const f32x4 u0 = p[0], u1 = p[1];
-                    xs[0] = u0.x; xs[1] = u0.y; xs[2] = u0.z; xs[3] = u0.w;
-                    xs[4] = u1.x; xs[5] = u1.y; xs[6] = u1.z; xs[7] = u1.w;
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) xs[e] = 0.0f;
-                }
-                uint32_t hi[8], mi[8], lo[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    bad |= !isfinite(xs[e]);
-                    split3(xs[e], hi[e], mi[e], lo[e]);
-                }
-#pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    bq[j][0][w] = hi[2 * w] | (hi[2 * w + 1] << 16);
-                    bq[j][1][w] = mi[2 * w] | (mi[2 * w + 1] << 16);
-                    bq[j][2][w] = lo[2 * w] | (lo[2 * w + 1] << 16);
-                }
-            }
-            if (bad) atomicOr(sc.status, MD_DEV_NONFINITE);
-        }
-
-        const int nt = v.n_tokens[s];
-        const int* ptab = v.page_table + (size_t)s * dm.MP;
-        const int tok0 = c * kChunk;
-        int phys_t[8], sub_t[8];
-        bool tv[8];
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-            const int tok = tok0 + 16 * t;
-            tv[t] = tok < nt;
-            phys_t[t] = 0;
-            sub_t[t] = 0;
-            if (tv[t]) {
-                const int pg = tok >> dm.Pshift;
-                const int p = ptab[pg];
-                if ((unsigned)p < (unsigned)dm.NP) {
-                    phys_t[t] = p;
-                    sub_t[t] = tok - (pg << dm.Pshift);
-                } else {
-                    tv[t] = false;
-                    if (lane == 0) atomicOr(sc.status, kDevCorrupt);
-                }
-            }
-        }
-        u32x4 a[8][4];
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-            if (tv[t]) {
-                const u32x4* rowp = reinterpret_cast<const u32x4*>(
-                    v.k_pool + (((size_t)phys_t[t] * dm.LHkv + lkv) * dm.P + sub_t[t] + h) * kHeadDim);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) a[t][j] = rowp[4 * j + g];
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) a[t][j] = u32x4{0u, 0u, 0u, 0u};
-            }
-        }
-        f32x4 acc[8];
-#pragma unroll
-        for (int t = 0; t < 8; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-#pragma unroll
-            for (int p = 0; p < 3; ++p) {
-#pragma unroll
-                for (int t = 0; t < 8; ++t) {
-                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf16x8, a[t][j]), __builtin_bit_cast(bf16x8, bq[j][p]),
-                        acc[t], 0, 0, 0);
-                }
-            }
-        }
-
-        // Base-2 logits; tokens past the session's count are masked out.
-        float m = -INFINITY;
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int tok = tok0 + 16 * t + 4 * g + i;
-                const float x = (tv[t] && tok < nt) ? acc[t][i] * kLogitScale : -INFINITY;
-                acc[t][i] = x;
-                m = fmaxf(m, x);
-            }
-        }
-        m = fmaxf(m, __shfl_xor(m, 16));
-        m = fmaxf(m, __shfl_xor(m, 32));
-        float lsum = 0.0f;
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) lsum += exp2f(acc[t][i] - m);
-        }
-        lsum += __shfl_xor(lsum, 16);
-        lsum += __shfl_xor(lsum, 32);
-
-        if (h < dm.G) {
-            const int row = l * dm.Hq + kv * dm.G + h;
-#pragma unroll
-            for (int t = 0; t < 8; ++t) {
-                if (tv[t]) {
-                    f32x4* dst = reinterpret_cast<f32x4*>(
-                        sc.logits + ((size_t)phys_t[t] * dm.R + row) * dm.P + sub_t[t] + 4 * g);
-                    *dst = acc[t];
-                }
-            }
-            if (g == 0)
-                sc.cstats[((size_t)s * dm.R + row) * dm.max_chunks + c] = make_float2(m, lsum);
-        }
-
-        // next item
-        if (++c == nch) {
-            c = 0;
-            if (++lkv == dm.LHkv) {
-                lkv = 0;
-                do { ++s; } while (s < S && s_pref[s + 1] == s_pref[s]);
-                if (s < S) nch = (s_pref[s + 1] - s_pref[s]) / dm.LHkv;
-            }
+__device__ __forceinline__ void cursor_next(Cursor& cu, const int* s_pref, int S, int LHkv) {
+    if (++cu.c == cu.nch) {
+        cu.c = 0;
+        if (++cu.lkv == LHkv) {
+            cu.lkv = 0;
+            do { ++cu.s; } while (cu.s < S && uni(s_pref[cu.s + 1]) == uni(s_pref[cu.s]));
+            if (cu.s < S) cu.nch = uni((uni(s_pref[cu.s + 1]) - uni(s_pref[cu.s])) / LHkv);
         }
     }
 }
 
-hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q,
-                         int n_blocks, hipStream_t st) {
-    hipLaunchKernelGGL(k_logits, dim3(n_blocks), dim3(256), 0, st, dm, v, sc, q);
+// What the logits kernel reads besides its pointers.
+struct LogitsDims {
+    int L, Hq, Hkv, G, P, Pshift, S, MP, NP, R, LHkv, max_chunks;
+};
+
+// B operands of one row (session s, lkv = layer * Hkv + KV head) in
+// registers: lane column h = lane & 15 is query head kv * G + h (zero past
+// G); k-group g = lane >> 4 holds dims 32j + 8g .. +7; each float32 term is
+// split into hi, mid and lo bf16 terms.
+__device__ __forceinline__ void split_query_regs(u32x4 (&bq)[4][3], const float* __restrict__ q,
+                                                 const LogitsDims& dm, int s, int lkv, int h, int g,
+                                                 int32_t* status) {
+    const int l = lkv / dm.Hkv, kv = lkv - l * dm.Hkv;
+    const float* qh = q + (((size_t)s * dm.L + l) * dm.Hq + kv * dm.G + h) * kHeadDim;
+    bool bad = false;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        f32x4 u0 = f32x4{0.f, 0.f, 0.f, 0.f}, u1 = u0;
+        if (h < dm.G) {
+            const f32x4* p = reinterpret_cast<const f32x4*>(qh + 32 * j + 8 * g);
+            u0 = p[0];
+            u1 = p[1];
+        }
+        const float xs[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+            uint32_t h0, m0, l0, h1, m1, l1;
+            bad |= !isfinite(xs[e]) || !isfinite(xs[e + 1]);
+            split3(xs[e], h0, m0, l0);
+            split3(xs[e + 1], h1, m1, l1);
+            bq[j][0][e >> 1] = h0 | (h1 << 16);
+            bq[j][1][e >> 1] = m0 | (m1 << 16);
+            bq[j][2][e >> 1] = l0 | (l1 << 16);
+        }
+    }
+    if (bad) atomicOr(status, MD_DEV_NONFINITE);
+}
+
+// The eight 16-token row tiles of an item: slot index (physical page * P +
+// offset in the page) of each tile's first token, and a mask of the tiles
+// that hold cached tokens.  Page-table reads are clamped into the session's
+// table, so the lookup never branches; out-of-range entries drop the tile
+// and report MD_DEV_CORRUPT once per item.
+struct ItemTiles {
+    int slot0[8];
+    unsigned vmask;
+    int nt;
+};
+
+__device__ __forceinline__ void item_tiles(ItemTiles& it, const Cursor& cu, const LogitsDims& dm,
+                                           const int32_t* __restrict__ page_table,
+                                           const int32_t* __restrict__ n_tokens, int32_t* status,
+                                           int lane) {
+    const int nt = n_tokens[cu.s];
+    const int np = (nt + dm.P - 1) >> dm.Pshift;
+    const int* ptab = page_table + (size_t)cu.s * dm.MP;
+    unsigned vm = 0, bad = 0;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        const int tok = cu.c * kChunk + 16 * t;
+        const int pg = min(tok >> dm.Pshift, max(np - 1, 0));
+        const int p = ptab[pg];
+        const bool in_seq = tok < nt;
+        const bool in_pool = (unsigned)p < (unsigned)dm.NP;
+        vm |= (in_seq && in_pool) ? 1u << t : 0u;
+        bad |= (in_seq && !in_pool) ? 1u : 0u;
+        it.slot0[t] = (in_seq && in_pool) ? (p << dm.Pshift) + (tok & (dm.P - 1)) : 0;
+    }
+    it.vmask = vm;
+    it.nt = nt;
+    if (bad && lane == 0) atomicOr(status, kDevCorrupt);
+}
+
+typedef const __attribute__((address_space(1))) uint8_t* gbytes;
+typedef const __attribute__((address_space(1))) u32x4* gvec;
+
+// A wave-uniform global pointer held in scalar registers.
+__device__ __forceinline__ gbytes uni_ptr(const void* p) {
+    const uint64_t u = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+    return (gbytes)(((uint64_t)hi << 32) | lo);
+}
+
+// Four 16-byte pieces of one K row tile in the MFMA A layout: lane (h, g)
+// holds token h's dims 32j + 8g .. +7 for j = 0..3 (voff = 256 h + 16 g).
+// A tile without cached tokens reads the pool's first row tile instead
+// (always in bounds; its logits are masked), so loads never branch.
+__device__ __forceinline__ void load_tile(u32x4 (&a)[4], const LogitsDims& dm,
+                                          const uint16_t* __restrict__ k_pool, const ItemTiles& it,
+                                          int t, int lkv, uint32_t voff) {
+    const bool ok = it.vmask & (1u << t);
+    const int slot = it.slot0[t];
+    const size_t tile = ok ? ((size_t)(slot >> dm.Pshift) * dm.LHkv + lkv) * dm.P + (slot & (dm.P - 1)) : 0;
+    gbytes base = uni_ptr(k_pool + tile * kHeadDim);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        a[j] = __builtin_nontemporal_load(reinterpret_cast<gvec>(base + voff + 64 * j));
+}
+
+// Each wave streams a contiguous run of work items (128-token chunks of one
+// (session, layer, KV head) row) tile by tile through a ring of four 16-token
+// K tiles held in registers: while tile t is multiplied, tiles t+1..t+3 are in
+// flight, and the slot tile t frees is refilled with tile t+4, which may
+// belong to the next item (whose page-table entries are fetched one item
+// ahead).  Per tile: one 16x16x32 bf16 MFMA row tile, A = 16 tokens x 32 dims
+// of K, B = 32 dims x 16 columns holding the G heads' query terms (hi, mid
+// and lo accumulate into the same C), C = 16 tokens x 16 heads in float32.
+// Lane layout (16x16x32): A/B lane l holds row/column l & 15 and the eight
+// consecutive k = 8 (l >> 4) .. +7; C lane l holds column l & 15, rows
+// 4 (l >> 4) .. +3.  Softmax statistics of the chunk are kept online per
+// lane and merged across the four row quads at the end of the chunk.
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3)))
+k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __restrict__ page_table,
+         const int32_t* __restrict__ n_tokens, const float* __restrict__ q,
+         float* __restrict__ logits, float2* __restrict__ cstats, int32_t* status,
+         const int32_t* __restrict__ item_prefix) {
+    __shared__ int s_pref[kMaxSessions + 1];
+    const int S = dm.S;
+    for (int i = threadIdx.x; i <= S; i += blockDim.x) s_pref[i] = item_prefix[i];
+    __syncthreads();
+    const int total = uni(s_pref[S]);
+    const int lane = lane_id();
+    const int n_waves = gridDim.x * (blockDim.x >> 6);
+    const int gw = uni(blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6));
+    const int per = uni((total + n_waves - 1) / n_waves);
+    int it = gw * per;
+    const int end = min(total, it + per);
+    if (it >= end) return;
+
+    const int h = lane & 15;         // MFMA column = query head within the group
+    const int g = lane >> 4;         // k-group of A/B, row quad of C
+    const uint32_t voff = 256u * h + 16u * g;
+    Cursor cu;
+    cu.s = find_session_uni(s_pref, S, it);
+    const int base_it = uni(s_pref[cu.s]);
+    cu.nch = uni((uni(s_pref[cu.s + 1]) - base_it) / dm.LHkv);
+    cu.lkv = uni((it - base_it) / cu.nch);
+    cu.c = uni((it - base_it) - cu.lkv * cu.nch);
+    u32x4 ring[4][4];
+    u32x4 bq[4][3];
+
+    // Outer loop: one row segment (items of one (session, layer, KV head) row)
+    // at a time; the query operands load once per segment.
+    while (it < end) {
+        const int seg_end = min(end, it + (cu.nch - cu.c));
+        const int row_id = cu.s * dm.LHkv + cu.lkv;
+        split_query_regs(bq, q, dm, cu.s, cu.lkv, h, g, status);
+        const int l = uni(cu.lkv / dm.Hkv);
+        const int kv = cu.lkv - l * dm.Hkv;
+        const int row0 = uni(l * dm.Hq + kv * dm.G);  // first logits row of the group
+        ItemTiles cur;
+        item_tiles(cur, cu, dm, page_table, n_tokens, status, lane);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) load_tile(ring[t], dm, k_pool, cur, t, cu.lkv, voff);
+
+        // Inner loop: the segment's items, streamed without a break.
+        for (; it < seg_end; ++it) {
+            ItemTiles nxt;
+            if (it + 1 < seg_end) {
+                Cursor nx = cu;
+                ++nx.c;
+                item_tiles(nxt, nx, dm, page_table, n_tokens, status, lane);
+            } else {
+                nxt = cur;
+                nxt.vmask = 0;
+            }
+            const int tok0 = cu.c * kChunk;
+            float m = -INFINITY, lsum = 0.0f;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+#pragma unroll
+                    for (int p = 0; p < 3; ++p)
+                        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            __builtin_bit_cast(bf16x8, ring[t & 3][j]), __builtin_bit_cast(bf16x8, bq[j][p]),
+                            acc, 0, 0, 0);
+                }
+                // refill the slot with the tile four ahead
+                if (t < 4) load_tile(ring[t & 3], dm, k_pool, cur, t + 4, cu.lkv, voff);
+                else load_tile(ring[t & 3], dm, k_pool, nxt, t - 4, cu.lkv, voff);
+
+                // base-2 logits; tokens past the session's count are masked out
+                const bool tvalid = cur.vmask & (1u << t);
+                float x[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int tok = tok0 + 16 * t + 4 * g + i;
+                    x[i] = (tvalid && tok < cur.nt) ? acc[i] * kLogitScale : -INFINITY;
+                }
+                const float mn = fmaxf(m, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+                const bool live = mn != -INFINITY;
+                const float ms = live ? mn : 0.0f;
+                const float part = (hw_exp2(x[0] - ms) + hw_exp2(x[1] - ms)) +
+                                   (hw_exp2(x[2] - ms) + hw_exp2(x[3] - ms));
+                lsum = live ? lsum * hw_exp2(m - ms) + part : lsum;
+                m = live ? mn : m;
+                if (tvalid && h < dm.G) {
+                    const int slot = cur.slot0[t];
+                    gbytes base = uni_ptr(logits + ((size_t)(slot >> dm.Pshift) * dm.R + row0) * dm.P +
+                                          (slot & (dm.P - 1)));
+                    const uint32_t so = 4u * (h * dm.P + 4 * g);
+                    *(__attribute__((address_space(1))) f32x4*)(base + so) = f32x4{x[0], x[1], x[2], x[3]};
+                }
+            }
+            // merge the four row quads' (max, sum) pairs; the merge is
+            // symmetric, so every lane of a column ends with the same values
+#pragma unroll
+            for (int o = 16; o <= 32; o <<= 1) {
+                const float m2 = __shfl_xor(m, o);
+                const float l2 = __shfl_xor(lsum, o);
+                const float M = fmaxf(m, m2);
+                lsum = (M == -INFINITY) ? 0.0f : lsum * hw_exp2(m - M) + l2 * hw_exp2(m2 - M);
+                m = M;
+            }
+            if (h < dm.G && g == 0)
+                cstats[((size_t)cu.s * dm.R + row0 + h) * dm.max_chunks + cu.c] = make_float2(m, lsum);
+            ++cu.c;
+            cur = nxt;
+        }
+        // next row
+        cu.c = cu.nch - 1;
+        cursor_next(cu, s_pref, S, dm.LHkv);
+    }
+}
+
+hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q, int n_blocks,
+                         hipStream_t st) {
+    LogitsDims ld{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.S, dm.MP, dm.NP, dm.R, dm.LHkv, dm.max_chunks};
+    hipLaunchKernelGGL(k_logits, dim3(n_blocks), dim3(256), 0, st, ld, v.k_pool, v.page_table,
+                       v.n_tokens, q, sc.logits, sc.cstats, sc.status, sc.item_prefix);
     return hipGetLastError();
 }
 
@@ -429,7 +526,7 @@ __global__ void __launch_bounds__(256) k_rowstats(Dims dm, Scratch sc) {
     float l = 0.0f;
     for (int c = lane; c < nch; c += 64) {
         const float2 st = cs[c];
-        l += st.y * exp2f(st.x - m);
+        l += st.y * hw_exp2(st.x - m);
     }
     l = wave_sum(l);
     if (lane == 0) sc.rstats[(size_t)s * dm.R + row] = make_float2(m, 1.0f / l);
@@ -482,7 +579,7 @@ __global__ void __launch_bounds__(256) k_mass(Dims dm, View v, Scratch sc, float
 #pragma unroll 8
                 for (int row = rg; row < dm.R; row += 4) {
                     const float2 rs = s_rs[row];
-                    acc += exp2f(lp[(size_t)row * dm.P] - rs.x) * rs.y;
+                    acc += hw_exp2(lp[(size_t)row * dm.P] - rs.x) * rs.y;
                 }
             }
         }
