@@ -13,9 +13,10 @@ timed steps are the steady state that follows.
 
 Printed on stdout: one JSON line.  value = tokens scored per second (the
 sum over sessions and timed steps of the cached tokens scored, divided by
-the wall time of the timed steps); roofline = the attention-logits kernel's
-algorithmic bytes per launch over its event-timed average duration, against
-MI355X's 8 TB/s; cpu_baseline = the CPU oracle on one session of the same
+the wall time of the timed steps); roofline = the dominant kernel's (the
+fused attention-mass kernel, or the attention-logits kernel of the
+multi-kernel path) algorithmic bytes per launch over its event-timed average
+duration, against MI355X's 8 TB/s; cpu_baseline = the CPU oracle on one session of the same
 workload.
 """
 from __future__ import annotations
@@ -34,15 +35,16 @@ sys.path.insert(0, ROOT)
 
 METRIC = "cached tokens scored+evicted per second per decode step; achieved HBM GB/s vs peak"
 PEAK_HBM_GBS = 8000.0
-KERNEL_SRC = os.path.join(ROOT, "paper_2607_10582_amd", "csrc", "md_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_2607_10582_amd", "csrc")
+KERNEL_SRC = {"logits": os.path.join(CSRC, "md_kernels.hip"), "attend": os.path.join(CSRC, "md_attend.hip")}
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
+def kernel_source_hash(kernel: str) -> str:
+    with open(KERNEL_SRC[kernel], "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
@@ -134,15 +136,15 @@ def cpu_baseline(w, n0s, B, budget_s: float, max_steps: int):
             "seconds_per_step": elapsed / max(steps, 1)}
 
 
-def load_traffic(workload: str, avg_launch_bytes: float):
-    """Counter-measured HBM bytes per launch of the logits kernel, if a
-    profile of the current kernel source exists."""
-    path = os.path.join(ROOT, "profiles", f"k_logits_{workload}_pmc.json")
+def load_traffic(kernel: str, workload: str):
+    """Counter-measured HBM bytes per launch of ``kernel``, if a profile of
+    the current kernel source exists."""
+    path = os.path.join(ROOT, "profiles", f"k_{kernel}_{workload}_pmc.json")
     if not os.path.exists(path):
         return None, None
     with open(path) as f:
         d = json.load(f)
-    if d.get("kernel_source_sha256_16") != kernel_source_hash():
+    if d.get("kernel_source_sha256_16") != kernel_source_hash(kernel):
         return None, "stale"
     return d.get("hbm_bytes_per_launch"), path
 
@@ -200,7 +202,10 @@ def main():
         md.step(k, q, nk, reg)
     torch.cuda.synchronize(dev)
     c0 = md.counters()
-    md.profile(("logits",))
+    kcfg = md.kernel_config()
+    hot = "attend" if kcfg["fused"] and not kcfg["spill"] else "logits"
+    log(f"kernel config {kcfg}; timing k_{hot}")
+    md.profile((hot,))
     stream = md.stream
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -214,7 +219,7 @@ def main():
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0
     gpu_ms = ev0.elapsed_time(ev1)
-    logits_ms, launches = md.profile_read("logits")
+    hot_ms, launches = md.profile_read(hot)
     md.profile(())
     c1 = md.counters()
     status = md.device_status()
@@ -227,11 +232,14 @@ def main():
     evicted_pages = c1[2] - c0[2]
     kb = w.k_bytes_per_token
     q_bytes = w.S * w.L * w.Hq * w.d * 4
-    logits_bytes = scored * kb + K * q_bytes              # algorithmic, over the timed launches
-    avg_launch_s = logits_ms / 1e3 / max(launches, 1)
-    per_launch_bytes = logits_bytes / max(launches, 1)
+    # algorithmic bytes over the timed launches: every cached key once and the
+    # queries once; the fused kernel also reads and writes each token's
+    # importance (Eq. 2)
+    hot_bytes = scored * kb + K * q_bytes + (scored * 8 if hot == "attend" else 0)
+    avg_launch_s = hot_ms / 1e3 / max(launches, 1)
+    per_launch_bytes = hot_bytes / max(launches, 1)
     achieved = per_launch_bytes / avg_launch_s / 1e9
-    traffic, traffic_src = load_traffic(w.name, per_launch_bytes)
+    traffic, traffic_src = load_traffic(hot, w.name)
     # whole step: K + per-token state (region 1, a 4+4, t_ref 4+4) + per-page
     # score and page-table entry + the queries
     step_bytes = scored * (kb + 17) + scored // w.P * 8 + K * q_bytes
@@ -255,7 +263,7 @@ def main():
                    "page_size": w.P, "budget_frac": w.budget_frac, "parallelism": "none"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
-                     "kernel": "k_logits", "launches": launches,
+                     "kernel": f"k_{hot}", "launches": launches,
                      "avg_launch_us": avg_launch_s * 1e6,
                      "algorithmic_bytes_per_launch": per_launch_bytes},
         "tokens_scored_per_step": scored / K,

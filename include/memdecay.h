@@ -77,6 +77,14 @@ enum {
 #define MD_DEV_CORRUPT    0x8   /* a session's counters, page table or region   */
                                 /* codes are out of range; the session is      */
                                 /* skipped for the step                         */
+#define MD_DEV_TIMEOUT    0x10  /* a bounded wait between the workgroups of the */
+                                /* fused observation kernel ran out; the step's */
+                                /* attention mass is not valid                  */
+
+/* Bits of md_config.flags. */
+#define MD_FLAG_NO_FUSED  0x1   /* observe every session with the multi-kernel  */
+                                /* path (logits through HBM) instead of the     */
+                                /* fused one; results agree to rounding         */
 
 typedef struct md_config {
     int32_t n_layers;           /* L                                              */
@@ -92,7 +100,7 @@ typedef struct md_config {
     float rho;                  /* EWMA smoothing, 0 <= rho < 1 (Eq. 2)           */
     float alpha;                /* attention weight, alpha >= 0 (Eq. 4)           */
     float tau_scale;            /* tau = tau_scale / |K_t| (Eq. 3's scaled form)  */
-    int32_t reserved;           /* must be 0                                      */
+    int32_t flags;              /* MD_FLAG_* bits; other bits must be 0           */
 } md_config;
 
 /* Region priors (Sec. III-B): b_r >= 0 and lambda_r >= 0 per session and
@@ -207,7 +215,7 @@ md_status md_read_device_status(md_handle h, int32_t* host_out);
 /* Kernel ids for md_profile_enable / md_profile_read. */
 enum {
     MD_K_APPEND = 0, MD_K_LOGITS = 1, MD_K_ROWSTATS = 2, MD_K_MASS = 3,
-    MD_K_SCORE = 4, MD_K_SELECT = 5, MD_K_COMPACT = 6, MD_K_COUNT = 7
+    MD_K_SCORE = 4, MD_K_SELECT = 5, MD_K_COMPACT = 6, MD_K_ATTEND = 7, MD_K_COUNT = 8
 };
 
 /* Diagnostics.  md_profile_enable: from now on, bracket every launch of the
@@ -222,6 +230,13 @@ md_status md_profile_read(md_handle h, int32_t kernel, double* total_ms, int64_t
  * out[0] tokens scored (sum over steps and sessions of |K_t|), out[1] steps
  * observed, out[2] pages evicted, out[3] tokens evicted. */
 md_status md_read_counters(md_handle h, int64_t* out);
+
+/* How md_init laid out the observation step on this device: out[0] 1 when
+ * the fused observation kernel is used, out[1] 1 when the multi-kernel path
+ * may run (flag MD_FLAG_NO_FUSED, or a session could outgrow one pass of the
+ * fused kernel), out[2] the largest fused unit in tokens, out[3] the fused
+ * kernel's workgroups (all resident at once).  Host-only, no device work. */
+md_status md_kernel_config(md_handle h, int32_t* out);
 
 /* Release the scratch and the handle (synchronises the stream first). */
 md_status md_destroy(md_handle h);

@@ -23,14 +23,19 @@ MD_DEV_CAPACITY = 0x1
 MD_DEV_NONFINITE = 0x2
 MD_DEV_BAD_EVICT = 0x4
 MD_DEV_CORRUPT = 0x8
+MD_DEV_TIMEOUT = 0x10
+
+MD_FLAG_NO_FUSED = 0x1
 
 EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_observe_step",
            "md_score_pages", "md_select_evict", "md_compact", "md_read_device_status",
-           "md_profile_enable", "md_profile_read", "md_read_counters", "md_destroy")
+           "md_profile_enable", "md_profile_read", "md_read_counters", "md_kernel_config",
+           "md_destroy")
 
 # kernel ids of md_profile_enable / md_profile_read
-KERNELS = ("append", "logits", "rowstats", "mass", "score", "select", "compact")
-MD_K_APPEND, MD_K_LOGITS, MD_K_ROWSTATS, MD_K_MASS, MD_K_SCORE, MD_K_SELECT, MD_K_COMPACT = range(7)
+KERNELS = ("append", "logits", "rowstats", "mass", "score", "select", "compact", "attend")
+(MD_K_APPEND, MD_K_LOGITS, MD_K_ROWSTATS, MD_K_MASS, MD_K_SCORE, MD_K_SELECT, MD_K_COMPACT,
+ MD_K_ATTEND) = range(8)
 
 
 class md_config(ctypes.Structure):
@@ -40,7 +45,7 @@ class md_config(ctypes.Structure):
                 ("max_pages", ctypes.c_int32), ("n_phys_pages", ctypes.c_int32),
                 ("n_regions", ctypes.c_int32), ("pinned_region_mask", ctypes.c_uint32),
                 ("rho", ctypes.c_float), ("alpha", ctypes.c_float),
-                ("tau_scale", ctypes.c_float), ("reserved", ctypes.c_int32)]
+                ("tau_scale", ctypes.c_float), ("flags", ctypes.c_int32)]
 
 
 class md_region_params(ctypes.Structure):
@@ -96,6 +101,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                     ctypes.POINTER(ctypes.c_int64)]
     lib.md_read_counters.restype = i32
     lib.md_read_counters.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
+    lib.md_kernel_config.restype = i32
+    lib.md_kernel_config.argtypes = [vp, ctypes.POINTER(i32)]
     lib.md_destroy.restype = i32
     lib.md_destroy.argtypes = [vp]
     _lib = lib
@@ -174,6 +181,14 @@ def md_read_counters(h: int):
     out = (ctypes.c_int64 * 4)()
     _check("md_read_counters", load_library().md_read_counters(h, out))
     return tuple(int(x) for x in out)
+
+
+def md_kernel_config(h: int) -> dict:
+    """How md_init laid out the observation step (fused kernel, spill path,
+    largest fused unit in tokens, fused workgroups)."""
+    out = (ctypes.c_int32 * 4)()
+    _check("md_kernel_config", load_library().md_kernel_config(h, out))
+    return {"fused": bool(out[0]), "spill": bool(out[1]), "unit_max": int(out[2]), "workgroups": int(out[3])}
 
 
 def md_destroy(h: int) -> int:

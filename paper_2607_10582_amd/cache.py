@@ -104,7 +104,8 @@ class MemDecay:
 
     def __init__(self, cache: PagedCache, base_priority: torch.Tensor, decay_rate: torch.Tensor, *,
                  rho: float, alpha: float, tau_scale: float, pinned_mask: int,
-                 n_regions: int = 7, stream: Optional[torch.cuda.Stream] = None):
+                 n_regions: int = 7, stream: Optional[torch.cuda.Stream] = None,
+                 fused: bool = True):
         self.cache = cache
         dev = cache.device
         self.b = base_priority.to(dev, torch.float32).contiguous()
@@ -113,7 +114,8 @@ class MemDecay:
                           head_dim=cache.d, page_size=cache.P, max_sessions=cache.S,
                           max_pages=cache.max_pages, n_phys_pages=cache.n_phys,
                           n_regions=n_regions, pinned_region_mask=pinned_mask, rho=rho,
-                          alpha=alpha, tau_scale=tau_scale, reserved=0)
+                          alpha=alpha, tau_scale=tau_scale,
+                          flags=0 if fused else B.MD_FLAG_NO_FUSED)
         rp = B.md_region_params(base_priority=self.b.data_ptr(), decay_rate=self.lam.data_ptr())
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
         self._cfg, self._rp, self._cv = cfg, rp, cache.view()
@@ -167,6 +169,9 @@ class MemDecay:
 
     def counters(self):
         return B.md_read_counters(self.handle)
+
+    def kernel_config(self) -> dict:
+        return B.md_kernel_config(self.handle)
 
     def close(self):
         if self.handle is not None:

@@ -101,7 +101,7 @@ const char* md_status_str(md_status s) {
 
 static md_status validate_config(const md_config* c) {
     if (c == nullptr) return MD_E_INVALID;
-    if (c->reserved != 0) return MD_E_INVALID;
+    if ((c->flags & ~MD_FLAG_NO_FUSED) != 0) return MD_E_INVALID;
     if (c->n_layers < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1) return MD_E_INVALID;
     if (c->n_q_heads % c->n_kv_heads != 0) return MD_E_INVALID;
     if (c->max_sessions < 1 || c->max_pages < 1 || c->n_phys_pages < 1) return MD_E_INVALID;
@@ -167,6 +167,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     dm.rho = cfg->rho;
     dm.alpha = cfg->alpha;
     dm.tau_scale = cfg->tau_scale;
+    dm.fused = (cfg->flags & MD_FLAG_NO_FUSED) ? 0 : 1;
 
     // ---- from here on the HIP runtime is used
     int dev = 0;
@@ -185,6 +186,71 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
         return MD_E_HIP;
     for (size_t i = 0; i < nrp; ++i)
         if (!(hb[i] >= 0.0f) || !isfinite(hb[i]) || !(hl[i] >= 0.0f) || !isfinite(hl[i])) return MD_E_INVALID;
+
+    // Fused observation kernel: LDS for three workgroups per CU sets the
+    // largest unit; the occupancy at that LDS size sets the grid, which md_init
+    // then checks on the device (all workgroups resident at once).
+    const int n_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
+    int occ = 0;
+    if (dm.fused) {
+        const size_t per_cu = prop.maxSharedMemoryPerMultiProcessor > 0 ? prop.maxSharedMemoryPerMultiProcessor
+                                                                        : (size_t)160 * 1024;
+        auto unit_max = [&](size_t budget) -> int64_t {
+            const size_t fixed = md::attend_lds_bytes(dm.G, 0);
+            if (budget <= fixed) return 0;
+            const int64_t stride = (int64_t)((budget - fixed) / ((size_t)md::kRowBufs * dm.G * sizeof(float)));
+            const int64_t t = (stride - 4) / md::kUnitQuantum * md::kUnitQuantum;
+            return t > md::kUnitMax ? md::kUnitMax : t;
+        };
+        for (size_t budget : {per_cu / 3, (size_t)64 * 1024}) {
+            const int64_t tmax = unit_max(budget);
+            if (tmax < md::kUnitMin) continue;
+            const size_t lds = md::attend_lds_bytes(dm.G, (int)tmax + 4);
+            if (hipFuncSetAttribute(md::attend_kernel(), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+                hipSuccess) {
+                (void)hipGetLastError();
+                continue;
+            }
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(), md::kAttendThreads, lds) !=
+                hipSuccess)
+                return MD_E_HIP;
+            if (occ >= 1) {
+                dm.Tmax = (int)tmax;
+                dm.Tstride = dm.Tmax + 4;
+                break;
+            }
+        }
+        dm.n_wg = occ * n_cu;
+        dm.fused = occ >= 1 && dm.Tmax >= md::kUnitMin;
+    }
+    if (dm.fused) {
+        dm.U_cap = (int)(((int64_t)dm.NP * dm.P + md::kUnitMin - 1) / md::kUnitMin + dm.S);
+    } else {
+        dm.Tmax = dm.Tstride = dm.n_wg = dm.U_cap = 0;
+    }
+    // The fused kernel's workgroups wait for each other, so all of them must
+    // be resident together: check it on the device, and step the grid down
+    // one workgroup per CU at a time until every workgroup arrives.
+    if (dm.fused) {
+        int32_t* probe = nullptr;
+        if (hipMalloc(&probe, 2 * sizeof(int32_t)) != hipSuccess) return MD_E_NOMEM;
+        int verified = 0;
+        for (int o = occ; o >= 1 && verified == 0; --o) {
+            int32_t seen[2] = {0, 0};
+            if (md::launch_attend_check(dm, probe, o * n_cu, hs) != hipSuccess ||
+                hipMemcpyAsync(seen, probe, sizeof(seen), hipMemcpyDeviceToHost, hs) != hipSuccess ||
+                hipStreamSynchronize(hs) != hipSuccess) {
+                (void)hipGetLastError();
+                continue;
+            }
+            if (seen[1] >= o * n_cu) verified = o * n_cu;
+        }
+        (void)hipFree(probe);
+        dm.n_wg = verified;
+        dm.fused = verified > 0;
+        if (!dm.fused) dm.Tmax = dm.Tstride = dm.U_cap = 0;
+    }
+    dm.spill = !dm.fused || (int64_t)dm.MP * dm.P > (int64_t)dm.n_wg * dm.Tmax;
 
     md_handle_s* h = new (std::nothrow) md_handle_s();
     if (h == nullptr) return MD_E_NOMEM;
@@ -214,18 +280,13 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
         return MD_E_NOMEM;
     }
     md::scratch_carve(dm, h->scratch, &h->sc);
-    // counters and status start at zero; work lists empty until the first append
-    if (hipMemsetAsync(h->sc.done, 0, 2 * sizeof(int32_t), hs) != hipSuccess ||
-        hipMemsetAsync(h->sc.counters, 0, 4 * sizeof(unsigned long long), hs) != hipSuccess ||
-        hipMemsetAsync(h->sc.item_prefix, 0, (size_t)(dm.S + 1) * sizeof(int32_t), hs) != hipSuccess ||
-        hipMemsetAsync(h->sc.tile_prefix, 0, (size_t)(dm.S + 1) * sizeof(int32_t), hs) != hipSuccess ||
-        hipMemsetAsync(h->sc.valid, 0, (size_t)(dm.S + 1) * sizeof(int32_t), hs) != hipSuccess ||
-        hipStreamSynchronize(hs) != hipSuccess) {
+    // counters, status, epoch and the tagged unit statistics start at zero
+    // (no step's tag is zero); work lists are empty until the first append
+    if (hipMemsetAsync(h->scratch, 0, bytes, hs) != hipSuccess || hipStreamSynchronize(hs) != hipSuccess) {
         (void)hipFree(h->scratch);
         delete h;
         return MD_E_HIP;
     }
-    const int n_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
     h->logits_blocks = 3 * n_cu;
     h->mass_blocks = 4 * n_cu;
     h->score_blocks = 2 * n_cu;
@@ -246,11 +307,16 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
     hipError_t e = timed_launch(h, MD_K_APPEND, [&] {
         return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, h->stream); });
-    if (e == hipSuccess) e = timed_launch(h, MD_K_LOGITS, [&] {
+    // Sessions that fit one pass of the fused kernel run there; the others
+    // (only possible when a session may outgrow n_wg * Tmax tokens) take the
+    // three-kernel path with the logits in HBM.
+    if (e == hipSuccess && h->dm.fused) e = timed_launch(h, MD_K_ATTEND, [&] {
+        return md::launch_attend(h->dm, h->v, h->sc, q, abar_out, h->stream); });
+    if (e == hipSuccess && h->dm.spill) e = timed_launch(h, MD_K_LOGITS, [&] {
         return md::launch_logits(h->dm, h->v, h->sc, q, h->logits_blocks, h->stream); });
-    if (e == hipSuccess) e = timed_launch(h, MD_K_ROWSTATS, [&] {
+    if (e == hipSuccess && h->dm.spill) e = timed_launch(h, MD_K_ROWSTATS, [&] {
         return md::launch_rowstats(h->dm, h->sc, h->stream); });
-    if (e == hipSuccess) e = timed_launch(h, MD_K_MASS, [&] {
+    if (e == hipSuccess && h->dm.spill) e = timed_launch(h, MD_K_MASS, [&] {
         return md::launch_mass(h->dm, h->v, h->sc, abar_out, h->mass_blocks, h->stream); });
     if (e != hipSuccess) return MD_E_HIP;
     h->have_step = true;
@@ -345,6 +411,15 @@ md_status md_read_counters(md_handle h, int64_t* out) {
         hipStreamSynchronize(h->stream) != hipSuccess)
         return MD_E_HIP;
     for (int i = 0; i < 4; ++i) out[i] = (int64_t)v[i];
+    return MD_OK;
+}
+
+md_status md_kernel_config(md_handle h, int32_t* out) {
+    if (h == nullptr || out == nullptr) return MD_E_INVALID;
+    out[0] = h->dm.fused;
+    out[1] = h->dm.spill;
+    out[2] = h->dm.Tmax;
+    out[3] = h->dm.n_wg;
     return MD_OK;
 }
 

@@ -1,0 +1,114 @@
+// Device helpers shared by the gfx950 kernels of the retention step.
+#pragma once
+
+#include <math.h>
+
+#include "md_internal.h"
+
+namespace md {
+
+typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// log2(e) / sqrt(128): logits are kept in base 2 so that 2^(x - m) is the
+// softmax numerator exp(q.k/sqrt(d) - m').
+constexpr float kLogitScale = (float)(1.4426950408889634074 / 11.313708498984760390);
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+// 2^x on the transcendental unit (v_exp_f32, about 1 ulp).  Results below
+// 2^-126 come out as zero or denormal; softmax weights that small are
+// negligible next to the row maximum's weight of 1.
+__device__ __forceinline__ float hw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+__device__ __forceinline__ int load_agent(const int32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Exclusive prefix of one int per thread across the whole block (any multiple
+// of 64 threads up to 1024).  lds needs 17 ints.  Contains __syncthreads.
+__device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
+    const int lane = lane_id(), wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    int incl = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(incl, o);
+        if (lane >= o) incl += t;
+    }
+    if (lane == 63) lds[wid] = incl;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int acc = 0;
+        for (int w = 0; w < nw; ++w) {
+            const int t = lds[w];
+            lds[w] = acc;
+            acc += t;
+        }
+        lds[16] = acc;
+    }
+    __syncthreads();
+    const int res = lds[wid] + incl - v;
+    *total = lds[16];
+    __syncthreads();
+    return res;
+}
+
+// Largest s in [0, S) with pref[s] <= x, given pref[0] <= x < pref[S].
+__device__ __forceinline__ int find_session(const int* pref, int S, int x) {
+    int lo = 0, hi = S;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (pref[mid] <= x) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ bool counters_ok(int np, int nt, const Dims& dm) {
+    if (np < 0 || np > dm.MP) return false;
+    if (np == 0) return nt == 0;
+    return nt > (np - 1) * dm.P && nt <= np * dm.P;
+}
+
+// Split a float32 into three bfloat16 terms with x == hi + mid + lo exactly:
+// hi and mid truncate (the differences are exact by Sterbenz's lemma), and
+// what is left has at most 8 significant bits, so lo holds it exactly.
+__device__ __forceinline__ void split3(float x, uint32_t& hi, uint32_t& mid, uint32_t& lo) {
+    const uint32_t u = __float_as_uint(x);
+    const uint32_t h = u & 0xFFFF0000u;
+    const float r1 = x - __uint_as_float(h);
+    const uint32_t m = __float_as_uint(r1) & 0xFFFF0000u;
+    const float r2 = r1 - __uint_as_float(m);
+    hi = h >> 16;
+    mid = m >> 16;
+    lo = __float_as_uint(r2) >> 16;
+}
+
+
+// Wave-uniform value kept in a scalar register.
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+typedef const __attribute__((address_space(1))) uint8_t* gbytes;
+typedef const __attribute__((address_space(1))) u32x4* gvec;
+
+// A wave-uniform global pointer held in scalar registers.
+__device__ __forceinline__ gbytes uni_ptr(const void* p) {
+    const uint64_t u = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+    return (gbytes)(((uint64_t)hi << 32) | lo);
+}
+
+}  // namespace md

@@ -17,11 +17,32 @@ constexpr int kMaxRows = 1024;      // L * Hq
 constexpr int kMaxPages = 8192;     // page-table capacity per session
 constexpr int kSelThreads = 1024;   // select / compact block size
 constexpr int kPerThread = kMaxPages / kSelThreads;
+// Fused observation kernel (k_attend): three producer waves and one manager
+// wave per workgroup (a multiple of the CU's four SIMDs: workgroups of other
+// wave counts do not all fit at the occupancy the runtime reports); a unit of
+// work is one session's block of T tokens (T a multiple of kUnitQuantum,
+// between kUnitMin and Dims::Tmax) over every (layer, KV head) row.
+constexpr int kProducers = 3;
+constexpr int kAttendThreads = 64 * (kProducers + 1);
+constexpr int kUnitQuantum = 16 * kProducers;   // one 16-token tile per producer
+constexpr int kUnitMin = 2 * kUnitQuantum;
+constexpr int kUnitMax = 16 * kUnitQuantum;     // 4 tokens per producer lane
+constexpr int kConsumeLag = 3;   // rows a producer runs ahead of the row it normalises
+constexpr int kRowBufs = kConsumeLag + 1;       // rows of logits held in LDS
+constexpr int kStatBufs = 4;     // producer -> manager statistic buffers
+constexpr int kNormBufs = 4;     // manager -> producer normaliser buffers
+constexpr int kMaxCand = (kUnitMax - kUnitMin) / kUnitQuantum + 1;
 
 constexpr int kDevCorrupt = MD_DEV_CORRUPT;
 
 struct Dims {
     int L, Hq, Hkv, G, P, Pshift, S, MP, NP, R, LHkv, n_regions, max_chunks;
+    int fused;     // 1: sessions that fit one pass run on k_attend
+    int spill;     // 1: some session may not fit a pass (the spill kernels run)
+    int Tmax;      // largest fused unit, tokens
+    int Tstride;   // LDS row stride of a fused logits row, floats (Tmax + 4)
+    int n_wg;      // k_attend workgroups (all co-resident)
+    int U_cap;     // capacity of the per-step fused unit list
     uint32_t pin_mask;
     float rho, alpha, tau_scale;
 };
@@ -47,11 +68,17 @@ struct View {
 
 struct Scratch {
     float* logits;       // [NP][R][P] base-2 logits of the step (log2(e) q.k / sqrt(d))
-    float2* cstats;      // [S][R][max_chunks] (max, sum of 2^(x - max)) per chunk
+    float2* cstats;      // [S][R][max_chunks] (max, sum of 2^(x - max)) per chunk or fused unit
     float2* rstats;      // [S][R] (row max M, 1 / row sum)
     float* pscore;       // [S][MP] page scores of the step
-    int32_t* item_prefix;  // [S + 1] prefix of attention work items (chunks * L * Hkv)
-    int32_t* tile_prefix;  // [S + 1] prefix of 64-token tiles
+    int32_t* item_prefix;  // [S + 1] prefix of attention work items (chunks * L * Hkv), spill path
+    int32_t* tile_prefix;  // [S + 1] prefix of 64-token tiles, spill path (mass)
+    int32_t* score_prefix; // [S + 1] prefix of 64-token tiles, every session (scores)
+    int32_t* ustart;       // [S + 1] prefix of fused units over the sessions
+    int32_t* plan;         // [1 + 3 (S + 1)]: passes, then (unit tokens, first, end session) per pass
+    int32_t* epoch;        // [1] observation counter; tags the fused unit statistics
+    unsigned long long* ustat;  // [U_cap][R][2] tagged (max, sum) of each fused unit's rows
+    unsigned long long* nstat;  // [S][R][2] tagged row normalisers (M, 1 / sum) of the fused path
     int32_t* chunks;       // [S] chunks per session (0 for a skipped session)
     int32_t* valid;        // [S] 1 when the session's counters are consistent
     int32_t* done;         // [1] completion counter of the append kernel
@@ -68,6 +95,14 @@ hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
 hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q,
                          int n_blocks, hipStream_t st);
 hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st);
+hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q,
+                         float* abar_out, hipStream_t st);
+size_t attend_lds_bytes(int G, int Tstride);
+const void* attend_kernel();
+// Launch the fused kernel in check mode with n_wg workgroups: every wave
+// waits (bounded, ~20 ms) until all workgroups have arrived; probe[1]
+// receives the fewest arrivals any workgroup saw (probe: 2 device ints).
+hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, hipStream_t st);
 hipError_t launch_mass(const Dims& dm, const View& v, const Scratch& sc, float* abar_out,
                        int n_blocks, hipStream_t st);
 hipError_t launch_score(const Dims& dm, const View& v, const Scratch& sc, float* page_score,

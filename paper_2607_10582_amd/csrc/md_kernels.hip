@@ -17,101 +17,9 @@
 //   k_compact   one block per session: page-table compaction, free-list push.
 // Every reduction is in a fixed order; no float atomics are used.
 
-#include <math.h>
-
-#include "md_internal.h"
+#include "md_device.h"
 
 namespace md {
-
-typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-// log2(e) / sqrt(128): logits are kept in base 2 so that 2^(x - m) is the
-// softmax numerator exp(q.k/sqrt(d) - m').
-constexpr float kLogitScale = (float)(1.4426950408889634074 / 11.313708498984760390);
-
-__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
-
-// 2^x on the transcendental unit (v_exp_f32, about 1 ulp).  Results below
-// 2^-126 come out as zero or denormal; softmax weights that small are
-// negligible next to the row maximum's weight of 1.
-__device__ __forceinline__ float hw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-    return v;
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
-}
-
-__device__ __forceinline__ int load_agent(const int32_t* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Exclusive prefix of one int per thread across the whole block (any multiple
-// of 64 threads up to 1024).  lds needs 17 ints.  Contains __syncthreads.
-__device__ int block_exclusive_scan(int v, int* lds, int* total) {
-    const int lane = lane_id(), wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    int incl = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int t = __shfl_up(incl, o);
-        if (lane >= o) incl += t;
-    }
-    if (lane == 63) lds[wid] = incl;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int acc = 0;
-        for (int w = 0; w < nw; ++w) {
-            const int t = lds[w];
-            lds[w] = acc;
-            acc += t;
-        }
-        lds[16] = acc;
-    }
-    __syncthreads();
-    const int res = lds[wid] + incl - v;
-    *total = lds[16];
-    __syncthreads();
-    return res;
-}
-
-// Largest s in [0, S) with pref[s] <= x, given pref[0] <= x < pref[S].
-__device__ __forceinline__ int find_session(const int* pref, int S, int x) {
-    int lo = 0, hi = S;
-    while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (pref[mid] <= x) lo = mid; else hi = mid;
-    }
-    return lo;
-}
-
-__device__ __forceinline__ bool counters_ok(int np, int nt, const Dims& dm) {
-    if (np < 0 || np > dm.MP) return false;
-    if (np == 0) return nt == 0;
-    return nt > (np - 1) * dm.P && nt <= np * dm.P;
-}
-
-// Split a float32 into three bfloat16 terms with x == hi + mid + lo exactly:
-// hi and mid truncate (the differences are exact by Sterbenz's lemma), and
-// what is left has at most 8 significant bits, so lo holds it exactly.
-__device__ __forceinline__ void split3(float x, uint32_t& hi, uint32_t& mid, uint32_t& lo) {
-    const uint32_t u = __float_as_uint(x);
-    const uint32_t h = u & 0xFFFF0000u;
-    const float r1 = x - __uint_as_float(h);
-    const uint32_t m = __float_as_uint(r1) & 0xFFFF0000u;
-    const float r2 = r1 - __uint_as_float(m);
-    hi = h >> 16;
-    mid = m >> 16;
-    lo = __float_as_uint(r2) >> 16;
-}
-
 
 // ---------------------------------------------------------------- append
 
@@ -192,44 +100,130 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     __syncthreads();
     if (!sh_last) return;
     __threadfence();
-    int it[4], ti[4];
-    int my_items = 0, my_tiles = 0, my_tokens = 0;
+    __shared__ int s_n[kMaxSessions];      // live tokens (0 for a skipped session)
+    __shared__ int s_pass[kMaxSessions];   // fused pass of the session, -1 on the spill path
+    __shared__ int s_cand[kMaxCand];       // fused units over all sessions, per unit size
+    __shared__ int s_T[kMaxSessions + 1];  // unit size of each pass
+    for (int s2 = threadIdx.x; s2 < dm.S; s2 += blockDim.x) {
+        const int np = load_agent(v.n_pages + s2);
+        const int nt = load_agent(v.n_tokens + s2);
+        const bool ok = counters_ok(np, nt, dm);
+        if (!ok) atomicOr(sc.status, kDevCorrupt);
+        sc.valid[s2] = ok ? 1 : 0;
+        s_n[s2] = ok ? nt : 0;
+        s_pass[s2] = -1;
+    }
+    const int n_cand = dm.fused ? (dm.Tmax - kUnitMin) / kUnitQuantum + 1 : 0;
+    for (int c = threadIdx.x; c < kMaxCand; c += blockDim.x) s_cand[c] = 0;
+    __syncthreads();
+    // Units each candidate size T = kUnitMin + c * kUnitQuantum would take if
+    // every session ran in one pass (one wave per candidate).
+    for (int c = threadIdx.x >> 6; c < n_cand; c += blockDim.x >> 6) {
+        const int T = kUnitMin + c * kUnitQuantum;
+        int u = 0;
+        for (int s2 = lane_id(); s2 < dm.S; s2 += 64) u += (s_n[s2] + T - 1) / T;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) u += __shfl_xor(u, o);
+        if (lane_id() == 0) s_cand[c] = u;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0 && dm.fused) {
+        // One pass with the smallest unit whose units fit the workgroups;
+        // otherwise sessions in order, packed greedily into passes of units
+        // of Tmax tokens (a session's units wait for each other row by row,
+        // so all of them run in the same pass).  A session larger than a
+        // whole pass takes the spill path.
+        int c = 0;
+        while (c < n_cand && s_cand[c] > dm.n_wg) ++c;
+        int np = 0;
+        if (c < n_cand) {
+            s_T[0] = kUnitMin + c * kUnitQuantum;
+            sc.plan[1] = s_T[0];
+            sc.plan[2] = 0;
+            sc.plan[3] = dm.S;
+            for (int s2 = 0; s2 < dm.S; ++s2) s_pass[s2] = 0;
+            np = 1;
+        } else {
+            int s0 = 0;
+            while (s0 < dm.S) {
+                int used = 0, e = s0;
+                while (e < dm.S) {
+                    const int u = (s_n[e] + dm.Tmax - 1) / dm.Tmax;
+                    if (used + u > dm.n_wg) break;
+                    used += u;
+                    s_pass[e] = np;
+                    ++e;
+                }
+                if (e == s0) {
+                    ++s0;
+                    continue;
+                }
+                s_T[np] = dm.Tmax;
+                sc.plan[1 + 3 * np] = dm.Tmax;
+                sc.plan[2 + 3 * np] = s0;
+                sc.plan[3 + 3 * np] = e;
+                ++np;
+                s0 = e;
+            }
+        }
+        sc.plan[0] = np;
+        *sc.epoch += 1;
+    }
+    __syncthreads();
+    // Work lists: fused units; attention items, chunks and mass tiles of the
+    // spill path; score tiles for every session.
+    int uu[4], it[4], ti[4], si[4];
+    int my_units = 0, my_items = 0, my_tiles = 0, my_stiles = 0, my_tokens = 0;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int s2 = threadIdx.x * 4 + k;
-        it[k] = ti[k] = 0;
+        uu[k] = it[k] = ti[k] = si[k] = 0;
         if (s2 < dm.S) {
-            const int np = load_agent(v.n_pages + s2);
-            const int nt = load_agent(v.n_tokens + s2);
-            const bool ok = counters_ok(np, nt, dm);
-            if (!ok) atomicOr(sc.status, kDevCorrupt);
-            const int ch = ok ? (np * dm.P + kChunk - 1) / kChunk : 0;
+            const int nt = s_n[s2];
+            const int ps = s_pass[s2];
+            const bool spill = ps < 0;
+            const int ch = spill ? (nt + kChunk - 1) / kChunk : 0;
             sc.chunks[s2] = ch;
-            sc.valid[s2] = ok ? 1 : 0;
+            uu[k] = spill ? 0 : (nt + s_T[ps] - 1) / s_T[ps];
             it[k] = ch * dm.LHkv;
-            ti[k] = ok ? (nt + kTile - 1) / kTile : 0;
-            my_tokens += ok ? nt : 0;
+            ti[k] = spill ? (nt + kTile - 1) / kTile : 0;
+            si[k] = (nt + kTile - 1) / kTile;
+            my_tokens += nt;
         }
+        my_units += uu[k];
         my_items += it[k];
         my_tiles += ti[k];
+        my_stiles += si[k];
     }
-    int tot_i, tot_t, tot_n;
+    int tot_u, tot_i, tot_t, tot_s, tot_n;
+    int ex_u = block_exclusive_scan(my_units, lds, &tot_u);
     int ex_i = block_exclusive_scan(my_items, lds, &tot_i);
     int ex_t = block_exclusive_scan(my_tiles, lds, &tot_t);
+    int ex_s = block_exclusive_scan(my_stiles, lds, &tot_s);
     block_exclusive_scan(my_tokens, lds, &tot_n);
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int s2 = threadIdx.x * 4 + k;
         if (s2 < dm.S) {
+            sc.ustart[s2] = ex_u;
             sc.item_prefix[s2] = ex_i;
             sc.tile_prefix[s2] = ex_t;
+            sc.score_prefix[s2] = ex_s;
         }
+        ex_u += uu[k];
         ex_i += it[k];
         ex_t += ti[k];
+        ex_s += si[k];
     }
     if (threadIdx.x == 0) {
+        if (tot_u > dm.U_cap) {            // cannot happen for consistent counters
+            atomicOr(sc.status, kDevCorrupt);
+            sc.plan[0] = 0;
+        }
+        sc.ustart[dm.S] = tot_u;
         sc.item_prefix[dm.S] = tot_i;
         sc.tile_prefix[dm.S] = tot_t;
+        sc.score_prefix[dm.S] = tot_s;
         *sc.done = 0;
         atomicAdd(&sc.counters[0], (unsigned long long)tot_n);
         atomicAdd(&sc.counters[1], 1ull);
@@ -249,9 +243,6 @@ hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
 struct Cursor {
     int s, lkv, c, nch;
 };
-
-// Wave-uniform value kept in a scalar register.
-__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // find_session with every LDS read made wave-uniform.
 __device__ __forceinline__ int find_session_uni(const int* pref, int S, int x) {
@@ -347,17 +338,6 @@ __device__ __forceinline__ void item_tiles(ItemTiles& it, const Cursor& cu, cons
     if (bad && lane == 0) atomicOr(status, kDevCorrupt);
 }
 
-typedef const __attribute__((address_space(1))) uint8_t* gbytes;
-typedef const __attribute__((address_space(1))) u32x4* gvec;
-
-// A wave-uniform global pointer held in scalar registers.
-__device__ __forceinline__ gbytes uni_ptr(const void* p) {
-    const uint64_t u = reinterpret_cast<uint64_t>(p);
-    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
-    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
-    return (gbytes)(((uint64_t)hi << 32) | lo);
-}
-
 // Four 16-byte pieces of one K row tile in the MFMA A layout: lane (h, g)
 // holds token h's dims 32j + 8g .. +7 for j = 0..3 (voff = 256 h + 16 g).
 // A tile without cached tokens reads the pool's first row tile instead
@@ -420,7 +400,6 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
     // at a time; the query operands load once per segment.
     while (it < end) {
         const int seg_end = min(end, it + (cu.nch - cu.c));
-        const int row_id = cu.s * dm.LHkv + cu.lkv;
         split_query_regs(bq, q, dm, cu.s, cu.lkv, h, g, status);
         const int l = uni(cu.lkv / dm.Hkv);
         const int kv = cu.lkv - l * dm.Hkv;
@@ -613,7 +592,7 @@ __global__ void __launch_bounds__(256) k_score(Dims dm, View v, Scratch sc, floa
                                                float* token_score) {
     __shared__ int s_pref[kMaxSessions + 1];
     const int S = dm.S;
-    for (int i = threadIdx.x; i <= S; i += blockDim.x) s_pref[i] = sc.tile_prefix[i];
+    for (int i = threadIdx.x; i <= S; i += blockDim.x) s_pref[i] = sc.score_prefix[i];
     __syncthreads();
     const int total = s_pref[S];
     const int lane = lane_id();
@@ -901,11 +880,16 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 size_t scratch_bytes(const Dims& dm) {
     size_t n = 0;
-    n += align256((size_t)dm.NP * dm.R * dm.P * sizeof(float));
-    n += align256((size_t)dm.S * dm.R * dm.max_chunks * sizeof(float2));
+    const size_t spill = dm.spill ? 1 : 0;   // the logits spill exists only when used
+    n += align256(spill * dm.NP * dm.R * dm.P * sizeof(float));
+    n += align256(spill * dm.S * dm.R * dm.max_chunks * sizeof(float2));
     n += align256((size_t)dm.S * dm.R * sizeof(float2));
     n += align256((size_t)dm.S * dm.MP * sizeof(float));
-    n += 4 * align256((size_t)(dm.S + 1) * sizeof(int32_t));
+    n += 6 * align256((size_t)(dm.S + 1) * sizeof(int32_t));
+    n += align256((size_t)(1 + 3 * (dm.S + 1)) * sizeof(int32_t));
+    n += align256(sizeof(int32_t));
+    n += align256((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long));
+    n += align256((size_t)dm.S * dm.R * 2 * sizeof(unsigned long long));
     n += align256(2 * sizeof(int32_t));
     n += align256(4 * sizeof(unsigned long long));
     return n;
@@ -918,14 +902,22 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
         p += align256(bytes);
         return r;
     };
-    sc->logits = reinterpret_cast<float*>(take((size_t)dm.NP * dm.R * dm.P * sizeof(float)));
-    sc->cstats = reinterpret_cast<float2*>(take((size_t)dm.S * dm.R * dm.max_chunks * sizeof(float2)));
+    const size_t spill = dm.spill ? 1 : 0;
+    sc->logits = reinterpret_cast<float*>(take(spill * dm.NP * dm.R * dm.P * sizeof(float)));
+    sc->cstats = reinterpret_cast<float2*>(take(spill * dm.S * dm.R * dm.max_chunks * sizeof(float2)));
     sc->rstats = reinterpret_cast<float2*>(take((size_t)dm.S * dm.R * sizeof(float2)));
     sc->pscore = reinterpret_cast<float*>(take((size_t)dm.S * dm.MP * sizeof(float)));
     sc->item_prefix = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
     sc->tile_prefix = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
     sc->chunks = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
     sc->valid = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
+    sc->score_prefix = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
+    sc->ustart = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
+    sc->plan = reinterpret_cast<int32_t*>(take((size_t)(1 + 3 * (dm.S + 1)) * sizeof(int32_t)));
+    sc->epoch = reinterpret_cast<int32_t*>(take(sizeof(int32_t)));
+    sc->ustat = reinterpret_cast<unsigned long long*>(
+        take((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long)));
+    sc->nstat = reinterpret_cast<unsigned long long*>(take((size_t)dm.S * dm.R * 2 * sizeof(unsigned long long)));
     int32_t* words = reinterpret_cast<int32_t*>(take(2 * sizeof(int32_t)));
     sc->done = words;
     sc->status = words + 1;

@@ -93,7 +93,7 @@ class Pair:
                  oracle_sessions: Optional[List[int]] = None, n0s=None, budgets=None,
                  regions=None, planted: int = 0, planted_strength=3.0, query_gain=0.0,
                  pinned_mask=None, alpha=None, n_phys_extra: int = 0, max_pages=None,
-                 steps=None):
+                 steps=None, fused: bool = True):
         self.w = w
         self.dev = torch.device(device)
         self.backend = backend
@@ -149,11 +149,12 @@ class Pair:
         self.cache.set_free_pages(perm[pos:][::-1])
         self.md = MemDecay(self.cache, torch.from_numpy(self.b), torch.from_numpy(self.lam),
                            rho=f32(w.rho), alpha=f32(self.alpha), tau_scale=f32(w.tau_scale),
-                           pinned_mask=self.pinned_mask)
+                           pinned_mask=self.pinned_mask, fused=fused)
         n_slots = n_phys * P
         self.abar = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
         self.tscore = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
         self.stats = Stats()
+        self.status_seen = 0
         self.k = 0
 
     # -------------------------------------------------------------- inputs
@@ -188,6 +189,9 @@ class Pair:
         md.score(token_score=self.tscore)
         md.select()
         torch.cuda.synchronize(self.dev)
+        dev_status = md.device_status()
+        self.status_seen |= dev_status
+        assert dev_status == 0, f"step {k}: device status {dev_status:#x}"
         c = self.cache
         host = {name: getattr(c, name).cpu().numpy() for name in
                 ("page_table", "page_serial", "n_pages", "n_tokens", "importance", "t_ref")}
@@ -283,7 +287,7 @@ class Pair:
         return self.stats
 
     def device_status(self) -> int:
-        return self.md.device_status()
+        return self.md.device_status() | self.status_seen
 
     def free_pages_consistent(self) -> bool:
         """Live pages plus free pages account for every physical page."""

@@ -56,7 +56,7 @@ def test_struct_layout_matches_the_header(lib):
     #include "memdecay.h"
     int main(void) {
       printf("%zu %zu %zu %zu %zu\n", sizeof(md_config), offsetof(md_config, rho),
-             offsetof(md_config, reserved), sizeof(md_region_params), sizeof(md_cache_view));
+             offsetof(md_config, flags), sizeof(md_region_params), sizeof(md_cache_view));
       printf("%zu %zu\n", offsetof(md_cache_view, importance), offsetof(md_cache_view, free_count));
       return 0; }
     '''
@@ -66,7 +66,7 @@ def test_struct_layout_matches_the_header(lib):
         open(c, "w").write(src)
         subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), c, "-o", exe], check=True)
         out = subprocess.run([exe], capture_output=True, text=True, check=True).stdout.split()
-    got = [ctypes.sizeof(B.md_config), B.md_config.rho.offset, B.md_config.reserved.offset,
+    got = [ctypes.sizeof(B.md_config), B.md_config.rho.offset, B.md_config.flags.offset,
            ctypes.sizeof(B.md_region_params), ctypes.sizeof(B.md_cache_view),
            B.md_cache_view.importance.offset, B.md_cache_view.free_count.offset]
     assert [int(x) for x in out] == got
@@ -75,7 +75,7 @@ def test_struct_layout_matches_the_header(lib):
 def good_config(**kw):
     c = dict(n_layers=28, n_q_heads=12, n_kv_heads=2, head_dim=128, page_size=16,
              max_sessions=16, max_pages=2100, n_phys_pages=40000, n_regions=7,
-             pinned_region_mask=1, rho=0.9, alpha=1.0, tau_scale=2.0, reserved=0)
+             pinned_region_mask=1, rho=0.9, alpha=1.0, tau_scale=2.0, flags=0)
     c.update(kw)
     return B.md_config(**c)
 
@@ -113,7 +113,7 @@ def fake_rp():
     (dict(alpha=-1.0), B.MD_E_INVALID),
     (dict(alpha=float("inf")), B.MD_E_INVALID),
     (dict(tau_scale=-2.0), B.MD_E_INVALID),
-    (dict(reserved=1), B.MD_E_INVALID),
+    (dict(flags=2), B.MD_E_INVALID),
 ])
 def test_init_rejects_bad_configs_on_the_host(lib, kw, expect):
     st, h = B.md_init_raw(good_config(**kw), fake_rp(), fake_view(), 0)

@@ -44,9 +44,12 @@ def run_pair(p: Pair, steps: int, label: str):
     return st
 
 
-def test_small_workload_free_run():
+@pytest.mark.parametrize("fused", [True, False])
+def test_small_workload_free_run(fused):
     w = C.get("small")
-    st = run_pair(Pair(w), w.steps, "small")
+    p = Pair(w, fused=fused)
+    assert p.md.kernel_config()["fused"] == fused
+    st = run_pair(p, w.steps, f"small-fused{int(fused)}")
     assert st.evicted_pages > 10
 
 
@@ -72,18 +75,19 @@ def test_small_workload_near_tau():
     run_pair(p, w.steps, "small-near-tau")
 
 
+@pytest.mark.parametrize("fused", [True, False])
 @pytest.mark.parametrize("P", [16, 64])
-def test_ragged_edge_sessions(P):
+def test_ragged_edge_sessions(P, fused):
     # empty, single-token, exact-page, page+1, partial-tail and longer
     # sessions in one batch; budgets below, at and above the pinned span.
     w = C.with_overrides(C.get("small"), L=3, Hq=4, Hkv=2, S=7, n0=None, P=P,
                          n0_range=(1, 2), steps=40, system_len=20)
     n0s = [0, 1, 15, 16, 17, 130, 700]
     budgets = [0, 0, 5, 16, 10, 100, 200]
-    run_pair(Pair(w, n0s=n0s, budgets=budgets), 40, f"ragged-edges-P{P}")
+    run_pair(Pair(w, n0s=n0s, budgets=budgets, fused=fused), 40, f"ragged-edges-P{P}-fused{int(fused)}")
 
 
-@pytest.mark.parametrize("Hq,Hkv", [(16, 2), (16, 1), (4, 4), (2, 1)])
+@pytest.mark.parametrize("Hq,Hkv", [(16, 2), (16, 1), (4, 4), (2, 1), (12, 12)])
 def test_group_sizes(Hq, Hkv):
     w = C.with_overrides(C.get("small"), L=2, Hq=Hq, Hkv=Hkv, steps=12)
     run_pair(Pair(w), 12, f"G={Hq // Hkv}")
@@ -123,13 +127,57 @@ def test_max_pages_per_session():
     run_pair(p, 4, "max-pages")
 
 
-def test_long32k_sampled_sessions():
+@pytest.mark.parametrize("fused", [True, False])
+def test_long32k_sampled_sessions(fused):
     # The 16 x 32,768-token workload at full size, inputs drawn on the
     # device; two sessions are checked token by token against the oracle
     # through the bulk eviction and the following steps.
     w = C.get("long32k")
-    p = Pair(w, backend="torch", oracle_sessions=[0, 11], steps=6)
-    run_pair(p, 3, "long32k")
+    p = Pair(w, backend="torch", oracle_sessions=[0, 11], steps=6, fused=fused)
+    cfg = p.md.kernel_config()
+    say(f"[long32k] kernel config {cfg}")
+    if fused:
+        assert cfg["fused"] and not cfg["spill"]
+    run_pair(p, 3, f"long32k-fused{int(fused)}")
+
+
+def test_hybrid_fused_and_spill_sessions():
+    # One session longer than a whole pass of the fused kernel (it takes the
+    # multi-kernel path) next to short ones (fused) in the same steps.
+    w = C.with_overrides(C.get("small"), L=1, Hq=16, Hkv=2, S=3, n0=None, P=64,
+                         n0_range=(1, 2), steps=3, system_len=1024, mean_span=512.0)
+    probe = Pair(C.with_overrides(w, S=1), n0s=[64], budgets=[64], max_pages=8192,
+                 oracle_sessions=[])
+    cfg = probe.md.kernel_config()
+    probe.close()
+    big = cfg["unit_max"] * cfg["workgroups"] + 1000
+    assert big <= 8190 * 64
+    say(f"[hybrid] kernel config {cfg}, long session {big} tokens")
+    p = Pair(w, n0s=[900, big, 3000], budgets=[300, big // 4, 3000], max_pages=8192)
+    assert p.md.kernel_config()["spill"]
+    run_pair(p, 3, "hybrid")
+
+
+def test_fused_matches_multikernel_path():
+    # Both device paths on the same inputs: attention masses and page scores
+    # agree to rounding.  The budget holds every token and no step opens a
+    # page (1700 + 3 tokens stay within 107 pages), so the slots line up.
+    w = C.with_overrides(C.get("qwen3_32x1700"), S=6, steps=3, budget_frac=1.0)
+    outs = []
+    for fused in (True, False):
+        p = Pair(w, oracle_sessions=[], fused=fused)
+        res = []
+        for _ in range(3):
+            p.step(compare=False)
+            res.append((p.abar.cpu().numpy().copy(), p.md.page_score.cpu().numpy().copy()))
+        assert p.device_status() == 0
+        outs.append(res)
+        p.close()
+    for (a1, s1), (a2, s2) in zip(*outs):
+        np.testing.assert_allclose(a1, a2, rtol=REL, atol=1e-30)
+        fin = np.isfinite(s1)
+        assert np.array_equal(fin, np.isfinite(s2))
+        np.testing.assert_allclose(s1[fin], s2[fin], rtol=REL, atol=1e-30)
 
 
 @pytest.mark.parametrize("name", ["ragged_p16", "ragged_p64"])
