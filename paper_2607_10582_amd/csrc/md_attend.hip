@@ -22,11 +22,11 @@
 //              and at each row end hand the row statistics to the manager and
 //              normalise the row kConsumeLag rows back.
 //   manager    stages the query terms of upcoming rows in LDS, merges the
-//              producers' row statistics and publishes them with a tag.  The
-//              manager of the session's first unit (the leader) gathers all
-//              units' statistics of the previous row into the row normaliser
-//              (max M, 1 / sum) and publishes it; the other managers read it
-//              a row later.  Traffic per row is linear in the unit count.
+//              producers' row statistics and publishes them with a tag, and
+//              gathers every unit's statistics of an earlier row into the row
+//              normaliser (max M, 1 / sum).  Each unit reads the others'
+//              words itself (one hop; the words are a few KB per row and stay
+//              in the caches).
 // Producer <-> manager hand-offs are LDS counters; unit <-> unit hand-offs are
 // 64-bit words (tag << 32 | float bits, the tag being the step's epoch)
 // written and polled with agent-scope atomics, so a word is either absent or
@@ -58,7 +58,6 @@ struct AttendArgs {
     const int32_t* plan;
     const int32_t* epoch;
     unsigned long long* ustat;
-    unsigned long long* nstat;
     int32_t* status;
     int32_t* probe;    // check mode only: [arrivals, least seen]
 };
@@ -72,8 +71,7 @@ enum { kFlagProd = 0, kFlagQ = kProducers, kFlagNorm = kProducers + 1, kFlagStop
 
 struct Lds {
     float* rowbuf;    // [kRowBufs][G][Tstride] base-2 logits of the held rows
-    uint32_t* qs;     // [2][3][G][64] hi, mid, lo bf16 query terms (pairs) of two rows
-    float* qraw;      // [2][qraw_floats(G)] float32 query rows as loaded
+    uint32_t* qs;     // [kQBufs][3][G][64] hi, mid, lo bf16 query terms (pairs) of staged rows
     float2* wstat;    // [kStatBufs][kProducers][16] producer row statistics
     float2* norm;     // [kNormBufs][16] row normalisers (M, 1 / Lambda)
     int* flags;       // [kFlagCount]
@@ -82,10 +80,7 @@ struct Lds {
 __host__ __device__ inline size_t rowbuf_bytes(int G, int Tstride) {
     return (size_t)kRowBufs * G * Tstride * sizeof(float);
 }
-__host__ __device__ inline size_t qs_bytes(int G) { return (size_t)2 * 3 * G * 64 * sizeof(uint32_t); }
-// A query row (G heads x 128 floats) rounded up to whole 64-lane x 16-byte
-// direct-to-LDS loads.
-__host__ __device__ inline int qraw_floats(int G) { return (G * kHeadDim + 255) / 256 * 256; }
+__host__ __device__ inline size_t qs_bytes(int G) { return (size_t)kQBufs * 3 * G * 64 * sizeof(uint32_t); }
 constexpr size_t kWstatBytes = (size_t)kStatBufs * kProducers * 16 * sizeof(float2);
 constexpr size_t kNormBytes = (size_t)kNormBufs * 16 * sizeof(float2);
 constexpr size_t kFlagBytes = 8 * sizeof(int);
@@ -98,8 +93,6 @@ __device__ __forceinline__ Lds carve(unsigned char* smem, int G, int Tstride) {
     o += rowbuf_bytes(G, Tstride);
     l.qs = reinterpret_cast<uint32_t*>(smem + o);
     o += qs_bytes(G);
-    l.qraw = reinterpret_cast<float*>(smem + o);
-    o += (size_t)2 * qraw_floats(G) * sizeof(float);
     l.wstat = reinterpret_cast<float2*>(smem + o);
     o += kWstatBytes;
     l.norm = reinterpret_cast<float2*>(smem + o);
@@ -108,24 +101,30 @@ __device__ __forceinline__ Lds carve(unsigned char* smem, int G, int Tstride) {
     return l;
 }
 
-// LDS hand-offs inside the workgroup use workgroup-scope acquire / release;
-// on gfx950 these order LDS accesses only (lgkmcnt waits) and leave the
-// global loads in flight untouched.
+// LDS hand-offs inside the workgroup.  A wave's LDS operations complete in
+// issue order, so publishing a flag after the data only needs the data's LDS
+// writes done (lgkmcnt) and the compiler kept from reordering; a C++
+// release store would also wait for the wave's outstanding global loads and
+// stores (vmcnt), which would drain the producers' load ring and stall the
+// manager on its in-flight requests.
 __device__ __forceinline__ int lds_get(int* p) {
-    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    const int v = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    asm volatile("" ::: "memory");
+    return v;
 }
 
 __device__ __forceinline__ void lds_publish(int* p, int v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-// Wait until *p >= target.  False when the wait ran out or the workgroup
-// stopped waiting after an earlier time-out.
 // Time limits of the waits, in ticks of the 100 MHz real-time counter.
 // Waits inside a workgroup outlast waits on other workgroups, so a stalled
 // session is reported by the wait that polls the other units.
-constexpr uint64_t kLdsWaitTicks = 40000000ull;      // 400 ms
-constexpr uint64_t kGlobalWaitTicks = 20000000ull;   // 200 ms
+constexpr uint64_t kLdsWaitTicks = 10000000ull;      // 100 ms
+constexpr uint64_t kGlobalWaitTicks = 5000000ull;    // 50 ms
+constexpr uint64_t kRecheckTicks = 300;              // 3 us: re-check an unanswered request
+constexpr uint64_t kUnitTicks = 100000000ull;        // 1 s: a unit stops waiting after this
 
 __device__ __forceinline__ uint64_t now_ticks() { return __builtin_amdgcn_s_memrealtime(); }
 
@@ -134,12 +133,16 @@ __device__ __forceinline__ void stop_all(int* flags, int32_t* status) {
     atomicOr(status, MD_DEV_TIMEOUT);
 }
 
-__device__ __forceinline__ bool lds_wait(int* p, int target, int* flags, int32_t* status) {
+// Wait until *p >= target.  False when the wait ran out (at its own limit
+// or the unit's deadline) or the workgroup stopped waiting after an earlier
+// time-out.
+__device__ __forceinline__ bool lds_wait(int* p, int target, int* flags, int32_t* status, uint64_t deadline) {
     if (lds_get(p) >= target) return true;
     const uint64_t t0 = now_ticks();
     while (lds_get(p) < target) {
         if (lds_get(flags + kFlagStop)) return false;
-        if (now_ticks() - t0 > kLdsWaitTicks) {
+        const uint64_t t = now_ticks();
+        if (t - t0 > kLdsWaitTicks || t > deadline) {
             stop_all(flags, status);
             return false;
         }
@@ -154,8 +157,39 @@ __device__ __forceinline__ void merge_stat(float& m, float& l, float m2, float l
     m = M;
 }
 
+// Wave-wide max and sum with DPP row shifts and row broadcasts (VALU only;
+// no LDS round trips).  Kogge-Stone within each 16-lane row (shifts 1, 2, 4,
+// 8; a lane whose source falls outside its row keeps the identity), then
+// lane 15 of rows 0 and 2 is folded into rows 1 and 3, and lane 31 into
+// rows 2 and 3: lane 63 ends with the reduction of all 64 lanes, read as a
+// wave-uniform value.
+#define MD_DPP(old, v, ctrl, rm) \
+    __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), ctrl, rm, 0xf, false))
+__device__ __forceinline__ float wave_max_dpp(float v) {
+    const float id = -INFINITY;
+    v = fmaxf(v, MD_DPP(id, v, 0x111, 0xf));   // row_shr:1
+    v = fmaxf(v, MD_DPP(id, v, 0x112, 0xf));   // row_shr:2
+    v = fmaxf(v, MD_DPP(id, v, 0x114, 0xf));   // row_shr:4
+    v = fmaxf(v, MD_DPP(id, v, 0x118, 0xf));   // row_shr:8
+    v = fmaxf(v, MD_DPP(id, v, 0x142, 0xa));   // row_bcast:15 into rows 1, 3
+    v = fmaxf(v, MD_DPP(id, v, 0x143, 0xc));   // row_bcast:31 into rows 2, 3
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+    const float id = 0.0f;
+    v += MD_DPP(id, v, 0x111, 0xf);
+    v += MD_DPP(id, v, 0x112, 0xf);
+    v += MD_DPP(id, v, 0x114, 0xf);
+    v += MD_DPP(id, v, 0x118, 0xf);
+    v += MD_DPP(id, v, 0x142, 0xa);
+    v += MD_DPP(id, v, 0x143, 0xc);
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+#undef MD_DPP
+
 struct Unit {
     int s, j, T, kt, ntok, nt_s, nu, us;
+    uint64_t deadline;   // real-time tick after which the unit stops waiting
 };
 
 // First query row (layer * Hq + KV head * G) of (layer, KV head) row r.
@@ -167,8 +201,7 @@ __device__ __forceinline__ int qrow0(const AttendDims& dm, int r) {
 // ------------------------------------------------------------ producer
 
 __device__ __forceinline__ void producer(const AttendDims& dm, const AttendArgs& a, const Lds& sm,
-                                         const Unit& un, int wv) {
-    const int lane = lane_id();
+                                         const Unit& un, int wv, int lane, uint32_t tag) {
     const int h = lane & 15;          // MFMA column: query head of the group
     const int g = lane >> 4;          // k-group of A/B, row quad of C
     const int hh = min(h, dm.G - 1);  // in-bounds head for the unused columns
@@ -214,7 +247,7 @@ __device__ __forceinline__ void producer(const AttendDims& dm, const AttendArgs&
 
     u32x4 bq[4][3];
     auto read_bq = [&](int r) {
-        const uint32_t* qb = sm.qs + (size_t)(r & 1) * 3 * dm.G * 64;
+        const uint32_t* qb = sm.qs + (size_t)(r % kQBufs) * 3 * dm.G * 64;
 #pragma unroll
         for (int p = 0; p < 3; ++p)
 #pragma unroll
@@ -225,7 +258,7 @@ __device__ __forceinline__ void producer(const AttendDims& dm, const AttendArgs&
     float acc_tok[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     const int my_tokens = kt * 16;
     auto consume = [&](int rc) {
-        lds_wait(flags + kFlagNorm, rc + 1, flags, a.status);
+        lds_wait(flags + kFlagNorm, rc + 1, flags, a.status, un.deadline);
         const float* rb = sm.rowbuf + (size_t)(rc % kRowBufs) * dm.G * dm.Tstride;
         const float2* nm = sm.norm + (rc % kNormBufs) * 16;
 #pragma unroll
@@ -242,7 +275,7 @@ __device__ __forceinline__ void producer(const AttendDims& dm, const AttendArgs&
         }
     };
 
-    lds_wait(flags + kFlagQ, 1, flags, a.status);
+    lds_wait(flags + kFlagQ, 1, flags, a.status, un.deadline);
     read_bq(0);
     u32x4 ring[4][4];
 #pragma unroll
@@ -289,8 +322,31 @@ __device__ __forceinline__ void producer(const AttendDims& dm, const AttendArgs&
                     m = -INFINITY;
                     lsum = 0.0f;
                     if (lane == 0) lds_publish(flags + kFlagProd + wv, row + 1);
+                    if (wv == 0) {
+                        // Producer 0 publishes the unit's statistics of the
+                        // row for the other units (the manager issues no
+                        // stores: its waits on its own loads must not wait
+                        // for a store's round trip too).
+#pragma unroll
+                        for (int pw = 1; pw < kProducers; ++pw)
+                            lds_wait(flags + kFlagProd + pw, row + 1, flags, a.status, un.deadline);
+                        if (lane < dm.G) {
+                            float um = -INFINITY, ul = 0.0f;
+#pragma unroll
+                            for (int pw = 0; pw < kProducers; ++pw) {
+                                const float2 st = sm.wstat[((row % kStatBufs) * kProducers + pw) * 16 + lane];
+                                merge_stat(um, ul, st.x, st.y);
+                            }
+                            unsigned long long* p =
+                                a.ustat + (((size_t)(un.us + un.j) * dm.R + qrow0(dm, row) + lane) << 1);
+                            const unsigned long long hi = (unsigned long long)tag << 32;
+                            __hip_atomic_store(p, hi | __float_as_uint(um), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            __hip_atomic_store(p + 1, hi | __float_as_uint(ul), __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+                        }
+                    }
                     if (row + 1 < dm.LHkv) {
-                        lds_wait(flags + kFlagQ, row + 2, flags, a.status);
+                        lds_wait(flags + kFlagQ, row + 2, flags, a.status, un.deadline);
                         read_bq(row + 1);
                     }
                     if (row >= kConsumeLag) consume(row - kConsumeLag);
@@ -324,187 +380,211 @@ __device__ __forceinline__ void producer(const AttendDims& dm, const AttendArgs&
 // ------------------------------------------------------------ manager
 
 __device__ __forceinline__ void manager(const AttendDims& dm, const AttendArgs& a, const Lds& sm,
-                                        const Unit& un, uint32_t tag) {
-    const int lane = lane_id();
+                                        const Unit& un, uint32_t tag, int lane) {
     int* flags = sm.flags;
     const int G = dm.G;
 
-    // Query row r: G heads x 128 floats, copied straight into LDS (no
-    // registers held while the copy is in flight), then split into the three
-    // bf16 terms the producers' B operands take.
-    const int qn = G * kHeadDim;
+    // Query row r: G heads x 128 floats, loaded a row ahead into registers
+    // (lane + 64 k holds float4 k), then split into the three bf16 terms the
+    // producers' B operands take.  (A direct-to-LDS copy would make every
+    // later LDS access of this wave wait for all its outstanding loads.)
+    f32x4 qv[4];
+    auto q_row = [&](int r) {
+        return reinterpret_cast<const f32x4*>(a.q + ((size_t)un.s * dm.L * dm.Hq + qrow0(dm, r)) * kHeadDim);
+    };
+    // Loads are unconditional (indices clamped into the row): loads under
+    // lane conditions make the compiler wait for every outstanding load
+    // before each of them.
     auto load_q = [&](int r) {
-        const float* qr = a.q + ((size_t)un.s * dm.L * dm.Hq + qrow0(dm, r)) * kHeadDim;
-        float* dst = sm.qraw + (size_t)(r & 1) * qraw_floats(G);
-        for (int i = 0; i < qraw_floats(G); i += 256) {
-            const int f = i + 4 * lane;
-            const float* src = qr + (f < qn ? f : 0);
-            __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                             (__attribute__((address_space(3))) void*)(dst + i), 16, 0, 0);
+        const f32x4* qr = q_row(r);
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            if (64 * k < G * 32) qv[k] = qr[min(lane + 64 * k, G * 32 - 1)];   // uniform condition
+    };
+    auto split_store = [&](uint32_t* qb, int f, const f32x4& x, bool& bad) {
+        const int hd = f >> 5, d2 = 2 * (f & 31);
+        uint32_t t[3][4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            bad |= !isfinite(x[e]);
+            split3(x[e], t[0][e], t[1][e], t[2][e]);
         }
+#pragma unroll
+        for (int p = 0; p < 3; ++p)
+            *reinterpret_cast<uint2*>(qb + (p * G + hd) * 64 + d2) =
+                make_uint2(t[p][0] | (t[p][1] << 16), t[p][2] | (t[p][3] << 16));
     };
     auto store_q = [&](int r) {
-        __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): the direct-to-LDS copy has landed
-        const float* src = sm.qraw + (size_t)(r & 1) * qraw_floats(G);
-        uint32_t* qb = sm.qs + (size_t)(r & 1) * 3 * G * 64;
+        uint32_t* qb = sm.qs + (size_t)(r % kQBufs) * 3 * G * 64;
         bool bad = false;
-#pragma unroll 1
-        for (int f = lane; f < G * 32; f += 64) {
-            const f32x4 x = *reinterpret_cast<const f32x4*>(src + 4 * f);
-            const int hd = f >> 5, d2 = 2 * (f & 31);
-            uint32_t t[3][4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                bad |= !isfinite(x[e]);
-                split3(x[e], t[0][e], t[1][e], t[2][e]);
-            }
-#pragma unroll
-            for (int p = 0; p < 3; ++p)
-                *reinterpret_cast<uint2*>(qb + (p * G + hd) * 64 + d2) =
-                    make_uint2(t[p][0] | (t[p][1] << 16), t[p][2] | (t[p][3] << 16));
+        for (int k = 0; k < 4; ++k) {
+            const int f = lane + 64 * k;
+            if (f < G * 32) split_store(qb, f, qv[k], bad);
+            __builtin_amdgcn_sched_barrier(0);   // one float4 at a time: few live registers
         }
+        // heads past the eighth (G > 8) are loaded here
+        const f32x4* qr = q_row(r);
+        for (int f = lane + 256; f < G * 32; f += 64) split_store(qb, f, qr[f], bad);
         if (bad) atomicOr(a.status, MD_DEV_NONFINITE);
     };
 
-    // Bounded poll of tagged words until every active lane holds words with
-    // this step's tag; false after a time-out (or a stop seen).
-    auto poll_words = [&](auto&& load_all) -> bool {
-        if (__all(load_all())) return true;
-        const uint64_t t0 = now_ticks();
-        while (true) {
-            __builtin_amdgcn_s_sleep(8);   // back off: many units may poll the same words
-            if (__all(load_all())) return true;
-            if (lds_get(flags + kFlagStop)) return false;
-            if (now_ticks() - t0 > kGlobalWaitTicks) {
-                stop_all(flags, a.status);
-                return false;
-            }
-        }
-    };
     auto set_norm = [&](int rc, int hd, float M, float inv) {
         sm.norm[(rc % kNormBufs) * 16 + hd] = make_float2(M, inv);
     };
-    const unsigned long long hi_tag = (unsigned long long)tag << 32;
-
-    // Leader (unit 0 of the session): every unit's statistics of row rc ->
-    // the row normaliser, eight heads at a time (lane k holds units k, k + 64,
-    // ...; a butterfly merges the lanes), published to the session's other
-    // units as tagged words and kept for this workgroup.
-    auto lead = [&](int rc) {
-        const int r0 = qrow0(dm, rc);
-        for (int h0 = 0; h0 < G; h0 += 8) {
-            float Mh[8], Lh[8];
+    auto tag_ok = [&](unsigned long long v) { return (uint32_t)(v >> 32) == tag; };
+    // Requests for the other units' words go out at one row's publication
+    // and are checked at the next, so the manager never waits on a global
+    // round trip while it has LDS work: lane k holds unit k of the first 64,
+    // its first eight heads.
+    unsigned long long w[8][2];
+    // p: the unit's words of head h0 (a valid unit for every lane)
+    auto load_words = [&](const unsigned long long* p, int h0) {
 #pragma unroll
-            for (int hd = 0; hd < 8; ++hd) {
-                Mh[hd] = -INFINITY;
-                Lh[hd] = 0.0f;
+        for (int hd = 0; hd < 8; ++hd) {
+            if (h0 + hd < G) {   // uniform condition
+                w[hd][0] = __hip_atomic_load(p + 2 * hd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                w[hd][1] = __hip_atomic_load(p + 2 * hd + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
+        }
+    };
+    auto words_ok = [&](int h0, bool act) {
+        bool ok = true;
+#pragma unroll
+        for (int hd = 0; hd < 8; ++hd)
+            if (h0 + hd < G && act) ok &= tag_ok(w[hd][0]) && tag_ok(w[hd][1]);
+        return ok;
+    };
+    auto unit_words = [&](int x, int k, int h0) {
+        return a.ustat + (((size_t)(un.us + k) * dm.R + qrow0(dm, x) + h0) << 1);
+    };
+    auto issue = [&](int x) {
+        const bool act = lane < un.nu;
+        load_words(unit_words(x, act ? lane : 0, 0), 0);
+    };
+    auto ready = [&]() -> bool { return __all(words_ok(0, lane < un.nu)); };
+
+    // Row x's normaliser: per head, a wave max of the units' maxima, then a
+    // wave sum of their sums rescaled to it (one exp2 per unit), both with
+    // DPP; eight heads at a time (the first eight of the first 64 units came
+    // with the request; the rest are fetched here with bounded waits).  Lane h
+    // keeps head h's running result.
+    auto finish = [&](int x) {
+        float run_m = -INFINITY, run_l = 0.0f;
+        for (int h0 = 0; h0 < G; h0 += 8) {
             for (int c0 = 0; c0 < un.nu; c0 += 64) {
                 const int k = c0 + lane;
                 const bool act = k < un.nu;
-                unsigned long long* p = a.ustat + (((size_t)(un.us + (act ? k : 0)) * dm.R + r0 + h0) << 1);
-                unsigned long long w[8][2];
-                poll_words([&]() {
-                    bool ok = true;
-#pragma unroll
-                    for (int hd = 0; hd < 8; ++hd) {
-                        if (h0 + hd < G && act) {
-                            w[hd][0] = __hip_atomic_load(p + 2 * hd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                            w[hd][1] = __hip_atomic_load(p + 2 * hd + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (c0 > 0 || h0 > 0) {
+                    const unsigned long long* p = unit_words(x, act ? k : 0, h0);
+                    const uint64_t t0 = now_ticks();
+                    while (true) {
+                        load_words(p, h0);
+                        if (__all(words_ok(h0, act)) || lds_get(flags + kFlagStop)) break;
+                        const uint64_t t = now_ticks();
+                        if (t - t0 > kGlobalWaitTicks || t > un.deadline) {
+                            stop_all(flags, a.status);
+                            break;
                         }
+                        __builtin_amdgcn_s_sleep(8);
                     }
-#pragma unroll
-                    for (int hd = 0; hd < 8; ++hd)
-                        if (h0 + hd < G && act)
-                            ok &= (uint32_t)(w[hd][0] >> 32) == tag && (uint32_t)(w[hd][1] >> 32) == tag;
-                    return ok;
-                });
-#pragma unroll
-                for (int hd = 0; hd < 8; ++hd)
-                    if (h0 + hd < G && act)
-                        merge_stat(Mh[hd], Lh[hd], __uint_as_float((uint32_t)w[hd][0]),
-                                   __uint_as_float((uint32_t)w[hd][1]));
-            }
-            float mine_m = 0.0f, mine_l = 1.0f;
-#pragma unroll
-            for (int hd = 0; hd < 8; ++hd) {
-#pragma unroll
-                for (int o = 1; o < 64; o <<= 1) merge_stat(Mh[hd], Lh[hd], __shfl_xor(Mh[hd], o), __shfl_xor(Lh[hd], o));
-                if (lane == hd) {
-                    mine_m = Mh[hd];
-                    mine_l = Lh[hd];
                 }
-            }
-            if (lane < 8 && h0 + lane < G) {
-                const float inv = 1.0f / mine_l;
-                set_norm(rc, h0 + lane, mine_m, inv);
-                if (un.nu > 1) {
-                    unsigned long long* q = a.nstat + (((size_t)un.s * dm.R + r0 + h0 + lane) << 1);
-                    __hip_atomic_store(q, hi_tag | __float_as_uint(mine_m), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    __hip_atomic_store(q + 1, hi_tag | __float_as_uint(inv), __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+                for (int hd = 0; hd < 8; ++hd) {
+                    if (h0 + hd < G) {
+                        const float m = act ? __uint_as_float((uint32_t)w[hd][0]) : -INFINITY;
+                        const float l = act ? __uint_as_float((uint32_t)w[hd][1]) : 0.0f;
+                        const float M = wave_max_dpp(m);
+                        const float L = wave_sum_dpp(m == -INFINITY ? 0.0f : l * hw_exp2(m - M));
+                        if (lane == h0 + hd) merge_stat(run_m, run_l, M, L);
+                    }
                 }
             }
         }
-        lds_publish(flags + kFlagNorm, rc + 1);
+        if (lane < G) set_norm(x, lane, run_m, 1.0f / run_l);
+        lds_publish(flags + kFlagNorm, x + 1);
     };
 
-    // Other units: the leader's normaliser of row rc.
-    auto follow = [&](int rc) {
-        const int r0 = qrow0(dm, rc);
-        const bool act = lane < G;
-        unsigned long long* q = a.nstat + (((size_t)un.s * dm.R + r0 + (act ? lane : 0)) << 1);
-        unsigned long long w0 = 0, w1 = 0;
-        poll_words([&]() {
-            if (!act) return true;
-            w0 = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            w1 = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            return (uint32_t)(w0 >> 32) == tag && (uint32_t)(w1 >> 32) == tag;
-        });
-        if (act) set_norm(rc, lane, __uint_as_float((uint32_t)w0), __uint_as_float((uint32_t)w1));
-        lds_publish(flags + kFlagNorm, rc + 1);
-    };
-
-    const bool leader = un.j == 0;
-    load_q(0);
-    store_q(0);
-    if (dm.LHkv > 1) {
-        load_q(1);
-        store_q(1);
+    // the first kQBufs query rows up front, the next one in flight
+    for (int r = 0; r < min(kQBufs, dm.LHkv); ++r) {
+        load_q(r);
+        store_q(r);
     }
-    lds_publish(flags + kFlagQ, min(2, dm.LHkv));
-    if (dm.LHkv > 2) load_q(2);
-    // Iteration r: publish row r's statistics; the leader reduces row r - 1
-    // (every unit has had a row's time to publish it), the others read the
-    // leader's normaliser of row r - 2.
-    for (int r = 0; r <= dm.LHkv + 1; ++r) {
-        if (r < dm.LHkv) {
-#pragma unroll
-            for (int w = 0; w < kProducers; ++w) lds_wait(flags + kFlagProd + w, r + 1, flags, a.status);
-            // query row r + 2 (its copy was started an iteration ago) into the
-            // buffer row r used: every producer has read row r's terms by now
-            if (r + 2 < dm.LHkv) {
-                store_q(r + 2);
-                lds_publish(flags + kFlagQ, r + 3);
-            }
-            if (lane < G) {
-                float m = -INFINITY, l = 0.0f;
-#pragma unroll
-                for (int w = 0; w < kProducers; ++w) {
-                    const float2 st = sm.wstat[((r % kStatBufs) * kProducers + w) * 16 + lane];
-                    merge_stat(m, l, st.x, st.y);
-                }
-                unsigned long long* p = a.ustat + (((size_t)(un.us + un.j) * dm.R + qrow0(dm, r) + lane) << 1);
-                __hip_atomic_store(p, hi_tag | __float_as_uint(m), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(p + 1, hi_tag | __float_as_uint(l), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            if (r + 3 < dm.LHkv) load_q(r + 3);
+    lds_publish(flags + kFlagQ, min(kQBufs, dm.LHkv));
+    if (dm.LHkv > kQBufs) load_q(kQBufs);
+
+    // Event loop, driven by the producers' progress.  Loads come back in
+    // issue order, so every load this wave waits on must be about a row old:
+    // the next query row and the request for the units' words go out
+    // together when a row is published, and both are consumed when the next
+    // row is.  The request for row x goes out at the publication of row
+    // x + 1 (every unit has had about a row to publish row x) and normally
+    // completes at the publication of row x + 2, kConsumeLag - 2 rows before
+    // the producers need it.  If the producers stop (they may be waiting
+    // for that very row), an unanswered request is checked and re-sent every
+    // kRecheckTicks on its own.  Only publishing and finishing rows count as
+    // progress for the time limit.
+    const int ahead = 2;
+    int r_pub = 0, x_next = 0, x_pend = -1, n_done = 0;
+    uint64_t last_prog = now_ticks(), issued_t = 0;
+    auto check = [&]() {   // x_pend >= 0; its words are a row or kRecheckTicks old
+        if (ready()) {
+            finish(x_pend);
+            ++n_done;
+            x_pend = -1;
+            last_prog = now_ticks();
+            return true;
         }
-        if (leader) {
-            if (r >= 1 && r <= dm.LHkv) lead(r - 1);
-        } else if (r >= 2) {
-            follow(r - 2);
+        return false;
+    };
+    while (n_done < dm.LHkv) {
+        bool all = r_pub < dm.LHkv;
+        if (all) {
+#pragma unroll
+            for (int pw = 0; pw < kProducers; ++pw) all &= lds_get(flags + kFlagProd + pw) > r_pub;
         }
+        if (all) {
+            const int r = r_pub;
+            // query row r + kQBufs (loaded at the previous publication) into
+            // the buffer row r used: every producer has read row r's terms
+            if (r + kQBufs < dm.LHkv) {
+                store_q(r + kQBufs);
+                lds_publish(flags + kFlagQ, r + kQBufs + 1);
+            }
+            const bool resend = x_pend >= 0 && !check();
+            r_pub = r + 1;
+            last_prog = now_ticks();
+            if (r + kQBufs + 1 < dm.LHkv) load_q(r + kQBufs + 1);
+            if (resend) {
+                issue(x_pend);
+                issued_t = now_ticks();
+            } else if (x_pend < 0 && x_next < dm.LHkv && (x_next + ahead <= r_pub || r_pub == dm.LHkv)) {
+                issue(x_next);
+                x_pend = x_next++;
+                issued_t = now_ticks();
+            }
+            continue;
+        }
+        if (x_pend >= 0) {
+            if (now_ticks() - issued_t > kRecheckTicks && !check()) {
+                issue(x_pend);
+                issued_t = now_ticks();
+            }
+        } else if (x_next < dm.LHkv && (x_next + ahead <= r_pub || r_pub == dm.LHkv)) {
+            issue(x_next);
+            x_pend = x_next++;
+            issued_t = now_ticks();
+            continue;
+        }
+        const uint64_t t = now_ticks();
+        if (lds_get(flags + kFlagStop) || t - last_prog > kGlobalWaitTicks || t > un.deadline) {
+            // give up on the step: release the producers
+            if (!lds_get(flags + kFlagStop)) stop_all(flags, a.status);
+            lds_publish(flags + kFlagQ, dm.LHkv + kQBufs);
+            lds_publish(flags + kFlagNorm, dm.LHkv);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
     }
 }
 
@@ -557,16 +637,21 @@ k_attend(AttendDims dm, AttendArgs a) {
         __syncthreads();   // the previous unit is done with the LDS
         if (threadIdx.x < kFlagCount) sm.flags[threadIdx.x] = 0;
         __syncthreads();
-        if (wv < kProducers) producer(dm, a, sm, un, wv);
-        else manager(dm, a, sm, un, tag);
+        un.deadline = now_ticks() + kUnitTicks;
+        // The lane index is made opaque here so that per-lane address
+        // arithmetic stays inside each role instead of being hoisted to the
+        // kernel entry and kept live (and spilled) across both roles.
+        int lane = (int)threadIdx.x & 63;
+        asm volatile("" : "+v"(lane));
+        if (wv < kProducers) producer(dm, a, sm, un, wv, lane, tag);
+        else manager(dm, a, sm, un, tag, lane);
     }
 }
 
 }  // namespace
 
 size_t attend_lds_bytes(int G, int Tstride) {
-    return rowbuf_bytes(G, Tstride) + qs_bytes(G) + (size_t)2 * qraw_floats(G) * sizeof(float) + kWstatBytes +
-           kNormBytes + kFlagBytes;
+    return rowbuf_bytes(G, Tstride) + qs_bytes(G) + kWstatBytes + kNormBytes + kFlagBytes;
 }
 
 const void* attend_kernel() { return reinterpret_cast<const void*>(&k_attend); }
@@ -576,7 +661,7 @@ hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const
     AttendDims ad{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.MP, dm.NP, dm.R, dm.LHkv, dm.Tstride, dm.U_cap,
                   dm.rho, dm.tau_scale};
     AttendArgs aa{v.k_pool, v.page_table, v.n_tokens, v.clock, v.imp, v.t_ref, q, abar_out,
-                  sc.ustart, sc.plan, sc.epoch, sc.ustat, sc.nstat, sc.status, nullptr};
+                  sc.ustart, sc.plan, sc.epoch, sc.ustat, sc.status, nullptr};
     void* args[] = {&ad, &aa};
     return hipLaunchCooperativeKernel(attend_kernel(), dim3(dm.n_wg), dim3(kAttendThreads), args,
                                       (unsigned)attend_lds_bytes(dm.G, dm.Tstride), st);

@@ -27,10 +27,11 @@ constexpr int kAttendThreads = 64 * (kProducers + 1);
 constexpr int kUnitQuantum = 16 * kProducers;   // one 16-token tile per producer
 constexpr int kUnitMin = 2 * kUnitQuantum;
 constexpr int kUnitMax = 16 * kUnitQuantum;     // 4 tokens per producer lane
-constexpr int kConsumeLag = 3;   // rows a producer runs ahead of the row it normalises
+constexpr int kConsumeLag = 5;   // rows a producer runs ahead of the row it normalises
 constexpr int kRowBufs = kConsumeLag + 1;       // rows of logits held in LDS
 constexpr int kStatBufs = 4;     // producer -> manager statistic buffers
-constexpr int kNormBufs = 4;     // manager -> producer normaliser buffers
+constexpr int kNormBufs = 8;     // manager -> producer normaliser buffers
+constexpr int kQBufs = 3;        // query rows staged ahead of the producers
 constexpr int kMaxCand = (kUnitMax - kUnitMin) / kUnitQuantum + 1;
 
 constexpr int kDevCorrupt = MD_DEV_CORRUPT;
@@ -78,7 +79,6 @@ struct Scratch {
     int32_t* plan;         // [1 + 3 (S + 1)]: passes, then (unit tokens, first, end session) per pass
     int32_t* epoch;        // [1] observation counter; tags the fused unit statistics
     unsigned long long* ustat;  // [U_cap][R][2] tagged (max, sum) of each fused unit's rows
-    unsigned long long* nstat;  // [S][R][2] tagged row normalisers (M, 1 / sum) of the fused path
     int32_t* chunks;       // [S] chunks per session (0 for a skipped session)
     int32_t* valid;        // [S] 1 when the session's counters are consistent
     int32_t* done;         // [1] completion counter of the append kernel

@@ -889,7 +889,6 @@ size_t scratch_bytes(const Dims& dm) {
     n += align256((size_t)(1 + 3 * (dm.S + 1)) * sizeof(int32_t));
     n += align256(sizeof(int32_t));
     n += align256((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long));
-    n += align256((size_t)dm.S * dm.R * 2 * sizeof(unsigned long long));
     n += align256(2 * sizeof(int32_t));
     n += align256(4 * sizeof(unsigned long long));
     return n;
@@ -917,7 +916,6 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
     sc->epoch = reinterpret_cast<int32_t*>(take(sizeof(int32_t)));
     sc->ustat = reinterpret_cast<unsigned long long*>(
         take((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long)));
-    sc->nstat = reinterpret_cast<unsigned long long*>(take((size_t)dm.S * dm.R * 2 * sizeof(unsigned long long)));
     int32_t* words = reinterpret_cast<int32_t*>(take(2 * sizeof(int32_t)));
     sc->done = words;
     sc->status = words + 1;
