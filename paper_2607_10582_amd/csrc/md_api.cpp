@@ -187,46 +187,28 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     for (size_t i = 0; i < nrp; ++i)
         if (!(hb[i] >= 0.0f) || !isfinite(hb[i]) || !(hl[i] >= 0.0f) || !isfinite(hl[i])) return MD_E_INVALID;
 
-    // Fused observation kernel: LDS for three workgroups per CU sets the
-    // largest unit; the occupancy at that LDS size sets the grid, which md_init
-    // then checks on the device (all workgroups resident at once).
+    // Fused observation kernel: up to kAttendPerCu workgroups per CU, as
+    // many as its LDS and registers allow; md_init then checks on the device
+    // that all of them are resident at once.
     const int n_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
     int occ = 0;
     if (dm.fused) {
-        const size_t per_cu = prop.maxSharedMemoryPerMultiProcessor > 0 ? prop.maxSharedMemoryPerMultiProcessor
-                                                                        : (size_t)160 * 1024;
-        auto unit_max = [&](size_t budget) -> int64_t {
-            const size_t fixed = md::attend_lds_bytes(dm.G, 0);
-            if (budget <= fixed) return 0;
-            const int64_t stride = (int64_t)((budget - fixed) / ((size_t)md::kRowBufs * dm.G * sizeof(float)));
-            const int64_t t = (stride - 4) / md::kUnitQuantum * md::kUnitQuantum;
-            return t > md::kUnitMax ? md::kUnitMax : t;
-        };
-        for (size_t budget : {per_cu / 3, (size_t)64 * 1024}) {
-            const int64_t tmax = unit_max(budget);
-            if (tmax < md::kUnitMin) continue;
-            const size_t lds = md::attend_lds_bytes(dm.G, (int)tmax + 4);
-            if (hipFuncSetAttribute(md::attend_kernel(), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
-                hipSuccess) {
-                (void)hipGetLastError();
-                continue;
-            }
-            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(), md::kAttendThreads, lds) !=
-                hipSuccess)
-                return MD_E_HIP;
-            if (occ >= 1) {
-                dm.Tmax = (int)tmax;
-                dm.Tstride = dm.Tmax + 4;
-                break;
-            }
+        const size_t lds = md::attend_lds_bytes(dm.G);
+        if (hipFuncSetAttribute(md::attend_kernel(dm.G), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+            hipSuccess) {
+            (void)hipGetLastError();
+        } else if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(dm.G), md::kAttendThreads,
+                                                                lds) != hipSuccess) {
+            return MD_E_HIP;
         }
+        if (occ > md::kAttendPerCu) occ = md::kAttendPerCu;
         dm.n_wg = occ * n_cu;
-        dm.fused = occ >= 1 && dm.Tmax >= md::kUnitMin;
+        dm.fused = occ >= 1;
     }
     if (dm.fused) {
-        dm.U_cap = (int)(((int64_t)dm.NP * dm.P + md::kUnitMin - 1) / md::kUnitMin + dm.S);
+        dm.U_cap = (int)(((int64_t)dm.NP * dm.P + md::kUnitTokens - 1) / md::kUnitTokens + dm.S);
     } else {
-        dm.Tmax = dm.Tstride = dm.n_wg = dm.U_cap = 0;
+        dm.n_wg = dm.U_cap = 0;
     }
     // The fused kernel's workgroups wait for each other, so all of them must
     // be resident together: check it on the device, and step the grid down
@@ -248,9 +230,9 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
         (void)hipFree(probe);
         dm.n_wg = verified;
         dm.fused = verified > 0;
-        if (!dm.fused) dm.Tmax = dm.Tstride = dm.U_cap = 0;
+        if (!dm.fused) dm.U_cap = 0;
     }
-    dm.spill = !dm.fused || (int64_t)dm.MP * dm.P > (int64_t)dm.n_wg * dm.Tmax;
+    dm.spill = !dm.fused || (int64_t)dm.MP * dm.P > (int64_t)dm.n_wg * md::kUnitTokens;
 
     md_handle_s* h = new (std::nothrow) md_handle_s();
     if (h == nullptr) return MD_E_NOMEM;
@@ -308,7 +290,7 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     hipError_t e = timed_launch(h, MD_K_APPEND, [&] {
         return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, h->stream); });
     // Sessions that fit one pass of the fused kernel run there; the others
-    // (only possible when a session may outgrow n_wg * Tmax tokens) take the
+    // (only possible when a session may outgrow n_wg * kUnitTokens tokens) take the
     // three-kernel path with the logits in HBM.
     if (e == hipSuccess && h->dm.fused) e = timed_launch(h, MD_K_ATTEND, [&] {
         return md::launch_attend(h->dm, h->v, h->sc, q, abar_out, h->stream); });
@@ -418,7 +400,7 @@ md_status md_kernel_config(md_handle h, int32_t* out) {
     if (h == nullptr || out == nullptr) return MD_E_INVALID;
     out[0] = h->dm.fused;
     out[1] = h->dm.spill;
-    out[2] = h->dm.Tmax;
+    out[2] = h->dm.fused ? md::kUnitTokens : 0;
     out[3] = h->dm.n_wg;
     return MD_OK;
 }

@@ -17,22 +17,15 @@ constexpr int kMaxRows = 1024;      // L * Hq
 constexpr int kMaxPages = 8192;     // page-table capacity per session
 constexpr int kSelThreads = 1024;   // select / compact block size
 constexpr int kPerThread = kMaxPages / kSelThreads;
-// Fused observation kernel (k_attend): three producer waves and one manager
-// wave per workgroup (a multiple of the CU's four SIMDs: workgroups of other
-// wave counts do not all fit at the occupancy the runtime reports); a unit of
-// work is one session's block of T tokens (T a multiple of kUnitQuantum,
-// between kUnitMin and Dims::Tmax) over every (layer, KV head) row.
-constexpr int kProducers = 3;
-constexpr int kAttendThreads = 64 * (kProducers + 1);
-constexpr int kUnitQuantum = 16 * kProducers;   // one 16-token tile per producer
-constexpr int kUnitMin = 2 * kUnitQuantum;
-constexpr int kUnitMax = 16 * kUnitQuantum;     // 4 tokens per producer lane
-constexpr int kConsumeLag = 5;   // rows a producer runs ahead of the row it normalises
+// Fused observation kernel (k_attend): four waves per workgroup, all doing
+// the same job; a unit of work is one session's block of kUnitTokens tokens
+// (16 tokens per lane row of a wave's four MFMA tiles) over every
+// (layer, KV head) row.
+constexpr int kAttendThreads = 256;
+constexpr int kUnitTokens = 256;
+constexpr int kAttendPerCu = 2;   // workgroups per CU: eight waves stream enough loads to saturate HBM
+constexpr int kConsumeLag = 7;   // rows a unit runs ahead of the row it normalises
 constexpr int kRowBufs = kConsumeLag + 1;       // rows of logits held in LDS
-constexpr int kStatBufs = 4;     // producer -> manager statistic buffers
-constexpr int kNormBufs = 8;     // manager -> producer normaliser buffers
-constexpr int kQBufs = 3;        // query rows staged ahead of the producers
-constexpr int kMaxCand = (kUnitMax - kUnitMin) / kUnitQuantum + 1;
 
 constexpr int kDevCorrupt = MD_DEV_CORRUPT;
 
@@ -40,8 +33,6 @@ struct Dims {
     int L, Hq, Hkv, G, P, Pshift, S, MP, NP, R, LHkv, n_regions, max_chunks;
     int fused;     // 1: sessions that fit one pass run on k_attend
     int spill;     // 1: some session may not fit a pass (the spill kernels run)
-    int Tmax;      // largest fused unit, tokens
-    int Tstride;   // LDS row stride of a fused logits row, floats (Tmax + 4)
     int n_wg;      // k_attend workgroups (all co-resident)
     int U_cap;     // capacity of the per-step fused unit list
     uint32_t pin_mask;
@@ -79,6 +70,7 @@ struct Scratch {
     int32_t* plan;         // [1 + 3 (S + 1)]: passes, then (unit tokens, first, end session) per pass
     int32_t* epoch;        // [1] observation counter; tags the fused unit statistics
     unsigned long long* ustat;  // [U_cap][R][2] tagged (max, sum) of each fused unit's rows
+    unsigned long long* unorm;  // [S][R][2] tagged row normalisers (M, 1 / Lambda) of the fused sessions
     int32_t* chunks;       // [S] chunks per session (0 for a skipped session)
     int32_t* valid;        // [S] 1 when the session's counters are consistent
     int32_t* done;         // [1] completion counter of the append kernel
@@ -97,8 +89,8 @@ hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const
 hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st);
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q,
                          float* abar_out, hipStream_t st);
-size_t attend_lds_bytes(int G, int Tstride);
-const void* attend_kernel();
+size_t attend_lds_bytes(int G);
+const void* attend_kernel(int G);   // the instantiation for query group size G
 // Launch the fused kernel in check mode with n_wg workgroups: every wave
 // waits (bounded, ~20 ms) until all workgroups have arrived; probe[1]
 // receives the fewest arrivals any workgroup saw (probe: 2 device ints).

@@ -102,8 +102,6 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     __threadfence();
     __shared__ int s_n[kMaxSessions];      // live tokens (0 for a skipped session)
     __shared__ int s_pass[kMaxSessions];   // fused pass of the session, -1 on the spill path
-    __shared__ int s_cand[kMaxCand];       // fused units over all sessions, per unit size
-    __shared__ int s_T[kMaxSessions + 1];  // unit size of each pass
     for (int s2 = threadIdx.x; s2 < dm.S; s2 += blockDim.x) {
         const int np = load_agent(v.n_pages + s2);
         const int nt = load_agent(v.n_tokens + s2);
@@ -113,58 +111,31 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         s_n[s2] = ok ? nt : 0;
         s_pass[s2] = -1;
     }
-    const int n_cand = dm.fused ? (dm.Tmax - kUnitMin) / kUnitQuantum + 1 : 0;
-    for (int c = threadIdx.x; c < kMaxCand; c += blockDim.x) s_cand[c] = 0;
-    __syncthreads();
-    // Units each candidate size T = kUnitMin + c * kUnitQuantum would take if
-    // every session ran in one pass (one wave per candidate).
-    for (int c = threadIdx.x >> 6; c < n_cand; c += blockDim.x >> 6) {
-        const int T = kUnitMin + c * kUnitQuantum;
-        int u = 0;
-        for (int s2 = lane_id(); s2 < dm.S; s2 += 64) u += (s_n[s2] + T - 1) / T;
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) u += __shfl_xor(u, o);
-        if (lane_id() == 0) s_cand[c] = u;
-    }
     __syncthreads();
     if (threadIdx.x == 0 && dm.fused) {
-        // One pass with the smallest unit whose units fit the workgroups;
-        // otherwise sessions in order, packed greedily into passes of units
-        // of Tmax tokens (a session's units wait for each other row by row,
-        // so all of them run in the same pass).  A session larger than a
-        // whole pass takes the spill path.
-        int c = 0;
-        while (c < n_cand && s_cand[c] > dm.n_wg) ++c;
-        int np = 0;
-        if (c < n_cand) {
-            s_T[0] = kUnitMin + c * kUnitQuantum;
-            sc.plan[1] = s_T[0];
-            sc.plan[2] = 0;
-            sc.plan[3] = dm.S;
-            for (int s2 = 0; s2 < dm.S; ++s2) s_pass[s2] = 0;
-            np = 1;
-        } else {
-            int s0 = 0;
-            while (s0 < dm.S) {
-                int used = 0, e = s0;
-                while (e < dm.S) {
-                    const int u = (s_n[e] + dm.Tmax - 1) / dm.Tmax;
-                    if (used + u > dm.n_wg) break;
-                    used += u;
-                    s_pass[e] = np;
-                    ++e;
-                }
-                if (e == s0) {
-                    ++s0;
-                    continue;
-                }
-                s_T[np] = dm.Tmax;
-                sc.plan[1 + 3 * np] = dm.Tmax;
-                sc.plan[2 + 3 * np] = s0;
-                sc.plan[3 + 3 * np] = e;
-                ++np;
-                s0 = e;
+        // Sessions in order, packed greedily into passes of at most n_wg
+        // units (a session's units wait for each other row by row, so all of
+        // them run in the same pass).  A session larger than a whole pass
+        // takes the spill path.
+        int np = 0, s0 = 0;
+        while (s0 < dm.S) {
+            int used = 0, e = s0;
+            while (e < dm.S) {
+                const int u = (s_n[e] + kUnitTokens - 1) / kUnitTokens;
+                if (used + u > dm.n_wg) break;
+                used += u;
+                s_pass[e] = np;
+                ++e;
             }
+            if (e == s0) {   // too large for any pass
+                ++s0;
+                continue;
+            }
+            sc.plan[1 + 3 * np] = kUnitTokens;
+            sc.plan[2 + 3 * np] = s0;
+            sc.plan[3 + 3 * np] = e;
+            ++np;
+            s0 = e;
         }
         sc.plan[0] = np;
         *sc.epoch += 1;
@@ -184,7 +155,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             const bool spill = ps < 0;
             const int ch = spill ? (nt + kChunk - 1) / kChunk : 0;
             sc.chunks[s2] = ch;
-            uu[k] = spill ? 0 : (nt + s_T[ps] - 1) / s_T[ps];
+            uu[k] = spill ? 0 : (nt + kUnitTokens - 1) / kUnitTokens;
             it[k] = ch * dm.LHkv;
             ti[k] = spill ? (nt + kTile - 1) / kTile : 0;
             si[k] = (nt + kTile - 1) / kTile;
@@ -889,6 +860,7 @@ size_t scratch_bytes(const Dims& dm) {
     n += align256((size_t)(1 + 3 * (dm.S + 1)) * sizeof(int32_t));
     n += align256(sizeof(int32_t));
     n += align256((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long));
+    n += align256((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long));
     n += align256(2 * sizeof(int32_t));
     n += align256(4 * sizeof(unsigned long long));
     return n;
@@ -916,6 +888,8 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
     sc->epoch = reinterpret_cast<int32_t*>(take(sizeof(int32_t)));
     sc->ustat = reinterpret_cast<unsigned long long*>(
         take((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long)));
+    sc->unorm = reinterpret_cast<unsigned long long*>(
+        take((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long)));
     int32_t* words = reinterpret_cast<int32_t*>(take(2 * sizeof(int32_t)));
     sc->done = words;
     sc->status = words + 1;
