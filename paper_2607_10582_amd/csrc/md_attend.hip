@@ -192,6 +192,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         }
     }
     const unsigned long long vmask = __ballot(myok);
+    const bool wave_full = (vmask & 0xFull) == 0xFull && wtok0 + 16 * kTiles <= un.ntok;
 
     // K tile u of row r in the MFMA A layout; a tile without cached tokens,
     // or past the last row, reads the pool's first tile (its logits are
@@ -361,18 +362,31 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         }
     };
 
+    // Row x's softmax weights of this wave's tokens, added to their mass.
+    // The held values are 2^(logit - m_w), m_w being the wave's maximum of
+    // the row for head h, so a weight is the held value times
+    // f_h = 2^(m_w - M_h) / Lambda_h: lane h works f_h out once, and every
+    // lane reads it from lane h.
     float acc = 0.0f;   // attention mass of token wtok0 + lane, summed over rows
-    auto consume = [&](int x) {
+    auto consume = [&](int x, float mw) {
         const float* rb = sm.rowbuf + (size_t)(x % kRowBufs) * G * kTstride + wtok0 + lane;
-        const float2* nm = sm.norm + (x & 1) * 16;
+        const float2 n = sm.norm[(x & 1) * 16 + hh];
+        const float f = h < G ? hw_exp2(mw - n.x) * n.y : 0.0f;
         float sum = 0.0f;
 #pragma unroll
-        for (int hd = 0; hd < 4 * NH; ++hd) {
-            const int hc = min(hd, G - 1);
-            const float2 n = nm[hc];
-            sum += hw_exp2(rb[hc * kTstride] - n.x) * (hd < G ? n.y : 0.0f);
-        }
+        for (int hd = 0; hd < 4 * NH; ++hd)   // heads past the group read a valid row and weigh zero
+            sum = fmaf(rb[min(hd, G - 1) * kTstride], __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), hd)), sum);
         acc += sum;
+    };
+    // The wave's row maxima of the last kConsumeLag rows (lane h: head h),
+    // newest first.
+    float mh[kConsumeLag];
+#pragma unroll
+    for (int k = 0; k < kConsumeLag; ++k) mh[k] = 0.0f;
+    auto push_max = [&](float v) {
+#pragma unroll
+        for (int k = kConsumeLag - 1; k > 0; --k) mh[k] = mh[k - 1];
+        mh[0] = v;
     };
 
     // Bookkeeping of iteration r (a row of tiles for r < LHkv, then
@@ -401,7 +415,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     auto after_tiles = [&](int r) {   // publish row r - 1, normalise row r - 7
         if (r >= 1 && r - 1 <= last) publish(r - 1);
         const int xf = r - kConsumeLag;
-        if (xf >= 0 && xf <= last) consume(xf);
+        if (xf >= 0 && xf <= last) consume(xf, mh[kConsumeLag - 1]);
     };
 
     // ---- prologue: query row 0 staged; then the loads in the order every
@@ -456,28 +470,43 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
 #pragma unroll
         for (int u = 0; u < kTiles; ++u) load_tile(ring[u], row + 2, u);
 
-        float m = -INFINITY, lsum = 0.0f;
+        // Base-2 logits of the wave's 64 tokens (lane: head h, tokens
+        // 16 u + 4 g + i), their maximum and the sum of 2^(logit - max) per
+        // head; the LDS row keeps 2^(logit - max).
+        float xs[kTiles][4];
+#pragma unroll
+        for (int u = 0; u < kTiles; ++u)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) xs[u][i] = c[u][i] * kLogitScale;
+        if (!wave_full) {   // tokens past the unit's end, tiles without a page
+#pragma unroll
+            for (int u = 0; u < kTiles; ++u)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (!((vmask >> u) & 1ull) || wtok0 + 16 * u + 4 * g + i >= un.ntok) xs[u][i] = -INFINITY;
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int u = 0; u < kTiles; ++u)
+            mx = fmaxf(mx, fmaxf(fmaxf(xs[u][0], xs[u][1]), fmaxf(xs[u][2], xs[u][3])));
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float ms = mx == -INFINITY ? 0.0f : mx;
+        float ls = 0.0f;
         float* rbw = sm.rowbuf + ((size_t)(row % kRowBufs) * G + h) * kTstride + wtok0 + 4 * g;
 #pragma unroll
         for (int u = 0; u < kTiles; ++u) {
-            const int lt0 = wtok0 + 16 * u + 4 * g;   // unit-local token of c[u][0]
-            const bool tok_ok = (vmask >> u) & 1ull;
-            float xs[4];
+            f32x4 pv;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) xs[i] = (tok_ok && lt0 + i < un.ntok) ? c[u][i] * kLogitScale : -INFINITY;
-            const float mn = fmaxf(m, fmaxf(fmaxf(xs[0], xs[1]), fmaxf(xs[2], xs[3])));
-            const bool live = mn != -INFINITY;
-            const float ms = live ? mn : 0.0f;
-            const float part =
-                (hw_exp2(xs[0] - ms) + hw_exp2(xs[1] - ms)) + (hw_exp2(xs[2] - ms) + hw_exp2(xs[3] - ms));
-            lsum = live ? lsum * hw_exp2(m - ms) + part : lsum;
-            m = live ? mn : m;
-            if (h < G) *reinterpret_cast<f32x4*>(rbw + 16 * u) = f32x4{xs[0], xs[1], xs[2], xs[3]};
+            for (int i = 0; i < 4; ++i) pv[i] = hw_exp2(xs[u][i] - ms);
+            ls += (pv[0] + pv[1]) + (pv[2] + pv[3]);
+            if (h < G) *reinterpret_cast<f32x4*>(rbw + 16 * u) = pv;
         }
+        ls += __shfl_xor(ls, 16);
+        ls += __shfl_xor(ls, 32);
         after_tiles(row);
-#pragma unroll
-        for (int o = 16; o <= 32; o <<= 1) merge_stat(m, lsum, __shfl_xor(m, o), __shfl_xor(lsum, o));
-        if (g == 0 && h < G) sm.wstat[((row & 1) * kWaves + wv) * 16 + h] = make_float2(m, lsum);
+        push_max(ms);
+        if (g == 0 && h < G) sm.wstat[((row & 1) * kWaves + wv) * 16 + h] = make_float2(mx, ls);
         lds_sync();
     };
     int row = 0;
@@ -492,6 +521,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         use_loads(r);
         issue_loads(r);
         after_tiles(r);
+        push_max(0.0f);
         lds_sync();
     }
 
@@ -509,8 +539,11 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
 
 // ------------------------------------------------------------ kernel
 
+// Two workgroups per CU (two waves per SIMD) for groups of up to eight query
+// heads; larger groups need a CU's LDS for one workgroup, which then may use
+// the whole register file.
 template <int NH>
-__global__ void __launch_bounds__(kAttendThreads) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(kAttendThreads) __attribute__((amdgpu_waves_per_eu(NH == 4 ? 1 : 2)))
 k_attend(AttendDims dm, AttendArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     if (a.probe != nullptr) {
