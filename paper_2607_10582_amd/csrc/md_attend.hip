@@ -157,11 +157,9 @@ struct Unit {
     uint64_t deadline;   // real-time tick after which the unit stops waiting
 };
 
-// First query row (layer * Hq + KV head * G) of (layer, KV head) row r.
-__device__ __forceinline__ int qrow0(const AttendDims& dm, int r) {
-    const int l = r / dm.Hkv;
-    return l * dm.Hq + (r - l * dm.Hkv) * dm.G;
-}
+// First query row (layer * Hq + KV head * G) of (layer, KV head) row r:
+// with Hq = Hkv * G that is r * G.
+__device__ __forceinline__ int qrow0(const AttendDims& dm, int r) { return r * dm.G; }
 
 // One wave's part of a unit.  NH = normaliser heads per wave (G <= 4 NH).
 template <int NH>
@@ -252,7 +250,11 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     auto norm_word = [&](int x, int hd) {
         return a.unorm + ((((size_t)un.s) * dm.R + qrow0(dm, x) + hd) << 1);
     };
-    auto is_lead = [&](int x) { return x % un.nu == un.j; };
+    // Rows this unit leads are j, j + nu, j + 2 nu, ...: lead_next is the
+    // next one to request, lead_now says whether the previous request was
+    // this unit's (both advance once per iteration).
+    int lead_next = un.j;
+    bool lead_now = false;
     // Re-read until every active lane's words carry the step's tag (bounded).
     auto await_tags = [&](auto&& ready, auto&& reload) {
         if (__all(ready()) || dead) return;
@@ -403,14 +405,18 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // r + 1 came in, so no wait ever holds the tile loads up (loads come back
     // in issue order).
     auto use_loads = [&](int r) {   // steps of iteration r that use iteration r - 1's loads
-        const int xa = r - 6, xb = r - 4;
+        const int xa = r - 6;
         if (xa >= 0 && xa <= last) check_norm(xa);
-        if (xb >= 0 && xb <= last && is_lead(xb)) lead(xb);
+        if (lead_now) lead(r - 4);
     };
     auto issue_loads = [&](int r) {
         load_norm(min(max(r - 5, 0), last));
         const int xd = r - 3;
-        if (xd >= 0 && xd <= last && is_lead(xd)) load_stats(xd, 0);
+        lead_now = xd == lead_next && xd <= last;
+        if (lead_now) {
+            load_stats(xd, 0);
+            lead_next += un.nu;
+        }
     };
     auto after_tiles = [&](int r) {   // publish row r - 1, normalise row r - 7
         if (r >= 1 && r - 1 <= last) publish(r - 1);
