@@ -272,20 +272,19 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         }
     };
 
-    // Normaliser words of row x: lane i < NH reads head wv + 4 i (other
-    // lanes a valid head) and, once they carry the tag, writes them to LDS.
+    // Normaliser words of row x: wave x mod 4 reads them (lane h: head h)
+    // and, once they carry the tag, writes them to LDS.
     const bool hd_lane = lane < NH && wv + 4 * lane < G;
-    const int my_hd = min(wv + 4 * min(lane, NH - 1), G - 1);
     unsigned long long nw[2];
     auto load_norm = [&](int x) {
-        const unsigned long long* p = norm_word(x, my_hd);
+        const unsigned long long* p = norm_word(x, min(lane, G - 1));
         nw[0] = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         nw[1] = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     };
     auto check_norm = [&](int x) {
-        await_tags([&] { return !hd_lane || (tag_ok(nw[0]) && tag_ok(nw[1])); }, [&] { load_norm(x); });
-        if (hd_lane)
-            sm.norm[(x & 1) * 16 + wv + 4 * lane] =
+        await_tags([&] { return lane >= G || (tag_ok(nw[0]) && tag_ok(nw[1])); }, [&] { load_norm(x); });
+        if (lane < G)
+            sm.norm[(x & 1) * 16 + lane] =
                 make_float2(__uint_as_float((uint32_t)nw[0]), __uint_as_float((uint32_t)nw[1]));
     };
 
@@ -406,11 +405,11 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // in issue order).
     auto use_loads = [&](int r) {   // steps of iteration r that use iteration r - 1's loads
         const int xa = r - 6;
-        if (xa >= 0 && xa <= last) check_norm(xa);
+        if (xa >= 0 && xa <= last && (xa & 3) == wv) check_norm(xa);
         if (lead_now) lead(r - 4);
     };
     auto issue_loads = [&](int r) {
-        load_norm(min(max(r - 5, 0), last));
+        if (((r - 5) & 3) == wv) load_norm(min(max(r - 5, 0), last));
         const int xd = r - 3;
         lead_now = xd == lead_next && xd <= last;
         if (lead_now) {
@@ -436,7 +435,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     u32x4 ringA[kTiles][4], ringB[kTiles][4];
 #pragma unroll
     for (int u = 0; u < kTiles; ++u) load_tile(ringA[u], 0, u);
-    load_norm(0);
+    if (((0 - 5) & 3) == wv) load_norm(0);
     load_q(min(1, last));
 #pragma unroll
     for (int u = 0; u < kTiles; ++u) load_tile(ringB[u], min(1, last + 2), u);
