@@ -192,6 +192,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     // that all of them are resident at once.
     const int n_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
     int occ = 0;
+    dm.T = md::attend_unit_tokens(dm.G);
     if (dm.fused) {
         const size_t lds = md::attend_lds_bytes(dm.G);
         if (hipFuncSetAttribute(md::attend_kernel(dm.G), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
@@ -206,7 +207,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
         dm.fused = occ >= 1;
     }
     if (dm.fused) {
-        dm.U_cap = (int)(((int64_t)dm.NP * dm.P + md::kUnitTokens - 1) / md::kUnitTokens + dm.S);
+        dm.U_cap = (int)(((int64_t)dm.NP * dm.P + dm.T - 1) / dm.T + dm.S);
     } else {
         dm.n_wg = dm.U_cap = 0;
     }
@@ -232,7 +233,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
         dm.fused = verified > 0;
         if (!dm.fused) dm.U_cap = 0;
     }
-    dm.spill = !dm.fused || (int64_t)dm.MP * dm.P > (int64_t)dm.n_wg * md::kUnitTokens;
+    dm.spill = !dm.fused || (int64_t)dm.MP * dm.P > (int64_t)dm.n_wg * dm.T;
 
     md_handle_s* h = new (std::nothrow) md_handle_s();
     if (h == nullptr) return MD_E_NOMEM;
@@ -290,7 +291,7 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     hipError_t e = timed_launch(h, MD_K_APPEND, [&] {
         return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, h->stream); });
     // Sessions that fit one pass of the fused kernel run there; the others
-    // (only possible when a session may outgrow n_wg * kUnitTokens tokens) take the
+    // (only possible when a session may outgrow n_wg * T tokens) take the
     // three-kernel path with the logits in HBM.
     if (e == hipSuccess && h->dm.fused) e = timed_launch(h, MD_K_ATTEND, [&] {
         return md::launch_attend(h->dm, h->v, h->sc, q, abar_out, h->stream); });
@@ -400,7 +401,7 @@ md_status md_kernel_config(md_handle h, int32_t* out) {
     if (h == nullptr || out == nullptr) return MD_E_INVALID;
     out[0] = h->dm.fused;
     out[1] = h->dm.spill;
-    out[2] = h->dm.fused ? md::kUnitTokens : 0;
+    out[2] = h->dm.fused ? h->dm.T : 0;
     out[3] = h->dm.n_wg;
     return MD_OK;
 }

@@ -6,7 +6,7 @@
 // the token's softmax weight in that row.  A row's softmax needs the row's
 // maximum and sum over all of the session's tokens, so the logits of a block
 // of tokens cannot be normalised where they are produced.  Here a session's
-// tokens are split into units of kUnitTokens tokens, one workgroup per unit,
+// tokens are split into units of T tokens, one workgroup per unit,
 // all units of a session resident at once.  Each workgroup walks the
 // (layer, KV head) rows in order: it computes the logits of its tokens for
 // the G query heads of the row on MFMA, keeps them in an LDS ring of
@@ -71,27 +71,26 @@ struct AttendArgs {
 };
 
 constexpr int kWaves = kAttendThreads / 64;
-constexpr int kTiles = kUnitTokens / 16 / kWaves;   // 16-token tiles per wave
-static_assert(kTiles == 4, "one row of a wave's tiles fills the four-deep load ring");
-constexpr int kTstride = kUnitTokens + 4;           // LDS row stride (floats) of a head's logits
+// LDS row stride (floats) of a head's values for KT tiles per wave
+__host__ __device__ constexpr int tstride(int KT) { return 16 * kWaves * KT + 4; }
 
 struct Lds {
-    float* rowbuf;    // [kRowBufs][G][kTstride] base-2 logits of the held rows
+    float* rowbuf;    // [kRowBufs][G][tstride] 2^(logit - wave max) of the held rows
     uint32_t* qs;     // [2][3][G][64] hi, mid, lo bf16 query terms (pairs) of two rows
     float2* wstat;    // [2][kWaves][16] per-wave row statistics
     float2* norm;     // [2][16] row normalisers (M, 1 / Lambda)
 };
 
-__host__ __device__ inline size_t rowbuf_bytes(int G) { return (size_t)kRowBufs * G * kTstride * sizeof(float); }
+__host__ __device__ inline size_t rowbuf_bytes(int G, int KT) { return (size_t)kRowBufs * G * tstride(KT) * sizeof(float); }
 __host__ __device__ inline size_t qs_bytes(int G) { return (size_t)2 * 3 * G * 64 * sizeof(uint32_t); }
 constexpr size_t kWstatBytes = (size_t)2 * kWaves * 16 * sizeof(float2);
 constexpr size_t kNormBytes = (size_t)2 * 16 * sizeof(float2);
 
-__device__ __forceinline__ Lds carve(unsigned char* smem, int G) {
+__device__ __forceinline__ Lds carve(unsigned char* smem, int G, int KT) {
     Lds l;
     size_t o = 0;
     l.rowbuf = reinterpret_cast<float*>(smem + o);
-    o += rowbuf_bytes(G);
+    o += rowbuf_bytes(G, KT);
     l.qs = reinterpret_cast<uint32_t*>(smem + o);
     o += qs_bytes(G);
     l.wstat = reinterpret_cast<float2*>(smem + o);
@@ -161,8 +160,9 @@ struct Unit {
 // with Hq = Hkv * G that is r * G.
 __device__ __forceinline__ int qrow0(const AttendDims& dm, int r) { return r * dm.G; }
 
-// One wave's part of a unit.  NH = normaliser heads per wave (G <= 4 NH).
-template <int NH>
+// One wave's part of a unit.  NH = normaliser heads per wave (G <= 4 NH),
+// KT = tiles per wave (unit of 64 KT tokens).
+template <int NH, int KT>
 __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendArgs& a, const Lds& sm,
                                             const Unit& un, int wv, int lane, uint32_t tag) {
     constexpr int KQ = (NH + 1) / 2;   // float4 of the query row per lane (G * 32 <= 256 KQ)
@@ -171,14 +171,17 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     const int g = lane >> 4;          // k-group of A/B, row quad of C
     const int hh = min(h, G - 1);     // in-bounds head for the unused columns
     const uint32_t voff = 256u * h + 16u * g;
-    const int wtok0 = wv * 16 * kTiles;   // unit-local token of this wave's first tile
+    constexpr int kT = 16 * kWaves * KT;   // tokens per unit
+    constexpr int kTs = tstride(KT);
+    constexpr int kTok = KT / 4;          // tokens per lane
+    const int wtok0 = wv * 16 * KT;       // unit-local token of this wave's first tile
     bool dead = false;                    // a wait of this wave ran out: stop waiting
 
-    // lane i < kTiles: slot (physical page * P + offset) of tile i's first token
+    // lane i < KT: slot (physical page * P + offset) of tile i's first token
     int myslot = 0;
     bool myok = false;
-    if (lane < kTiles) {
-        const int tok = un.j * kUnitTokens + wtok0 + 16 * lane;
+    if (lane < KT) {
+        const int tok = un.j * kT + wtok0 + 16 * lane;
         if (tok < un.nt_s) {
             const int p = a.page_table[(size_t)un.s * dm.MP + (tok >> dm.Pshift)];
             if ((unsigned)p < (unsigned)dm.NP) {
@@ -190,7 +193,8 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         }
     }
     const unsigned long long vmask = __ballot(myok);
-    const bool wave_full = (vmask & 0xFull) == 0xFull && wtok0 + 16 * kTiles <= un.ntok;
+    constexpr unsigned long long kAll = (1ull << KT) - 1;
+    const bool wave_full = (vmask & kAll) == kAll && wtok0 + 16 * KT <= un.ntok;
 
     // K tile u of row r in the MFMA A layout; a tile without cached tokens,
     // or past the last row, reads the pool's first tile (its logits are
@@ -368,16 +372,19 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // the row for head h, so a weight is the held value times
     // f_h = 2^(m_w - M_h) / Lambda_h: lane h works f_h out once, and every
     // lane reads it from lane h.
-    float acc = 0.0f;   // attention mass of token wtok0 + lane, summed over rows
+    float acc[kTok];   // attention mass of tokens wtok0 + lane + 64 k, summed over rows
+#pragma unroll
+    for (int k = 0; k < kTok; ++k) acc[k] = 0.0f;
     auto consume = [&](int x, float mw) {
-        const float* rb = sm.rowbuf + (size_t)(x % kRowBufs) * G * kTstride + wtok0 + lane;
+        const float* rb = sm.rowbuf + (size_t)(x % kRowBufs) * G * kTs + wtok0 + lane;
         const float2 n = sm.norm[(x & 1) * 16 + hh];
         const float f = h < G ? hw_exp2(mw - n.x) * n.y : 0.0f;
-        float sum = 0.0f;
 #pragma unroll
-        for (int hd = 0; hd < 4 * NH; ++hd)   // heads past the group read a valid row and weigh zero
-            sum = fmaf(rb[min(hd, G - 1) * kTstride], __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), hd)), sum);
-        acc += sum;
+        for (int hd = 0; hd < 4 * NH; ++hd) {   // heads past the group read a valid row and weigh zero
+            const float fh = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), hd));
+#pragma unroll
+            for (int k = 0; k < kTok; ++k) acc[k] = fmaf(rb[min(hd, G - 1) * kTs + 64 * k], fh, acc[k]);
+        }
     };
     // The wave's row maxima of the last kConsumeLag rows (lane h: head h),
     // newest first.
@@ -432,13 +439,13 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // Two rings of four tiles: row r's tiles sit in ring r & 1, and the
     // loads of row r + 2 go out as soon as row r's tiles have been through
     // MFMA, so two rows of loads are in flight while a wave works on a row.
-    u32x4 ringA[kTiles][4], ringB[kTiles][4];
+    u32x4 ringA[KT][4], ringB[KT][4];
 #pragma unroll
-    for (int u = 0; u < kTiles; ++u) load_tile(ringA[u], 0, u);
+    for (int u = 0; u < KT; ++u) load_tile(ringA[u], 0, u);
     if (((0 - 5) & 3) == wv) load_norm(0);
     load_q(min(1, last));
 #pragma unroll
-    for (int u = 0; u < kTiles; ++u) load_tile(ringB[u], min(1, last + 2), u);
+    for (int u = 0; u < KT; ++u) load_tile(ringB[u], min(1, last + 2), u);
 
     // Row r:
     //   1. logits of the four tiles on MFMA, k-chunk by k-chunk (the chunk's
@@ -451,18 +458,18 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     //   4. softmax statistics of row r, its logits into LDS;
     //   5. publish row r - 1, normalise row r - 7; row r's statistics into
     //      LDS; barrier.
-    auto do_row = [&](u32x4 (&ring)[kTiles][4], int row) {
+    auto do_row = [&](u32x4 (&ring)[KT][4], int row) {
         const uint32_t* qb = sm.qs + (size_t)(row & 1) * 3 * G * 64 + hh * 64 + 4 * g;
-        f32x4 c[kTiles];
+        f32x4 c[KT];
 #pragma unroll
-        for (int u = 0; u < kTiles; ++u) c[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int u = 0; u < KT; ++u) c[u] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             u32x4 bq[3];
 #pragma unroll
             for (int p = 0; p < 3; ++p) bq[p] = *reinterpret_cast<const u32x4*>(qb + p * G * 64 + 16 * j);
 #pragma unroll
-            for (int u = 0; u < kTiles; ++u)
+            for (int u = 0; u < KT; ++u)
 #pragma unroll
                 for (int p = 0; p < 3; ++p)
                     c[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
@@ -473,34 +480,34 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         issue_loads(row);
         load_q(min(row + 2, last));
 #pragma unroll
-        for (int u = 0; u < kTiles; ++u) load_tile(ring[u], row + 2, u);
+        for (int u = 0; u < KT; ++u) load_tile(ring[u], row + 2, u);
 
         // Base-2 logits of the wave's 64 tokens (lane: head h, tokens
         // 16 u + 4 g + i), their maximum and the sum of 2^(logit - max) per
         // head; the LDS row keeps 2^(logit - max).
-        float xs[kTiles][4];
+        float xs[KT][4];
 #pragma unroll
-        for (int u = 0; u < kTiles; ++u)
+        for (int u = 0; u < KT; ++u)
 #pragma unroll
             for (int i = 0; i < 4; ++i) xs[u][i] = c[u][i] * kLogitScale;
         if (!wave_full) {   // tokens past the unit's end, tiles without a page
 #pragma unroll
-            for (int u = 0; u < kTiles; ++u)
+            for (int u = 0; u < KT; ++u)
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
                     if (!((vmask >> u) & 1ull) || wtok0 + 16 * u + 4 * g + i >= un.ntok) xs[u][i] = -INFINITY;
         }
         float mx = -INFINITY;
 #pragma unroll
-        for (int u = 0; u < kTiles; ++u)
+        for (int u = 0; u < KT; ++u)
             mx = fmaxf(mx, fmaxf(fmaxf(xs[u][0], xs[u][1]), fmaxf(xs[u][2], xs[u][3])));
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
         const float ms = mx == -INFINITY ? 0.0f : mx;
         float ls = 0.0f;
-        float* rbw = sm.rowbuf + ((size_t)(row % kRowBufs) * G + h) * kTstride + wtok0 + 4 * g;
+        float* rbw = sm.rowbuf + ((size_t)(row % kRowBufs) * G + h) * kTs + wtok0 + 4 * g;
 #pragma unroll
-        for (int u = 0; u < kTiles; ++u) {
+        for (int u = 0; u < KT; ++u) {
             f32x4 pv;
 #pragma unroll
             for (int i = 0; i < 4; ++i) pv[i] = hw_exp2(xs[u][i] - ms);
@@ -531,14 +538,18 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     }
 
     // ---- Eq. 2 and Eq. 3 for this wave's tokens
-    const int tile = lane >> 4;
-    const int slot0 = __shfl(myslot, tile);
-    if (wtok0 + lane < un.ntok && ((vmask >> tile) & 1ull)) {
-        const float abar = acc / (float)dm.R;
-        const size_t si = (size_t)slot0 + (lane & 15);
-        a.imp[si] = fmaf(dm.rho, a.imp[si], (1.0f - dm.rho) * abar);
-        if (abar >= dm.tau_scale / (float)un.nt_s) a.t_ref[si] = a.clock[un.s];
-        if (a.abar_out != nullptr) a.abar_out[si] = abar;
+#pragma unroll
+    for (int k = 0; k < kTok; ++k) {
+        const int lt = lane + 64 * k;   // wave-local token
+        const int tile = lt >> 4;
+        const int slot0 = __shfl(myslot, tile);
+        if (wtok0 + lt < un.ntok && ((vmask >> tile) & 1ull)) {
+            const float abar = acc[k] / (float)dm.R;
+            const size_t si = (size_t)slot0 + (lt & 15);
+            a.imp[si] = fmaf(dm.rho, a.imp[si], (1.0f - dm.rho) * abar);
+            if (abar >= dm.tau_scale / (float)un.nt_s) a.t_ref[si] = a.clock[un.s];
+            if (a.abar_out != nullptr) a.abar_out[si] = abar;
+        }
     }
 }
 
@@ -547,7 +558,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
 // Two workgroups per CU (two waves per SIMD) for groups of up to eight query
 // heads; larger groups need a CU's LDS for one workgroup, which then may use
 // the whole register file.
-template <int NH>
+template <int NH, int KT>
 __global__ void __launch_bounds__(kAttendThreads) __attribute__((amdgpu_waves_per_eu(NH == 4 ? 1 : 2)))
 k_attend(AttendDims dm, AttendArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -568,7 +579,7 @@ k_attend(AttendDims dm, AttendArgs a) {
         }
         return;
     }
-    const Lds sm = carve(smem, dm.G);
+    const Lds sm = carve(smem, dm.G, KT);
     const int wv = uni(threadIdx.x >> 6);
     const uint32_t tag = (uint32_t)a.epoch[0];
     const int n_pass = a.plan[0];
@@ -589,25 +600,29 @@ k_attend(AttendDims dm, AttendArgs a) {
         un.nu = a.ustart[lo + 1] - un.us;
         un.j = u0 + w - un.us;
         un.nt_s = a.n_tokens[lo];
-        un.ntok = min(kUnitTokens, un.nt_s - un.j * kUnitTokens);
+        constexpr int kT = 16 * kWaves * KT;
+        un.ntok = min(kT, un.nt_s - un.j * kT);
         un.deadline = now_ticks() + kUnitTicks;
         lds_sync();   // the previous unit is done with the LDS
         // The lane index is made opaque here so that per-lane address
         // arithmetic is not hoisted out of the pass loop and kept live.
         int lane = (int)threadIdx.x & 63;
         asm volatile("" : "+v"(lane));
-        attend_wave<NH>(dm, a, sm, un, wv, lane, tag);
+        attend_wave<NH, KT>(dm, a, sm, un, wv, lane, tag);
     }
 }
 
 }  // namespace
 
-size_t attend_lds_bytes(int G) { return rowbuf_bytes(G) + qs_bytes(G) + kWstatBytes + kNormBytes; }
+size_t attend_lds_bytes(int G) {
+    return rowbuf_bytes(G, attend_unit_tokens(G) / (16 * kWaves)) + qs_bytes(G) + kWstatBytes + kNormBytes;
+}
 
 const void* attend_kernel(int G) {
-    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<1>);
-    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<2>);
-    return reinterpret_cast<const void*>(&k_attend<4>);
+    static_assert(16 * kWaves * 4 == 256, "unit size of attend_unit_tokens");
+    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<1, 4>);
+    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<2, 4>);
+    return reinterpret_cast<const void*>(&k_attend<4, 4>);
 }
 
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q, float* abar_out,

@@ -18,12 +18,13 @@ constexpr int kMaxPages = 8192;     // page-table capacity per session
 constexpr int kSelThreads = 1024;   // select / compact block size
 constexpr int kPerThread = kMaxPages / kSelThreads;
 // Fused observation kernel (k_attend): four waves per workgroup, all doing
-// the same job; a unit of work is one session's block of kUnitTokens tokens
-// (16 tokens per lane row of a wave's four MFMA tiles) over every
-// (layer, KV head) row.
+// the same job; a unit of work is one session's block of T tokens (a wave's
+// KT tiles of 16 tokens, four waves) over every (layer, KV head) row.  Units
+// are 256 tokens (KT = 4): two workgroups per CU keep two waves on each SIMD
+// (units of 512 tokens, one wave per SIMD, measured slower).
 constexpr int kAttendThreads = 256;
-constexpr int kUnitTokens = 256;
-constexpr int kAttendPerCu = 2;   // workgroups per CU: eight waves stream enough loads to saturate HBM
+constexpr int kAttendPerCu = 2;   // at most two workgroups per CU
+inline int attend_unit_tokens(int) { return 256; }
 constexpr int kConsumeLag = 7;   // rows a unit runs ahead of the row it normalises
 constexpr int kRowBufs = kConsumeLag + 1;       // rows of logits held in LDS
 
@@ -34,6 +35,7 @@ struct Dims {
     int fused;     // 1: sessions that fit one pass run on k_attend
     int spill;     // 1: some session may not fit a pass (the spill kernels run)
     int n_wg;      // k_attend workgroups (all co-resident)
+    int T;         // tokens per fused unit (attend_unit_tokens(G))
     int U_cap;     // capacity of the per-step fused unit list
     uint32_t pin_mask;
     float rho, alpha, tau_scale;

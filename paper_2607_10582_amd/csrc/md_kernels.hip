@@ -121,7 +121,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         while (s0 < dm.S) {
             int used = 0, e = s0;
             while (e < dm.S) {
-                const int u = (s_n[e] + kUnitTokens - 1) / kUnitTokens;
+                const int u = (s_n[e] + dm.T - 1) / dm.T;
                 if (used + u > dm.n_wg) break;
                 used += u;
                 s_pass[e] = np;
@@ -131,7 +131,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                 ++s0;
                 continue;
             }
-            sc.plan[1 + 3 * np] = kUnitTokens;
+            sc.plan[1 + 3 * np] = dm.T;
             sc.plan[2 + 3 * np] = s0;
             sc.plan[3 + 3 * np] = e;
             ++np;
@@ -155,7 +155,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             const bool spill = ps < 0;
             const int ch = spill ? (nt + kChunk - 1) / kChunk : 0;
             sc.chunks[s2] = ch;
-            uu[k] = spill ? 0 : (nt + kUnitTokens - 1) / kUnitTokens;
+            uu[k] = spill ? 0 : (nt + dm.T - 1) / dm.T;
             it[k] = ch * dm.LHkv;
             ti[k] = spill ? (nt + kTile - 1) / kTile : 0;
             si[k] = (nt + kTile - 1) / kTile;
