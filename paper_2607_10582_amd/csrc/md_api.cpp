@@ -198,7 +198,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
         if (hipFuncSetAttribute(md::attend_kernel(dm.G), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
             hipSuccess) {
             (void)hipGetLastError();
-        } else if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(dm.G), md::kAttendThreads,
+        } else if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(dm.G), md::attend_threads(dm.G),
                                                                 lds) != hipSuccess) {
             return MD_E_HIP;
         }

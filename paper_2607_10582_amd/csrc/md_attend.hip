@@ -70,31 +70,32 @@ struct AttendArgs {
     int32_t* probe;    // check mode only: [arrivals, least seen]
 };
 
-constexpr int kWaves = kAttendThreads / 64;
-// LDS row stride (floats) of a head's values for KT tiles per wave
-__host__ __device__ constexpr int tstride(int KT) { return 16 * kWaves * KT + 4; }
+// LDS row stride (floats) of a head's values: W waves of KT tiles
+__host__ __device__ constexpr int tstride(int W, int KT) { return 16 * W * KT + 4; }
 
 struct Lds {
     float* rowbuf;    // [kRowBufs][G][tstride] 2^(logit - wave max) of the held rows
     uint32_t* qs;     // [2][3][G][64] hi, mid, lo bf16 query terms (pairs) of two rows
-    float2* wstat;    // [2][kWaves][16] per-wave row statistics
+    float2* wstat;    // [2][W][16] per-wave row statistics
     float2* norm;     // [2][16] row normalisers (M, 1 / Lambda)
 };
 
-__host__ __device__ inline size_t rowbuf_bytes(int G, int KT) { return (size_t)kRowBufs * G * tstride(KT) * sizeof(float); }
+__host__ __device__ inline size_t rowbuf_bytes(int G, int W, int KT) {
+    return (size_t)kRowBufs * G * tstride(W, KT) * sizeof(float);
+}
 __host__ __device__ inline size_t qs_bytes(int G) { return (size_t)2 * 3 * G * 64 * sizeof(uint32_t); }
-constexpr size_t kWstatBytes = (size_t)2 * kWaves * 16 * sizeof(float2);
+__host__ __device__ inline size_t wstat_bytes(int W) { return (size_t)2 * W * 16 * sizeof(float2); }
 constexpr size_t kNormBytes = (size_t)2 * 16 * sizeof(float2);
 
-__device__ __forceinline__ Lds carve(unsigned char* smem, int G, int KT) {
+__device__ __forceinline__ Lds carve(unsigned char* smem, int G, int W, int KT) {
     Lds l;
     size_t o = 0;
     l.rowbuf = reinterpret_cast<float*>(smem + o);
-    o += rowbuf_bytes(G, KT);
+    o += rowbuf_bytes(G, W, KT);
     l.qs = reinterpret_cast<uint32_t*>(smem + o);
     o += qs_bytes(G);
     l.wstat = reinterpret_cast<float2*>(smem + o);
-    o += kWstatBytes;
+    o += wstat_bytes(W);
     l.norm = reinterpret_cast<float2*>(smem + o);
     return l;
 }
@@ -160,19 +161,19 @@ struct Unit {
 // with Hq = Hkv * G that is r * G.
 __device__ __forceinline__ int qrow0(const AttendDims& dm, int r) { return r * dm.G; }
 
-// One wave's part of a unit.  NH = normaliser heads per wave (G <= 4 NH),
-// KT = tiles per wave (unit of 64 KT tokens).
-template <int NH, int KT>
+// One wave's part of a unit.  W = waves per workgroup, NH = normaliser
+// heads per wave (G <= W NH), KT = tiles per wave (units of 16 W KT tokens).
+template <int W, int NH, int KT>
 __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendArgs& a, const Lds& sm,
                                             const Unit& un, int wv, int lane, uint32_t tag) {
-    constexpr int KQ = (NH + 1) / 2;   // float4 of the query row per lane (G * 32 <= 256 KQ)
+    constexpr int KQ = (W * NH * 32 + 64 * W - 1) / (64 * W);   // float4 of the query row per lane
     const int G = dm.G;
     const int h = lane & 15;          // MFMA column: query head of the group
     const int g = lane >> 4;          // k-group of A/B, row quad of C
     const int hh = min(h, G - 1);     // in-bounds head for the unused columns
     const uint32_t voff = 256u * h + 16u * g;
-    constexpr int kT = 16 * kWaves * KT;   // tokens per unit
-    constexpr int kTs = tstride(KT);
+    constexpr int kT = 16 * W * KT;   // tokens per unit
+    constexpr int kTs = tstride(W, KT);
     constexpr int kTok = KT / 4;          // tokens per lane
     const int wtok0 = wv * 16 * KT;       // unit-local token of this wave's first tile
     bool dead = false;                    // a wait of this wave ran out: stop waiting
@@ -209,7 +210,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
             rg[j] = __builtin_nontemporal_load(reinterpret_cast<gvec>(base + voff + 64 * j));
     };
 
-    // ---- query staging: this wave's float4 f = lane + 64 (wv + 4 k) of a row
+    // ---- query staging: this wave's float4 f = lane + 64 (wv + W k) of a row
     f32x4 qv[KQ];
     auto q_row = [&](int r) {
         return reinterpret_cast<const f32x4*>(a.q + ((size_t)un.s * dm.L * dm.Hq + qrow0(dm, r)) * kHeadDim);
@@ -217,14 +218,14 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     auto load_q = [&](int r) {   // unconditional loads, indices clamped into the row
         const f32x4* qr = q_row(r);
 #pragma unroll
-        for (int k = 0; k < KQ; ++k) qv[k] = qr[min(lane + 64 * (wv + 4 * k), G * 32 - 1)];
+        for (int k = 0; k < KQ; ++k) qv[k] = qr[min(lane + 64 * (wv + W * k), G * 32 - 1)];
     };
     auto store_q = [&](int r) {
         uint32_t* qb = sm.qs + (size_t)(r & 1) * 3 * G * 64;
         bool bad = false;
 #pragma unroll
         for (int k = 0; k < KQ; ++k) {
-            const int f = lane + 64 * (wv + 4 * k);
+            const int f = lane + 64 * (wv + W * k);
             if (f < G * 32) {
                 const int hd = f >> 5, d2 = 2 * (f & 31);
                 uint32_t t[3][4];
@@ -244,7 +245,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // ---- cross-unit words.  Every unit publishes its (max, sum) of each
     // (row, query head); the leader of row x (unit x mod nu of the session)
     // gathers them into the row's normaliser words (M, 1 / Lambda), which
-    // every unit reads.  Wave wv looks after heads wv + 4 i (i < NH).
+    // every unit reads.  Wave wv looks after heads wv + W i (i < NH).
     const int last = dm.LHkv - 1;
     const unsigned long long tag_hi = (unsigned long long)tag << 32;
     auto tag_ok = [&](unsigned long long v) { return (uint32_t)(v >> 32) == tag; };
@@ -278,7 +279,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
 
     // Normaliser words of row x: wave x mod 4 reads them (lane h: head h)
     // and, once they carry the tag, writes them to LDS.
-    const bool hd_lane = lane < NH && wv + 4 * lane < G;
+    const bool hd_lane = lane < NH && wv + W * lane < G;
     unsigned long long nw[2];
     auto load_norm = [&](int x) {
         const unsigned long long* p = norm_word(x, min(lane, G - 1));
@@ -292,14 +293,14 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
                 make_float2(__uint_as_float((uint32_t)nw[0]), __uint_as_float((uint32_t)nw[1]));
     };
 
-    // Leader: the units' words of heads wv + 4 i, lane k = unit k (the first
+    // Leader: the units' words of heads wv + W i, lane k = unit k (the first
     // 64 units are requested a row ahead; further units are read here).
     unsigned long long w[NH][2];
     auto load_stats = [&](int x, int c0) {
         const int k = c0 + lane < un.nu ? c0 + lane : 0;
 #pragma unroll
         for (int i = 0; i < NH; ++i) {
-            const unsigned long long* p = stat_word(x, k, min(wv + 4 * i, G - 1));
+            const unsigned long long* p = stat_word(x, k, min(wv + W * i, G - 1));
             w[i][0] = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             w[i][1] = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
@@ -345,7 +346,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
             // a row with no live token gives zero weights, never NaN
             M = M == -INFINITY ? 0.0f : M;
             const float inv = Ls > 0.0f ? 1.0f / Ls : 0.0f;
-            unsigned long long* p = norm_word(x, wv + 4 * lane);
+            unsigned long long* p = norm_word(x, wv + W * lane);
             __hip_atomic_store(p, tag_hi | __float_as_uint(M), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(p + 1, tag_hi | __float_as_uint(inv), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
@@ -354,11 +355,11 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // The unit's (max, sum) of row r, merged over the four waves; wave r mod 4
     // publishes all heads (lane h = head h).
     auto publish = [&](int r) {
-        if (wv == (r & 3) && lane < G) {
+        if (wv == (r & (W - 1)) && lane < G) {
             float um = -INFINITY, ul = 0.0f;
 #pragma unroll
-            for (int pw = 0; pw < kWaves; ++pw) {
-                const float2 st = sm.wstat[((r & 1) * kWaves + pw) * 16 + lane];
+            for (int pw = 0; pw < W; ++pw) {
+                const float2 st = sm.wstat[((r & 1) * W + pw) * 16 + lane];
                 merge_stat(um, ul, st.x, st.y);
             }
             unsigned long long* p = stat_word(r, un.j, lane);
@@ -380,7 +381,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         const float2 n = sm.norm[(x & 1) * 16 + hh];
         const float f = h < G ? hw_exp2(mw - n.x) * n.y : 0.0f;
 #pragma unroll
-        for (int hd = 0; hd < 4 * NH; ++hd) {   // heads past the group read a valid row and weigh zero
+        for (int hd = 0; hd < W * NH; ++hd) {   // heads past the group read a valid row and weigh zero
             const float fh = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), hd));
 #pragma unroll
             for (int k = 0; k < kTok; ++k) acc[k] = fmaf(rb[min(hd, G - 1) * kTs + 64 * k], fh, acc[k]);
@@ -412,11 +413,11 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // in issue order).
     auto use_loads = [&](int r) {   // steps of iteration r that use iteration r - 1's loads
         const int xa = r - 6;
-        if (xa >= 0 && xa <= last && (xa & 3) == wv) check_norm(xa);
+        if (xa >= 0 && xa <= last && (xa & (W - 1)) == wv) check_norm(xa);
         if (lead_now) lead(r - 4);
     };
     auto issue_loads = [&](int r) {
-        if (((r - 5) & 3) == wv) load_norm(min(max(r - 5, 0), last));
+        if (((r - 5) & (W - 1)) == wv) load_norm(min(max(r - 5, 0), last));
         const int xd = r - 3;
         lead_now = xd == lead_next && xd <= last;
         if (lead_now) {
@@ -442,7 +443,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     u32x4 ringA[KT][4], ringB[KT][4];
 #pragma unroll
     for (int u = 0; u < KT; ++u) load_tile(ringA[u], 0, u);
-    if (((0 - 5) & 3) == wv) load_norm(0);
+    if (((0 - 5) & (W - 1)) == wv) load_norm(0);
     load_q(min(1, last));
 #pragma unroll
     for (int u = 0; u < KT; ++u) load_tile(ringB[u], min(1, last + 2), u);
@@ -518,7 +519,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         ls += __shfl_xor(ls, 32);
         after_tiles(row);
         push_max(ms);
-        if (g == 0 && h < G) sm.wstat[((row & 1) * kWaves + wv) * 16 + h] = make_float2(mx, ls);
+        if (g == 0 && h < G) sm.wstat[((row & 1) * W + wv) * 16 + h] = make_float2(mx, ls);
         lds_sync();
     };
     int row = 0;
@@ -557,9 +558,11 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
 
 // Two workgroups per CU (two waves per SIMD) for groups of up to eight query
 // heads; larger groups need a CU's LDS for one workgroup, which then may use
-// the whole register file.
-template <int NH, int KT>
-__global__ void __launch_bounds__(kAttendThreads) __attribute__((amdgpu_waves_per_eu(NH == 4 ? 1 : 2)))
+// the whole register file.  (Workgroups that take a whole CU, with eight
+// waves or with eight tiles per wave, measured slower: the two workgroups'
+// row barriers fall at different times and fill each other's gaps.)
+template <int W, int NH, int KT>
+__global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(NH == 4 ? 1 : 2)))
 k_attend(AttendDims dm, AttendArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     if (a.probe != nullptr) {
@@ -579,7 +582,7 @@ k_attend(AttendDims dm, AttendArgs a) {
         }
         return;
     }
-    const Lds sm = carve(smem, dm.G, KT);
+    const Lds sm = carve(smem, dm.G, W, KT);
     const int wv = uni(threadIdx.x >> 6);
     const uint32_t tag = (uint32_t)a.epoch[0];
     const int n_pass = a.plan[0];
@@ -600,7 +603,7 @@ k_attend(AttendDims dm, AttendArgs a) {
         un.nu = a.ustart[lo + 1] - un.us;
         un.j = u0 + w - un.us;
         un.nt_s = a.n_tokens[lo];
-        constexpr int kT = 16 * kWaves * KT;
+        constexpr int kT = 16 * W * KT;
         un.ntok = min(kT, un.nt_s - un.j * kT);
         un.deadline = now_ticks() + kUnitTicks;
         lds_sync();   // the previous unit is done with the LDS
@@ -608,21 +611,21 @@ k_attend(AttendDims dm, AttendArgs a) {
         // arithmetic is not hoisted out of the pass loop and kept live.
         int lane = (int)threadIdx.x & 63;
         asm volatile("" : "+v"(lane));
-        attend_wave<NH, KT>(dm, a, sm, un, wv, lane, tag);
+        attend_wave<W, NH, KT>(dm, a, sm, un, wv, lane, tag);
     }
 }
 
 }  // namespace
 
 size_t attend_lds_bytes(int G) {
-    return rowbuf_bytes(G, attend_unit_tokens(G) / (16 * kWaves)) + qs_bytes(G) + kWstatBytes + kNormBytes;
+    const int W = attend_threads(G) / 64;
+    return rowbuf_bytes(G, W, attend_unit_tokens(G) / (16 * W)) + qs_bytes(G) + wstat_bytes(W) + kNormBytes;
 }
 
 const void* attend_kernel(int G) {
-    static_assert(16 * kWaves * 4 == 256, "unit size of attend_unit_tokens");
-    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<1, 4>);
-    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<2, 4>);
-    return reinterpret_cast<const void*>(&k_attend<4, 4>);
+    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<4, 1, 4>);
+    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<4, 2, 4>);
+    return reinterpret_cast<const void*>(&k_attend<4, 4, 4>);
 }
 
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q, float* abar_out,
@@ -631,7 +634,7 @@ hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const
     AttendArgs aa{v.k_pool, v.page_table, v.n_tokens, v.clock, v.imp, v.t_ref, q, abar_out,
                   sc.ustart, sc.plan, sc.epoch, sc.ustat, sc.unorm, sc.status, nullptr};
     void* args[] = {&ad, &aa};
-    return hipLaunchCooperativeKernel(attend_kernel(dm.G), dim3(dm.n_wg), dim3(kAttendThreads), args,
+    return hipLaunchCooperativeKernel(attend_kernel(dm.G), dim3(dm.n_wg), dim3(attend_threads(dm.G)), args,
                                       (unsigned)attend_lds_bytes(dm.G), st);
 }
 
@@ -643,7 +646,7 @@ hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, hipStre
     if (e == hipSuccess) e = hipMemsetD32Async(reinterpret_cast<hipDeviceptr_t>(probe + 1), 1 << 30, 1, st);
     if (e != hipSuccess) return e;
     void* args[] = {&ad, &aa};
-    return hipLaunchCooperativeKernel(attend_kernel(dm.G), dim3(n_wg), dim3(kAttendThreads), args,
+    return hipLaunchCooperativeKernel(attend_kernel(dm.G), dim3(n_wg), dim3(attend_threads(dm.G)), args,
                                       (unsigned)attend_lds_bytes(dm.G), st);
 }
 

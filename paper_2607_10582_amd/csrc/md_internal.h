@@ -18,12 +18,10 @@ constexpr int kMaxPages = 8192;     // page-table capacity per session
 constexpr int kSelThreads = 1024;   // select / compact block size
 constexpr int kPerThread = kMaxPages / kSelThreads;
 // Fused observation kernel (k_attend): four waves per workgroup, all doing
-// the same job; a unit of work is one session's block of T tokens (a wave's
-// KT tiles of 16 tokens, four waves) over every (layer, KV head) row.  Units
-// are 256 tokens (KT = 4): two workgroups per CU keep two waves on each SIMD
-// (units of 512 tokens, one wave per SIMD, measured slower).
-constexpr int kAttendThreads = 256;
+// the same job; a unit of work is one session's block of 256 tokens (each
+// wave's four tiles of 16 tokens) over every (layer, KV head) row.
 constexpr int kAttendPerCu = 2;   // at most two workgroups per CU
+inline int attend_threads(int) { return 256; }
 inline int attend_unit_tokens(int) { return 256; }
 constexpr int kConsumeLag = 7;   // rows a unit runs ahead of the row it normalises
 constexpr int kRowBufs = kConsumeLag + 1;       // rows of logits held in LDS
