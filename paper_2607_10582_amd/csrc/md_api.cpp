@@ -209,7 +209,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     if (dm.fused) {
         dm.U_cap = (int)(((int64_t)dm.NP * dm.P + dm.T - 1) / dm.T + dm.S);
     } else {
-        dm.n_wg = dm.U_cap = 0;
+        dm.n_wg = dm.U_cap = dm.wg_per_cu = dm.lane_cap = 0;
     }
     // The fused kernel's workgroups wait for each other, so all of them must
     // be resident together: check it on the device, and step the grid down
@@ -230,6 +230,8 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
         }
         (void)hipFree(probe);
         dm.n_wg = verified;
+        dm.wg_per_cu = verified / n_cu;
+        dm.lane_cap = n_cu;
         dm.fused = verified > 0;
         if (!dm.fused) dm.U_cap = 0;
     }

@@ -49,6 +49,7 @@ namespace {
 
 struct AttendDims {
     int L, Hq, Hkv, G, P, Pshift, MP, NP, R, LHkv;
+    int wg_per_cu, n_cu, S;
     float rho, tau_scale;
 };
 
@@ -64,6 +65,8 @@ struct AttendArgs {
     const int32_t* ustart;
     const int32_t* plan;
     const int32_t* epoch;
+    unsigned long long* claim;
+    unsigned long long* lane_box;
     unsigned long long* ustat;
     unsigned long long* unorm;
     int32_t* status;
@@ -315,9 +318,8 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
             run_m[i] = -INFINITY;
             run_l[i] = 0.0f;
         }
-        for (int c0 = 0; c0 < un.nu; c0 += 64) {
+        auto fold = [&](int c0) {
             const bool act = c0 + lane < un.nu;
-            if (c0 > 0) load_stats(x, c0);
             await_tags(
                 [&] {
                     bool ok = true;
@@ -334,6 +336,14 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
                 const float S = wave_sum_dpp(m == -INFINITY ? 0.0f : l * hw_exp2(m - M));
                 merge_stat(run_m[i], run_l[i], M, S);
             }
+        };
+        // The first 64 units' words were requested an iteration earlier and
+        // are folded outside the loop: inside it, the wait for them would
+        // also wait for every tile load issued since.
+        fold(0);
+        for (int c0 = 64; c0 < un.nu; c0 += 64) {
+            load_stats(x, c0);
+            fold(c0);
         }
         if (hd_lane) {
             float M = run_m[0], Ls = run_l[0];
@@ -554,6 +564,81 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     }
 }
 
+// ------------------------------------------------------------ passes
+
+// Number of threads of the workgroup with p set (tmp: 17 ints of LDS).
+// Contains barriers.
+__device__ int count_true(bool p, int* tmp) {
+    const int k = __popcll(__ballot(p));
+    if (threadIdx.x == 0) tmp[16] = 0;
+    __syncthreads();
+    if (lane_id() == 0 && k > 0) atomicAdd(&tmp[16], k);
+    __syncthreads();
+    const int total = tmp[16];
+    __syncthreads();
+    return total;
+}
+
+// Number of i < n with v[i] <= x, for non-decreasing v, counted by the whole
+// workgroup in chunks of blockDim.x (tmp: 17 ints of LDS).  Wave-uniform
+// result; contains barriers.
+__device__ int count_at_most(const int32_t* v, int n, int x, int* tmp) {
+    int total = 0;
+    for (int c = 0; c < n; c += blockDim.x) {
+        const int i = c + (int)threadIdx.x;
+        total += count_true(i < n && v[i] <= x, tmp);
+    }
+    return uni(total);
+}
+
+// Lane mode: the lane's first workgroup claims the next sessions of the
+// step for one pass of its lane: consecutive sessions whose units add up to
+// at most cap, from the front of the unclaimed range (lane 0) or from its
+// back (lane 1), by compare-and-swap on the (first, end) word.  Writes the
+// claimed [first, end) to xs[0], xs[1] (both 0 when nothing is left).
+// Whole workgroup; contains barriers.
+__device__ void claim_sessions(const AttendArgs& a, int* xs, int lane_no, int cap) {
+    const bool front = (lane_no & 1) == 0;
+    int* tmp = xs + 2;
+    while (true) {
+        if (threadIdx.x == 0) {
+            const unsigned long long c = __hip_atomic_load(a.claim, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            xs[4 + 17] = (int)(c >> 32);
+            xs[5 + 17] = (int)(c & 0xffffffffu);
+        }
+        __syncthreads();
+        const int f = xs[4 + 17], e = xs[5 + 17];
+        if (f >= e) {
+            if (threadIdx.x == 0) xs[0] = xs[1] = 0;
+            __syncthreads();
+            return;
+        }
+        // units of the t-th session from the claiming end (one window of
+        // blockDim.x sessions; a pass never holds more sessions than that
+        // unless some have no units, and then the next pass takes the rest)
+        const int t = (int)threadIdx.x;
+        const int s = front ? f + t : e - 1 - t;
+        const int u = (t < e - f) ? a.ustart[s + 1] - a.ustart[s] : (cap + 1);
+        int tot;
+        const int before = block_exclusive_scan(u, tmp, &tot);
+        const bool take = t < e - f && before + u <= cap;
+        const int k = count_true(take, tmp);   // sessions taken (a prefix)
+        if (threadIdx.x == 0) {
+            const int nf = front ? f + k : f, ne = front ? e : e - k;
+            const unsigned long long want = ((unsigned long long)(uint32_t)nf << 32) | (uint32_t)ne;
+            const unsigned long long seen = ((unsigned long long)(uint32_t)f << 32) | (uint32_t)e;
+            const unsigned long long got = atomicCAS(a.claim, seen, want);
+            xs[4 + 17] = got == seen;
+            xs[0] = front ? f : e - k;
+            xs[1] = front ? f + k : e;
+        }
+        __syncthreads();
+        const bool done = xs[4 + 17] != 0;
+        __syncthreads();
+        if (done) return;
+    }
+}
+
 // ------------------------------------------------------------ kernel
 
 // Two workgroups per CU (two waves per SIMD) for groups of up to eight query
@@ -585,28 +670,70 @@ k_attend(AttendDims dm, AttendArgs a) {
     const Lds sm = carve(smem, dm.G, W, KT);
     const int wv = uni(threadIdx.x >> 6);
     const uint32_t tag = (uint32_t)a.epoch[0];
+    // Between units the row buffer is free: it holds the pass bookkeeping.
+    int* xs = reinterpret_cast<int*>(sm.rowbuf);
     const int n_pass = a.plan[0];
-    const int w = blockIdx.x;
-    for (int ps = 0; ps < n_pass; ++ps) {
-        const int sb = a.plan[2 + 3 * ps], se = a.plan[3 + 3 * ps];
+    const bool lanes = n_pass < 0;
+    // Lane mode.  The first workgroup dispatched to each CU (blocks
+    // 0 .. n_cu - 1) wins most memory issue slots over the second, so the
+    // two kinds run at different speeds.  Each kind forms a lane with one
+    // workgroup per CU; a lane runs passes of whole sessions that it claims
+    // itself, lane 0 from the front of the session list and lane 1 from the
+    // back, so the units of one session always share a lane and start
+    // together, and the faster lane takes more sessions.
+    const int lane_no = lanes ? (int)blockIdx.x / dm.n_cu : 0;
+    const int w = lanes ? (int)blockIdx.x % dm.n_cu : (int)blockIdx.x;
+    const int cap = lanes ? dm.n_cu : 0;
+    for (int ps = 0;; ++ps) {
+        lds_sync();   // the previous unit is done with the LDS
+        int sb, se;
+        if (!lanes) {
+            if (ps >= n_pass) break;
+            sb = a.plan[2 + 3 * ps];
+            se = a.plan[3 + 3 * ps];
+        } else {
+            if (w == 0) claim_sessions(a, xs, lane_no, cap);
+            if (threadIdx.x == 0) {
+                unsigned long long* box = a.lane_box + (size_t)lane_no * (dm.S + 1) + ps;
+                if (w == 0) {
+                    __hip_atomic_store(box, ((unsigned long long)tag << 32) | ((uint32_t)xs[0] << 16) | (uint32_t)xs[1],
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                } else {
+                    // the lane's first workgroup publishes the pass once its
+                    // own unit of the last pass is done (bounded wait)
+                    const uint64_t t0 = now_ticks();
+                    unsigned long long v = __hip_atomic_load(box, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    while ((uint32_t)(v >> 32) != tag) {
+                        if (now_ticks() - t0 > kUnitTicks) {
+                            atomicOr(a.status, MD_DEV_TIMEOUT);
+                            v = 0;
+                            break;
+                        }
+                        __builtin_amdgcn_s_sleep(8);
+                        v = __hip_atomic_load(box, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                    xs[0] = (int)((v >> 16) & 0xffff);
+                    xs[1] = (int)(v & 0xffff);
+                }
+            }
+            __syncthreads();
+            sb = xs[0];
+            se = xs[1];
+            if (sb >= se) break;
+        }
         const int u0 = a.ustart[sb];
         if (w >= a.ustart[se] - u0) continue;
-        // session of unit u0 + w: largest s in [sb, se) with ustart[s] <= u0 + w
-        int lo = sb, hi = se;
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (a.ustart[mid] <= u0 + w) lo = mid; else hi = mid;
-        }
+        // session of unit u0 + w: the last s in [sb, se) with ustart[s] <= u0 + w
+        const int s = sb + count_at_most(a.ustart + sb, se - sb, u0 + w, xs + 2) - 1;
         Unit un;
-        un.s = lo;
-        un.us = a.ustart[lo];
-        un.nu = a.ustart[lo + 1] - un.us;
+        un.s = s;
+        un.us = a.ustart[s];
+        un.nu = a.ustart[s + 1] - un.us;
         un.j = u0 + w - un.us;
-        un.nt_s = a.n_tokens[lo];
+        un.nt_s = a.n_tokens[s];
         constexpr int kT = 16 * W * KT;
         un.ntok = min(kT, un.nt_s - un.j * kT);
         un.deadline = now_ticks() + kUnitTicks;
-        lds_sync();   // the previous unit is done with the LDS
         // The lane index is made opaque here so that per-lane address
         // arithmetic is not hoisted out of the pass loop and kept live.
         int lane = (int)threadIdx.x & 63;
@@ -630,9 +757,10 @@ const void* attend_kernel(int G) {
 
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q, float* abar_out,
                          hipStream_t st) {
-    AttendDims ad{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.MP, dm.NP, dm.R, dm.LHkv, dm.rho, dm.tau_scale};
+    AttendDims ad{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.MP, dm.NP, dm.R, dm.LHkv,
+                  dm.wg_per_cu, dm.n_wg / dm.wg_per_cu, dm.S, dm.rho, dm.tau_scale};
     AttendArgs aa{v.k_pool, v.page_table, v.n_tokens, v.clock, v.imp, v.t_ref, q, abar_out,
-                  sc.ustart, sc.plan, sc.epoch, sc.ustat, sc.unorm, sc.status, nullptr};
+                  sc.ustart, sc.plan, sc.epoch, sc.claim, sc.lane_box, sc.ustat, sc.unorm, sc.status, nullptr};
     void* args[] = {&ad, &aa};
     return hipLaunchCooperativeKernel(attend_kernel(dm.G), dim3(dm.n_wg), dim3(attend_threads(dm.G)), args,
                                       (unsigned)attend_lds_bytes(dm.G), st);

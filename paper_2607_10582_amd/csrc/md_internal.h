@@ -33,6 +33,8 @@ struct Dims {
     int fused;     // 1: sessions that fit one pass run on k_attend
     int spill;     // 1: some session may not fit a pass (the spill kernels run)
     int n_wg;      // k_attend workgroups (all co-resident)
+    int wg_per_cu; // k_attend workgroups per CU (n_wg = wg_per_cu * CUs)
+    int lane_cap;  // units one lane of k_attend workgroups holds (one workgroup per CU)
     int T;         // tokens per fused unit (attend_unit_tokens(G))
     int U_cap;     // capacity of the per-step fused unit list
     uint32_t pin_mask;
@@ -69,6 +71,8 @@ struct Scratch {
     int32_t* ustart;       // [S + 1] prefix of fused units over the sessions
     int32_t* plan;         // [1 + 3 (S + 1)]: passes, then (unit tokens, first, end session) per pass
     int32_t* epoch;        // [1] observation counter; tags the fused unit statistics
+    unsigned long long* claim;     // [1] lane mode: (first, end) of the sessions no lane has claimed
+    unsigned long long* lane_box;  // [kAttendPerCu][S + 1] lane mode: tagged session range of each lane pass
     unsigned long long* ustat;  // [U_cap][R][2] tagged (max, sum) of each fused unit's rows
     unsigned long long* unorm;  // [S][R][2] tagged row normalisers (M, 1 / Lambda) of the fused sessions
     int32_t* chunks;       // [S] chunks per session (0 for a skipped session)

@@ -111,12 +111,29 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         s_n[s2] = ok ? nt : 0;
         s_pass[s2] = -1;
     }
+    // Lane mode when every fused session fits one lane (one workgroup per
+    // CU): each lane then claims whole sessions as it goes (see k_attend).
+    __shared__ int s_lane_ok;
+    if (threadIdx.x == 0) s_lane_ok = dm.fused && dm.wg_per_cu >= 2;
     __syncthreads();
-    if (threadIdx.x == 0 && dm.fused) {
+    if (dm.fused) {
+        for (int s2 = threadIdx.x; s2 < dm.S; s2 += blockDim.x) {
+            const int u = (s_n[s2] + dm.T - 1) / dm.T;
+            if (u > dm.lane_cap) atomicExch(&s_lane_ok, 0);
+            if (u <= dm.n_wg) s_pass[s2] = 0;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0 && dm.fused && s_lane_ok) {
+        sc.plan[0] = -1;
+        *sc.claim = (unsigned long long)dm.S;   // first 0, end S
+        *sc.epoch += 1;
+    } else if (threadIdx.x == 0 && dm.fused) {
         // Sessions in order, packed greedily into passes of at most n_wg
         // units (a session's units wait for each other row by row, so all of
         // them run in the same pass).  A session larger than a whole pass
         // takes the spill path.
+        for (int s2 = 0; s2 < dm.S; ++s2) s_pass[s2] = -1;
         int np = 0, s0 = 0;
         while (s0 < dm.S) {
             int used = 0, e = s0;
@@ -859,6 +876,7 @@ size_t scratch_bytes(const Dims& dm) {
     n += 6 * align256((size_t)(dm.S + 1) * sizeof(int32_t));
     n += align256((size_t)(1 + 3 * (dm.S + 1)) * sizeof(int32_t));
     n += align256(sizeof(int32_t));
+    n += align256((1 + (size_t)kAttendPerCu * (dm.S + 1)) * sizeof(unsigned long long));
     n += align256((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long));
     n += align256((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long));
     n += align256(2 * sizeof(int32_t));
@@ -886,6 +904,9 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
     sc->ustart = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
     sc->plan = reinterpret_cast<int32_t*>(take((size_t)(1 + 3 * (dm.S + 1)) * sizeof(int32_t)));
     sc->epoch = reinterpret_cast<int32_t*>(take(sizeof(int32_t)));
+    sc->claim = reinterpret_cast<unsigned long long*>(
+        take((1 + (size_t)kAttendPerCu * (dm.S + 1)) * sizeof(unsigned long long)));
+    sc->lane_box = sc->claim + 1;
     sc->ustat = reinterpret_cast<unsigned long long*>(
         take((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long)));
     sc->unorm = reinterpret_cast<unsigned long long*>(
