@@ -2,8 +2,10 @@
 """Benchmark of MemDecay's per-decode-step retention path on one MI355X.
 
 A step is the whole path over one batch: md_observe_step (append, attention
-mass, EWMA, refresh), md_score_pages (token and page scores), md_select_evict
-(budgeted page selection) and md_compact (page-table compaction).  All inputs
+mass, EWMA, refresh, and on the fused kernel also the token and page scores),
+md_score_pages (here with no outputs requested, so it adds no work),
+md_select_evict (budgeted page selection) and md_compact (page-table
+compaction).  All inputs
 (the paged key cache, every step's queries and appended keys) are resident in
 HBM before timing starts.  The default workload is 16 sessions of 32,768
 cached tokens with Qwen2.5-1.5B's attention shape (28 layers, 12 query / 2 KV
@@ -199,7 +201,7 @@ def main():
 
     for k in range(1, W + 1):
         q, nk, reg = inputs[k - 1]
-        md.step(k, q, nk, reg)
+        md.step(k, q, nk, reg, page_scores=False)
     torch.cuda.synchronize(dev)
     c0 = md.counters()
     kcfg = md.kernel_config()
@@ -214,7 +216,7 @@ def main():
     ev0.record(stream)
     for k in range(W + 1, W + K + 1):
         q, nk, reg = inputs[k - 1]
-        md.step(k, q, nk, reg)
+        md.step(k, q, nk, reg, page_scores=False)
     ev1.record(stream)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0

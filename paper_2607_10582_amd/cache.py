@@ -148,9 +148,11 @@ class MemDecay:
         ec = self.evict_count if evict_count is None else evict_count
         B.md_compact(self.handle, _ptr(es, torch.int32), _ptr(ec, torch.int32))
 
-    def step(self, step: int, q, new_k=None, new_region=None):
+    def step(self, step: int, q, new_k=None, new_region=None, page_scores: bool = True):
+        """One decode step; page_scores=False leaves self.page_score untouched
+        (the library still scores every page for its own selection)."""
         self.observe(step, q, new_k, new_region)
-        self.score()
+        self.score(page_score=page_scores)
         self.select()
         self.compact()
 

@@ -317,7 +317,11 @@ md_status md_score_pages(md_handle h, float* page_score, float* token_score) {
         return MD_E_INVALID;
     if (h->phase != kObserved && h->phase != kScored) return MD_E_STATE;
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
-    if (timed_launch(h, MD_K_SCORE, [&] {
+    // The fused observation kernel already left every session's page scores
+    // in the library's copy; the scoring kernel runs again only to fill the
+    // caller's outputs, or for sessions of the multi-kernel path.
+    const bool needed = page_score != nullptr || token_score != nullptr || !h->dm.fused || h->dm.spill;
+    if (needed && timed_launch(h, MD_K_SCORE, [&] {
             return md::launch_score(h->dm, h->v, h->sc, page_score, token_score, h->score_blocks,
                                     h->stream); }) != hipSuccess)
         return MD_E_HIP;

@@ -49,8 +49,9 @@ namespace {
 
 struct AttendDims {
     int L, Hq, Hkv, G, P, Pshift, MP, NP, R, LHkv;
-    int wg_per_cu, n_cu, S;
-    float rho, tau_scale;
+    int wg_per_cu, n_cu, S, n_regions;
+    uint32_t pin_mask;
+    float rho, tau_scale, alpha;
 };
 
 struct AttendArgs {
@@ -58,8 +59,12 @@ struct AttendArgs {
     const int32_t* page_table;
     const int32_t* n_tokens;
     const int32_t* clock;
+    const uint8_t* region;
+    const float* b;
+    const float* lam;
     float* imp;
     int32_t* t_ref;
+    float* pscore;
     const float* q;
     float* abar_out;
     const int32_t* ustart;
@@ -548,19 +553,45 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         lds_sync();
     }
 
-    // ---- Eq. 2 and Eq. 3 for this wave's tokens
+    // ---- Eq. 2 and Eq. 3 for this wave's tokens, then their retention
+    // scores (Eq. 4) and the scores of their pages (Eq. 5): a page's P
+    // tokens are P consecutive lanes of one wave, since units and waves
+    // start at multiples of 64 tokens.
+    const int t_now = a.clock[un.s];
+    const size_t rbase = (size_t)un.s * dm.n_regions;
 #pragma unroll
     for (int k = 0; k < kTok; ++k) {
         const int lt = lane + 64 * k;   // wave-local token
         const int tile = lt >> 4;
         const int slot0 = __shfl(myslot, tile);
-        if (wtok0 + lt < un.ntok && ((vmask >> tile) & 1ull)) {
+        const bool live = wtok0 + lt < un.ntok && ((vmask >> tile) & 1ull);
+        float sc = 0.0f;
+        bool pin = false;
+        if (live) {
             const float abar = acc[k] / (float)dm.R;
             const size_t si = (size_t)slot0 + (lt & 15);
-            a.imp[si] = fmaf(dm.rho, a.imp[si], (1.0f - dm.rho) * abar);
-            if (abar >= dm.tau_scale / (float)un.nt_s) a.t_ref[si] = a.clock[un.s];
+            const float an = fmaf(dm.rho, a.imp[si], (1.0f - dm.rho) * abar);
+            a.imp[si] = an;
+            int tr;
+            if (abar >= dm.tau_scale / (float)un.nt_s) {
+                tr = t_now;
+                a.t_ref[si] = tr;
+            } else {
+                tr = a.t_ref[si];
+            }
             if (a.abar_out != nullptr) a.abar_out[si] = abar;
+            int r = a.region[si];
+            if (r >= dm.n_regions) {
+                atomicOr(a.status, kDevCorrupt);
+                r = dm.n_regions - 1;
+            }
+            pin = (dm.pin_mask >> r) & 1u;
+            sc = pin ? INFINITY : retention_score(a.b[rbase + r], a.lam[rbase + r], t_now, tr, dm.alpha, an);
         }
+        float ps;
+        const bool has = page_score_of(sc, live, pin, dm.P, &ps);
+        const int tok = un.j * kT + wtok0 + lt;
+        if ((lt & (dm.P - 1)) == 0 && has) a.pscore[(size_t)un.s * dm.MP + (tok >> dm.Pshift)] = ps;
     }
 }
 
@@ -758,9 +789,11 @@ const void* attend_kernel(int G) {
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q, float* abar_out,
                          hipStream_t st) {
     AttendDims ad{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.MP, dm.NP, dm.R, dm.LHkv,
-                  dm.wg_per_cu, dm.n_wg / dm.wg_per_cu, dm.S, dm.rho, dm.tau_scale};
-    AttendArgs aa{v.k_pool, v.page_table, v.n_tokens, v.clock, v.imp, v.t_ref, q, abar_out,
-                  sc.ustart, sc.plan, sc.epoch, sc.claim, sc.lane_box, sc.ustat, sc.unorm, sc.status, nullptr};
+                  dm.wg_per_cu, dm.n_wg / dm.wg_per_cu, dm.S, dm.n_regions, dm.pin_mask,
+                  dm.rho, dm.tau_scale, dm.alpha};
+    AttendArgs aa{v.k_pool, v.page_table, v.n_tokens, v.clock, v.region, v.b, v.lam, v.imp, v.t_ref,
+                  sc.pscore, q, abar_out, sc.ustart, sc.plan, sc.epoch, sc.claim, sc.lane_box, sc.ustat,
+                  sc.unorm, sc.status, nullptr};
     void* args[] = {&ad, &aa};
     return hipLaunchCooperativeKernel(attend_kernel(dm.G), dim3(dm.n_wg), dim3(attend_threads(dm.G)), args,
                                       (unsigned)attend_lds_bytes(dm.G), st);

@@ -97,6 +97,29 @@ __device__ __forceinline__ void split3(float x, uint32_t& hi, uint32_t& mid, uin
 }
 
 
+// Retention score of an unpinned token (Eq. 4): base priority b and decay
+// rate lam of its region, age t - t_ref, importance a.
+__device__ __forceinline__ float retention_score(float b, float lam, int t, int t_ref, float alpha, float a) {
+    return b * expf(-lam * (float)(t - t_ref)) + alpha * a;
+}
+
+// Page score (Eq. 5) over the P consecutive lanes that hold one page's
+// tokens: the mean of the unpinned members' scores, +inf when any member is
+// pinned.  Returns false when the page has no live member.  Every lane of
+// the page gets the same bits.
+__device__ __forceinline__ bool page_score_of(float score, bool live, bool pinned, int P, float* out) {
+    float sum = (live && !pinned) ? score : 0.0f;
+    int cnt = live ? 1 : 0;
+    int anyp = pinned ? 1 : 0;
+    for (int o = 1; o < P; o <<= 1) {
+        sum += __shfl_xor(sum, o);
+        cnt += __shfl_xor(cnt, o);
+        anyp |= __shfl_xor(anyp, o);
+    }
+    *out = anyp ? INFINITY : sum / (float)cnt;
+    return cnt > 0;
+}
+
 // Wave-uniform value kept in a scalar register.
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 

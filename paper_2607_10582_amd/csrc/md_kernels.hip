@@ -612,22 +612,14 @@ __global__ void __launch_bounds__(256) k_score(Dims dm, View v, Scratch sc, floa
                     sc_i = INFINITY;
                 } else {
                     const size_t ri = (size_t)s * dm.n_regions + r;
-                    const float dt = (float)(t - v.t_ref[si]);
-                    sc_i = v.b[ri] * expf(-v.lam[ri] * dt) + dm.alpha * v.imp[si];
+                    sc_i = retention_score(v.b[ri], v.lam[ri], t, v.t_ref[si], dm.alpha, v.imp[si]);
                 }
                 if (token_score != nullptr) token_score[si] = sc_i;
             }
         }
-        float sum = (valid && !pin) ? sc_i : 0.0f;
-        int cnt = valid ? 1 : 0;
-        int anyp = pin ? 1 : 0;
-        for (int o = 1; o < dm.P; o <<= 1) {
-            sum += __shfl_xor(sum, o);
-            cnt += __shfl_xor(cnt, o);
-            anyp |= __shfl_xor(anyp, o);
-        }
-        if ((lane & (dm.P - 1)) == 0 && cnt > 0) {
-            const float ps = anyp ? INFINITY : sum / (float)cnt;
+        float ps;
+        const bool has = page_score_of(sc_i, valid, pin, dm.P, &ps);
+        if ((lane & (dm.P - 1)) == 0 && has) {
             sc.pscore[(size_t)s * dm.MP + pg] = ps;
             if (page_score != nullptr) page_score[(size_t)s * dm.MP + pg] = ps;
         }

@@ -205,3 +205,40 @@ def test_determinism_two_runs():
         p.close()
     for a, b in zip(*outs):
         assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_selection_on_scores_of_the_fused_kernel():
+    # md_score_pages with both outputs NULL enqueues nothing: the selection
+    # then runs on the page scores the fused observation kernel wrote.  The
+    # same steps with the scoring kernel refilling them (outputs requested)
+    # must evict exactly the same pages, from the bulk eviction on.
+    w = C.with_overrides(C.get("qwen3_32x1700"), S=8, steps=8)
+    runs = []
+    for outputs in (True, False):
+        p = Pair(w, oracle_sessions=[])
+        assert p.md.kernel_config()["fused"] and not p.md.kernel_config()["spill"]
+        ev = []
+        for k in range(1, 9):
+            q, nk, reg, *_ = p.inputs(k)
+            p.md.observe(k, q, nk, reg)
+            p.md.score(page_score=outputs)
+            p.md.select()
+            cnt = p.md.evict_count.cpu().numpy().copy()
+            ser = p.md.evict_serial.cpu().numpy()
+            ev.append([ser[s, :cnt[s]].copy() for s in range(w.S)])
+            p.md.compact()
+        torch.cuda.synchronize()
+        assert p.device_status() == 0
+        c = p.cache
+        np_ = c.n_pages.cpu().numpy().copy()
+        runs.append((ev, c.n_tokens.cpu().numpy().copy(), np_,
+                     [c.page_serial.cpu().numpy()[s, :np_[s]].copy() for s in range(w.S)]))
+        p.close()
+    (ev1, nt1, np1, ser1), (ev2, nt2, np2, ser2) = runs
+    assert sum(len(x) for x in ev1[0]) > 0
+    for a, b in zip(ev1, ev2):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+    assert np.array_equal(nt1, nt2) and np.array_equal(np1, np2)
+    for x, y in zip(ser1, ser2):
+        assert np.array_equal(x, y)
