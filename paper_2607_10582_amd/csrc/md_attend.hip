@@ -468,12 +468,14 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     //      query terms are read from LDS once, the four accumulations run
     //      side by side);
     //   2. bookkeeping on the last iteration's loads; the query of row r + 1
-    //      into LDS;
-    //   3. this iteration's requests and row r + 2's query, then the tiles
-    //      of row r + 2;
-    //   4. softmax statistics of row r, its logits into LDS;
-    //   5. publish row r - 1, normalise row r - 7; row r's statistics into
+    //      into LDS; this iteration's requests and row r + 2's query;
+    //   3. softmax statistics of row r, its logits into LDS;
+    //   4. publish row r - 1, normalise row r - 7; row r's statistics into
     //      LDS; barrier.
+    // The four tiles of row r + 2 go out one by one between these steps
+    // rather than in one burst: a burst of all waves' loads at once stalls
+    // every wave at issue, while spread out the issue waits overlap the
+    // work of the row.
     auto do_row = [&](u32x4 (&ring)[KT][4], int row) {
         const uint32_t* qb = sm.qs + (size_t)(row & 1) * 3 * G * 64 + hh * 64 + 4 * g;
         f32x4 c[KT];
@@ -491,12 +493,13 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
                     c[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                         __builtin_bit_cast(bf16x8, ring[u][j]), __builtin_bit_cast(bf16x8, bq[p]), c[u], 0, 0, 0);
         }
+        load_tile(ring[0], row + 2, 0);
         use_loads(row);
+        load_tile(ring[1], row + 2, 1);
         if (row + 1 < dm.LHkv) store_q(row + 1);
         issue_loads(row);
         load_q(min(row + 2, last));
-#pragma unroll
-        for (int u = 0; u < KT; ++u) load_tile(ring[u], row + 2, u);
+        load_tile(ring[2], row + 2, 2);
 
         // Base-2 logits of the wave's 64 tokens (lane: head h, tokens
         // 16 u + 4 g + i), their maximum and the sum of 2^(logit - max) per
@@ -530,6 +533,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
             ls += (pv[0] + pv[1]) + (pv[2] + pv[3]);
             if (h < G) *reinterpret_cast<f32x4*>(rbw + 16 * u) = pv;
         }
+        load_tile(ring[3], row + 2, 3);
         ls += __shfl_xor(ls, 16);
         ls += __shfl_xor(ls, 32);
         after_tiles(row);
