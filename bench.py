@@ -56,7 +56,7 @@ def describe(w, n0s) -> str:
             f"d {w.d}, pages of {w.P}, budget {int(w.budget_frac * 100)}%")
 
 
-def setup(w, steps_total, dev):
+def setup(w, steps_total, dev, fused=None):
     import torch
     from paper_2607_10582_amd.cache import MemDecay, PagedCache
     from synth import configs as C
@@ -82,7 +82,7 @@ def setup(w, steps_total, dev):
         del keys
     cache.set_free_pages(perm[pos:][::-1])
     md = MemDecay(cache, torch.from_numpy(b), torch.from_numpy(lam), rho=w.rho, alpha=w.alpha,
-                  tau_scale=w.tau_scale, pinned_mask=w.pinned_mask)
+                  tau_scale=w.tau_scale, pinned_mask=w.pinned_mask, fused=fused)
     inputs = []
     for k in range(1, steps_total + 1):
         q = g.torch_queries(w, k, dev)
@@ -171,6 +171,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="long32k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--multi-kernel", action="store_true",
+                    help="observe on the multi-kernel path (logits in HBM) at every step instead of "
+                         "letting the library pick")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     args = ap.parse_args()
@@ -196,7 +199,7 @@ def main():
     if W + K > w.steps:
         log(f"note: {W + K} steps asked, the workload defines {w.steps} decode steps")
     t_setup = time.perf_counter()
-    n0s, B, cache, md, inputs = setup(w, W + K, dev)
+    n0s, B, cache, md, inputs = setup(w, W + K, dev, fused=False if args.multi_kernel else None)
     log(f"setup {time.perf_counter() - t_setup:.1f} s: {describe(w, n0s)}")
 
     for k in range(1, W + 1):
@@ -205,7 +208,7 @@ def main():
     torch.cuda.synchronize(dev)
     c0 = md.counters()
     kcfg = md.kernel_config()
-    hot = "attend" if kcfg["fused"] and not kcfg["spill"] else "logits"
+    hot = "attend" if kcfg["steady_fused"] and not kcfg["spill"] else "logits"
     log(f"kernel config {kcfg}; timing k_{hot}")
     md.profile((hot,))
     stream = md.stream
@@ -236,8 +239,12 @@ def main():
     q_bytes = w.S * w.L * w.Hq * w.d * 4
     # algorithmic bytes over the timed launches: every cached key once and the
     # queries once; the fused kernel also reads and writes each token's
-    # importance (Eq. 2)
-    hot_bytes = scored * kb + K * q_bytes + (scored * 8 if hot == "attend" else 0)
+    # importance (Eq. 2), reads its refresh clock and region (Eq. 3, Eq. 4),
+    # and reads each page's table entry and writes its score (Eq. 5)
+    if hot == "attend":
+        hot_bytes = scored * (kb + 13) + (scored // w.P) * 8 + K * q_bytes
+    else:
+        hot_bytes = scored * kb + K * q_bytes
     avg_launch_s = hot_ms / 1e3 / max(launches, 1)
     per_launch_bytes = hot_bytes / max(launches, 1)
     achieved = per_launch_bytes / avg_launch_s / 1e9

@@ -85,6 +85,14 @@ enum {
 #define MD_FLAG_NO_FUSED  0x1   /* observe every session with the multi-kernel  */
                                 /* path (logits through HBM) instead of the     */
                                 /* fused one; results agree to rounding         */
+#define MD_FLAG_FUSED     0x2   /* observe on the fused kernel whenever it can  */
+                                /* hold the sessions.  With neither flag,       */
+                                /* md_init picks the path of the first observe  */
+                                /* and of the later ones from the cache's sizes */
+                                /* and budgets at init: the fused kernel walks  */
+                                /* the layers in order, so for small caches the */
+                                /* multi-kernel path, parallel over layers, is  */
+                                /* faster                                       */
 
 typedef struct md_config {
     int32_t n_layers;           /* L                                              */
@@ -233,11 +241,13 @@ md_status md_profile_read(md_handle h, int32_t kernel, double* total_ms, int64_t
  * observed, out[2] pages evicted, out[3] tokens evicted. */
 md_status md_read_counters(md_handle h, int64_t* out);
 
-/* How md_init laid out the observation step on this device: out[0] 1 when
- * the fused observation kernel is used, out[1] 1 when the multi-kernel path
- * may run (flag MD_FLAG_NO_FUSED, or a session could outgrow one pass of the
- * fused kernel), out[2] the largest fused unit in tokens, out[3] the fused
- * kernel's workgroups (all resident at once).  Host-only, no device work. */
+/* How md_init laid out the observation step on this device (out: 6 ints):
+ * out[0] 1 when the fused observation kernel is available, out[1] 1 when a
+ * session could outgrow one pass of it (those sessions always take the
+ * multi-kernel path), out[2] the largest fused unit in tokens, out[3] the
+ * fused kernel's workgroups (all resident at once), out[4] 1 when the first
+ * md_observe_step runs the fused kernel, out[5] 1 when the later ones do.
+ * Host-only, no device work. */
 md_status md_kernel_config(md_handle h, int32_t* out);
 
 /* Release the scratch and the handle (synchronises the stream first). */

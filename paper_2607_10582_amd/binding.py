@@ -26,6 +26,7 @@ MD_DEV_CORRUPT = 0x8
 MD_DEV_TIMEOUT = 0x10
 
 MD_FLAG_NO_FUSED = 0x1
+MD_FLAG_FUSED = 0x2
 
 EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_observe_step",
            "md_score_pages", "md_select_evict", "md_compact", "md_read_device_status",
@@ -184,11 +185,13 @@ def md_read_counters(h: int):
 
 
 def md_kernel_config(h: int) -> dict:
-    """How md_init laid out the observation step (fused kernel, spill path,
-    largest fused unit in tokens, fused workgroups)."""
-    out = (ctypes.c_int32 * 4)()
+    """How md_init laid out the observation step (fused kernel available,
+    sessions that may outgrow it, largest fused unit in tokens, fused
+    workgroups, path of the first and of the later observes)."""
+    out = (ctypes.c_int32 * 6)()
     _check("md_kernel_config", load_library().md_kernel_config(h, out))
-    return {"fused": bool(out[0]), "spill": bool(out[1]), "unit_max": int(out[2]), "workgroups": int(out[3])}
+    return {"fused": bool(out[0]), "spill": bool(out[1]), "unit_max": int(out[2]), "workgroups": int(out[3]),
+            "first_fused": bool(out[4]), "steady_fused": bool(out[5])}
 
 
 def md_destroy(h: int) -> int:

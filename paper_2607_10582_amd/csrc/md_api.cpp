@@ -7,6 +7,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <vector>
 
@@ -36,6 +37,10 @@ struct md_handle_s {
     int score_blocks;
     bool have_step;
     int32_t last_step;
+    bool fused_first;    // the first observe runs the fused kernel
+    bool fused_steady;   // later observes run the fused kernel
+    bool fused_last;     // the last observe ran it
+    int64_t observed;    // observes enqueued
     Phase phase;
     uint32_t profile_mask;
     std::vector<Timed> pending[MD_K_COUNT];   // launches not yet read back
@@ -101,7 +106,8 @@ const char* md_status_str(md_status s) {
 
 static md_status validate_config(const md_config* c) {
     if (c == nullptr) return MD_E_INVALID;
-    if ((c->flags & ~MD_FLAG_NO_FUSED) != 0) return MD_E_INVALID;
+    if ((c->flags & ~(MD_FLAG_NO_FUSED | MD_FLAG_FUSED)) != 0) return MD_E_INVALID;
+    if ((c->flags & MD_FLAG_NO_FUSED) && (c->flags & MD_FLAG_FUSED)) return MD_E_INVALID;
     if (c->n_layers < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1) return MD_E_INVALID;
     if (c->n_q_heads % c->n_kv_heads != 0) return MD_E_INVALID;
     if (c->max_sessions < 1 || c->max_pages < 1 || c->n_phys_pages < 1) return MD_E_INVALID;
@@ -237,6 +243,33 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     }
     dm.spill = !dm.fused || (int64_t)dm.MP * dm.P > (int64_t)dm.n_wg * dm.T;
 
+    // Path of the first observe and of the later ones.  The fused kernel walks
+    // the L * Hkv key rows of each unit in order, a few microseconds per row,
+    // so it pays off once its units fill half its workgroups; below that the
+    // multi-kernel path, parallel over rows, is faster.  Units are counted
+    // from the cache's sizes now (first observe) and with each session at
+    // most one token over its budget (later observes, once evictions hold
+    // the budget).
+    bool fused_first = dm.fused, fused_steady = dm.fused;
+    if (dm.fused && !(cfg->flags & MD_FLAG_FUSED)) {
+        std::vector<int32_t> hn(dm.S), hbud(dm.S);
+        if (hipMemcpyAsync(hn.data(), cv->n_tokens, dm.S * sizeof(int32_t), hipMemcpyDeviceToHost, hs) != hipSuccess ||
+            hipMemcpyAsync(hbud.data(), cv->budget, dm.S * sizeof(int32_t), hipMemcpyDeviceToHost, hs) !=
+                hipSuccess ||
+            hipStreamSynchronize(hs) != hipSuccess)
+            return MD_E_HIP;
+        int64_t first = 0, steady = 0;
+        for (int s = 0; s < dm.S; ++s) {
+            const int64_t n = hn[s] > 0 ? hn[s] : 0;
+            const int64_t b = hbud[s] >= 0 ? (int64_t)hbud[s] + 1 : n;
+            first += (n + dm.T - 1) / dm.T;
+            steady += (std::min(n, b) + dm.T - 1) / dm.T;
+        }
+        fused_first = 2 * first >= dm.n_wg;
+        fused_steady = 2 * steady >= dm.n_wg;
+    }
+    dm.multi = dm.spill || !fused_first || !fused_steady;
+
     md_handle_s* h = new (std::nothrow) md_handle_s();
     if (h == nullptr) return MD_E_NOMEM;
     h->dm = dm;
@@ -277,6 +310,10 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     h->score_blocks = 2 * n_cu;
     h->have_step = false;
     h->last_step = 0;
+    h->fused_first = fused_first;
+    h->fused_steady = fused_steady;
+    h->fused_last = false;
+    h->observed = 0;
     h->phase = kNone;
     h->profile_mask = 0;
     *out = h;
@@ -290,20 +327,25 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     if (abar_out != nullptr && !aligned(abar_out, 4)) return MD_E_INVALID;
     if (h->have_step && step != h->last_step + 1) return MD_E_STEP;
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    const bool fused = h->observed == 0 ? h->fused_first : h->fused_steady;
     hipError_t e = timed_launch(h, MD_K_APPEND, [&] {
-        return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, h->stream); });
-    // Sessions that fit one pass of the fused kernel run there; the others
-    // (only possible when a session may outgrow n_wg * T tokens) take the
-    // three-kernel path with the logits in HBM.
-    if (e == hipSuccess && h->dm.fused) e = timed_launch(h, MD_K_ATTEND, [&] {
+        return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, fused ? 1 : 0, h->stream); });
+    // On a fused step, sessions that fit one pass of the fused kernel run
+    // there; the others (only possible when a session may outgrow n_wg * T
+    // tokens) take the three-kernel path with the logits in HBM, which on
+    // the other steps observes every session.
+    const bool multi = !fused || h->dm.spill;
+    if (e == hipSuccess && fused) e = timed_launch(h, MD_K_ATTEND, [&] {
         return md::launch_attend(h->dm, h->v, h->sc, q, abar_out, h->stream); });
-    if (e == hipSuccess && h->dm.spill) e = timed_launch(h, MD_K_LOGITS, [&] {
+    if (e == hipSuccess && multi) e = timed_launch(h, MD_K_LOGITS, [&] {
         return md::launch_logits(h->dm, h->v, h->sc, q, h->logits_blocks, h->stream); });
-    if (e == hipSuccess && h->dm.spill) e = timed_launch(h, MD_K_ROWSTATS, [&] {
+    if (e == hipSuccess && multi) e = timed_launch(h, MD_K_ROWSTATS, [&] {
         return md::launch_rowstats(h->dm, h->sc, h->stream); });
-    if (e == hipSuccess && h->dm.spill) e = timed_launch(h, MD_K_MASS, [&] {
+    if (e == hipSuccess && multi) e = timed_launch(h, MD_K_MASS, [&] {
         return md::launch_mass(h->dm, h->v, h->sc, abar_out, h->mass_blocks, h->stream); });
     if (e != hipSuccess) return MD_E_HIP;
+    h->fused_last = fused && !h->dm.spill;
+    h->observed += 1;
     h->have_step = true;
     h->last_step = step;
     h->phase = kObserved;
@@ -320,7 +362,7 @@ md_status md_score_pages(md_handle h, float* page_score, float* token_score) {
     // The fused observation kernel already left every session's page scores
     // in the library's copy; the scoring kernel runs again only to fill the
     // caller's outputs, or for sessions of the multi-kernel path.
-    const bool needed = page_score != nullptr || token_score != nullptr || !h->dm.fused || h->dm.spill;
+    const bool needed = page_score != nullptr || token_score != nullptr || !h->fused_last;
     if (needed && timed_launch(h, MD_K_SCORE, [&] {
             return md::launch_score(h->dm, h->v, h->sc, page_score, token_score, h->score_blocks,
                                     h->stream); }) != hipSuccess)
@@ -409,6 +451,8 @@ md_status md_kernel_config(md_handle h, int32_t* out) {
     out[1] = h->dm.spill;
     out[2] = h->dm.fused ? h->dm.T : 0;
     out[3] = h->dm.n_wg;
+    out[4] = h->fused_first ? 1 : 0;
+    out[5] = h->fused_steady ? 1 : 0;
     return MD_OK;
 }
 

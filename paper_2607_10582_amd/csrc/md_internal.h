@@ -32,6 +32,7 @@ struct Dims {
     int L, Hq, Hkv, G, P, Pshift, S, MP, NP, R, LHkv, n_regions, max_chunks;
     int fused;     // 1: sessions that fit one pass run on k_attend
     int spill;     // 1: some session may not fit a pass (the spill kernels run)
+    int multi;     // 1: the multi-kernel path runs at some step (its scratch exists)
     int n_wg;      // k_attend workgroups (all co-resident)
     int wg_per_cu; // k_attend workgroups per CU (n_wg = wg_per_cu * CUs)
     int lane_cap;  // units one lane of k_attend workgroups holds (one workgroup per CU)
@@ -86,8 +87,10 @@ size_t scratch_bytes(const Dims& dm);
 void scratch_carve(const Dims& dm, void* base, Scratch* sc);
 
 // Launchers; each returns the hipError_t of its launch.
+// fused: this step observes on the fused kernel (sessions that fit a pass)
+// or, when 0, every session on the multi-kernel path.
 hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
-                         const uint16_t* new_k, const uint8_t* new_region, hipStream_t st);
+                         const uint16_t* new_k, const uint8_t* new_region, int fused, hipStream_t st);
 hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q,
                          int n_blocks, hipStream_t st);
 hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st);

@@ -27,7 +27,7 @@ namespace md {
 // step's work lists.
 __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                                                 const uint16_t* __restrict__ new_k,
-                                                const uint8_t* __restrict__ new_region) {
+                                                const uint8_t* __restrict__ new_region, int fused) {
     const int s = blockIdx.x;
     __shared__ int sh_phys, sh_slot, sh_last;
     __shared__ int lds[17];
@@ -114,9 +114,9 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     // Lane mode when every fused session fits one lane (one workgroup per
     // CU): each lane then claims whole sessions as it goes (see k_attend).
     __shared__ int s_lane_ok;
-    if (threadIdx.x == 0) s_lane_ok = dm.fused && dm.wg_per_cu >= 2;
+    if (threadIdx.x == 0) s_lane_ok = fused && dm.wg_per_cu >= 2;
     __syncthreads();
-    if (dm.fused) {
+    if (fused) {
         for (int s2 = threadIdx.x; s2 < dm.S; s2 += blockDim.x) {
             const int u = (s_n[s2] + dm.T - 1) / dm.T;
             if (u > dm.lane_cap) atomicExch(&s_lane_ok, 0);
@@ -124,11 +124,11 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         }
     }
     __syncthreads();
-    if (threadIdx.x == 0 && dm.fused && s_lane_ok) {
+    if (threadIdx.x == 0 && fused && s_lane_ok) {
         sc.plan[0] = -1;
         *sc.claim = (unsigned long long)dm.S;   // first 0, end S
         *sc.epoch += 1;
-    } else if (threadIdx.x == 0 && dm.fused) {
+    } else if (threadIdx.x == 0 && fused) {
         // Sessions in order, packed greedily into passes of at most n_wg
         // units (a session's units wait for each other row by row, so all of
         // them run in the same pass).  A session larger than a whole pass
@@ -219,8 +219,8 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
 }
 
 hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
-                         const uint16_t* new_k, const uint8_t* new_region, hipStream_t st) {
-    hipLaunchKernelGGL(k_append, dim3(dm.S), dim3(256), 0, st, dm, v, sc, new_k, new_region);
+                         const uint16_t* new_k, const uint8_t* new_region, int fused, hipStream_t st) {
+    hipLaunchKernelGGL(k_append, dim3(dm.S), dim3(256), 0, st, dm, v, sc, new_k, new_region, fused);
     return hipGetLastError();
 }
 
@@ -860,7 +860,7 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 size_t scratch_bytes(const Dims& dm) {
     size_t n = 0;
-    const size_t spill = dm.spill ? 1 : 0;   // the logits spill exists only when used
+    const size_t spill = dm.multi ? 1 : 0;   // the logits spill exists only when used
     n += align256(spill * dm.NP * dm.R * dm.P * sizeof(float));
     n += align256(spill * dm.S * dm.R * dm.max_chunks * sizeof(float2));
     n += align256((size_t)dm.S * dm.R * sizeof(float2));
@@ -883,7 +883,7 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
         p += align256(bytes);
         return r;
     };
-    const size_t spill = dm.spill ? 1 : 0;
+    const size_t spill = dm.multi ? 1 : 0;
     sc->logits = reinterpret_cast<float*>(take(spill * dm.NP * dm.R * dm.P * sizeof(float)));
     sc->cstats = reinterpret_cast<float2*>(take(spill * dm.S * dm.R * dm.max_chunks * sizeof(float2)));
     sc->rstats = reinterpret_cast<float2*>(take((size_t)dm.S * dm.R * sizeof(float2)));

@@ -1,0 +1,148 @@
+"""Summaries of rocprofv3 CSV output for the retention path's kernels.
+
+Two uses:
+
+* ``trace``: per-kernel launch counts and durations from a
+  ``rocprofv3 --kernel-trace --stats --output-format csv`` run, as a short
+  markdown table, with the steady-state average of the library's kernels
+  (their first ``--skip`` launches left out: md_init's residency check and
+  the warm-up steps).
+* ``pmc``: HBM bytes per launch of one kernel from two counter runs
+  (``--pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE``), each scaled by what the
+  same counter reads for a plain device copy of known size.  Writes the JSON
+  file bench.py reads as ``roofline.traffic`` (tied to a hash of the kernel
+  source it was taken on) and prints a markdown summary.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+import statistics
+from collections import defaultdict
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(PKG, "csrc")
+KERNEL_SOURCES = {"k_attend": "md_attend.hip", "k_logits": "md_kernels.hip"}
+
+
+def source_hash(kernel: str) -> str:
+    with open(os.path.join(CSRC, KERNEL_SOURCES[kernel]), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def short_name(name: str) -> str:
+    n = name.replace("(anonymous namespace)::", "")
+    for p in ("void ", "md::"):
+        if n.startswith(p):
+            n = n[len(p):]
+    return n.split("(")[0].strip()
+
+
+def _one(pattern: str) -> str:
+    hits = sorted(glob.glob(pattern))
+    if not hits:
+        raise FileNotFoundError(pattern)
+    return hits[0]
+
+
+def trace_table(trace_dir: str, skip: int):
+    """Rows (kernel, launches, avg us, total us, steady avg us) from a kernel trace."""
+    rows = list(csv.DictReader(open(_one(os.path.join(trace_dir, "*kernel_trace.csv")))))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    durs = defaultdict(list)
+    for r in rows:
+        durs[r["Kernel_Name"]].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    out = []
+    for name, d in durs.items():
+        steady = d[skip:] if ("md::" in name and len(d) > skip) else d
+        out.append((short_name(name)[:60], len(d), sum(d) / len(d), sum(d), sum(steady) / len(steady),
+                    len(steady)))
+    out.sort(key=lambda x: -x[3])
+    return out
+
+
+def counter_values(pmc_dir: str, counter: str):
+    """{kernel name: [value per dispatch in dispatch order]} for one counter."""
+    rows = list(csv.DictReader(open(_one(os.path.join(pmc_dir, "*counter_collection.csv")))))
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    vals = defaultdict(list)
+    for r in rows:
+        if r["Counter_Name"] == counter:
+            vals[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+    return vals
+
+
+def copy_factor(pmc_dir: str, counter: str, copy_bytes: int) -> float:
+    """Bytes per counter unit, from the device copies of ``copy_bytes``."""
+    vals = counter_values(pmc_dir, counter)
+    cand = [v for k, v in vals.items() if "copyBuffer" in k]
+    if not cand:
+        raise RuntimeError(f"no copy kernel in {pmc_dir}")
+    med = statistics.median(cand[0])
+    return copy_bytes / med
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    sub = ap.add_subparsers(dest="mode", required=True)
+    t = sub.add_parser("trace")
+    t.add_argument("trace_dir")
+    t.add_argument("--skip", type=int, default=3)
+    t.add_argument("--top", type=int, default=14)
+    p = sub.add_parser("pmc")
+    p.add_argument("fetch_dir")
+    p.add_argument("write_dir")
+    p.add_argument("cal_fetch_dir")
+    p.add_argument("cal_write_dir")
+    p.add_argument("--kernel", default="k_attend")
+    p.add_argument("--workload", required=True)
+    p.add_argument("--skip", type=int, default=3)
+    p.add_argument("--copy-mib", type=int, default=256)
+    p.add_argument("--algorithmic-bytes", type=float, default=None,
+                   help="algorithmic bytes per launch, for the ratio")
+    p.add_argument("--json", required=True)
+    a = ap.parse_args()
+
+    if a.mode == "trace":
+        print("| kernel | launches | avg us | total us | steady avg us (launches) |")
+        print("|---|---:|---:|---:|---:|")
+        for name, n, avg, tot, st, ns in trace_table(a.trace_dir, a.skip)[:a.top]:
+            print(f"| `{name}` | {n} | {avg:.2f} | {tot:.1f} | {st:.2f} ({ns}) |")
+        return
+
+    nbytes = a.copy_mib << 20
+    ff = copy_factor(a.cal_fetch_dir, "FETCH_SIZE", nbytes)
+    fw = copy_factor(a.cal_write_dir, "WRITE_SIZE", nbytes)
+    fetch = counter_values(a.fetch_dir, "FETCH_SIZE")
+    write = counter_values(a.write_dir, "WRITE_SIZE")
+    key = [k for k in fetch if short_name(k).startswith(a.kernel)]
+    if not key:
+        raise RuntimeError(f"{a.kernel} not in {a.fetch_dir}")
+    kf = fetch[key[0]][a.skip:]
+    kw = write[[k for k in write if short_name(k).startswith(a.kernel)][0]][a.skip:]
+    rd = statistics.mean(kf) * ff
+    wr = statistics.mean(kw) * fw
+    rec = {"kernel": a.kernel, "workload": a.workload, "kernel_source_sha256_16": source_hash(a.kernel),
+           "launches": len(kf), "fetch_bytes_per_launch": rd, "write_bytes_per_launch": wr,
+           "hbm_bytes_per_launch": rd + wr, "fetch_bytes_per_counter_unit": ff,
+           "write_bytes_per_counter_unit": fw, "copy_bytes": nbytes}
+    if a.algorithmic_bytes:
+        rec["algorithmic_bytes_per_launch"] = a.algorithmic_bytes
+        rec["traffic_over_algorithmic"] = (rd + wr) / a.algorithmic_bytes
+    with open(a.json, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(f"| {a.kernel} on {a.workload} | per launch (mean of {len(kf)} steady launches) |")
+    print("|---|---:|")
+    print(f"| HBM read (FETCH_SIZE x {ff:.4g} B) | {rd / 1e9:.4f} GB |")
+    print(f"| HBM write (WRITE_SIZE x {fw:.4g} B) | {wr / 1e9:.4f} GB |")
+    if a.algorithmic_bytes:
+        print(f"| algorithmic bytes | {a.algorithmic_bytes / 1e9:.4f} GB |")
+        print(f"| traffic / algorithmic | {(rd + wr) / a.algorithmic_bytes:.3f} |")
+
+
+if __name__ == "__main__":
+    main()

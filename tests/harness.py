@@ -93,7 +93,7 @@ class Pair:
                  oracle_sessions: Optional[List[int]] = None, n0s=None, budgets=None,
                  regions=None, planted: int = 0, planted_strength=3.0, query_gain=0.0,
                  pinned_mask=None, alpha=None, n_phys_extra: int = 0, max_pages=None,
-                 steps=None, fused: bool = True):
+                 steps=None, fused: Optional[bool] = True):
         self.w = w
         self.dev = torch.device(device)
         self.backend = backend

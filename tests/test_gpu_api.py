@@ -118,7 +118,7 @@ def test_state_lives_in_caller_buffers():
     p.md.close()
     from paper_2607_10582_amd.cache import MemDecay
     p.md = MemDecay(p.cache, torch.from_numpy(p.b), torch.from_numpy(p.lam), rho=0.9,
-                    alpha=1.0, tau_scale=2.0, pinned_mask=1)
+                    alpha=1.0, tau_scale=2.0, pinned_mask=1, fused=True)   # the Pair's path
     p.k = 4
     for i in range(4):
         p.step(compare=False)

@@ -242,3 +242,18 @@ def test_selection_on_scores_of_the_fused_kernel():
     assert np.array_equal(nt1, nt2) and np.array_equal(np1, np2)
     for x, y in zip(ser1, ser2):
         assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("name,steady_fused", [("qwen15_1700", False), ("long32k", True)])
+def test_library_picks_the_path(name, steady_fused):
+    # Without a path flag the library runs the multi-kernel path for small
+    # caches and the fused kernel for large ones; either way the steps match
+    # the oracle.
+    w = C.get(name)
+    big = w.name == "long32k"
+    p = Pair(w, fused=None, backend="torch" if big else "numpy",
+             oracle_sessions=[3] if big else None, steps=4 if big else 12)
+    cfg = p.md.kernel_config()
+    say(f"[{name}] kernel config {cfg}")
+    assert cfg["steady_fused"] == steady_fused
+    run_pair(p, 3 if big else 12, f"{name}-auto")
