@@ -85,6 +85,10 @@ enum {
 #define MD_FLAG_NO_FUSED  0x1   /* observe every session with the multi-kernel  */
                                 /* path (logits through HBM) instead of the     */
                                 /* fused one; results agree to rounding         */
+#define MD_FLAG_NORM_ATTENTION 0x4  /* score the attention term against the */
+                                /* uniform attention level, as Sec. IV-D        */
+                                /* proposes: alpha * |K_t| * a_i in Eq. 4, with */
+                                /* |K_t| the session's tokens after the append  */
 #define MD_FLAG_FUSED     0x2   /* observe on the fused kernel whenever it can  */
                                 /* hold the sessions.  With neither flag,       */
                                 /* md_init picks the path of the first observe  */

@@ -38,7 +38,12 @@ design notes of the repository):
   * |p| in the page mean is the number of live members;
   * ties in S_p go to the smaller serial (the older page first);
   * if the pinned tokens alone exceed B, every unpinned page is evicted and
-    the session is flagged infeasible.
+    the session is flagged infeasible;
+  * optional magnitude-normalised attention term (the change Sec. IV-D
+    names, measured against the uniform attention level 1/|K_t|): the score
+    uses alpha * |K_t| * a_i in place of alpha * a_i, |K_t| being the same
+    count as in tau.  The slower usage memory named with it is the EWMA rate
+    rho taken closer to 1; it needs no change here.
 """
 from __future__ import annotations
 
@@ -97,7 +102,8 @@ class Session:
                  clock: int, region, keys_bits, t_ins=None, t_ref=None, a=None,
                  page_sizes: Optional[Sequence[int]] = None,
                  page_serials: Optional[Sequence[int]] = None,
-                 next_serial: Optional[int] = None, capacity: Optional[int] = None):
+                 next_serial: Optional[int] = None, capacity: Optional[int] = None,
+                 attention_norm: bool = False):
         if Hq % Hkv:
             raise ValueError("query heads must be a multiple of KV heads")
         self.L, self.Hq, self.Hkv, self.d, self.P = L, Hq, Hkv, d, P
@@ -106,6 +112,7 @@ class Session:
         self.lam = np.asarray(lam, dtype=np.float64)
         self.alpha, self.rho, self.tau_scale = float(alpha), float(rho), float(tau_scale)
         self.pinned_mask = int(pinned_mask)
+        self.attention_norm = bool(attention_norm)
         self.budget = int(budget)
         self.t = int(clock)
 
@@ -224,10 +231,13 @@ class Session:
         tau = self.tau_scale / n
         refreshed = live[abar >= tau]
         self.t_ref[refreshed] = t
-        # O6: retention score (Eq. 4); pinned tokens bypass scoring.
+        # O6: retention score (Eq. 4); pinned tokens bypass scoring.  With the
+        # normalised attention term, a_i is measured in units of the uniform
+        # attention level 1/n (Sec. IV-D).
         r = self.region[live]
         dt = (t - self.t_ref[live]).astype(np.float64)
-        score = self.b[r] * np.exp(-self.lam[r] * dt) + self.alpha * self.a[live]
+        weight = self.alpha * n if self.attention_norm else self.alpha
+        score = self.b[r] * np.exp(-self.lam[r] * dt) + weight * self.a[live]
         pinned_tok = self.is_pinned_region(r)
         score = np.where(pinned_tok, np.inf, score)
         # O7: page score (Eq. 5), mean over the page's live members.
@@ -280,7 +290,8 @@ def select_pages(page_score, serials, sizes, pinned, n: int, budget: int):
 
 
 def session_from_workload(w, session: int, *, region, keys_bits, b, lam, budget,
-                          alpha=None, rho=None, tau_scale=None, capacity=None) -> Session:
+                          alpha=None, rho=None, tau_scale=None, capacity=None,
+                          attention_norm=None) -> Session:
     """A session at the start of decoding: prefix token i has t_ins = t_ref = i,
     importance 0, and the clock stands at n0 (so decode step k runs at
     t = n0 + k)."""
@@ -291,4 +302,5 @@ def session_from_workload(w, session: int, *, region, keys_bits, b, lam, budget,
                    tau_scale=w.tau_scale if tau_scale is None else tau_scale,
                    pinned_mask=w.pinned_mask, budget=budget, clock=n0,
                    region=region, keys_bits=keys_bits,
-                   capacity=capacity if capacity is not None else n0 + w.steps)
+                   capacity=capacity if capacity is not None else n0 + w.steps,
+                   attention_norm=w.attention_norm if attention_norm is None else attention_norm)

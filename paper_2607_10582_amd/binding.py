@@ -27,6 +27,7 @@ MD_DEV_TIMEOUT = 0x10
 
 MD_FLAG_NO_FUSED = 0x1
 MD_FLAG_FUSED = 0x2
+MD_FLAG_NORM_ATTENTION = 0x4
 
 EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_observe_step",
            "md_score_pages", "md_select_evict", "md_compact", "md_read_device_status",

@@ -105,7 +105,7 @@ class MemDecay:
     def __init__(self, cache: PagedCache, base_priority: torch.Tensor, decay_rate: torch.Tensor, *,
                  rho: float, alpha: float, tau_scale: float, pinned_mask: int,
                  n_regions: int = 7, stream: Optional[torch.cuda.Stream] = None,
-                 fused: Optional[bool] = None):
+                 fused: Optional[bool] = None, attention_norm: bool = False):
         # fused: True = always the fused kernel, False = always the
         # multi-kernel path, None = the library picks from the cache's sizes
         self.cache = cache
@@ -117,7 +117,8 @@ class MemDecay:
                           max_pages=cache.max_pages, n_phys_pages=cache.n_phys,
                           n_regions=n_regions, pinned_region_mask=pinned_mask, rho=rho,
                           alpha=alpha, tau_scale=tau_scale,
-                          flags=0 if fused is None else (B.MD_FLAG_FUSED if fused else B.MD_FLAG_NO_FUSED))
+                          flags=(0 if fused is None else (B.MD_FLAG_FUSED if fused else B.MD_FLAG_NO_FUSED))
+                          | (B.MD_FLAG_NORM_ATTENTION if attention_norm else 0))
         rp = B.md_region_params(base_priority=self.b.data_ptr(), decay_rate=self.lam.data_ptr())
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
         self._cfg, self._rp, self._cv = cfg, rp, cache.view()

@@ -106,7 +106,7 @@ const char* md_status_str(md_status s) {
 
 static md_status validate_config(const md_config* c) {
     if (c == nullptr) return MD_E_INVALID;
-    if ((c->flags & ~(MD_FLAG_NO_FUSED | MD_FLAG_FUSED)) != 0) return MD_E_INVALID;
+    if ((c->flags & ~(MD_FLAG_NO_FUSED | MD_FLAG_FUSED | MD_FLAG_NORM_ATTENTION)) != 0) return MD_E_INVALID;
     if ((c->flags & MD_FLAG_NO_FUSED) && (c->flags & MD_FLAG_FUSED)) return MD_E_INVALID;
     if (c->n_layers < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1) return MD_E_INVALID;
     if (c->n_q_heads % c->n_kv_heads != 0) return MD_E_INVALID;
@@ -174,6 +174,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     dm.alpha = cfg->alpha;
     dm.tau_scale = cfg->tau_scale;
     dm.fused = (cfg->flags & MD_FLAG_NO_FUSED) ? 0 : 1;
+    dm.norm_attn = (cfg->flags & MD_FLAG_NORM_ATTENTION) ? 1 : 0;
 
     // ---- from here on the HIP runtime is used
     int dev = 0;

@@ -49,7 +49,7 @@ namespace {
 
 struct AttendDims {
     int L, Hq, Hkv, G, P, Pshift, MP, NP, R, LHkv;
-    int wg_per_cu, n_cu, S, n_regions;
+    int wg_per_cu, n_cu, S, n_regions, norm_attn;
     uint32_t pin_mask;
     float rho, tau_scale, alpha;
 };
@@ -563,6 +563,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // start at multiples of 64 tokens.
     const int t_now = a.clock[un.s];
     const size_t rbase = (size_t)un.s * dm.n_regions;
+    const float aw = attention_weight(dm.alpha, dm.norm_attn, un.nt_s);
 #pragma unroll
     for (int k = 0; k < kTok; ++k) {
         const int lt = lane + 64 * k;   // wave-local token
@@ -590,7 +591,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
                 r = dm.n_regions - 1;
             }
             pin = (dm.pin_mask >> r) & 1u;
-            sc = pin ? INFINITY : retention_score(a.b[rbase + r], a.lam[rbase + r], t_now, tr, dm.alpha, an);
+            sc = pin ? INFINITY : retention_score(a.b[rbase + r], a.lam[rbase + r], t_now, tr, aw, an);
         }
         float ps;
         const bool has = page_score_of(sc, live, pin, dm.P, &ps);
@@ -793,7 +794,7 @@ const void* attend_kernel(int G) {
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q, float* abar_out,
                          hipStream_t st) {
     AttendDims ad{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.MP, dm.NP, dm.R, dm.LHkv,
-                  dm.wg_per_cu, dm.n_wg / dm.wg_per_cu, dm.S, dm.n_regions, dm.pin_mask,
+                  dm.wg_per_cu, dm.n_wg / dm.wg_per_cu, dm.S, dm.n_regions, dm.norm_attn, dm.pin_mask,
                   dm.rho, dm.tau_scale, dm.alpha};
     AttendArgs aa{v.k_pool, v.page_table, v.n_tokens, v.clock, v.region, v.b, v.lam, v.imp, v.t_ref,
                   sc.pscore, q, abar_out, sc.ustart, sc.plan, sc.epoch, sc.claim, sc.lane_box, sc.ustat,

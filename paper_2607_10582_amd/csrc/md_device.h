@@ -120,6 +120,12 @@ __device__ __forceinline__ bool page_score_of(float score, bool live, bool pinne
     return cnt > 0;
 }
 
+// Weight of the attention term of Eq. 4: alpha, or alpha * |K_t| when the
+// term is measured against the uniform attention level 1/|K_t|.
+__device__ __forceinline__ float attention_weight(float alpha, int norm, int n_tokens) {
+    return norm ? alpha * (float)n_tokens : alpha;
+}
+
 // Wave-uniform value kept in a scalar register.
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 

@@ -33,6 +33,7 @@ struct Dims {
     int fused;     // 1: sessions that fit one pass run on k_attend
     int spill;     // 1: some session may not fit a pass (the spill kernels run)
     int multi;     // 1: the multi-kernel path runs at some step (its scratch exists)
+    int norm_attn; // 1: the attention term of Eq. 4 is alpha * |K_t| * a_i
     int n_wg;      // k_attend workgroups (all co-resident)
     int wg_per_cu; // k_attend workgroups per CU (n_wg = wg_per_cu * CUs)
     int lane_cap;  // units one lane of k_attend workgroups holds (one workgroup per CU)

@@ -612,7 +612,8 @@ __global__ void __launch_bounds__(256) k_score(Dims dm, View v, Scratch sc, floa
                     sc_i = INFINITY;
                 } else {
                     const size_t ri = (size_t)s * dm.n_regions + r;
-                    sc_i = retention_score(v.b[ri], v.lam[ri], t, v.t_ref[si], dm.alpha, v.imp[si]);
+                    sc_i = retention_score(v.b[ri], v.lam[ri], t, v.t_ref[si],
+                                           attention_weight(dm.alpha, dm.norm_attn, nt), v.imp[si]);
                 }
                 if (token_score != nullptr) token_score[si] = sc_i;
             }

@@ -61,6 +61,7 @@ class Workload:
     tau_scale: float = 2.0     # tau = tau_scale / |K_t|
     pinned_mask: int = 1 << SYSTEM
     halflife_jitter: Optional[Tuple[float, float]] = None
+    attention_norm: bool = False   # score's attention term relative to the uniform level
     b_range: Tuple[float, float] = (0.2, 1.0)
     extra: dict = field(default_factory=dict)
 

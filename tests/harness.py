@@ -145,11 +145,11 @@ class Pair:
                     alpha=f32(self.alpha), rho=f32(w.rho), tau_scale=f32(w.tau_scale),
                     pinned_mask=self.pinned_mask, budget=int(self.B[s]), clock=n0, region=reg,
                     keys_bits=kb if n0 else np.zeros((0, w.L, w.Hkv, w.d), np.uint16),
-                    capacity=n0 + self.steps)
+                    capacity=n0 + self.steps, attention_norm=w.attention_norm)
         self.cache.set_free_pages(perm[pos:][::-1])
         self.md = MemDecay(self.cache, torch.from_numpy(self.b), torch.from_numpy(self.lam),
                            rho=f32(w.rho), alpha=f32(self.alpha), tau_scale=f32(w.tau_scale),
-                           pinned_mask=self.pinned_mask, fused=fused)
+                           pinned_mask=self.pinned_mask, fused=fused, attention_norm=w.attention_norm)
         n_slots = n_phys * P
         self.abar = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
         self.tscore = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)

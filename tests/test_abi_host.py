@@ -113,7 +113,7 @@ def fake_rp():
     (dict(alpha=-1.0), B.MD_E_INVALID),
     (dict(alpha=float("inf")), B.MD_E_INVALID),
     (dict(tau_scale=-2.0), B.MD_E_INVALID),
-    (dict(flags=4), B.MD_E_INVALID),
+    (dict(flags=8), B.MD_E_INVALID),
     (dict(flags=3), B.MD_E_INVALID),
 ])
 def test_init_rejects_bad_configs_on_the_host(lib, kw, expect):

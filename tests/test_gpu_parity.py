@@ -257,3 +257,19 @@ def test_library_picks_the_path(name, steady_fused):
     say(f"[{name}] kernel config {cfg}")
     assert cfg["steady_fused"] == steady_fused
     run_pair(p, 3 if big else 12, f"{name}-auto")
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_normalised_attention_term(fused):
+    # The score's attention term measured against the uniform attention level
+    # (alpha * |K_t| * a_i, Sec. IV-D), on both observation paths; planted
+    # keys give some tokens attention well above uniform.
+    w = C.with_overrides(C.get("small"), attention_norm=True)
+    p = Pair(w, planted=48, planted_strength=3.0, query_gain=1.0, fused=fused)
+    st = run_pair(p, w.steps, f"norm-attention-fused{int(fused)}")
+    assert st.evicted_pages > 10
+
+
+def test_normalised_attention_term_batch():
+    w = C.with_overrides(C.get("qwen3_32x1700"), S=8, attention_norm=True)
+    run_pair(Pair(w, steps=10), 10, "norm-attention-qwen3x8")

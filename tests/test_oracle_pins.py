@@ -25,7 +25,7 @@ def bf16(x):
 
 def make_session(keys, *, L=1, Hq=1, Hkv=1, P=16, region=None, b=None, lam=None,
                  alpha=0.0, rho=0.9, tau_scale=2.0, pinned_mask=0, budget=10**9,
-                 clock=0, t_ins=None, page_sizes=None):
+                 clock=0, t_ins=None, page_sizes=None, attention_norm=False):
     keys = np.asarray(keys, dtype=np.float32)
     n = keys.shape[0]
     d = keys.shape[-1]
@@ -38,7 +38,7 @@ def make_session(keys, *, L=1, Hq=1, Hkv=1, P=16, region=None, b=None, lam=None,
                    budget=budget, clock=clock, region=region,
                    keys_bits=bf16(keys.reshape(n, L, Hkv, d)),
                    t_ins=np.zeros(n, np.int64) if t_ins is None else t_ins,
-                   page_sizes=page_sizes)
+                   page_sizes=page_sizes, attention_norm=attention_norm)
 
 
 # ----------------------------------------------------------- O2/O3 attention
@@ -375,3 +375,40 @@ def test_refresh_at_exactly_tau(n_planted, n):
     rec = s.step(q)
     assert rec.abar[0] == rec.tau == 2.0 / n
     assert np.all(rec.t_ref[:n_planted] == 4) and np.all(rec.t_ref[n_planted:] == 0)
+
+
+# ------------------------------------- normalised attention term (Sec. IV-D)
+
+@pytest.mark.parametrize("n", [12, 300])
+@pytest.mark.parametrize("m,factor", [(1, 0.1), (10, 0.6513215599)])
+def test_normalised_term_at_uniform_attention_is_independent_of_cache_size(n, m, factor):
+    # Sec. IV-D proposes measuring the attention term against the uniform
+    # attention level.  Equal keys give every token the uniform mass 1/n, so
+    # from a = 0 the EWMA gives (1 - rho^m)/n (Eq. 2) and the normalised term
+    # is alpha (1 - rho^m) whatever the cache size; the plain term shrinks
+    # as 1/n.
+    d = 128
+    b = np.full(NREG, 0.25)
+    for norm, expect in ((True, 0.25 + 1.5 * factor), (False, 0.25 + 1.5 * factor / n)):
+        s = make_session(np.zeros((n, d), np.float32), b=b, lam=np.zeros(NREG), alpha=1.5,
+                         rho=0.9, attention_norm=norm)
+        q = np.zeros((1, 1, d), np.float32)
+        for _ in range(m):
+            rec = s.step(q)
+        np.testing.assert_allclose(rec.score, expect, rtol=1e-9)
+
+
+def test_normalised_term_of_a_new_token_follows_the_cache_size_at_its_step():
+    # A token appended when the cache holds n tokens gets a = (1 - rho)/n at
+    # once (its own observation, Eq. 2); the normalised term is then
+    # alpha (1 - rho), for n = 10 and again for n = 11 one step later.
+    d = 128
+    s = make_session(np.zeros((9, d), np.float32), b=np.zeros(NREG), lam=np.zeros(NREG),
+                     alpha=2.0, rho=0.75, attention_norm=True)
+    q = np.zeros((1, 1, d), np.float32)
+    rec = s.step(q, bf16(np.zeros(d)), 3)
+    assert rec.n == 10 and rec.score[-1] == pytest.approx(2.0 * 0.25, rel=1e-14)
+    rec = s.step(q, bf16(np.zeros(d)), 3)
+    assert rec.n == 11 and rec.score[-1] == pytest.approx(2.0 * 0.25, rel=1e-14)
+    # the token added a step earlier: a = 0.75 * 0.25/10 + 0.25/11, measured in 1/11
+    assert rec.score[-2] == pytest.approx(2.0 * 11 * (0.75 * 0.25 / 10 + 0.25 / 11), rel=1e-13)
