@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define MD_ABI_VERSION 1
+#define MD_ABI_VERSION 2
 
 typedef int32_t md_status;
 
@@ -113,6 +113,9 @@ typedef struct md_config {
     float alpha;                /* attention weight, alpha >= 0 (Eq. 4)           */
     float tau_scale;            /* tau = tau_scale / |K_t| (Eq. 3's scaled form)  */
     int32_t flags;              /* MD_FLAG_* bits; other bits must be 0           */
+    int32_t window;             /* W >= 1 decode queries per observation, with    */
+                                /* (Hq/Hkv) W <= 16 and L Hq W <= 1024; W > 1     */
+                                /* runs on the multi-kernel path (Sec. III-C)     */
 } md_config;
 
 /* Region priors (Sec. III-B): b_r >= 0 and lambda_r >= 0 per session and
@@ -160,19 +163,27 @@ md_status md_init(const md_config* cfg, const md_region_params* rp,
                   const md_cache_view* cv, void* stream, md_handle* out);
 
 /*
- * md_observe_step — one observation step (Alg. 1, first two lines, with one
- * observation per decode step and a window of one query):
+ * md_observe_step — one decode step; with q given, also an observation step
+ * (Alg. 1, first two lines; attention is sampled every k-th decode step with
+ * a window of the W latest decode queries, Sec. III-C):
  *   append: each session's clock advances, t <- t + 1.  If new_k is not NULL
  *     the step's token joins the session's last page, or a page popped from
  *     the free list when the last page is full, with region new_region[s],
  *     t_ins = t_ref = t, a = 0 (Fig. 1, the decode engine's append).
- *   attention mass: for every cached token i, A_i = (1 / (L Hq)) sum over
- *     layers l and query heads h of softmax_i(q_{l,h} . k_{l,h/G,i} / sqrt(d)),
- *     the softmax running over the session's cached tokens (Sec. III-C).
+ *   attention mass: for every cached token i, A_i = (1 / (L Hq W)) sum over
+ *     layers l, query heads h and window queries w of
+ *     softmax_i(q_{w,l,h} . k_{l,h/G,i} / sqrt(d)), the softmax of window
+ *     query w running over the session's cached tokens inserted at or
+ *     before its step t - (W - 1 - w) (Sec. III-C).  With W = 1: every
+ *     cached token.
  *   EWMA (Eq. 2): a_i <- rho a_i + (1 - rho) A_i for every cached token.
  *   refresh (Eq. 3): t_ref_i <- t when A_i >= tau_scale / |K_t|, |K_t| the
  *     session's token count after the append.
- * q:          float32 [S][L][Hq][d] decode queries (device).
+ * q:          float32 [S][W][L][Hq][d] decode queries of steps t - W + 1 .. t,
+ *             oldest first (device), or NULL for a decode step without an
+ *             observation: then only the append and the clock advance run,
+ *             and md_score_pages, md_select_evict and md_compact answer
+ *             MD_E_STATE until the next observation.
  * new_k:      bf16 bits [S][L][Hkv][d] keys of the appended tokens, or NULL.
  * new_region: uint8 [S] region codes of the appended tokens; required with new_k.
  * abar_out:   optional float32 [NP][P]; receives A_i at each live slot.

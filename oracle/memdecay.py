@@ -26,7 +26,14 @@ steps in the paper's order:
 
 Readings where the paper leaves a choice (listed with their reasons in the
 design notes of the repository):
-  * one observation per decode step and a window of one query (k = 1, W = 1);
+  * observation steps and window (Sec. III-C): the caller decides which
+    decode steps observe (every k-th one in the workloads; k = 1 is the
+    study's setting); a step without an observation only appends.  At an
+    observation step the window is the decode queries of the W most recent
+    steps, this one last; each attends to the tokens cached now whose
+    insertion step is no later than its own, and A_i averages over layers,
+    query heads and window queries alike (W = 1 is the study's setting);
+    eviction runs at observation steps only (Alg. 1 runs per observation);
   * the mass averages over all L*Hq query heads; query head h reads KV head
     h // (Hq/Hkv); scale 1/sqrt(d); no mask over the cached tokens; the new
     token attends to itself;
@@ -193,23 +200,32 @@ class Session:
             self.next_serial += 1
 
     def attention_mass(self, q, live: np.ndarray) -> np.ndarray:
-        """A_i: softmax attention of the decode query, averaged over the L*Hq
-        query heads (Sec. III-C, window of one query)."""
-        q = np.asarray(q, dtype=np.float32).astype(np.float64).reshape(self.L, self.Hq, self.d)
+        """A_i: softmax attention of the window's decode queries, averaged
+        over the L*Hq query heads and the W window queries (Sec. III-C).
+        q is [W][L][Hq][d] (or [L][Hq][d] for W = 1), oldest query first;
+        window query w belongs to step t - (W - 1 - w) and sees only the
+        tokens inserted at or before that step."""
+        q = np.asarray(q, dtype=np.float32).astype(np.float64).reshape(-1, self.L, self.Hq, self.d)
+        W = q.shape[0]
         n = live.shape[0]
         mass = np.zeros(n, dtype=np.float64)
         inv_sqrt_d = 1.0 / math.sqrt(self.d)
-        for l in range(self.L):
-            for kv in range(self.Hkv):
-                k = self.keys[l, kv][live].astype(np.float64)          # [n][d]
-                heads = range(kv * self.G, (kv + 1) * self.G)
-                x = (k @ q[l, kv * self.G:(kv + 1) * self.G].T) * inv_sqrt_d   # [n][G]
-                for j, h in enumerate(heads):
-                    mass += softmax(x[:, j])
-        return mass / (self.L * self.Hq)
+        for w in range(W):
+            seen = self.t_ins[live] <= self.t - (W - 1 - w)
+            if not np.any(seen):
+                continue
+            for l in range(self.L):
+                for kv in range(self.Hkv):
+                    k = self.keys[l, kv][live[seen]].astype(np.float64)       # [n_seen][d]
+                    x = (k @ q[w, l, kv * self.G:(kv + 1) * self.G].T) * inv_sqrt_d   # [n_seen][G]
+                    for j in range(self.G):
+                        mass[seen] += softmax(x[:, j])
+        return mass / (self.L * self.Hq * W)
 
     def step(self, q, new_key_bits=None, new_region: Optional[int] = None) -> StepRecord:
-        """One observation step at the next clock value (Alg. 1)."""
+        """One decode step at the next clock value: the append, then, when q
+        is given, the observation and eviction of Alg. 1.  Without q the step
+        only appends (the record then holds the counts and empty arrays)."""
         self.t += 1
         t = self.t
         if new_key_bits is not None:
@@ -218,6 +234,10 @@ class Session:
         n = live.shape[0]
         m = len(self.pages)
         empty = np.zeros(0)
+        if q is None:
+            return StepRecord(t, n, math.inf, np.zeros(0, np.int64), np.zeros(0, np.int64),
+                              np.zeros(0, bool), empty, empty, empty, np.zeros(0, np.int64),
+                              np.zeros(0, np.int64), empty, np.zeros(0, np.int64), n, n > self.budget)
         if n == 0:
             return StepRecord(t, 0, math.inf, np.zeros(0, np.int64), np.zeros(0, np.int64),
                               np.zeros(0, bool), empty, empty, empty, np.zeros(0, np.int64),

@@ -47,7 +47,7 @@ class md_config(ctypes.Structure):
                 ("max_pages", ctypes.c_int32), ("n_phys_pages", ctypes.c_int32),
                 ("n_regions", ctypes.c_int32), ("pinned_region_mask", ctypes.c_uint32),
                 ("rho", ctypes.c_float), ("alpha", ctypes.c_float),
-                ("tau_scale", ctypes.c_float), ("flags", ctypes.c_int32)]
+                ("tau_scale", ctypes.c_float), ("flags", ctypes.c_int32), ("window", ctypes.c_int32)]
 
 
 class md_region_params(ctypes.Structure):

@@ -105,7 +105,7 @@ class MemDecay:
     def __init__(self, cache: PagedCache, base_priority: torch.Tensor, decay_rate: torch.Tensor, *,
                  rho: float, alpha: float, tau_scale: float, pinned_mask: int,
                  n_regions: int = 7, stream: Optional[torch.cuda.Stream] = None,
-                 fused: Optional[bool] = None, attention_norm: bool = False):
+                 fused: Optional[bool] = None, attention_norm: bool = False, window: int = 1):
         # fused: True = always the fused kernel, False = always the
         # multi-kernel path, None = the library picks from the cache's sizes
         self.cache = cache
@@ -118,7 +118,8 @@ class MemDecay:
                           n_regions=n_regions, pinned_region_mask=pinned_mask, rho=rho,
                           alpha=alpha, tau_scale=tau_scale,
                           flags=(0 if fused is None else (B.MD_FLAG_FUSED if fused else B.MD_FLAG_NO_FUSED))
-                          | (B.MD_FLAG_NORM_ATTENTION if attention_norm else 0))
+                          | (B.MD_FLAG_NORM_ATTENTION if attention_norm else 0),
+                          window=window)
         rp = B.md_region_params(base_priority=self.b.data_ptr(), decay_rate=self.lam.data_ptr())
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
         self._cfg, self._rp, self._cv = cfg, rp, cache.view()
@@ -132,7 +133,7 @@ class MemDecay:
     # ---- the four calls of one step
     def observe(self, step: int, q: torch.Tensor, new_k: Optional[torch.Tensor] = None,
                 new_region: Optional[torch.Tensor] = None, abar_out: Optional[torch.Tensor] = None):
-        B.md_observe_step(self.handle, step, _ptr(q, torch.float32),
+        B.md_observe_step(self.handle, step, None if q is None else _ptr(q, torch.float32),
                           None if new_k is None else _ptr(new_k, torch.bfloat16),
                           None if new_region is None else _ptr(new_region, torch.uint8),
                           None if abar_out is None else _ptr(abar_out, torch.float32))

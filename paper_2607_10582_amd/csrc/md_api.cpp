@@ -116,7 +116,11 @@ static md_status validate_config(const md_config* c) {
     if (!(c->rho >= 0.0f && c->rho < 1.0f)) return MD_E_INVALID;
     if (!(c->alpha >= 0.0f) || !isfinite(c->alpha)) return MD_E_INVALID;
     if (!(c->tau_scale >= 0.0f) || !isfinite(c->tau_scale)) return MD_E_INVALID;
+    if (c->window < 1) return MD_E_INVALID;
+    if ((c->flags & MD_FLAG_FUSED) && c->window > 1) return MD_E_UNSUPPORTED;
     if (c->head_dim != md::kHeadDim) return MD_E_UNSUPPORTED;
+    if ((int64_t)(c->n_q_heads / c->n_kv_heads) * c->window > 16) return MD_E_UNSUPPORTED;
+    if ((int64_t)c->n_layers * c->n_q_heads * c->window > md::kMaxRows) return MD_E_UNSUPPORTED;
     if (c->page_size != 16 && c->page_size != 64) return MD_E_UNSUPPORTED;
     if (c->n_q_heads / c->n_kv_heads > 16) return MD_E_UNSUPPORTED;
     if ((int64_t)c->n_layers * c->n_q_heads > md::kMaxRows) return MD_E_UNSUPPORTED;
@@ -165,7 +169,8 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     dm.S = cfg->max_sessions;
     dm.MP = cfg->max_pages;
     dm.NP = cfg->n_phys_pages;
-    dm.R = dm.L * dm.Hq;
+    dm.W = cfg->window;
+    dm.R = dm.L * dm.Hq * dm.W;   // softmax rows: (layer, query head, window query)
     dm.LHkv = dm.L * dm.Hkv;
     dm.n_regions = cfg->n_regions;
     dm.max_chunks = (int)(((int64_t)dm.MP * dm.P + md::kChunk - 1) / md::kChunk);
@@ -173,7 +178,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     dm.rho = cfg->rho;
     dm.alpha = cfg->alpha;
     dm.tau_scale = cfg->tau_scale;
-    dm.fused = (cfg->flags & MD_FLAG_NO_FUSED) ? 0 : 1;
+    dm.fused = ((cfg->flags & MD_FLAG_NO_FUSED) || dm.W > 1) ? 0 : 1;
     dm.norm_attn = (cfg->flags & MD_FLAG_NORM_ATTENTION) ? 1 : 0;
 
     // ---- from here on the HIP runtime is used
@@ -323,14 +328,25 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
 
 md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint16_t* new_k,
                           const uint8_t* new_region, float* abar_out) {
-    if (h == nullptr || q == nullptr || !aligned(q, 16)) return MD_E_INVALID;
+    if (h == nullptr || (q != nullptr && !aligned(q, 16))) return MD_E_INVALID;
     if (new_k != nullptr && (new_region == nullptr || !aligned(new_k, 16))) return MD_E_INVALID;
     if (abar_out != nullptr && !aligned(abar_out, 4)) return MD_E_INVALID;
     if (h->have_step && step != h->last_step + 1) return MD_E_STEP;
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    if (q == nullptr) {
+        // a decode step without an observation: the append and the clock only
+        if (timed_launch(h, MD_K_APPEND, [&] {
+                return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, 0, 0, h->stream); }) !=
+            hipSuccess)
+            return MD_E_HIP;
+        h->have_step = true;
+        h->last_step = step;
+        h->phase = kNone;
+        return MD_OK;
+    }
     const bool fused = h->observed == 0 ? h->fused_first : h->fused_steady;
     hipError_t e = timed_launch(h, MD_K_APPEND, [&] {
-        return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, fused ? 1 : 0, h->stream); });
+        return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, fused ? 1 : 0, 1, h->stream); });
     // On a fused step, sessions that fit one pass of the fused kernel run
     // there; the others (only possible when a session may outgrow n_wg * T
     // tokens) take the three-kernel path with the logits in HBM, which on

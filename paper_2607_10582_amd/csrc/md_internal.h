@@ -30,6 +30,7 @@ constexpr int kDevCorrupt = MD_DEV_CORRUPT;
 
 struct Dims {
     int L, Hq, Hkv, G, P, Pshift, S, MP, NP, R, LHkv, n_regions, max_chunks;
+    int W;         // window: decode queries per observation (R = L * Hq * W)
     int fused;     // 1: sessions that fit one pass run on k_attend
     int spill;     // 1: some session may not fit a pass (the spill kernels run)
     int multi;     // 1: the multi-kernel path runs at some step (its scratch exists)
@@ -89,9 +90,11 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc);
 
 // Launchers; each returns the hipError_t of its launch.
 // fused: this step observes on the fused kernel (sessions that fit a pass)
-// or, when 0, every session on the multi-kernel path.
+// or, when 0, every session on the multi-kernel path.  observe: 0 for a
+// decode step without an observation (no work lists, no scored tokens).
 hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
-                         const uint16_t* new_k, const uint8_t* new_region, int fused, hipStream_t st);
+                         const uint16_t* new_k, const uint8_t* new_region, int fused, int observe,
+                         hipStream_t st);
 hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q,
                          int n_blocks, hipStream_t st);
 hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st);

@@ -27,7 +27,8 @@ namespace md {
 // step's work lists.
 __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                                                 const uint16_t* __restrict__ new_k,
-                                                const uint8_t* __restrict__ new_region, int fused) {
+                                                const uint8_t* __restrict__ new_region, int fused,
+                                                int observe) {
     const int s = blockIdx.x;
     __shared__ int sh_phys, sh_slot, sh_last;
     __shared__ int lds[17];
@@ -213,14 +214,17 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         sc.tile_prefix[dm.S] = tot_t;
         sc.score_prefix[dm.S] = tot_s;
         *sc.done = 0;
-        atomicAdd(&sc.counters[0], (unsigned long long)tot_n);
-        atomicAdd(&sc.counters[1], 1ull);
+        if (observe) {
+            atomicAdd(&sc.counters[0], (unsigned long long)tot_n);
+            atomicAdd(&sc.counters[1], 1ull);
+        }
     }
 }
 
 hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
-                         const uint16_t* new_k, const uint8_t* new_region, int fused, hipStream_t st) {
-    hipLaunchKernelGGL(k_append, dim3(dm.S), dim3(256), 0, st, dm, v, sc, new_k, new_region, fused);
+                         const uint16_t* new_k, const uint8_t* new_region, int fused, int observe,
+                         hipStream_t st) {
+    hipLaunchKernelGGL(k_append, dim3(dm.S), dim3(256), 0, st, dm, v, sc, new_k, new_region, fused, observe);
     return hipGetLastError();
 }
 
@@ -256,22 +260,24 @@ __device__ __forceinline__ void cursor_next(Cursor& cu, const int* s_pref, int S
 // What the logits kernel reads besides its pointers.
 struct LogitsDims {
     int L, Hq, Hkv, G, P, Pshift, S, MP, NP, R, LHkv, max_chunks;
+    int W, Gw;   // window queries per observation; MFMA columns G * W
 };
 
 // B operands of one row (session s, lkv = layer * Hkv + KV head) in
-// registers: lane column h = lane & 15 is query head kv * G + h (zero past
-// G); k-group g = lane >> 4 holds dims 32j + 8g .. +7; each float32 term is
-// split into hi, mid and lo bf16 terms.
+// registers: lane column c = lane & 15 is window query w = c / G, query head
+// kv * G + c % G (zero past G W); k-group g = lane >> 4 holds dims
+// 32j + 8g .. +7; each float32 term is split into hi, mid and lo bf16 terms.
 __device__ __forceinline__ void split_query_regs(u32x4 (&bq)[4][3], const float* __restrict__ q,
                                                  const LogitsDims& dm, int s, int lkv, int h, int g,
                                                  int32_t* status) {
     const int l = lkv / dm.Hkv, kv = lkv - l * dm.Hkv;
-    const float* qh = q + (((size_t)s * dm.L + l) * dm.Hq + kv * dm.G + h) * kHeadDim;
+    const int w = h / dm.G, hh = h - w * dm.G;
+    const float* qh = q + ((((size_t)s * dm.W + w) * dm.L + l) * dm.Hq + kv * dm.G + hh) * kHeadDim;
     bool bad = false;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         f32x4 u0 = f32x4{0.f, 0.f, 0.f, 0.f}, u1 = u0;
-        if (h < dm.G) {
+        if (h < dm.Gw) {
             const f32x4* p = reinterpret_cast<const f32x4*>(qh + 32 * j + 8 * g);
             u0 = p[0];
             u1 = p[1];
@@ -358,7 +364,8 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3))
 k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __restrict__ page_table,
          const int32_t* __restrict__ n_tokens, const float* __restrict__ q,
          float* __restrict__ logits, float2* __restrict__ cstats, int32_t* status,
-         const int32_t* __restrict__ item_prefix) {
+         const int32_t* __restrict__ item_prefix, const int32_t* __restrict__ t_ins,
+         const int32_t* __restrict__ clock) {
     __shared__ int s_pref[kMaxSessions + 1];
     const int S = dm.S;
     for (int i = threadIdx.x; i <= S; i += blockDim.x) s_pref[i] = item_prefix[i];
@@ -391,7 +398,12 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
         split_query_regs(bq, q, dm, cu.s, cu.lkv, h, g, status);
         const int l = uni(cu.lkv / dm.Hkv);
         const int kv = cu.lkv - l * dm.Hkv;
-        const int row0 = uni(l * dm.Hq + kv * dm.G);  // first logits row of the group
+        const int row0 = uni(cu.lkv * dm.Gw);   // first logits row of the group: (lkv, w, h)
+        // window query of this lane's column sees tokens inserted up to
+        // step t - (W - 1 - w) (W = 1: every token)
+        const int t_lim = dm.W > 1 ? clock[cu.s] - (dm.W - 1 - h / dm.G) : 0;
+        (void)l;
+        (void)kv;
         ItemTiles cur;
         item_tiles(cur, cu, dm, page_table, n_tokens, status, lane);
 #pragma unroll
@@ -425,13 +437,20 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
                 if (t < 4) load_tile(ring[t & 3], dm, k_pool, cur, t + 4, cu.lkv, voff);
                 else load_tile(ring[t & 3], dm, k_pool, nxt, t - 4, cu.lkv, voff);
 
-                // base-2 logits; tokens past the session's count are masked out
+                // base-2 logits; tokens past the session's count, and tokens
+                // newer than the column's window query, are masked out
                 const bool tvalid = cur.vmask & (1u << t);
+                int tins[4] = {0, 0, 0, 0};
+                if (dm.W > 1 && tvalid) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) tins[i] = t_ins[cur.slot0[t] + 4 * g + i];
+                }
                 float x[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int tok = tok0 + 16 * t + 4 * g + i;
-                    x[i] = (tvalid && tok < cur.nt) ? acc[i] * kLogitScale : -INFINITY;
+                    const bool seen = dm.W == 1 || tins[i] <= t_lim;
+                    x[i] = (tvalid && tok < cur.nt && seen) ? acc[i] * kLogitScale : -INFINITY;
                 }
                 const float mn = fmaxf(m, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
                 const bool live = mn != -INFINITY;
@@ -440,7 +459,7 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
                                    (hw_exp2(x[2] - ms) + hw_exp2(x[3] - ms));
                 lsum = live ? lsum * hw_exp2(m - ms) + part : lsum;
                 m = live ? mn : m;
-                if (tvalid && h < dm.G) {
+                if (tvalid && h < dm.Gw) {
                     const int slot = cur.slot0[t];
                     gbytes base = uni_ptr(logits + ((size_t)(slot >> dm.Pshift) * dm.R + row0) * dm.P +
                                           (slot & (dm.P - 1)));
@@ -458,7 +477,7 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
                 lsum = (M == -INFINITY) ? 0.0f : lsum * hw_exp2(m - M) + l2 * hw_exp2(m2 - M);
                 m = M;
             }
-            if (h < dm.G && g == 0)
+            if (h < dm.Gw && g == 0)
                 cstats[((size_t)cu.s * dm.R + row0 + h) * dm.max_chunks + cu.c] = make_float2(m, lsum);
             ++cu.c;
             cur = nxt;
@@ -471,9 +490,10 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
 
 hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q, int n_blocks,
                          hipStream_t st) {
-    LogitsDims ld{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.S, dm.MP, dm.NP, dm.R, dm.LHkv, dm.max_chunks};
+    LogitsDims ld{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.S, dm.MP, dm.NP, dm.R, dm.LHkv, dm.max_chunks,
+                  dm.W, dm.G * dm.W};
     hipLaunchKernelGGL(k_logits, dim3(n_blocks), dim3(256), 0, st, ld, v.k_pool, v.page_table,
-                       v.n_tokens, q, sc.logits, sc.cstats, sc.status, sc.item_prefix);
+                       v.n_tokens, q, sc.logits, sc.cstats, sc.status, sc.item_prefix, v.t_ins, v.clock);
     return hipGetLastError();
 }
 
@@ -496,7 +516,10 @@ __global__ void __launch_bounds__(256) k_rowstats(Dims dm, Scratch sc) {
         l += st.y * hw_exp2(st.x - m);
     }
     l = wave_sum(l);
-    if (lane == 0) sc.rstats[(size_t)s * dm.R + row] = make_float2(m, 1.0f / l);
+    // a window query that sees none of the session's tokens gives them no
+    // weight (its row has no live logit)
+    if (lane == 0) sc.rstats[(size_t)s * dm.R + row] = m == -INFINITY ? make_float2(0.0f, 0.0f)
+                                                                       : make_float2(m, 1.0f / l);
 }
 
 hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st) {

@@ -62,6 +62,8 @@ class Workload:
     pinned_mask: int = 1 << SYSTEM
     halflife_jitter: Optional[Tuple[float, float]] = None
     attention_norm: bool = False   # score's attention term relative to the uniform level
+    window: int = 1                # decode queries per observation (W)
+    obs_interval: int = 1          # one observation every k decode steps (k >= W)
     b_range: Tuple[float, float] = (0.2, 1.0)
     extra: dict = field(default_factory=dict)
 

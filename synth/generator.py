@@ -152,6 +152,18 @@ def q_step(w: Workload, session: int, step: int) -> np.ndarray:
     return rng(w, session, "q", step).standard_normal((w.L, w.Hq, w.d), dtype=np.float32)
 
 
+def observes(w: Workload, step: int) -> bool:
+    """Whether decode step ``step`` (1-based) is an observation step: every
+    k-th one, k = w.obs_interval."""
+    return step % w.obs_interval == 0
+
+
+def q_window(w: Workload, session: int, step: int) -> np.ndarray:
+    """float32 [W][L][Hq][d]: the decode queries of steps step - W + 1 ..
+    step, oldest first (W = w.window)."""
+    return np.stack([q_step(w, session, step - w.window + 1 + j) for j in range(w.window)])
+
+
 # ---------------------------------------------------------------- device draws
 
 def _torch_seed(w: Workload, session: int, stream: str, step: int) -> int:

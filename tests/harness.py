@@ -149,7 +149,8 @@ class Pair:
         self.cache.set_free_pages(perm[pos:][::-1])
         self.md = MemDecay(self.cache, torch.from_numpy(self.b), torch.from_numpy(self.lam),
                            rho=f32(w.rho), alpha=f32(self.alpha), tau_scale=f32(w.tau_scale),
-                           pinned_mask=self.pinned_mask, fused=fused, attention_norm=w.attention_norm)
+                           pinned_mask=self.pinned_mask, fused=fused, attention_norm=w.attention_norm,
+                           window=w.window)
         n_slots = n_phys * P
         self.abar = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
         self.tscore = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
@@ -161,17 +162,22 @@ class Pair:
     def inputs(self, k: int):
         w, S = self.w, self.w.S
         reg = np.full(S, g.append_region(w, k), dtype=np.uint8)
+        obs = g.observes(w, k)       # queries exist only at observation steps
         if self.backend == "numpy":
-            q = np.stack([g.q_step(w, s, k) for s in range(S)])
+            q = np.stack([g.q_window(w, s, k) if obs else np.zeros((w.window, w.L, w.Hq, w.d), np.float32)
+                          for s in range(S)])                            # [S][W][L][Hq][d]
             if self.query_gain:
-                q = np.stack([g.planted_query(w, s, q[s], self.query_gain) for s in range(S)])
+                q = np.stack([np.stack([g.planted_query(w, s, qw, self.query_gain) for qw in q[s]])
+                              for s in range(S)])
             nk = np.stack([g.k_append(w, s, k) for s in range(S)])
             qt = torch.from_numpy(q).to(self.dev)
             nkt = bits_to_torch(nk, self.dev)
             qo = {s: q[s] for s in self.oracle_sessions}
             nko = {s: nk[s] for s in self.oracle_sessions}
         else:
-            qt = g.torch_queries(w, k, self.dev)
+            qt = torch.stack([g.torch_queries(w, k - w.window + 1 + j, self.dev) if obs else
+                              torch.zeros((S, w.L, w.Hq, w.d), device=self.dev)
+                              for j in range(w.window)], dim=1).contiguous()
             nkt = g.torch_append_keys(w, k, self.dev)
             qo = {s: qt[s].cpu().numpy() for s in self.oracle_sessions}
             nb = torch_to_bits(nkt)
@@ -185,6 +191,17 @@ class Pair:
         w, P, S = self.w, self.w.P, self.w.S
         qt, nkt, regt, qo, nko, reg = self.inputs(k)
         md = self.md
+        if not g.observes(w, k):
+            # a decode step without an observation: append only, on both sides
+            md.observe(k, None, nkt, regt)
+            torch.cuda.synchronize(self.dev)
+            nt_dev = self.cache.n_tokens.cpu().numpy()
+            for s in self.oracle_sessions:
+                rec = self.oracles[s].step(None, nko[s], int(reg[s]))
+                if compare:
+                    assert int(nt_dev[s]) == rec.n, (k, s, "append-only n")
+            self.stats.steps += 1
+            return self.stats
         md.observe(k, qt, nkt, regt, abar_out=self.abar)
         md.score(token_score=self.tscore)
         md.select()

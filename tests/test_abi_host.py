@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert B.md_abi_version() == 1
+    assert B.md_abi_version() == 2
     for st in (0, -1, -2, -3, -4, -5, -6):
         assert B.md_status_str(st)
     assert B.md_status_str(12345) == "unknown status"
@@ -55,8 +55,9 @@ def test_struct_layout_matches_the_header(lib):
     #include <stddef.h>
     #include "memdecay.h"
     int main(void) {
-      printf("%zu %zu %zu %zu %zu\n", sizeof(md_config), offsetof(md_config, rho),
-             offsetof(md_config, flags), sizeof(md_region_params), sizeof(md_cache_view));
+      printf("%zu %zu %zu %zu %zu %zu\n", sizeof(md_config), offsetof(md_config, rho),
+             offsetof(md_config, flags), offsetof(md_config, window), sizeof(md_region_params),
+             sizeof(md_cache_view));
       printf("%zu %zu\n", offsetof(md_cache_view, importance), offsetof(md_cache_view, free_count));
       return 0; }
     '''
@@ -67,6 +68,7 @@ def test_struct_layout_matches_the_header(lib):
         subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), c, "-o", exe], check=True)
         out = subprocess.run([exe], capture_output=True, text=True, check=True).stdout.split()
     got = [ctypes.sizeof(B.md_config), B.md_config.rho.offset, B.md_config.flags.offset,
+           B.md_config.window.offset,
            ctypes.sizeof(B.md_region_params), ctypes.sizeof(B.md_cache_view),
            B.md_cache_view.importance.offset, B.md_cache_view.free_count.offset]
     assert [int(x) for x in out] == got
@@ -75,7 +77,7 @@ def test_struct_layout_matches_the_header(lib):
 def good_config(**kw):
     c = dict(n_layers=28, n_q_heads=12, n_kv_heads=2, head_dim=128, page_size=16,
              max_sessions=16, max_pages=2100, n_phys_pages=40000, n_regions=7,
-             pinned_region_mask=1, rho=0.9, alpha=1.0, tau_scale=2.0, flags=0)
+             pinned_region_mask=1, rho=0.9, alpha=1.0, tau_scale=2.0, flags=0, window=1)
     c.update(kw)
     return B.md_config(**c)
 
@@ -114,6 +116,9 @@ def fake_rp():
     (dict(alpha=float("inf")), B.MD_E_INVALID),
     (dict(tau_scale=-2.0), B.MD_E_INVALID),
     (dict(flags=8), B.MD_E_INVALID),
+    (dict(window=0), B.MD_E_INVALID),
+    (dict(window=3), B.MD_E_UNSUPPORTED),            # G = 6: 18 MFMA columns
+    (dict(window=2, flags=2), B.MD_E_UNSUPPORTED),   # the fused kernel takes W = 1
     (dict(flags=3), B.MD_E_INVALID),
 ])
 def test_init_rejects_bad_configs_on_the_host(lib, kw, expect):

@@ -74,7 +74,7 @@ def test_free_list_exhaustion_sets_capacity():
 def test_nonfinite_query_sets_status():
     p = small_pair(oracle_sessions=[])
     q, nk, reg, *_ = p.inputs(1)
-    q[0, 0, 3, 17] = float("nan")
+    q[0, 0, 0, 3, 17] = float("nan")      # [S][W][L][Hq][d]
     p.md.observe(1, q, nk, reg)
     torch.cuda.synchronize()
     assert p.md.device_status() & B.MD_DEV_NONFINITE

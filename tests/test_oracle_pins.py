@@ -412,3 +412,58 @@ def test_normalised_term_of_a_new_token_follows_the_cache_size_at_its_step():
     assert rec.n == 11 and rec.score[-1] == pytest.approx(2.0 * 0.25, rel=1e-14)
     # the token added a step earlier: a = 0.75 * 0.25/10 + 0.25/11, measured in 1/11
     assert rec.score[-2] == pytest.approx(2.0 * 11 * (0.75 * 0.25 / 10 + 0.25 / 11), rel=1e-13)
+
+
+# ------------------------------ observation interval and window (Sec. III-C)
+
+def test_window_mass_is_the_mean_of_its_queries_softmaxes():
+    # Sec. III-C averages the attention mass over the window as well.  With
+    # one layer and one head, and every token inserted before the window,
+    # A is the mean of the window queries' textbook softmaxes.
+    rng = np.random.default_rng(11)
+    d, n, W = 128, 13, 3
+    keys = widen_bf16(bf16(rng.normal(size=(n, d))))
+    q = rng.normal(size=(W, 1, 1, d)).astype(np.float32)
+    s = make_session(keys, clock=5)              # t_ins = 0, steps 4..6 see them all
+    rec = s.step(q)
+    x = keys.astype(np.float64) @ q[:, 0, 0].astype(np.float64).T / math.sqrt(d)   # [n][W]
+    expect = np.mean([scipy.special.softmax(x[:, w]) for w in range(W)], axis=0)
+    np.testing.assert_allclose(rec.abar, expect, rtol=1e-12)
+
+
+def test_window_query_sees_only_tokens_of_its_step():
+    # The older window query belongs to the previous step, before this
+    # step's token was cached: it cannot attend to it, however well it
+    # matches.  Here it matches nothing else (zero keys), the newer query is
+    # zero: the new token gets (0 + 1/n) / 2, the others (1/(n-1) + 1/n) / 2.
+    d, n0 = 128, 7
+    s = make_session(np.zeros((n0, d), np.float32))
+    newk = np.zeros(d, np.float32)
+    newk[3] = 1.0
+    q = np.zeros((2, 1, 1, d), np.float32)
+    q[0, 0, 0, 3] = 40.0 * math.sqrt(d)            # older query: aimed at the new key
+    rec = s.step(q, bf16(newk), 2)
+    n = n0 + 1
+    assert rec.abar[-1] == pytest.approx(0.5 / n, rel=1e-12)
+    np.testing.assert_allclose(rec.abar[:-1], 0.5 * (1.0 / (n - 1) + 1.0 / n), rtol=1e-12)
+
+
+def test_steps_without_observation_only_append_and_eviction_waits():
+    # Attention is sampled only at observation steps (Sec. III-C); Alg. 1
+    # runs per observation.  Steps in between append, advance the clock and
+    # leave importance, refresh clocks and pages alone, even over budget.
+    d, n0, P = 128, 32, 16
+    s = make_session(np.zeros((n0, d), np.float32), P=P, budget=32, b=np.full(NREG, 0.5),
+                     lam=np.full(NREG, 0.01))
+    q = np.zeros((1, 1, d), np.float32)
+    s.step(q)
+    a0 = s.a[:n0].copy()
+    tr0 = s.t_ref[:n0].copy()
+    for k in range(3):
+        rec = s.step(None, bf16(np.zeros(d)), 6)
+        assert rec.evicted.size == 0 and rec.n == n0 + k + 1
+    assert s.t == 4 and s.n_tokens() == n0 + 3
+    np.testing.assert_array_equal(s.a[:n0], a0)
+    np.testing.assert_array_equal(s.t_ref[:n0], tr0)
+    rec = s.step(q, bf16(np.zeros(d)), 6)          # observation: 36 tokens > 32
+    assert rec.n == 36 and rec.n_after <= 32 and rec.evicted.size >= 1
