@@ -265,6 +265,37 @@ md_status md_read_counters(md_handle h, int64_t* out);
  * Host-only, no device work. */
 md_status md_kernel_config(md_handle h, int32_t* out);
 
+/*
+ * md_calib_accumulate — region-lifetime statistics for the calibration of
+ * the decay rates (Sec. IV-B): adds every token now in the page tables, of
+ * every session, to its bin (s, r(i), b), b = (t - t_ins_i) / bucket_steps
+ * (ages of n_buckets * bucket_steps steps and more are left out):
+ *   mass_fx[s][r][b] += round(A_i * 2^40)   (A_i read from abar at the slot)
+ *   count[s][r][b]   += 1
+ *   age_sum[s][r][b] += t - t_ins_i
+ * abar: float32 [NP][P], e.g. md_observe_step's abar_out of this step.
+ * mass_fx, count, age_sum: uint64 [S][n_regions][n_buckets] (device), owned
+ * and zeroed by the caller; the integer sums make the result independent of
+ * the order of the additions.  Requires an observation since the last
+ * md_compact (MD_E_STATE otherwise); enqueued on the handle's stream.
+ */
+md_status md_calib_accumulate(md_handle h, const float* abar, int32_t bucket_steps, int32_t n_buckets,
+                              uint64_t* mass_fx, uint64_t* count, uint64_t* age_sum);
+
+/*
+ * md_calib_fit — the log-linear decay of Eq. 6, log A_r(dt) ~ log c_r -
+ * lambda_r dt, fitted per region by least squares weighted with each
+ * bucket's observation count (Sec. IV-A), on HOST copies of the sums above,
+ * added over the n_sessions sessions.  A bucket contributes its mean age and
+ * the log of its mean mass; buckets without observations or mass are left
+ * out.  Writes lambda_hat[r] and log_c[r] (doubles, n_regions each), NaN for
+ * a region with fewer than two usable buckets.  The half-life is
+ * ln 2 / lambda_hat (Eq. 7).  Host only, no handle.
+ */
+md_status md_calib_fit(const uint64_t* mass_fx, const uint64_t* count, const uint64_t* age_sum,
+                       int32_t n_sessions, int32_t n_regions, int32_t n_buckets, double* lambda_hat,
+                       double* log_c);
+
 /* Release the scratch and the handle (synchronises the stream first). */
 md_status md_destroy(md_handle h);
 

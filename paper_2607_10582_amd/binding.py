@@ -32,6 +32,7 @@ MD_FLAG_NORM_ATTENTION = 0x4
 EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_observe_step",
            "md_score_pages", "md_select_evict", "md_compact", "md_read_device_status",
            "md_profile_enable", "md_profile_read", "md_read_counters", "md_kernel_config",
+           "md_calib_accumulate", "md_calib_fit",
            "md_destroy")
 
 # kernel ids of md_profile_enable / md_profile_read
@@ -103,6 +104,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                     ctypes.POINTER(ctypes.c_int64)]
     lib.md_read_counters.restype = i32
     lib.md_read_counters.argtypes = [vp, ctypes.POINTER(ctypes.c_int64)]
+    lib.md_calib_accumulate.restype = i32
+    lib.md_calib_accumulate.argtypes = [vp, vp, i32, i32, vp, vp, vp]
+    lib.md_calib_fit.restype = i32
+    lib.md_calib_fit.argtypes = [vp, vp, vp, i32, i32, i32, vp, vp]
     lib.md_kernel_config.restype = i32
     lib.md_kernel_config.argtypes = [vp, ctypes.POINTER(i32)]
     lib.md_destroy.restype = i32
@@ -176,6 +181,26 @@ def md_profile_read(h: int, kernel: int):
     _check("md_profile_read", load_library().md_profile_read(h, kernel, ctypes.byref(ms),
                                                              ctypes.byref(n)))
     return ms.value, n.value
+
+
+def md_calib_accumulate(h: int, abar: int, bucket_steps: int, n_buckets: int, mass_fx: int, count: int,
+                        age_sum: int) -> int:
+    return _check("md_calib_accumulate", load_library().md_calib_accumulate(
+        h, abar, bucket_steps, n_buckets, mass_fx, count, age_sum))
+
+
+def md_calib_fit(mass_fx, count, age_sum):
+    """Eq. 6 fit on host numpy uint64 arrays [S][n_regions][n_buckets];
+    returns (lambda_hat, log_c) as float64 arrays [n_regions]."""
+    import numpy as np
+    arrs = [np.ascontiguousarray(x, dtype=np.uint64) for x in (mass_fx, count, age_sum)]
+    S, nr, nb = arrs[0].shape
+    lam = np.zeros(nr, np.float64)
+    logc = np.zeros(nr, np.float64)
+    _check("md_calib_fit", load_library().md_calib_fit(
+        arrs[0].ctypes.data, arrs[1].ctypes.data, arrs[2].ctypes.data, S, nr, nb,
+        lam.ctypes.data, logc.ctypes.data))
+    return lam, logc
 
 
 def md_read_counters(h: int):

@@ -160,6 +160,13 @@ class MemDecay:
         self.select()
         self.compact()
 
+    def calib_accumulate(self, abar: torch.Tensor, bucket_steps: int, stats) -> None:
+        """Add this observation to stats = (mass_fx, count, age_sum), int64
+        tensors [S][n_regions][n_buckets] viewed as uint64 by the library."""
+        mass, count, age = stats
+        B.md_calib_accumulate(self.handle, _ptr(abar, torch.float32), bucket_steps, mass.shape[-1],
+                              mass.data_ptr(), count.data_ptr(), age.data_ptr())
+
     def device_status(self) -> int:
         return B.md_read_device_status(self.handle)
 

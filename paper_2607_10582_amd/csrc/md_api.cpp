@@ -451,6 +451,71 @@ md_status md_profile_read(md_handle h, int32_t kernel, double* total_ms, int64_t
     return st;
 }
 
+md_status md_calib_accumulate(md_handle h, const float* abar, int32_t bucket_steps, int32_t n_buckets,
+                              uint64_t* mass_fx, uint64_t* count, uint64_t* age_sum) {
+    if (h == nullptr || abar == nullptr || mass_fx == nullptr || count == nullptr || age_sum == nullptr)
+        return MD_E_INVALID;
+    if (bucket_steps < 1 || n_buckets < 1 || (int64_t)n_buckets * h->dm.n_regions > (1 << 20))
+        return MD_E_INVALID;
+    if (!aligned(abar, 4) || !aligned(mass_fx, 8) || !aligned(count, 8) || !aligned(age_sum, 8))
+        return MD_E_INVALID;
+    if (h->phase == kNone) return MD_E_STATE;
+    if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    if (md::launch_calib(h->dm, h->v, h->sc, abar, bucket_steps, n_buckets,
+                         reinterpret_cast<unsigned long long*>(mass_fx),
+                         reinterpret_cast<unsigned long long*>(count),
+                         reinterpret_cast<unsigned long long*>(age_sum), h->stream) != hipSuccess)
+        return MD_E_HIP;
+    return MD_OK;
+}
+
+md_status md_calib_fit(const uint64_t* mass_fx, const uint64_t* count, const uint64_t* age_sum,
+                       int32_t n_sessions, int32_t n_regions, int32_t n_buckets, double* lambda_hat,
+                       double* log_c) {
+    if (mass_fx == nullptr || count == nullptr || age_sum == nullptr || lambda_hat == nullptr ||
+        log_c == nullptr || n_sessions < 1 || n_regions < 1 || n_buckets < 1)
+        return MD_E_INVALID;
+    const double unit = 1.0 / 1099511627776.0;   // 2^-40
+    for (int r = 0; r < n_regions; ++r) {
+        // per bucket: weight = observations, x = their mean age, y = log of
+        // their mean mass (buckets without observations or mass left out)
+        std::vector<double> w, x, y;
+        for (int b = 0; b < n_buckets; ++b) {
+            double m = 0.0, n = 0.0, a = 0.0;
+            for (int s = 0; s < n_sessions; ++s) {
+                const size_t i = ((size_t)s * n_regions + r) * n_buckets + b;
+                m += (double)mass_fx[i] * unit;
+                n += (double)count[i];
+                a += (double)age_sum[i];
+            }
+            if (n > 0.0 && m > 0.0) {
+                w.push_back(n);
+                x.push_back(a / n);
+                y.push_back(log(m / n));
+            }
+        }
+        lambda_hat[r] = log_c[r] = NAN;
+        if (w.size() < 2) continue;
+        double sw = 0.0, sx = 0.0, sy = 0.0;
+        for (size_t i = 0; i < w.size(); ++i) {
+            sw += w[i];
+            sx += w[i] * x[i];
+            sy += w[i] * y[i];
+        }
+        const double xm = sx / sw, ym = sy / sw;
+        double sxx = 0.0, sxy = 0.0;
+        for (size_t i = 0; i < w.size(); ++i) {
+            sxx += w[i] * (x[i] - xm) * (x[i] - xm);
+            sxy += w[i] * (x[i] - xm) * (y[i] - ym);
+        }
+        if (sxx == 0.0) continue;
+        const double slope = sxy / sxx;
+        lambda_hat[r] = -slope;
+        log_c[r] = ym - slope * xm;
+    }
+    return MD_OK;
+}
+
 md_status md_read_counters(md_handle h, int64_t* out) {
     if (h == nullptr || out == nullptr) return MD_E_INVALID;
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;

@@ -112,6 +112,9 @@ hipError_t launch_score(const Dims& dm, const View& v, const Scratch& sc, float*
                         float* token_score, int n_blocks, hipStream_t st);
 hipError_t launch_select(const Dims& dm, const View& v, const Scratch& sc, int32_t* ev_serial,
                          int32_t* ev_count, uint8_t* infeasible, hipStream_t st);
+hipError_t launch_calib(const Dims& dm, const View& v, const Scratch& sc, const float* abar, int bucket_steps,
+                        int n_buckets, unsigned long long* mass_fx, unsigned long long* count,
+                        unsigned long long* age_sum, hipStream_t st);
 hipError_t launch_compact(const Dims& dm, const View& v, const Scratch& sc,
                           const int32_t* ev_serial, const int32_t* ev_count, hipStream_t st);
 

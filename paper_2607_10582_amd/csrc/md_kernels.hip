@@ -878,6 +878,70 @@ hipError_t launch_compact(const Dims& dm, const View& v, const Scratch& sc,
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- calibration
+
+// Lifetime statistics (Sec. IV-B): one thread per token position of one
+// session (blockIdx.y); tokens past the session's count do nothing.  The
+// lanes of a wave that share a (region, age bucket) bin add their mass,
+// count and age sum with wave reductions, and one lane adds them to the bin
+// with 64-bit integer atomics (mass in fixed point, A * 2^40), so the sums
+// do not depend on the order of the additions.
+__global__ void __launch_bounds__(256) k_calib(Dims dm, View v, Scratch sc, const float* __restrict__ abar,
+                                               int bucket_steps, int n_buckets,
+                                               unsigned long long* mass_fx, unsigned long long* count,
+                                               unsigned long long* age_sum) {
+    const int s = blockIdx.y;
+    const int tok = blockIdx.x * blockDim.x + threadIdx.x;
+    const int nt = v.n_tokens[s];
+    int key = -1;
+    unsigned long long fx = 0, ag = 0;
+    if (tok < nt && tok < dm.MP * dm.P) {
+        const int p = v.page_table[(size_t)s * dm.MP + (tok >> dm.Pshift)];
+        if ((unsigned)p < (unsigned)dm.NP) {
+            const size_t si = (size_t)p * dm.P + (tok & (dm.P - 1));
+            const int r = v.region[si];
+            const int age = v.clock[s] - v.t_ins[si];
+            const int b = age >= 0 ? age / bucket_steps : n_buckets;
+            if (r < dm.n_regions && b < n_buckets) {
+                key = r * n_buckets + b;
+                fx = (unsigned long long)llrint((double)abar[si] * 1099511627776.0);   // 2^40
+                ag = (unsigned long long)age;
+            }
+        } else {
+            atomicOr(sc.status, kDevCorrupt);
+        }
+    }
+    bool todo = key >= 0;
+    while (__ballot(todo) != 0ull) {
+        const int first = __ffsll((long long)__ballot(todo)) - 1;
+        const int k = __shfl(key, first);
+        const bool mine = todo && key == k;
+        unsigned long long m = mine ? fx : 0ull, a = mine ? ag : 0ull;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            m += __shfl_xor(m, o);
+            a += __shfl_xor(a, o);
+        }
+        const int c = __popcll(__ballot(mine));
+        if (lane_id() == first) {
+            const size_t bin = (size_t)s * dm.n_regions * n_buckets + k;
+            atomicAdd(mass_fx + bin, m);
+            atomicAdd(count + bin, (unsigned long long)c);
+            atomicAdd(age_sum + bin, a);
+        }
+        todo = todo && !mine;
+    }
+}
+
+hipError_t launch_calib(const Dims& dm, const View& v, const Scratch& sc, const float* abar, int bucket_steps,
+                        int n_buckets, unsigned long long* mass_fx, unsigned long long* count,
+                        unsigned long long* age_sum, hipStream_t st) {
+    const int per_session = dm.MP * dm.P;
+    hipLaunchKernelGGL(k_calib, dim3((per_session + 255) / 256, dm.S), dim3(256), 0, st, dm, v, sc, abar,
+                       bucket_steps, n_buckets, mass_fx, count, age_sum);
+    return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- scratch layout
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }

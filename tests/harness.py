@@ -155,6 +155,7 @@ class Pair:
         self.abar = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
         self.tscore = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
         self.stats = Stats()
+        self.last_rec = {}
         self.status_seen = 0
         self.k = 0
 
@@ -223,6 +224,7 @@ class Pair:
         tref_fix = []
         for s in self.oracle_sessions:
             rec = self.oracles[s].step(qo[s], nko[s], int(reg[s]))
+            self.last_rec[s] = rec
             if not compare:
                 continue
             npg, nt = int(host["n_pages"][s]), int(host["n_tokens"][s])

@@ -8,6 +8,7 @@ import re
 import subprocess
 import tempfile
 
+import numpy as np
 import pytest
 
 from paper_2607_10582_amd import binding as B
@@ -149,3 +150,25 @@ def test_calls_reject_a_null_handle(lib):
     out = ctypes.c_int32()
     assert L.md_read_device_status(None, ctypes.byref(out)) == B.MD_E_INVALID
     assert L.md_init(None, None, None, None, None) == B.MD_E_INVALID
+
+
+def test_calib_fit_matches_the_oracle_fit(lib):
+    # md_calib_fit is host code: count-weighted least squares of Eq. 6 on
+    # sums added over sessions, against the oracle's fit of the same sums.
+    from oracle.calibration import fit_decay
+    rng = np.random.default_rng(5)
+    S, nr, nb = 3, 7, 20
+    count = rng.integers(0, 60, (S, nr, nb)).astype(np.uint64)
+    count[:, 6, 1:] = 0                          # region 6: a single bucket, no fit
+    count[:, 6, 0] = 5
+    ages = (np.arange(nb) * 8 + 3.5)[None, None, :]
+    mean = 0.01 * np.exp(-rng.uniform(0.01, 0.1, (1, nr, 1)) * ages) * np.exp(rng.normal(0, 0.2, (S, nr, nb)))
+    mass_fx = np.round(count * mean * 2.0**40).astype(np.uint64)
+    age_sum = (count * np.round(ages)).astype(np.uint64)
+    lam, logc = B.md_calib_fit(mass_fx, count, age_sum)
+    olam, ologc = fit_decay(mass_fx.sum(0).astype(np.float64) / 2.0**40, count.sum(0).astype(np.float64),
+                            age_sum.sum(0).astype(np.float64))
+    assert np.array_equal(np.isnan(lam), np.isnan(olam)) and np.isnan(lam[6])
+    ok = ~np.isnan(olam)
+    np.testing.assert_allclose(lam[ok], olam[ok], rtol=1e-9)
+    np.testing.assert_allclose(logc[ok], ologc[ok], rtol=1e-9)

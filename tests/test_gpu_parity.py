@@ -298,3 +298,39 @@ def test_window_on_a_batch_with_empty_and_short_sessions():
                          window=3, obs_interval=3, steps=30, system_len=20)
     p = Pair(w, n0s=[0, 1, 17, 130, 700], budgets=[0, 5, 10, 100, 200], fused=None)
     run_pair(p, 30, "window3-edges")
+
+
+def test_lifetime_statistics_and_decay_fit():
+    # Region-lifetime calibration (Sec. IV-B): after every observation the
+    # device adds each cached token's attention mass to its (region, age
+    # bucket) bin; the oracle does the same in float64.  The budget holds
+    # every token, as in a measurement pass.  Counts and age sums are exact
+    # integers; mass sums agree within 1e-5 relative plus the fixed-point
+    # rounding; the Eq. 6 fits of the two agree closely.
+    from oracle.calibration import LifetimeStats, fit_decay
+    from paper_2607_10582_amd import binding as B
+    w = C.with_overrides(C.get("qwen15_1700"), L=4, steps=24)
+    p = Pair(w, planted=64, planted_strength=2.0, query_gain=0.5, budgets=[10**6])
+    bucket, nb, nr = 64, 32, 7
+    dev = [torch.zeros((w.S, nr, nb), dtype=torch.int64, device="cuda") for _ in range(3)]
+    ost = LifetimeStats(nr, bucket, nb)
+    for _ in range(24):
+        p.step()
+        p.md.calib_accumulate(p.abar, bucket, dev)
+        o, rec = p.oracles[0], p.last_rec[0]
+        live = o.live()
+        ost.add(rec.t, o.t_ins[live], o.region[live], rec.abar)
+    torch.cuda.synchronize()
+    assert p.device_status() == 0
+    mass, count, age = [x.cpu().numpy().view(np.uint64)[0] for x in dev]
+    assert np.array_equal(count.astype(np.int64), ost.count)
+    assert np.array_equal(age.astype(np.int64), ost.age_sum)
+    got = mass.astype(np.float64) / 2.0**40
+    np.testing.assert_allclose(got, ost.mass, rtol=1e-5, atol=ost.count.max() * 2.0**-40)
+    lam, logc = B.md_calib_fit(mass[None], count[None], age[None])
+    olam, ologc = fit_decay(ost.mass, ost.count, ost.age_sum)
+    assert np.array_equal(np.isnan(lam), np.isnan(olam)) and np.count_nonzero(~np.isnan(olam)) >= 5
+    ok = ~np.isnan(olam)
+    np.testing.assert_allclose(lam[ok], olam[ok], rtol=1e-3, atol=1e-7)
+    say(f"[calibration] fitted half-lives {np.round(np.log(2) / lam, 1)}")
+    p.close()
