@@ -50,7 +50,13 @@ design notes of the repository):
     names, measured against the uniform attention level 1/|K_t|): the score
     uses alpha * |K_t| * a_i in place of alpha * a_i, |K_t| being the same
     count as in tau.  The slower usage memory named with it is the EWMA rate
-    rho taken closer to 1; it needs no change here.
+    rho taken closer to 1; it needs no change here;
+  * optional region-aligned pages (the allocator variant Sec. III-D leaves
+    to future work): a page holds tokens of one region only.  An appended
+    token opens a fresh page when the last page is full or its last token's
+    region differs; a prompt is laid out the same way, token by token.  The
+    rest of the method is unchanged: page sizes simply vary more, and Eq. 5
+    still averages over the live members.
 """
 from __future__ import annotations
 
@@ -110,7 +116,7 @@ class Session:
                  page_sizes: Optional[Sequence[int]] = None,
                  page_serials: Optional[Sequence[int]] = None,
                  next_serial: Optional[int] = None, capacity: Optional[int] = None,
-                 attention_norm: bool = False):
+                 attention_norm: bool = False, region_aligned: bool = False):
         if Hq % Hkv:
             raise ValueError("query heads must be a multiple of KV heads")
         self.L, self.Hq, self.Hkv, self.d, self.P = L, Hq, Hkv, d, P
@@ -120,6 +126,7 @@ class Session:
         self.alpha, self.rho, self.tau_scale = float(alpha), float(rho), float(tau_scale)
         self.pinned_mask = int(pinned_mask)
         self.attention_norm = bool(attention_norm)
+        self.region_aligned = bool(region_aligned)
         self.budget = int(budget)
         self.t = int(clock)
 
@@ -143,7 +150,8 @@ class Session:
         self.keys[:, :, :n, :] = widen_bf16(kb).transpose(1, 2, 0, 3)
 
         if page_sizes is None:
-            page_sizes = [min(P, n - i) for i in range(0, n, P)]
+            page_sizes = (aligned_page_sizes(region, P) if self.region_aligned
+                          else [min(P, n - i) for i in range(0, n, P)])
         if sum(page_sizes) != n or any(not 1 <= s <= P for s in page_sizes):
             raise ValueError("page sizes must be in [1, P] and cover the tokens")
         if page_serials is None:
@@ -193,8 +201,12 @@ class Session:
         self.t_ref[j] = self.t
         self.a[j] = 0.0
         self.keys[:, :, j, :] = widen_bf16(key_bits).reshape(self.L, self.Hkv, self.d)
-        if self.pages and len(self.pages[-1].slots) < self.P:
-            self.pages[-1].slots.append(j)
+        tail = self.pages[-1].slots if self.pages else None
+        joins = tail is not None and len(tail) < self.P
+        if joins and self.region_aligned:
+            joins = int(self.region[tail[-1]]) == int(region)
+        if joins:
+            tail.append(j)
         else:
             self.pages.append(Page(self.next_serial, [j]))
             self.next_serial += 1
@@ -292,6 +304,21 @@ class Session:
         return out
 
 
+def aligned_page_sizes(region, P: int) -> List[int]:
+    """Page sizes of a token sequence laid out with region-aligned pages:
+    tokens in order, each joining the open page unless it is full or holds
+    another region."""
+    sizes: List[int] = []
+    last = None
+    for r in np.asarray(region, dtype=np.int64).tolist():
+        if sizes and sizes[-1] < P and r == last:
+            sizes[-1] += 1
+        else:
+            sizes.append(1)
+        last = r
+    return sizes
+
+
 def select_pages(page_score, serials, sizes, pinned, n: int, budget: int):
     """Greedy page eviction (Alg. 1): while |K| > B, evict the non-pinned page
     of smallest (S_p, serial).  Returns (evicted serials ascending, n after,
@@ -311,7 +338,7 @@ def select_pages(page_score, serials, sizes, pinned, n: int, budget: int):
 
 def session_from_workload(w, session: int, *, region, keys_bits, b, lam, budget,
                           alpha=None, rho=None, tau_scale=None, capacity=None,
-                          attention_norm=None) -> Session:
+                          attention_norm=None, region_aligned=None) -> Session:
     """A session at the start of decoding: prefix token i has t_ins = t_ref = i,
     importance 0, and the clock stands at n0 (so decode step k runs at
     t = n0 + k)."""
@@ -323,4 +350,5 @@ def session_from_workload(w, session: int, *, region, keys_bits, b, lam, budget,
                    pinned_mask=w.pinned_mask, budget=budget, clock=n0,
                    region=region, keys_bits=keys_bits,
                    capacity=capacity if capacity is not None else n0 + w.steps,
-                   attention_norm=w.attention_norm if attention_norm is None else attention_norm)
+                   attention_norm=w.attention_norm if attention_norm is None else attention_norm,
+                   region_aligned=w.region_aligned if region_aligned is None else region_aligned)

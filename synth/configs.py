@@ -64,6 +64,8 @@ class Workload:
     attention_norm: bool = False   # score's attention term relative to the uniform level
     window: int = 1                # decode queries per observation (W)
     obs_interval: int = 1          # one observation every k decode steps (k >= W)
+    region_aligned: bool = False   # pages hold one region each (allocator variant)
+    append_run: int = 1            # decode tokens per region run of the append cycle
     b_range: Tuple[float, float] = (0.2, 1.0)
     extra: dict = field(default_factory=dict)
 
@@ -107,6 +109,16 @@ WORKLOADS = {
                            mean_span=512.0, budget_frac=0.2, steps=64,
                            append_cycle=APPEND_CYCLE,
                            halflife_jitter=(0.8, 1.2)),
+    # region-aligned pages: the small workload with turns of 5 decode tokens
+    # per region, and the 32k batch with turns of 24
+    "small_aligned": Workload("small_aligned", 5, L=1, Hq=12, Hkv=2, d=128, P=16, S=1, n0=450,
+                              n0_range=None, system_len=60, mean_span=40.0,
+                              budget_frac=0.5, steps=32, append_cycle=APPEND_CYCLE,
+                              region_aligned=True, append_run=5),
+    "long32k_aligned": Workload("long32k_aligned", 3, **QWEN15, P=16, S=16, n0=32768,
+                                n0_range=None, system_len=1024, mean_span=512.0,
+                                budget_frac=0.25, steps=128, append_cycle=APPEND_CYCLE,
+                                region_aligned=True, append_run=24),
 }
 
 

@@ -116,15 +116,27 @@ def budgets(w: Workload, n0s: np.ndarray) -> np.ndarray:
 
 
 def append_region(w: Workload, step: int) -> int:
-    """Region of the token appended at decode step ``step`` (1-based)."""
-    return int(w.append_cycle[(step - 1) % len(w.append_cycle)])
+    """Region of the token appended at decode step ``step`` (1-based): the
+    append cycle's regions in turn, each for ``append_run`` steps."""
+    return int(w.append_cycle[((step - 1) // w.append_run) % len(w.append_cycle)])
 
 
 def pages_needed(w: Workload, n0s: np.ndarray) -> int:
     """Physical pages for every prefix plus every appended token, plus one
-    spare page per session for the page a step may open."""
-    pre = int(sum((int(n) + w.P - 1) // w.P for n in n0s))
-    app = w.S * ((w.steps + w.P - 1) // w.P + 1)
+    spare page per session for the page a step may open.  With region-aligned
+    pages, an upper bound: every region span of a prefix, and every region
+    run of the appended tokens, may start a page of its own."""
+    if not w.region_aligned:
+        pre = int(sum((int(n) + w.P - 1) // w.P for n in n0s))
+        app = w.S * ((w.steps + w.P - 1) // w.P + 1)
+        return pre + app
+    pre = 0
+    for s, n in enumerate(n0s):
+        reg = region_spans(w, s, int(n))
+        spans = int(np.count_nonzero(np.diff(reg.astype(np.int64)))) + 1 if n else 0
+        pre += (int(n) + w.P - 1) // w.P + spans
+    runs = (w.steps + w.append_run - 1) // w.append_run
+    app = w.S * ((w.steps + w.P - 1) // w.P + runs + 1)
     return pre + app
 
 
