@@ -53,7 +53,8 @@ def kernel_source_hash(kernel: str) -> str:
 def describe(w, n0s) -> str:
     n = f"{int(n0s[0])}" if len(set(n0s.tolist())) == 1 else f"U[{w.n0_range[0]},{w.n0_range[1]}]"
     return (f"{w.name}: {w.S} sessions x {n} cached tokens, {w.L} layers, {w.Hq}/{w.Hkv} heads, "
-            f"d {w.d}, pages of {w.P}, budget {int(w.budget_frac * 100)}%")
+            f"d {w.d}, pages of {w.P}{' (region-aligned)' if w.region_aligned else ''}, "
+            f"budget {int(w.budget_frac * 100)}%")
 
 
 def setup(w, steps_total, dev, fused=None):
@@ -67,22 +68,27 @@ def setup(w, steps_total, dev, fused=None):
     b, lam = g.region_priors(w)
     ws = C.with_overrides(w, steps=max(steps_total, 1))
     n_phys = g.pages_needed(ws, n0s)
-    max_pages = int(np.max((n0s + steps_total + w.P - 1) // w.P)) + 1
+    spans = [g.region_spans(w, s, int(n0s[s])) for s in range(w.S)]
+    pages = [PagedCache.pages_for(spans[s], w.P, w.region_aligned) for s in range(w.S)]
+    # every decode step may open a page with region-aligned pages
+    grow = steps_total if w.region_aligned else (steps_total + w.P - 1) // w.P
+    max_pages = max(pages) + grow + 1
     cache = PagedCache(L=w.L, Hq=w.Hq, Hkv=w.Hkv, d=w.d, P=w.P, S=w.S, max_pages=max_pages,
                        n_phys=n_phys, device=dev)
     perm = g.page_permutation(w, n_phys)
     pos = 0
     for s in range(w.S):
         n0 = int(n0s[s])
-        m = (n0 + w.P - 1) // w.P
+        m = pages[s]
         keys = g.torch_keys(w, s, n0, dev)
-        cache.load_session(s, keys, g.region_spans(w, s, n0), perm[pos:pos + m],
-                           budget=int(B[s]), clock=n0)
+        cache.load_session(s, keys, spans[s], perm[pos:pos + m], budget=int(B[s]), clock=n0,
+                           region_aligned=w.region_aligned)
         pos += m
         del keys
     cache.set_free_pages(perm[pos:][::-1])
     md = MemDecay(cache, torch.from_numpy(b), torch.from_numpy(lam), rho=w.rho, alpha=w.alpha,
-                  tau_scale=w.tau_scale, pinned_mask=w.pinned_mask, fused=fused)
+                  tau_scale=w.tau_scale, pinned_mask=w.pinned_mask, fused=fused,
+                  region_aligned=w.region_aligned)
     inputs = []
     for k in range(1, steps_total + 1):
         q = g.torch_queries(w, k, dev)

@@ -42,9 +42,14 @@
  *  page_serial  int32  [S][MP]   opening serial of each listed page (ascending)
  *  n_pages, n_tokens, clock, next_serial, budget   int32 [S]
  *  free_list    int32  [NP]      stack of free physical ids; free_count int32 [1]
- * Every page of a session except the last holds exactly P live tokens; the
- * last holds n_tokens - (n_pages - 1) * P.  Region codes follow the paper's
- * label list: system 0, plan 1, user 2, tool_in 3, tool_out 4, retrieval 5,
+ *  n_live       int32  [S]       tokens of each session (region-aligned pages only)
+ * Every page of a session except the last has all P slots in use; the last
+ * has n_tokens - (n_pages - 1) * P.  A slot in use holds a token, except with
+ * MD_FLAG_REGION_ALIGNED: there the slots of a page after its last token,
+ * left unused when the page was closed at a region boundary, are holes
+ * (region code MD_REGION_HOLE), n_tokens counts them with the tokens, and
+ * n_live counts the tokens alone.  Region codes follow the paper's label
+ * list: system 0, plan 1, user 2, tool_in 3, tool_out 4, retrieval 5,
  * scratchpad 6.
  */
 #ifndef MEMDECAY_H
@@ -56,7 +61,7 @@
 extern "C" {
 #endif
 
-#define MD_ABI_VERSION 2
+#define MD_ABI_VERSION 3
 
 typedef int32_t md_status;
 
@@ -89,6 +94,13 @@ enum {
                                 /* uniform attention level, as Sec. IV-D        */
                                 /* proposes: alpha * |K_t| * a_i in Eq. 4, with */
                                 /* |K_t| the session's tokens after the append  */
+#define MD_FLAG_REGION_ALIGNED 0x8  /* region-aligned pages (the allocator   */
+                                /* variant of Sec. III-D): an appended token    */
+                                /* opens a fresh page also when its region      */
+                                /* differs from that of the session's last      */
+                                /* token, and the last page's unused slots      */
+                                /* become holes; needs md_cache_view.n_live     */
+#define MD_REGION_HOLE    0xFF  /* region code of a hole slot                   */
 #define MD_FLAG_FUSED     0x2   /* observe on the fused kernel whenever it can  */
                                 /* hold the sessions.  With neither flag,       */
                                 /* md_init picks the path of the first observe  */
@@ -140,6 +152,8 @@ typedef struct md_cache_view {
     int32_t*  budget;
     int32_t*  free_list;
     int32_t*  free_count;
+    int32_t*  n_live;     /* MD_FLAG_REGION_ALIGNED: |K_t| per session; else   */
+                          /* ignored (may be NULL: |K_t| is n_tokens)          */
 } md_cache_view;
 
 typedef struct md_handle_s* md_handle;
@@ -169,7 +183,11 @@ md_status md_init(const md_config* cfg, const md_region_params* rp,
  *   append: each session's clock advances, t <- t + 1.  If new_k is not NULL
  *     the step's token joins the session's last page, or a page popped from
  *     the free list when the last page is full, with region new_region[s],
- *     t_ins = t_ref = t, a = 0 (Fig. 1, the decode engine's append).
+ *     t_ins = t_ref = t, a = 0 (Fig. 1, the decode engine's append).  With
+ *     MD_FLAG_REGION_ALIGNED the token also opens a fresh page when its
+ *     region differs from the last token's; the old page's unused slots
+ *     become holes (region MD_REGION_HOLE, t_ins = t_ref = 0, a = 0).
+ *     Holes take no part in anything below.
  *   attention mass: for every cached token i, A_i = (1 / (L Hq W)) sum over
  *     layers l, query heads h and window queries w of
  *     softmax_i(q_{w,l,h} . k_{l,h/G,i} / sqrt(d)), the softmax of window
@@ -178,7 +196,8 @@ md_status md_init(const md_config* cfg, const md_region_params* rp,
  *     cached token.
  *   EWMA (Eq. 2): a_i <- rho a_i + (1 - rho) A_i for every cached token.
  *   refresh (Eq. 3): t_ref_i <- t when A_i >= tau_scale / |K_t|, |K_t| the
- *     session's token count after the append.
+ *     session's token count after the append (n_live with region-aligned
+ *     pages, n_tokens otherwise).
  * q:          float32 [S][W][L][Hq][d] decode queries of steps t - W + 1 .. t,
  *             oldest first (device), or NULL for a decode step without an
  *             observation: then only the append and the clock advance run,
@@ -211,7 +230,8 @@ md_status md_score_pages(md_handle h, float* page_score, float* token_score);
 
 /*
  * md_select_evict — budget-aware page eviction (Alg. 1, lines 5-8): when a
- * session holds n > B tokens (B = budget[s]), the shortest prefix of its
+ * session holds n > B tokens (B = budget[s]; a page counts its tokens, not
+ * its holes), the shortest prefix of its
  * non-pinned pages in ascending (S_p, serial) order whose removal leaves
  * n <= B.  If even all non-pinned pages are not enough, all of them are
  * selected and infeasible[s] = 1 (the pinned set alone exceeds B).
@@ -226,7 +246,8 @@ md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_cou
 /*
  * md_compact — apply an eviction (Sec. III-E: irreversible): remove the
  * listed pages from each session's page table and serial list keeping the
- * order of the rest, update n_pages / n_tokens, and push the freed physical
+ * order of the rest, update n_pages / n_tokens (and n_live with
+ * region-aligned pages), and push the freed physical
  * ids onto the free list.  evict_serial / evict_count have md_select_evict's
  * layout and are normally its output; serials a session does not hold set
  * MD_DEV_BAD_EVICT and are ignored.

@@ -28,6 +28,8 @@ MD_DEV_TIMEOUT = 0x10
 MD_FLAG_NO_FUSED = 0x1
 MD_FLAG_FUSED = 0x2
 MD_FLAG_NORM_ATTENTION = 0x4
+MD_FLAG_REGION_ALIGNED = 0x8
+MD_REGION_HOLE = 0xFF
 
 EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_observe_step",
            "md_score_pages", "md_select_evict", "md_compact", "md_read_device_status",
@@ -58,7 +60,7 @@ class md_region_params(ctypes.Structure):
 class md_cache_view(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "k_pool", "region", "t_ins", "t_ref", "importance", "page_table", "page_serial",
-        "n_pages", "n_tokens", "clock", "next_serial", "budget", "free_list", "free_count")]
+        "n_pages", "n_tokens", "clock", "next_serial", "budget", "free_list", "free_count", "n_live")]
 
 
 class MemDecayError(RuntimeError):

@@ -41,6 +41,7 @@ class PagedCache:
         self.page_serial = torch.full((S, max_pages), -1, **i32)
         self.n_pages = torch.zeros(S, **i32)
         self.n_tokens = torch.zeros(S, **i32)
+        self.n_live = torch.zeros(S, **i32)   # tokens without holes (region-aligned pages)
         self.clock = torch.zeros(S, **i32)
         self.next_serial = torch.zeros(S, **i32)
         self.budget = torch.zeros(S, **i32)
@@ -51,31 +52,65 @@ class PagedCache:
         v = B.md_cache_view()
         for name in ("k_pool", "region", "t_ins", "t_ref", "importance", "page_table",
                      "page_serial", "n_pages", "n_tokens", "clock", "next_serial", "budget",
-                     "free_list", "free_count"):
+                     "free_list", "free_count", "n_live"):
             setattr(v, name, getattr(self, name).data_ptr())
         return v
 
+    @staticmethod
+    def positions(region, P: int, region_aligned: bool) -> np.ndarray:
+        """Slot position (page * P + offset) of each prompt token in the
+        session's page sequence: consecutive, or with region-aligned pages a
+        fresh page at every region change (the positions skipped are holes)."""
+        reg = np.asarray(region, dtype=np.int64)
+        n = reg.size
+        if not region_aligned or n == 0:
+            return np.arange(n, dtype=np.int64)
+        pos = np.empty(n, dtype=np.int64)
+        p = 0
+        for i in range(n):
+            if i > 0 and reg[i] != reg[i - 1] and p % P:
+                p += P - p % P          # close the page at the region boundary
+            pos[i] = p
+            p += 1
+        return pos
+
+    @classmethod
+    def pages_for(cls, region, P: int, region_aligned: bool) -> int:
+        """Pages a prompt with these region codes takes."""
+        n = len(region)
+        return 0 if n == 0 else (int(cls.positions(region, P, region_aligned)[-1]) + P) // P
+
     def load_session(self, s: int, keys: torch.Tensor, region, page_ids: Sequence[int],
-                     budget: int, clock: int, t_ins=None):
+                     budget: int, clock: int, t_ins=None, region_aligned: bool = False):
         """Place a session's prompt: keys bf16 [n][L][Hkv][d] (device), region
-        codes [n], physical page ids in logical order (ceil(n / P) of them).
-        Token i gets t_ins = t_ref = t_ins[i] (default i) and importance 0."""
+        codes [n], physical page ids in logical order (as many as the layout
+        takes: ceil(n / P), or with region-aligned pages one more per region
+        change inside a page; ``pages_for``).  Token i gets t_ins = t_ref =
+        t_ins[i] (default i) and importance 0; holes get the hole code."""
         P = self.P
         n = int(keys.shape[0])
-        m = (n + P - 1) // P
+        pos = self.positions(region, P, region_aligned)
+        n_pos = int(pos[-1]) + 1 if n else 0
+        m = (n_pos + P - 1) // P
         if len(page_ids) != m or m > self.max_pages:
-            raise ValueError("need ceil(n / P) page ids within max_pages")
+            raise ValueError("need one page id per page of the layout, within max_pages")
         ids = torch.as_tensor(np.asarray(page_ids, dtype=np.int64), device=self.device)
-        pad = m * P - n
+        posd = torch.as_tensor(pos, device=self.device)
         k = keys.to(self.device, torch.bfloat16)
-        if pad:
-            k = torch.cat([k, torch.zeros((pad,) + tuple(k.shape[1:]), dtype=k.dtype, device=k.device)])
+        full = torch.zeros((m * P,) + tuple(k.shape[1:]), dtype=k.dtype, device=k.device)
+        full[posd] = k
         # [m][P][L][Hkv][d] -> [m][L][Hkv][P][d]
-        self.k_pool.index_copy_(0, ids, k.view(m, P, self.L, self.Hkv, self.d).permute(0, 2, 3, 1, 4))
+        self.k_pool.index_copy_(0, ids, full.view(m, P, self.L, self.Hkv, self.d).permute(0, 2, 3, 1, 4))
         reg = torch.as_tensor(np.asarray(region, dtype=np.uint8), device=self.device)
         t0 = torch.arange(n, dtype=torch.int32, device=self.device) if t_ins is None else \
             torch.as_tensor(np.asarray(t_ins, dtype=np.int32), device=self.device)
-        flat = (ids.view(-1, 1) * P + torch.arange(P, device=self.device).view(1, -1)).view(-1)[:n]
+        slots = (ids.view(-1, 1) * P + torch.arange(P, device=self.device).view(1, -1)).view(-1)
+        used = slots[:n_pos]
+        self.region.view(-1)[used] = B.MD_REGION_HOLE
+        self.t_ins.view(-1)[used] = 0
+        self.t_ref.view(-1)[used] = 0
+        self.importance.view(-1)[used] = 0.0
+        flat = slots[posd]
         self.region.view(-1)[flat] = reg
         self.t_ins.view(-1)[flat] = t0
         self.t_ref.view(-1)[flat] = t0
@@ -85,7 +120,8 @@ class PagedCache:
         self.page_serial[s, :m] = torch.arange(m, dtype=torch.int32, device=self.device)
         self.page_serial[s, m:] = -1
         self.n_pages[s] = m
-        self.n_tokens[s] = n
+        self.n_tokens[s] = n_pos
+        self.n_live[s] = n
         self.clock[s] = clock
         self.next_serial[s] = m
         self.budget[s] = budget
@@ -105,7 +141,8 @@ class MemDecay:
     def __init__(self, cache: PagedCache, base_priority: torch.Tensor, decay_rate: torch.Tensor, *,
                  rho: float, alpha: float, tau_scale: float, pinned_mask: int,
                  n_regions: int = 7, stream: Optional[torch.cuda.Stream] = None,
-                 fused: Optional[bool] = None, attention_norm: bool = False, window: int = 1):
+                 fused: Optional[bool] = None, attention_norm: bool = False, window: int = 1,
+                 region_aligned: bool = False):
         # fused: True = always the fused kernel, False = always the
         # multi-kernel path, None = the library picks from the cache's sizes
         self.cache = cache
@@ -118,7 +155,8 @@ class MemDecay:
                           n_regions=n_regions, pinned_region_mask=pinned_mask, rho=rho,
                           alpha=alpha, tau_scale=tau_scale,
                           flags=(0 if fused is None else (B.MD_FLAG_FUSED if fused else B.MD_FLAG_NO_FUSED))
-                          | (B.MD_FLAG_NORM_ATTENTION if attention_norm else 0),
+                          | (B.MD_FLAG_NORM_ATTENTION if attention_norm else 0)
+                          | (B.MD_FLAG_REGION_ALIGNED if region_aligned else 0),
                           window=window)
         rp = B.md_region_params(base_priority=self.b.data_ptr(), decay_rate=self.lam.data_ptr())
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)

@@ -106,7 +106,8 @@ const char* md_status_str(md_status s) {
 
 static md_status validate_config(const md_config* c) {
     if (c == nullptr) return MD_E_INVALID;
-    if ((c->flags & ~(MD_FLAG_NO_FUSED | MD_FLAG_FUSED | MD_FLAG_NORM_ATTENTION)) != 0) return MD_E_INVALID;
+    if ((c->flags & ~(MD_FLAG_NO_FUSED | MD_FLAG_FUSED | MD_FLAG_NORM_ATTENTION | MD_FLAG_REGION_ALIGNED)) != 0)
+        return MD_E_INVALID;
     if ((c->flags & MD_FLAG_NO_FUSED) && (c->flags & MD_FLAG_FUSED)) return MD_E_INVALID;
     if (c->n_layers < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1) return MD_E_INVALID;
     if (c->n_q_heads % c->n_kv_heads != 0) return MD_E_INVALID;
@@ -132,8 +133,10 @@ static md_status validate_config(const md_config* c) {
     return MD_OK;
 }
 
-static md_status validate_view(const md_cache_view* v) {
+static md_status validate_view(const md_cache_view* v, bool region_aligned) {
     if (v == nullptr) return MD_E_INVALID;
+    if (region_aligned && (v->n_live == nullptr || !aligned(v->n_live, 4) || !aligned(v->region, 4)))
+        return MD_E_INVALID;
     const void* ptrs[] = {v->k_pool, v->region, v->t_ins, v->t_ref, v->importance,
                           v->page_table, v->page_serial, v->n_pages, v->n_tokens, v->clock,
                           v->next_serial, v->budget, v->free_list, v->free_count};
@@ -154,7 +157,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     *out = nullptr;
     md_status st = validate_config(cfg);
     if (st != MD_OK) return st;
-    st = validate_view(cv);
+    st = validate_view(cv, (cfg->flags & MD_FLAG_REGION_ALIGNED) != 0);
     if (st != MD_OK) return st;
     if (rp == nullptr || rp->base_priority == nullptr || rp->decay_rate == nullptr) return MD_E_INVALID;
     if (!aligned(rp->base_priority, 4) || !aligned(rp->decay_rate, 4)) return MD_E_INVALID;
@@ -180,6 +183,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     dm.tau_scale = cfg->tau_scale;
     dm.fused = ((cfg->flags & MD_FLAG_NO_FUSED) || dm.W > 1) ? 0 : 1;
     dm.norm_attn = (cfg->flags & MD_FLAG_NORM_ATTENTION) ? 1 : 0;
+    dm.aligned = (cfg->flags & MD_FLAG_REGION_ALIGNED) ? 1 : 0;
 
     // ---- from here on the HIP runtime is used
     int dev = 0;
@@ -207,10 +211,12 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     dm.T = md::attend_unit_tokens(dm.G);
     if (dm.fused) {
         const size_t lds = md::attend_lds_bytes(dm.G);
-        if (hipFuncSetAttribute(md::attend_kernel(dm.G), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+        if (hipFuncSetAttribute(md::attend_kernel(dm.G, dm.aligned), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)lds) !=
             hipSuccess) {
             (void)hipGetLastError();
-        } else if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(dm.G), md::attend_threads(dm.G),
+        } else if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(dm.G, dm.aligned),
+                                                                md::attend_threads(dm.G),
                                                                 lds) != hipSuccess) {
             return MD_E_HIP;
         }
@@ -288,6 +294,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     h->v.page_serial = cv->page_serial;
     h->v.n_pages = cv->n_pages;
     h->v.n_tokens = cv->n_tokens;
+    h->v.n_live = dm.aligned ? cv->n_live : cv->n_tokens;
     h->v.clock = cv->clock;
     h->v.next_serial = cv->next_serial;
     h->v.budget = cv->budget;

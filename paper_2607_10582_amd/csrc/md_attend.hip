@@ -52,6 +52,7 @@ struct AttendDims {
     int wg_per_cu, n_cu, S, n_regions, norm_attn;
     uint32_t pin_mask;
     float rho, tau_scale, alpha;
+    int aligned;
 };
 
 struct AttendArgs {
@@ -76,6 +77,7 @@ struct AttendArgs {
     unsigned long long* unorm;
     int32_t* status;
     int32_t* probe;    // check mode only: [arrivals, least seen]
+    const int32_t* n_live;   // tokens |K_t| (the n_tokens array unless pages are region-aligned)
 };
 
 // LDS row stride (floats) of a head's values: W waves of KT tiles
@@ -163,6 +165,7 @@ __device__ __forceinline__ float wave_sum_dpp(float v) {
 struct Unit {
     int s, j, ntok, nt_s, nu, us;
     uint64_t deadline;   // real-time tick after which the unit stops waiting
+    int nl_s;            // region-aligned pages: the session's tokens |K_t| (nt_s counts holes too)
 };
 
 // First query row (layer * Hq + KV head * G) of (layer, KV head) row r:
@@ -170,8 +173,10 @@ struct Unit {
 __device__ __forceinline__ int qrow0(const AttendDims& dm, int r) { return r * dm.G; }
 
 // One wave's part of a unit.  W = waves per workgroup, NH = normaliser
-// heads per wave (G <= W NH), KT = tiles per wave (units of 16 W KT tokens).
-template <int W, int NH, int KT>
+// heads per wave (G <= W NH), KT = tiles per wave (units of 16 W KT tokens),
+// AL = region-aligned pages (hole slots are masked; a separate instantiation
+// keeps the plain layout's register budget).
+template <int W, int NH, int KT, bool AL>
 __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendArgs& a, const Lds& sm,
                                             const Unit& un, int wv, int lane, uint32_t tag) {
     constexpr int KQ = (W * NH * 32 + 64 * W - 1) / (64 * W);   // float4 of the query row per lane
@@ -203,7 +208,23 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     }
     const unsigned long long vmask = __ballot(myok);
     constexpr unsigned long long kAll = (1ull << KT) - 1;
-    const bool wave_full = (vmask & kAll) == kAll && wtok0 + 16 * KT <= un.ntok;
+    // Region-aligned pages: a page's holes follow its last token, so the
+    // holes of a 16-slot tile are a suffix of it; byte u of `lims` is the
+    // number of slots of tile u before its first hole (16: none).  Lane
+    // u < KT counts them for tile u.  Wave-uniform.
+    uint32_t lims = 0x10101010u;
+    if constexpr (AL) {
+        int mylim = 16;
+        if (myok) {
+            const u32x4 rb = *reinterpret_cast<const u32x4*>(a.region + myslot);
+            for (int k = 15; k >= 0; --k)
+                if (((rb[k >> 2] >> (8 * (k & 3))) & 0xffu) == (uint32_t)kHole) mylim = k;
+        }
+        lims = 0;
+#pragma unroll
+        for (int u = 0; u < KT; ++u) lims |= (uint32_t)__builtin_amdgcn_readlane(mylim, u) << (8 * u);
+    }
+    const bool wave_full = (vmask & kAll) == kAll && wtok0 + 16 * KT <= un.ntok && (!AL || lims == 0x10101010u);
 
     // K tile u of row r in the MFMA A layout; a tile without cached tokens,
     // or past the last row, reads the pool's first tile (its logits are
@@ -514,7 +535,9 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
             for (int u = 0; u < KT; ++u)
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    if (!((vmask >> u) & 1ull) || wtok0 + 16 * u + 4 * g + i >= un.ntok) xs[u][i] = -INFINITY;
+                    if (!((vmask >> u) & 1ull) || wtok0 + 16 * u + 4 * g + i >= un.ntok ||
+                        (AL && 4 * g + i >= (int)((lims >> (8 * u)) & 0xffu)))
+                        xs[u][i] = -INFINITY;
         }
         float mx = -INFINITY;
 #pragma unroll
@@ -563,13 +586,16 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // start at multiples of 64 tokens.
     const int t_now = a.clock[un.s];
     const size_t rbase = (size_t)un.s * dm.n_regions;
-    const float aw = attention_weight(dm.alpha, dm.norm_attn, un.nt_s);
+    const int n_tok = AL ? un.nl_s : un.nt_s;   // |K_t|
+    const float aw = attention_weight(dm.alpha, dm.norm_attn, n_tok);
 #pragma unroll
     for (int k = 0; k < kTok; ++k) {
         const int lt = lane + 64 * k;   // wave-local token
         const int tile = lt >> 4;
         const int slot0 = __shfl(myslot, tile);
-        const bool live = wtok0 + lt < un.ntok && ((vmask >> tile) & 1ull);
+        // holes hold no token
+        const bool live = wtok0 + lt < un.ntok && ((vmask >> tile) & 1ull) &&
+                          (!AL || (lt & 15) < (int)((lims >> (8 * tile)) & 0xffu));
         float sc = 0.0f;
         bool pin = false;
         if (live) {
@@ -578,7 +604,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
             const float an = fmaf(dm.rho, a.imp[si], (1.0f - dm.rho) * abar);
             a.imp[si] = an;
             int tr;
-            if (abar >= dm.tau_scale / (float)un.nt_s) {
+            if (abar >= dm.tau_scale / (float)n_tok) {
                 tr = t_now;
                 a.t_ref[si] = tr;
             } else {
@@ -682,7 +708,7 @@ __device__ void claim_sessions(const AttendArgs& a, int* xs, int lane_no, int ca
 // the whole register file.  (Workgroups that take a whole CU, with eight
 // waves or with eight tiles per wave, measured slower: the two workgroups'
 // row barriers fall at different times and fill each other's gaps.)
-template <int W, int NH, int KT>
+template <int W, int NH, int KT, bool AL>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(NH == 4 ? 1 : 2)))
 k_attend(AttendDims dm, AttendArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -767,6 +793,7 @@ k_attend(AttendDims dm, AttendArgs a) {
         un.nu = a.ustart[s + 1] - un.us;
         un.j = u0 + w - un.us;
         un.nt_s = a.n_tokens[s];
+        un.nl_s = AL ? a.n_live[s] : 0;
         constexpr int kT = 16 * W * KT;
         un.ntok = min(kT, un.nt_s - un.j * kT);
         un.deadline = now_ticks() + kUnitTicks;
@@ -774,7 +801,7 @@ k_attend(AttendDims dm, AttendArgs a) {
         // arithmetic is not hoisted out of the pass loop and kept live.
         int lane = (int)threadIdx.x & 63;
         asm volatile("" : "+v"(lane));
-        attend_wave<W, NH, KT>(dm, a, sm, un, wv, lane, tag);
+        attend_wave<W, NH, KT, AL>(dm, a, sm, un, wv, lane, tag);
     }
 }
 
@@ -785,22 +812,27 @@ size_t attend_lds_bytes(int G) {
     return rowbuf_bytes(G, W, attend_unit_tokens(G) / (16 * W)) + qs_bytes(G) + wstat_bytes(W) + kNormBytes;
 }
 
-const void* attend_kernel(int G) {
-    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<4, 1, 4>);
-    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<4, 2, 4>);
-    return reinterpret_cast<const void*>(&k_attend<4, 4, 4>);
+const void* attend_kernel(int G, int aligned) {
+    if (aligned) {
+        if (G <= 4) return reinterpret_cast<const void*>(&k_attend<4, 1, 4, true>);
+        if (G <= 8) return reinterpret_cast<const void*>(&k_attend<4, 2, 4, true>);
+        return reinterpret_cast<const void*>(&k_attend<4, 4, 4, true>);
+    }
+    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<4, 1, 4, false>);
+    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<4, 2, 4, false>);
+    return reinterpret_cast<const void*>(&k_attend<4, 4, 4, false>);
 }
 
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q, float* abar_out,
                          hipStream_t st) {
     AttendDims ad{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.MP, dm.NP, dm.R, dm.LHkv,
                   dm.wg_per_cu, dm.n_wg / dm.wg_per_cu, dm.S, dm.n_regions, dm.norm_attn, dm.pin_mask,
-                  dm.rho, dm.tau_scale, dm.alpha};
+                  dm.rho, dm.tau_scale, dm.alpha, dm.aligned};
     AttendArgs aa{v.k_pool, v.page_table, v.n_tokens, v.clock, v.region, v.b, v.lam, v.imp, v.t_ref,
                   sc.pscore, q, abar_out, sc.ustart, sc.plan, sc.epoch, sc.claim, sc.lane_box, sc.ustat,
-                  sc.unorm, sc.status, nullptr};
+                  sc.unorm, sc.status, nullptr, v.n_live};
     void* args[] = {&ad, &aa};
-    return hipLaunchCooperativeKernel(attend_kernel(dm.G), dim3(dm.n_wg), dim3(attend_threads(dm.G)), args,
+    return hipLaunchCooperativeKernel(attend_kernel(dm.G, dm.aligned), dim3(dm.n_wg), dim3(attend_threads(dm.G)), args,
                                       (unsigned)attend_lds_bytes(dm.G), st);
 }
 
@@ -812,7 +844,7 @@ hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, hipStre
     if (e == hipSuccess) e = hipMemsetD32Async(reinterpret_cast<hipDeviceptr_t>(probe + 1), 1 << 30, 1, st);
     if (e != hipSuccess) return e;
     void* args[] = {&ad, &aa};
-    return hipLaunchCooperativeKernel(attend_kernel(dm.G), dim3(n_wg), dim3(attend_threads(dm.G)), args,
+    return hipLaunchCooperativeKernel(attend_kernel(dm.G, dm.aligned), dim3(n_wg), dim3(attend_threads(dm.G)), args,
                                       (unsigned)attend_lds_bytes(dm.G), st);
 }
 

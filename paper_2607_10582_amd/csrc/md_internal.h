@@ -27,6 +27,7 @@ constexpr int kConsumeLag = 7;   // rows a unit runs ahead of the row it normali
 constexpr int kRowBufs = kConsumeLag + 1;       // rows of logits held in LDS
 
 constexpr int kDevCorrupt = MD_DEV_CORRUPT;
+constexpr int kHole = MD_REGION_HOLE;   // region code of a hole slot (region-aligned pages)
 
 struct Dims {
     int L, Hq, Hkv, G, P, Pshift, S, MP, NP, R, LHkv, n_regions, max_chunks;
@@ -35,6 +36,7 @@ struct Dims {
     int spill;     // 1: some session may not fit a pass (the spill kernels run)
     int multi;     // 1: the multi-kernel path runs at some step (its scratch exists)
     int norm_attn; // 1: the attention term of Eq. 4 is alpha * |K_t| * a_i
+    int aligned;   // 1: region-aligned pages (hole slots; n_live counts the tokens)
     int n_wg;      // k_attend workgroups (all co-resident)
     int wg_per_cu; // k_attend workgroups per CU (n_wg = wg_per_cu * CUs)
     int lane_cap;  // units one lane of k_attend workgroups holds (one workgroup per CU)
@@ -54,6 +56,7 @@ struct View {
     int32_t* page_serial;
     int32_t* n_pages;
     int32_t* n_tokens;
+    int32_t* n_live;   // [S] tokens |K_t|: the n_tokens array itself unless aligned
     int32_t* clock;
     int32_t* next_serial;
     int32_t* budget;
@@ -101,7 +104,7 @@ hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st);
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q,
                          float* abar_out, hipStream_t st);
 size_t attend_lds_bytes(int G);
-const void* attend_kernel(int G);   // the instantiation for query group size G
+const void* attend_kernel(int G, int aligned);   // the instantiation for group size G and page layout
 // Launch the fused kernel in check mode with n_wg workgroups: every wave
 // waits (bounded, ~20 ms) until all workgroups have arrived; probe[1]
 // receives the fewest arrivals any workgroup saw (probe: 2 device ints).

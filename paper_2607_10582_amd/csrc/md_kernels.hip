@@ -36,17 +36,36 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         const int t = v.clock[s] + 1;
         v.clock[s] = t;
         int phys = -1, slot = 0;
-        const int np = v.n_pages[s], nt = v.n_tokens[s];
+        const int np = v.n_pages[s];
+        int nt = v.n_tokens[s];
         if (new_k != nullptr && counters_ok(np, nt, dm)) {
             const size_t row = (size_t)s * dm.MP;
-            if (np > 0 && nt < np * dm.P) {
+            bool open = !(np > 0 && nt < np * dm.P);
+            if (!open) {
                 const int p = v.page_table[row + np - 1];
                 if (p >= 0 && p < dm.NP) {
                     phys = p;
                     slot = nt - (np - 1) * dm.P;
+                    const size_t s0 = (size_t)p * dm.P;
+                    // region-aligned pages: a new region closes the last
+                    // page, its unused slots becoming holes
+                    if (dm.aligned && slot > 0 && v.region[s0 + slot - 1] != new_region[s]) {
+                        for (int o = slot; o < dm.P; ++o) {
+                            v.region[s0 + o] = (uint8_t)kHole;
+                            v.t_ins[s0 + o] = 0;
+                            v.t_ref[s0 + o] = 0;
+                            v.imp[s0 + o] = 0.0f;
+                        }
+                        v.n_tokens[s] = nt = np * dm.P;
+                        phys = -1;
+                        open = true;
+                    }
                 } else {
                     atomicOr(sc.status, kDevCorrupt);
                 }
+            }
+            if (!open) {
+                // the token joins the last page (or the page was corrupt)
             } else if (np < dm.MP) {
                 const int old = atomicSub(v.free_count, 1);
                 if (old > 0 && old <= dm.NP) {
@@ -70,6 +89,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             }
             if (phys >= 0) {
                 v.n_tokens[s] = nt + 1;
+                if (dm.aligned) v.n_live[s] += 1;
                 const size_t si = (size_t)phys * dm.P + slot;
                 v.region[si] = new_region[s];
                 v.t_ins[si] = t;
@@ -177,7 +197,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             it[k] = ch * dm.LHkv;
             ti[k] = spill ? (nt + kTile - 1) / kTile : 0;
             si[k] = (nt + kTile - 1) / kTile;
-            my_tokens += nt;
+            my_tokens += (dm.aligned && nt > 0) ? load_agent(v.n_live + s2) : nt;
         }
         my_units += uu[k];
         my_items += it[k];
@@ -261,6 +281,7 @@ __device__ __forceinline__ void cursor_next(Cursor& cu, const int* s_pref, int S
 struct LogitsDims {
     int L, Hq, Hkv, G, P, Pshift, S, MP, NP, R, LHkv, max_chunks;
     int W, Gw;   // window queries per observation; MFMA columns G * W
+    int aligned; // region-aligned pages: hole slots are masked
 };
 
 // B operands of one row (session s, lkv = layer * Hkv + KV head) in
@@ -365,7 +386,7 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
          const int32_t* __restrict__ n_tokens, const float* __restrict__ q,
          float* __restrict__ logits, float2* __restrict__ cstats, int32_t* status,
          const int32_t* __restrict__ item_prefix, const int32_t* __restrict__ t_ins,
-         const int32_t* __restrict__ clock) {
+         const int32_t* __restrict__ clock, const uint8_t* __restrict__ region) {
     __shared__ int s_pref[kMaxSessions + 1];
     const int S = dm.S;
     for (int i = threadIdx.x; i <= S; i += blockDim.x) s_pref[i] = item_prefix[i];
@@ -437,20 +458,24 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
                 if (t < 4) load_tile(ring[t & 3], dm, k_pool, cur, t + 4, cu.lkv, voff);
                 else load_tile(ring[t & 3], dm, k_pool, nxt, t - 4, cu.lkv, voff);
 
-                // base-2 logits; tokens past the session's count, and tokens
-                // newer than the column's window query, are masked out
+                // base-2 logits; tokens past the session's count, tokens
+                // newer than the column's window query, and hole slots are
+                // masked out
                 const bool tvalid = cur.vmask & (1u << t);
                 int tins[4] = {0, 0, 0, 0};
                 if (dm.W > 1 && tvalid) {
 #pragma unroll
                     for (int i = 0; i < 4; ++i) tins[i] = t_ins[cur.slot0[t] + 4 * g + i];
                 }
+                uint32_t rb = 0;   // region codes of this lane's four tokens
+                if (dm.aligned && tvalid) rb = *reinterpret_cast<const uint32_t*>(region + cur.slot0[t] + 4 * g);
                 float x[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int tok = tok0 + 16 * t + 4 * g + i;
                     const bool seen = dm.W == 1 || tins[i] <= t_lim;
-                    x[i] = (tvalid && tok < cur.nt && seen) ? acc[i] * kLogitScale : -INFINITY;
+                    const bool hole = dm.aligned && ((rb >> (8 * i)) & 0xffu) == (uint32_t)kHole;
+                    x[i] = (tvalid && tok < cur.nt && seen && !hole) ? acc[i] * kLogitScale : -INFINITY;
                 }
                 const float mn = fmaxf(m, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
                 const bool live = mn != -INFINITY;
@@ -491,9 +516,10 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
 hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q, int n_blocks,
                          hipStream_t st) {
     LogitsDims ld{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.S, dm.MP, dm.NP, dm.R, dm.LHkv, dm.max_chunks,
-                  dm.W, dm.G * dm.W};
+                  dm.W, dm.G * dm.W, dm.aligned};
     hipLaunchKernelGGL(k_logits, dim3(n_blocks), dim3(256), 0, st, ld, v.k_pool, v.page_table,
-                       v.n_tokens, q, sc.logits, sc.cstats, sc.status, sc.item_prefix, v.t_ins, v.clock);
+                       v.n_tokens, q, sc.logits, sc.cstats, sc.status, sc.item_prefix, v.t_ins, v.clock,
+                       v.region);
     return hipGetLastError();
 }
 
@@ -564,6 +590,8 @@ __global__ void __launch_bounds__(256) k_mass(Dims dm, View v, Scratch sc, float
             if ((unsigned)phys >= (unsigned)dm.NP) {
                 valid = false;
                 atomicOr(sc.status, kDevCorrupt);
+            } else if (dm.aligned && v.region[(size_t)phys * dm.P + slot] == kHole) {
+                valid = false;   // a hole holds no token
             } else {
                 const float* lp = sc.logits + (size_t)phys * dm.R * dm.P + slot;
 #pragma unroll 8
@@ -581,7 +609,7 @@ __global__ void __launch_bounds__(256) k_mass(Dims dm, View v, Scratch sc, float
             const size_t si = (size_t)phys * dm.P + slot;
             const float a = v.imp[si];
             v.imp[si] = fmaf(dm.rho, a, one_m_rho * abar);
-            if (abar >= dm.tau_scale / (float)nt) v.t_ref[si] = v.clock[s];
+            if (abar >= dm.tau_scale / (float)v.n_live[s]) v.t_ref[si] = v.clock[s];
             if (abar_out != nullptr) abar_out[si] = abar;
         }
         __syncthreads();
@@ -626,19 +654,23 @@ __global__ void __launch_bounds__(256) k_score(Dims dm, View v, Scratch sc, floa
             } else {
                 const size_t si = (size_t)phys * dm.P + (tok - (pg << dm.Pshift));
                 int r = v.region[si];
-                if (r >= dm.n_regions) {
-                    atomicOr(sc.status, kDevCorrupt);
-                    r = dm.n_regions - 1;
-                }
-                pin = (dm.pin_mask >> r) & 1u;
-                if (pin) {
-                    sc_i = INFINITY;
+                if (dm.aligned && r == kHole) {
+                    valid = false;   // a hole holds no token
                 } else {
-                    const size_t ri = (size_t)s * dm.n_regions + r;
-                    sc_i = retention_score(v.b[ri], v.lam[ri], t, v.t_ref[si],
-                                           attention_weight(dm.alpha, dm.norm_attn, nt), v.imp[si]);
+                    if (r >= dm.n_regions) {
+                        atomicOr(sc.status, kDevCorrupt);
+                        r = dm.n_regions - 1;
+                    }
+                    pin = (dm.pin_mask >> r) & 1u;
+                    if (pin) {
+                        sc_i = INFINITY;
+                    } else {
+                        const size_t ri = (size_t)s * dm.n_regions + r;
+                        sc_i = retention_score(v.b[ri], v.lam[ri], t, v.t_ref[si],
+                                               attention_weight(dm.alpha, dm.norm_attn, v.n_live[s]), v.imp[si]);
+                    }
+                    if (token_score != nullptr) token_score[si] = sc_i;
                 }
-                if (token_score != nullptr) token_score[si] = sc_i;
             }
         }
         float ps;
@@ -658,6 +690,24 @@ hipError_t launch_score(const Dims& dm, const View& v, const Scratch& sc, float*
 
 // ---------------------------------------------------------------- select
 
+// Tokens of page i (physical id phys) of a session with np pages and nt
+// slots in use: P, or the last page's slots; with region-aligned pages the
+// slots that are not holes.
+__device__ int page_tokens(const Dims& dm, const View& v, int phys, int i, int np, int nt) {
+    const int used = (i == np - 1) ? nt - (np - 1) * dm.P : dm.P;
+    if (!dm.aligned) return used;
+    if ((unsigned)phys >= (unsigned)dm.NP) return 0;
+    const uint32_t* w = reinterpret_cast<const uint32_t*>(v.region + (size_t)phys * dm.P);
+    int holes = 0;
+    for (int k = 0; k < dm.P / 4; ++k) {
+        const uint32_t x = w[k];
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+            holes += (4 * k + b < used && ((x >> (8 * b)) & 0xffu) == (uint32_t)kHole) ? 1 : 0;
+    }
+    return used - holes;
+}
+
 // Radix select over the float bit patterns of the page scores (non-negative,
 // so the unsigned order of the bits is the numeric order), weighted by each
 // page's live token count: the threshold key T is where the ascending
@@ -674,7 +724,7 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
     __shared__ int sh_digit, sh_before;
     const int tid = threadIdx.x;
     const int np = v.n_pages[s], nt = v.n_tokens[s], B = v.budget[s];
-    const int need = nt - B;
+    const int need = v.n_live[s] - B;
     if (!sc.valid[s] || need <= 0 || np == 0) {
         if (tid == 0) {
             ev_count[s] = 0;
@@ -685,7 +735,7 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
     const uint32_t kInf = 0x7F800000u;
     const float* ps = sc.pscore + (size_t)s * dm.MP;
     const int* ser = v.page_serial + (size_t)s * dm.MP;
-    const int tailw = nt - (np - 1) * dm.P;
+    const int* ptab = v.page_table + (size_t)s * dm.MP;
     const int per = (np + kSelThreads - 1) / kSelThreads;
     const int i0 = min(np, tid * per), i1 = min(np, i0 + per);
     uint32_t key[kPerThread];
@@ -698,7 +748,7 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
         wt[k] = 0;
         if (i < i1) {
             key[k] = __float_as_uint(ps[i]);
-            wt[k] = (i == np - 1) ? tailw : dm.P;
+            wt[k] = page_tokens(dm, v, dm.aligned ? ptab[i] : 0, i, np, nt);
             if (key[k] < kInf) wsum += wt[k];
         }
     }
@@ -813,7 +863,7 @@ __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratc
     const int i0 = min(np, tid * per), i1 = min(np, i0 + per);
     int ph[kPerThread], se[kPerThread];
     bool keep[kPerThread];
-    int n_keep = 0, n_gone = 0;
+    int n_keep = 0, n_gone = 0, live_gone = 0;
 #pragma unroll
     for (int k = 0; k < kPerThread; ++k) {
         const int i = i0 + k;
@@ -831,11 +881,14 @@ __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratc
             keep[k] = !gone;
             n_keep += gone ? 0 : 1;
             n_gone += gone ? 1 : 0;
+            if (gone) live_gone += page_tokens(dm, v, ph[k], i, np, nt);
         }
     }
     int kept_total, gone_total;
     int kpos = block_exclusive_scan(n_keep, lds, &kept_total);
     int gpos = block_exclusive_scan(n_gone, lds, &gone_total);
+    int live_gone_total;
+    block_exclusive_scan(live_gone, lds, &live_gone_total);
     if (tid == 0) {
         if (gone_total != cnt) atomicOr(sc.status, MD_DEV_BAD_EVICT);
         sh_base = gone_total > 0 ? atomicAdd(v.free_count, gone_total) : 0;
@@ -867,8 +920,9 @@ __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratc
         const int nt_new = last_kept ? nt - gone_total * dm.P : kept_total * dm.P;
         v.n_pages[s] = kept_total;
         v.n_tokens[s] = nt_new;
+        if (dm.aligned) v.n_live[s] -= live_gone_total;
         atomicAdd(&sc.counters[2], (unsigned long long)gone_total);
-        atomicAdd(&sc.counters[3], (unsigned long long)(nt - nt_new));
+        atomicAdd(&sc.counters[3], (unsigned long long)live_gone_total);
     }
 }
 

@@ -27,6 +27,7 @@ import numpy as np
 import torch
 
 import oracle
+from paper_2607_10582_amd import binding as B
 from paper_2607_10582_amd.cache import MemDecay, PagedCache
 from synth import configs as C
 from synth import generator as g
@@ -109,9 +110,14 @@ class Pair:
         self.query_gain = query_gain
         self.planted = planted
         P = w.P
+        al = w.region_aligned
         w_steps = C.with_overrides(w, steps=self.steps)
         n_phys = g.pages_needed(w_steps, self.n0s) + n_phys_extra
-        mp = max(int(np.max((self.n0s + self.steps + P - 1) // P)) + 1, 1) if max_pages is None else max_pages
+        regs = [g.region_spans(w, s, int(self.n0s[s])) if regions is None else np.asarray(regions[s], np.uint8)
+                for s in range(S)]
+        pages = [PagedCache.pages_for(regs[s], P, al) for s in range(S)]
+        grow = self.steps if al else (self.steps + P - 1) // P
+        mp = max(max(pages) + grow + 1, 1) if max_pages is None else max_pages
         self.cache = PagedCache(L=w.L, Hq=w.Hq, Hkv=w.Hkv, d=w.d, P=P, S=S, max_pages=mp,
                                 n_phys=n_phys, device=self.dev)
         perm = g.page_permutation(w, n_phys)
@@ -119,8 +125,8 @@ class Pair:
         self.oracles: Dict[int, oracle.Session] = {}
         for s in range(S):
             n0 = int(self.n0s[s])
-            reg = g.region_spans(w, s, n0) if regions is None else np.asarray(regions[s], np.uint8)
-            m = (n0 + P - 1) // P
+            reg = regs[s]
+            m = pages[s]
             ids = perm[pos:pos + m]
             pos += m
             if backend == "numpy":
@@ -134,7 +140,7 @@ class Pair:
                 kb = torch_to_bits(kt) if s in self.oracle_sessions else None
             if n0:
                 self.cache.load_session(s, kt.view(n0, w.L, w.Hkv, w.d), reg, ids,
-                                        budget=int(self.B[s]), clock=n0)
+                                        budget=int(self.B[s]), clock=n0, region_aligned=al)
             else:
                 self.cache.budget[s] = int(self.B[s])
                 self.cache.clock[s] = 0
@@ -145,12 +151,12 @@ class Pair:
                     alpha=f32(self.alpha), rho=f32(w.rho), tau_scale=f32(w.tau_scale),
                     pinned_mask=self.pinned_mask, budget=int(self.B[s]), clock=n0, region=reg,
                     keys_bits=kb if n0 else np.zeros((0, w.L, w.Hkv, w.d), np.uint16),
-                    capacity=n0 + self.steps, attention_norm=w.attention_norm)
+                    capacity=n0 + self.steps, attention_norm=w.attention_norm, region_aligned=al)
         self.cache.set_free_pages(perm[pos:][::-1])
         self.md = MemDecay(self.cache, torch.from_numpy(self.b), torch.from_numpy(self.lam),
                            rho=f32(w.rho), alpha=f32(self.alpha), tau_scale=f32(w.tau_scale),
                            pinned_mask=self.pinned_mask, fused=fused, attention_norm=w.attention_norm,
-                           window=w.window)
+                           window=w.window, region_aligned=al)
         n_slots = n_phys * P
         self.abar = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
         self.tscore = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
@@ -196,7 +202,7 @@ class Pair:
             # a decode step without an observation: append only, on both sides
             md.observe(k, None, nkt, regt)
             torch.cuda.synchronize(self.dev)
-            nt_dev = self.cache.n_tokens.cpu().numpy()
+            nt_dev = self.live_counts()
             for s in self.oracle_sessions:
                 rec = self.oracles[s].step(None, nko[s], int(reg[s]))
                 if compare:
@@ -212,7 +218,8 @@ class Pair:
         assert dev_status == 0, f"step {k}: device status {dev_status:#x}"
         c = self.cache
         host = {name: getattr(c, name).cpu().numpy() for name in
-                ("page_table", "page_serial", "n_pages", "n_tokens", "importance", "t_ref")}
+                ("page_table", "page_serial", "n_pages", "n_tokens", "importance", "t_ref", "region")}
+        host["n_live"] = self.live_counts()
         abar = self.abar.cpu().numpy()
         tsc = self.tscore.cpu().numpy()
         psc = md.page_score.cpu().numpy()
@@ -227,12 +234,15 @@ class Pair:
             self.last_rec[s] = rec
             if not compare:
                 continue
-            npg, nt = int(host["n_pages"][s]), int(host["n_tokens"][s])
+            npg, nt = int(host["n_pages"][s]), int(host["n_live"][s])
             assert nt == rec.n, (k, s, nt, rec.n)
             ptab = host["page_table"][s, :npg].astype(np.int64)
             pser = host["page_serial"][s, :npg]
             assert pser.tolist() == rec.page_serial.tolist(), (k, s)
-            slots = (ptab[:, None] * P + np.arange(P)[None, :]).reshape(-1)[:nt]
+            slots = self.token_slots(host, s)
+            assert slots.size == nt, (k, s, "tokens in the page tables", slots.size, nt)
+            dev_sizes = np.bincount(slots // P, minlength=c.n_phys)[ptab] if npg else np.zeros(0, np.int64)
+            assert dev_sizes.tolist() == rec.page_size.tolist(), (k, s, "tokens per page")
             st = self.stats
             st.tokens += nt
             # attention mass and importance
@@ -296,7 +306,7 @@ class Pair:
         torch.cuda.synchronize(self.dev)
         if compare:
             n_pages = c.n_pages.cpu().numpy()
-            n_tokens = c.n_tokens.cpu().numpy()
+            n_tokens = self.live_counts()
             pser = c.page_serial.cpu().numpy()
             for s in self.oracle_sessions:
                 o = self.oracles[s]
@@ -304,6 +314,22 @@ class Pair:
                 assert pser[s, :n_pages[s]].tolist() == [p.serial for p in o.pages], (k, s)
         self.stats.steps += 1
         return self.stats
+
+    def live_counts(self) -> np.ndarray:
+        """|K_t| per session on the device: n_live with region-aligned pages."""
+        c = self.cache
+        return (c.n_live if self.w.region_aligned else c.n_tokens).cpu().numpy()
+
+    def token_slots(self, host, s: int) -> np.ndarray:
+        """Slots of session s's tokens in logical order, read from the device's
+        page table, counters and region codes (holes left out)."""
+        P = self.w.P
+        npg, npos = int(host["n_pages"][s]), int(host["n_tokens"][s])
+        ptab = host["page_table"][s, :npg].astype(np.int64)
+        slots = (ptab[:, None] * P + np.arange(P)[None, :]).reshape(-1)[:npos]
+        if self.w.region_aligned:
+            slots = slots[host["region"].reshape(-1)[slots] != B.MD_REGION_HOLE]
+        return slots
 
     def device_status(self) -> int:
         return self.md.device_status() | self.status_seen

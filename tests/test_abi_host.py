@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert B.md_abi_version() == 2
+    assert B.md_abi_version() == 3
     for st in (0, -1, -2, -3, -4, -5, -6):
         assert B.md_status_str(st)
     assert B.md_status_str(12345) == "unknown status"
@@ -59,7 +59,8 @@ def test_struct_layout_matches_the_header(lib):
       printf("%zu %zu %zu %zu %zu %zu\n", sizeof(md_config), offsetof(md_config, rho),
              offsetof(md_config, flags), offsetof(md_config, window), sizeof(md_region_params),
              sizeof(md_cache_view));
-      printf("%zu %zu\n", offsetof(md_cache_view, importance), offsetof(md_cache_view, free_count));
+      printf("%zu %zu %zu\n", offsetof(md_cache_view, importance), offsetof(md_cache_view, free_count),
+             offsetof(md_cache_view, n_live));
       return 0; }
     '''
     with tempfile.TemporaryDirectory() as d:
@@ -71,7 +72,8 @@ def test_struct_layout_matches_the_header(lib):
     got = [ctypes.sizeof(B.md_config), B.md_config.rho.offset, B.md_config.flags.offset,
            B.md_config.window.offset,
            ctypes.sizeof(B.md_region_params), ctypes.sizeof(B.md_cache_view),
-           B.md_cache_view.importance.offset, B.md_cache_view.free_count.offset]
+           B.md_cache_view.importance.offset, B.md_cache_view.free_count.offset,
+           B.md_cache_view.n_live.offset]
     assert [int(x) for x in out] == got
 
 
@@ -116,7 +118,7 @@ def fake_rp():
     (dict(alpha=-1.0), B.MD_E_INVALID),
     (dict(alpha=float("inf")), B.MD_E_INVALID),
     (dict(tau_scale=-2.0), B.MD_E_INVALID),
-    (dict(flags=8), B.MD_E_INVALID),
+    (dict(flags=16), B.MD_E_INVALID),
     (dict(window=0), B.MD_E_INVALID),
     (dict(window=3), B.MD_E_UNSUPPORTED),            # G = 6: 18 MFMA columns
     (dict(window=2, flags=2), B.MD_E_UNSUPPORTED),   # the fused kernel takes W = 1
@@ -127,10 +129,18 @@ def test_init_rejects_bad_configs_on_the_host(lib, kw, expect):
     assert st == expect and h is None
 
 
-@pytest.mark.parametrize("field", [f for f, _ in B.md_cache_view._fields_])
+@pytest.mark.parametrize("field", [f for f, _ in B.md_cache_view._fields_ if f != "n_live"])
 def test_init_rejects_null_buffers(lib, field):
     st, h = B.md_init_raw(good_config(), fake_rp(), fake_view(**{field: 0}), 0)
     assert st == B.MD_E_INVALID
+
+
+@pytest.mark.parametrize("kw", [dict(n_live=0), dict(n_live=0x10002), dict(region=0x10001)])
+def test_region_aligned_pages_need_the_token_counts(lib, kw):
+    # n_live is required (and word-aligned) with region-aligned pages, and the
+    # region codes are read four at a time
+    st, h = B.md_init_raw(good_config(flags=B.MD_FLAG_REGION_ALIGNED), fake_rp(), fake_view(**kw), 0)
+    assert st == B.MD_E_INVALID and h is None
 
 
 def test_init_rejects_misaligned_buffers(lib):

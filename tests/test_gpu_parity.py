@@ -300,7 +300,8 @@ def test_window_on_a_batch_with_empty_and_short_sessions():
     run_pair(p, 30, "window3-edges")
 
 
-def test_lifetime_statistics_and_decay_fit():
+@pytest.mark.parametrize("aligned", [False, True])
+def test_lifetime_statistics_and_decay_fit(aligned):
     # Region-lifetime calibration (Sec. IV-B): after every observation the
     # device adds each cached token's attention mass to its (region, age
     # bucket) bin; the oracle does the same in float64.  The budget holds
@@ -309,7 +310,7 @@ def test_lifetime_statistics_and_decay_fit():
     # rounding; the Eq. 6 fits of the two agree closely.
     from oracle.calibration import LifetimeStats, fit_decay
     from paper_2607_10582_amd import binding as B
-    w = C.with_overrides(C.get("qwen15_1700"), L=4, steps=24)
+    w = C.with_overrides(C.get("qwen15_1700"), L=4, steps=24, region_aligned=aligned, append_run=4)
     p = Pair(w, planted=64, planted_strength=2.0, query_gain=0.5, budgets=[10**6])
     bucket, nb, nr = 64, 32, 7
     dev = [torch.zeros((w.S, nr, nb), dtype=torch.int64, device="cuda") for _ in range(3)]
@@ -334,3 +335,79 @@ def test_lifetime_statistics_and_decay_fit():
     np.testing.assert_allclose(lam[ok], olam[ok], rtol=1e-3, atol=1e-7)
     say(f"[calibration] fitted half-lives {np.round(np.log(2) / lam, 1)}")
     p.close()
+
+
+# ---------------------------------------------------------------- region-aligned pages
+
+def check_aligned_layout(p: Pair):
+    """On the device: every page of every session holds one region, its holes
+    come after its last token, and only pages closed at a region boundary
+    have holes."""
+    from paper_2607_10582_amd import binding as B
+    c, P = p.cache, p.w.P
+    reg = c.region.cpu().numpy()
+    npg = c.n_pages.cpu().numpy()
+    npos = c.n_tokens.cpu().numpy()
+    nlive = c.n_live.cpu().numpy()
+    ptab = c.page_table.cpu().numpy()
+    for s in range(p.w.S):
+        live = 0
+        for i in range(int(npg[s])):
+            used = P if i < npg[s] - 1 else int(npos[s]) - (int(npg[s]) - 1) * P
+            r = reg[ptab[s, i], :used]
+            hole = r == B.MD_REGION_HOLE
+            k = int(np.count_nonzero(~hole))
+            assert k >= 1 and not hole[:k].any() and hole[k:].all(), (s, i, r)
+            assert np.all(r[:k] == r[0]), (s, i, r)
+            live += k
+        assert live == int(nlive[s]), (s, live, int(nlive[s]))
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_region_aligned_small(fused):
+    # Region-aligned pages (the allocator variant of Sec. III-D): a fresh page
+    # at every region boundary, in the prompt and in the decode stream (turns
+    # of 5 tokens per region).  Parity step by step, then the layout.
+    w = C.get("small_aligned")
+    p = Pair(w, fused=fused, planted=24, planted_strength=2.5, query_gain=0.7)
+    say(f"[aligned-small] pages {int(p.cache.n_pages[0])}, slots {int(p.cache.n_tokens[0])}, "
+        f"tokens {int(p.cache.n_live[0])}")
+    check_aligned_layout(p)
+    for _ in range(w.steps):
+        st = p.step()
+        check_aligned_layout(p)
+    assert p.device_status() == 0 and p.free_pages_consistent()
+    say(f"[aligned-small-fused{int(fused)}] ok: {st.steps} steps, max rel {st.max_rel}, "
+        f"evicted pages {st.evicted_pages}")
+    p.close()
+    assert st.evicted_pages > 10
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_region_aligned_long32k_sampled_sessions(fused):
+    # The 16 x 32,768-token batch with region-aligned pages, inputs drawn on
+    # the device, two sessions checked token by token.
+    w = C.get("long32k_aligned")
+    p = Pair(w, backend="torch", oracle_sessions=[0, 11], steps=6, fused=fused)
+    check_aligned_layout(p)
+    run_pair(p, 3, f"aligned-long32k-fused{int(fused)}")
+
+
+@pytest.mark.parametrize("P", [16, 64])
+def test_region_aligned_ragged_batch(P):
+    # Short spans (mean 40) so that most pages of P = 64 close early, empty
+    # and one-token sessions, and the fused kernel with its lanes.
+    w = C.with_overrides(C.get("small"), L=2, Hq=16, Hkv=2, S=6, n0=None, n0_range=(1, 2), P=P,
+                         append_cycle=C.APPEND_CYCLE, region_aligned=True, append_run=3, steps=12,
+                         system_len=30)
+    p = Pair(w, n0s=[0, 1, 40, 333, 1200, 3000], budgets=[0, 1, 20, 150, 500, 1000], fused=True)
+    check_aligned_layout(p)
+    run_pair(p, 12, f"aligned-ragged-P{P}")
+
+
+def test_region_aligned_window():
+    # W = 2 window queries every other step on the multi-kernel path: the
+    # causal mask and the hole mask together.
+    w = C.with_overrides(C.get("small_aligned"), window=2, obs_interval=2, steps=24)
+    p = Pair(w, fused=None, planted=24, planted_strength=2.5, query_gain=0.7)
+    run_pair(p, 24, "aligned-window2")
