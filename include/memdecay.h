@@ -34,7 +34,12 @@
  *    scores, selections and logical page orders are deterministic.
  *
  * Layouts (S = max_sessions, NP = n_phys_pages, P = page_size, MP = max_pages)
- *  k_pool       uint16 bf16 bits [NP][L][Hkv][P][d]   keys of each physical page
+ *  k_pool       uint16 bf16 bits [NP][L][Hkv][P/16][d/8][16][8]   keys of each
+ *               physical page: for each (layer, KV head), blocks of 16 tokens,
+ *               each block holding dims 8b .. 8b+7 of its 16 tokens together
+ *               (block-interleaved, so that the attention kernels read 1 KiB
+ *               contiguous per load); element (t, e) of a (page, l, kv) tile
+ *               sits at (t & ~15) * d + (e / 8) * 128 + (t % 16) * 8 + e % 8
  *  region       uint8  [NP][P]   region code of each slot
  *  t_ins, t_ref int32  [NP][P]   insertion step, refresh clock of each slot
  *  importance   float  [NP][P]   a_i of each slot
@@ -61,7 +66,7 @@
 extern "C" {
 #endif
 
-#define MD_ABI_VERSION 3
+#define MD_ABI_VERSION 4
 
 typedef int32_t md_status;
 

@@ -32,7 +32,7 @@ class PagedCache:
         i32 = dict(dtype=torch.int32, device=dev)
         # Slots past a session's token count are never used, so the pool is
         # left uninitialised.
-        self.k_pool = torch.empty((n_phys, L, Hkv, P, d), dtype=torch.bfloat16, device=dev)
+        self.k_pool = torch.empty((n_phys, L, Hkv, P // 16, d // 8, 16, 8), dtype=torch.bfloat16, device=dev)
         self.region = torch.zeros((n_phys, P), dtype=torch.uint8, device=dev)
         self.t_ins = torch.zeros((n_phys, P), **i32)
         self.t_ref = torch.zeros((n_phys, P), **i32)
@@ -55,6 +55,20 @@ class PagedCache:
                      "free_list", "free_count", "n_live"):
             setattr(v, name, getattr(self, name).data_ptr())
         return v
+
+    @staticmethod
+    def to_pool_layout(k: torch.Tensor) -> torch.Tensor:
+        """Keys [m][P][L][Hkv][d] of m pages -> the pool's page layout
+        [m][L][Hkv][P/16][d/8][16][8] (memdecay.h)."""
+        m, P, L, Hkv, d = k.shape
+        return k.view(m, P // 16, 16, L, Hkv, d // 8, 8).permute(0, 3, 4, 1, 5, 2, 6).contiguous()
+
+    @staticmethod
+    def from_pool_layout(pages: torch.Tensor) -> torch.Tensor:
+        """The inverse: pool pages [m][L][Hkv][P/16][d/8][16][8] (or the pool
+        itself) -> keys [m][P][L][Hkv][d]."""
+        m, L, Hkv, nb, db = pages.shape[:5]
+        return pages.permute(0, 3, 5, 1, 2, 4, 6).reshape(m, nb * 16, L, Hkv, db * 8)
 
     @staticmethod
     def positions(region, P: int, region_aligned: bool) -> np.ndarray:
@@ -100,7 +114,7 @@ class PagedCache:
         full = torch.zeros((m * P,) + tuple(k.shape[1:]), dtype=k.dtype, device=k.device)
         full[posd] = k
         # [m][P][L][Hkv][d] -> [m][L][Hkv][P][d]
-        self.k_pool.index_copy_(0, ids, full.view(m, P, self.L, self.Hkv, self.d).permute(0, 2, 3, 1, 4))
+        self.k_pool.index_copy_(0, ids, self.to_pool_layout(full.view(m, P, self.L, self.Hkv, self.d)))
         reg = torch.as_tensor(np.asarray(region, dtype=np.uint8), device=self.device)
         t0 = torch.arange(n, dtype=torch.int32, device=self.device) if t_ins is None else \
             torch.as_tensor(np.asarray(t_ins, dtype=np.int32), device=self.device)

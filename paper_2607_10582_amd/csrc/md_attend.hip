@@ -184,7 +184,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     const int h = lane & 15;          // MFMA column: query head of the group
     const int g = lane >> 4;          // k-group of A/B, row quad of C
     const int hh = min(h, G - 1);     // in-bounds head for the unused columns
-    const uint32_t voff = 256u * h + 16u * g;
+    const uint32_t voff = 16u * lane;   // piece (8-dim block 4j + g, token h) of a 16-token block
     constexpr int kT = 16 * W * KT;   // tokens per unit
     constexpr int kTs = tstride(W, KT);
     constexpr int kTok = KT / 4;          // tokens per lane
@@ -226,9 +226,11 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     }
     const bool wave_full = (vmask & kAll) == kAll && wtok0 + 16 * KT <= un.ntok && (!AL || lims == 0x10101010u);
 
-    // K tile u of row r in the MFMA A layout; a tile without cached tokens,
-    // or past the last row, reads the pool's first tile (its logits are
-    // masked), so loads never branch.
+    // K tile u of row r in the MFMA A layout: the pool keeps each block of
+    // 16 tokens as [d / 8][16][8], so load j reads 1 KiB contiguous and lane
+    // (h, g) gets token h's dims 32j + 8g .. +7.  A tile without cached
+    // tokens, or past the last row, reads the pool's first tile (its logits
+    // are masked), so loads never branch.
     auto load_tile = [&](u32x4 (&rg)[4], int r, int u) {
         const bool ok = r < dm.LHkv && ((vmask >> u) & 1ull);
         const int slot = __builtin_amdgcn_readlane(myslot, u);
@@ -236,7 +238,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         gbytes base = uni_ptr(a.k_pool + e * kHeadDim);
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            rg[j] = __builtin_nontemporal_load(reinterpret_cast<gvec>(base + voff + 64 * j));
+            rg[j] = __builtin_nontemporal_load(reinterpret_cast<gvec>(base + voff + 1024 * j));
     };
 
     // ---- query staging: this wave's float4 f = lane + 64 (wv + W k) of a row

@@ -103,14 +103,15 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     __syncthreads();
     const int phys = sh_phys;
     if (phys >= 0) {
-        // L*Hkv rows of d bf16 = 16 pieces of 16 bytes per row.
+        // L*Hkv rows of d bf16 = 16 pieces of 16 bytes per row; piece b of
+        // the token goes to its 16-token block's [b][slot mod 16] place.
         const int slot = sh_slot;
         const u32x4* src = reinterpret_cast<const u32x4*>(new_k + (size_t)s * dm.LHkv * kHeadDim);
         for (int i = threadIdx.x; i < dm.LHkv * 16; i += blockDim.x) {
             const int r = i >> 4, part = i & 15;
-            u32x4* dst = reinterpret_cast<u32x4*>(
-                v.k_pool + (((size_t)phys * dm.LHkv + r) * dm.P + slot) * kHeadDim);
-            dst[part] = src[i];
+            u32x4* blk = reinterpret_cast<u32x4*>(
+                v.k_pool + (((size_t)phys * dm.LHkv + r) * dm.P + (slot & ~15)) * kHeadDim);
+            blk[part * 16 + (slot & 15)] = src[i];
         }
     }
 
@@ -354,7 +355,9 @@ __device__ __forceinline__ void item_tiles(ItemTiles& it, const Cursor& cu, cons
 }
 
 // Four 16-byte pieces of one K row tile in the MFMA A layout: lane (h, g)
-// holds token h's dims 32j + 8g .. +7 for j = 0..3 (voff = 256 h + 16 g).
+// holds token h's dims 32j + 8g .. +7 for j = 0..3.  The pool keeps each
+// block of 16 tokens as [d / 8][16][8], so piece j of all 64 lanes is 1 KiB
+// contiguous (voff = 16 lane).
 // A tile without cached tokens reads the pool's first row tile instead
 // (always in bounds; its logits are masked), so loads never branch.
 __device__ __forceinline__ void load_tile(u32x4 (&a)[4], const LogitsDims& dm,
@@ -366,7 +369,7 @@ __device__ __forceinline__ void load_tile(u32x4 (&a)[4], const LogitsDims& dm,
     gbytes base = uni_ptr(k_pool + tile * kHeadDim);
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-        a[j] = __builtin_nontemporal_load(reinterpret_cast<gvec>(base + voff + 64 * j));
+        a[j] = __builtin_nontemporal_load(reinterpret_cast<gvec>(base + voff + 1024 * j));
 }
 
 // Each wave streams a contiguous run of work items (128-token chunks of one
@@ -402,7 +405,7 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
 
     const int h = lane & 15;         // MFMA column = query head within the group
     const int g = lane >> 4;         // k-group of A/B, row quad of C
-    const uint32_t voff = 256u * h + 16u * g;
+    const uint32_t voff = 16u * lane;
     Cursor cu;
     cu.s = find_session_uni(s_pref, S, it);
     const int base_it = uni(s_pref[cu.s]);

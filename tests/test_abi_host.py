@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert B.md_abi_version() == 3
+    assert B.md_abi_version() == 4
     for st in (0, -1, -2, -3, -4, -5, -6):
         assert B.md_status_str(st)
     assert B.md_status_str(12345) == "unknown status"
@@ -182,3 +182,19 @@ def test_calib_fit_matches_the_oracle_fit(lib):
     ok = ~np.isnan(olam)
     np.testing.assert_allclose(lam[ok], olam[ok], rtol=1e-9)
     np.testing.assert_allclose(logc[ok], ologc[ok], rtol=1e-9)
+
+
+def test_pool_layout_matches_the_header():
+    # memdecay.h: element (t, e) of a (page, layer, KV head) tile sits at
+    # (t & ~15) d + (e / 8) 128 + (t % 16) 8 + e % 8; the caller-side helpers
+    # place keys there and read them back
+    import torch
+    from paper_2607_10582_amd.cache import PagedCache
+    m, P, L, Hkv, d = 2, 64, 3, 2, 128
+    k = torch.arange(m * P * L * Hkv * d, dtype=torch.float64).view(m, P, L, Hkv, d)
+    pool = PagedCache.to_pool_layout(k)
+    flat = pool.reshape(m, L, Hkv, P * d)
+    for (pg, t, l, kv, e) in [(0, 0, 0, 0, 0), (1, 17, 2, 1, 9), (0, 63, 1, 0, 127), (1, 40, 0, 1, 64)]:
+        off = (t & ~15) * d + (e // 8) * 128 + (t % 16) * 8 + e % 8
+        assert flat[pg, l, kv, off] == k[pg, t, l, kv, e]
+    assert torch.equal(PagedCache.from_pool_layout(pool), k)
