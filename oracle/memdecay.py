@@ -56,7 +56,15 @@ design notes of the repository):
     token opens a fresh page when the last page is full or its last token's
     region differs; a prompt is laid out the same way, token by token.  The
     rest of the method is unchanged: page sizes simply vary more, and Eq. 5
-    still averages over the live members.
+    still averages over the live members;
+  * optional quantised tier (the first tier of the tiered extension,
+    Sec. III-E): after an observation step's eviction, every surviving page
+    that is not pinned, is not the page the step's token went to (the last
+    page before eviction), is still in full precision and scores
+    S_p < quant_threshold is quantised, once and for good.  Each group of
+    16 consecutive tokens of the page, per (layer, KV head), gets one scale
+    s = max|k| / 127 and codes c = clamp(rint(k / s), -127, 127), both in
+    float32 (s = 0 and c = 0 when max|k| = 0); attention then uses s * c.
 """
 from __future__ import annotations
 
@@ -83,6 +91,20 @@ def softmax(x: np.ndarray) -> np.ndarray:
 class Page:
     serial: int
     slots: List[int]
+    quant: bool = False     # keys held as 8-bit codes and a scale per 16 tokens
+
+
+def quantise_block(x: np.ndarray):
+    """Codes and scale of one group of keys (float32 values, any shape): the
+    scale max|x| / 127 and the codes rint(x / scale) clamped to [-127, 127],
+    both computed in float32; an all-zero group gets scale 0 and codes 0."""
+    x = np.asarray(x, dtype=np.float32)
+    m = np.float32(np.max(np.abs(x))) if x.size else np.float32(0)
+    if m == 0:
+        return np.zeros(x.shape, np.int8), np.float32(0)
+    s = np.float32(m / np.float32(127))
+    c = np.clip(np.rint(x / s), -127, 127).astype(np.int8)
+    return c, s
 
 
 @dataclass
@@ -116,7 +138,8 @@ class Session:
                  page_sizes: Optional[Sequence[int]] = None,
                  page_serials: Optional[Sequence[int]] = None,
                  next_serial: Optional[int] = None, capacity: Optional[int] = None,
-                 attention_norm: bool = False, region_aligned: bool = False):
+                 attention_norm: bool = False, region_aligned: bool = False,
+                 quant_threshold: float = 0.0):
         if Hq % Hkv:
             raise ValueError("query heads must be a multiple of KV heads")
         self.L, self.Hq, self.Hkv, self.d, self.P = L, Hq, Hkv, d, P
@@ -127,6 +150,7 @@ class Session:
         self.pinned_mask = int(pinned_mask)
         self.attention_norm = bool(attention_norm)
         self.region_aligned = bool(region_aligned)
+        self.quant_threshold = float(quant_threshold)
         self.budget = int(budget)
         self.t = int(clock)
 
@@ -140,6 +164,10 @@ class Session:
         self.t_ref = np.zeros(cap, dtype=np.int64)
         self.a = np.zeros(cap, dtype=np.float64)
         self.keys = np.zeros((L, Hkv, cap, d), dtype=np.float32)
+        # quantised tokens: codes [L][Hkv][slot][d] and their group's scale
+        self.codes = np.zeros((L, Hkv, cap, d), dtype=np.int8) if self.quant_threshold > 0 else None
+        self.qscale = np.zeros((L, Hkv, cap), dtype=np.float32) if self.quant_threshold > 0 else None
+        self.is_quant = np.zeros(cap, dtype=bool)
         self.n_slots = n
         self.region[:n] = region
         self.t_ins[:n] = np.arange(n) if t_ins is None else np.asarray(t_ins)
@@ -186,9 +214,17 @@ class Session:
             arr = getattr(self, name)
             setattr(self, name, np.concatenate([arr, np.zeros(new - cap, dtype=arr.dtype)]))
         self.a = np.concatenate([self.a, np.zeros(new - cap)])
+        self.is_quant = np.concatenate([self.is_quant, np.zeros(new - cap, dtype=bool)])
         k = np.zeros((self.L, self.Hkv, new, self.d), dtype=np.float32)
         k[:, :, :cap, :] = self.keys
         self.keys = k
+        if self.codes is not None:
+            c = np.zeros((self.L, self.Hkv, new, self.d), dtype=np.int8)
+            c[:, :, :cap, :] = self.codes
+            self.codes = c
+            sc = np.zeros((self.L, self.Hkv, new), dtype=np.float32)
+            sc[:, :, :cap] = self.qscale
+            self.qscale = sc
 
     # ------------------------------------------------------------ steps
     def append(self, key_bits, region: int):
@@ -211,6 +247,31 @@ class Session:
             self.pages.append(Page(self.next_serial, [j]))
             self.next_serial += 1
 
+    def key_rows(self, l: int, kv: int, slots: np.ndarray) -> np.ndarray:
+        """float64 keys of the given slots at (layer l, KV head kv): the cached
+        values, or scale * code for quantised tokens."""
+        k = self.keys[l, kv][slots].astype(np.float64)
+        if self.codes is not None:
+            qz = self.is_quant[slots]
+            if np.any(qz):
+                qs = slots[qz]
+                k[qz] = self.codes[l, kv][qs].astype(np.float64) * \
+                    self.qscale[l, kv][qs].astype(np.float64)[:, None]
+        return k
+
+    def quantise_page(self, page: Page):
+        """The quantised tier for one page, per 16-token group and (l, kv)."""
+        slots = np.asarray(page.slots, dtype=np.int64)
+        for g0 in range(0, slots.size, 16):
+            grp = slots[g0:g0 + 16]
+            for l in range(self.L):
+                for kv in range(self.Hkv):
+                    c, s = quantise_block(self.keys[l, kv][grp])
+                    self.codes[l, kv][grp] = c
+                    self.qscale[l, kv][grp] = s
+        self.is_quant[slots] = True
+        page.quant = True
+
     def attention_mass(self, q, live: np.ndarray) -> np.ndarray:
         """A_i: softmax attention of the window's decode queries, averaged
         over the L*Hq query heads and the W window queries (Sec. III-C).
@@ -228,7 +289,7 @@ class Session:
                 continue
             for l in range(self.L):
                 for kv in range(self.Hkv):
-                    k = self.keys[l, kv][live[seen]].astype(np.float64)       # [n_seen][d]
+                    k = self.key_rows(l, kv, live[seen])                      # [n_seen][d]
                     x = (k @ q[w, l, kv * self.G:(kv + 1) * self.G].T) * inv_sqrt_d   # [n_seen][G]
                     for j in range(self.G):
                         mass[seen] += softmax(x[:, j])
@@ -286,9 +347,17 @@ class Session:
         evicted, n_after, infeasible = select_pages(page_score, serials, sizes,
                                                     page_pinned, n, self.budget)
         # O9: drop the evicted pages (irreversible, Sec. III-E).
+        last_serial = self.pages[-1].serial
         if evicted.size:
             gone = set(int(x) for x in evicted)
             self.pages = [p for p in self.pages if p.serial not in gone]
+        # Quantised tier (Sec. III-E): surviving pages below the threshold.
+        if self.quant_threshold > 0:
+            score_of = {int(s): (float(v), bool(pn)) for s, v, pn in zip(serials, page_score, page_pinned)}
+            for p in self.pages:
+                v, pn = score_of[p.serial]
+                if not pn and not p.quant and p.serial != last_serial and v < self.quant_threshold:
+                    self.quantise_page(p)
         return StepRecord(t, n, tau, serials, sizes, page_pinned, page_score, abar,
                           self.a[live].copy(), self.t_ref[live].copy(), r.copy(), score,
                           evicted, n_after, infeasible)
@@ -338,7 +407,7 @@ def select_pages(page_score, serials, sizes, pinned, n: int, budget: int):
 
 def session_from_workload(w, session: int, *, region, keys_bits, b, lam, budget,
                           alpha=None, rho=None, tau_scale=None, capacity=None,
-                          attention_norm=None, region_aligned=None) -> Session:
+                          attention_norm=None, region_aligned=None, quant_threshold=None) -> Session:
     """A session at the start of decoding: prefix token i has t_ins = t_ref = i,
     importance 0, and the clock stands at n0 (so decode step k runs at
     t = n0 + k)."""
@@ -351,4 +420,5 @@ def session_from_workload(w, session: int, *, region, keys_bits, b, lam, budget,
                    region=region, keys_bits=keys_bits,
                    capacity=capacity if capacity is not None else n0 + w.steps,
                    attention_norm=w.attention_norm if attention_norm is None else attention_norm,
-                   region_aligned=w.region_aligned if region_aligned is None else region_aligned)
+                   region_aligned=w.region_aligned if region_aligned is None else region_aligned,
+                   quant_threshold=w.quant_threshold if quant_threshold is None else quant_threshold)

@@ -66,6 +66,7 @@ class Workload:
     obs_interval: int = 1          # one observation every k decode steps (k >= W)
     region_aligned: bool = False   # pages hold one region each (allocator variant)
     append_run: int = 1            # decode tokens per region run of the append cycle
+    quant_threshold: float = 0.0   # quantised tier: pages scoring below it (0: off)
     b_range: Tuple[float, float] = (0.2, 1.0)
     extra: dict = field(default_factory=dict)
 
