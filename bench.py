@@ -88,7 +88,7 @@ def setup(w, steps_total, dev, fused=None):
     cache.set_free_pages(perm[pos:][::-1])
     md = MemDecay(cache, torch.from_numpy(b), torch.from_numpy(lam), rho=w.rho, alpha=w.alpha,
                   tau_scale=w.tau_scale, pinned_mask=w.pinned_mask, fused=fused,
-                  region_aligned=w.region_aligned)
+                  region_aligned=w.region_aligned, quant_threshold=w.quant_threshold)
     inputs = []
     for k in range(1, steps_total + 1):
         q = g.torch_queries(w, k, dev)

@@ -53,7 +53,13 @@
  * MD_FLAG_REGION_ALIGNED: there the slots of a page after its last token,
  * left unused when the page was closed at a region boundary, are holes
  * (region code MD_REGION_HOLE), n_tokens counts them with the tokens, and
- * n_live counts the tokens alone.  Region codes follow the paper's label
+ * n_live counts the tokens alone.
+ * Quantised pages (quant_threshold > 0, page_format[p] = 1): each 16-token
+ * block of a (layer, KV head) tile keeps, in the first 2 KiB of its 4 KiB,
+ * int8 codes c with key = s * c, and its scale s as float32 in bytes 2048 ..
+ * 2051 (repeated in 2052 .. 2063); the code of token t (0..15) and dim e
+ * sits at byte 1024 (e / 64) + 16 (t + 16 ((e / 8) % 4)) + 8 ((e / 32) % 2)
+ * + e % 8.  Region codes follow the paper's label
  * list: system 0, plan 1, user 2, tool_in 3, tool_out 4, retrieval 5,
  * scratchpad 6.
  */
@@ -66,7 +72,7 @@
 extern "C" {
 #endif
 
-#define MD_ABI_VERSION 4
+#define MD_ABI_VERSION 5
 
 typedef int32_t md_status;
 
@@ -133,6 +139,9 @@ typedef struct md_config {
     int32_t window;             /* W >= 1 decode queries per observation, with    */
                                 /* (Hq/Hkv) W <= 16 and L Hq W <= 1024; W > 1     */
                                 /* runs on the multi-kernel path (Sec. III-C)     */
+    float quant_threshold;      /* quantised tier (Sec. III-E): md_compact turns  */
+                                /* pages scoring below it into 8-bit codes; 0 =   */
+                                /* off, +INFINITY = every eligible page           */
 } md_config;
 
 /* Region priors (Sec. III-B): b_r >= 0 and lambda_r >= 0 per session and
@@ -159,6 +168,8 @@ typedef struct md_cache_view {
     int32_t*  free_count;
     int32_t*  n_live;     /* MD_FLAG_REGION_ALIGNED: |K_t| per session; else   */
                           /* ignored (may be NULL: |K_t| is n_tokens)          */
+    uint8_t*  page_format;/* quant_threshold > 0: [NP], 0 = bf16 keys, 1 =     */
+                          /* quantised; else ignored (may be NULL)             */
 } md_cache_view;
 
 typedef struct md_handle_s* md_handle;
@@ -256,6 +267,14 @@ md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_cou
  * ids onto the free list.  evict_serial / evict_count have md_select_evict's
  * layout and are normally its output; serials a session does not hold set
  * MD_DEV_BAD_EVICT and are ignored.
+ * Quantised tier (quant_threshold > 0; Sec. III-E's first tier): before the
+ * compaction, every page that survives, is not pinned, is not the session's
+ * last page, is still bf16 and has page score S_p < quant_threshold (the
+ * scores of this step's md_score_pages) is quantised in place: per 16-token
+ * block and (layer, KV head), s = max|k| / 127 and c = clamp(rint(k / s),
+ * -127, 127) in float32 (s = 0, c = 0 for an all-zero block; holes get
+ * c = 0), page_format = 1.  Irreversible.  Requires md_score_pages since the
+ * last md_observe_step (MD_E_STATE otherwise).
  */
 md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* evict_count);
 

@@ -50,7 +50,8 @@ class md_config(ctypes.Structure):
                 ("max_pages", ctypes.c_int32), ("n_phys_pages", ctypes.c_int32),
                 ("n_regions", ctypes.c_int32), ("pinned_region_mask", ctypes.c_uint32),
                 ("rho", ctypes.c_float), ("alpha", ctypes.c_float),
-                ("tau_scale", ctypes.c_float), ("flags", ctypes.c_int32), ("window", ctypes.c_int32)]
+                ("tau_scale", ctypes.c_float), ("flags", ctypes.c_int32), ("window", ctypes.c_int32),
+                ("quant_threshold", ctypes.c_float)]
 
 
 class md_region_params(ctypes.Structure):
@@ -60,7 +61,8 @@ class md_region_params(ctypes.Structure):
 class md_cache_view(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "k_pool", "region", "t_ins", "t_ref", "importance", "page_table", "page_serial",
-        "n_pages", "n_tokens", "clock", "next_serial", "budget", "free_list", "free_count", "n_live")]
+        "n_pages", "n_tokens", "clock", "next_serial", "budget", "free_list", "free_count", "n_live",
+        "page_format")]
 
 
 class MemDecayError(RuntimeError):

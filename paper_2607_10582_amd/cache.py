@@ -42,6 +42,7 @@ class PagedCache:
         self.n_pages = torch.zeros(S, **i32)
         self.n_tokens = torch.zeros(S, **i32)
         self.n_live = torch.zeros(S, **i32)   # tokens without holes (region-aligned pages)
+        self.page_format = torch.zeros(n_phys, dtype=torch.uint8, device=dev)   # 1: quantised page
         self.clock = torch.zeros(S, **i32)
         self.next_serial = torch.zeros(S, **i32)
         self.budget = torch.zeros(S, **i32)
@@ -52,7 +53,7 @@ class PagedCache:
         v = B.md_cache_view()
         for name in ("k_pool", "region", "t_ins", "t_ref", "importance", "page_table",
                      "page_serial", "n_pages", "n_tokens", "clock", "next_serial", "budget",
-                     "free_list", "free_count", "n_live"):
+                     "free_list", "free_count", "n_live", "page_format"):
             setattr(v, name, getattr(self, name).data_ptr())
         return v
 
@@ -129,6 +130,7 @@ class PagedCache:
         self.t_ins.view(-1)[flat] = t0
         self.t_ref.view(-1)[flat] = t0
         self.importance.view(-1)[flat] = 0.0
+        self.page_format[ids] = 0
         self.page_table[s, :m] = ids.to(torch.int32)
         self.page_table[s, m:] = -1
         self.page_serial[s, :m] = torch.arange(m, dtype=torch.int32, device=self.device)
@@ -156,7 +158,7 @@ class MemDecay:
                  rho: float, alpha: float, tau_scale: float, pinned_mask: int,
                  n_regions: int = 7, stream: Optional[torch.cuda.Stream] = None,
                  fused: Optional[bool] = None, attention_norm: bool = False, window: int = 1,
-                 region_aligned: bool = False):
+                 region_aligned: bool = False, quant_threshold: float = 0.0):
         # fused: True = always the fused kernel, False = always the
         # multi-kernel path, None = the library picks from the cache's sizes
         self.cache = cache
@@ -171,7 +173,7 @@ class MemDecay:
                           flags=(0 if fused is None else (B.MD_FLAG_FUSED if fused else B.MD_FLAG_NO_FUSED))
                           | (B.MD_FLAG_NORM_ATTENTION if attention_norm else 0)
                           | (B.MD_FLAG_REGION_ALIGNED if region_aligned else 0),
-                          window=window)
+                          window=window, quant_threshold=quant_threshold)
         rp = B.md_region_params(base_priority=self.b.data_ptr(), decay_rate=self.lam.data_ptr())
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
         self._cfg, self._rp, self._cv = cfg, rp, cache.view()

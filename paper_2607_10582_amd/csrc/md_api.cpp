@@ -118,6 +118,7 @@ static md_status validate_config(const md_config* c) {
     if (!(c->alpha >= 0.0f) || !isfinite(c->alpha)) return MD_E_INVALID;
     if (!(c->tau_scale >= 0.0f) || !isfinite(c->tau_scale)) return MD_E_INVALID;
     if (c->window < 1) return MD_E_INVALID;
+    if (!(c->quant_threshold >= 0.0f)) return MD_E_INVALID;   // NaN too
     if ((c->flags & MD_FLAG_FUSED) && c->window > 1) return MD_E_UNSUPPORTED;
     if (c->head_dim != md::kHeadDim) return MD_E_UNSUPPORTED;
     if ((int64_t)(c->n_q_heads / c->n_kv_heads) * c->window > 16) return MD_E_UNSUPPORTED;
@@ -133,8 +134,9 @@ static md_status validate_config(const md_config* c) {
     return MD_OK;
 }
 
-static md_status validate_view(const md_cache_view* v, bool region_aligned) {
+static md_status validate_view(const md_cache_view* v, bool region_aligned, bool quant) {
     if (v == nullptr) return MD_E_INVALID;
+    if (quant && v->page_format == nullptr) return MD_E_INVALID;
     if (region_aligned && (v->n_live == nullptr || !aligned(v->n_live, 4) || !aligned(v->region, 4)))
         return MD_E_INVALID;
     const void* ptrs[] = {v->k_pool, v->region, v->t_ins, v->t_ref, v->importance,
@@ -157,7 +159,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     *out = nullptr;
     md_status st = validate_config(cfg);
     if (st != MD_OK) return st;
-    st = validate_view(cv, (cfg->flags & MD_FLAG_REGION_ALIGNED) != 0);
+    st = validate_view(cv, (cfg->flags & MD_FLAG_REGION_ALIGNED) != 0, cfg->quant_threshold > 0.0f);
     if (st != MD_OK) return st;
     if (rp == nullptr || rp->base_priority == nullptr || rp->decay_rate == nullptr) return MD_E_INVALID;
     if (!aligned(rp->base_priority, 4) || !aligned(rp->decay_rate, 4)) return MD_E_INVALID;
@@ -184,6 +186,8 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     dm.fused = ((cfg->flags & MD_FLAG_NO_FUSED) || dm.W > 1) ? 0 : 1;
     dm.norm_attn = (cfg->flags & MD_FLAG_NORM_ATTENTION) ? 1 : 0;
     dm.aligned = (cfg->flags & MD_FLAG_REGION_ALIGNED) ? 1 : 0;
+    dm.quant = cfg->quant_threshold > 0.0f ? 1 : 0;
+    dm.quant_thr = cfg->quant_threshold;
 
     // ---- from here on the HIP runtime is used
     int dev = 0;
@@ -211,11 +215,11 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     dm.T = md::attend_unit_tokens(dm.G);
     if (dm.fused) {
         const size_t lds = md::attend_lds_bytes(dm.G);
-        if (hipFuncSetAttribute(md::attend_kernel(dm.G, dm.aligned), hipFuncAttributeMaxDynamicSharedMemorySize,
+        if (hipFuncSetAttribute(md::attend_kernel(dm.G, dm.aligned, dm.quant), hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)lds) !=
             hipSuccess) {
             (void)hipGetLastError();
-        } else if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(dm.G, dm.aligned),
+        } else if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(dm.G, dm.aligned, dm.quant),
                                                                 md::attend_threads(dm.G),
                                                                 lds) != hipSuccess) {
             return MD_E_HIP;
@@ -295,6 +299,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     h->v.n_pages = cv->n_pages;
     h->v.n_tokens = cv->n_tokens;
     h->v.n_live = dm.aligned ? cv->n_live : cv->n_tokens;
+    h->v.page_format = dm.quant ? cv->page_format : nullptr;
     h->v.clock = cv->clock;
     h->v.next_serial = cv->next_serial;
     h->v.budget = cv->budget;
@@ -412,7 +417,11 @@ md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* ev
     if (h == nullptr || evict_serial == nullptr || evict_count == nullptr) return MD_E_INVALID;
     if (!aligned(evict_serial, 4) || !aligned(evict_count, 4)) return MD_E_INVALID;
     if (h->phase == kNone) return MD_E_STATE;
+    if (h->dm.quant && h->phase != kScored) return MD_E_STATE;   // the tier needs this step's scores
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    if (h->dm.quant &&
+        md::launch_quant(h->dm, h->v, h->sc, evict_serial, evict_count, h->stream) != hipSuccess)
+        return MD_E_HIP;
     if (timed_launch(h, MD_K_COMPACT, [&] {
             return md::launch_compact(h->dm, h->v, h->sc, evict_serial, evict_count, h->stream); }) !=
         hipSuccess)

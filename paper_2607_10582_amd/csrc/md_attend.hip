@@ -78,6 +78,7 @@ struct AttendArgs {
     int32_t* status;
     int32_t* probe;    // check mode only: [arrivals, least seen]
     const int32_t* n_live;   // tokens |K_t| (the n_tokens array unless pages are region-aligned)
+    const uint8_t* page_format;   // quantised tier: 1 = the page holds 8-bit codes
 };
 
 // LDS row stride (floats) of a head's values: W waves of KT tiles
@@ -174,9 +175,10 @@ __device__ __forceinline__ int qrow0(const AttendDims& dm, int r) { return r * d
 
 // One wave's part of a unit.  W = waves per workgroup, NH = normaliser
 // heads per wave (G <= W NH), KT = tiles per wave (units of 16 W KT tokens),
-// AL = region-aligned pages (hole slots are masked; a separate instantiation
-// keeps the plain layout's register budget).
-template <int W, int NH, int KT, bool AL>
+// AL = region-aligned pages (hole slots are masked), QT = quantised tier
+// (tiles of quantised pages hold 8-bit codes); separate instantiations keep
+// the plain kernel's register budget.
+template <int W, int NH, int KT, bool AL, bool QT>
 __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendArgs& a, const Lds& sm,
                                             const Unit& un, int wv, int lane, uint32_t tag) {
     constexpr int KQ = (W * NH * 32 + 64 * W - 1) / (64 * W);   // float4 of the query row per lane
@@ -225,6 +227,13 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         for (int u = 0; u < KT; ++u) lims |= (uint32_t)__builtin_amdgcn_readlane(mylim, u) << (8 * u);
     }
     const bool wave_full = (vmask & kAll) == kAll && wtok0 + 16 * KT <= un.ntok && (!AL || lims == 0x10101010u);
+    // Quantised tier: bit u of qmask marks tile u as 8-bit codes (its page's
+    // format); wave-uniform.
+    uint32_t qmask = 0;
+    if constexpr (QT) {
+        const bool qz = myok && a.page_format[myslot >> dm.Pshift] != 0;
+        qmask = (uint32_t)(__ballot(qz) & kAll);
+    }
 
     // K tile u of row r in the MFMA A layout: the pool keeps each block of
     // 16 tokens as [d / 8][16][8], so load j reads 1 KiB contiguous and lane
@@ -236,10 +245,21 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         const int slot = __builtin_amdgcn_readlane(myslot, u);
         const size_t e = ok ? ((size_t)(slot >> dm.Pshift) * dm.LHkv + r) * dm.P + (slot & (dm.P - 1)) : 0;
         gbytes base = uni_ptr(a.k_pool + e * kHeadDim);
+        if constexpr (QT) {
+            // a quantised block: codes in its first 2 KiB (rg[0], rg[1]), the
+            // scale at byte 2048 (rg[2], rg[3] the same)
+            const bool qt = (qmask >> u) & 1u;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            rg[j] = __builtin_nontemporal_load(reinterpret_cast<gvec>(base + voff + 1024 * j));
+            for (int j = 0; j < 4; ++j)
+                rg[j] = __builtin_nontemporal_load(
+                    reinterpret_cast<gvec>(base + ((qt && j >= 2) ? 2048u : voff + 1024u * j)));
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                rg[j] = __builtin_nontemporal_load(reinterpret_cast<gvec>(base + voff + 1024 * j));
+        }
     };
+
 
     // ---- query staging: this wave's float4 f = lane + 64 (wv + W k) of a row
     f32x4 qv[KQ];
@@ -510,11 +530,25 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
 #pragma unroll
             for (int p = 0; p < 3; ++p) bq[p] = *reinterpret_cast<const u32x4*>(qb + p * G * 64 + 16 * j);
 #pragma unroll
-            for (int u = 0; u < KT; ++u)
+            for (int u = 0; u < KT; ++u) {
+                u32x4 av = ring[u][j];
+                if constexpr (QT) {   // codes as bf16 (exact); the scale after the sum
+                    if ((qmask >> u) & 1u) av = (j & 1) ? codes_to_bf16<1>(ring[u][j >> 1]) : codes_to_bf16<0>(ring[u][j >> 1]);
+                }
 #pragma unroll
                 for (int p = 0; p < 3; ++p)
                     c[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf16x8, ring[u][j]), __builtin_bit_cast(bf16x8, bq[p]), c[u], 0, 0, 0);
+                        __builtin_bit_cast(bf16x8, av), __builtin_bit_cast(bf16x8, bq[p]), c[u], 0, 0, 0);
+            }
+        }
+        if constexpr (QT) {
+#pragma unroll
+            for (int u = 0; u < KT; ++u)
+                if ((qmask >> u) & 1u) {
+                    const float qs = __uint_as_float(ring[u][2][0]);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) c[u][i] *= qs;
+                }
         }
         load_tile(ring[0], row + 2, 0);
         use_loads(row);
@@ -710,7 +744,7 @@ __device__ void claim_sessions(const AttendArgs& a, int* xs, int lane_no, int ca
 // the whole register file.  (Workgroups that take a whole CU, with eight
 // waves or with eight tiles per wave, measured slower: the two workgroups'
 // row barriers fall at different times and fill each other's gaps.)
-template <int W, int NH, int KT, bool AL>
+template <int W, int NH, int KT, bool AL, bool QT>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(NH == 4 ? 1 : 2)))
 k_attend(AttendDims dm, AttendArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -803,7 +837,7 @@ k_attend(AttendDims dm, AttendArgs a) {
         // arithmetic is not hoisted out of the pass loop and kept live.
         int lane = (int)threadIdx.x & 63;
         asm volatile("" : "+v"(lane));
-        attend_wave<W, NH, KT, AL>(dm, a, sm, un, wv, lane, tag);
+        attend_wave<W, NH, KT, AL, QT>(dm, a, sm, un, wv, lane, tag);
     }
 }
 
@@ -814,15 +848,18 @@ size_t attend_lds_bytes(int G) {
     return rowbuf_bytes(G, W, attend_unit_tokens(G) / (16 * W)) + qs_bytes(G) + wstat_bytes(W) + kNormBytes;
 }
 
-const void* attend_kernel(int G, int aligned) {
-    if (aligned) {
-        if (G <= 4) return reinterpret_cast<const void*>(&k_attend<4, 1, 4, true>);
-        if (G <= 8) return reinterpret_cast<const void*>(&k_attend<4, 2, 4, true>);
-        return reinterpret_cast<const void*>(&k_attend<4, 4, 4, true>);
-    }
-    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<4, 1, 4, false>);
-    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<4, 2, 4, false>);
-    return reinterpret_cast<const void*>(&k_attend<4, 4, 4, false>);
+namespace {
+template <bool AL, bool QT>
+const void* attend_for(int G) {
+    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<4, 1, 4, AL, QT>);
+    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<4, 2, 4, AL, QT>);
+    return reinterpret_cast<const void*>(&k_attend<4, 4, 4, AL, QT>);
+}
+}  // namespace
+
+const void* attend_kernel(int G, int aligned, int quant) {
+    if (aligned) return quant ? attend_for<true, true>(G) : attend_for<true, false>(G);
+    return quant ? attend_for<false, true>(G) : attend_for<false, false>(G);
 }
 
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q, float* abar_out,
@@ -832,9 +869,9 @@ hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const
                   dm.rho, dm.tau_scale, dm.alpha, dm.aligned};
     AttendArgs aa{v.k_pool, v.page_table, v.n_tokens, v.clock, v.region, v.b, v.lam, v.imp, v.t_ref,
                   sc.pscore, q, abar_out, sc.ustart, sc.plan, sc.epoch, sc.claim, sc.lane_box, sc.ustat,
-                  sc.unorm, sc.status, nullptr, v.n_live};
+                  sc.unorm, sc.status, nullptr, v.n_live, v.page_format};
     void* args[] = {&ad, &aa};
-    return hipLaunchCooperativeKernel(attend_kernel(dm.G, dm.aligned), dim3(dm.n_wg), dim3(attend_threads(dm.G)), args,
+    return hipLaunchCooperativeKernel(attend_kernel(dm.G, dm.aligned, dm.quant), dim3(dm.n_wg), dim3(attend_threads(dm.G)), args,
                                       (unsigned)attend_lds_bytes(dm.G), st);
 }
 
@@ -846,7 +883,7 @@ hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, hipStre
     if (e == hipSuccess) e = hipMemsetD32Async(reinterpret_cast<hipDeviceptr_t>(probe + 1), 1 << 30, 1, st);
     if (e != hipSuccess) return e;
     void* args[] = {&ad, &aa};
-    return hipLaunchCooperativeKernel(attend_kernel(dm.G, dm.aligned), dim3(n_wg), dim3(attend_threads(dm.G)), args,
+    return hipLaunchCooperativeKernel(attend_kernel(dm.G, dm.aligned, dm.quant), dim3(n_wg), dim3(attend_threads(dm.G)), args,
                                       (unsigned)attend_lds_bytes(dm.G), st);
 }
 

@@ -120,6 +120,21 @@ __device__ __forceinline__ bool page_score_of(float score, bool live, bool pinne
     return cnt > 0;
 }
 
+// Eight int8 key codes (bytes 8 half .. 8 half + 7 of v) as eight bf16
+// values in the MFMA operand order: codes are integers of magnitude <= 127,
+// exact in bf16, so the product with the query stays exact.
+__device__ __forceinline__ uint32_t codes_pair_to_bf16(uint32_t x, int sh) {
+    const uint32_t lo = __float_as_uint((float)(int8_t)((x >> sh) & 0xffu)) >> 16;
+    const uint32_t hi = __float_as_uint((float)(int8_t)((x >> (sh + 8)) & 0xffu)) >> 16;
+    return lo | (hi << 16);
+}
+template <int HALF>
+__device__ __forceinline__ u32x4 codes_to_bf16(u32x4 v) {
+    const uint32_t w0 = HALF ? v[2] : v[0], w1 = HALF ? v[3] : v[1];
+    return u32x4{codes_pair_to_bf16(w0, 0), codes_pair_to_bf16(w0, 16), codes_pair_to_bf16(w1, 0),
+                 codes_pair_to_bf16(w1, 16)};
+}
+
 // Weight of the attention term of Eq. 4: alpha, or alpha * |K_t| when the
 // term is measured against the uniform attention level 1/|K_t|.
 __device__ __forceinline__ float attention_weight(float alpha, int norm, int n_tokens) {

@@ -37,6 +37,8 @@ struct Dims {
     int multi;     // 1: the multi-kernel path runs at some step (its scratch exists)
     int norm_attn; // 1: the attention term of Eq. 4 is alpha * |K_t| * a_i
     int aligned;   // 1: region-aligned pages (hole slots; n_live counts the tokens)
+    int quant;     // 1: quantised tier on (pages may hold 8-bit codes)
+    float quant_thr;  // quantised tier: pages scoring below it are quantised
     int n_wg;      // k_attend workgroups (all co-resident)
     int wg_per_cu; // k_attend workgroups per CU (n_wg = wg_per_cu * CUs)
     int lane_cap;  // units one lane of k_attend workgroups holds (one workgroup per CU)
@@ -57,6 +59,7 @@ struct View {
     int32_t* n_pages;
     int32_t* n_tokens;
     int32_t* n_live;   // [S] tokens |K_t|: the n_tokens array itself unless aligned
+    uint8_t* page_format;  // [NP] quantised tier: 1 = the page holds 8-bit codes
     int32_t* clock;
     int32_t* next_serial;
     int32_t* budget;
@@ -104,7 +107,7 @@ hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st);
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q,
                          float* abar_out, hipStream_t st);
 size_t attend_lds_bytes(int G);
-const void* attend_kernel(int G, int aligned);   // the instantiation for group size G and page layout
+const void* attend_kernel(int G, int aligned, int quant);   // the instantiation for G, layout, tier
 // Launch the fused kernel in check mode with n_wg workgroups: every wave
 // waits (bounded, ~20 ms) until all workgroups have arrived; probe[1]
 // receives the fewest arrivals any workgroup saw (probe: 2 device ints).
@@ -120,5 +123,8 @@ hipError_t launch_calib(const Dims& dm, const View& v, const Scratch& sc, const 
                         unsigned long long* age_sum, hipStream_t st);
 hipError_t launch_compact(const Dims& dm, const View& v, const Scratch& sc,
                           const int32_t* ev_serial, const int32_t* ev_count, hipStream_t st);
+// Quantised tier, before the compaction of the same eviction lists.
+hipError_t launch_quant(const Dims& dm, const View& v, const Scratch& sc,
+                        const int32_t* ev_serial, const int32_t* ev_count, hipStream_t st);
 
 }  // namespace md

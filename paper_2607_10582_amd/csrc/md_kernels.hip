@@ -75,6 +75,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                         slot = 0;
                         v.page_table[row + np] = p;
                         v.page_serial[row + np] = v.next_serial[s];
+                        if (dm.quant) v.page_format[p] = 0;   // a reused page holds bf16 keys again
                         v.next_serial[s] += 1;
                         v.n_pages[s] = np + 1;
                     } else {
@@ -283,6 +284,7 @@ struct LogitsDims {
     int L, Hq, Hkv, G, P, Pshift, S, MP, NP, R, LHkv, max_chunks;
     int W, Gw;   // window queries per observation; MFMA columns G * W
     int aligned; // region-aligned pages: hole slots are masked
+    int quant;   // quantised tier: tiles of quantised pages hold 8-bit codes
 };
 
 // B operands of one row (session s, lkv = layer * Hkv + KV head) in
@@ -327,13 +329,15 @@ __device__ __forceinline__ void split_query_regs(u32x4 (&bq)[4][3], const float*
 struct ItemTiles {
     int slot0[8];
     unsigned vmask;
+    unsigned qmask;   // quantised tier: tiles holding 8-bit codes
     int nt;
 };
 
+template <bool QT>
 __device__ __forceinline__ void item_tiles(ItemTiles& it, const Cursor& cu, const LogitsDims& dm,
                                            const int32_t* __restrict__ page_table,
                                            const int32_t* __restrict__ n_tokens, int32_t* status,
-                                           int lane) {
+                                           int lane, const uint8_t* __restrict__ page_format) {
     const int nt = n_tokens[cu.s];
     const int np = (nt + dm.P - 1) >> dm.Pshift;
     const int* ptab = page_table + (size_t)cu.s * dm.MP;
@@ -350,6 +354,12 @@ __device__ __forceinline__ void item_tiles(ItemTiles& it, const Cursor& cu, cons
         it.slot0[t] = (in_seq && in_pool) ? (p << dm.Pshift) + (tok & (dm.P - 1)) : 0;
     }
     it.vmask = vm;
+    it.qmask = 0;
+    if constexpr (QT) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+            if ((vm & (1u << t)) && page_format[it.slot0[t] >> dm.Pshift]) it.qmask |= 1u << t;
+    }
     it.nt = nt;
     if (bad && lane == 0) atomicOr(status, kDevCorrupt);
 }
@@ -360,6 +370,7 @@ __device__ __forceinline__ void item_tiles(ItemTiles& it, const Cursor& cu, cons
 // contiguous (voff = 16 lane).
 // A tile without cached tokens reads the pool's first row tile instead
 // (always in bounds; its logits are masked), so loads never branch.
+template <bool QT>
 __device__ __forceinline__ void load_tile(u32x4 (&a)[4], const LogitsDims& dm,
                                           const uint16_t* __restrict__ k_pool, const ItemTiles& it,
                                           int t, int lkv, uint32_t voff) {
@@ -367,9 +378,19 @@ __device__ __forceinline__ void load_tile(u32x4 (&a)[4], const LogitsDims& dm,
     const int slot = it.slot0[t];
     const size_t tile = ok ? ((size_t)(slot >> dm.Pshift) * dm.LHkv + lkv) * dm.P + (slot & (dm.P - 1)) : 0;
     gbytes base = uni_ptr(k_pool + tile * kHeadDim);
+    if constexpr (QT) {
+        // a quantised block: codes in its first 2 KiB (a[0], a[1]), the
+        // scale at byte 2048 (a[2], a[3] the same)
+        const bool qt = it.qmask & (1u << t);
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-        a[j] = __builtin_nontemporal_load(reinterpret_cast<gvec>(base + voff + 1024 * j));
+        for (int j = 0; j < 4; ++j)
+            a[j] = __builtin_nontemporal_load(
+                reinterpret_cast<gvec>(base + ((qt && j >= 2) ? 2048u : voff + 1024u * j)));
+    } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            a[j] = __builtin_nontemporal_load(reinterpret_cast<gvec>(base + voff + 1024 * j));
+    }
 }
 
 // Each wave streams a contiguous run of work items (128-token chunks of one
@@ -384,12 +405,14 @@ __device__ __forceinline__ void load_tile(u32x4 (&a)[4], const LogitsDims& dm,
 // consecutive k = 8 (l >> 4) .. +7; C lane l holds column l & 15, rows
 // 4 (l >> 4) .. +3.  Softmax statistics of the chunk are kept online per
 // lane and merged across the four row quads at the end of the chunk.
+template <bool QT>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3, 3)))
 k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __restrict__ page_table,
          const int32_t* __restrict__ n_tokens, const float* __restrict__ q,
          float* __restrict__ logits, float2* __restrict__ cstats, int32_t* status,
          const int32_t* __restrict__ item_prefix, const int32_t* __restrict__ t_ins,
-         const int32_t* __restrict__ clock, const uint8_t* __restrict__ region) {
+         const int32_t* __restrict__ clock, const uint8_t* __restrict__ region,
+         const uint8_t* __restrict__ page_format) {
     __shared__ int s_pref[kMaxSessions + 1];
     const int S = dm.S;
     for (int i = threadIdx.x; i <= S; i += blockDim.x) s_pref[i] = item_prefix[i];
@@ -429,9 +452,9 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
         (void)l;
         (void)kv;
         ItemTiles cur;
-        item_tiles(cur, cu, dm, page_table, n_tokens, status, lane);
+        item_tiles<QT>(cur, cu, dm, page_table, n_tokens, status, lane, page_format);
 #pragma unroll
-        for (int t = 0; t < 4; ++t) load_tile(ring[t], dm, k_pool, cur, t, cu.lkv, voff);
+        for (int t = 0; t < 4; ++t) load_tile<QT>(ring[t], dm, k_pool, cur, t, cu.lkv, voff);
 
         // Inner loop: the segment's items, streamed without a break.
         for (; it < seg_end; ++it) {
@@ -439,27 +462,43 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
             if (it + 1 < seg_end) {
                 Cursor nx = cu;
                 ++nx.c;
-                item_tiles(nxt, nx, dm, page_table, n_tokens, status, lane);
+                item_tiles<QT>(nxt, nx, dm, page_table, n_tokens, status, lane, page_format);
             } else {
                 nxt = cur;
                 nxt.vmask = 0;
+                nxt.qmask = 0;
             }
             const int tok0 = cu.c * kChunk;
             float m = -INFINITY, lsum = 0.0f;
 #pragma unroll
             for (int t = 0; t < 8; ++t) {
                 f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+                if (QT && (cur.qmask & (1u << t))) {
+                    // quantised tile: codes as bf16 (exact), the scale after the sum
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
+                    for (int j = 0; j < 4; ++j) {
+                        const u32x4 av = (j & 1) ? codes_to_bf16<1>(ring[t & 3][j >> 1]) : codes_to_bf16<0>(ring[t & 3][j >> 1]);
 #pragma unroll
-                    for (int p = 0; p < 3; ++p)
-                        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            __builtin_bit_cast(bf16x8, ring[t & 3][j]), __builtin_bit_cast(bf16x8, bq[j][p]),
-                            acc, 0, 0, 0);
+                        for (int p = 0; p < 3; ++p)
+                            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                __builtin_bit_cast(bf16x8, av), __builtin_bit_cast(bf16x8, bq[j][p]), acc, 0, 0, 0);
+                    }
+                    const float qs = __uint_as_float(ring[t & 3][2][0]);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[i] *= qs;
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+                        for (int p = 0; p < 3; ++p)
+                            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                __builtin_bit_cast(bf16x8, ring[t & 3][j]), __builtin_bit_cast(bf16x8, bq[j][p]),
+                                acc, 0, 0, 0);
+                    }
                 }
                 // refill the slot with the tile four ahead
-                if (t < 4) load_tile(ring[t & 3], dm, k_pool, cur, t + 4, cu.lkv, voff);
-                else load_tile(ring[t & 3], dm, k_pool, nxt, t - 4, cu.lkv, voff);
+                if (t < 4) load_tile<QT>(ring[t & 3], dm, k_pool, cur, t + 4, cu.lkv, voff);
+                else load_tile<QT>(ring[t & 3], dm, k_pool, nxt, t - 4, cu.lkv, voff);
 
                 // base-2 logits; tokens past the session's count, tokens
                 // newer than the column's window query, and hole slots are
@@ -519,10 +558,10 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
 hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q, int n_blocks,
                          hipStream_t st) {
     LogitsDims ld{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.S, dm.MP, dm.NP, dm.R, dm.LHkv, dm.max_chunks,
-                  dm.W, dm.G * dm.W, dm.aligned};
-    hipLaunchKernelGGL(k_logits, dim3(n_blocks), dim3(256), 0, st, ld, v.k_pool, v.page_table,
+                  dm.W, dm.G * dm.W, dm.aligned, dm.quant};
+    hipLaunchKernelGGL(dm.quant ? k_logits<true> : k_logits<false>, dim3(n_blocks), dim3(256), 0, st, ld, v.k_pool, v.page_table,
                        v.n_tokens, q, sc.logits, sc.cstats, sc.status, sc.item_prefix, v.t_ins, v.clock,
-                       v.region);
+                       v.region, v.page_format);
     return hipGetLastError();
 }
 
@@ -927,6 +966,97 @@ __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratc
         atomicAdd(&sc.counters[2], (unsigned long long)gone_total);
         atomicAdd(&sc.counters[3], (unsigned long long)live_gone_total);
     }
+}
+
+// ---------------------------------------------------------------- quantised tier
+
+// Quantised tier (Sec. III-E), before the compaction of the same lists:
+// every page that survives the eviction, is not pinned (its score is +inf),
+// is not the session's last page, is still bf16 and scores below the
+// threshold becomes 8-bit codes.  Grid (blocks, S): block x takes the page
+// indices x, x + gridDim.x, ...; an eligible page's (row, 16-token block)
+// pairs go to the four waves in turn.  A wave reads its block's 4 KiB (lane
+// l: 16 bytes at 16 l + 1024 j, i.e. token l % 16, dims 32 j + 8 (l / 16)
+// .. +7), reduces max|k| over the block's tokens, and writes the codes over
+// the block's first 2 KiB (lane l: 16 bytes at 16 l + 1024 j', the codes of
+// its chunks 2 j' and 2 j' + 1) and the scale (four copies) at byte 2048,
+// once every lane has read (the reduction needs them all).
+__global__ void __launch_bounds__(256) k_quant(Dims dm, View v, Scratch sc, const int32_t* __restrict__ ev_serial,
+                                               const int32_t* __restrict__ ev_count) {
+    const int s = blockIdx.y;
+    const int np = v.n_pages[s];
+    if (!sc.valid[s] || np < 2) return;
+    const int cnt = min(max(ev_count[s], 0), dm.MP);
+    const int32_t* evs = ev_serial + (size_t)s * dm.MP;
+    const int32_t* ptab = v.page_table + (size_t)s * dm.MP;
+    const int32_t* pser = v.page_serial + (size_t)s * dm.MP;
+    const int lane = lane_id(), wv = threadIdx.x >> 6;
+    const int nblk = dm.P >> 4;
+    for (int i = blockIdx.x; i < np - 1; i += gridDim.x) {   // never the last page
+        const float ps = sc.pscore[(size_t)s * dm.MP + i];
+        const int phys = ptab[i];
+        bool ok = ps < dm.quant_thr && (unsigned)phys < (unsigned)dm.NP;
+        if (ok) ok = v.page_format[phys] == 0;
+        if (ok) {   // not evicted by this step (the serials in the list ascend)
+            const int se = pser[i];
+            int lo = 0, hi = cnt;
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (evs[mid] < se) lo = mid + 1; else hi = mid;
+            }
+            ok = !(lo < cnt && evs[lo] == se);
+        }
+        if (!ok) continue;   // uniform over the block
+        for (int b = wv; b < dm.LHkv * nblk; b += 4) {
+            const int r = b / nblk, blk = b - r * nblk;
+            char* base = reinterpret_cast<char*>(v.k_pool + (((size_t)phys * dm.LHkv + r) * dm.P + 16 * blk) * kHeadDim);
+            u32x4 x[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) x[j] = *reinterpret_cast<const u32x4*>(base + 16 * lane + 1024 * j);
+            // a hole (region-aligned pages) holds no token
+            const bool tok = !dm.aligned || v.region[(size_t)phys * dm.P + 16 * blk + (lane & 15)] != kHole;
+            float m = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    m = fmaxf(m, fabsf(__uint_as_float(x[j][w] << 16)));
+                    m = fmaxf(m, fabsf(__uint_as_float(x[j][w] & 0xffff0000u)));
+                }
+            m = wave_max(tok ? m : 0.0f);
+            const float scale = m > 0.0f ? __fdiv_rn(m, 127.0f) : 0.0f;
+            u32x4 out[2] = {u32x4{0u, 0u, 0u, 0u}, u32x4{0u, 0u, 0u, 0u}};
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    uint32_t pair = 0;
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        const float f = __uint_as_float(e ? (x[j][w] & 0xffff0000u) : (x[j][w] << 16));
+                        int c = 0;
+                        if (tok && m > 0.0f) c = (int)fminf(fmaxf(rintf(__fdiv_rn(f, scale)), -127.0f), 127.0f);
+                        pair |= ((uint32_t)c & 0xffu) << (8 * e);
+                    }
+                    // dims 2w, 2w + 1 of chunk j: bytes 8 (j & 1) + 2w, +1 of out[j >> 1]
+                    out[j >> 1][2 * (j & 1) + (w >> 1)] |= pair << (16 * (w & 1));
+                }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) *reinterpret_cast<u32x4*>(base + 16 * lane + 1024 * j) = out[j];
+            if (lane == 0) {
+                const uint32_t sb = __float_as_uint(scale);
+                *reinterpret_cast<u32x4*>(base + 2048) = u32x4{sb, sb, sb, sb};
+            }
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) v.page_format[phys] = 1;
+    }
+}
+
+hipError_t launch_quant(const Dims& dm, const View& v, const Scratch& sc, const int32_t* ev_serial,
+                        const int32_t* ev_count, hipStream_t st) {
+    hipLaunchKernelGGL(k_quant, dim3(64, dm.S), dim3(256), 0, st, dm, v, sc, ev_serial, ev_count);
+    return hipGetLastError();
 }
 
 hipError_t launch_compact(const Dims& dm, const View& v, const Scratch& sc,

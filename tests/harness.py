@@ -151,12 +151,13 @@ class Pair:
                     alpha=f32(self.alpha), rho=f32(w.rho), tau_scale=f32(w.tau_scale),
                     pinned_mask=self.pinned_mask, budget=int(self.B[s]), clock=n0, region=reg,
                     keys_bits=kb if n0 else np.zeros((0, w.L, w.Hkv, w.d), np.uint16),
-                    capacity=n0 + self.steps, attention_norm=w.attention_norm, region_aligned=al)
+                    capacity=n0 + self.steps, attention_norm=w.attention_norm, region_aligned=al,
+                    quant_threshold=w.quant_threshold)
         self.cache.set_free_pages(perm[pos:][::-1])
         self.md = MemDecay(self.cache, torch.from_numpy(self.b), torch.from_numpy(self.lam),
                            rho=f32(w.rho), alpha=f32(self.alpha), tau_scale=f32(w.tau_scale),
                            pinned_mask=self.pinned_mask, fused=fused, attention_norm=w.attention_norm,
-                           window=w.window, region_aligned=al)
+                           window=w.window, region_aligned=al, quant_threshold=w.quant_threshold)
         n_slots = n_phys * P
         self.abar = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
         self.tscore = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
@@ -229,6 +230,7 @@ class Pair:
         final_ser = ev_ser.copy()
         final_cnt = ev_cnt.copy()
         tref_fix = []
+        quant_before = {s: {p.serial for p in self.oracles[s].pages if p.quant} for s in self.oracle_sessions}
         for s in self.oracle_sessions:
             rec = self.oracles[s].step(qo[s], nko[s], int(reg[s]))
             self.last_rec[s] = rec
@@ -312,8 +314,38 @@ class Pair:
                 o = self.oracles[s]
                 assert int(n_tokens[s]) == o.n_tokens(), (k, s, "n after compaction")
                 assert pser[s, :n_pages[s]].tolist() == [p.serial for p in o.pages], (k, s)
+                if w.quant_threshold > 0:
+                    self.check_quantised(s, quant_before[s])
         self.stats.steps += 1
         return self.stats
+
+    def check_quantised(self, s: int, before):
+        """Quantised tier: the device's page formats equal the oracle's, and
+        the codes and scales of the pages quantised this step are bit-exact
+        (decoded from the pool with the byte layout memdecay.h gives)."""
+        c, o, P, w = self.cache, self.oracles[s], self.w.P, self.w
+        npg = int(c.n_pages[s].item())
+        ptab = c.page_table[s, :npg].cpu().numpy().astype(np.int64)
+        fmt = c.page_format.cpu().numpy()[ptab]
+        assert fmt.tolist() == [int(p.quant) for p in o.pages], (self.k, s, "page formats")
+        t_ = np.arange(16)[:, None]
+        e_ = np.arange(w.d)[None, :]
+        off = 1024 * (e_ // 64) + 16 * (t_ + 16 * ((e_ // 8) % 4)) + 8 * ((e_ // 32) % 2) + e_ % 8   # [16][d]
+        for i, p in enumerate(o.pages):
+            if not p.quant or p.serial in before:
+                continue
+            raw = c.k_pool[int(ptab[i])].contiguous().view(torch.uint8).view(w.L, w.Hkv, P // 16, 4096).cpu().numpy()
+            slots = np.asarray(p.slots, np.int64)
+            for g0 in range(0, slots.size, 16):
+                grp = slots[g0:g0 + 16]
+                blk = raw[:, :, g0 // 16]                                        # [L][Hkv][4096]
+                codes = blk[:, :, off].view(np.int8)[:, :, :grp.size]            # [L][Hkv][tokens][d]
+                scale = blk[:, :, 2048:2052].copy().view(np.float32)[:, :, 0]    # [L][Hkv]
+                want_c = o.codes[:, :, grp].astype(np.int8)                      # [L][Hkv][tokens][d]
+                want_s = o.qscale[:, :, grp[0]]
+                assert np.array_equal(codes, want_c), (self.k, s, p.serial, "codes")
+                assert np.array_equal(scale.view(np.uint32), want_s.astype(np.float32).view(np.uint32)), \
+                    (self.k, s, p.serial, "scales")
 
     def live_counts(self) -> np.ndarray:
         """|K_t| per session on the device: n_live with region-aligned pages."""

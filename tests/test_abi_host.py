@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert B.md_abi_version() == 4
+    assert B.md_abi_version() == 5
     for st in (0, -1, -2, -3, -4, -5, -6):
         assert B.md_status_str(st)
     assert B.md_status_str(12345) == "unknown status"
@@ -56,11 +56,11 @@ def test_struct_layout_matches_the_header(lib):
     #include <stddef.h>
     #include "memdecay.h"
     int main(void) {
-      printf("%zu %zu %zu %zu %zu %zu\n", sizeof(md_config), offsetof(md_config, rho),
-             offsetof(md_config, flags), offsetof(md_config, window), sizeof(md_region_params),
-             sizeof(md_cache_view));
-      printf("%zu %zu %zu\n", offsetof(md_cache_view, importance), offsetof(md_cache_view, free_count),
-             offsetof(md_cache_view, n_live));
+      printf("%zu %zu %zu %zu %zu %zu %zu\n", sizeof(md_config), offsetof(md_config, rho),
+             offsetof(md_config, flags), offsetof(md_config, window),
+             offsetof(md_config, quant_threshold), sizeof(md_region_params), sizeof(md_cache_view));
+      printf("%zu %zu %zu %zu\n", offsetof(md_cache_view, importance), offsetof(md_cache_view, free_count),
+             offsetof(md_cache_view, n_live), offsetof(md_cache_view, page_format));
       return 0; }
     '''
     with tempfile.TemporaryDirectory() as d:
@@ -70,10 +70,10 @@ def test_struct_layout_matches_the_header(lib):
         subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), c, "-o", exe], check=True)
         out = subprocess.run([exe], capture_output=True, text=True, check=True).stdout.split()
     got = [ctypes.sizeof(B.md_config), B.md_config.rho.offset, B.md_config.flags.offset,
-           B.md_config.window.offset,
+           B.md_config.window.offset, B.md_config.quant_threshold.offset,
            ctypes.sizeof(B.md_region_params), ctypes.sizeof(B.md_cache_view),
            B.md_cache_view.importance.offset, B.md_cache_view.free_count.offset,
-           B.md_cache_view.n_live.offset]
+           B.md_cache_view.n_live.offset, B.md_cache_view.page_format.offset]
     assert [int(x) for x in out] == got
 
 
@@ -120,6 +120,8 @@ def fake_rp():
     (dict(tau_scale=-2.0), B.MD_E_INVALID),
     (dict(flags=16), B.MD_E_INVALID),
     (dict(window=0), B.MD_E_INVALID),
+    (dict(quant_threshold=-1.0), B.MD_E_INVALID),
+    (dict(quant_threshold=float("nan")), B.MD_E_INVALID),
     (dict(window=3), B.MD_E_UNSUPPORTED),            # G = 6: 18 MFMA columns
     (dict(window=2, flags=2), B.MD_E_UNSUPPORTED),   # the fused kernel takes W = 1
     (dict(flags=3), B.MD_E_INVALID),
@@ -129,10 +131,15 @@ def test_init_rejects_bad_configs_on_the_host(lib, kw, expect):
     assert st == expect and h is None
 
 
-@pytest.mark.parametrize("field", [f for f, _ in B.md_cache_view._fields_ if f != "n_live"])
+@pytest.mark.parametrize("field", [f for f, _ in B.md_cache_view._fields_ if f not in ("n_live", "page_format")])
 def test_init_rejects_null_buffers(lib, field):
     st, h = B.md_init_raw(good_config(), fake_rp(), fake_view(**{field: 0}), 0)
     assert st == B.MD_E_INVALID
+
+
+def test_quantised_tier_needs_the_page_formats(lib):
+    st, h = B.md_init_raw(good_config(quant_threshold=0.5), fake_rp(), fake_view(page_format=0), 0)
+    assert st == B.MD_E_INVALID and h is None
 
 
 @pytest.mark.parametrize("kw", [dict(n_live=0), dict(n_live=0x10002), dict(region=0x10001)])

@@ -411,3 +411,50 @@ def test_region_aligned_window():
     w = C.with_overrides(C.get("small_aligned"), window=2, obs_interval=2, steps=24)
     p = Pair(w, fused=None, planted=24, planted_strength=2.5, query_gain=0.7)
     run_pair(p, 24, "aligned-window2")
+
+
+# ---------------------------------------------------------------- quantised tier
+
+def run_quant(p: Pair, steps: int, label: str):
+    say(f"[{label}] S={p.w.S} L={p.w.L} Hq={p.w.Hq} P={p.w.P} thr={p.w.quant_threshold} steps={steps}")
+    for _ in range(steps):
+        st = p.step()
+    assert p.device_status() == 0 and p.free_pages_consistent()
+    nq = sum(int(pg.quant) for o in p.oracles.values() for pg in o.pages)
+    say(f"[{label}] ok: {st.steps} steps, max rel {st.max_rel}, evicted pages {st.evicted_pages}, "
+        f"quantised pages now {nq}")
+    p.close()
+    return nq
+
+
+@pytest.mark.parametrize("fused", [True, False])
+@pytest.mark.parametrize("thr", [0.35, float("inf")])
+def test_quantised_tier_small(thr, fused):
+    # The quantised tier (Sec. III-E): pages scoring below the threshold keep
+    # 8-bit codes; the codes and scales written on the device equal the
+    # oracle's bit for bit (checked in the harness after every step), and the
+    # attention over them matches within the usual tolerance.
+    w = C.with_overrides(C.get("small"), quant_threshold=thr)
+    p = Pair(w, fused=fused, planted=24, planted_strength=2.5, query_gain=0.7)
+    assert run_quant(p, w.steps, f"quant-small-{thr}-fused{int(fused)}") > 2
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_quantised_tier_3b_shape_pages_of_64_region_aligned(fused):
+    w = C.with_overrides(C.get("small"), L=2, Hq=16, Hkv=2, P=64, n0=900, budget_frac=0.6,
+                         append_cycle=C.APPEND_CYCLE, region_aligned=True, append_run=4,
+                         quant_threshold=0.4, steps=20)
+    p = Pair(w, fused=fused)
+    assert run_quant(p, 20, f"quant-3b-p64-aligned-fused{int(fused)}") > 0
+
+
+def test_quantised_tier_with_a_window():
+    w = C.with_overrides(C.get("small"), L=2, window=2, obs_interval=2, quant_threshold=0.35, steps=24)
+    p = Pair(w, fused=None, planted=24, planted_strength=2.5, query_gain=0.7)
+    assert run_quant(p, 24, "quant-window2") > 0
+
+
+def test_quantised_tier_long32k_sampled_sessions():
+    w = C.with_overrides(C.get("long32k"), quant_threshold=0.3)
+    p = Pair(w, backend="torch", oracle_sessions=[0, 11], steps=6, fused=True)
+    assert run_quant(p, 3, "quant-long32k") > 0
