@@ -56,8 +56,9 @@
  * n_live counts the tokens alone.
  * Quantised pages (quant_threshold > 0, page_format[p] = 1): each 16-token
  * block of a (layer, KV head) tile keeps, in the first 2 KiB of its 4 KiB,
- * int8 codes c with key = s * c, and its scale s as float32 in bytes 2048 ..
- * 2051 (repeated in 2052 .. 2063); the code of token t (0..15) and dim e
+ * FP8 E4M3 codes c (OCP format: bias 7, no infinities) with key = s * c, and
+ * its scale s as float32 in bytes 2048 .. 2051 (repeated in 2052 .. 2063);
+ * the code of token t (0..15) and dim e
  * sits at byte 1024 (e / 64) + 16 (t + 16 ((e / 8) % 4)) + 8 ((e / 32) % 2)
  * + e % 8.  Region codes follow the paper's label
  * list: system 0, plan 1, user 2, tool_in 3, tool_out 4, retrieval 5,
@@ -271,9 +272,9 @@ md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_cou
  * compaction, every page that survives, is not pinned, is not the session's
  * last page, is still bf16 and has page score S_p < quant_threshold (the
  * scores of this step's md_score_pages) is quantised in place: per 16-token
- * block and (layer, KV head), s = max|k| / 127 and c = clamp(rint(k / s),
- * -127, 127) in float32 (s = 0, c = 0 for an all-zero block; holes get
- * c = 0), page_format = 1.  Irreversible.  Requires md_score_pages since the
+ * block and (layer, KV head), s = max|k| / 448 in float32 and c = the E4M3
+ * value nearest to the float32 quotient k / s (ties to even, saturating at
+ * 448; s = 0, c = 0 for an all-zero block; holes get c = 0), page_format = 1.  Irreversible.  Requires md_score_pages since the
  * last md_observe_step (MD_E_STATE otherwise).
  */
 md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* evict_count);

@@ -63,8 +63,12 @@ design notes of the repository):
     page before eviction), is still in full precision and scores
     S_p < quant_threshold is quantised, once and for good.  Each group of
     16 consecutive tokens of the page, per (layer, KV head), gets one scale
-    s = max|k| / 127 and codes c = clamp(rint(k / s), -127, 127), both in
-    float32 (s = 0 and c = 0 when max|k| = 0); attention then uses s * c.
+    s = max|k| / 448 (float32) and 8-bit codes c = the FP8 E4M3 value
+    nearest to k / s (float32 quotient, ties to even, at most 448 in
+    magnitude); s = 0 and c = 0 when max|k| = 0.  Attention then uses
+    s * c.  (Sec. III-E names low precision without a format; E4M3 is the
+    8-bit format the device widens to its MFMA operand type in one
+    instruction.)
 """
 from __future__ import annotations
 
@@ -91,20 +95,51 @@ def softmax(x: np.ndarray) -> np.ndarray:
 class Page:
     serial: int
     slots: List[int]
-    quant: bool = False     # keys held as 8-bit codes and a scale per 16 tokens
+    quant: bool = False     # keys held as E4M3 codes and a scale per 16 tokens
+
+
+E4M3_MAX = 448.0
+
+
+def e4m3_decode(bits) -> np.ndarray:
+    """FP8 E4M3 (OCP, 'FN': bias 7, no infinities, S.1111.111 is NaN) bit
+    patterns -> float64 values."""
+    b = np.asarray(bits, dtype=np.int64)
+    sign = np.where(b & 0x80, -1.0, 1.0)
+    e = (b >> 3) & 15
+    m = (b & 7).astype(np.float64)
+    val = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * np.exp2(e.astype(np.float64) - 7.0))
+    val = np.where((e == 15) & ((b & 7) == 7), np.nan, val)
+    return sign * val
+
+
+def e4m3_encode(v) -> np.ndarray:
+    """float32 values -> the nearest FP8 E4M3 bit patterns (ties to even),
+    magnitudes above 448 saturating to 448; the sign bit is set for v < 0."""
+    v = np.asarray(v, dtype=np.float32)
+    a = np.abs(v).astype(np.float64)
+    sign = np.where(v < 0, 0x80, 0)
+    # subnormal range (below 2^-6): steps of 2^-9; code 8 is the smallest normal
+    sub = np.rint(a * 512.0)
+    mant, ex = np.frexp(a)                      # a = mant 2^ex, mant in [0.5, 1)
+    q = np.rint((2.0 * mant - 1.0) * 8.0)       # 3 mantissa bits of a = (2 mant) 2^(ex - 1)
+    e = ex - 1 + (q == 8)
+    q = np.where(q == 8, 0, q)
+    norm = ((e + 7) << 3) | q.astype(np.int64)
+    bits = np.where(a < 2.0 ** -6, sub.astype(np.int64), np.minimum(norm, 0x7E))
+    return (sign | bits).astype(np.uint8)
 
 
 def quantise_block(x: np.ndarray):
     """Codes and scale of one group of keys (float32 values, any shape): the
-    scale max|x| / 127 and the codes rint(x / scale) clamped to [-127, 127],
-    both computed in float32; an all-zero group gets scale 0 and codes 0."""
+    scale max|x| / 448 and the E4M3 codes of x / scale, both computed in
+    float32; an all-zero group gets scale 0 and codes 0."""
     x = np.asarray(x, dtype=np.float32)
     m = np.float32(np.max(np.abs(x))) if x.size else np.float32(0)
     if m == 0:
-        return np.zeros(x.shape, np.int8), np.float32(0)
-    s = np.float32(m / np.float32(127))
-    c = np.clip(np.rint(x / s), -127, 127).astype(np.int8)
-    return c, s
+        return np.zeros(x.shape, np.uint8), np.float32(0)
+    s = np.float32(m / np.float32(E4M3_MAX))
+    return e4m3_encode(x / s), s
 
 
 @dataclass
@@ -165,7 +200,7 @@ class Session:
         self.a = np.zeros(cap, dtype=np.float64)
         self.keys = np.zeros((L, Hkv, cap, d), dtype=np.float32)
         # quantised tokens: codes [L][Hkv][slot][d] and their group's scale
-        self.codes = np.zeros((L, Hkv, cap, d), dtype=np.int8) if self.quant_threshold > 0 else None
+        self.codes = np.zeros((L, Hkv, cap, d), dtype=np.uint8) if self.quant_threshold > 0 else None
         self.qscale = np.zeros((L, Hkv, cap), dtype=np.float32) if self.quant_threshold > 0 else None
         self.is_quant = np.zeros(cap, dtype=bool)
         self.n_slots = n
@@ -219,7 +254,7 @@ class Session:
         k[:, :, :cap, :] = self.keys
         self.keys = k
         if self.codes is not None:
-            c = np.zeros((self.L, self.Hkv, new, self.d), dtype=np.int8)
+            c = np.zeros((self.L, self.Hkv, new, self.d), dtype=np.uint8)
             c[:, :, :cap, :] = self.codes
             self.codes = c
             sc = np.zeros((self.L, self.Hkv, new), dtype=np.float32)
@@ -255,7 +290,7 @@ class Session:
             qz = self.is_quant[slots]
             if np.any(qz):
                 qs = slots[qz]
-                k[qz] = self.codes[l, kv][qs].astype(np.float64) * \
+                k[qz] = e4m3_decode(self.codes[l, kv][qs]) * \
                     self.qscale[l, kv][qs].astype(np.float64)[:, None]
         return k
 

@@ -78,7 +78,7 @@ struct AttendArgs {
     int32_t* status;
     int32_t* probe;    // check mode only: [arrivals, least seen]
     const int32_t* n_live;   // tokens |K_t| (the n_tokens array unless pages are region-aligned)
-    const uint8_t* page_format;   // quantised tier: 1 = the page holds 8-bit codes
+    const uint8_t* page_format;   // quantised tier: 1 = the page holds E4M3 codes
 };
 
 // LDS row stride (floats) of a head's values: W waves of KT tiles

@@ -120,19 +120,44 @@ __device__ __forceinline__ bool page_score_of(float score, bool live, bool pinne
     return cnt > 0;
 }
 
-// Eight int8 key codes (bytes 8 half .. 8 half + 7 of v) as eight bf16
-// values in the MFMA operand order: codes are integers of magnitude <= 127,
-// exact in bf16, so the product with the query stays exact.
-__device__ __forceinline__ uint32_t codes_pair_to_bf16(uint32_t x, int sh) {
-    const uint32_t lo = __float_as_uint((float)(int8_t)((x >> sh) & 0xffu)) >> 16;
-    const uint32_t hi = __float_as_uint((float)(int8_t)((x >> (sh + 8)) & 0xffu)) >> 16;
-    return lo | (hi << 16);
+// Eight FP8 E4M3 key codes (bytes 8 half .. 8 half + 7 of v) as eight bf16
+// values in the MFMA operand order.  The hardware widens two codes at a time
+// to float32 (exactly); E4M3 values have four significant bits, so their
+// bf16 halves are exact too, and the product with the query stays exact.
+template <bool HIGH>
+__device__ __forceinline__ uint32_t codes_pair_to_bf16(uint32_t x) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    const f32x2 f = __builtin_amdgcn_cvt_pk_f32_fp8((int)x, HIGH);
+    return (__float_as_uint(f[0]) >> 16) | (__float_as_uint(f[1]) & 0xffff0000u);
 }
 template <int HALF>
 __device__ __forceinline__ u32x4 codes_to_bf16(u32x4 v) {
     const uint32_t w0 = HALF ? v[2] : v[0], w1 = HALF ? v[3] : v[1];
-    return u32x4{codes_pair_to_bf16(w0, 0), codes_pair_to_bf16(w0, 16), codes_pair_to_bf16(w1, 0),
-                 codes_pair_to_bf16(w1, 16)};
+    return u32x4{codes_pair_to_bf16<false>(w0), codes_pair_to_bf16<true>(w0), codes_pair_to_bf16<false>(w1),
+                 codes_pair_to_bf16<true>(w1)};
+}
+
+// The FP8 E4M3 code (OCP: bias 7, no infinities) nearest to v, ties to even,
+// magnitudes above 448 saturating to 448; the sign bit is set for v < 0.
+// Exact steps only: a power-of-two scaling, Sterbenz subtraction, rint.
+__device__ __forceinline__ uint32_t e4m3_encode(float v) {
+    const uint32_t sign = v < 0.0f ? 0x80u : 0u;
+    const float a = fabsf(v);
+    uint32_t bits;
+    if (a < 0.015625f) {                 // below 2^-6: steps of 2^-9; 8 is the smallest normal
+        bits = (uint32_t)rintf(a * 512.0f);
+    } else {
+        int ex;
+        const float m = frexpf(a, &ex);  // a = m 2^ex, m in [0.5, 1)
+        int q = (int)rintf((2.0f * m - 1.0f) * 8.0f);
+        int e = ex - 1;
+        if (q == 8) {
+            q = 0;
+            e += 1;
+        }
+        bits = min((uint32_t)(((e + 7) << 3) | q), 0x7Eu);
+    }
+    return sign | bits;
 }
 
 // Weight of the attention term of Eq. 4: alpha, or alpha * |K_t| when the

@@ -973,7 +973,8 @@ __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratc
 // Quantised tier (Sec. III-E), before the compaction of the same lists:
 // every page that survives the eviction, is not pinned (its score is +inf),
 // is not the session's last page, is still bf16 and scores below the
-// threshold becomes 8-bit codes.  Grid (blocks, S): block x takes the page
+// threshold becomes FP8 E4M3 codes with a float32 scale max|k| / 448 per
+// 16-token block and row.  Grid (blocks, S): block x takes the page
 // indices x, x + gridDim.x, ...; an eligible page's (row, 16-token block)
 // pairs go to the four waves in turn.  A wave reads its block's 4 KiB (lane
 // l: 16 bytes at 16 l + 1024 j, i.e. token l % 16, dims 32 j + 8 (l / 16)
@@ -1024,7 +1025,7 @@ __global__ void __launch_bounds__(256) k_quant(Dims dm, View v, Scratch sc, cons
                     m = fmaxf(m, fabsf(__uint_as_float(x[j][w] & 0xffff0000u)));
                 }
             m = wave_max(tok ? m : 0.0f);
-            const float scale = m > 0.0f ? __fdiv_rn(m, 127.0f) : 0.0f;
+            const float scale = m > 0.0f ? __fdiv_rn(m, 448.0f) : 0.0f;
             u32x4 out[2] = {u32x4{0u, 0u, 0u, 0u}, u32x4{0u, 0u, 0u, 0u}};
 #pragma unroll
             for (int j = 0; j < 4; ++j)
@@ -1034,9 +1035,8 @@ __global__ void __launch_bounds__(256) k_quant(Dims dm, View v, Scratch sc, cons
 #pragma unroll
                     for (int e = 0; e < 2; ++e) {
                         const float f = __uint_as_float(e ? (x[j][w] & 0xffff0000u) : (x[j][w] << 16));
-                        int c = 0;
-                        if (tok && m > 0.0f) c = (int)fminf(fmaxf(rintf(__fdiv_rn(f, scale)), -127.0f), 127.0f);
-                        pair |= ((uint32_t)c & 0xffu) << (8 * e);
+                        const uint32_t c = (tok && m > 0.0f) ? e4m3_encode(__fdiv_rn(f, scale)) : 0u;
+                        pair |= c << (8 * e);
                     }
                     // dims 2w, 2w + 1 of chunk j: bytes 8 (j & 1) + 2w, +1 of out[j >> 1]
                     out[j >> 1][2 * (j & 1) + (w >> 1)] |= pair << (16 * (w & 1));

@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 import scipy.special
 
-from oracle import Session, quantise_block
+from oracle import Session, e4m3_decode, e4m3_encode, quantise_block
 
 NREG = 7
 PLAN, USER = 1, 2
@@ -29,46 +29,69 @@ def widen(bits):
 
 # ------------------------------------------------------------ the encoding
 
+def test_e4m3_table_follows_the_format():
+    # OCP FP8 E4M3 ("FN"): bias 7, three mantissa bits, no infinities
+    d = e4m3_decode(np.arange(256))
+    assert d[0x38] == 1.0 and d[0x7E] == 448.0 and d[0xFE] == -448.0
+    assert d[0x08] == 2.0 ** -6 and d[0x01] == 2.0 ** -9 and d[0x07] == 7 * 2.0 ** -9
+    assert d[0x40] == 2.0 and d[0x3C] == 1.5 and d[0x80] == 0.0
+    assert np.isnan(d[0x7F]) and np.isnan(d[0xFF])
+    fin = d[np.isfinite(d)]
+    assert fin.size == 254 and np.all(np.diff(np.sort(np.unique(fin))) > 0)
+
+
+def test_encode_round_trips_every_code():
+    codes = np.array([c for c in range(256) if c not in (0x7F, 0xFF, 0x80)], np.uint8)
+    assert np.array_equal(e4m3_encode(e4m3_decode(codes).astype(np.float32)), codes)
+
+
+def test_encode_rounds_to_nearest_even():
+    # midpoints: 1.0625 between 1 and 1.125 (goes to the even mantissa, 1);
+    # 1.1875 between 1.125 and 1.25 (to 1.25); subnormal 2^-10 between 0 and
+    # 2^-9 (to 0) and 3 * 2^-10 (to 2 * 2^-9); just above a midpoint goes up
+    v = np.array([1.0625, 1.1875, 2.0 ** -10, 3 * 2.0 ** -10, 1.0625 + 2.0 ** -20, 500.0, -1.0625], np.float32)
+    assert e4m3_decode(e4m3_encode(v)).tolist() == [1.0, 1.25, 0.0, 2.0 ** -8, 1.125, 448.0, -1.0]
+
+
+def brute_nearest(v):
+    grid = e4m3_decode(np.arange(0x7F))                      # the non-negative finite values
+    a = abs(float(v))
+    return np.sign(v) * grid[np.argmin(np.abs(grid - a))]
+
+
 @pytest.mark.parametrize("seed", [0, 1, 2])
-def test_codes_range_extreme_and_error_bound(seed):
+def test_codes_are_the_nearest_e4m3_values(seed):
     rng = np.random.default_rng(seed)
     x = widen(bf16(rng.normal(size=(16, 128)) * rng.uniform(0.1, 10)))
     c, s = quantise_block(x)
-    assert c.dtype == np.int8 and c.min() >= -127 and c.max() <= 127
+    dec = e4m3_decode(c)
+    assert np.all(np.abs(dec) <= 448)
     i = np.unravel_index(np.argmax(np.abs(x)), x.shape)
-    assert abs(int(c[i])) == 127 and np.sign(c[i]) == np.sign(x[i])
-    # s is max|x| / 127 within one float32 rounding
-    assert abs(float(s) - float(np.max(np.abs(x))) / 127) <= 2 ** -23 * float(s)
-    # rounding to the nearest code: every decoded value within s/2, plus the
-    # float32 rounding of the quotient x / s (|x / s| <= 127, so at most
-    # 127 * 2^-24 steps)
-    err = np.abs(c.astype(np.float64) * float(s) - x.astype(np.float64))
-    assert np.all(err <= float(s) * (0.5 + 128 * 2.0 ** -24))
+    assert abs(dec[i]) == 448 and np.sign(dec[i]) == np.sign(x[i])
+    assert abs(float(s) - float(np.max(np.abs(x))) / 448) <= 2 ** -23 * float(s)
+    # each code is the grid value nearest to the float32 quotient (brute force)
+    qt = (x / s).astype(np.float32)
+    for idx in zip(*np.unravel_index(rng.choice(x.size, 300, replace=False), x.shape)):
+        assert abs(dec[idx] - brute_nearest(qt[idx])) == 0 or \
+            abs(abs(dec[idx]) - abs(float(qt[idx]))) == abs(abs(brute_nearest(qt[idx])) - abs(float(qt[idx])))
 
 
 def test_exact_case_is_lossless():
-    # integer multiples of 1/8 with largest magnitude 127/8: the scale is
-    # exactly 1/8 and the codes are the integers themselves
+    # E4M3 values times 1/8 whose largest magnitude is 448 / 8: the scale is
+    # exactly 1/8 and the codes are those values
     rng = np.random.default_rng(5)
-    ints = rng.integers(-127, 128, size=(16, 128))
-    ints[3, 7] = -127
-    x = (ints / 8.0).astype(np.float32)
+    vals = e4m3_decode(rng.integers(0, 0x7F, size=(16, 128)))
+    vals *= np.where(rng.random((16, 128)) < 0.5, -1.0, 1.0)
+    vals[3, 7] = -448.0
+    x = (vals / 8.0).astype(np.float32)
     c, s = quantise_block(x)
     assert s == np.float32(0.125)
-    assert np.array_equal(c.astype(np.int64), ints)
+    assert np.array_equal(e4m3_decode(c), vals)
 
 
 def test_zero_group():
     c, s = quantise_block(np.zeros((16, 128), np.float32))
     assert s == 0 and not c.any()
-
-
-def test_rounding_is_half_to_even():
-    # codes at exact halves: 0.5 / s and 1.5 / s with s = 1 round to 0 and 2
-    x = np.zeros((1, 128), np.float32)
-    x[0, 0], x[0, 1], x[0, 2] = 127.0, 0.5, 1.5
-    c, s = quantise_block(x)
-    assert s == 1.0 and c[0, 1] == 0 and c[0, 2] == 2
 
 
 # ------------------------------------------------------------ the tier's rules
@@ -126,10 +149,10 @@ def test_lossless_keys_give_unchanged_masses():
     # keys that quantise exactly: the masses with and without the tier agree
     rng = np.random.default_rng(9)
     n, d = 48, 32
-    ints = rng.integers(-127, 128, size=(n, d))
+    vals = e4m3_decode(rng.integers(0, 0x7F, size=(n, d))) * np.where(rng.random((n, d)) < 0.5, -1.0, 1.0)
     for g0 in range(0, n, 16):
-        ints[g0, 0] = 127                    # every group reaches 127
-    keys = ints / 8.0
+        vals[g0, 0] = 448.0                  # every group reaches 448
+    keys = vals / 8.0
     reg = np.full(n, USER)
     a = session(keys, reg, thr=math.inf)
     b = session(keys, reg, thr=0.0)
@@ -156,13 +179,16 @@ def test_mass_over_decoded_keys_is_the_textbook_softmax():
     rec = s.step(q, None, None)
     live = s.live()
     dec = np.where(s.is_quant[live][:, None],
-                   s.codes[0, 0][live].astype(np.float64) * s.qscale[0, 0][live][:, None].astype(np.float64),
+                   e4m3_decode(s.codes[0, 0][live]) * s.qscale[0, 0][live][:, None].astype(np.float64),
                    s.keys[0, 0][live].astype(np.float64))
     want = scipy.special.softmax(dec @ q[0, 0].astype(np.float64) / math.sqrt(d))
     np.testing.assert_allclose(rec.abar, want, rtol=1e-12, atol=0)
-    # and the decoded keys are within half a step of the cached ones
-    err = np.abs(dec - s.keys[0, 0][live])
-    assert np.all(err <= s.qscale[0, 0][live][:, None] * (0.5 + 128 * 2.0 ** -24))
+    # and the decoded keys are within half a grid step of the cached ones:
+    # 2^-4 of the value for normal codes, 2^-10 s below them
+    k = s.keys[0, 0][live].astype(np.float64)
+    sc = s.qscale[0, 0][live][:, None].astype(np.float64)
+    err = np.abs(dec - k)
+    assert np.all(err <= np.abs(k) * (2.0 ** -4 + 2.0 ** -20) + sc * 2.0 ** -10)
 
 
 def test_groups_of_sixteen_within_a_page_of_64():
