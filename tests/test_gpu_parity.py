@@ -128,6 +128,16 @@ def test_max_pages_per_session():
 
 
 @pytest.mark.parametrize("fused", [True, False])
+def test_max_sessions(fused):
+    # 1,024 sessions (the most a handle takes) of 1 to 400 tokens: the work
+    # lists, lane claims and passes at their largest; a sample of sessions
+    # checked token by token, among them the first and the last.
+    w = C.with_overrides(C.get("small"), S=1024, n0=None, n0_range=(1, 400), steps=4, system_len=30)
+    p = Pair(w, oracle_sessions=[0, 1, 255, 256, 511, 700, 1022, 1023], fused=fused)
+    run_pair(p, 4, f"max-sessions-fused{int(fused)}")
+
+
+@pytest.mark.parametrize("fused", [True, False])
 def test_long32k_sampled_sessions(fused):
     # The 16 x 32,768-token workload at full size, inputs drawn on the
     # device; two sessions are checked token by token against the oracle
