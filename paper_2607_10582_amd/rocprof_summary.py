@@ -7,6 +7,8 @@ Two uses:
   markdown table, with the steady-state average of the library's kernels
   (their first ``--skip`` launches left out: md_init's residency check and
   the warm-up steps).
+* ``hits``: L2 (TCC) hit rate of one kernel's steady launches from a
+  ``--pmc TCC_HIT_sum TCC_MISS_sum`` run.
 * ``pmc``: HBM bytes per launch of one kernel from two counter runs
   (``--pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE``), each scaled by what the
   same counter reads for a plain device copy of known size.  Writes the JSON
@@ -93,6 +95,10 @@ def main():
     t.add_argument("trace_dir")
     t.add_argument("--skip", type=int, default=3)
     t.add_argument("--top", type=int, default=14)
+    h = sub.add_parser("hits")
+    h.add_argument("pmc_dir")
+    h.add_argument("--kernel", default="k_attend")
+    h.add_argument("--skip", type=int, default=3)
     p = sub.add_parser("pmc")
     p.add_argument("fetch_dir")
     p.add_argument("write_dir")
@@ -112,6 +118,17 @@ def main():
         print("|---|---:|---:|---:|---:|")
         for name, n, avg, tot, st, ns in trace_table(a.trace_dir, a.skip)[:a.top]:
             print(f"| `{name}` | {n} | {avg:.2f} | {tot:.1f} | {st:.2f} ({ns}) |")
+        return
+
+    if a.mode == "hits":
+        hit = counter_values(a.pmc_dir, "TCC_HIT_sum")
+        miss = counter_values(a.pmc_dir, "TCC_MISS_sum")
+        k = [n for n in hit if short_name(n).startswith(a.kernel)][0]
+        hs, ms = hit[k][a.skip:], miss[k][a.skip:]
+        rate = sum(hs) / max(sum(hs) + sum(ms), 1.0)
+        print(f"| {a.kernel} | steady launches | TCC hits per launch | TCC misses per launch | hit rate |")
+        print("|---|---:|---:|---:|---:|")
+        print(f"| | {len(hs)} | {statistics.mean(hs):.4g} | {statistics.mean(ms):.4g} | {100 * rate:.1f} % |")
         return
 
     nbytes = a.copy_mib << 20
