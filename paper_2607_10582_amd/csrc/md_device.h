@@ -40,6 +40,44 @@ __device__ __forceinline__ int load_agent(const int32_t* p) {
 
 // Exclusive prefix of one int per thread across the whole block (any multiple
 // of 64 threads up to 1024).  lds needs 17 ints.  Contains __syncthreads.
+// N exclusive block-wide scans side by side, with one pair of barriers
+// (lds: 17 N ints).
+template <int N>
+__device__ inline void block_exclusive_scan_n(const int (&v)[N], int* lds, int (&ex)[N], int (&total)[N]) {
+    const int lane = lane_id(), wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    int incl[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) incl[k] = v[k];
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1)
+#pragma unroll
+        for (int k = 0; k < N; ++k) {
+            const int t = __shfl_up(incl[k], o);
+            if (lane >= o) incl[k] += t;
+        }
+    if (lane == 63)
+#pragma unroll
+        for (int k = 0; k < N; ++k) lds[17 * k + wid] = incl[k];
+    __syncthreads();
+    if ((int)threadIdx.x < N) {
+        int* l = lds + 17 * threadIdx.x;
+        int acc = 0;
+        for (int w = 0; w < nw; ++w) {
+            const int t = l[w];
+            l[w] = acc;
+            acc += t;
+        }
+        l[16] = acc;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        ex[k] = lds[17 * k + wid] + incl[k] - v[k];
+        total[k] = lds[17 * k + 16];
+    }
+    __syncthreads();
+}
+
 __device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
     const int lane = lane_id(), wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
     int incl = v;

@@ -31,7 +31,23 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                                                 int observe) {
     const int s = blockIdx.x;
     __shared__ int sh_phys, sh_slot, sh_last;
-    __shared__ int lds[17];
+    __shared__ int lds[5 * 17];
+    // The step's key rows (16 pieces of 16 bytes per (layer, KV head) row)
+    // do not depend on the slot: waves 1.. read their first kPre pieces now
+    // and write them once the slot is known, while wave 0 finds the slot
+    // (its loads are then not queued behind the copy's).
+    constexpr int kPre = 8;
+    const int n_pieces = new_k != nullptr ? dm.LHkv * 16 : 0;
+    const u32x4* src = new_k != nullptr ? reinterpret_cast<const u32x4*>(new_k) + (size_t)s * dm.LHkv * 16 : nullptr;
+    const int ct = (int)threadIdx.x - 64, nct = (int)blockDim.x - 64;   // copy threads
+    u32x4 kr[kPre];
+    if (ct >= 0) {
+#pragma unroll
+        for (int c = 0; c < kPre; ++c) {
+            const int i = ct + c * nct;
+            if (i < n_pieces) kr[c] = src[i];
+        }
+    }
     if (threadIdx.x == 0) {
         const int t = v.clock[s] + 1;
         v.clock[s] = t;
@@ -104,15 +120,21 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     __syncthreads();
     const int phys = sh_phys;
     if (phys >= 0) {
-        // L*Hkv rows of d bf16 = 16 pieces of 16 bytes per row; piece b of
-        // the token goes to its 16-token block's [b][slot mod 16] place.
+        // piece b of row r goes to its 16-token block's [b][slot mod 16] place
         const int slot = sh_slot;
-        const u32x4* src = reinterpret_cast<const u32x4*>(new_k + (size_t)s * dm.LHkv * kHeadDim);
-        for (int i = threadIdx.x; i < dm.LHkv * 16; i += blockDim.x) {
+        auto place = [&](int i) {
             const int r = i >> 4, part = i & 15;
             u32x4* blk = reinterpret_cast<u32x4*>(
                 v.k_pool + (((size_t)phys * dm.LHkv + r) * dm.P + (slot & ~15)) * kHeadDim);
-            blk[part * 16 + (slot & 15)] = src[i];
+            return blk + part * 16 + (slot & 15);
+        };
+        if (ct >= 0) {
+#pragma unroll
+            for (int c = 0; c < kPre; ++c) {
+                const int i = ct + c * nct;
+                if (i < n_pieces) *place(i) = kr[c];
+            }
+            for (int i = ct + kPre * nct; i < n_pieces; i += nct) *place(i) = src[i];
         }
     }
 
@@ -206,12 +228,11 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         my_tiles += ti[k];
         my_stiles += si[k];
     }
-    int tot_u, tot_i, tot_t, tot_s, tot_n;
-    int ex_u = block_exclusive_scan(my_units, lds, &tot_u);
-    int ex_i = block_exclusive_scan(my_items, lds, &tot_i);
-    int ex_t = block_exclusive_scan(my_tiles, lds, &tot_t);
-    int ex_s = block_exclusive_scan(my_stiles, lds, &tot_s);
-    block_exclusive_scan(my_tokens, lds, &tot_n);
+    const int mine[5] = {my_units, my_items, my_tiles, my_stiles, my_tokens};
+    int ex[5], tot[5];
+    block_exclusive_scan_n<5>(mine, lds, ex, tot);
+    int ex_u = ex[0], ex_i = ex[1], ex_t = ex[2], ex_s = ex[3];
+    const int tot_u = tot[0], tot_i = tot[1], tot_t = tot[2], tot_s = tot[3], tot_n = tot[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int s2 = threadIdx.x * 4 + k;
@@ -892,7 +913,7 @@ __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratc
                                                          const int32_t* __restrict__ ev_serial,
                                                          const int32_t* __restrict__ ev_count) {
     const int s = blockIdx.x;
-    __shared__ int lds[17];
+    __shared__ int lds[3 * 17];
     __shared__ int sh_base;
     const int tid = threadIdx.x;
     const int cnt = ev_count[s];
@@ -927,10 +948,13 @@ __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratc
         }
     }
     int kept_total, gone_total;
-    int kpos = block_exclusive_scan(n_keep, lds, &kept_total);
-    int gpos = block_exclusive_scan(n_gone, lds, &gone_total);
-    int live_gone_total;
-    block_exclusive_scan(live_gone, lds, &live_gone_total);
+    const int mine[3] = {n_keep, n_gone, live_gone};
+    int ex[3], tot[3];
+    block_exclusive_scan_n<3>(mine, lds, ex, tot);
+    int kpos = ex[0], gpos = ex[1];
+    kept_total = tot[0];
+    gone_total = tot[1];
+    const int live_gone_total = tot[2];
     if (tid == 0) {
         if (gone_total != cnt) atomicOr(sc.status, MD_DEV_BAD_EVICT);
         sh_base = gone_total > 0 ? atomicAdd(v.free_count, gone_total) : 0;
