@@ -88,10 +88,11 @@ def setup(w, steps_total, dev, fused=None):
     cache.set_free_pages(perm[pos:][::-1])
     md = MemDecay(cache, torch.from_numpy(b), torch.from_numpy(lam), rho=w.rho, alpha=w.alpha,
                   tau_scale=w.tau_scale, pinned_mask=w.pinned_mask, fused=fused,
-                  region_aligned=w.region_aligned, quant_threshold=w.quant_threshold)
+                  region_aligned=w.region_aligned, quant_threshold=w.quant_threshold,
+                  attention_norm=w.attention_norm, window=w.window)
     inputs = []
     for k in range(1, steps_total + 1):
-        q = g.torch_queries(w, k, dev)
+        q = g.torch_window_queries(w, k, dev)
         nk = g.torch_append_keys(w, k, dev)
         reg = torch.full((w.S,), g.append_region(w, k), dtype=torch.uint8, device=dev)
         inputs.append((q, nk, reg))
@@ -121,25 +122,34 @@ def cpu_baseline(w, n0s, B, budget_s: float, max_steps: int):
     del kb
 
     def inputs(k):
-        q = g.torch_queries(w, k, dev)[0].cpu().numpy()
+        qt = g.torch_window_queries(w, k, dev)
+        q = None if qt is None else qt[0].cpu().numpy()
         nk = g.torch_append_keys(w, k, dev)[0].view(torch.int16).cpu().numpy().view(np.uint16)
         return q, nk, g.append_region(w, k)
 
-    sess.step(*inputs(1))
+    # untimed up to the first observation (the bulk eviction)
+    k = 1
+    while True:
+        q, nk, r = inputs(k)
+        sess.step(q, nk, r)
+        k += 1
+        if q is not None:
+            break
+    k0 = k
     scored = 0
     steps = 0
     elapsed = 0.0
-    k = 2
     while elapsed < budget_s and k <= max_steps:
         q, nk, r = inputs(k)
         t0 = time.perf_counter()
         rec = sess.step(q, nk, r)
         elapsed += time.perf_counter() - t0
-        scored += rec.n
+        if q is not None:     # only observation steps score tokens
+            scored += rec.n
         steps += 1
         k += 1
     return {"value": scored / elapsed, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"session 0 of {w.S} ({w.name}), {steps} steady decode steps (steps 2-{k - 1}, "
+            "sample": f"session 0 of {w.S} ({w.name}), {steps} steady decode steps (steps {k0}-{k - 1}, "
                       f"after the bulk eviction), {scored} token-steps in {elapsed:.1f} s, numpy float64",
             "seconds_per_step": elapsed / max(steps, 1)}
 
@@ -155,6 +165,19 @@ def load_traffic(kernel: str, workload: str):
     if d.get("kernel_source_sha256_16") != kernel_source_hash(kernel):
         return None, "stale"
     return d.get("hbm_bytes_per_launch"), path
+
+
+def quantised_tokens(cache) -> int:
+    """Tokens held in quantised pages now (such pages are never a session's
+    last page, so each holds P slots)."""
+    import torch
+    npg = cache.n_pages.cpu().numpy()
+    fmt = cache.page_format.cpu().numpy()
+    tot = 0
+    for s in range(cache.S):
+        ids = cache.page_table[s, :int(npg[s])].cpu().numpy()
+        tot += int(fmt[ids].sum()) * cache.P
+    return tot
 
 
 def calibrate_copy(mib: int):
@@ -182,6 +205,8 @@ def main():
                          "letting the library pick")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
+    ap.add_argument("--quant-threshold", type=float, default=None,
+                    help="quantised tier: override the workload's threshold (0: off)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -196,11 +221,14 @@ def main():
     import torch
     from paper_2607_10582_amd import binding
     from synth import configs as C
+    from synth import generator as g
 
     binding.load_library()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = C.get(args.workload)
+    if args.quant_threshold is not None:
+        w = C.with_overrides(w, quant_threshold=args.quant_threshold)
     W, K = args.warmup, args.steps
     if W + K > w.steps:
         log(f"note: {W + K} steps asked, the workload defines {w.steps} decode steps")
@@ -211,16 +239,19 @@ def main():
     # warm-up; the first step (the bulk eviction down to the budget) is
     # timed on its own with an event pair on the library's stream
     first_ms = None
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    first_obs = None
     for k in range(1, W + 1):
         q, nk, reg = inputs[k - 1]
-        if k == 1:
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        timed = first_obs is None and q is not None
+        if timed:
+            first_obs = k
             e0.record(md.stream)
         md.step(k, q, nk, reg, page_scores=False)
-        if k == 1:
+        if timed:
             e1.record(md.stream)
     torch.cuda.synchronize(dev)
-    if W >= 1:
+    if first_obs is not None:
         first_ms = e0.elapsed_time(e1)
     c0 = md.counters()
     kcfg = md.kernel_config()
@@ -231,6 +262,7 @@ def main():
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     step_ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    q_tok0 = quantised_tokens(cache) if w.quant_threshold > 0 else 0
     torch.cuda.synchronize(dev)
     t0 = time.perf_counter()
     ev0.record(stream)
@@ -253,25 +285,33 @@ def main():
         sys.exit(1)
 
     scored = c1[0] - c0[0]
+    # quantised tier: tokens in quantised pages per step, the mean of the
+    # counts before and after the timed steps (the set changes slowly); their
+    # keys take d + 1 bytes per (layer, KV head) row instead of 2 d (codes,
+    # and a 16-byte scale line per 16 tokens)
+    q_tok = (q_tok0 + quantised_tokens(cache)) / 2 if w.quant_threshold > 0 else 0
+    q_saved = K * q_tok * (w.k_bytes_per_token - w.L * w.Hkv * (w.d + 1))
     evicted_tokens = c1[3] - c0[3]
     evicted_pages = c1[2] - c0[2]
     kb = w.k_bytes_per_token
-    q_bytes = w.S * w.L * w.Hq * w.d * 4
+    # the queries of the observation steps: W per session and step
+    n_obs = sum(1 for k in range(W + 1, W + K + 1) if g.observes(w, k))
+    q_bytes = w.S * w.L * w.Hq * w.d * 4 * w.window * n_obs / K
     # algorithmic bytes over the timed launches: every cached key once and the
     # queries once; the fused kernel also reads and writes each token's
     # importance (Eq. 2), reads its refresh clock and region (Eq. 3, Eq. 4),
     # and reads each page's table entry and writes its score (Eq. 5)
     if hot == "attend":
-        hot_bytes = scored * (kb + 13) + (scored // w.P) * 8 + K * q_bytes
+        hot_bytes = scored * (kb + 13) + (scored // w.P) * 8 + K * q_bytes - q_saved
     else:
-        hot_bytes = scored * kb + K * q_bytes
+        hot_bytes = scored * kb + K * q_bytes - q_saved
     avg_launch_s = hot_ms / 1e3 / max(launches, 1)
     per_launch_bytes = hot_bytes / max(launches, 1)
     achieved = per_launch_bytes / avg_launch_s / 1e9
     traffic, traffic_src = load_traffic(hot, w.name)
     # whole step: K + per-token state (region 1, a 4+4, t_ref 4+4) + per-page
     # score and page-table entry + the queries
-    step_bytes = scored * (kb + 17) + scored // w.P * 8 + K * q_bytes
+    step_bytes = scored * (kb + 17) + scored // w.P * 8 + K * q_bytes - q_saved
 
     line = {
         "metric": METRIC,
@@ -296,6 +336,7 @@ def main():
                      "avg_launch_us": avg_launch_s * 1e6,
                      "algorithmic_bytes_per_launch": per_launch_bytes},
         "tokens_scored_per_step": scored / K,
+        "quantised_tokens_per_step": q_tok,
         "tokens_evicted_per_step": evicted_tokens / K,
         "pages_evicted": evicted_pages,
         "gpu_event_ms_per_step": gpu_ms / K,

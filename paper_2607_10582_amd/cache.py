@@ -210,6 +210,8 @@ class MemDecay:
         """One decode step; page_scores=False leaves self.page_score untouched
         (the library still scores every page for its own selection)."""
         self.observe(step, q, new_k, new_region)
+        if q is None:   # a decode step without an observation only appends
+            return
         self.score(page_score=page_scores)
         self.select()
         self.compact()

@@ -116,6 +116,12 @@ WORKLOADS = {
                               n0_range=None, system_len=60, mean_span=40.0,
                               budget_frac=0.5, steps=32, append_cycle=APPEND_CYCLE,
                               region_aligned=True, append_run=5),
+    # the 32k batch observed every other decode step with a window of the
+    # two latest queries (the multi-kernel path)
+    "long32k_w2k2": Workload("long32k_w2k2", 3, **QWEN15, P=16, S=16, n0=32768,
+                             n0_range=None, system_len=1024, mean_span=512.0,
+                             budget_frac=0.25, steps=128, append_cycle=APPEND_CYCLE,
+                             window=2, obs_interval=2),
     "long32k_aligned": Workload("long32k_aligned", 3, **QWEN15, P=16, S=16, n0=32768,
                                 n0_range=None, system_len=1024, mean_span=512.0,
                                 budget_frac=0.25, steps=128, append_cycle=APPEND_CYCLE,

@@ -200,6 +200,19 @@ def torch_queries(w: Workload, step: int, device):
     return torch.randn((w.S, w.L, w.Hq, w.d), generator=g, device=device, dtype=torch.float32)
 
 
+def torch_window_queries(w: Workload, step: int, device):
+    """The decode queries of an observation step, drawn on ``device``:
+    [S][L][Hq][d] for W = 1, else [S][W][L][Hq][d] for steps step - W + 1 ..
+    step, oldest first; None for a step without an observation."""
+    import torch
+    if not observes(w, step):
+        return None
+    if w.window == 1:
+        return torch_queries(w, step, device)
+    return torch.stack([torch_queries(w, step - w.window + 1 + j, device) for j in range(w.window)],
+                       dim=1).contiguous()
+
+
 def torch_append_keys(w: Workload, step: int, device):
     """bf16 tensor [S][L][Hkv][d] drawn on ``device`` for one step."""
     import torch
