@@ -205,6 +205,9 @@ def main():
                          "letting the library pick")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
+    ap.add_argument("--calibrate", type=int, default=0, metavar="BUCKET_STEPS",
+                    help="also accumulate the region-lifetime statistics (Sec. IV-B) at every "
+                         "observation, in age buckets of this many steps, and time it")
     ap.add_argument("--quant-threshold", type=float, default=None,
                     help="quantised tier: override the workload's threshold (0: off)")
     args = ap.parse_args()
@@ -266,10 +269,27 @@ def main():
     torch.cuda.synchronize(dev)
     t0 = time.perf_counter()
     ev0.record(stream)
+    if args.calibrate:
+        n_buckets = 64
+        abar = torch.zeros(cache.n_phys * w.P, dtype=torch.float32, device=dev)
+        stats = [torch.zeros((w.S, 7, n_buckets), dtype=torch.int64, device=dev) for _ in range(3)]
+        cal_ev = []
     for i, k in enumerate(range(W + 1, W + K + 1)):
         q, nk, reg = inputs[k - 1]
         step_ev[i].record(stream)
-        md.step(k, q, nk, reg, page_scores=False)
+        if args.calibrate and q is not None:
+            # a calibration pass: the step's masses go to the lifetime bins
+            md.observe(k, q, nk, reg, abar_out=abar)
+            ce = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            ce[0].record(stream)
+            md.calib_accumulate(abar, args.calibrate, stats)
+            ce[1].record(stream)
+            cal_ev.append(ce)
+            md.score(page_score=False)
+            md.select()
+            md.compact()
+        else:
+            md.step(k, q, nk, reg, page_scores=False)
     step_ev[K].record(stream)
     ev1.record(stream)
     torch.cuda.synchronize(dev)
@@ -342,6 +362,8 @@ def main():
         "gpu_event_ms_per_step": gpu_ms / K,
         "step_ms_median": per_step[K // 2],
         "first_step_ms": first_ms,
+        "calib_us_per_observation": (sum(a.elapsed_time(b) for a, b in cal_ev) * 1e3 / len(cal_ev)
+                                     if args.calibrate and cal_ev else None),
         "step_algorithmic_gbs": step_bytes / wall / 1e9,
         "step_frac_of_peak": step_bytes / wall / 1e9 / PEAK_HBM_GBS,
     }
