@@ -119,7 +119,10 @@ static md_status validate_config(const md_config* c) {
     if (!(c->tau_scale >= 0.0f) || !isfinite(c->tau_scale)) return MD_E_INVALID;
     if (c->window < 1) return MD_E_INVALID;
     if (!(c->quant_threshold >= 0.0f)) return MD_E_INVALID;   // NaN too
-    if ((c->flags & MD_FLAG_FUSED) && c->window > 1) return MD_E_UNSUPPORTED;
+    // the fused kernel takes a window only on plain pages in full precision
+    if ((c->flags & MD_FLAG_FUSED) && c->window > 1 &&
+        ((c->flags & MD_FLAG_REGION_ALIGNED) || c->quant_threshold > 0.0f))
+        return MD_E_UNSUPPORTED;
     if (c->head_dim != md::kHeadDim) return MD_E_UNSUPPORTED;
     if ((int64_t)(c->n_q_heads / c->n_kv_heads) * c->window > 16) return MD_E_UNSUPPORTED;
     if ((int64_t)c->n_layers * c->n_q_heads * c->window > md::kMaxRows) return MD_E_UNSUPPORTED;
@@ -183,7 +186,8 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     dm.rho = cfg->rho;
     dm.alpha = cfg->alpha;
     dm.tau_scale = cfg->tau_scale;
-    dm.fused = ((cfg->flags & MD_FLAG_NO_FUSED) || dm.W > 1) ? 0 : 1;
+    dm.fused = ((cfg->flags & MD_FLAG_NO_FUSED) ||
+                (dm.W > 1 && ((cfg->flags & MD_FLAG_REGION_ALIGNED) || cfg->quant_threshold > 0.0f))) ? 0 : 1;
     dm.norm_attn = (cfg->flags & MD_FLAG_NORM_ATTENTION) ? 1 : 0;
     dm.aligned = (cfg->flags & MD_FLAG_REGION_ALIGNED) ? 1 : 0;
     dm.quant = cfg->quant_threshold > 0.0f ? 1 : 0;
@@ -214,13 +218,13 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     int occ = 0;
     dm.T = md::attend_unit_tokens(dm.G);
     if (dm.fused) {
-        const size_t lds = md::attend_lds_bytes(dm.G);
-        if (hipFuncSetAttribute(md::attend_kernel(dm.G, dm.aligned, dm.quant), hipFuncAttributeMaxDynamicSharedMemorySize,
+        const size_t lds = md::attend_lds_bytes(dm.G * dm.W);
+        if (hipFuncSetAttribute(md::attend_kernel(dm.G * dm.W, dm.aligned, dm.quant, dm.W), hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)lds) !=
             hipSuccess) {
             (void)hipGetLastError();
-        } else if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(dm.G, dm.aligned, dm.quant),
-                                                                md::attend_threads(dm.G),
+        } else if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(dm.G * dm.W, dm.aligned, dm.quant, dm.W),
+                                                                md::attend_threads(dm.G * dm.W),
                                                                 lds) != hipSuccess) {
             return MD_E_HIP;
         }

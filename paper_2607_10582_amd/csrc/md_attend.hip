@@ -53,6 +53,8 @@ struct AttendDims {
     uint32_t pin_mask;
     float rho, tau_scale, alpha;
     int aligned;
+    int Gq, Wn;   // window (WN instantiations): query heads per KV head and window
+                  // queries; G above counts the MFMA columns, Gq * Wn
 };
 
 struct AttendArgs {
@@ -79,6 +81,7 @@ struct AttendArgs {
     int32_t* probe;    // check mode only: [arrivals, least seen]
     const int32_t* n_live;   // tokens |K_t| (the n_tokens array unless pages are region-aligned)
     const uint8_t* page_format;   // quantised tier: 1 = the page holds E4M3 codes
+    const int32_t* t_ins;         // window: insertion steps, for the causal mask
 };
 
 // LDS row stride (floats) of a head's values: W waves of KT tiles
@@ -176,9 +179,11 @@ __device__ __forceinline__ int qrow0(const AttendDims& dm, int r) { return r * d
 // One wave's part of a unit.  W = waves per workgroup, NH = normaliser
 // heads per wave (G <= W NH), KT = tiles per wave (units of 16 W KT tokens),
 // AL = region-aligned pages (hole slots are masked), QT = quantised tier
-// (tiles of quantised pages hold 8-bit codes); separate instantiations keep
-// the plain kernel's register budget.
-template <int W, int NH, int KT, bool AL, bool QT>
+// (tiles of quantised pages hold 8-bit codes), WN = a window of several
+// decode queries (column c of a row is window query c / Gq, head c % Gq, and
+// a causal mask keeps each query to the tokens inserted by its step);
+// separate instantiations keep the plain kernel's register budget.
+template <int W, int NH, int KT, bool AL, bool QT, bool WN>
 __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendArgs& a, const Lds& sm,
                                             const Unit& un, int wv, int lane, uint32_t tag) {
     constexpr int KQ = (W * NH * 32 + 64 * W - 1) / (64 * W);   // float4 of the query row per lane
@@ -226,7 +231,23 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
 #pragma unroll
         for (int u = 0; u < KT; ++u) lims |= (uint32_t)__builtin_amdgcn_readlane(mylim, u) << (8 * u);
     }
-    const bool wave_full = (vmask & kAll) == kAll && wtok0 + 16 * KT <= un.ntok && (!AL || lims == 0x10101010u);
+    // Window: bit 4u + i marks this lane's logit column (window query
+    // h / Gq) of tile u, token 4g + i, as inserted after that query's step.
+    uint32_t unseen = 0;
+    if constexpr (WN) {
+        const int t_lim = a.clock[un.s] - (dm.Wn - 1 - min(h / dm.Gq, dm.Wn - 1));
+#pragma unroll
+        for (int u = 0; u < KT; ++u) {
+            const int slot = __builtin_amdgcn_readlane(myslot, u);
+            if ((vmask >> u) & 1ull) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    unseen |= (a.t_ins[slot + 4 * g + i] > t_lim) ? 1u << (4 * u + i) : 0u;
+            }
+        }
+    }
+    const bool wave_full = (vmask & kAll) == kAll && wtok0 + 16 * KT <= un.ntok && (!AL || lims == 0x10101010u) &&
+                           (!WN || !__any(unseen != 0));
     // Quantised tier: bit u of qmask marks tile u as 8-bit codes (its page's
     // format); wave-uniform.
     uint32_t qmask = 0;
@@ -267,9 +288,21 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         return reinterpret_cast<const f32x4*>(a.q + ((size_t)un.s * dm.L * dm.Hq + qrow0(dm, r)) * kHeadDim);
     };
     auto load_q = [&](int r) {   // unconditional loads, indices clamped into the row
-        const f32x4* qr = q_row(r);
+        if constexpr (WN) {
+            // queries [S][Wn][L][Hq][d]: column c is query c / Gq, head c % Gq
+            const int l = r / dm.Hkv, kv = r - l * dm.Hkv;
 #pragma unroll
-        for (int k = 0; k < KQ; ++k) qv[k] = qr[min(lane + 64 * (wv + W * k), G * 32 - 1)];
+            for (int k = 0; k < KQ; ++k) {
+                const int f = min(lane + 64 * (wv + W * k), G * 32 - 1);
+                const int c = f >> 5, w = c / dm.Gq, hd = c - w * dm.Gq;
+                qv[k] = reinterpret_cast<const f32x4*>(
+                    a.q + ((((size_t)un.s * dm.Wn + w) * dm.L + l) * dm.Hq + kv * dm.Gq + hd) * kHeadDim)[f & 31];
+            }
+        } else {
+            const f32x4* qr = q_row(r);
+#pragma unroll
+            for (int k = 0; k < KQ; ++k) qv[k] = qr[min(lane + 64 * (wv + W * k), G * 32 - 1)];
+        }
     };
     auto store_q = [&](int r) {
         uint32_t* qb = sm.qs + (size_t)(r & 1) * 3 * G * 64;
@@ -572,7 +605,8 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
                     if (!((vmask >> u) & 1ull) || wtok0 + 16 * u + 4 * g + i >= un.ntok ||
-                        (AL && 4 * g + i >= (int)((lims >> (8 * u)) & 0xffu)))
+                        (AL && 4 * g + i >= (int)((lims >> (8 * u)) & 0xffu)) ||
+                        (WN && ((unseen >> (4 * u + i)) & 1u)))
                         xs[u][i] = -INFINITY;
         }
         float mx = -INFINITY;
@@ -744,7 +778,7 @@ __device__ void claim_sessions(const AttendArgs& a, int* xs, int lane_no, int ca
 // the whole register file.  (Workgroups that take a whole CU, with eight
 // waves or with eight tiles per wave, measured slower: the two workgroups'
 // row barriers fall at different times and fill each other's gaps.)
-template <int W, int NH, int KT, bool AL, bool QT>
+template <int W, int NH, int KT, bool AL, bool QT, bool WN>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(NH == 4 ? 1 : 2)))
 k_attend(AttendDims dm, AttendArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -837,7 +871,7 @@ k_attend(AttendDims dm, AttendArgs a) {
         // arithmetic is not hoisted out of the pass loop and kept live.
         int lane = (int)threadIdx.x & 63;
         asm volatile("" : "+v"(lane));
-        attend_wave<W, NH, KT, AL, QT>(dm, a, sm, un, wv, lane, tag);
+        attend_wave<W, NH, KT, AL, QT, WN>(dm, a, sm, un, wv, lane, tag);
     }
 }
 
@@ -849,30 +883,34 @@ size_t attend_lds_bytes(int G) {
 }
 
 namespace {
-template <bool AL, bool QT>
+template <bool AL, bool QT, bool WN>
 const void* attend_for(int G) {
-    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<4, 1, 4, AL, QT>);
-    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<4, 2, 4, AL, QT>);
-    return reinterpret_cast<const void*>(&k_attend<4, 4, 4, AL, QT>);
+    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<4, 1, 4, AL, QT, WN>);
+    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<4, 2, 4, AL, QT, WN>);
+    return reinterpret_cast<const void*>(&k_attend<4, 4, 4, AL, QT, WN>);
 }
 }  // namespace
 
-const void* attend_kernel(int G, int aligned, int quant) {
-    if (aligned) return quant ? attend_for<true, true>(G) : attend_for<true, false>(G);
-    return quant ? attend_for<false, true>(G) : attend_for<false, false>(G);
+// G: MFMA columns (query heads per KV head times window queries).  The
+// window runs only on plain pages in full precision.
+const void* attend_kernel(int G, int aligned, int quant, int window) {
+    if (window > 1) return attend_for<false, false, true>(G);
+    if (aligned) return quant ? attend_for<true, true, false>(G) : attend_for<true, false, false>(G);
+    return quant ? attend_for<false, true, false>(G) : attend_for<false, false, false>(G);
 }
 
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q, float* abar_out,
                          hipStream_t st) {
-    AttendDims ad{dm.L, dm.Hq, dm.Hkv, dm.G, dm.P, dm.Pshift, dm.MP, dm.NP, dm.R, dm.LHkv,
+    AttendDims ad{dm.L, dm.Hq, dm.Hkv, dm.G * dm.W, dm.P, dm.Pshift, dm.MP, dm.NP, dm.R, dm.LHkv,
                   dm.wg_per_cu, dm.n_wg / dm.wg_per_cu, dm.S, dm.n_regions, dm.norm_attn, dm.pin_mask,
-                  dm.rho, dm.tau_scale, dm.alpha, dm.aligned};
+                  dm.rho, dm.tau_scale, dm.alpha, dm.aligned, dm.G, dm.W};
     AttendArgs aa{v.k_pool, v.page_table, v.n_tokens, v.clock, v.region, v.b, v.lam, v.imp, v.t_ref,
                   sc.pscore, q, abar_out, sc.ustart, sc.plan, sc.epoch, sc.claim, sc.lane_box, sc.ustat,
-                  sc.unorm, sc.status, nullptr, v.n_live, v.page_format};
+                  sc.unorm, sc.status, nullptr, v.n_live, v.page_format, v.t_ins};
     void* args[] = {&ad, &aa};
-    return hipLaunchCooperativeKernel(attend_kernel(dm.G, dm.aligned, dm.quant), dim3(dm.n_wg), dim3(attend_threads(dm.G)), args,
-                                      (unsigned)attend_lds_bytes(dm.G), st);
+    return hipLaunchCooperativeKernel(attend_kernel(dm.G * dm.W, dm.aligned, dm.quant, dm.W), dim3(dm.n_wg),
+                                      dim3(attend_threads(dm.G * dm.W)), args,
+                                      (unsigned)attend_lds_bytes(dm.G * dm.W), st);
 }
 
 hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, hipStream_t st) {
@@ -883,8 +921,9 @@ hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, hipStre
     if (e == hipSuccess) e = hipMemsetD32Async(reinterpret_cast<hipDeviceptr_t>(probe + 1), 1 << 30, 1, st);
     if (e != hipSuccess) return e;
     void* args[] = {&ad, &aa};
-    return hipLaunchCooperativeKernel(attend_kernel(dm.G, dm.aligned, dm.quant), dim3(n_wg), dim3(attend_threads(dm.G)), args,
-                                      (unsigned)attend_lds_bytes(dm.G), st);
+    return hipLaunchCooperativeKernel(attend_kernel(dm.G * dm.W, dm.aligned, dm.quant, dm.W), dim3(n_wg),
+                                      dim3(attend_threads(dm.G * dm.W)), args,
+                                      (unsigned)attend_lds_bytes(dm.G * dm.W), st);
 }
 
 }  // namespace md

@@ -107,7 +107,8 @@ hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st);
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q,
                          float* abar_out, hipStream_t st);
 size_t attend_lds_bytes(int G);
-const void* attend_kernel(int G, int aligned, int quant);   // the instantiation for G, layout, tier
+// the instantiation for G MFMA columns (heads per KV head x window), layout, tier, window
+const void* attend_kernel(int G, int aligned, int quant, int window);
 // Launch the fused kernel in check mode with n_wg workgroups: every wave
 // waits (bounded, ~20 ms) until all workgroups have arrived; probe[1]
 // receives the fewest arrivals any workgroup saw (probe: 2 device ints).

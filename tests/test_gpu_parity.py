@@ -285,29 +285,40 @@ def test_normalised_attention_term_batch():
     run_pair(Pair(w, steps=10), 10, "norm-attention-qwen3x8")
 
 
+@pytest.mark.parametrize("fused", [True, False])
 @pytest.mark.parametrize("shape,W,k", [("g6", 2, 2), ("g4", 4, 4), ("g6", 1, 3), ("g6p64", 2, 3)])
-def test_window_and_observation_interval(shape, W, k):
+def test_window_and_observation_interval(shape, W, k, fused):
     # Attention sampled every k-th decode step with a window of the W latest
-    # decode queries (Sec. III-C); the steps in between only append.  W > 1
-    # runs on the multi-kernel path, whose causal mask keeps each window
-    # query to the tokens of its own step.
+    # decode queries (Sec. III-C); the steps in between only append.  A
+    # causal mask keeps each window query to the tokens of its own step; on
+    # the fused kernel the window's queries are extra MFMA columns.
     base = C.get("small")
     if shape == "g4":
         base = C.with_overrides(base, L=2, Hq=8, Hkv=2)
     if shape == "g6p64":
         base = C.with_overrides(base, L=2, P=64, n0=700, budget_frac=0.3)
     w = C.with_overrides(base, window=W, obs_interval=k, steps=24)
-    p = Pair(w, fused=None if W > 1 else True, planted=24, planted_strength=2.5, query_gain=0.7)
-    assert p.md.kernel_config()["steady_fused"] == (W == 1)
-    st = run_pair(p, 24, f"window{W}-every{k}-{shape}")
+    p = Pair(w, fused=fused, planted=24, planted_strength=2.5, query_gain=0.7)
+    assert p.md.kernel_config()["steady_fused"] == fused
+    st = run_pair(p, 24, f"window{W}-every{k}-{shape}-fused{int(fused)}")
     assert st.evicted_pages > 5
 
 
-def test_window_on_a_batch_with_empty_and_short_sessions():
+@pytest.mark.parametrize("fused", [True, False])
+def test_window_on_a_batch_with_empty_and_short_sessions(fused):
     w = C.with_overrides(C.get("small"), L=3, Hq=4, Hkv=2, S=5, n0=None, n0_range=(1, 2),
                          window=3, obs_interval=3, steps=30, system_len=20)
-    p = Pair(w, n0s=[0, 1, 17, 130, 700], budgets=[0, 5, 10, 100, 200], fused=None)
-    run_pair(p, 30, "window3-edges")
+    p = Pair(w, n0s=[0, 1, 17, 130, 700], budgets=[0, 5, 10, 100, 200], fused=fused)
+    run_pair(p, 30, f"window3-edges-fused{int(fused)}")
+
+
+def test_window_long32k_sampled_sessions():
+    # the 32k batch observed every other step with a window of two, on the
+    # fused kernel (G W = 12 columns)
+    w = C.get("long32k_w2k2")
+    p = Pair(w, backend="torch", oracle_sessions=[0, 11], steps=6, fused=True)
+    assert p.md.kernel_config()["steady_fused"]
+    run_pair(p, 6, "window2-long32k-fused")
 
 
 @pytest.mark.parametrize("aligned", [False, True])
