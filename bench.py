@@ -214,7 +214,7 @@ def main():
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the retention path shards over sessions with no "
-              f"exchange, and this build measures the one-GPU share (asked for --gpus {args.gpus}).",
+              f"exchange, and the benchmark measures one GPU's share (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
     if args.calibrate_copy:

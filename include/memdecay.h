@@ -195,7 +195,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp,
 
 /*
  * md_observe_step — one decode step; with q given, also an observation step
- * (Alg. 1, first two lines; attention is sampled every k-th decode step with
+ * (Alg. 1's importance and refresh updates; attention is sampled every k-th decode step with
  * a window of the W latest decode queries, Sec. III-C):
  *   append: each session's clock advances, t <- t + 1.  If new_k is not NULL
  *     the step's token joins the session's last page, or a page popped from
@@ -231,7 +231,7 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q,
                           float* abar_out);
 
 /*
- * md_score_pages — retention scores and page scores (Alg. 1, lines 3-4):
+ * md_score_pages — retention scores and page scores (Alg. 1's scoring steps):
  *   s_i = b_{r(i)} exp(-lambda_{r(i)} (t - t_ref_i)) + alpha a_i    (Eq. 4)
  *   S_p = (1/|p|) sum_{i in p} s_i over the page's live tokens      (Eq. 5)
  * Pinned tokens bypass scoring (+INFINITY); a page with any pinned member
@@ -246,7 +246,7 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q,
 md_status md_score_pages(md_handle h, float* page_score, float* token_score);
 
 /*
- * md_select_evict — budget-aware page eviction (Alg. 1, lines 5-8): when a
+ * md_select_evict — budget-aware page eviction (Alg. 1's eviction loop): when a
  * session holds n > B tokens (B = budget[s]; a page counts its tokens, not
  * its holes), the shortest prefix of its
  * non-pinned pages in ascending (S_p, serial) order whose removal leaves

@@ -9,7 +9,7 @@ the log-linear decay of Eq. 6 by count-weighted least squares:
 
     log A_r(dt) ~= log c_r - lambda_r dt,        half-life ln 2 / lambda_r (Eq. 7)
 
-Readings (listed in the design notes): a token's age is the decode steps
+Readings where the paper leaves a choice: a token's age is the decode steps
 since its insertion, t - t_ins; ages are grouped into buckets of
 ``bucket_steps`` steps and ages past the last bucket are left out; a
 bucket's abscissa is the mean age of its observations and its ordinate the

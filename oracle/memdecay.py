@@ -24,8 +24,7 @@ steps in the paper's order:
            the budget holds                                 (Sec. III-D, Alg. 1)
   O9       drop the evicted pages
 
-Readings where the paper leaves a choice (listed with their reasons in the
-design notes of the repository):
+Readings where the paper leaves a choice:
   * observation steps and window (Sec. III-C): the caller decides which
     decode steps observe (every k-th one in the workloads; k = 1 is the
     study's setting); a step without an observation only appends.  At an
