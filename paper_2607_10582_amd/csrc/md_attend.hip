@@ -812,7 +812,9 @@ k_attend(AttendDims dm, AttendArgs a) {
     // workgroup per CU; a lane runs passes of whole sessions that it claims
     // itself, lane 0 from the front of the session list and lane 1 from the
     // back, so the units of one session always share a lane and start
-    // together, and the faster lane takes more sessions.
+    // together, and the faster lane takes more sessions.  The first pass of
+    // each lane is claimed and published before the kernel starts (by the
+    // append kernel), so no workgroup waits to begin.
     const int lane_no = lanes ? (int)blockIdx.x / dm.n_cu : 0;
     const int w = lanes ? (int)blockIdx.x % dm.n_cu : (int)blockIdx.x;
     const int cap = lanes ? dm.n_cu : 0;
@@ -824,10 +826,10 @@ k_attend(AttendDims dm, AttendArgs a) {
             sb = a.plan[2 + 3 * ps];
             se = a.plan[3 + 3 * ps];
         } else {
-            if (w == 0) claim_sessions(a, xs, lane_no, cap);
+            if (w == 0 && ps > 0) claim_sessions(a, xs, lane_no, cap);
             if (threadIdx.x == 0) {
                 unsigned long long* box = a.lane_box + (size_t)lane_no * (dm.S + 1) + ps;
-                if (w == 0) {
+                if (w == 0 && ps > 0) {
                     __hip_atomic_store(box, ((unsigned long long)tag << 32) | ((uint32_t)xs[0] << 16) | (uint32_t)xs[1],
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 } else {

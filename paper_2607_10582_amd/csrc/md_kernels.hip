@@ -170,9 +170,23 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     }
     __syncthreads();
     if (threadIdx.x == 0 && fused && s_lane_ok) {
+        // The first pass of each lane, claimed here: lane 0 the longest
+        // prefix of sessions, lane 1 the longest suffix of the rest, each
+        // within one workgroup per CU and at most blockDim.x sessions (what
+        // the kernel's own claims take); the rest stays to be claimed.
         sc.plan[0] = -1;
-        *sc.claim = (unsigned long long)dm.S;   // first 0, end S
-        *sc.epoch += 1;
+        const int ep = *sc.epoch + 1;
+        *sc.epoch = ep;
+        auto units = [&](int s2) { return (s_n[s2] + dm.T - 1) / dm.T; };
+        int f0 = 0, used = 0;
+        while (f0 < dm.S && f0 < (int)blockDim.x && used + units(f0) <= dm.lane_cap) used += units(f0++);
+        int e1 = dm.S;
+        used = 0;
+        while (e1 > f0 && dm.S - e1 < (int)blockDim.x && used + units(e1 - 1) <= dm.lane_cap) used += units(--e1);
+        const unsigned long long tag = (unsigned long long)(uint32_t)ep << 32;
+        sc.lane_box[0] = tag | ((unsigned long long)0 << 16) | (unsigned long long)f0;
+        sc.lane_box[dm.S + 1] = tag | ((unsigned long long)e1 << 16) | (unsigned long long)dm.S;
+        *sc.claim = ((unsigned long long)(uint32_t)f0 << 32) | (uint32_t)e1;
     } else if (threadIdx.x == 0 && fused) {
         // Sessions in order, packed greedily into passes of at most n_wg
         // units (a session's units wait for each other row by row, so all of
