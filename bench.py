@@ -328,7 +328,11 @@ def main():
     avg_launch_s = hot_ms / 1e3 / max(launches, 1)
     per_launch_bytes = hot_bytes / max(launches, 1)
     achieved = per_launch_bytes / avg_launch_s / 1e9
-    traffic, traffic_src = load_traffic(hot, w.name)
+    # the counters were taken on the workload as named: a quantised tier
+    # switched on from the command line reads other bytes (its own profile
+    # name carries the threshold)
+    prof_name = w.name if w.quant_threshold == C.get(w.name).quant_threshold else f"{w.name}_quant{w.quant_threshold:g}"
+    traffic, traffic_src = load_traffic(hot, prof_name)
     # whole step: K + per-token state (region 1, a 4+4, t_ref 4+4) + per-page
     # score and page-table entry + the queries
     step_bytes = scored * (kb + 17) + scored // w.P * 8 + K * q_bytes - q_saved
