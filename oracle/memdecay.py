@@ -53,7 +53,10 @@ Readings where the paper leaves a choice:
   * optional region-aligned pages (the allocator variant Sec. III-D leaves
     to future work): a page holds tokens of one region only.  An appended
     token opens a fresh page when the last page is full or its last token's
-    region differs; a prompt is laid out the same way, token by token.  The
+    region differs; a prompt is laid out the same way, token by token.  A
+    page left at a region boundary is closed for good: it takes no later
+    token, also when the pages after it are evicted and it becomes the last
+    page again (its unused places were given up when it was closed).  The
     rest of the method is unchanged: page sizes simply vary more, and Eq. 5
     still averages over the live members;
   * optional quantised tier (the first tier of the tiered extension,
@@ -95,6 +98,7 @@ class Page:
     serial: int
     slots: List[int]
     quant: bool = False     # keys held as E4M3 codes and a scale per 16 tokens
+    closed: bool = False    # region-aligned pages: left at a region boundary
 
 
 E4M3_MAX = 448.0
@@ -192,12 +196,13 @@ class Session:
         n = region.shape[0]
         cap = n if capacity is None else max(int(capacity), n)
         # Slot store: slot j holds one token's state; keys layer-major
-        # [L][Hkv][slot][d] as float32 (bf16 values are exact in float32).
+        # [L][Hkv][slot][d] as their bfloat16 bit patterns, widened exactly
+        # wherever they are used.
         self.region = np.zeros(cap, dtype=np.int64)
         self.t_ins = np.zeros(cap, dtype=np.int64)
         self.t_ref = np.zeros(cap, dtype=np.int64)
         self.a = np.zeros(cap, dtype=np.float64)
-        self.keys = np.zeros((L, Hkv, cap, d), dtype=np.float32)
+        self.keys = np.zeros((L, Hkv, cap, d), dtype=np.uint16)
         # quantised tokens: codes [L][Hkv][slot][d] and their group's scale
         self.codes = np.zeros((L, Hkv, cap, d), dtype=np.uint8) if self.quant_threshold > 0 else None
         self.qscale = np.zeros((L, Hkv, cap), dtype=np.float32) if self.quant_threshold > 0 else None
@@ -209,7 +214,7 @@ class Session:
         if a is not None:
             self.a[:n] = np.asarray(a, dtype=np.float64)
         kb = np.asarray(keys_bits, dtype=np.uint16).reshape(n, L, Hkv, d)
-        self.keys[:, :, :n, :] = widen_bf16(kb).transpose(1, 2, 0, 3)
+        self.keys[:, :, :n, :] = kb.transpose(1, 2, 0, 3)
 
         if page_sizes is None:
             page_sizes = (aligned_page_sizes(region, P) if self.region_aligned
@@ -223,6 +228,11 @@ class Session:
         for ser, sz in zip(page_serials, page_sizes):
             self.pages.append(Page(int(ser), list(range(pos, pos + sz))))
             pos += sz
+        # region-aligned prompt: every page but the last was left full or at
+        # a region boundary
+        if self.region_aligned:
+            for p in self.pages[:-1]:
+                p.closed = True
         self.next_serial = (max(page_serials) + 1 if page_serials else 0) \
             if next_serial is None else int(next_serial)
 
@@ -249,7 +259,7 @@ class Session:
             setattr(self, name, np.concatenate([arr, np.zeros(new - cap, dtype=arr.dtype)]))
         self.a = np.concatenate([self.a, np.zeros(new - cap)])
         self.is_quant = np.concatenate([self.is_quant, np.zeros(new - cap, dtype=bool)])
-        k = np.zeros((self.L, self.Hkv, new, self.d), dtype=np.float32)
+        k = np.zeros((self.L, self.Hkv, new, self.d), dtype=np.uint16)
         k[:, :, :cap, :] = self.keys
         self.keys = k
         if self.codes is not None:
@@ -270,13 +280,14 @@ class Session:
         self.t_ins[j] = self.t
         self.t_ref[j] = self.t
         self.a[j] = 0.0
-        self.keys[:, :, j, :] = widen_bf16(key_bits).reshape(self.L, self.Hkv, self.d)
-        tail = self.pages[-1].slots if self.pages else None
-        joins = tail is not None and len(tail) < self.P
-        if joins and self.region_aligned:
-            joins = int(self.region[tail[-1]]) == int(region)
+        self.keys[:, :, j, :] = np.asarray(key_bits, dtype=np.uint16).reshape(self.L, self.Hkv, self.d)
+        tail = self.pages[-1] if self.pages else None
+        joins = tail is not None and len(tail.slots) < self.P and not tail.closed
+        if joins and self.region_aligned and int(self.region[tail.slots[-1]]) != int(region):
+            tail.closed = True      # a region boundary closes the page for good
+            joins = False
         if joins:
-            tail.append(j)
+            tail.slots.append(j)
         else:
             self.pages.append(Page(self.next_serial, [j]))
             self.next_serial += 1
@@ -284,7 +295,7 @@ class Session:
     def key_rows(self, l: int, kv: int, slots: np.ndarray) -> np.ndarray:
         """float64 keys of the given slots at (layer l, KV head kv): the cached
         values, or scale * code for quantised tokens."""
-        k = self.keys[l, kv][slots].astype(np.float64)
+        k = widen_bf16(self.keys[l, kv][slots]).astype(np.float64)
         if self.codes is not None:
             qz = self.is_quant[slots]
             if np.any(qz):
@@ -300,7 +311,7 @@ class Session:
             grp = slots[g0:g0 + 16]
             for l in range(self.L):
                 for kv in range(self.Hkv):
-                    c, s = quantise_block(self.keys[l, kv][grp])
+                    c, s = quantise_block(widen_bf16(self.keys[l, kv][grp]))
                     self.codes[l, kv][grp] = c
                     self.qscale[l, kv][grp] = s
         self.is_quant[slots] = True

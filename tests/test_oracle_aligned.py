@@ -182,3 +182,36 @@ def test_whole_run_invariants():
             assert rec.n_after <= B
             if rec.evicted.size:
                 assert rec.n_after > B - w.P
+
+
+def test_a_page_closed_at_a_region_boundary_stays_closed():
+    # 16 system tokens and 5 plan tokens; a user token closes the plan page
+    # and opens a page of its own, which the step then evicts (user scores
+    # 0, plan 1, system pinned).  The plan page is the last page again, yet
+    # a later plan token opens a fresh page: the places the plan page gave up
+    # at the boundary are not handed out again.
+    b = np.zeros(NREG)
+    b[PLAN] = 1.0
+    reg = runs((0, 16), (PLAN, 5))
+    s = session(reg, b=b, pinned_mask=1, budget=21, alpha=0.0)
+    assert [len(p.slots) for p in s.pages] == [16, 5]
+    rec = s.step(np.ones((1, 1, 8), np.float32), bf16(np.ones((1, 1, 8))), USER)
+    assert rec.page_serial.tolist() == [0, 1, 2] and rec.page_size.tolist() == [16, 5, 1]
+    assert rec.evicted.tolist() == [2] and rec.n_after == 21
+    assert s.pages[-1].closed
+    s.step(None, bf16(np.ones((1, 1, 8))), PLAN)          # a step that only appends
+    assert [p.serial for p in s.pages] == [0, 1, 3]
+    assert [len(p.slots) for p in s.pages] == [16, 5, 1]
+    # the plain layout has no closed pages: the same tokens fill the page
+    s2 = session(reg, b=b, pinned_mask=1, budget=21, alpha=0.0, aligned=False)
+    rec2 = s2.step(np.ones((1, 1, 8), np.float32), bf16(np.ones((1, 1, 8))), USER)
+    assert rec2.page_size.tolist() == [16, 6] and not any(p.closed for p in s2.pages)
+
+
+def test_prompt_pages_before_the_last_are_closed():
+    s = session(runs((PLAN, 5), (USER, 20), (TOOL_OUT, 3)))
+    assert [len(p.slots) for p in s.pages] == [5, 16, 4, 3]
+    assert [p.closed for p in s.pages] == [True, True, True, False]
+    # the open last page takes a token of its own region
+    s.step(None, bf16(np.ones((1, 1, 8))), TOOL_OUT)
+    assert [len(p.slots) for p in s.pages] == [5, 16, 4, 4]

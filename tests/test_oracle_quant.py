@@ -14,6 +14,7 @@ import pytest
 import scipy.special
 
 from oracle import Session, e4m3_decode, e4m3_encode, quantise_block
+from oracle.memdecay import widen_bf16
 
 NREG = 7
 PLAN, USER = 1, 2
@@ -180,12 +181,12 @@ def test_mass_over_decoded_keys_is_the_textbook_softmax():
     live = s.live()
     dec = np.where(s.is_quant[live][:, None],
                    e4m3_decode(s.codes[0, 0][live]) * s.qscale[0, 0][live][:, None].astype(np.float64),
-                   s.keys[0, 0][live].astype(np.float64))
+                   widen_bf16(s.keys[0, 0][live]).astype(np.float64))
     want = scipy.special.softmax(dec @ q[0, 0].astype(np.float64) / math.sqrt(d))
     np.testing.assert_allclose(rec.abar, want, rtol=1e-12, atol=0)
     # and the decoded keys are within half a grid step of the cached ones:
     # 2^-4 of the value for normal codes, 2^-10 s below them
-    k = s.keys[0, 0][live].astype(np.float64)
+    k = widen_bf16(s.keys[0, 0][live]).astype(np.float64)
     sc = s.qscale[0, 0][live][:, None].astype(np.float64)
     err = np.abs(dec - k)
     assert np.all(err <= np.abs(k) * (2.0 ** -4 + 2.0 ** -20) + sc * 2.0 ** -10)
