@@ -28,10 +28,12 @@
  *  * Negative return values are errors detected on the host before anything
  *    was enqueued; the session state is unchanged.  Conditions only the
  *    device can see (free list empty, non-finite query) set bits in a device
- *    status word read by md_read_device_status.
+ *    status word read by md_read_device_status.  Positive values are
+ *    warnings (MD_W_*).
  *  * A handle is not thread-safe; calls on one handle must be serialised.
- *  * Physical page ids handed out by the free list depend on scheduling; all
- *    scores, selections and logical page orders are deterministic.
+ *  * Every result is deterministic, the physical page ids included: an
+ *    append takes pages off the free list in session order, and md_compact
+ *    pushes the freed ids in (session, serial) order.
  *
  * Layouts (S = max_sessions, NP = n_phys_pages, P = page_size, MP = max_pages)
  *  k_pool       uint16 bf16 bits [NP][L][Hkv][P/16][d/8][16][8]   keys of each
@@ -73,7 +75,7 @@
 extern "C" {
 #endif
 
-#define MD_ABI_VERSION 5
+#define MD_ABI_VERSION 6
 
 typedef int32_t md_status;
 
@@ -84,12 +86,17 @@ enum {
     MD_E_STEP = -3,         /* step did not advance by exactly one              */
     MD_E_HIP = -4,          /* a HIP runtime call failed                        */
     MD_E_STATE = -5,        /* call out of order (e.g. select before score)     */
-    MD_E_NOMEM = -6         /* scratch allocation failed in md_init             */
+    MD_E_NOMEM = -6,        /* scratch allocation failed in md_init             */
+    MD_W_BUDGET_INFEASIBLE = 1  /* warning (md_read_device_status): some        */
+                            /* selection found a session whose pinned tokens   */
+                            /* alone exceed its budget (Eq. 1 has no feasible  */
+                            /* set); its infeasible flag says which            */
 };
 
 /* Bits of the device status word. */
 #define MD_DEV_CAPACITY   0x1   /* free list empty or page table full at append */
-#define MD_DEV_NONFINITE  0x2   /* NaN or infinity in a decode query            */
+#define MD_DEV_NONFINITE  0x2   /* NaN or infinity in a decode query: the       */
+                                /* session's step is void (see below)          */
 #define MD_DEV_BAD_EVICT  0x4   /* md_compact got a serial the session lacks    */
 #define MD_DEV_CORRUPT    0x8   /* a session's counters, page table or region   */
                                 /* codes are out of range; the session is      */
@@ -97,6 +104,12 @@ enum {
 #define MD_DEV_TIMEOUT    0x10  /* a bounded wait between the workgroups of the */
                                 /* fused observation kernel ran out; the step's */
                                 /* attention mass is not valid                  */
+/* A void step.  A session whose decode query is not finite, or whose
+ * workgroups of the fused kernel ran out of time, takes no part in the
+ * step's selection (evict_count 0), compaction or quantisation, and its
+ * tokens keep their importance and refresh clocks (on a time-out, the
+ * workgroups that did complete their share of the session's tokens have
+ * updated those tokens).  The append and the clock advance stand. */
 
 /* Bits of md_config.flags. */
 #define MD_FLAG_NO_FUSED  0x1   /* observe every session with the multi-kernel  */
@@ -264,10 +277,14 @@ md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_cou
  * md_compact — apply an eviction (Sec. III-E: irreversible): remove the
  * listed pages from each session's page table and serial list keeping the
  * order of the rest, update n_pages / n_tokens (and n_live with
- * region-aligned pages), and push the freed physical
- * ids onto the free list.  evict_serial / evict_count have md_select_evict's
- * layout and are normally its output; serials a session does not hold set
- * MD_DEV_BAD_EVICT and are ignored.
+ * region-aligned pages), and push the freed physical ids onto the free list
+ * in (session, serial) order.
+ * evict_serial / evict_count: both NULL to apply this step's selection (the
+ * lists of the last md_select_evict since md_observe_step; MD_E_STATE when
+ * there was none), or both given, with md_select_evict's layout, to apply
+ * other lists (a caller's own choice; one NULL and one not is
+ * MD_E_INVALID).  Serials a session does not hold set MD_DEV_BAD_EVICT and
+ * are ignored.  Sessions whose step is void are left as they are.
  * Quantised tier (quant_threshold > 0; Sec. III-E's first tier): before the
  * compaction, every page that survives, is not pinned, is not the session's
  * last page, is still bf16 and has page score S_p < quant_threshold (the
@@ -280,7 +297,10 @@ md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_cou
 md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* evict_count);
 
 /* Synchronise the stream and copy the device status word to *host_out, then
- * clear it.  Returns MD_E_HIP if the stream reports an error. */
+ * clear it.  Returns MD_W_BUDGET_INFEASIBLE when a selection since the last
+ * read found a session whose pinned tokens exceed its budget (the
+ * selection itself cannot report it without synchronising), MD_OK
+ * otherwise, and MD_E_HIP if the stream reports an error. */
 md_status md_read_device_status(md_handle h, int32_t* host_out);
 
 /* Kernel ids for md_profile_enable / md_profile_read. */

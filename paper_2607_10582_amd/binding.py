@@ -18,6 +18,7 @@ MD_E_STEP = -3
 MD_E_HIP = -4
 MD_E_STATE = -5
 MD_E_NOMEM = -6
+MD_W_BUDGET_INFEASIBLE = 1
 
 MD_DEV_CAPACITY = 0x1
 MD_DEV_NONFINITE = 0x2
@@ -74,14 +75,38 @@ class MemDecayError(RuntimeError):
 _lib = None
 
 
+def _start_hip_runtime() -> None:
+    """Start the HIP runtime before the library is loaded.
+
+    Loading libmemdecay.so registers its GPU code object, and with it an
+    exit handler that unregisters the code object through the HIP runtime.
+    Exit handlers run in the reverse order of their registration, so when
+    the runtime (and any tool attached to it, such as a profiler, which
+    registers its own exit handler when the runtime starts) starts after the
+    library is loaded, the runtime's shutdown runs first and the library's
+    handler then calls into a runtime that is gone.  Starting the runtime
+    first puts the library's handler ahead of the runtime's.  Without a
+    device (a build host) the call fails and nothing else happens.
+    """
+    try:
+        hip = ctypes.CDLL("libamdhip64.so", mode=ctypes.RTLD_GLOBAL)
+        hip.hipInit.restype = ctypes.c_int
+        hip.hipInit.argtypes = [ctypes.c_uint]
+        hip.hipInit(0)
+    except (OSError, AttributeError):
+        pass
+
+
 def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load libmemdecay.so (built by paper_2607_10582_amd.build)."""
+    """Load libmemdecay.so (built by paper_2607_10582_amd.build), after
+    starting the HIP runtime."""
     global _lib
     if _lib is not None:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it first "
                            "(python -m paper_2607_10582_amd.build)")
+    _start_hip_runtime()
     lib = ctypes.CDLL(path)
     vp, i32 = ctypes.c_void_p, ctypes.c_int32
     lib.md_abi_version.restype = i32
@@ -164,14 +189,18 @@ def md_select_evict(h: int, evict_serial: int, evict_count: int, infeasible: int
         h, evict_serial, evict_count, infeasible))
 
 
-def md_compact(h: int, evict_serial: int, evict_count: int) -> int:
-    return _check("md_compact", load_library().md_compact(h, evict_serial, evict_count))
+def md_compact(h: int, evict_serial: int | None = None, evict_count: int | None = None) -> int:
+    """Both lists None: apply this step's selection."""
+    return _check("md_compact", load_library().md_compact(h, evict_serial or None, evict_count or None))
 
 
-def md_read_device_status(h: int) -> int:
+def md_read_device_status(h: int, with_warning: bool = False):
+    """The device status word (cleared by the read); with_warning=True
+    returns (return code, status word), the return code being
+    MD_W_BUDGET_INFEASIBLE or MD_OK."""
     out = ctypes.c_int32(0)
-    _check("md_read_device_status", load_library().md_read_device_status(h, ctypes.byref(out)))
-    return out.value
+    rc = _check("md_read_device_status", load_library().md_read_device_status(h, ctypes.byref(out)))
+    return (rc, out.value) if with_warning else out.value
 
 
 def md_profile_enable(h: int, kernel_mask: int) -> int:

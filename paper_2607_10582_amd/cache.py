@@ -202,9 +202,11 @@ class MemDecay:
 
     def compact(self, evict_serial: Optional[torch.Tensor] = None,
                 evict_count: Optional[torch.Tensor] = None):
-        es = self.evict_serial if evict_serial is None else evict_serial
-        ec = self.evict_count if evict_count is None else evict_count
-        B.md_compact(self.handle, _ptr(es, torch.int32), _ptr(ec, torch.int32))
+        """Apply this step's selection (no arguments), or the given lists."""
+        if evict_serial is None and evict_count is None:
+            B.md_compact(self.handle, None, None)
+        else:
+            B.md_compact(self.handle, _ptr(evict_serial, torch.int32), _ptr(evict_count, torch.int32))
 
     def step(self, step: int, q, new_k=None, new_region=None, page_scores: bool = True):
         """One decode step; page_scores=False leaves self.page_score untouched
@@ -223,8 +225,8 @@ class MemDecay:
         B.md_calib_accumulate(self.handle, _ptr(abar, torch.float32), bucket_steps, mass.shape[-1],
                               mass.data_ptr(), count.data_ptr(), age.data_ptr())
 
-    def device_status(self) -> int:
-        return B.md_read_device_status(self.handle)
+    def device_status(self, with_warning: bool = False):
+        return B.md_read_device_status(self.handle, with_warning)
 
     def profile(self, kernels=("logits",)):
         """Time the named kernels with events from now on (() turns it off)."""

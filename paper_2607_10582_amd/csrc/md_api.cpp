@@ -42,6 +42,8 @@ struct md_handle_s {
     bool fused_last;     // the last observe ran it
     int64_t observed;    // observes enqueued
     Phase phase;
+    const int32_t* sel_serial;   // md_select_evict's lists since the last observe
+    const int32_t* sel_count;    // (NULL: no selection yet)
     uint32_t profile_mask;
     std::vector<Timed> pending[MD_K_COUNT];   // launches not yet read back
     std::vector<Timed> spare;                  // recycled event pairs
@@ -100,6 +102,7 @@ const char* md_status_str(md_status s) {
         case MD_E_STATE: return "call out of order (score needs an observe, select needs a score, "
                                 "and neither may follow a compact before the next observe)";
         case MD_E_NOMEM: return "could not allocate the library scratch";
+        case MD_W_BUDGET_INFEASIBLE: return "warning: a session's pinned tokens exceed its budget";
         default: return "unknown status";
     }
 }
@@ -337,6 +340,8 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     h->fused_last = false;
     h->observed = 0;
     h->phase = kNone;
+    h->sel_serial = nullptr;
+    h->sel_count = nullptr;
     h->profile_mask = 0;
     *out = h;
     return MD_OK;
@@ -358,6 +363,7 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
         h->have_step = true;
         h->last_step = step;
         h->phase = kNone;
+        h->sel_serial = h->sel_count = nullptr;
         return MD_OK;
     }
     const bool fused = h->observed == 0 ? h->fused_first : h->fused_steady;
@@ -382,6 +388,7 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     h->have_step = true;
     h->last_step = step;
     h->phase = kObserved;
+    h->sel_serial = h->sel_count = nullptr;
     return MD_OK;
 }
 
@@ -414,13 +421,20 @@ md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_cou
             return md::launch_select(h->dm, h->v, h->sc, evict_serial, evict_count, infeasible,
                                      h->stream); }) != hipSuccess)
         return MD_E_HIP;
+    h->sel_serial = evict_serial;
+    h->sel_count = evict_count;
     return MD_OK;
 }
 
 md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* evict_count) {
-    if (h == nullptr || evict_serial == nullptr || evict_count == nullptr) return MD_E_INVALID;
-    if (!aligned(evict_serial, 4) || !aligned(evict_count, 4)) return MD_E_INVALID;
+    if (h == nullptr || ((evict_serial == nullptr) != (evict_count == nullptr))) return MD_E_INVALID;
     if (h->phase == kNone) return MD_E_STATE;
+    if (evict_serial == nullptr) {   // the selection of this step
+        if (h->sel_serial == nullptr || h->phase != kScored) return MD_E_STATE;
+        evict_serial = h->sel_serial;
+        evict_count = h->sel_count;
+    }
+    if (!aligned(evict_serial, 4) || !aligned(evict_count, 4)) return MD_E_INVALID;
     if (h->dm.quant && h->phase != kScored) return MD_E_STATE;   // the tier needs this step's scores
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
     if (h->dm.quant &&
@@ -431,19 +445,20 @@ md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* ev
         hipSuccess)
         return MD_E_HIP;
     h->phase = kCompacted;
+    h->sel_serial = h->sel_count = nullptr;
     return MD_OK;
 }
 
 md_status md_read_device_status(md_handle h, int32_t* host_out) {
     if (h == nullptr || host_out == nullptr) return MD_E_INVALID;
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
-    int32_t v = 0;
-    if (hipMemcpyAsync(&v, h->sc.status, sizeof(int32_t), hipMemcpyDeviceToHost, h->stream) != hipSuccess ||
-        hipMemsetAsync(h->sc.status, 0, sizeof(int32_t), h->stream) != hipSuccess ||
+    int32_t v[2] = {0, 0};   // the status word and the warning word next to it
+    if (hipMemcpyAsync(v, h->sc.status, sizeof(v), hipMemcpyDeviceToHost, h->stream) != hipSuccess ||
+        hipMemsetAsync(h->sc.status, 0, sizeof(v), h->stream) != hipSuccess ||
         hipStreamSynchronize(h->stream) != hipSuccess)
         return MD_E_HIP;
-    *host_out = v;
-    return MD_OK;
+    *host_out = v[0];
+    return (v[1] & 1) ? MD_W_BUDGET_INFEASIBLE : MD_OK;
 }
 
 md_status md_profile_enable(md_handle h, uint32_t kernel_mask) {

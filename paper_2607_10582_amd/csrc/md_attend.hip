@@ -82,6 +82,7 @@ struct AttendArgs {
     const int32_t* n_live;   // tokens |K_t| (the n_tokens array unless pages are region-aligned)
     const uint8_t* page_format;   // quantised tier: 1 = the page holds E4M3 codes
     const int32_t* t_ins;         // window: insertion steps, for the causal mask
+    int32_t* valid;               // [S] cleared for a session whose step is void
 };
 
 // LDS row stride (floats) of a head's values: W waves of KT tiles
@@ -92,6 +93,7 @@ struct Lds {
     uint32_t* qs;     // [2][3][G][64] hi, mid, lo bf16 query terms (pairs) of two rows
     float2* wstat;    // [2][W][16] per-wave row statistics
     float2* norm;     // [2][16] row normalisers (M, 1 / Lambda)
+    int* vflag;       // [1] the unit's step is void: a non-finite query, or a wait ran out
 };
 
 __host__ __device__ inline size_t rowbuf_bytes(int G, int W, int KT) {
@@ -100,6 +102,7 @@ __host__ __device__ inline size_t rowbuf_bytes(int G, int W, int KT) {
 __host__ __device__ inline size_t qs_bytes(int G) { return (size_t)2 * 3 * G * 64 * sizeof(uint32_t); }
 __host__ __device__ inline size_t wstat_bytes(int W) { return (size_t)2 * W * 16 * sizeof(float2); }
 constexpr size_t kNormBytes = (size_t)2 * 16 * sizeof(float2);
+constexpr size_t kFlagBytes = 16;
 
 __device__ __forceinline__ Lds carve(unsigned char* smem, int G, int W, int KT) {
     Lds l;
@@ -111,6 +114,8 @@ __device__ __forceinline__ Lds carve(unsigned char* smem, int G, int W, int KT) 
     l.wstat = reinterpret_cast<float2*>(smem + o);
     o += wstat_bytes(W);
     l.norm = reinterpret_cast<float2*>(smem + o);
+    o += kNormBytes;
+    l.vflag = reinterpret_cast<int*>(smem + o);
     return l;
 }
 
@@ -324,7 +329,10 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
                         make_uint2(t[p][0] | (t[p][1] << 16), t[p][2] | (t[p][3] << 16));
             }
         }
-        if (bad) atomicOr(a.status, MD_DEV_NONFINITE);
+        if (bad) {   // the step of the session is void
+            atomicOr(a.status, MD_DEV_NONFINITE);
+            *sm.vflag = 1;
+        }
     };
     // ---- cross-unit words.  Every unit publishes its (max, sum) of each
     // (row, query head); the leader of row x (unit x mod nu of the session)
@@ -356,6 +364,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
             if (t - t0 > kGlobalWaitTicks || t > un.deadline) {
                 atomicOr(a.status, MD_DEV_TIMEOUT);
                 dead = true;
+                *sm.vflag = 1;
                 return;
             }
         }
@@ -426,7 +435,10 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
             load_stats(x, c0);
             fold(c0);
         }
-        if (hd_lane) {
+        // a leader whose wait ran out publishes nothing: every unit of the
+        // session then runs out of time on this row too, and all of them
+        // leave the step void
+        if (hd_lane && !dead) {
             float M = run_m[0], Ls = run_l[0];
 #pragma unroll
             for (int i = 1; i < NH; ++i)
@@ -654,6 +666,13 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // scores (Eq. 4) and the scores of their pages (Eq. 5): a page's P
     // tokens are P consecutive lanes of one wave, since units and waves
     // start at multiples of 64 tokens.
+    // A void step (a non-finite query, or a wait that ran out) changes no
+    // token's state and leaves the session out of this step's selection and
+    // compaction.
+    if (*sm.vflag != 0) {
+        if (threadIdx.x == 0) a.valid[un.s] = 0;
+        return;
+    }
     const int t_now = a.clock[un.s];
     const size_t rbase = (size_t)un.s * dm.n_regions;
     const int n_tok = AL ? un.nl_s : un.nt_s;   // |K_t|
@@ -820,6 +839,7 @@ k_attend(AttendDims dm, AttendArgs a) {
     const int cap = lanes ? dm.n_cu : 0;
     for (int ps = 0;; ++ps) {
         lds_sync();   // the previous unit is done with the LDS
+        if (threadIdx.x == 0) *sm.vflag = 0;   // ordered before the unit by the barriers below
         int sb, se;
         if (!lanes) {
             if (ps >= n_pass) break;
@@ -881,7 +901,8 @@ k_attend(AttendDims dm, AttendArgs a) {
 
 size_t attend_lds_bytes(int G) {
     const int W = attend_threads(G) / 64;
-    return rowbuf_bytes(G, W, attend_unit_tokens(G) / (16 * W)) + qs_bytes(G) + wstat_bytes(W) + kNormBytes;
+    return rowbuf_bytes(G, W, attend_unit_tokens(G) / (16 * W)) + qs_bytes(G) + wstat_bytes(W) + kNormBytes +
+           kFlagBytes;
 }
 
 namespace {
@@ -908,7 +929,7 @@ hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const
                   dm.rho, dm.tau_scale, dm.alpha, dm.aligned, dm.G, dm.W};
     AttendArgs aa{v.k_pool, v.page_table, v.n_tokens, v.clock, v.region, v.b, v.lam, v.imp, v.t_ref,
                   sc.pscore, q, abar_out, sc.ustart, sc.plan, sc.epoch, sc.claim, sc.lane_box, sc.ustat,
-                  sc.unorm, sc.status, nullptr, v.n_live, v.page_format, v.t_ins};
+                  sc.unorm, sc.status, nullptr, v.n_live, v.page_format, v.t_ins, sc.valid};
     void* args[] = {&ad, &aa};
     return hipLaunchCooperativeKernel(attend_kernel(dm.G * dm.W, dm.aligned, dm.quant, dm.W), dim3(dm.n_wg),
                                       dim3(attend_threads(dm.G * dm.W)), args,

@@ -85,9 +85,15 @@ struct Scratch {
     unsigned long long* ustat;  // [U_cap][R][2] tagged (max, sum) of each fused unit's rows
     unsigned long long* unorm;  // [S][R][2] tagged row normalisers (M, 1 / Lambda) of the fused sessions
     int32_t* chunks;       // [S] chunks per session (0 for a skipped session)
-    int32_t* valid;        // [S] 1 when the session's counters are consistent
+    int32_t* valid;        // [S] 1 while the session's step stands: its counters are
+                           // consistent, its query finite and no wait of the fused
+                           // kernel ran out; 0 leaves it out of selection and compaction
+    int32_t* freed;        // [S + 1] pages each session's compaction frees
     int32_t* done;         // [1] completion counter of the append kernel
     int32_t* status;       // [1] device status word
+    int32_t* warn;         // [1] warning bits (1: some session's budget was infeasible)
+    int32_t* done_compact; // [1] completion counter of the compaction kernel
+    int32_t* opened;       // [1] pages the append kernel takes from the free list
     unsigned long long* counters;  // [4] tokens scored, steps, pages evicted, tokens evicted
 };
 

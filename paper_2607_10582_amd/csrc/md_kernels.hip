@@ -23,14 +23,35 @@ namespace md {
 
 // ---------------------------------------------------------------- append
 
+// Whether the append of session s2 opens a page (takes one from the free
+// list), judged on the counters as they stand before the append: the last
+// page is full, or with region-aligned pages the token's region differs
+// from the last token's; and the page table has room.
+__device__ bool opens_page(const Dims& dm, const View& v, int s2, const uint8_t* __restrict__ new_region) {
+    const int np = v.n_pages[s2];
+    const int nt = v.n_tokens[s2];
+    if (!counters_ok(np, nt, dm) || np >= dm.MP) return false;
+    if (!(np > 0 && nt < np * dm.P)) return true;
+    if (!dm.aligned) return false;
+    const int p = v.page_table[(size_t)s2 * dm.MP + np - 1];
+    if (p < 0 || p >= dm.NP) return false;
+    const int slot = nt - (np - 1) * dm.P;
+    return v.region[(size_t)p * dm.P + slot - 1] != new_region[s2];
+}
+
 // One block per session: the append.  The last block to finish lays out the
 // step's work lists.
+// Pages leave the free list in session order: session s takes the entry
+// below those of the sessions before it that open a page at this append.
+// No block changes a session's page or token count before the last block
+// (each block leaves its session's new counts in sc.freed / sc.chunks), so
+// every block judges the earlier sessions on the counts before the append.
 __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                                                 const uint16_t* __restrict__ new_k,
                                                 const uint8_t* __restrict__ new_region, int fused,
                                                 int observe) {
     const int s = blockIdx.x;
-    __shared__ int sh_phys, sh_slot, sh_last;
+    __shared__ int sh_phys, sh_slot, sh_last, sh_rank;
     __shared__ int lds[5 * 17];
     // The step's key rows (16 pieces of 16 bytes per (layer, KV head) row)
     // do not depend on the slot: waves 1.. read their first kPre pieces now
@@ -48,11 +69,22 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             if (i < n_pieces) kr[c] = src[i];
         }
     }
+    // pages the sessions before this one take at this append
+    if (threadIdx.x == 0) sh_rank = 0;
+    __syncthreads();
+    if (new_k != nullptr) {
+        int mine = 0;
+        for (int s2 = threadIdx.x; s2 < s; s2 += blockDim.x) mine += opens_page(dm, v, s2, new_region) ? 1 : 0;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o);
+        if (lane_id() == 0 && mine > 0) atomicAdd(&sh_rank, mine);
+    }
+    __syncthreads();
     if (threadIdx.x == 0) {
         const int t = v.clock[s] + 1;
         v.clock[s] = t;
         int phys = -1, slot = 0;
-        const int np = v.n_pages[s];
+        int np = v.n_pages[s];
         int nt = v.n_tokens[s];
         if (new_k != nullptr && counters_ok(np, nt, dm)) {
             const size_t row = (size_t)s * dm.MP;
@@ -72,7 +104,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                             v.t_ref[s0 + o] = 0;
                             v.imp[s0 + o] = 0.0f;
                         }
-                        v.n_tokens[s] = nt = np * dm.P;
+                        nt = np * dm.P;
                         phys = -1;
                         open = true;
                     }
@@ -83,9 +115,13 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             if (!open) {
                 // the token joins the last page (or the page was corrupt)
             } else if (np < dm.MP) {
-                const int old = atomicSub(v.free_count, 1);
-                if (old > 0 && old <= dm.NP) {
-                    const int p = v.free_list[old - 1];
+                // the free list is a stack: this session takes the entry
+                // below the earlier sessions' ones (free_count changes only
+                // in the last block)
+                const int fc = v.free_count[0];
+                const int idx = min(fc, dm.NP) - 1 - sh_rank;
+                if (idx >= 0) {
+                    const int p = v.free_list[idx];
                     if (p >= 0 && p < dm.NP) {
                         phys = p;
                         slot = 0;
@@ -93,19 +129,19 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                         v.page_serial[row + np] = v.next_serial[s];
                         if (dm.quant) v.page_format[p] = 0;   // a reused page holds bf16 keys again
                         v.next_serial[s] += 1;
-                        v.n_pages[s] = np + 1;
+                        np += 1;
+                        atomicAdd(sc.opened, 1);
                     } else {
                         atomicOr(sc.status, kDevCorrupt);
                     }
                 } else {
-                    atomicAdd(v.free_count, 1);
                     atomicOr(sc.status, MD_DEV_CAPACITY);
                 }
             } else {
                 atomicOr(sc.status, MD_DEV_CAPACITY);
             }
             if (phys >= 0) {
-                v.n_tokens[s] = nt + 1;
+                nt += 1;
                 if (dm.aligned) v.n_live[s] += 1;
                 const size_t si = (size_t)phys * dm.P + slot;
                 v.region[si] = new_region[s];
@@ -116,6 +152,9 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         }
         sh_phys = phys;
         sh_slot = slot;
+        // the session's counts after the append, applied by the last block
+        sc.freed[s] = np;
+        sc.chunks[s] = nt;
     }
     __syncthreads();
     const int phys = sh_phys;
@@ -147,9 +186,17 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     __threadfence();
     __shared__ int s_n[kMaxSessions];      // live tokens (0 for a skipped session)
     __shared__ int s_pass[kMaxSessions];   // fused pass of the session, -1 on the spill path
+    if (threadIdx.x == 0) {
+        // pages taken from the free list by this append
+        const int fc = v.free_count[0];
+        v.free_count[0] = max(min(fc, dm.NP) - load_agent(sc.opened), 0);
+        *sc.opened = 0;
+    }
     for (int s2 = threadIdx.x; s2 < dm.S; s2 += blockDim.x) {
-        const int np = load_agent(v.n_pages + s2);
-        const int nt = load_agent(v.n_tokens + s2);
+        const int np = load_agent(sc.freed + s2);
+        const int nt = load_agent(sc.chunks + s2);
+        v.n_pages[s2] = np;
+        v.n_tokens[s2] = nt;
         const bool ok = counters_ok(np, nt, dm);
         if (!ok) atomicOr(sc.status, kDevCorrupt);
         sc.valid[s2] = ok ? 1 : 0;
@@ -328,7 +375,7 @@ struct LogitsDims {
 // 32j + 8g .. +7; each float32 term is split into hi, mid and lo bf16 terms.
 __device__ __forceinline__ void split_query_regs(u32x4 (&bq)[4][3], const float* __restrict__ q,
                                                  const LogitsDims& dm, int s, int lkv, int h, int g,
-                                                 int32_t* status) {
+                                                 int32_t* status, int32_t* valid) {
     const int l = lkv / dm.Hkv, kv = lkv - l * dm.Hkv;
     const int w = h / dm.G, hh = h - w * dm.G;
     const float* qh = q + ((((size_t)s * dm.W + w) * dm.L + l) * dm.Hq + kv * dm.G + hh) * kHeadDim;
@@ -353,7 +400,10 @@ __device__ __forceinline__ void split_query_regs(u32x4 (&bq)[4][3], const float*
             bq[j][2][e >> 1] = l0 | (l1 << 16);
         }
     }
-    if (bad) atomicOr(status, MD_DEV_NONFINITE);
+    if (bad) {   // a non-finite query voids the session's step
+        atomicOr(status, MD_DEV_NONFINITE);
+        valid[s] = 0;
+    }
 }
 
 // The eight 16-token row tiles of an item: slot index (physical page * P +
@@ -447,7 +497,7 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
          float* __restrict__ logits, float2* __restrict__ cstats, int32_t* status,
          const int32_t* __restrict__ item_prefix, const int32_t* __restrict__ t_ins,
          const int32_t* __restrict__ clock, const uint8_t* __restrict__ region,
-         const uint8_t* __restrict__ page_format) {
+         const uint8_t* __restrict__ page_format, int32_t* valid) {
     __shared__ int s_pref[kMaxSessions + 1];
     const int S = dm.S;
     for (int i = threadIdx.x; i <= S; i += blockDim.x) s_pref[i] = item_prefix[i];
@@ -477,7 +527,7 @@ k_logits(LogitsDims dm, const uint16_t* __restrict__ k_pool, const int32_t* __re
     // at a time; the query operands load once per segment.
     while (it < end) {
         const int seg_end = min(end, it + (cu.nch - cu.c));
-        split_query_regs(bq, q, dm, cu.s, cu.lkv, h, g, status);
+        split_query_regs(bq, q, dm, cu.s, cu.lkv, h, g, status, valid);
         const int l = uni(cu.lkv / dm.Hkv);
         const int kv = cu.lkv - l * dm.Hkv;
         const int row0 = uni(cu.lkv * dm.Gw);   // first logits row of the group: (lkv, w, h)
@@ -596,7 +646,7 @@ hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const
                   dm.W, dm.G * dm.W, dm.aligned, dm.quant};
     hipLaunchKernelGGL(dm.quant ? k_logits<true> : k_logits<false>, dim3(n_blocks), dim3(256), 0, st, ld, v.k_pool, v.page_table,
                        v.n_tokens, q, sc.logits, sc.cstats, sc.status, sc.item_prefix, v.t_ins, v.clock,
-                       v.region, v.page_format);
+                       v.region, v.page_format, sc.valid);
     return hipGetLastError();
 }
 
@@ -680,7 +730,7 @@ __global__ void __launch_bounds__(256) k_mass(Dims dm, View v, Scratch sc, float
         }
         s_part[rg][tl] = acc;
         __syncthreads();
-        if (rg == 0 && valid) {
+        if (rg == 0 && valid && sc.valid[s]) {   // a void step writes nothing
             const float abar =
                 (((s_part[0][tl] + s_part[1][tl]) + s_part[2][tl]) + s_part[3][tl]) / (float)dm.R;
             const size_t si = (size_t)phys * dm.P + slot;
@@ -911,6 +961,7 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
     if (tid == 0) {
         ev_count[s] = n_ev;
         infeasible[s] = infeas ? 1 : 0;
+        if (infeas) atomicOr(sc.warn, 1);
     }
 }
 
@@ -923,86 +974,154 @@ hipError_t launch_select(const Dims& dm, const View& v, const Scratch& sc, int32
 
 // ---------------------------------------------------------------- compact
 
+// Pages listed for eviction in a session whose step stands (0 otherwise):
+// the places the session's freed ids take on the free list.
+__device__ __forceinline__ int evict_listed(const Dims& dm, const Scratch& sc, const int32_t* ev_count, int s) {
+    return sc.valid[s] ? min(max(ev_count[s], 0), dm.MP) : 0;
+}
+
+// One block per session.  Freed physical ids go onto the free list in
+// (session, serial) order: session s pushes above the places of the
+// sessions before it, which reserve one place per listed serial; the last
+// block to finish sets the new count and, if some list named serials its
+// session does not hold, closes the gaps they left, keeping the order.
 __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratch sc,
                                                          const int32_t* __restrict__ ev_serial,
                                                          const int32_t* __restrict__ ev_count) {
     const int s = blockIdx.x;
     __shared__ int lds[3 * 17];
-    __shared__ int sh_base;
+    __shared__ int sh_last, sh_before;
     const int tid = threadIdx.x;
-    const int cnt = ev_count[s];
+    const int cnt = evict_listed(dm, sc, ev_count, s);
     const int np = v.n_pages[s], nt = v.n_tokens[s];
-    if (!sc.valid[s] || cnt <= 0 || np == 0) return;
-    const int* evs = ev_serial + (size_t)s * dm.MP;
-    int* ptab = v.page_table + (size_t)s * dm.MP;
-    int* pser = v.page_serial + (size_t)s * dm.MP;
-    const int per = (np + kSelThreads - 1) / kSelThreads;
-    const int i0 = min(np, tid * per), i1 = min(np, i0 + per);
-    int ph[kPerThread], se[kPerThread];
-    bool keep[kPerThread];
-    int n_keep = 0, n_gone = 0, live_gone = 0;
+    if (tid == 0) sh_before = 0;
+    __syncthreads();
+    {
+        int mine = 0;
+        for (int s2 = tid; s2 < s; s2 += blockDim.x) mine += evict_listed(dm, sc, ev_count, s2);
 #pragma unroll
-    for (int k = 0; k < kPerThread; ++k) {
-        const int i = i0 + k;
-        keep[k] = false;
-        ph[k] = se[k] = 0;
-        if (i < i1) {
-            ph[k] = ptab[i];
-            se[k] = pser[i];
-            int lo = 0, hi = min(cnt, dm.MP);
-            while (lo < hi) {  // serials in the list ascend
-                const int mid = (lo + hi) >> 1;
-                if (evs[mid] < se[k]) lo = mid + 1; else hi = mid;
+        for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o);
+        if (lane_id() == 0 && mine > 0) atomicAdd(&sh_before, mine);
+    }
+    __syncthreads();
+    const int fc = v.free_count[0];   // changes only in the last block
+    int gone_total = 0;
+    if (cnt > 0 && np == 0) {
+        if (tid == 0) atomicOr(sc.status, MD_DEV_BAD_EVICT);
+    } else if (cnt > 0) {
+        const int* evs = ev_serial + (size_t)s * dm.MP;
+        int* ptab = v.page_table + (size_t)s * dm.MP;
+        int* pser = v.page_serial + (size_t)s * dm.MP;
+        const int per = (np + kSelThreads - 1) / kSelThreads;
+        const int i0 = min(np, tid * per), i1 = min(np, i0 + per);
+        int ph[kPerThread], se[kPerThread];
+        bool keep[kPerThread];
+        int n_keep = 0, n_gone = 0, live_gone = 0;
+#pragma unroll
+        for (int k = 0; k < kPerThread; ++k) {
+            const int i = i0 + k;
+            keep[k] = false;
+            ph[k] = se[k] = 0;
+            if (i < i1) {
+                ph[k] = ptab[i];
+                se[k] = pser[i];
+                int lo = 0, hi = min(cnt, dm.MP);
+                while (lo < hi) {  // serials in the list ascend
+                    const int mid = (lo + hi) >> 1;
+                    if (evs[mid] < se[k]) lo = mid + 1; else hi = mid;
+                }
+                const bool gone = lo < min(cnt, dm.MP) && evs[lo] == se[k];
+                keep[k] = !gone;
+                n_keep += gone ? 0 : 1;
+                n_gone += gone ? 1 : 0;
+                if (gone) live_gone += page_tokens(dm, v, ph[k], i, np, nt);
             }
-            const bool gone = lo < min(cnt, dm.MP) && evs[lo] == se[k];
-            keep[k] = !gone;
-            n_keep += gone ? 0 : 1;
-            n_gone += gone ? 1 : 0;
-            if (gone) live_gone += page_tokens(dm, v, ph[k], i, np, nt);
+        }
+        int kept_total;
+        const int mine[3] = {n_keep, n_gone, live_gone};
+        int ex[3], tot[3];
+        block_exclusive_scan_n<3>(mine, lds, ex, tot);   // ends with a barrier: the old table is read
+        int kpos = ex[0], gpos = ex[1];
+        kept_total = tot[0];
+        gone_total = tot[1];
+        const int live_gone_total = tot[2];
+        const int base = fc + sh_before;
+        if (tid == 0) {
+            if (gone_total != cnt) atomicOr(sc.status, MD_DEV_BAD_EVICT);
+            if (fc < 0 || base + gone_total > dm.NP) atomicOr(sc.status, kDevCorrupt);
+        }
+#pragma unroll
+        for (int k = 0; k < kPerThread; ++k) {
+            if (i0 + k < i1) {
+                if (keep[k]) {
+                    ptab[kpos] = ph[k];
+                    pser[kpos] = se[k];
+                    ++kpos;
+                } else {
+                    if (base + gpos >= 0 && base + gpos < dm.NP) v.free_list[base + gpos] = ph[k];
+                    ++gpos;
+                }
+            }
+        }
+        // The thread owning the last page knows whether it survived; all pages
+        // but the last are full, so the token count follows from that.
+        if (i1 == np && i1 > i0) {
+            const int k_last = np - 1 - i0;
+            bool last_kept = false;
+#pragma unroll
+            for (int k = 0; k < kPerThread; ++k)
+                if (k == k_last) last_kept = keep[k];
+            const int nt_new = last_kept ? nt - gone_total * dm.P : kept_total * dm.P;
+            v.n_pages[s] = kept_total;
+            v.n_tokens[s] = nt_new;
+            if (dm.aligned) v.n_live[s] -= live_gone_total;
+            atomicAdd(&sc.counters[2], (unsigned long long)gone_total);
+            atomicAdd(&sc.counters[3], (unsigned long long)live_gone_total);
         }
     }
-    int kept_total, gone_total;
-    const int mine[3] = {n_keep, n_gone, live_gone};
-    int ex[3], tot[3];
-    block_exclusive_scan_n<3>(mine, lds, ex, tot);
-    int kpos = ex[0], gpos = ex[1];
-    kept_total = tot[0];
-    gone_total = tot[1];
-    const int live_gone_total = tot[2];
+    if (tid == 0) sc.freed[s] = gone_total;
+
+    // The last block to finish: the new free count; gaps left by listed
+    // serials a session did not hold are closed session by session, each
+    // chunk read before it is written (destinations never pass sources).
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) sh_last = (atomicAdd(sc.done_compact, 1) == (int)gridDim.x - 1);
+    __syncthreads();
+    if (!sh_last) return;
+    __threadfence();
+    int pushed = 0, listed = 0;
+    for (int s2 = tid; s2 < dm.S; s2 += blockDim.x) {
+        pushed += load_agent(sc.freed + s2);
+        listed += evict_listed(dm, sc, ev_count, s2);
+    }
+    int tot2[2];
+    {
+        const int m2[2] = {pushed, listed};
+        int ex2[2];
+        block_exclusive_scan_n<2>(m2, lds, ex2, tot2);
+    }
+    if (tot2[0] != tot2[1] && fc >= 0) {
+        int src = fc, dst = fc;
+        for (int s2 = 0; s2 < dm.S; ++s2) {
+            const int g = load_agent(sc.freed + s2);
+            if (dst != src) {
+                for (int c = 0; c < g; c += blockDim.x) {
+                    const int i = c + tid;
+                    const bool in = i < g && src + i < dm.NP && dst + i >= 0;
+                    const int id = in ? load_agent(v.free_list + src + i) : 0;
+                    __syncthreads();
+                    if (in) v.free_list[dst + i] = id;
+                    __syncthreads();
+                }
+            }
+            src += evict_listed(dm, sc, ev_count, s2);
+            dst += g;
+        }
+    }
     if (tid == 0) {
-        if (gone_total != cnt) atomicOr(sc.status, MD_DEV_BAD_EVICT);
-        sh_base = gone_total > 0 ? atomicAdd(v.free_count, gone_total) : 0;
-        if (sh_base < 0 || sh_base + gone_total > dm.NP) atomicOr(sc.status, kDevCorrupt);
-    }
-    __syncthreads();  // every read of the old table is done before any write
-    const int base = sh_base;
-#pragma unroll
-    for (int k = 0; k < kPerThread; ++k) {
-        if (i0 + k < i1) {
-            if (keep[k]) {
-                ptab[kpos] = ph[k];
-                pser[kpos] = se[k];
-                ++kpos;
-            } else {
-                if (base + gpos >= 0 && base + gpos < dm.NP) v.free_list[base + gpos] = ph[k];
-                ++gpos;
-            }
-        }
-    }
-    // The thread owning the last page knows whether it survived; all pages
-    // but the last are full, so the token count follows from that.
-    if (i1 == np && i1 > i0) {
-        const int k_last = np - 1 - i0;
-        bool last_kept = false;
-#pragma unroll
-        for (int k = 0; k < kPerThread; ++k)
-            if (k == k_last) last_kept = keep[k];
-        const int nt_new = last_kept ? nt - gone_total * dm.P : kept_total * dm.P;
-        v.n_pages[s] = kept_total;
-        v.n_tokens[s] = nt_new;
-        if (dm.aligned) v.n_live[s] -= live_gone_total;
-        atomicAdd(&sc.counters[2], (unsigned long long)gone_total);
-        atomicAdd(&sc.counters[3], (unsigned long long)live_gone_total);
+        v.free_count[0] = min(max(fc, 0) + tot2[0], dm.NP);
+        *sc.done_compact = 0;
     }
 }
 
@@ -1117,7 +1236,7 @@ __global__ void __launch_bounds__(256) k_calib(Dims dm, View v, Scratch sc, cons
                                                unsigned long long* age_sum) {
     const int s = blockIdx.y;
     const int tok = blockIdx.x * blockDim.x + threadIdx.x;
-    const int nt = v.n_tokens[s];
+    const int nt = sc.valid[s] ? v.n_tokens[s] : 0;   // a void step adds nothing
     int key = -1;
     unsigned long long fx = 0, ag = 0;
     if (tok < nt && tok < dm.MP * dm.P) {
@@ -1178,13 +1297,13 @@ size_t scratch_bytes(const Dims& dm) {
     n += align256(spill * dm.S * dm.R * dm.max_chunks * sizeof(float2));
     n += align256((size_t)dm.S * dm.R * sizeof(float2));
     n += align256((size_t)dm.S * dm.MP * sizeof(float));
-    n += 6 * align256((size_t)(dm.S + 1) * sizeof(int32_t));
+    n += 7 * align256((size_t)(dm.S + 1) * sizeof(int32_t));
     n += align256((size_t)(1 + 3 * (dm.S + 1)) * sizeof(int32_t));
     n += align256(sizeof(int32_t));
     n += align256((1 + (size_t)kAttendPerCu * (dm.S + 1)) * sizeof(unsigned long long));
     n += align256((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long));
     n += align256((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long));
-    n += align256(2 * sizeof(int32_t));
+    n += align256(5 * sizeof(int32_t));
     n += align256(4 * sizeof(unsigned long long));
     return n;
 }
@@ -1205,6 +1324,7 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
     sc->tile_prefix = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
     sc->chunks = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
     sc->valid = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
+    sc->freed = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
     sc->score_prefix = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
     sc->ustart = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
     sc->plan = reinterpret_cast<int32_t*>(take((size_t)(1 + 3 * (dm.S + 1)) * sizeof(int32_t)));
@@ -1216,9 +1336,12 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
         take((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long)));
     sc->unorm = reinterpret_cast<unsigned long long*>(
         take((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long)));
-    int32_t* words = reinterpret_cast<int32_t*>(take(2 * sizeof(int32_t)));
+    int32_t* words = reinterpret_cast<int32_t*>(take(5 * sizeof(int32_t)));
     sc->done = words;
     sc->status = words + 1;
+    sc->warn = words + 2;
+    sc->done_compact = words + 3;
+    sc->opened = words + 4;
     sc->counters = reinterpret_cast<unsigned long long*>(take(4 * sizeof(unsigned long long)));
 }
 

@@ -13,6 +13,11 @@ Comparison rules
   or pages holding an excused token: there several answers are correct.  The
   device's own selection must in any case be the ascending-(score, serial)
   prefix of its own scores that meets the budget (checked here, in the test).
+* With strict_ties=True (inputs built so that page scores tie exactly on
+  both sides) the evicted serials must be identical: no tie band.
+* With check_free_list=True the free list is checked at every step: an
+  append takes its pages in session order off the top of the stack, and a
+  compaction pushes the freed physical ids in (session, serial) order.
 * After a comparison the oracle's discrete decisions are carried to the
   device when an excusal let them differ: the oracle's refresh clock is
   written over the device's for excused tokens, and md_compact applies the
@@ -94,7 +99,8 @@ class Pair:
                  oracle_sessions: Optional[List[int]] = None, n0s=None, budgets=None,
                  regions=None, planted: int = 0, planted_strength=3.0, query_gain=0.0,
                  pinned_mask=None, alpha=None, n_phys_extra: int = 0, max_pages=None,
-                 steps=None, fused: Optional[bool] = True):
+                 steps=None, fused: Optional[bool] = True, priors=None, strict_ties: bool = False,
+                 check_free_list: bool = False):
         self.w = w
         self.dev = torch.device(device)
         self.backend = backend
@@ -103,7 +109,10 @@ class Pair:
         S = len(self.n0s)
         assert S == w.S
         self.B = g.budgets(w, self.n0s) if budgets is None else np.asarray(budgets, np.int64)
-        self.b, self.lam = g.region_priors(w)
+        self.b, self.lam = g.region_priors(w) if priors is None else \
+            (np.asarray(priors[0], np.float32), np.asarray(priors[1], np.float32))
+        self.strict_ties = strict_ties
+        self.check_free_list = check_free_list
         self.pinned_mask = w.pinned_mask if pinned_mask is None else pinned_mask
         self.alpha = w.alpha if alpha is None else alpha
         self.oracle_sessions = list(range(S)) if oracle_sessions is None else list(oracle_sessions)
@@ -164,6 +173,7 @@ class Pair:
         self.stats = Stats()
         self.last_rec = {}
         self.status_seen = 0
+        self.warned = False        # md_read_device_status returned MD_W_BUDGET_INFEASIBLE
         self.k = 0
 
     # -------------------------------------------------------------- inputs
@@ -199,6 +209,9 @@ class Pair:
         w, P, S = self.w, self.w.P, self.w.S
         qt, nkt, regt, qo, nko, reg = self.inputs(k)
         md = self.md
+        if self.check_free_list:
+            torch.cuda.synchronize(self.dev)
+            before = self.free_list_state()
         if not g.observes(w, k):
             # a decode step without an observation: append only, on both sides
             md.observe(k, None, nkt, regt)
@@ -211,10 +224,14 @@ class Pair:
             self.stats.steps += 1
             return self.stats
         md.observe(k, qt, nkt, regt, abar_out=self.abar)
+        if self.check_free_list:
+            torch.cuda.synchronize(self.dev)
+            self.check_pops(before, self.free_list_state())
         md.score(token_score=self.tscore)
         md.select()
         torch.cuda.synchronize(self.dev)
-        dev_status = md.device_status()
+        rc, dev_status = md.device_status(with_warning=True)
+        self.warned |= rc == B.MD_W_BUDGET_INFEASIBLE
         self.status_seen |= dev_status
         assert dev_status == 0, f"step {k}: device status {dev_status:#x}"
         c = self.cache
@@ -287,6 +304,8 @@ class Pair:
             assert bool(infeas[s]) == rec.infeasible, (k, s, "infeasible")
             check_selection_prefix(gp, pser, rec.page_size, np.isinf(gp), nt, int(self.B[s]), P,
                                    g_ev, bool(infeas[s]))
+            if self.strict_ties:
+                assert g_ev.tolist() == rec.evicted.tolist(), (k, s, "evicted serials (exact ties)")
             if g_ev.tolist() != rec.evicted.tolist():
                 diff = set(g_ev.tolist()) ^ set(rec.evicted.tolist())
                 thr = max((rec.page_score[i] for i in range(npg)
@@ -304,8 +323,12 @@ class Pair:
         for slots_, vals in tref_fix:
             c.t_ref.view(-1)[torch.from_numpy(slots_).to(self.dev)] = \
                 torch.from_numpy(vals.astype(np.int32)).to(self.dev)
+        if self.check_free_list:
+            pre_compact = self.free_list_state()
         md.compact(torch.from_numpy(final_ser).to(self.dev), torch.from_numpy(final_cnt).to(self.dev))
         torch.cuda.synchronize(self.dev)
+        if self.check_free_list:
+            self.check_pushes(pre_compact, final_ser, final_cnt, self.free_list_state())
         if compare:
             n_pages = c.n_pages.cpu().numpy()
             n_tokens = self.live_counts()
@@ -346,6 +369,40 @@ class Pair:
                 assert np.array_equal(codes, want_c), (self.k, s, p.serial, "codes")
                 assert np.array_equal(scale.view(np.uint32), want_s.astype(np.float32).view(np.uint32)), \
                     (self.k, s, p.serial, "scales")
+
+    def free_list_state(self):
+        c = self.cache
+        return {"fc": int(c.free_count.item()), "free": c.free_list.cpu().numpy().copy(),
+                "np": c.n_pages.cpu().numpy().copy(), "ptab": c.page_table.cpu().numpy().copy(),
+                "pser": c.page_serial.cpu().numpy().copy()}
+
+    def check_pops(self, a, b):
+        """An append takes pages off the top of the free-list stack in
+        session order: the first session that opens a page gets the top
+        entry, the next one the entry below, and so on."""
+        fc, rank = a["fc"], 0
+        for s in range(self.w.S):
+            if b["np"][s] == a["np"][s] + 1:
+                assert b["ptab"][s, b["np"][s] - 1] == a["free"][fc - 1 - rank], (self.k, s, "pop order")
+                rank += 1
+            else:
+                assert b["np"][s] == a["np"][s], (self.k, s)
+        assert b["fc"] == fc - rank, (self.k, "free count after the append", b["fc"], fc, rank)
+
+    def check_pushes(self, a, ev_ser, ev_cnt, b):
+        """A compaction pushes the freed physical ids in (session, serial)
+        order on top of the free-list stack."""
+        want = []
+        for s in range(self.w.S):
+            ser = a["pser"][s, :a["np"][s]]
+            for x in ev_ser[s, :ev_cnt[s]]:
+                i = np.flatnonzero(ser == x)
+                assert i.size == 1, (self.k, s, int(x))
+                want.append(int(a["ptab"][s, i[0]]))
+        fc = a["fc"]
+        assert b["fc"] == fc + len(want), (self.k, "free count after the compaction")
+        assert b["free"][fc:fc + len(want)].tolist() == want, (self.k, "push order")
+        assert np.array_equal(b["free"][:fc], a["free"][:fc]), (self.k, "entries below untouched")
 
     def live_counts(self) -> np.ndarray:
         """|K_t| per session on the device: n_live with region-aligned pages."""

@@ -82,6 +82,82 @@ def test_nonfinite_query_sets_status():
     p.close()
 
 
+@pytest.mark.parametrize("fused", [True, False])
+def test_nonfinite_query_voids_the_sessions_step(fused):
+    # Two sessions of 450 tokens with a budget of 225: the first observation
+    # would evict about half of each.  Session 0's query holds a NaN: its step
+    # is void (nothing selected, compacted or quantised; importance and
+    # refresh clocks as before; the append stands), while session 1 evicts as
+    # usual.  The next step, with a finite query, evicts session 0 too.
+    w = C.with_overrides(C.get("small"), S=2, n0=None, n0_range=(1, 2), steps=8)
+    p = Pair(w, n0s=[450, 450], budgets=[225, 225], oracle_sessions=[], fused=fused)
+    c = p.cache
+    slots0 = (c.page_table[0, :int(c.n_pages[0])].long().view(-1, 1) * 16 +
+              torch.arange(16, device=c.page_table.device).view(1, -1)).view(-1)[:450]
+    imp0, tref0 = c.importance.view(-1)[slots0].clone(), c.t_ref.view(-1)[slots0].clone()
+    np0, ptab0 = int(c.n_pages[0]), c.page_table[0].clone()
+    q, nk, reg, *_ = p.inputs(1)
+    q[0, 0, 0, 3, 17] = float("nan")
+    p.md.observe(1, q, nk, reg)
+    p.md.score()
+    p.md.select()
+    p.md.compact()
+    torch.cuda.synchronize()
+    assert p.md.device_status() == B.MD_DEV_NONFINITE
+    cnt = p.md.evict_count.cpu().tolist()
+    assert cnt[0] == 0 and cnt[1] > 0
+    assert int(c.n_pages[0]) == np0 and torch.equal(c.page_table[0], ptab0)
+    assert int(c.n_tokens[0]) == 451                      # the append stands
+    assert torch.equal(c.importance.view(-1)[slots0].view(torch.int32), imp0.view(torch.int32))
+    assert torch.equal(c.t_ref.view(-1)[slots0], tref0)
+    assert int(c.n_tokens[1]) <= 225
+    q, nk, reg, *_ = p.inputs(2)
+    p.md.observe(2, q, nk, reg)
+    p.md.score()
+    p.md.select()
+    p.md.compact()
+    torch.cuda.synchronize()
+    assert p.md.device_status() == 0
+    assert p.md.evict_count.cpu().tolist()[0] > 0 and int(c.n_tokens[0]) <= 225
+    p.close()
+
+
+def test_compact_applies_this_steps_selection():
+    # md_compact with NULL lists applies the lists of this step's
+    # md_select_evict; without a selection since the observation it is out
+    # of order, and one list without the other is invalid.
+    p = small_pair(oracle_sessions=[], n0s=[450], budgets=[225])
+    md = p.md
+    q, nk, reg, *_ = p.inputs(1)
+    md.observe(1, q, nk, reg)
+    md.score()
+    with pytest.raises(B.MemDecayError) as e:
+        md.compact()
+    assert e.value.status == B.MD_E_STATE
+    with pytest.raises(B.MemDecayError) as e:
+        B.md_compact(md.handle, md.evict_serial.data_ptr(), None)
+    assert e.value.status == B.MD_E_INVALID
+    md.select()
+    md.compact()
+    torch.cuda.synchronize()
+    n_after = int(p.cache.n_tokens[0])
+    cnt = int(md.evict_count[0])
+    assert cnt > 0 and 225 - 16 < n_after <= 225
+    q, nk, reg, *_ = p.inputs(2)
+    md.observe(2, q, nk, reg)
+    md.score()
+    md.select()
+    with pytest.raises(B.MemDecayError) as e:
+        B.md_compact(md.handle, md.evict_serial.data_ptr(), None)
+    md.compact(md.evict_serial, md.evict_count)         # explicit lists still work
+    with pytest.raises(B.MemDecayError) as e:
+        md.compact()                                      # the selection was applied
+    assert e.value.status == B.MD_E_STATE
+    torch.cuda.synchronize()
+    assert md.device_status() == 0
+    p.close()
+
+
 def test_bad_eviction_serial_sets_status():
     p = small_pair(oracle_sessions=[])
     q, nk, reg, *_ = p.inputs(1)

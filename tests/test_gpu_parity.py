@@ -95,7 +95,9 @@ def test_group_sizes(Hq, Hkv):
 
 def test_no_pinning_zero_alpha():
     w = C.with_overrides(C.get("small"), steps=20)
-    run_pair(Pair(w, pinned_mask=0, alpha=0.0), 20, "unpinned-alpha0")
+    p = Pair(w, pinned_mask=0, alpha=0.0)
+    run_pair(p, 20, "unpinned-alpha0")
+    assert not p.warned
 
 
 def test_infeasible_budget():
@@ -104,6 +106,7 @@ def test_infeasible_budget():
     p.step()
     inf = p.md.infeasible.cpu().numpy()
     assert inf.tolist() == [1, 0, 1]
+    assert p.warned          # md_read_device_status returned MD_W_BUDGET_INFEASIBLE
     run_pair(p, 9, "infeasible")
 
 
@@ -479,3 +482,100 @@ def test_quantised_tier_long32k_sampled_sessions():
     w = C.with_overrides(C.get("long32k"), quant_threshold=0.3)
     p = Pair(w, backend="torch", oracle_sessions=[0, 11], steps=6, fused=True)
     assert run_quant(p, 3, "quant-long32k") > 0
+
+
+# ---------------------------------------------------------------- exact ties
+
+def flat_priors(w, b_of_region):
+    """Region tables with lambda = 0 (no decay): a token scores b of its
+    region exactly when alpha = 0."""
+    b = np.zeros((w.S, 7), np.float32)
+    for r, v in b_of_region.items():
+        b[:, r] = v
+    return b, np.zeros((w.S, 7), np.float32)
+
+
+@pytest.mark.parametrize("fused", [True, False])
+@pytest.mark.parametrize("P", [16, 64])
+def test_exact_ties_go_to_the_older_page(P, fused):
+    # lambda = 0, alpha = 0 and b = 0.5 for every movable region: every
+    # unpinned page scores exactly 0.5 on both sides (sums of 0.5 and their
+    # quotients by the member count are exact in float32), so the eviction
+    # is decided by serial alone, the older page first (the min-heap order
+    # read as ascending (S_p, serial)).  With 20,000 tokens at P = 16 a
+    # session holds 1,250 pages, more than the selection's 1,024 threads, so
+    # the walk over the pages of the threshold key crosses thread runs.  The
+    # evicted serials must equal the oracle's exactly.
+    w = C.with_overrides(C.get("small"), S=3, n0=None, n0_range=(1, 2), P=P, system_len=64,
+                         mean_span=512.0, steps=6, append_cycle=C.APPEND_CYCLE)
+    b, lam = flat_priors(w, {r: 0.5 for r in range(1, 7)} | {0: 1.0})
+    p = Pair(w, n0s=[20000, 17001, 3000], budgets=[10000, 4000, 2999], priors=(b, lam), alpha=0.0,
+             strict_ties=True, fused=fused)
+    st = run_pair(p, 6, f"exact-ties-P{P}-fused{int(fused)}")
+    assert st.evicted_pages > 500 // (P // 16) and st.tie_excused == 0
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_exact_ties_on_region_aligned_pages_below_and_at_the_threshold(fused):
+    # Region-aligned pages hold one region each, so a page scores its
+    # region's b exactly: 0.25 for plan, tool_in and retrieval, 0.5 for the
+    # others.  The bulk eviction takes every 0.25 page, then 0.5 pages in
+    # serial order until the budget holds.
+    w = C.with_overrides(C.get("small"), S=2, n0=None, n0_range=(1, 2), system_len=64, mean_span=300.0,
+                         steps=6, append_cycle=C.APPEND_CYCLE, region_aligned=True, append_run=2)
+    b, lam = flat_priors(w, {0: 1.0, 1: 0.25, 2: 0.5, 3: 0.25, 4: 0.5, 5: 0.25, 6: 0.5})
+    p = Pair(w, n0s=[18000, 9000], budgets=[5000, 4500], priors=(b, lam), alpha=0.0, strict_ties=True,
+             fused=fused)
+    st = run_pair(p, 6, f"exact-ties-aligned-fused{int(fused)}")
+    assert st.evicted_pages > 500 and st.tie_excused == 0
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_region_aligned_closed_page_stays_closed(fused):
+    # 16 system and 5 plan tokens.  Step 1 appends a user token (b = 0): it
+    # closes the plan page, opens its own page and is evicted at once.  Step 2
+    # appends a plan token: the plan page is the last page again but stays
+    # closed, so the token opens a fresh page (serial 3); the tie between the
+    # two plan pages (both score 1) then evicts the older one.
+    from synth.configs import PLAN, USER
+    w = C.with_overrides(C.get("small"), n0=21, system_len=16, region_aligned=True, append_cycle=(USER, PLAN),
+                         append_run=1, steps=4)
+    b, lam = flat_priors(w, {0: 1.0, PLAN: 1.0, USER: 0.0, 3: 1.0, 4: 1.0, 5: 1.0, 6: 1.0})
+    p = Pair(w, regions=[np.array([0] * 16 + [PLAN] * 5, np.uint8)], budgets=[21], priors=(b, lam),
+             alpha=0.0, strict_ties=True, fused=fused)
+    p.step()
+    assert p.cache.page_serial[0, :int(p.cache.n_pages[0])].tolist() == [0, 1]
+    p.step()
+    assert p.cache.page_serial[0, :int(p.cache.n_pages[0])].tolist() == [0, 3]
+    run_pair(p, 2, f"aligned-closed-page-fused{int(fused)}")
+
+
+# ---------------------------------------------------------------- free list
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_free_list_order(fused):
+    # 12 sessions: each append takes pages off the top of the free list in
+    # session order, and each compaction pushes the freed ids in (session,
+    # serial) order; the harness checks both at every step.
+    w = C.with_overrides(C.get("qwen3_32x1700"), L=2, S=12, steps=24)
+    p = Pair(w, oracle_sessions=[0, 7], check_free_list=True, fused=fused)
+    run_pair(p, 24, f"free-list-order-fused{int(fused)}")
+
+
+def test_physical_pages_are_reproducible():
+    # Two runs of the same batch hand out the same physical pages.
+    w = C.with_overrides(C.get("qwen3_32x1700"), L=2, S=10, steps=20)
+    runs = []
+    for _ in range(2):
+        p = Pair(w, oracle_sessions=[])
+        tabs = []
+        for _ in range(20):
+            p.step(compare=False)
+            c = p.cache
+            tabs.append((c.page_table.cpu().numpy().copy(), c.free_list.cpu().numpy().copy(),
+                         int(c.free_count.item())))
+        assert p.device_status() == 0
+        runs.append(tabs)
+        p.close()
+    for (t1, f1, c1), (t2, f2, c2) in zip(*runs):
+        assert np.array_equal(t1, t2) and c1 == c2 and np.array_equal(f1[:c1], f2[:c2])
