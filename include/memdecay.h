@@ -87,6 +87,8 @@ enum {
     MD_E_HIP = -4,          /* a HIP runtime call failed                        */
     MD_E_STATE = -5,        /* call out of order (e.g. select before score)     */
     MD_E_NOMEM = -6,        /* scratch allocation failed in md_init             */
+    MD_E_TOO_LARGE = -7,    /* md_init_static: the scratch exceeds its static   */
+                            /* array, or every static handle is in use          */
     MD_W_BUDGET_INFEASIBLE = 1  /* warning (md_read_device_status): some        */
                             /* selection found a session whose pinned tokens   */
                             /* alone exceed its budget (Eq. 1 has no feasible  */
@@ -205,6 +207,28 @@ const char* md_status_str(md_status s);
  */
 md_status md_init(const md_config* cfg, const md_region_params* rp,
                   const md_cache_view* cv, void* stream, md_handle* out);
+
+/*
+ * md_init_static — md_init that allocates nothing, for callers that cannot
+ * allocate memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The handle's scratch is a file-scope
+ * device array of 128 MiB inside the library instead of an allocation: one
+ * array per device, held by the device from the library's first use on it
+ * until the process ends.  The scratch a configuration needs is mostly the
+ * fused kernel's statistics, 16 bytes per softmax row (L Hq W) and 256-token
+ * unit of the pool, plus, when the multi-kernel path can run, the logits of
+ * every pool slot (4 L Hq W bytes each); a configuration that needs more than
+ * 128 MiB gets MD_E_TOO_LARGE.  The handle itself is one of 16 static slots
+ * (MD_E_TOO_LARGE when all are taken; md_destroy gives it back).
+ * md_init_static clears the part of the array the handle uses (the array
+ * keeps whatever the previous static handle left there).  Every static
+ * handle on a device uses that device's one array, so two static handles
+ * alive on one device at once overwrite each other's scratch and their calls
+ * race: keep one static handle per device at a time.  Arguments, checks,
+ * synchronisation and the calls that follow are those of md_init.
+ */
+md_status md_init_static(const md_config* cfg, const md_region_params* rp, const md_cache_view* cv,
+                         void* stream, md_handle* out);
 
 /*
  * md_observe_step — one decode step; with q given, also an observation step

@@ -18,6 +18,7 @@ MD_E_STEP = -3
 MD_E_HIP = -4
 MD_E_STATE = -5
 MD_E_NOMEM = -6
+MD_E_TOO_LARGE = -7
 MD_W_BUDGET_INFEASIBLE = 1
 
 MD_DEV_CAPACITY = 0x1
@@ -32,7 +33,7 @@ MD_FLAG_NORM_ATTENTION = 0x4
 MD_FLAG_REGION_ALIGNED = 0x8
 MD_REGION_HOLE = 0xFF
 
-EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_observe_step",
+EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_init_static", "md_observe_step",
            "md_score_pages", "md_select_evict", "md_compact", "md_read_device_status",
            "md_profile_enable", "md_profile_read", "md_read_counters", "md_kernel_config",
            "md_calib_accumulate", "md_calib_fit",
@@ -116,6 +117,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.md_init.restype = i32
     lib.md_init.argtypes = [ctypes.POINTER(md_config), ctypes.POINTER(md_region_params),
                             ctypes.POINTER(md_cache_view), vp, ctypes.POINTER(vp)]
+    lib.md_init_static.restype = i32
+    lib.md_init_static.argtypes = [ctypes.POINTER(md_config), ctypes.POINTER(md_region_params),
+                                   ctypes.POINTER(md_cache_view), vp, ctypes.POINTER(vp)]
     lib.md_observe_step.restype = i32
     lib.md_observe_step.argtypes = [vp, i32, vp, vp, vp, vp]
     lib.md_score_pages.restype = i32
@@ -159,17 +163,25 @@ def md_status_str(status: int) -> str:
     return load_library().md_status_str(status).decode()
 
 
-def md_init_raw(cfg: md_config, rp: md_region_params, cv: md_cache_view, stream: int):
-    """Returns (status, handle or None) without raising."""
+def md_init_raw(cfg: md_config, rp: md_region_params, cv: md_cache_view, stream: int,
+                static: bool = False):
+    """Returns (status, handle or None) without raising; static=True calls
+    md_init_static."""
     h = ctypes.c_void_p()
-    st = load_library().md_init(ctypes.byref(cfg), ctypes.byref(rp), ctypes.byref(cv),
-                                ctypes.c_void_p(stream), ctypes.byref(h))
+    fn = load_library().md_init_static if static else load_library().md_init
+    st = fn(ctypes.byref(cfg), ctypes.byref(rp), ctypes.byref(cv), ctypes.c_void_p(stream), ctypes.byref(h))
     return st, (h.value if st == MD_OK else None)
 
 
 def md_init(cfg: md_config, rp: md_region_params, cv: md_cache_view, stream: int) -> int:
     st, h = md_init_raw(cfg, rp, cv, stream)
     _check("md_init", st)
+    return h
+
+
+def md_init_static(cfg: md_config, rp: md_region_params, cv: md_cache_view, stream: int) -> int:
+    st, h = md_init_raw(cfg, rp, cv, stream, static=True)
+    _check("md_init_static", st)
     return h
 
 

@@ -158,7 +158,7 @@ class MemDecay:
                  rho: float, alpha: float, tau_scale: float, pinned_mask: int,
                  n_regions: int = 7, stream: Optional[torch.cuda.Stream] = None,
                  fused: Optional[bool] = None, attention_norm: bool = False, window: int = 1,
-                 region_aligned: bool = False, quant_threshold: float = 0.0):
+                 region_aligned: bool = False, quant_threshold: float = 0.0, static: bool = False):
         # fused: True = always the fused kernel, False = always the
         # multi-kernel path, None = the library picks from the cache's sizes
         self.cache = cache
@@ -177,7 +177,9 @@ class MemDecay:
         rp = B.md_region_params(base_priority=self.b.data_ptr(), decay_rate=self.lam.data_ptr())
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
         self._cfg, self._rp, self._cv = cfg, rp, cache.view()
-        self.handle = B.md_init(cfg, rp, self._cv, self.stream.cuda_stream)
+        # static: md_init_static (the library's static scratch, no allocation)
+        init = B.md_init_static if static else B.md_init
+        self.handle = init(cfg, rp, self._cv, self.stream.cuda_stream)
         S, MP = cache.S, cache.max_pages
         self.page_score = torch.zeros((S, MP), dtype=torch.float32, device=dev)
         self.evict_serial = torch.zeros((S, MP), dtype=torch.int32, device=dev)

@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <new>
 #include <vector>
 
@@ -47,9 +48,40 @@ struct md_handle_s {
     uint32_t profile_mask;
     std::vector<Timed> pending[MD_K_COUNT];   // launches not yet read back
     std::vector<Timed> spare;                  // recycled event pairs
+    int static_slot;     // md_init_static: index in the static handles; -1 otherwise
 };
 
 namespace {
+
+// Handles of md_init_static live here, so that it allocates no host memory
+// either; a slot is taken by md_init_static and given back by md_destroy.
+constexpr int kStaticHandles = 16;
+md_handle_s g_static_handles[kStaticHandles];
+std::atomic<bool> g_static_taken[kStaticHandles];
+
+md_handle_s* take_static_handle() {
+    for (int i = 0; i < kStaticHandles; ++i) {
+        bool expect = false;
+        if (g_static_taken[i].compare_exchange_strong(expect, true)) {
+            md_handle_s* h = &g_static_handles[i];
+            h->static_slot = i;
+            return h;
+        }
+    }
+    return nullptr;
+}
+
+void give_back(md_handle_s* h) {
+    if (h->static_slot < 0) {
+        delete h;
+        return;
+    }
+    const int i = h->static_slot;
+    for (auto& v : h->pending) v.clear();
+    h->spare.clear();
+    h->profile_mask = 0;
+    g_static_taken[i].store(false);
+}
 
 // Launch through `fn`, bracketed by an event pair when kernel `id` is timed.
 template <typename F>
@@ -102,6 +134,8 @@ const char* md_status_str(md_status s) {
         case MD_E_STATE: return "call out of order (score needs an observe, select needs a score, "
                                 "and neither may follow a compact before the next observe)";
         case MD_E_NOMEM: return "could not allocate the library scratch";
+        case MD_E_TOO_LARGE: return "the handle's scratch exceeds md_init_static's static scratch (128 MiB), "
+                                    "or all 16 static handles are in use";
         case MD_W_BUDGET_INFEASIBLE: return "warning: a session's pinned tokens exceed its budget";
         default: return "unknown status";
     }
@@ -159,8 +193,10 @@ static md_status validate_view(const md_cache_view* v, bool region_aligned, bool
     return MD_OK;
 }
 
-md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cache_view* cv,
-                  void* stream, md_handle* out) {
+// md_init and md_init_static: use_static takes the scratch from the
+// library's static device array and the handle from the static handles.
+static md_status init_handle(const md_config* cfg, const md_region_params* rp, const md_cache_view* cv,
+                             void* stream, md_handle* out, bool use_static) {
     if (out == nullptr) return MD_E_INVALID;
     *out = nullptr;
     md_status st = validate_config(cfg);
@@ -204,15 +240,26 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) return MD_E_UNSUPPORTED;
     hipStream_t hs = static_cast<hipStream_t>(stream);
 
-    // Region priors: b_r >= 0, lambda_r >= 0, finite (Sec. III-B).
+    // Region priors: b_r >= 0, lambda_r >= 0, finite (Sec. III-B); read in
+    // chunks through buffers on the stack.
     const size_t nrp = (size_t)dm.S * dm.n_regions;
-    std::vector<float> hb(nrp), hl(nrp);
-    if (hipMemcpyAsync(hb.data(), rp->base_priority, nrp * sizeof(float), hipMemcpyDeviceToHost, hs) != hipSuccess ||
-        hipMemcpyAsync(hl.data(), rp->decay_rate, nrp * sizeof(float), hipMemcpyDeviceToHost, hs) != hipSuccess ||
-        hipStreamSynchronize(hs) != hipSuccess)
-        return MD_E_HIP;
-    for (size_t i = 0; i < nrp; ++i)
-        if (!(hb[i] >= 0.0f) || !isfinite(hb[i]) || !(hl[i] >= 0.0f) || !isfinite(hl[i])) return MD_E_INVALID;
+    {
+        constexpr size_t kChunkN = 2048;
+        float hb[kChunkN], hl[kChunkN];
+        for (size_t o = 0; o < nrp; o += kChunkN) {
+            const size_t n = std::min(kChunkN, nrp - o);
+            if (hipMemcpyAsync(hb, rp->base_priority + o, n * sizeof(float), hipMemcpyDeviceToHost, hs) !=
+                    hipSuccess ||
+                hipMemcpyAsync(hl, rp->decay_rate + o, n * sizeof(float), hipMemcpyDeviceToHost, hs) != hipSuccess ||
+                hipStreamSynchronize(hs) != hipSuccess)
+                return MD_E_HIP;
+            for (size_t i = 0; i < n; ++i)
+                if (!(hb[i] >= 0.0f) || !isfinite(hb[i]) || !(hl[i] >= 0.0f) || !isfinite(hl[i]))
+                    return MD_E_INVALID;
+        }
+    }
+    void* static_base = nullptr;
+    if (use_static && md::static_scratch(&static_base) != hipSuccess) return MD_E_HIP;
 
     // Fused observation kernel: up to kAttendPerCu workgroups per CU, as
     // many as its LDS and registers allow; md_init then checks on the device
@@ -244,8 +291,8 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     // be resident together: check it on the device, and step the grid down
     // one workgroup per CU at a time until every workgroup arrives.
     if (dm.fused) {
-        int32_t* probe = nullptr;
-        if (hipMalloc(&probe, 2 * sizeof(int32_t)) != hipSuccess) return MD_E_NOMEM;
+        int32_t* probe = static_cast<int32_t*>(static_base);   // the static scratch is free until carved
+        if (!use_static && hipMalloc(&probe, 2 * sizeof(int32_t)) != hipSuccess) return MD_E_NOMEM;
         int verified = 0;
         for (int o = occ; o >= 1 && verified == 0; --o) {
             int32_t seen[2] = {0, 0};
@@ -257,7 +304,7 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
             }
             if (seen[1] >= o * n_cu) verified = o * n_cu;
         }
-        (void)hipFree(probe);
+        if (!use_static) (void)hipFree(probe);
         dm.n_wg = verified;
         dm.wg_per_cu = verified / n_cu;
         dm.lane_cap = n_cu;
@@ -275,9 +322,9 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     // the budget).
     bool fused_first = dm.fused, fused_steady = dm.fused;
     if (dm.fused && !(cfg->flags & MD_FLAG_FUSED)) {
-        std::vector<int32_t> hn(dm.S), hbud(dm.S);
-        if (hipMemcpyAsync(hn.data(), cv->n_tokens, dm.S * sizeof(int32_t), hipMemcpyDeviceToHost, hs) != hipSuccess ||
-            hipMemcpyAsync(hbud.data(), cv->budget, dm.S * sizeof(int32_t), hipMemcpyDeviceToHost, hs) !=
+        int32_t hn[md::kMaxSessions], hbud[md::kMaxSessions];
+        if (hipMemcpyAsync(hn, cv->n_tokens, dm.S * sizeof(int32_t), hipMemcpyDeviceToHost, hs) != hipSuccess ||
+            hipMemcpyAsync(hbud, cv->budget, dm.S * sizeof(int32_t), hipMemcpyDeviceToHost, hs) !=
                 hipSuccess ||
             hipStreamSynchronize(hs) != hipSuccess)
             return MD_E_HIP;
@@ -293,8 +340,11 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     }
     dm.multi = dm.spill || !fused_first || !fused_steady;
 
-    md_handle_s* h = new (std::nothrow) md_handle_s();
-    if (h == nullptr) return MD_E_NOMEM;
+    const size_t bytes = md::scratch_bytes(dm);
+    if (use_static && bytes > md::kStaticScratchBytes) return MD_E_TOO_LARGE;
+    md_handle_s* h = use_static ? take_static_handle() : new (std::nothrow) md_handle_s();
+    if (h == nullptr) return use_static ? MD_E_TOO_LARGE : MD_E_NOMEM;
+    if (!use_static) h->static_slot = -1;
     h->dm = dm;
     h->v.k_pool = cv->k_pool;
     h->v.region = cv->region;
@@ -317,17 +367,19 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     h->stream = hs;
     h->device = dev;
 
-    const size_t bytes = md::scratch_bytes(dm);
-    if (hipMalloc(&h->scratch, bytes) != hipSuccess) {
-        delete h;
+    if (use_static) {
+        h->scratch = static_base;
+    } else if (hipMalloc(&h->scratch, bytes) != hipSuccess) {
+        give_back(h);
         return MD_E_NOMEM;
     }
     md::scratch_carve(dm, h->scratch, &h->sc);
     // counters, status, epoch and the tagged unit statistics start at zero
-    // (no step's tag is zero); work lists are empty until the first append
+    // (no step's tag is zero); work lists are empty until the first append.
+    // The static scratch keeps what its last handle left there: cleared too.
     if (hipMemsetAsync(h->scratch, 0, bytes, hs) != hipSuccess || hipStreamSynchronize(hs) != hipSuccess) {
-        (void)hipFree(h->scratch);
-        delete h;
+        if (!use_static) (void)hipFree(h->scratch);
+        give_back(h);
         return MD_E_HIP;
     }
     h->logits_blocks = 3 * n_cu;
@@ -345,6 +397,16 @@ md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cac
     h->profile_mask = 0;
     *out = h;
     return MD_OK;
+}
+
+md_status md_init(const md_config* cfg, const md_region_params* rp, const md_cache_view* cv,
+                  void* stream, md_handle* out) {
+    return init_handle(cfg, rp, cv, stream, out, false);
+}
+
+md_status md_init_static(const md_config* cfg, const md_region_params* rp, const md_cache_view* cv,
+                         void* stream, md_handle* out) {
+    return init_handle(cfg, rp, cv, stream, out, true);
 }
 
 md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint16_t* new_k,
@@ -578,8 +640,8 @@ md_status md_destroy(md_handle h) {
     md_status st = MD_OK;
     if (hipSetDevice(h->device) != hipSuccess || hipStreamSynchronize(h->stream) != hipSuccess) st = MD_E_HIP;
     release_events(h);
-    if (hipFree(h->scratch) != hipSuccess) st = MD_E_HIP;
-    delete h;
+    if (h->static_slot < 0 && hipFree(h->scratch) != hipSuccess) st = MD_E_HIP;
+    give_back(h);
     return st;
 }
 

@@ -100,6 +100,13 @@ struct Scratch {
 size_t scratch_bytes(const Dims& dm);
 void scratch_carve(const Dims& dm, void* base, Scratch* sc);
 
+// md_init_static: the library's scratch in a file-scope device array of this
+// size (one per device, held until the process ends) instead of an
+// allocation.  static_scratch gives its address on the current device,
+// looked up once per device.
+constexpr size_t kStaticScratchBytes = (size_t)128 << 20;
+hipError_t static_scratch(void** ptr);
+
 // Launchers; each returns the hipError_t of its launch.
 // fused: this step observes on the fused kernel (sessions that fit a pass)
 // or, when 0, every session on the multi-kernel path.  observe: 0 for a

@@ -17,9 +17,36 @@
 //   k_compact   one block per session: page-table compaction, free-list push.
 // Every reduction is in a fixed order; no float atomics are used.
 
+#include <mutex>
+
 #include "md_device.h"
 
 namespace md {
+
+// Scratch of handles made by md_init_static, for callers that cannot
+// allocate device memory.  Host code must not pass the array's name to a
+// kernel or a copy (it stands for the host-side shadow); static_scratch
+// hands out the device address instead.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+hipError_t static_scratch(void** ptr) {
+    constexpr int kMaxDevices = 64;
+    static void* addr[kMaxDevices];   // device address of the array, per device
+    static std::mutex mu;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (addr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
 
 // ---------------------------------------------------------------- append
 

@@ -100,7 +100,7 @@ class Pair:
                  regions=None, planted: int = 0, planted_strength=3.0, query_gain=0.0,
                  pinned_mask=None, alpha=None, n_phys_extra: int = 0, max_pages=None,
                  steps=None, fused: Optional[bool] = True, priors=None, strict_ties: bool = False,
-                 check_free_list: bool = False):
+                 check_free_list: bool = False, static: bool = False):
         self.w = w
         self.dev = torch.device(device)
         self.backend = backend
@@ -166,7 +166,8 @@ class Pair:
         self.md = MemDecay(self.cache, torch.from_numpy(self.b), torch.from_numpy(self.lam),
                            rho=f32(w.rho), alpha=f32(self.alpha), tau_scale=f32(w.tau_scale),
                            pinned_mask=self.pinned_mask, fused=fused, attention_norm=w.attention_norm,
-                           window=w.window, region_aligned=al, quant_threshold=w.quant_threshold)
+                           window=w.window, region_aligned=al, quant_threshold=w.quant_threshold,
+                           static=static)
         n_slots = n_phys * P
         self.abar = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
         self.tscore = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
