@@ -32,6 +32,7 @@ import numpy as np
 import torch
 
 import oracle
+from oracle.pool import SessionPool
 from paper_2607_10582_amd import binding as B
 from paper_2607_10582_amd.cache import MemDecay, PagedCache
 from synth import configs as C
@@ -100,7 +101,9 @@ class Pair:
                  regions=None, planted: int = 0, planted_strength=3.0, query_gain=0.0,
                  pinned_mask=None, alpha=None, n_phys_extra: int = 0, max_pages=None,
                  steps=None, fused: Optional[bool] = True, priors=None, strict_ties: bool = False,
-                 check_free_list: bool = False, static: bool = False):
+                 check_free_list: bool = False, static: bool = False, pool: int = 0):
+        # pool > 0: the oracle sessions run in that many worker processes
+        # (oracle.pool), all sessions of a step at once
         self.w = w
         self.dev = torch.device(device)
         self.backend = backend
@@ -132,6 +135,7 @@ class Pair:
         perm = g.page_permutation(w, n_phys)
         pos = 0
         self.oracles: Dict[int, oracle.Session] = {}
+        self.pool = SessionPool(pool) if pool else None
         for s in range(S):
             n0 = int(self.n0s[s])
             reg = regs[s]
@@ -155,13 +159,17 @@ class Pair:
                 self.cache.clock[s] = 0
             del kt
             if s in self.oracle_sessions:
-                self.oracles[s] = oracle.Session(
-                    L=w.L, Hq=w.Hq, Hkv=w.Hkv, d=w.d, P=P, b=self.b[s], lam=self.lam[s],
-                    alpha=f32(self.alpha), rho=f32(w.rho), tau_scale=f32(w.tau_scale),
-                    pinned_mask=self.pinned_mask, budget=int(self.B[s]), clock=n0, region=reg,
-                    keys_bits=kb if n0 else np.zeros((0, w.L, w.Hkv, w.d), np.uint16),
-                    capacity=n0 + self.steps, attention_norm=w.attention_norm, region_aligned=al,
-                    quant_threshold=w.quant_threshold)
+                kw = dict(L=w.L, Hq=w.Hq, Hkv=w.Hkv, d=w.d, P=P, b=self.b[s], lam=self.lam[s],
+                          alpha=f32(self.alpha), rho=f32(w.rho), tau_scale=f32(w.tau_scale),
+                          pinned_mask=self.pinned_mask, budget=int(self.B[s]), clock=n0, region=reg,
+                          capacity=n0 + self.steps, attention_norm=w.attention_norm, region_aligned=al,
+                          quant_threshold=w.quant_threshold)
+                kbs = kb if n0 else np.zeros((0, w.L, w.Hkv, w.d), np.uint16)
+                if self.pool is not None:
+                    self.pool.add(s, kw, kbs, n0)
+                else:
+                    self.oracles[s] = oracle.Session(keys_bits=kbs, **kw)
+            del kb
         self.cache.set_free_pages(perm[pos:][::-1])
         self.md = MemDecay(self.cache, torch.from_numpy(self.b), torch.from_numpy(self.lam),
                            rho=f32(w.rho), alpha=f32(self.alpha), tau_scale=f32(w.tau_scale),
@@ -198,7 +206,8 @@ class Pair:
                               torch.zeros((S, w.L, w.Hq, w.d), device=self.dev)
                               for j in range(w.window)], dim=1).contiguous()
             nkt = g.torch_append_keys(w, k, self.dev)
-            qo = {s: qt[s].cpu().numpy() for s in self.oracle_sessions}
+            qh = qt.cpu().numpy()
+            qo = {s: qh[s] for s in self.oracle_sessions}
             nb = torch_to_bits(nkt)
             nko = {s: nb[s] for s in self.oracle_sessions}
         return qt, nkt, torch.from_numpy(reg).to(self.dev), qo, nko, reg
@@ -218,8 +227,9 @@ class Pair:
             md.observe(k, None, nkt, regt)
             torch.cuda.synchronize(self.dev)
             nt_dev = self.live_counts()
+            recs = self.oracle_step({s: (None, nko[s], int(reg[s])) for s in self.oracle_sessions})
             for s in self.oracle_sessions:
-                rec = self.oracles[s].step(None, nko[s], int(reg[s]))
+                rec = recs[s]
                 if compare:
                     assert int(nt_dev[s]) == rec.n, (k, s, "append-only n")
             self.stats.steps += 1
@@ -248,9 +258,11 @@ class Pair:
         final_ser = ev_ser.copy()
         final_cnt = ev_cnt.copy()
         tref_fix = []
-        quant_before = {s: {p.serial for p in self.oracles[s].pages if p.quant} for s in self.oracle_sessions}
+        quant_before = {s: {p.serial for p in self.oracles[s].pages if p.quant}
+                        for s in self.oracle_sessions} if w.quant_threshold > 0 else {}
+        recs = self.oracle_step({s: (qo[s], nko[s], int(reg[s])) for s in self.oracle_sessions})
         for s in self.oracle_sessions:
-            rec = self.oracles[s].step(qo[s], nko[s], int(reg[s]))
+            rec = recs[s]
             self.last_rec[s] = rec
             if not compare:
                 continue
@@ -335,9 +347,10 @@ class Pair:
             n_tokens = self.live_counts()
             pser = c.page_serial.cpu().numpy()
             for s in self.oracle_sessions:
-                o = self.oracles[s]
-                assert int(n_tokens[s]) == o.n_tokens(), (k, s, "n after compaction")
-                assert pser[s, :n_pages[s]].tolist() == [p.serial for p in o.pages], (k, s)
+                rec = recs[s]
+                gone = set(rec.evicted.tolist())
+                assert int(n_tokens[s]) == rec.n_after, (k, s, "n after compaction")
+                assert pser[s, :n_pages[s]].tolist() == [x for x in rec.page_serial.tolist() if x not in gone], (k, s)
                 if w.quant_threshold > 0:
                     self.check_quantised(s, quant_before[s])
         self.stats.steps += 1
@@ -370,6 +383,13 @@ class Pair:
                 assert np.array_equal(codes, want_c), (self.k, s, p.serial, "codes")
                 assert np.array_equal(scale.view(np.uint32), want_s.astype(np.float32).view(np.uint32)), \
                     (self.k, s, p.serial, "scales")
+
+    def oracle_step(self, inputs):
+        """One oracle step of the given sessions: {s: (q, new_key_bits,
+        new_region)} -> {s: StepRecord}."""
+        if self.pool is not None:
+            return self.pool.step(inputs)
+        return {s: self.oracles[s].step(*inp) for s, inp in inputs.items()}
 
     def free_list_state(self):
         c = self.cache
@@ -437,3 +457,6 @@ class Pair:
 
     def close(self):
         self.md.close()
+        if self.pool is not None:
+            self.pool.close()
+            self.pool = None
