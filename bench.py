@@ -5,21 +5,31 @@ A step is the whole path over one batch: md_observe_step (append, attention
 mass, EWMA, refresh, and on the fused kernel also the token and page scores),
 md_score_pages (here with no outputs requested, so it adds no work),
 md_select_evict (budgeted page selection) and md_compact (page-table
-compaction).  All inputs
-(the paged key cache, every step's queries and appended keys) are resident in
-HBM before timing starts.  The default workload is 16 sessions of 32,768
-cached tokens with Qwen2.5-1.5B's attention shape (28 layers, 12 query / 2 KV
-heads, d = 128), 16-token pages and a 25 % budget.  The warm-up steps include
-the first step's bulk eviction (32,768 -> 8,192 tokens per session); the
-timed steps are the steady state that follows.
+compaction).  All inputs (the paged key cache, every step's queries and
+appended keys) are resident in HBM before timing starts.
 
-Printed on stdout: one JSON line.  value = tokens scored per second (the
-sum over sessions and timed steps of the cached tokens scored, divided by
-the wall time of the timed steps); roofline = the dominant kernel's (the
-fused attention-mass kernel, or the attention-logits kernel of the
-multi-kernel path) algorithmic bytes per launch over its event-timed average
-duration, against MI355X's 8 TB/s; cpu_baseline = the CPU oracle on one session of the same
-workload.
+The default workload is the ragged batch: 64 agent sessions of U[2,048,
+65,536] cached tokens with Qwen2.5-3B's attention shape (36 layers, 16 query
+/ 2 KV heads, d = 128), 16-token pages and a 20 % budget, 64 decode steps.
+The same run also measures the ragged batch with 64-token pages and the
+long-horizon batch (16 sessions x 32,768 tokens, 1.5B shape, 25 % budget,
+128 steps) as sub-records.
+
+For every workload, step 1 runs three times on a copy of the state first
+(so the code objects are loaded), then one trajectory from the fresh cache:
+step 1 (the bulk eviction down to the budget) and the warm-up steps, then
+the timed steps, then the rest of the workload's steps.  Every step is bracketed by an event
+pair on the library's stream, so the record holds the first step, the timed
+steady steps and the mean over the workload's whole run.
+
+Printed on stdout: one JSON line.  value = tokens scored per second over the
+timed steps (the sum over sessions and timed steps of the cached tokens
+scored, divided by the wall time of the timed steps, bracketed by
+synchronisations); roofline = the dominant kernel's (the fused
+attention-mass kernel, or the attention-logits kernel of the multi-kernel
+path) algorithmic bytes per launch over its event-timed average duration,
+against MI355X's 8 TB/s; cpu_baseline = the CPU oracle, session-parallel on
+the host's cores, on a sample of the same workload.
 """
 from __future__ import annotations
 
@@ -39,6 +49,8 @@ METRIC = "cached tokens scored+evicted per second per decode step; achieved HBM 
 PEAK_HBM_GBS = 8000.0
 CSRC = os.path.join(ROOT, "paper_2607_10582_amd", "csrc")
 KERNEL_SRC = {"logits": os.path.join(CSRC, "md_kernels.hip"), "attend": os.path.join(CSRC, "md_attend.hip")}
+DEFAULT_WORKLOAD = "ragged_p16"
+DEFAULT_ALSO = "ragged_p64,long32k"
 
 
 def log(*a):
@@ -54,7 +66,7 @@ def describe(w, n0s) -> str:
     n = f"{int(n0s[0])}" if len(set(n0s.tolist())) == 1 else f"U[{w.n0_range[0]},{w.n0_range[1]}]"
     return (f"{w.name}: {w.S} sessions x {n} cached tokens, {w.L} layers, {w.Hq}/{w.Hkv} heads, "
             f"d {w.d}, pages of {w.P}{' (region-aligned)' if w.region_aligned else ''}, "
-            f"budget {int(w.budget_frac * 100)}%")
+            f"budget {int(w.budget_frac * 100)}%, {w.steps} decode steps")
 
 
 def setup(w, steps_total, dev, fused=None):
@@ -86,10 +98,13 @@ def setup(w, steps_total, dev, fused=None):
         pos += m
         del keys
     cache.set_free_pages(perm[pos:][::-1])
-    md = MemDecay(cache, torch.from_numpy(b), torch.from_numpy(lam), rho=w.rho, alpha=w.alpha,
-                  tau_scale=w.tau_scale, pinned_mask=w.pinned_mask, fused=fused,
-                  region_aligned=w.region_aligned, quant_threshold=w.quant_threshold,
-                  attention_norm=w.attention_norm, window=w.window)
+
+    def make_md():
+        return MemDecay(cache, torch.from_numpy(b), torch.from_numpy(lam), rho=w.rho, alpha=w.alpha,
+                        tau_scale=w.tau_scale, pinned_mask=w.pinned_mask, fused=fused,
+                        region_aligned=w.region_aligned, quant_threshold=w.quant_threshold,
+                        attention_norm=w.attention_norm, window=w.window)
+
     inputs = []
     for k in range(1, steps_total + 1):
         q = g.torch_window_queries(w, k, dev)
@@ -97,60 +112,94 @@ def setup(w, steps_total, dev, fused=None):
         reg = torch.full((w.S,), g.append_region(w, k), dtype=torch.uint8, device=dev)
         inputs.append((q, nk, reg))
     torch.cuda.synchronize(dev)
-    return n0s, B, cache, md, inputs
+    # Timing protocol: the first observation runs three times on a copy of
+    # the caller-side state (restored after each run; the key pool too when
+    # the quantised tier may rewrite it), so that the measured trajectory
+    # starts with the code objects loaded; then a fresh handle.
+    first = next(k for k in range(1, steps_total + 1) if inputs[k - 1][0] is not None)
+    names = ["region", "t_ins", "t_ref", "importance", "page_table", "page_serial", "n_pages", "n_tokens",
+             "n_live", "page_format", "clock", "next_serial", "budget", "free_list", "free_count"]
+    if w.quant_threshold > 0:
+        names.append("k_pool")
+    snap = {n: getattr(cache, n).clone() for n in names}
+    for r in range(3):
+        md = make_md()
+        for k in range(1, first + 1):
+            q, nk, reg = inputs[k - 1]
+            md.step(k, q, nk, reg, page_scores=False)
+        md.close()
+        for n in names:
+            getattr(cache, n).copy_(snap[n])
+    del snap
+    torch.cuda.synchronize(dev)
+    return n0s, B, cache, make_md(), inputs
 
 
-def cpu_baseline(w, n0s, B, budget_s: float, max_steps: int):
-    """The CPU oracle, as it stands, on session 0 of the workload: step 1 (the
-    bulk eviction) untimed, then steady steps timed until ``budget_s``."""
+def cpu_baseline(w, n0s, B, budget_s: float):
+    """The CPU oracle, as it stands, session-parallel on the host's cores:
+    one worker process per core (one BLAS thread each), one session per
+    worker (the workload's first sessions).  Step 1 (the bulk eviction) runs
+    untimed; then whole steps of all sampled sessions are timed until
+    ``budget_s``.  The keys and queries are the device-drawn ones the GPU
+    run uses, copied to the host."""
     import torch
-    import oracle
+    from oracle.pool import SessionPool, host_cores
     from synth import generator as g
 
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([1] + [int(i.get("num_threads", 1)) for i in threadpool_info()])
-    except Exception:
-        threads = 1
+    cores = host_cores()
+    n_s = min(cores, w.S)
+    sample = list(range(n_s))
     b, lam = g.region_priors(w)
-    n0 = int(n0s[0])
     dev = torch.device("cuda:0")
-    kb = g.torch_keys(w, 0, n0, dev).view(torch.int16).cpu().numpy().view(np.uint16)
-    sess = oracle.session_from_workload(w, 0, region=g.region_spans(w, 0, n0), keys_bits=kb,
-                                        b=b[0], lam=lam[0], budget=int(B[0]),
-                                        capacity=n0 + max_steps)
-    del kb
+    t_setup = time.perf_counter()
+    pool = SessionPool(cores)
+    try:
+        for s in sample:
+            n0 = int(n0s[s])
+            kb = g.torch_keys(w, s, n0, dev).view(torch.int16).cpu().numpy().view(np.uint16)
+            kw = dict(L=w.L, Hq=w.Hq, Hkv=w.Hkv, d=w.d, P=w.P, b=b[s], lam=lam[s], alpha=w.alpha, rho=w.rho,
+                      tau_scale=w.tau_scale, pinned_mask=w.pinned_mask, budget=int(B[s]), clock=n0,
+                      region=g.region_spans(w, s, n0), capacity=n0 + w.steps,
+                      attention_norm=w.attention_norm, region_aligned=w.region_aligned,
+                      quant_threshold=w.quant_threshold)
+            pool.add(s, kw, kb, n0)
+            del kb
 
-    def inputs(k):
-        qt = g.torch_window_queries(w, k, dev)
-        q = None if qt is None else qt[0].cpu().numpy()
-        nk = g.torch_append_keys(w, k, dev)[0].view(torch.int16).cpu().numpy().view(np.uint16)
-        return q, nk, g.append_region(w, k)
+        def inputs(k):
+            qt = g.torch_window_queries(w, k, dev)
+            q = None if qt is None else qt.cpu().numpy()
+            nk = g.torch_append_keys(w, k, dev).view(torch.int16).cpu().numpy().view(np.uint16)
+            r = g.append_region(w, k)
+            return {s: (None if q is None else q[s], nk[s], r) for s in sample}
 
-    # untimed up to the first observation (the bulk eviction)
-    k = 1
-    while True:
-        q, nk, r = inputs(k)
-        sess.step(q, nk, r)
-        k += 1
-        if q is not None:
-            break
-    k0 = k
-    scored = 0
-    steps = 0
-    elapsed = 0.0
-    while elapsed < budget_s and k <= max_steps:
-        q, nk, r = inputs(k)
-        t0 = time.perf_counter()
-        rec = sess.step(q, nk, r)
-        elapsed += time.perf_counter() - t0
-        if q is not None:     # only observation steps score tokens
-            scored += rec.n
-        steps += 1
-        k += 1
-    return {"value": scored / elapsed, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"session 0 of {w.S} ({w.name}), {steps} steady decode steps (steps {k0}-{k - 1}, "
-                      f"after the bulk eviction), {scored} token-steps in {elapsed:.1f} s, numpy float64",
+        log(f"cpu baseline: {n_s} sessions on {pool.workers} workers, set up in "
+            f"{time.perf_counter() - t_setup:.1f} s")
+        k = 1
+        while True:                     # untimed up to the first observation (the bulk eviction)
+            inp = inputs(k)
+            pool.step(inp)
+            k += 1
+            if next(iter(inp.values()))[0] is not None:
+                break
+        k0 = k
+        scored = steps = 0
+        elapsed = 0.0
+        while elapsed < budget_s and k <= w.steps:
+            inp = inputs(k)
+            t0 = time.perf_counter()
+            recs = pool.step(inp)
+            elapsed += time.perf_counter() - t0
+            if next(iter(inp.values()))[0] is not None:     # only observation steps score tokens
+                scored += sum(r.n for r in recs.values())
+            steps += 1
+            k += 1
+    finally:
+        pool.close()
+    return {"value": scored / elapsed, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"sessions 0-{n_s - 1} of {w.S} ({w.name}), one per worker process "
+                      f"({pool.workers} workers x 1 BLAS thread on {cores} cores), {steps} steady decode steps "
+                      f"(steps {k0}-{k - 1}, after the untimed bulk eviction), {scored} token-steps in "
+                      f"{elapsed:.1f} s of wall time, numpy float64",
             "seconds_per_step": elapsed / max(steps, 1)}
 
 
@@ -170,7 +219,6 @@ def load_traffic(kernel: str, workload: str):
 def quantised_tokens(cache) -> int:
     """Tokens held in quantised pages now (such pages are never a session's
     last page, so each holds P slots)."""
-    import torch
     npg = cache.n_pages.cpu().numpy()
     fmt = cache.page_format.cpu().numpy()
     tot = 0
@@ -193,112 +241,74 @@ def calibrate_copy(mib: int):
     log(f"copied {n} bytes 5 times")
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=32)
-    ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="long32k")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--multi-kernel", action="store_true",
-                    help="observe on the multi-kernel path (logits in HBM) at every step instead of "
-                         "letting the library pick")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
-    ap.add_argument("--calibrate", type=int, default=0, metavar="BUCKET_STEPS",
-                    help="also accumulate the region-lifetime statistics (Sec. IV-B) at every "
-                         "observation, in age buckets of this many steps, and time it")
-    ap.add_argument("--quant-threshold", type=float, default=None,
-                    help="quantised tier: override the workload's threshold (0: off)")
-    args = ap.parse_args()
-
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: the retention path shards over sessions with no "
-              f"exchange, and the benchmark measures one GPU's share (asked for --gpus {args.gpus}).",
-              file=sys.stderr)
-        sys.exit(2)
-    if args.calibrate_copy:
-        calibrate_copy(args.calibrate_copy)
-        return
-
+def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0):
+    """One trajectory of workload w from a fresh cache: steps 1..W (warm-up;
+    step 1 the bulk eviction), W+1..W+K timed, then on to the workload's
+    last step.  Returns the record (value, roofline, step times)."""
     import torch
-    from paper_2607_10582_amd import binding
     from synth import configs as C
     from synth import generator as g
 
-    binding.load_library()
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    w = C.get(args.workload)
-    if args.quant_threshold is not None:
-        w = C.with_overrides(w, quant_threshold=args.quant_threshold)
-    W, K = args.warmup, args.steps
-    if W + K > w.steps:
-        log(f"note: {W + K} steps asked, the workload defines {w.steps} decode steps")
+    total = max(w.steps, W + K)
     t_setup = time.perf_counter()
-    n0s, B, cache, md, inputs = setup(w, W + K, dev, fused=False if args.multi_kernel else None)
+    n0s, B, cache, md, inputs = setup(w, total, dev, fused=False if multi_kernel else None)
     log(f"setup {time.perf_counter() - t_setup:.1f} s: {describe(w, n0s)}")
+    stream = md.stream
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(total + 1)]
 
-    # warm-up; the first step (the bulk eviction down to the budget) is
-    # timed on its own with an event pair on the library's stream
-    first_ms = None
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    first_obs = None
-    for k in range(1, W + 1):
+    def run(k):
         q, nk, reg = inputs[k - 1]
-        timed = first_obs is None and q is not None
-        if timed:
-            first_obs = k
-            e0.record(md.stream)
         md.step(k, q, nk, reg, page_scores=False)
-        if timed:
-            e1.record(md.stream)
+
+    # warm-up, every step event-timed
+    for k in range(1, W + 1):
+        ev[k - 1].record(stream)
+        run(k)
+    ev[W].record(stream)
     torch.cuda.synchronize(dev)
-    if first_obs is not None:
-        first_ms = e0.elapsed_time(e1)
     c0 = md.counters()
     kcfg = md.kernel_config()
     hot = "attend" if kcfg["steady_fused"] and not kcfg["spill"] else "logits"
     log(f"kernel config {kcfg}; timing k_{hot}")
     md.profile((hot,))
-    stream = md.stream
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    step_ev = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     q_tok0 = quantised_tokens(cache) if w.quant_threshold > 0 else 0
-    torch.cuda.synchronize(dev)
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    if args.calibrate:
+    if calibrate:
         n_buckets = 64
         abar = torch.zeros(cache.n_phys * w.P, dtype=torch.float32, device=dev)
         stats = [torch.zeros((w.S, 7, n_buckets), dtype=torch.int64, device=dev) for _ in range(3)]
         cal_ev = []
-    for i, k in enumerate(range(W + 1, W + K + 1)):
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for k in range(W + 1, W + K + 1):
         q, nk, reg = inputs[k - 1]
-        step_ev[i].record(stream)
-        if args.calibrate and q is not None:
+        ev[k - 1].record(stream)
+        if calibrate and q is not None:
             # a calibration pass: the step's masses go to the lifetime bins
             md.observe(k, q, nk, reg, abar_out=abar)
             ce = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             ce[0].record(stream)
-            md.calib_accumulate(abar, args.calibrate, stats)
+            md.calib_accumulate(abar, calibrate, stats)
             ce[1].record(stream)
             cal_ev.append(ce)
             md.score(page_score=False)
             md.select()
             md.compact()
         else:
-            md.step(k, q, nk, reg, page_scores=False)
-    step_ev[K].record(stream)
-    ev1.record(stream)
+            run(k)
+    ev[W + K].record(stream)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0
-    per_step = sorted(step_ev[i].elapsed_time(step_ev[i + 1]) for i in range(K))
-    gpu_ms = ev0.elapsed_time(ev1)
     hot_ms, launches = md.profile_read(hot)
     md.profile(())
     c1 = md.counters()
+    q_tok1 = quantised_tokens(cache) if w.quant_threshold > 0 else 0
+    # the rest of the workload's run
+    for k in range(W + K + 1, total + 1):
+        ev[k - 1].record(stream)
+        run(k)
+    ev[total].record(stream)
+    torch.cuda.synchronize(dev)
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(total)]
     status = md.device_status()
     if status != 0:
         log(f"device status {status:#x}")
@@ -309,10 +319,8 @@ def main():
     # counts before and after the timed steps (the set changes slowly); their
     # keys take d + 1 bytes per (layer, KV head) row instead of 2 d (codes,
     # and a 16-byte scale line per 16 tokens)
-    q_tok = (q_tok0 + quantised_tokens(cache)) / 2 if w.quant_threshold > 0 else 0
+    q_tok = (q_tok0 + q_tok1) / 2 if w.quant_threshold > 0 else 0
     q_saved = K * q_tok * (w.k_bytes_per_token - w.L * w.Hkv * (w.d + 1))
-    evicted_tokens = c1[3] - c0[3]
-    evicted_pages = c1[2] - c0[2]
     kb = w.k_bytes_per_token
     # the queries of the observation steps: W per session and step
     n_obs = sum(1 for k in range(W + 1, W + K + 1) if g.observes(w, k))
@@ -336,46 +344,126 @@ def main():
     # whole step: K + per-token state (region 1, a 4+4, t_ref 4+4) + per-page
     # score and page-table entry + the queries
     step_bytes = scored * (kb + 17) + scored // w.P * 8 + K * q_bytes - q_saved
+    timed = step_ms[W:W + K]
+    rec = {
+        "value": scored / wall,
+        "unit": "tokens/s",
+        "ms_per_step": wall * 1e3 / K,
+        "workload": describe(w, n0s),
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
+                     "traffic_source": None if traffic is None else os.path.relpath(traffic_src, ROOT),
+                     "kernel": f"k_{hot}", "launches": launches,
+                     "avg_launch_us": avg_launch_s * 1e6,
+                     "algorithmic_bytes_per_launch": per_launch_bytes},
+        "tokens_scored_per_step": scored / K,
+        "tokens_evicted_per_step": (c1[3] - c0[3]) / K,
+        "quantised_tokens_per_step": q_tok,
+        "pages_evicted": c1[2] - c0[2],
+        "first_step_ms": step_ms[0],
+        "steady_step_ms_mean": float(np.mean(timed)),
+        "step_ms_median": float(np.median(timed)),
+        "run_mean_ms": float(np.mean(step_ms)),
+        "run_steps": total,
+        "calib_us_per_observation": (sum(a.elapsed_time(b) for a, b in cal_ev) * 1e3 / len(cal_ev)
+                                     if calibrate and cal_ev else None),
+        "step_algorithmic_gbs": step_bytes / wall / 1e9,
+        "step_frac_of_peak": step_bytes / wall / 1e9 / PEAK_HBM_GBS,
+    }
+    md.close()
+    del cache, inputs, md
+    torch.cuda.synchronize(dev)
+    torch.cuda.empty_cache()
+    return rec, n0s, B
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--also", default=None,
+                    help=f"comma-separated workloads measured as sub-records in the same run "
+                         f"(default with the default workload: {DEFAULT_ALSO}; '' for none)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--multi-kernel", action="store_true",
+                    help="observe on the multi-kernel path (logits in HBM) at every step instead of "
+                         "letting the library pick")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
+    ap.add_argument("--calibrate", type=int, default=0, metavar="BUCKET_STEPS",
+                    help="also accumulate the region-lifetime statistics (Sec. IV-B) at every "
+                         "observation, in age buckets of this many steps, and time it")
+    ap.add_argument("--quant-threshold", type=float, default=None,
+                    help="quantised tier: override the workload's threshold (0: off)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the retention path shards over sessions with no "
+              f"exchange, and the benchmark measures one GPU's share (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
+
+    import torch
+    # The HIP runtime starts before the library is loaded (see
+    # binding.load_library): its exit handlers then run after the library's.
+    dev = torch.device("cuda:0")
+    torch.cuda.init()
+    torch.cuda.set_device(dev)
+    torch.cuda.synchronize(dev)
+    from paper_2607_10582_amd import binding
+    from synth import configs as C
+
+    binding.load_library()
+    w = C.get(args.workload)
+    if args.quant_threshold is not None:
+        w = C.with_overrides(w, quant_threshold=args.quant_threshold)
+    also = args.also if args.also is not None else (DEFAULT_ALSO if args.workload == DEFAULT_WORKLOAD else "")
+    also = [a for a in also.split(",") if a and a != w.name]
+    W, K = args.warmup, args.steps
+    if W < 1:
+        log("note: the warm-up includes step 1, the bulk eviction; --warmup raised to 1")
+        W = 1
+
+    main_rec, n0s, B = measure(w, W, K, dev, multi_kernel=args.multi_kernel, calibrate=args.calibrate)
+    subs = {}
+    for name in also:
+        rec, _, _ = measure(C.get(name), W, K, dev, multi_kernel=args.multi_kernel)
+        subs[name] = rec
+        log(f"{name}: {rec['value']:.4g} tokens/s, k_{rec['roofline']['kernel'][2:]} "
+            f"{rec['roofline']['frac']:.3f} of peak")
 
     line = {
         "metric": METRIC,
-        "value": scored / wall,
+        "value": main_rec["value"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": W,
-        "ms_per_step": wall * 1e3 / K,
+        "ms_per_step": main_rec["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": describe(w, n0s), "sessions": w.S,
-                   "cached_tokens_per_session": int(n0s[0]) if w.n0 else "ragged",
+        "config": {"workload": main_rec["workload"], "sessions": w.S,
+                   "cached_tokens_per_session": int(n0s[0]) if w.n0 else f"U[{w.n0_range[0]},{w.n0_range[1]}]",
                    "layers": w.L, "q_heads": w.Hq, "kv_heads": w.Hkv, "head_dim": w.d,
-                   "page_size": w.P, "budget_frac": w.budget_frac, "parallelism": "none"},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBS, "traffic": traffic,
-                     "kernel": f"k_{hot}", "launches": launches,
-                     "avg_launch_us": avg_launch_s * 1e6,
-                     "algorithmic_bytes_per_launch": per_launch_bytes},
-        "tokens_scored_per_step": scored / K,
-        "quantised_tokens_per_step": q_tok,
-        "tokens_evicted_per_step": evicted_tokens / K,
-        "pages_evicted": evicted_pages,
-        "gpu_event_ms_per_step": gpu_ms / K,
-        "step_ms_median": per_step[K // 2],
-        "first_step_ms": first_ms,
-        "calib_us_per_observation": (sum(a.elapsed_time(b) for a, b in cal_ev) * 1e3 / len(cal_ev)
-                                     if args.calibrate and cal_ev else None),
-        "step_algorithmic_gbs": step_bytes / wall / 1e9,
-        "step_frac_of_peak": step_bytes / wall / 1e9 / PEAK_HBM_GBS,
+                   "page_size": w.P, "budget_frac": w.budget_frac, "decode_steps": w.steps,
+                   "parallelism": "none"},
+        "roofline": main_rec["roofline"],
     }
-    md.close()
-    del cache, inputs
-    torch.cuda.empty_cache()
+    for key in ("tokens_scored_per_step", "tokens_evicted_per_step", "quantised_tokens_per_step",
+                "pages_evicted", "first_step_ms", "steady_step_ms_mean", "step_ms_median", "run_mean_ms",
+                "run_steps", "calib_us_per_observation", "step_algorithmic_gbs", "step_frac_of_peak"):
+        line[key] = main_rec[key]
+    line["workloads"] = subs
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, n0s, B, args.cpu_seconds, w.steps)
+        line["cpu_baseline"] = cpu_baseline(w, n0s, B, args.cpu_seconds)
     else:
         line["cpu_baseline"] = None
     print(json.dumps(line), flush=True)
