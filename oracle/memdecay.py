@@ -71,11 +71,31 @@ Readings where the paper leaves a choice:
     s * c.  (Sec. III-E names low precision without a format; E4M3 is the
     8-bit format the device widens to its MFMA operand type in one
     instruction.)
+  * optional offload tier (the second tier of Sec. III-E: pages below a
+    second threshold go to host memory and come back when later queries make
+    them relevant; below a final threshold they are dropped).  The budget
+    bounds the pages in the cache (|K_t| and B count them only); a session
+    keeps at most ``offload_pages`` pages in host memory.  At an observation
+    step, after the attention over the cached tokens, every offloaded token
+    is observed with the same query: its mass is the mean over the (layer,
+    query head) rows of the weight exp(x - M_r) / Lambda_r it would take
+    next to the cached tokens, M_r and Lambda_r being row r's maximum and
+    sum over the cached tokens (so the cached tokens' masses do not change;
+    with no cached token the weight is 0).  The EWMA and the refresh test
+    (same tau) apply to it as to a cached token, and it is scored by Eq. 4
+    and Eq. 5.  An offloaded page with a token refreshed by this step is
+    recalled: it rejoins the cache in serial order before the eviction, which
+    then counts it.  Offloaded pages that stay and score below
+    ``drop_threshold`` are dropped.  Of the pages the eviction removes, those
+    that take no more tokens (full) and score at least ``drop_threshold`` go
+    to host memory, highest page score first (then the older page), while
+    the session's host tier has room; the rest are dropped.  An offloaded
+    page keeps its keys as they were (quantised or not).
 """
 from __future__ import annotations
 
 import math
-from dataclasses import dataclass
+from dataclasses import dataclass, field
 from typing import List, Optional, Sequence
 
 import numpy as np
@@ -164,6 +184,20 @@ class StepRecord:
     evicted: np.ndarray          # serials evicted this step, ascending
     n_after: int
     infeasible: bool
+    # offload tier (empty without it).  The page and token arrays above cover
+    # the cached pages at the selection, recalled pages included; n_select
+    # counts their tokens (n is still the |K_t| of tau, before the recall).
+    n_select: int = -1
+    off_serial: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int64))   # observed, after recall
+    off_abar: np.ndarray = field(default_factory=lambda: np.zeros(0))     # their tokens, page by page
+    off_a: np.ndarray = field(default_factory=lambda: np.zeros(0))
+    off_t_ref: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int64))
+    off_score: np.ndarray = field(default_factory=lambda: np.zeros(0))
+    off_page_score: np.ndarray = field(default_factory=lambda: np.zeros(0))
+    recalled: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int64))
+    dropped: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int64))       # from host memory
+    offloaded_now: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int64))
+    off_after: np.ndarray = field(default_factory=lambda: np.zeros(0, np.int64))     # in host memory after
 
 
 class Session:
@@ -177,7 +211,7 @@ class Session:
                  page_serials: Optional[Sequence[int]] = None,
                  next_serial: Optional[int] = None, capacity: Optional[int] = None,
                  attention_norm: bool = False, region_aligned: bool = False,
-                 quant_threshold: float = 0.0):
+                 quant_threshold: float = 0.0, offload_pages: int = 0, drop_threshold: float = 0.0):
         if Hq % Hkv:
             raise ValueError("query heads must be a multiple of KV heads")
         self.L, self.Hq, self.Hkv, self.d, self.P = L, Hq, Hkv, d, P
@@ -189,6 +223,9 @@ class Session:
         self.attention_norm = bool(attention_norm)
         self.region_aligned = bool(region_aligned)
         self.quant_threshold = float(quant_threshold)
+        self.offload_pages = int(offload_pages)
+        self.drop_threshold = float(drop_threshold)
+        self.offloaded: List[Page] = []     # pages in host memory, serial order
         self.budget = int(budget)
         self.t = int(clock)
 
@@ -340,6 +377,49 @@ class Session:
                         mass[seen] += softmax(x[:, j])
         return mass / (self.L * self.Hq * W)
 
+    def offloaded_mass(self, q, live: np.ndarray, off: np.ndarray) -> np.ndarray:
+        """Offload tier: the mass each offloaded token would take from the
+        query q ([L][Hq][d], one query) next to the cached tokens ``live``:
+        the mean over the (layer, query head) rows of exp(x - M) / Lambda,
+        M and Lambda being the row's maximum and sum over the cached tokens;
+        0 when no token is cached."""
+        mass = np.zeros(off.shape[0], dtype=np.float64)
+        if live.shape[0] == 0 or off.shape[0] == 0:
+            return mass
+        q = np.asarray(q, dtype=np.float32).astype(np.float64).reshape(self.L, self.Hq, self.d)
+        inv_sqrt_d = 1.0 / math.sqrt(self.d)
+        for l in range(self.L):
+            for kv in range(self.Hkv):
+                qg = q[l, kv * self.G:(kv + 1) * self.G].T
+                x = (self.key_rows(l, kv, live) @ qg) * inv_sqrt_d          # [n][G]
+                xo = (self.key_rows(l, kv, off) @ qg) * inv_sqrt_d          # [n_off][G]
+                for j in range(self.G):
+                    m = np.max(x[:, j])
+                    lam = np.sum(np.exp(x[:, j] - m))
+                    mass += np.exp(xo[:, j] - m) / lam
+        return mass / (self.L * self.Hq)
+
+    def token_scores(self, slots: np.ndarray, n: int) -> np.ndarray:
+        """s_i of Eq. 4 at the current clock (+inf for pinned tokens)."""
+        r = self.region[slots]
+        dt = (self.t - self.t_ref[slots]).astype(np.float64)
+        weight = self.alpha * n if self.attention_norm else self.alpha
+        score = self.b[r] * np.exp(-self.lam[r] * dt) + weight * self.a[slots]
+        return np.where(self.is_pinned_region(r), np.inf, score)
+
+    def page_scores(self, pages: List[Page], score_of_slot: np.ndarray):
+        """S_p of Eq. 5 per page: the mean over its members, +inf when any
+        member is pinned.  Returns (sizes, pinned, scores)."""
+        m = len(pages)
+        sizes = np.array([len(p.slots) for p in pages], dtype=np.int64)
+        pinned = np.zeros(m, dtype=bool)
+        scores = np.zeros(m, dtype=np.float64)
+        for i, p in enumerate(pages):
+            sl = np.asarray(p.slots, dtype=np.int64)
+            pinned[i] = bool(np.any(self.is_pinned_region(self.region[sl])))
+            scores[i] = np.inf if pinned[i] else float(np.sum(score_of_slot[sl])) / sizes[i]
+        return sizes, pinned, scores
+
     def step(self, q, new_key_bits=None, new_region: Optional[int] = None) -> StepRecord:
         """One decode step at the next clock value: the append, then, when q
         is given, the observation and eviction of Alg. 1.  Without q the step
@@ -350,62 +430,101 @@ class Session:
             self.append(new_key_bits, new_region)
         live = self.live()
         n = live.shape[0]
-        m = len(self.pages)
         empty = np.zeros(0)
         if q is None:
             return StepRecord(t, n, math.inf, np.zeros(0, np.int64), np.zeros(0, np.int64),
                               np.zeros(0, bool), empty, empty, empty, np.zeros(0, np.int64),
-                              np.zeros(0, np.int64), empty, np.zeros(0, np.int64), n, n > self.budget)
-        if n == 0:
+                              np.zeros(0, np.int64), empty, np.zeros(0, np.int64), n, n > self.budget,
+                              n_select=n)
+        if n == 0 and not self.offloaded:
             return StepRecord(t, 0, math.inf, np.zeros(0, np.int64), np.zeros(0, np.int64),
                               np.zeros(0, bool), empty, empty, empty, np.zeros(0, np.int64),
-                              np.zeros(0, np.int64), empty, np.zeros(0, np.int64), 0, False)
+                              np.zeros(0, np.int64), empty, np.zeros(0, np.int64), 0, False, n_select=0)
 
-        # O2-O3: attention mass.
-        abar = self.attention_mass(q, live)
-        # O4: EWMA over every cached token, pinned included (Eq. 2).
+        # O2-O3: attention mass of the cached tokens; offload tier: the
+        # offloaded tokens' mass next to them.
+        abar = self.attention_mass(q, live) if n else empty
+        off_pages = list(self.offloaded)
+        off = (np.concatenate([np.asarray(p.slots, dtype=np.int64) for p in off_pages])
+               if off_pages else np.zeros(0, dtype=np.int64))
+        abar_off = self.offloaded_mass(q, live, off)
+        # O4: EWMA over every cached token, pinned included (Eq. 2), and over
+        # the offloaded tokens observed.
         self.a[live] = self.rho * self.a[live] + (1.0 - self.rho) * abar
+        self.a[off] = self.rho * self.a[off] + (1.0 - self.rho) * abar_off
         # O5: refresh clock (Eq. 3), threshold scaled to the uniform level.
-        tau = self.tau_scale / n
-        refreshed = live[abar >= tau]
-        self.t_ref[refreshed] = t
+        tau = self.tau_scale / n if n else math.inf
+        self.t_ref[live[abar >= tau]] = t
+        self.t_ref[off[abar_off >= tau]] = t
         # O6: retention score (Eq. 4); pinned tokens bypass scoring.  With the
         # normalised attention term, a_i is measured in units of the uniform
         # attention level 1/n (Sec. IV-D).
-        r = self.region[live]
-        dt = (t - self.t_ref[live]).astype(np.float64)
-        weight = self.alpha * n if self.attention_norm else self.alpha
-        score = self.b[r] * np.exp(-self.lam[r] * dt) + weight * self.a[live]
-        pinned_tok = self.is_pinned_region(r)
-        score = np.where(pinned_tok, np.inf, score)
+        score_of = np.zeros(self.region.shape[0], dtype=np.float64)
+        score_of[live] = self.token_scores(live, n)
+        score_of[off] = self.token_scores(off, n)
+        abar_of = np.zeros(self.region.shape[0], dtype=np.float64)
+        abar_of[live] = abar
+        abar_of[off] = abar_off
+        # Offload tier: pages with a token refreshed now come back, in serial
+        # order, before the eviction.
+        refreshed_now = set(off[abar_off >= tau].tolist())
+        recalled = [p for p in off_pages if any(x in refreshed_now for x in p.slots)]
+        if recalled:
+            self.offloaded = [p for p in off_pages if p not in recalled]
+            self.pages = sorted(self.pages + recalled, key=lambda p: p.serial)
+        live_sel = self.live()
+        n_sel = live_sel.shape[0]
         # O7: page score (Eq. 5), mean over the page's live members.
-        sizes = np.array([len(p.slots) for p in self.pages], dtype=np.int64)
+        sizes, page_pinned, page_score = self.page_scores(self.pages, score_of)
         serials = np.array([p.serial for p in self.pages], dtype=np.int64)
-        bounds = np.concatenate([[0], np.cumsum(sizes)])
-        page_pinned = np.zeros(m, dtype=bool)
-        page_score = np.zeros(m, dtype=np.float64)
-        for i in range(m):
-            seg = slice(bounds[i], bounds[i + 1])
-            page_pinned[i] = bool(np.any(pinned_tok[seg]))
-            page_score[i] = np.inf if page_pinned[i] else float(np.sum(score[seg])) / sizes[i]
+        o_sizes, o_pinned, o_scores = self.page_scores(self.offloaded, score_of)
+        o_serials = np.array([p.serial for p in self.offloaded], dtype=np.int64)
+        o_slots = (np.concatenate([np.asarray(p.slots, dtype=np.int64) for p in self.offloaded])
+                   if self.offloaded else np.zeros(0, dtype=np.int64))
         # O8: budget-aware page eviction (Alg. 1, min-heap order).
         evicted, n_after, infeasible = select_pages(page_score, serials, sizes,
-                                                    page_pinned, n, self.budget)
-        # O9: drop the evicted pages (irreversible, Sec. III-E).
-        last_serial = self.pages[-1].serial
+                                                    page_pinned, n_sel, self.budget)
+        # O9: the evicted pages leave the cache (irreversible, Sec. III-E,
+        # unless the offload tier keeps them).
+        last_serial = self.pages[-1].serial if self.pages else -1
+        score_of_page = {int(s_): float(v) for s_, v in zip(serials, page_score)}
+        leaving = [p for p in self.pages if int(p.serial) in set(evicted.tolist())]
         if evicted.size:
             gone = set(int(x) for x in evicted)
             self.pages = [p for p in self.pages if p.serial not in gone]
+        dropped, offloaded_now = [], []
+        if self.offload_pages > 0:
+            # offloaded pages below the final threshold are dropped
+            keep = []
+            for p, v in zip(self.offloaded, o_scores):
+                (keep if v >= self.drop_threshold else dropped).append(p)
+            self.offloaded = keep
+            # full pages leaving the cache at or above it go to host memory,
+            # the best first, while there is room
+            cand = [p for p in leaving if len(p.slots) == self.P
+                    and score_of_page[p.serial] >= self.drop_threshold]
+            cand.sort(key=lambda p: (-score_of_page[p.serial], p.serial))
+            room = self.offload_pages - len(self.offloaded)
+            chosen = cand[:max(room, 0)]
+            offloaded_now = sorted(p.serial for p in chosen)
+            self.offloaded = sorted(self.offloaded + chosen, key=lambda p: p.serial)
         # Quantised tier (Sec. III-E): surviving pages below the threshold.
         if self.quant_threshold > 0:
-            score_of = {int(s): (float(v), bool(pn)) for s, v, pn in zip(serials, page_score, page_pinned)}
+            sc_of = {int(s_): (float(v), bool(pn)) for s_, v, pn in zip(serials, page_score, page_pinned)}
             for p in self.pages:
-                v, pn = score_of[p.serial]
+                v, pn = sc_of[p.serial]
                 if not pn and not p.quant and p.serial != last_serial and v < self.quant_threshold:
                     self.quantise_page(p)
-        return StepRecord(t, n, tau, serials, sizes, page_pinned, page_score, abar,
-                          self.a[live].copy(), self.t_ref[live].copy(), r.copy(), score,
-                          evicted, n_after, infeasible)
+        return StepRecord(t, n, tau, serials, sizes, page_pinned, page_score, abar_of[live_sel].copy(),
+                          self.a[live_sel].copy(), self.t_ref[live_sel].copy(), self.region[live_sel].copy(),
+                          score_of[live_sel].copy(), evicted, n_after, infeasible, n_select=n_sel,
+                          off_serial=o_serials, off_abar=abar_of[o_slots].copy(), off_a=self.a[o_slots].copy(),
+                          off_t_ref=self.t_ref[o_slots].copy(), off_score=score_of[o_slots].copy(),
+                          off_page_score=o_scores,
+                          recalled=np.array(sorted(p.serial for p in recalled), dtype=np.int64),
+                          dropped=np.array(sorted(p.serial for p in dropped), dtype=np.int64),
+                          offloaded_now=np.array(offloaded_now, dtype=np.int64),
+                          off_after=np.array([p.serial for p in self.offloaded], dtype=np.int64))
 
     # ------------------------------------------------------------ views
     def state(self):
