@@ -75,7 +75,7 @@
 extern "C" {
 #endif
 
-#define MD_ABI_VERSION 6
+#define MD_ABI_VERSION 7
 
 typedef int32_t md_status;
 
@@ -158,6 +158,11 @@ typedef struct md_config {
     float quant_threshold;      /* quantised tier (Sec. III-E): md_compact turns  */
                                 /* pages scoring below it into 8-bit codes; 0 =   */
                                 /* off, +INFINITY = every eligible page           */
+    int32_t offload_pages;      /* offload tier (Sec. III-E): host-memory pages   */
+                                /* per session, 0..64; 0 = off.  Needs window 1   */
+                                /* and plain pages (MD_E_UNSUPPORTED otherwise)   */
+    float drop_threshold;       /* offload tier: pages scoring below it are       */
+                                /* dropped, not kept in host memory (>= 0)        */
 } md_config;
 
 /* Region priors (Sec. III-B): b_r >= 0 and lambda_r >= 0 per session and
@@ -186,6 +191,27 @@ typedef struct md_cache_view {
                           /* ignored (may be NULL: |K_t| is n_tokens)          */
     uint8_t*  page_format;/* quant_threshold > 0: [NP], 0 = bf16 keys, 1 =     */
                           /* quantised; else ignored (may be NULL)             */
+    /* Offload tier (offload_pages = H > 0; else ignored, may be NULL).  The   */
+    /* pages in host memory of session s are listed in entries 0 .. count-1 of */
+    /* row s, serials ascending; each sits in a host slot 0 .. H-1, which      */
+    /* indexes the keys and the per-token state.  The caller zeroes off_count; */
+    /* the library maintains the rest.                                         */
+    void*     host_keys;  /* PINNED HOST memory from hipHostMalloc, 16-byte    */
+                          /* aligned: [S][H][L Hkv P d] bf16 bits, each slot a  */
+                          /* page in the pool's page layout (codes and scales   */
+                          /* for a quantised page)                             */
+    int32_t*  off_count;  /* [S]                                               */
+    int32_t*  off_serial; /* [S][H] serials of the listed pages, ascending     */
+    int32_t*  off_slot;   /* [S][H] host slot of each listed page              */
+    uint8_t*  off_region; /* [S][H][P] per host slot and token                 */
+    int32_t*  off_t_ins;  /* [S][H][P]                                         */
+    int32_t*  off_t_ref;  /* [S][H][P]                                         */
+    float*    off_importance; /* [S][H][P]                                     */
+    uint8_t*  off_format; /* [S][H] per host slot: 1 = quantised keys          */
+    float*    off_score;  /* [S][H] page score of each listed page at the last */
+                          /* observation (written by the library)              */
+    float*    off_abar;   /* [S][H][P] the last observation's mass of each     */
+                          /* host-memory token (written by the library)        */
 } md_cache_view;
 
 typedef struct md_handle_s* md_handle;
@@ -252,6 +278,17 @@ md_status md_init_static(const md_config* cfg, const md_region_params* rp, const
  *   refresh (Eq. 3): t_ref_i <- t when A_i >= tau_scale / |K_t|, |K_t| the
  *     session's token count after the append (n_live with region-aligned
  *     pages, n_tokens otherwise).
+ *   offload tier (offload_pages > 0; Sec. III-E's second tier): every token
+ *     of a page in host memory is observed with the same query, its keys read
+ *     over the host link: A_i = the mean over rows of its weight
+ *     exp(x_i - M_r) / Lambda_r next to the cached tokens (M_r, Lambda_r:
+ *     row r's maximum and sum over the cached tokens, which keep their
+ *     masses; 0 without cached tokens); EWMA, refresh (same tau), token and
+ *     page scores as for a cached token (off_importance, off_t_ref,
+ *     off_abar, off_score).  A page with a token refreshed now is recalled:
+ *     a device page comes off the free list (sessions in order), the keys
+ *     and token state come back, and the page rejoins the page table in
+ *     serial order, so this step's selection counts it.
  * q:          float32 [S][W][L][Hq][d] decode queries of steps t - W + 1 .. t,
  *             oldest first (device), or NULL for a decode step without an
  *             observation: then only the append and the clock advance run,
@@ -309,6 +346,13 @@ md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_cou
  * other lists (a caller's own choice; one NULL and one not is
  * MD_E_INVALID).  Serials a session does not hold set MD_DEV_BAD_EVICT and
  * are ignored.  Sessions whose step is void are left as they are.
+ * Offload tier (offload_pages > 0; Sec. III-E), first: pages in host memory
+ * whose score of this step is below drop_threshold are dropped; of the
+ * listed pages, those that take no more tokens (all but the last page, or a
+ * full last page) and score at least drop_threshold are copied to host
+ * memory with their tokens' state, the highest score first (then the older
+ * page), while the session has free host slots; the others are dropped.
+ * Requires md_score_pages since the last md_observe_step.
  * Quantised tier (quant_threshold > 0; Sec. III-E's first tier): before the
  * compaction, every page that survives, is not pinned, is not the session's
  * last page, is still bf16 and has page score S_p < quant_threshold (the
@@ -341,9 +385,12 @@ enum {
 md_status md_profile_enable(md_handle h, uint32_t kernel_mask);
 md_status md_profile_read(md_handle h, int32_t kernel, double* total_ms, int64_t* launches);
 
-/* Device-side running totals since md_init, read after synchronising:
- * out[0] tokens scored (sum over steps and sessions of |K_t|), out[1] steps
- * observed, out[2] pages evicted, out[3] tokens evicted. */
+/* Device-side running totals since md_init, read after synchronising (out:
+ * 8 values): out[0] tokens scored (sum over steps and sessions of |K_t|),
+ * out[1] steps observed, out[2] pages evicted, out[3] tokens evicted; offload
+ * tier: out[4] pages moved to host memory, out[5] pages recalled from it,
+ * out[6] pages dropped from it, out[7] host-memory pages observed (each read
+ * once over the host link per observation). */
 md_status md_read_counters(md_handle h, int64_t* out);
 
 /* How md_init laid out the observation step on this device (out: 6 ints):

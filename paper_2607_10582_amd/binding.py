@@ -53,7 +53,8 @@ class md_config(ctypes.Structure):
                 ("n_regions", ctypes.c_int32), ("pinned_region_mask", ctypes.c_uint32),
                 ("rho", ctypes.c_float), ("alpha", ctypes.c_float),
                 ("tau_scale", ctypes.c_float), ("flags", ctypes.c_int32), ("window", ctypes.c_int32),
-                ("quant_threshold", ctypes.c_float)]
+                ("quant_threshold", ctypes.c_float), ("offload_pages", ctypes.c_int32),
+                ("drop_threshold", ctypes.c_float)]
 
 
 class md_region_params(ctypes.Structure):
@@ -64,7 +65,8 @@ class md_cache_view(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "k_pool", "region", "t_ins", "t_ref", "importance", "page_table", "page_serial",
         "n_pages", "n_tokens", "clock", "next_serial", "budget", "free_list", "free_count", "n_live",
-        "page_format")]
+        "page_format", "host_keys", "off_count", "off_serial", "off_slot", "off_region", "off_t_ins",
+        "off_t_ref", "off_importance", "off_format", "off_score", "off_abar")]
 
 
 class MemDecayError(RuntimeError):
@@ -249,8 +251,10 @@ def md_calib_fit(mass_fx, count, age_sum):
 
 
 def md_read_counters(h: int):
-    """(tokens scored, steps observed, pages evicted, tokens evicted) since md_init."""
-    out = (ctypes.c_int64 * 4)()
+    """(tokens scored, steps observed, pages evicted, tokens evicted, pages
+    offloaded, recalled, dropped from host memory, host-memory pages
+    observed) since md_init."""
+    out = (ctypes.c_int64 * 8)()
     _check("md_read_counters", load_library().md_read_counters(h, out))
     return tuple(int(x) for x in out)
 

@@ -10,7 +10,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmemdecay.so")
-SOURCES = ["md_kernels.hip", "md_attend.hip", "md_api.cpp"]
+SOURCES = ["md_kernels.hip", "md_attend.hip", "md_offload.hip", "md_api.cpp"]
 
 # Packed FP32 instructions stay off: the compiler would otherwise form
 # v_pk_* FP32 ops from plain float code.

@@ -24,7 +24,7 @@ class PagedCache:
     """Device buffers of one batch of sessions (layouts as in memdecay.h)."""
 
     def __init__(self, *, L: int, Hq: int, Hkv: int, d: int, P: int, S: int,
-                 max_pages: int, n_phys: int, device="cuda"):
+                 max_pages: int, n_phys: int, device="cuda", offload_pages: int = 0):
         self.L, self.Hq, self.Hkv, self.d, self.P = L, Hq, Hkv, d, P
         self.S, self.max_pages, self.n_phys = S, max_pages, n_phys
         self.device = torch.device(device)
@@ -48,12 +48,34 @@ class PagedCache:
         self.budget = torch.zeros(S, **i32)
         self.free_list = torch.zeros(n_phys, **i32)
         self.free_count = torch.zeros(1, **i32)
+        # offload tier: offload_pages host-memory pages per session, their
+        # keys in pinned host memory (hipHostMalloc underneath), their
+        # per-token state on the device
+        self.offload_pages = H = int(offload_pages)
+        if H > 0:
+            self.host_keys = torch.zeros((S, H, L * Hkv * P * d), dtype=torch.bfloat16, pin_memory=True)
+            self.off_count = torch.zeros(S, **i32)
+            self.off_serial = torch.full((S, H), -1, **i32)
+            self.off_slot = torch.full((S, H), -1, **i32)
+            self.off_region = torch.zeros((S, H, P), dtype=torch.uint8, device=dev)
+            self.off_t_ins = torch.zeros((S, H, P), **i32)
+            self.off_t_ref = torch.zeros((S, H, P), **i32)
+            self.off_importance = torch.zeros((S, H, P), dtype=torch.float32, device=dev)
+            self.off_format = torch.zeros((S, H), dtype=torch.uint8, device=dev)
+            self.off_score = torch.zeros((S, H), dtype=torch.float32, device=dev)
+            self.off_abar = torch.zeros((S, H, P), dtype=torch.float32, device=dev)
+
+    OFFLOAD_BUFFERS = ("host_keys", "off_count", "off_serial", "off_slot", "off_region", "off_t_ins",
+                       "off_t_ref", "off_importance", "off_format", "off_score", "off_abar")
 
     def view(self) -> B.md_cache_view:
         v = B.md_cache_view()
-        for name in ("k_pool", "region", "t_ins", "t_ref", "importance", "page_table",
-                     "page_serial", "n_pages", "n_tokens", "clock", "next_serial", "budget",
-                     "free_list", "free_count", "n_live", "page_format"):
+        names = ["k_pool", "region", "t_ins", "t_ref", "importance", "page_table",
+                 "page_serial", "n_pages", "n_tokens", "clock", "next_serial", "budget",
+                 "free_list", "free_count", "n_live", "page_format"]
+        if self.offload_pages > 0:
+            names += list(self.OFFLOAD_BUFFERS)
+        for name in names:
             setattr(v, name, getattr(self, name).data_ptr())
         return v
 
@@ -158,7 +180,8 @@ class MemDecay:
                  rho: float, alpha: float, tau_scale: float, pinned_mask: int,
                  n_regions: int = 7, stream: Optional[torch.cuda.Stream] = None,
                  fused: Optional[bool] = None, attention_norm: bool = False, window: int = 1,
-                 region_aligned: bool = False, quant_threshold: float = 0.0, static: bool = False):
+                 region_aligned: bool = False, quant_threshold: float = 0.0, static: bool = False,
+                 drop_threshold: float = 0.0):
         # fused: True = always the fused kernel, False = always the
         # multi-kernel path, None = the library picks from the cache's sizes
         self.cache = cache
@@ -173,7 +196,8 @@ class MemDecay:
                           flags=(0 if fused is None else (B.MD_FLAG_FUSED if fused else B.MD_FLAG_NO_FUSED))
                           | (B.MD_FLAG_NORM_ATTENTION if attention_norm else 0)
                           | (B.MD_FLAG_REGION_ALIGNED if region_aligned else 0),
-                          window=window, quant_threshold=quant_threshold)
+                          window=window, quant_threshold=quant_threshold,
+                          offload_pages=cache.offload_pages, drop_threshold=drop_threshold)
         rp = B.md_region_params(base_priority=self.b.data_ptr(), decay_rate=self.lam.data_ptr())
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
         self._cfg, self._rp, self._cv = cfg, rp, cache.view()

@@ -146,6 +146,10 @@ static md_status validate_config(const md_config* c) {
     if ((c->flags & ~(MD_FLAG_NO_FUSED | MD_FLAG_FUSED | MD_FLAG_NORM_ATTENTION | MD_FLAG_REGION_ALIGNED)) != 0)
         return MD_E_INVALID;
     if ((c->flags & MD_FLAG_NO_FUSED) && (c->flags & MD_FLAG_FUSED)) return MD_E_INVALID;
+    if (c->offload_pages < 0 || c->offload_pages > md::kMaxOffload) return MD_E_INVALID;
+    if (!(c->drop_threshold >= 0.0f)) return MD_E_INVALID;   // NaN too
+    // the offload tier runs with one query per observation on plain pages
+    if (c->offload_pages > 0 && (c->window > 1 || (c->flags & MD_FLAG_REGION_ALIGNED))) return MD_E_UNSUPPORTED;
     if (c->n_layers < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1) return MD_E_INVALID;
     if (c->n_q_heads % c->n_kv_heads != 0) return MD_E_INVALID;
     if (c->max_sessions < 1 || c->max_pages < 1 || c->n_phys_pages < 1) return MD_E_INVALID;
@@ -174,9 +178,19 @@ static md_status validate_config(const md_config* c) {
     return MD_OK;
 }
 
-static md_status validate_view(const md_cache_view* v, bool region_aligned, bool quant) {
+static md_status validate_view(const md_cache_view* v, bool region_aligned, bool quant, bool offload) {
     if (v == nullptr) return MD_E_INVALID;
     if (quant && v->page_format == nullptr) return MD_E_INVALID;
+    if (offload) {
+        const void* op[] = {v->host_keys, v->off_count, v->off_serial, v->off_slot, v->off_region, v->off_t_ins,
+                            v->off_t_ref, v->off_importance, v->off_format, v->off_score, v->off_abar};
+        for (const void* p : op)
+            if (p == nullptr) return MD_E_INVALID;
+        const void* ow[] = {v->host_keys, v->off_count, v->off_serial, v->off_slot, v->off_t_ins, v->off_t_ref,
+                            v->off_importance, v->off_score, v->off_abar};
+        for (const void* p : ow)
+            if (!aligned(p, 16 / (p == v->host_keys ? 1 : 4))) return MD_E_INVALID;
+    }
     if (region_aligned && (v->n_live == nullptr || !aligned(v->n_live, 4) || !aligned(v->region, 4)))
         return MD_E_INVALID;
     const void* ptrs[] = {v->k_pool, v->region, v->t_ins, v->t_ref, v->importance,
@@ -201,7 +215,8 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     *out = nullptr;
     md_status st = validate_config(cfg);
     if (st != MD_OK) return st;
-    st = validate_view(cv, (cfg->flags & MD_FLAG_REGION_ALIGNED) != 0, cfg->quant_threshold > 0.0f);
+    st = validate_view(cv, (cfg->flags & MD_FLAG_REGION_ALIGNED) != 0, cfg->quant_threshold > 0.0f,
+                       cfg->offload_pages > 0);
     if (st != MD_OK) return st;
     if (rp == nullptr || rp->base_priority == nullptr || rp->decay_rate == nullptr) return MD_E_INVALID;
     if (!aligned(rp->base_priority, 4) || !aligned(rp->decay_rate, 4)) return MD_E_INVALID;
@@ -231,6 +246,9 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     dm.aligned = (cfg->flags & MD_FLAG_REGION_ALIGNED) ? 1 : 0;
     dm.quant = cfg->quant_threshold > 0.0f ? 1 : 0;
     dm.quant_thr = cfg->quant_threshold;
+    dm.H = cfg->offload_pages;
+    dm.drop_thr = cfg->drop_threshold;
+    dm.page_bytes = (size_t)dm.LHkv * dm.P * md::kHeadDim * sizeof(uint16_t);
 
     // ---- from here on the HIP runtime is used
     int dev = 0;
@@ -346,6 +364,7 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     if (h == nullptr) return use_static ? MD_E_TOO_LARGE : MD_E_NOMEM;
     if (!use_static) h->static_slot = -1;
     h->dm = dm;
+    h->v = md::View{};
     h->v.k_pool = cv->k_pool;
     h->v.region = cv->region;
     h->v.t_ins = cv->t_ins;
@@ -364,6 +383,26 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     h->v.free_count = cv->free_count;
     h->v.b = rp->base_priority;
     h->v.lam = rp->decay_rate;
+    if (dm.H > 0) {
+        // the pinned host memory's address on the device
+        void* dk = nullptr;
+        if (hipHostGetDevicePointer(&dk, cv->host_keys, 0) != hipSuccess) {
+            (void)hipGetLastError();
+            give_back(h);
+            return MD_E_INVALID;
+        }
+        h->v.host_keys = static_cast<unsigned char*>(dk);
+        h->v.off_count = cv->off_count;
+        h->v.off_serial = cv->off_serial;
+        h->v.off_slot = cv->off_slot;
+        h->v.off_region = cv->off_region;
+        h->v.off_t_ins = cv->off_t_ins;
+        h->v.off_t_ref = cv->off_t_ref;
+        h->v.off_imp = cv->off_importance;
+        h->v.off_format = cv->off_format;
+        h->v.off_score = cv->off_score;
+        h->v.off_abar = cv->off_abar;
+    }
     h->stream = hs;
     h->device = dev;
 
@@ -444,6 +483,7 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
         return md::launch_rowstats(h->dm, h->sc, h->stream); });
     if (e == hipSuccess && multi) e = timed_launch(h, MD_K_MASS, [&] {
         return md::launch_mass(h->dm, h->v, h->sc, abar_out, h->mass_blocks, h->stream); });
+    if (e == hipSuccess && h->dm.H > 0) e = md::launch_recall(h->dm, h->v, h->sc, q, abar_out, h->stream);
     if (e != hipSuccess) return MD_E_HIP;
     h->fused_last = fused && !h->dm.spill;
     h->observed += 1;
@@ -499,6 +539,10 @@ md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* ev
     if (!aligned(evict_serial, 4) || !aligned(evict_count, 4)) return MD_E_INVALID;
     if (h->dm.quant && h->phase != kScored) return MD_E_STATE;   // the tier needs this step's scores
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    if (h->dm.H > 0 && h->phase != kScored) return MD_E_STATE;   // the tier needs this step's scores
+    if (h->dm.H > 0 &&
+        md::launch_offload(h->dm, h->v, h->sc, evict_serial, evict_count, h->stream) != hipSuccess)
+        return MD_E_HIP;
     if (h->dm.quant &&
         md::launch_quant(h->dm, h->v, h->sc, evict_serial, evict_count, h->stream) != hipSuccess)
         return MD_E_HIP;
@@ -616,11 +660,11 @@ md_status md_calib_fit(const uint64_t* mass_fx, const uint64_t* count, const uin
 md_status md_read_counters(md_handle h, int64_t* out) {
     if (h == nullptr || out == nullptr) return MD_E_INVALID;
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
-    unsigned long long v[4] = {0, 0, 0, 0};
+    unsigned long long v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if (hipMemcpyAsync(v, h->sc.counters, sizeof(v), hipMemcpyDeviceToHost, h->stream) != hipSuccess ||
         hipStreamSynchronize(h->stream) != hipSuccess)
         return MD_E_HIP;
-    for (int i = 0; i < 4; ++i) out[i] = (int64_t)v[i];
+    for (int i = 0; i < 8; ++i) out[i] = (int64_t)v[i];
     return MD_OK;
 }
 

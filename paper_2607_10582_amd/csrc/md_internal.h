@@ -26,6 +26,8 @@ inline int attend_unit_tokens(int) { return 256; }
 constexpr int kConsumeLag = 7;   // rows a unit runs ahead of the row it normalises
 constexpr int kRowBufs = kConsumeLag + 1;       // rows of logits held in LDS
 
+constexpr int kMaxOffload = 64;     // host-tier pages per session at most (one 64-bit slot mask)
+
 constexpr int kDevCorrupt = MD_DEV_CORRUPT;
 constexpr int kHole = MD_REGION_HOLE;   // region code of a hole slot (region-aligned pages)
 
@@ -39,6 +41,9 @@ struct Dims {
     int aligned;   // 1: region-aligned pages (hole slots; n_live counts the tokens)
     int quant;     // 1: quantised tier on (pages may hold 8-bit codes)
     float quant_thr;  // quantised tier: pages scoring below it are quantised
+    int H;         // offload tier: host-memory pages per session (0: off)
+    float drop_thr;   // offload tier: pages scoring below it are dropped
+    size_t page_bytes;  // bytes of one page's keys, L * Hkv * P * d * 2
     int n_wg;      // k_attend workgroups (all co-resident)
     int wg_per_cu; // k_attend workgroups per CU (n_wg = wg_per_cu * CUs)
     int lane_cap;  // units one lane of k_attend workgroups holds (one workgroup per CU)
@@ -67,6 +72,19 @@ struct View {
     int32_t* free_count;
     const float* b;
     const float* lam;
+    // offload tier (H > 0): the keys of host-memory pages and their
+    // per-token state, indexed by (session, host slot)
+    unsigned char* host_keys;  // device address of the pinned host memory [S][H][page_bytes]
+    int32_t* off_count;        // [S] pages in host memory
+    int32_t* off_serial;       // [S][H] their serials, ascending
+    int32_t* off_slot;         // [S][H] host slot of each listed page
+    uint8_t* off_region;       // [S][H][P] by host slot
+    int32_t* off_t_ins;
+    int32_t* off_t_ref;
+    float* off_imp;
+    uint8_t* off_format;       // [S][H] by host slot
+    float* off_score;          // [S][H] page score of each listed page
+    float* off_abar;           // [S][H][P] by host slot: the step's mass
 };
 
 struct Scratch {
@@ -94,7 +112,10 @@ struct Scratch {
     int32_t* warn;         // [1] warning bits (1: some session's budget was infeasible)
     int32_t* done_compact; // [1] completion counter of the compaction kernel
     int32_t* opened;       // [1] pages the append kernel takes from the free list
-    unsigned long long* counters;  // [4] tokens scored, steps, pages evicted, tokens evicted
+    unsigned long long* counters;  // [8] tokens scored, steps, pages evicted, tokens evicted, pages
+                                   // offloaded, recalled, dropped from host memory, observed there
+    int32_t* recall;       // [S][H] offload tier: the listed page is recalled at this step
+    int32_t* rcount;       // [S] pages each session recalls at this step
 };
 
 size_t scratch_bytes(const Dims& dm);
@@ -140,5 +161,14 @@ hipError_t launch_compact(const Dims& dm, const View& v, const Scratch& sc,
 // Quantised tier, before the compaction of the same eviction lists.
 hipError_t launch_quant(const Dims& dm, const View& v, const Scratch& sc,
                         const int32_t* ev_serial, const int32_t* ev_count, hipStream_t st);
+// Offload tier.  At an observation, after the attention: launch_recall
+// observes the host-memory pages and recalls those that became relevant
+// (q: the step's queries, abar_out: optional masses).  At md_compact,
+// before the quantised tier and the compaction: launch_offload drops
+// host-memory pages below the threshold and moves leaving pages there.
+hipError_t launch_recall(const Dims& dm, const View& v, const Scratch& sc, const float* q, float* abar_out,
+                         hipStream_t st);
+hipError_t launch_offload(const Dims& dm, const View& v, const Scratch& sc, const int32_t* ev_serial,
+                          const int32_t* ev_count, hipStream_t st);
 
 }  // namespace md

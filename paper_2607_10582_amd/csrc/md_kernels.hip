@@ -1331,7 +1331,9 @@ size_t scratch_bytes(const Dims& dm) {
     n += align256((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long));
     n += align256((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long));
     n += align256(5 * sizeof(int32_t));
-    n += align256(4 * sizeof(unsigned long long));
+    n += align256(8 * sizeof(unsigned long long));
+    n += align256((size_t)dm.S * dm.H * sizeof(int32_t));
+    n += align256((size_t)(dm.S + 1) * sizeof(int32_t));
     return n;
 }
 
@@ -1369,7 +1371,9 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
     sc->warn = words + 2;
     sc->done_compact = words + 3;
     sc->opened = words + 4;
-    sc->counters = reinterpret_cast<unsigned long long*>(take(4 * sizeof(unsigned long long)));
+    sc->counters = reinterpret_cast<unsigned long long*>(take(8 * sizeof(unsigned long long)));
+    sc->recall = reinterpret_cast<int32_t*>(take((size_t)dm.S * dm.H * sizeof(int32_t)));
+    sc->rcount = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
 }
 
 }  // namespace md

@@ -87,6 +87,9 @@ class Stats:
     tau_excused: int = 0
     tie_excused: int = 0
     evicted_pages: int = 0
+    offloaded: int = 0        # offload tier: pages moved to host memory,
+    recalled: int = 0         # recalled from it,
+    dropped: int = 0          # dropped from it
 
     def bump(self, key, arr):
         if arr.size:
@@ -101,7 +104,8 @@ class Pair:
                  regions=None, planted: int = 0, planted_strength=3.0, query_gain=0.0,
                  pinned_mask=None, alpha=None, n_phys_extra: int = 0, max_pages=None,
                  steps=None, fused: Optional[bool] = True, priors=None, strict_ties: bool = False,
-                 check_free_list: bool = False, static: bool = False, pool: int = 0):
+                 check_free_list: bool = False, static: bool = False, pool: int = 0,
+                 offload_pages: int = 0, drop_threshold: float = 0.0):
         # pool > 0: the oracle sessions run in that many worker processes
         # (oracle.pool), all sessions of a step at once
         self.w = w
@@ -131,7 +135,8 @@ class Pair:
         grow = self.steps if al else (self.steps + P - 1) // P
         mp = max(max(pages) + grow + 1, 1) if max_pages is None else max_pages
         self.cache = PagedCache(L=w.L, Hq=w.Hq, Hkv=w.Hkv, d=w.d, P=P, S=S, max_pages=mp,
-                                n_phys=n_phys, device=self.dev)
+                                n_phys=n_phys, device=self.dev, offload_pages=offload_pages)
+        self.offload_pages = offload_pages
         perm = g.page_permutation(w, n_phys)
         pos = 0
         self.oracles: Dict[int, oracle.Session] = {}
@@ -163,7 +168,8 @@ class Pair:
                           alpha=f32(self.alpha), rho=f32(w.rho), tau_scale=f32(w.tau_scale),
                           pinned_mask=self.pinned_mask, budget=int(self.B[s]), clock=n0, region=reg,
                           capacity=n0 + self.steps, attention_norm=w.attention_norm, region_aligned=al,
-                          quant_threshold=w.quant_threshold)
+                          quant_threshold=w.quant_threshold, offload_pages=offload_pages,
+                          drop_threshold=drop_threshold)
                 kbs = kb if n0 else np.zeros((0, w.L, w.Hkv, w.d), np.uint16)
                 if self.pool is not None:
                     self.pool.add(s, kw, kbs, n0)
@@ -175,7 +181,7 @@ class Pair:
                            rho=f32(w.rho), alpha=f32(self.alpha), tau_scale=f32(w.tau_scale),
                            pinned_mask=self.pinned_mask, fused=fused, attention_norm=w.attention_norm,
                            window=w.window, region_aligned=al, quant_threshold=w.quant_threshold,
-                           static=static)
+                           static=static, drop_threshold=f32(drop_threshold))
         n_slots = n_phys * P
         self.abar = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
         self.tscore = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
@@ -267,7 +273,7 @@ class Pair:
             if not compare:
                 continue
             npg, nt = int(host["n_pages"][s]), int(host["n_live"][s])
-            assert nt == rec.n, (k, s, nt, rec.n)
+            assert nt == rec.n_select, (k, s, nt, rec.n_select)
             ptab = host["page_table"][s, :npg].astype(np.int64)
             pser = host["page_serial"][s, :npg]
             assert pser.tolist() == rec.page_serial.tolist(), (k, s)
@@ -330,6 +336,8 @@ class Pair:
                                                   ser_, rec.page_score[i], thr)
                 st.tie_excused += len(diff)
             st.evicted_pages += len(rec.evicted)
+            if self.offload_pages:
+                self.check_offloaded_observation(s, rec)
             final_ser[s, :] = 0
             final_ser[s, :len(rec.evicted)] = rec.evicted
             final_cnt[s] = len(rec.evicted)
@@ -353,8 +361,64 @@ class Pair:
                 assert pser[s, :n_pages[s]].tolist() == [x for x in rec.page_serial.tolist() if x not in gone], (k, s)
                 if w.quant_threshold > 0:
                     self.check_quantised(s, quant_before[s])
+                if self.offload_pages:
+                    self.check_offloaded_after(s, rec)
         self.stats.steps += 1
         return self.stats
+
+    # -------------------------------------------------------------- offload tier
+    def off_list(self, s: int):
+        c = self.cache
+        n = int(c.off_count[s].item())
+        return c.off_serial[s, :n].cpu().numpy(), c.off_slot[s, :n].cpu().numpy()
+
+    def check_offloaded_observation(self, s: int, rec):
+        """After the observation: the pages in host memory (recalled ones
+        gone), their tokens' mass, importance and refresh clock, and their
+        page scores, against the oracle's."""
+        c, P, k = self.cache, self.w.P, self.k
+        ser, slot = self.off_list(s)
+        assert ser.tolist() == rec.off_serial.tolist(), (k, s, "pages in host memory", ser, rec.off_serial)
+        if not ser.size:
+            return
+        st = self.stats
+        abar = c.off_abar[s].cpu().numpy()[slot].reshape(-1)
+        e = rel_err(abar, rec.off_abar)
+        st.bump("abar", e)
+        assert np.all(e <= REL), (k, s, "host-memory abar", float(e.max()))
+        a = c.off_importance[s].cpu().numpy()[slot].reshape(-1)
+        e = rel_err(a, rec.off_a)
+        st.bump("a", e)
+        assert np.all(e <= REL), (k, s, "host-memory importance", float(e.max()))
+        tref = c.off_t_ref[s].cpu().numpy()[slot].reshape(-1)
+        assert np.array_equal(tref, rec.off_t_ref), (k, s, "host-memory refresh clocks")
+        ps = c.off_score[s, :ser.size].cpu().numpy()
+        e = rel_err(ps, rec.off_page_score)
+        st.bump("page", e)
+        assert np.all(e <= REL), (k, s, "host-memory page scores", float(e.max()))
+
+    def check_offloaded_after(self, s: int, rec):
+        """After the compaction: the pages in host memory, and the keys of
+        those moved there this step, bit for bit."""
+        c, w = self.cache, self.w
+        ser, slot = self.off_list(s)
+        assert ser.tolist() == rec.off_after.tolist(), (self.k, s, "host memory after", ser, rec.off_after)
+        self.stats.offloaded += len(rec.offloaded_now)
+        self.stats.recalled += len(rec.recalled)
+        self.stats.dropped += len(rec.dropped)
+        o = self.oracles.get(s)
+        if o is None or not rec.offloaded_now.size:
+            return
+        pages = {p.serial: p for p in o.offloaded}
+        for x in rec.offloaded_now.tolist():
+            p = pages[x]
+            if p.quant:
+                continue
+            j = int(slot[int(np.flatnonzero(ser == x)[0])])
+            keys = np.asarray(o.keys[:, :, p.slots, :]).transpose(2, 0, 1, 3)          # [P][L][Hkv][d]
+            want = PagedCache.to_pool_layout(torch.from_numpy(keys.astype(np.int16)).view(1, w.P, w.L, w.Hkv, w.d))
+            got = c.host_keys[s, j].view(torch.int16)
+            assert torch.equal(got, want.reshape(-1)), (self.k, s, x, "keys in host memory")
 
     def check_quantised(self, s: int, before):
         """Quantised tier: the device's page formats equal the oracle's, and

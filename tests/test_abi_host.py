@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert B.md_abi_version() == 6
+    assert B.md_abi_version() == 7
     for st in (0, -1, -2, -3, -4, -5, -6):
         assert B.md_status_str(st)
     assert B.md_status_str(12345) == "unknown status"
@@ -59,8 +59,10 @@ def test_struct_layout_matches_the_header(lib):
       printf("%zu %zu %zu %zu %zu %zu %zu\n", sizeof(md_config), offsetof(md_config, rho),
              offsetof(md_config, flags), offsetof(md_config, window),
              offsetof(md_config, quant_threshold), sizeof(md_region_params), sizeof(md_cache_view));
-      printf("%zu %zu %zu %zu\n", offsetof(md_cache_view, importance), offsetof(md_cache_view, free_count),
-             offsetof(md_cache_view, n_live), offsetof(md_cache_view, page_format));
+      printf("%zu %zu %zu %zu %zu %zu %zu\n", offsetof(md_cache_view, importance), offsetof(md_cache_view, free_count),
+             offsetof(md_cache_view, n_live), offsetof(md_cache_view, page_format),
+             offsetof(md_cache_view, host_keys), offsetof(md_cache_view, off_abar),
+             offsetof(md_config, drop_threshold));
       return 0; }
     '''
     with tempfile.TemporaryDirectory() as d:
@@ -73,7 +75,8 @@ def test_struct_layout_matches_the_header(lib):
            B.md_config.window.offset, B.md_config.quant_threshold.offset,
            ctypes.sizeof(B.md_region_params), ctypes.sizeof(B.md_cache_view),
            B.md_cache_view.importance.offset, B.md_cache_view.free_count.offset,
-           B.md_cache_view.n_live.offset, B.md_cache_view.page_format.offset]
+           B.md_cache_view.n_live.offset, B.md_cache_view.page_format.offset,
+           B.md_cache_view.host_keys.offset, B.md_cache_view.off_abar.offset, B.md_config.drop_threshold.offset]
     assert [int(x) for x in out] == got
 
 
@@ -126,16 +129,33 @@ def fake_rp():
     (dict(window=2, flags=2 | 8), B.MD_E_UNSUPPORTED),   # fused with a window: plain pages only
     (dict(window=2, flags=2, quant_threshold=0.5), B.MD_E_UNSUPPORTED),
     (dict(flags=3), B.MD_E_INVALID),
+    (dict(offload_pages=-1), B.MD_E_INVALID),
+    (dict(offload_pages=65), B.MD_E_INVALID),
+    (dict(offload_pages=4, drop_threshold=-0.5), B.MD_E_INVALID),
+    (dict(offload_pages=4, drop_threshold=float("nan")), B.MD_E_INVALID),
+    (dict(offload_pages=4, window=2), B.MD_E_UNSUPPORTED),          # the tier takes one query per observation
+    (dict(offload_pages=4, flags=8), B.MD_E_UNSUPPORTED),           # and plain pages
 ])
 def test_init_rejects_bad_configs_on_the_host(lib, kw, expect):
     st, h = B.md_init_raw(good_config(**kw), fake_rp(), fake_view(), 0)
     assert st == expect and h is None
 
 
-@pytest.mark.parametrize("field", [f for f, _ in B.md_cache_view._fields_ if f not in ("n_live", "page_format")])
+OPTIONAL = ("n_live", "page_format", "host_keys", "off_count", "off_serial", "off_slot", "off_region", "off_t_ins",
+            "off_t_ref", "off_importance", "off_format", "off_score", "off_abar")
+
+
+@pytest.mark.parametrize("field", [f for f, _ in B.md_cache_view._fields_ if f not in OPTIONAL])
 def test_init_rejects_null_buffers(lib, field):
     st, h = B.md_init_raw(good_config(), fake_rp(), fake_view(**{field: 0}), 0)
     assert st == B.MD_E_INVALID
+
+
+@pytest.mark.parametrize("field", ["host_keys", "off_count", "off_serial", "off_slot", "off_region", "off_t_ins",
+                                   "off_t_ref", "off_importance", "off_format", "off_score", "off_abar"])
+def test_offload_tier_needs_its_buffers(lib, field):
+    st, h = B.md_init_raw(good_config(offload_pages=4), fake_rp(), fake_view(**{field: 0}), 0)
+    assert st == B.MD_E_INVALID and h is None
 
 
 def test_quantised_tier_needs_the_page_formats(lib):

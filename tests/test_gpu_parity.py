@@ -558,3 +558,67 @@ def test_physical_pages_are_reproducible():
         p.close()
     for (t1, f1, c1), (t2, f2, c2) in zip(*runs):
         assert np.array_equal(t1, t2) and c1 == c2 and np.array_equal(f1[:c1], f2[:c2])
+
+
+# ---------------------------------------------------------------- offload tier
+
+def run_offload(p: Pair, steps: int, label: str):
+    say(f"[{label}] S={p.w.S} L={p.w.L} Hq={p.w.Hq} P={p.w.P} host pages {p.offload_pages} steps={steps}")
+    for _ in range(steps):
+        st = p.step()
+    assert p.device_status() == 0 and p.free_pages_consistent()
+    c = p.md.counters()
+    say(f"[{label}] ok: {st.steps} steps, max rel {st.max_rel}, evicted {st.evicted_pages}, offloaded "
+        f"{st.offloaded}, recalled {st.recalled}, dropped {st.dropped}; device counters {c}")
+    if len(p.oracle_sessions) == p.w.S:   # the counters cover every session
+        assert c[4] == st.offloaded and c[5] == st.recalled and c[6] == st.dropped
+    p.close()
+    return st
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_offload_tier_small_batch(fused):
+    # The offload tier (Sec. III-E's second tier): three sessions, keys
+    # planted so that attention moves between tokens; pages leaving the
+    # cache go to host memory (8 per session) and come back when a token's
+    # mass next to the cached tokens reaches tau.  Everything is compared
+    # with the oracle at every step, the host-memory list, its tokens'
+    # state and scores and the copied keys included.
+    w = C.with_overrides(C.get("small"), S=3, n0=None, n0_range=(1, 2), steps=48, system_len=60)
+    p = Pair(w, n0s=[450, 700, 300], budgets=[225, 300, 200], planted=24, planted_strength=2.5, query_gain=0.7,
+             fused=fused, offload_pages=8, drop_threshold=1e-3)
+    st = run_offload(p, 48, f"offload-small-fused{int(fused)}")
+    assert st.offloaded > 30 and st.recalled > 20
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_offload_tier_drops_pages_below_the_threshold(fused):
+    # a larger refresh scale (tau = 8 / |K_t|) keeps most host-memory pages
+    # from coming back, so they age below the drop threshold and are dropped
+    w = C.with_overrides(C.get("small"), S=2, n0=None, n0_range=(1, 2), steps=48, tau_scale=8.0)
+    p = Pair(w, n0s=[450, 600], budgets=[225, 240], planted=24, planted_strength=2.5, query_gain=0.7,
+             fused=fused, offload_pages=4, drop_threshold=0.05)
+    st = run_offload(p, 48, f"offload-drops-fused{int(fused)}")
+    assert st.offloaded > 5 and st.dropped > 0
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_offload_tier_with_quantised_pages_of_64(fused):
+    # 3B shape, pages of 64, the quantised tier on: quantised pages move to
+    # host memory as codes and scales and come back unchanged
+    w = C.with_overrides(C.get("small"), L=2, Hq=16, Hkv=2, P=64, n0=900, budget_frac=0.6,
+                         append_cycle=C.APPEND_CYCLE, quant_threshold=0.4, steps=20)
+    p = Pair(w, planted=24, planted_strength=2.5, query_gain=0.7, fused=fused, offload_pages=8, drop_threshold=1e-3)
+    st = run_offload(p, 20, f"offload-quant-p64-fused{int(fused)}")
+    assert st.offloaded > 10 and st.recalled > 5
+
+
+def test_offload_tier_long32k_sampled_sessions():
+    # the 16 x 32,768-token batch with 16 host-memory pages per session and
+    # no drop threshold: the bulk eviction fills host memory with the best
+    # of the 1,536 pages each session evicts, later steps observe them
+    w = C.get("long32k")
+    p = Pair(w, backend="torch", oracle_sessions=[0, 11], steps=6, fused=True, offload_pages=16,
+             drop_threshold=0.0)
+    st = run_offload(p, 4, "offload-long32k")
+    assert st.offloaded >= 32
