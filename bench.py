@@ -69,7 +69,7 @@ def describe(w, n0s) -> str:
             f"budget {int(w.budget_frac * 100)}%, {w.steps} decode steps")
 
 
-def setup(w, steps_total, dev, fused=None):
+def setup(w, steps_total, dev, fused=None, offload_pages=0, drop_threshold=0.0):
     import torch
     from paper_2607_10582_amd.cache import MemDecay, PagedCache
     from synth import configs as C
@@ -86,7 +86,7 @@ def setup(w, steps_total, dev, fused=None):
     grow = steps_total if w.region_aligned else (steps_total + w.P - 1) // w.P
     max_pages = max(pages) + grow + 1
     cache = PagedCache(L=w.L, Hq=w.Hq, Hkv=w.Hkv, d=w.d, P=w.P, S=w.S, max_pages=max_pages,
-                       n_phys=n_phys, device=dev)
+                       n_phys=n_phys, device=dev, offload_pages=offload_pages)
     perm = g.page_permutation(w, n_phys)
     pos = 0
     for s in range(w.S):
@@ -103,7 +103,7 @@ def setup(w, steps_total, dev, fused=None):
         return MemDecay(cache, torch.from_numpy(b), torch.from_numpy(lam), rho=w.rho, alpha=w.alpha,
                         tau_scale=w.tau_scale, pinned_mask=w.pinned_mask, fused=fused,
                         region_aligned=w.region_aligned, quant_threshold=w.quant_threshold,
-                        attention_norm=w.attention_norm, window=w.window)
+                        attention_norm=w.attention_norm, window=w.window, drop_threshold=drop_threshold)
 
     inputs = []
     for k in range(1, steps_total + 1):
@@ -121,6 +121,8 @@ def setup(w, steps_total, dev, fused=None):
              "n_live", "page_format", "clock", "next_serial", "budget", "free_list", "free_count"]
     if w.quant_threshold > 0:
         names.append("k_pool")
+    if offload_pages > 0:
+        names += list(PagedCache.OFFLOAD_BUFFERS)
     snap = {n: getattr(cache, n).clone() for n in names}
     for r in range(3):
         md = make_md()
@@ -241,7 +243,7 @@ def calibrate_copy(mib: int):
     log(f"copied {n} bytes 5 times")
 
 
-def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0):
+def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0, offload_pages=0, drop_threshold=0.0):
     """One trajectory of workload w from a fresh cache: steps 1..W (warm-up;
     step 1 the bulk eviction), W+1..W+K timed, then on to the workload's
     last step.  Returns the record (value, roofline, step times)."""
@@ -251,7 +253,8 @@ def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0):
 
     total = max(w.steps, W + K)
     t_setup = time.perf_counter()
-    n0s, B, cache, md, inputs = setup(w, total, dev, fused=False if multi_kernel else None)
+    n0s, B, cache, md, inputs = setup(w, total, dev, fused=False if multi_kernel else None,
+                                      offload_pages=offload_pages, drop_threshold=drop_threshold)
     log(f"setup {time.perf_counter() - t_setup:.1f} s: {describe(w, n0s)}")
     stream = md.stream
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(total + 1)]
@@ -370,6 +373,19 @@ def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0):
         "step_algorithmic_gbs": step_bytes / wall / 1e9,
         "step_frac_of_peak": step_bytes / wall / 1e9 / PEAK_HBM_GBS,
     }
+    if offload_pages > 0:
+        # offload tier: pages moved over the host link in the timed steps,
+        # each a page of keys (L Hkv P d bf16 values): to host memory,
+        # back from it, and read by the observation of host-memory pages
+        page_bytes = w.L * w.Hkv * w.P * w.d * 2
+        moved = (c1[4] - c0[4]) + (c1[5] - c0[5]) + (c1[7] - c0[7])
+        rec["offload"] = {"host_pages_per_session": offload_pages, "drop_threshold": drop_threshold,
+                          "pages_offloaded_per_step": (c1[4] - c0[4]) / K,
+                          "pages_recalled_per_step": (c1[5] - c0[5]) / K,
+                          "pages_dropped_per_step": (c1[6] - c0[6]) / K,
+                          "host_pages_observed_per_step": (c1[7] - c0[7]) / K,
+                          "host_link_bytes_per_step": moved * page_bytes / K,
+                          "host_link_gbs": moved * page_bytes / wall / 1e9}
     md.close()
     del cache, inputs, md
     torch.cuda.synchronize(dev)
@@ -397,6 +413,10 @@ def main():
                          "observation, in age buckets of this many steps, and time it")
     ap.add_argument("--quant-threshold", type=float, default=None,
                     help="quantised tier: override the workload's threshold (0: off)")
+    ap.add_argument("--offload-pages", type=int, default=0,
+                    help="offload tier: host-memory pages per session (0: off)")
+    ap.add_argument("--drop-threshold", type=float, default=0.0,
+                    help="offload tier: pages scoring below it are dropped, not kept in host memory")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -429,7 +449,8 @@ def main():
         log("note: the warm-up includes step 1, the bulk eviction; --warmup raised to 1")
         W = 1
 
-    main_rec, n0s, B = measure(w, W, K, dev, multi_kernel=args.multi_kernel, calibrate=args.calibrate)
+    main_rec, n0s, B = measure(w, W, K, dev, multi_kernel=args.multi_kernel, calibrate=args.calibrate,
+                               offload_pages=args.offload_pages, drop_threshold=args.drop_threshold)
     subs = {}
     for name in also:
         rec, _, _ = measure(C.get(name), W, K, dev, multi_kernel=args.multi_kernel)
@@ -461,6 +482,8 @@ def main():
                 "pages_evicted", "first_step_ms", "steady_step_ms_mean", "step_ms_median", "run_mean_ms",
                 "run_steps", "calib_us_per_observation", "step_algorithmic_gbs", "step_frac_of_peak"):
         line[key] = main_rec[key]
+    if "offload" in main_rec:
+        line["offload"] = main_rec["offload"]
     line["workloads"] = subs
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, n0s, B, args.cpu_seconds)

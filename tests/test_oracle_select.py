@@ -1,9 +1,11 @@
 """Pins of the oracle's eviction (Sec. III-D, Alg. 1, Eq. 1).
 
-* Brute force over every subset of non-pinned pages: with equal-size pages
-  the greedy ascending-S_p rule is optimal for the page-level objective
-  (the paper's claim), and with one-token pages it keeps the top-B tokens
-  after forcing the pinned set (the token-level optimum of Eq. 1).
+* Brute force over every subset of non-pinned pages: when every page holds
+  the same number of tokens, evicting pages in ascending S_p order keeps a
+  total page score no smaller than any other set of pages meeting the budget
+  (Sec. III-D, Eq. 1 taken at page granularity), and
+  with one-token pages it keeps the top-B tokens after forcing the pinned
+  set (the token-level optimum of Eq. 1).
 * Invariants on whole runs of the synthetic workloads: pinned pages are
   never evicted, the budget is met with retained n in (B - P, B], the
   evicted set is the ascending-(S_p, serial) prefix, compaction keeps the
