@@ -94,6 +94,8 @@ struct Lds {
     float2* wstat;    // [2][W][16] per-wave row statistics
     float2* norm;     // [2][16] row normalisers (M, 1 / Lambda)
     int* vflag;       // [1] the unit's step is void: a non-finite query, or a wait ran out
+    int* claim;       // [32] lane mode: the next pass claimed early (sessions [0], [1];
+                      // [24] set when it was), and claim_sessions' bookkeeping
 };
 
 __host__ __device__ inline size_t rowbuf_bytes(int G, int W, int KT) {
@@ -103,6 +105,7 @@ __host__ __device__ inline size_t qs_bytes(int G) { return (size_t)2 * 3 * G * 6
 __host__ __device__ inline size_t wstat_bytes(int W) { return (size_t)2 * W * 16 * sizeof(float2); }
 constexpr size_t kNormBytes = (size_t)2 * 16 * sizeof(float2);
 constexpr size_t kFlagBytes = 16;
+constexpr size_t kClaimBytes = 32 * sizeof(int);
 
 __device__ __forceinline__ Lds carve(unsigned char* smem, int G, int W, int KT) {
     Lds l;
@@ -116,6 +119,8 @@ __device__ __forceinline__ Lds carve(unsigned char* smem, int G, int W, int KT) 
     l.norm = reinterpret_cast<float2*>(smem + o);
     o += kNormBytes;
     l.vflag = reinterpret_cast<int*>(smem + o);
+    o += kFlagBytes;
+    l.claim = reinterpret_cast<int*>(smem + o);
     return l;
 }
 
@@ -177,6 +182,8 @@ struct Unit {
     int nl_s;            // region-aligned pages: the session's tokens |K_t| (nt_s counts holes too)
 };
 
+__device__ void claim_sessions(const AttendArgs& a, int* xs, int lane_no, int cap);
+
 // First query row (layer * Hq + KV head * G) of (layer, KV head) row r:
 // with Hq = Hkv * G that is r * G.
 __device__ __forceinline__ int qrow0(const AttendDims& dm, int r) { return r * dm.G; }
@@ -188,9 +195,13 @@ __device__ __forceinline__ int qrow0(const AttendDims& dm, int r) { return r * d
 // decode queries (column c of a row is window query c / Gq, head c % Gq, and
 // a causal mask keeps each query to the tokens inserted by its step);
 // separate instantiations keep the plain kernel's register budget.
+// next_box (lane mode, the lane's first workgroup; else NULL): the lane's
+// next pass is claimed with claim_lane and cap once the unit's rows are
+// done, and published there.
 template <int W, int NH, int KT, bool AL, bool QT, bool WN>
 __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendArgs& a, const Lds& sm,
-                                            const Unit& un, int wv, int lane, uint32_t tag) {
+                                            const Unit& un, int wv, int lane, uint32_t tag, int claim_lane,
+                                            int cap, unsigned long long* next_box) {
     constexpr int KQ = (W * NH * 32 + 64 * W - 1) / (64 * W);   // float4 of the query row per lane
     const int G = dm.G;
     const int h = lane & 15;          // MFMA column: query head of the group
@@ -653,6 +664,19 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     }
     if (row < dm.LHkv) do_row(ringA, row);
 
+    // ---- lane mode: the lane's next pass, claimed before this unit's
+    // drain, so that the lane's other workgroups find it published as they
+    // finish (claimed after the drain, they waited for it about 10 us)
+    if (next_box != nullptr) {
+        claim_sessions(a, sm.claim, claim_lane, cap);
+        if (threadIdx.x == 0) {
+            __hip_atomic_store(next_box,
+                               ((unsigned long long)tag << 32) | ((uint32_t)sm.claim[0] << 16) | (uint32_t)sm.claim[1],
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            sm.claim[24] = 1;
+        }
+    }
+
     // ---- iterations without tiles, until the last row is normalised
     for (int r = dm.LHkv; r < dm.LHkv + kConsumeLag; ++r) {
         use_loads(r);
@@ -837,6 +861,7 @@ k_attend(AttendDims dm, AttendArgs a) {
     const int lane_no = lanes ? (int)blockIdx.x / dm.n_cu : 0;
     const int w = lanes ? (int)blockIdx.x % dm.n_cu : (int)blockIdx.x;
     const int cap = lanes ? dm.n_cu : 0;
+    if (threadIdx.x == 0) sm.claim[24] = 0;   // ordered before its reads by the barrier below
     for (int ps = 0;; ++ps) {
         lds_sync();   // the previous unit is done with the LDS
         if (threadIdx.x == 0) *sm.vflag = 0;   // ordered before the unit by the barriers below
@@ -846,10 +871,16 @@ k_attend(AttendDims dm, AttendArgs a) {
             sb = a.plan[2 + 3 * ps];
             se = a.plan[3 + 3 * ps];
         } else {
-            if (w == 0 && ps > 0) claim_sessions(a, xs, lane_no, cap);
+            // the lane's first workgroup claimed this pass during its last
+            // unit (unless that pass gave it no unit)
+            const bool ahead = w == 0 && ps > 0 && sm.claim[24] != 0;
+            if (w == 0 && ps > 0 && !ahead) claim_sessions(a, xs, lane_no, cap);
             if (threadIdx.x == 0) {
                 unsigned long long* box = a.lane_box + (size_t)lane_no * (dm.S + 1) + ps;
-                if (w == 0 && ps > 0) {
+                if (ahead) {
+                    xs[0] = sm.claim[0];
+                    xs[1] = sm.claim[1];
+                } else if (w == 0 && ps > 0) {
                     __hip_atomic_store(box, ((unsigned long long)tag << 32) | ((uint32_t)xs[0] << 16) | (uint32_t)xs[1],
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 } else {
@@ -873,6 +904,7 @@ k_attend(AttendDims dm, AttendArgs a) {
             __syncthreads();
             sb = xs[0];
             se = xs[1];
+            if (threadIdx.x == 0 && ahead) sm.claim[24] = 0;   // read by all threads before the barrier above
             if (sb >= se) break;
         }
         const int u0 = a.ustart[sb];
@@ -893,7 +925,9 @@ k_attend(AttendDims dm, AttendArgs a) {
         // arithmetic is not hoisted out of the pass loop and kept live.
         int lane = (int)threadIdx.x & 63;
         asm volatile("" : "+v"(lane));
-        attend_wave<W, NH, KT, AL, QT, WN>(dm, a, sm, un, wv, lane, tag);
+        unsigned long long* next_box =
+            (lanes && w == 0) ? a.lane_box + (size_t)lane_no * (dm.S + 1) + ps + 1 : nullptr;
+        attend_wave<W, NH, KT, AL, QT, WN>(dm, a, sm, un, wv, lane, tag, lane_no, cap, next_box);
     }
 }
 
@@ -902,7 +936,7 @@ k_attend(AttendDims dm, AttendArgs a) {
 size_t attend_lds_bytes(int G) {
     const int W = attend_threads(G) / 64;
     return rowbuf_bytes(G, W, attend_unit_tokens(G) / (16 * W)) + qs_bytes(G) + wstat_bytes(W) + kNormBytes +
-           kFlagBytes;
+           kFlagBytes + kClaimBytes;
 }
 
 namespace {

@@ -230,15 +230,21 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         s_n[s2] = ok ? nt : 0;
         s_pass[s2] = -1;
     }
-    // Lane mode when every fused session fits one lane (one workgroup per
-    // CU): each lane then claims whole sessions as it goes (see k_attend).
+    // Lane mode when every fused session fits half a lane (one workgroup
+    // per CU): each lane then claims whole sessions as it goes (see
+    // k_attend), at least two per pass.  A larger session would leave the
+    // rest of its lane idle for the whole pass (a 32,769-token session is
+    // 129 units: one per lane pass, half of the grid idle), so steps with
+    // such sessions, typically the first observation of long prompts, run
+    // the plan's passes over the whole grid instead, which pack them closer
+    // and let each workgroup start its next unit as soon as it is done.
     __shared__ int s_lane_ok;
     if (threadIdx.x == 0) s_lane_ok = fused && dm.wg_per_cu >= 2;
     __syncthreads();
     if (fused) {
         for (int s2 = threadIdx.x; s2 < dm.S; s2 += blockDim.x) {
             const int u = (s_n[s2] + dm.T - 1) / dm.T;
-            if (u > dm.lane_cap) atomicExch(&s_lane_ok, 0);
+            if (2 * u > dm.lane_cap) atomicExch(&s_lane_ok, 0);
             if (u <= dm.n_wg) s_pass[s2] = 0;
         }
     }
