@@ -96,6 +96,7 @@ struct Lds {
     int* vflag;       // [1] the unit's step is void: a non-finite query, or a wait ran out
     int* claim;       // [32] lane mode: the next pass claimed early (sessions [0], [1];
                       // [24] set when it was), and claim_sessions' bookkeeping
+    float* wmax;      // [kRowBufs][W][head slots] each wave's maximum of the held rows per head
 };
 
 __host__ __device__ inline size_t rowbuf_bytes(int G, int W, int KT) {
@@ -106,6 +107,11 @@ __host__ __device__ inline size_t wstat_bytes(int W) { return (size_t)2 * W * 16
 constexpr size_t kNormBytes = (size_t)2 * 16 * sizeof(float2);
 constexpr size_t kFlagBytes = 16;
 constexpr size_t kClaimBytes = 32 * sizeof(int);
+// head slots of a wave's row maxima: W NH of the instantiation for G columns
+__host__ __device__ inline int head_slots(int G) { return G <= 4 ? 4 : G <= 8 ? 8 : 16; }
+__host__ __device__ inline size_t wmax_bytes(int G, int W) {
+    return (size_t)kRowBufs * W * head_slots(G) * sizeof(float);
+}
 
 __device__ __forceinline__ Lds carve(unsigned char* smem, int G, int W, int KT) {
     Lds l;
@@ -121,6 +127,8 @@ __device__ __forceinline__ Lds carve(unsigned char* smem, int G, int W, int KT) 
     l.vflag = reinterpret_cast<int*>(smem + o);
     o += kFlagBytes;
     l.claim = reinterpret_cast<int*>(smem + o);
+    o += kClaimBytes;
+    l.wmax = reinterpret_cast<float*>(smem + o);
     return l;
 }
 
@@ -490,8 +498,15 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     float acc[kTok];   // attention mass of tokens wtok0 + lane + 64 k, summed over rows
 #pragma unroll
     for (int k = 0; k < kTok; ++k) acc[k] = 0.0f;
-    auto consume = [&](int x, float mw) {
+    // The wave's maximum of held row x for head h (the values it held are
+    // 2^(logit - that maximum)) sits in LDS next to the row, not in
+    // registers: kRowBufs rows of it would cost the plain kernel seven
+    // registers and push the quantised and window instantiations into spills.
+    constexpr int kSlots = W * NH;
+    float* const wm_wave = sm.wmax + (size_t)wv * kSlots;
+    auto consume = [&](int x) {
         const float* rb = sm.rowbuf + (size_t)(x % kRowBufs) * G * kTs + wtok0 + lane;
+        const float mw = wm_wave[(size_t)(x % kRowBufs) * W * kSlots + min(h, kSlots - 1)];
         const float2 n = sm.norm[(x & 1) * 16 + hh];
         const float f = h < G ? hw_exp2(mw - n.x) * n.y : 0.0f;
 #pragma unroll
@@ -500,16 +515,6 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
 #pragma unroll
             for (int k = 0; k < kTok; ++k) acc[k] = fmaf(rb[min(hd, G - 1) * kTs + 64 * k], fh, acc[k]);
         }
-    };
-    // The wave's row maxima of the last kConsumeLag rows (lane h: head h),
-    // newest first.
-    float mh[kConsumeLag];
-#pragma unroll
-    for (int k = 0; k < kConsumeLag; ++k) mh[k] = 0.0f;
-    auto push_max = [&](float v) {
-#pragma unroll
-        for (int k = kConsumeLag - 1; k > 0; --k) mh[k] = mh[k - 1];
-        mh[0] = v;
     };
 
     // Bookkeeping of iteration r (a row of tiles for r < LHkv, then
@@ -542,7 +547,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     auto after_tiles = [&](int r) {   // publish row r - 1, normalise row r - 7
         if (r >= 1 && r - 1 <= last) publish(r - 1);
         const int xf = r - kConsumeLag;
-        if (xf >= 0 && xf <= last) consume(xf, mh[kConsumeLag - 1]);
+        if (xf >= 0 && xf <= last) consume(xf);
     };
 
     // ---- prologue: query row 0 staged; then the loads in the order every
@@ -577,6 +582,25 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // work of the row.
     auto do_row = [&](u32x4 (&ring)[KT][4], int row) {
         const uint32_t* qb = sm.qs + (size_t)(row & 1) * 3 * G * 64 + hh * 64 + 4 * g;
+        // Quantised tiles: the scale (the same 16 bytes in every lane) goes
+        // to a scalar, and the codes are widened to bf16 (exact) in place,
+        // so the MFMA loop below is the plain one and holds no second copy
+        // of the tile; the scale multiplies the finished sums.
+        float qsc[KT];
+        if constexpr (QT) {
+#pragma unroll
+            for (int u = 0; u < KT; ++u) {
+                qsc[u] = 1.0f;
+                if ((qmask >> u) & 1u) {
+                    qsc[u] = __uint_as_float(__builtin_amdgcn_readfirstlane(ring[u][2][0]));
+                    const u32x4 c0 = ring[u][0], c1 = ring[u][1];
+                    ring[u][0] = codes_to_bf16<0>(c0);
+                    ring[u][1] = codes_to_bf16<1>(c0);
+                    ring[u][2] = codes_to_bf16<0>(c1);
+                    ring[u][3] = codes_to_bf16<1>(c1);
+                }
+            }
+        }
         f32x4 c[KT];
 #pragma unroll
         for (int u = 0; u < KT; ++u) c[u] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -587,23 +611,18 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
             for (int p = 0; p < 3; ++p) bq[p] = *reinterpret_cast<const u32x4*>(qb + p * G * 64 + 16 * j);
 #pragma unroll
             for (int u = 0; u < KT; ++u) {
-                u32x4 av = ring[u][j];
-                if constexpr (QT) {   // codes as bf16 (exact); the scale after the sum
-                    if ((qmask >> u) & 1u) av = (j & 1) ? codes_to_bf16<1>(ring[u][j >> 1]) : codes_to_bf16<0>(ring[u][j >> 1]);
-                }
 #pragma unroll
                 for (int p = 0; p < 3; ++p)
                     c[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf16x8, av), __builtin_bit_cast(bf16x8, bq[p]), c[u], 0, 0, 0);
+                        __builtin_bit_cast(bf16x8, ring[u][j]), __builtin_bit_cast(bf16x8, bq[p]), c[u], 0, 0, 0);
             }
         }
         if constexpr (QT) {
 #pragma unroll
             for (int u = 0; u < KT; ++u)
                 if ((qmask >> u) & 1u) {
-                    const float qs = __uint_as_float(ring[u][2][0]);
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) c[u][i] *= qs;
+                    for (int i = 0; i < 4; ++i) c[u][i] *= qsc[u];
                 }
         }
         load_tile(ring[0], row + 2, 0);
@@ -653,7 +672,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         ls += __shfl_xor(ls, 16);
         ls += __shfl_xor(ls, 32);
         after_tiles(row);
-        push_max(ms);
+        if (g == 0 && h < kSlots) wm_wave[(size_t)(row % kRowBufs) * W * kSlots + h] = ms;
         if (g == 0 && h < G) sm.wstat[((row & 1) * W + wv) * 16 + h] = make_float2(mx, ls);
         lds_sync();
     };
@@ -682,7 +701,6 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         use_loads(r);
         issue_loads(r);
         after_tiles(r);
-        push_max(0.0f);
         lds_sync();
     }
 
@@ -936,7 +954,7 @@ k_attend(AttendDims dm, AttendArgs a) {
 size_t attend_lds_bytes(int G) {
     const int W = attend_threads(G) / 64;
     return rowbuf_bytes(G, W, attend_unit_tokens(G) / (16 * W)) + qs_bytes(G) + wstat_bytes(W) + kNormBytes +
-           kFlagBytes + kClaimBytes;
+           kFlagBytes + kClaimBytes + wmax_bytes(G, W);
 }
 
 namespace {
