@@ -75,7 +75,7 @@
 extern "C" {
 #endif
 
-#define MD_ABI_VERSION 7
+#define MD_ABI_VERSION 8
 
 typedef int32_t md_status;
 
@@ -127,6 +127,18 @@ enum {
                                 /* differs from that of the session's last      */
                                 /* token, and the last page's unused slots      */
                                 /* become holes; needs md_cache_view.n_live     */
+#define MD_FLAG_COOPERATIVE 0x10 /* launch the fused observation kernel as a  */
+                                /* cooperative launch, which the runtime keeps  */
+                                /* from sharing the device with other work; for */
+                                /* callers that run kernels on other streams or */
+                                /* processes of the same GPU at the same time.  */
+                                /* By default it is an ordinary launch (15-20   */
+                                /* us less per step): md_init checks that all   */
+                                /* its workgroups are resident together on an   */
+                                /* idle device, and work on other streams that  */
+                                /* takes CUs while it runs can make its bounded */
+                                /* waits run out (MD_DEV_TIMEOUT, a void step   */
+                                /* for the sessions affected; never a hang)     */
 #define MD_REGION_HOLE    0xFF  /* region code of a hole slot                   */
 #define MD_FLAG_FUSED     0x2   /* observe on the fused kernel whenever it can  */
                                 /* hold the sessions.  With neither flag,       */

@@ -31,6 +31,7 @@ MD_FLAG_NO_FUSED = 0x1
 MD_FLAG_FUSED = 0x2
 MD_FLAG_NORM_ATTENTION = 0x4
 MD_FLAG_REGION_ALIGNED = 0x8
+MD_FLAG_COOPERATIVE = 0x10
 MD_REGION_HOLE = 0xFF
 
 EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_init_static", "md_observe_step",

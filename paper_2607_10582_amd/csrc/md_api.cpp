@@ -143,7 +143,8 @@ const char* md_status_str(md_status s) {
 
 static md_status validate_config(const md_config* c) {
     if (c == nullptr) return MD_E_INVALID;
-    if ((c->flags & ~(MD_FLAG_NO_FUSED | MD_FLAG_FUSED | MD_FLAG_NORM_ATTENTION | MD_FLAG_REGION_ALIGNED)) != 0)
+    if ((c->flags & ~(MD_FLAG_NO_FUSED | MD_FLAG_FUSED | MD_FLAG_NORM_ATTENTION | MD_FLAG_REGION_ALIGNED |
+                      MD_FLAG_COOPERATIVE)) != 0)
         return MD_E_INVALID;
     if ((c->flags & MD_FLAG_NO_FUSED) && (c->flags & MD_FLAG_FUSED)) return MD_E_INVALID;
     if (c->offload_pages < 0 || c->offload_pages > md::kMaxOffload) return MD_E_INVALID;
@@ -243,6 +244,7 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     dm.fused = ((cfg->flags & MD_FLAG_NO_FUSED) ||
                 (dm.W > 1 && ((cfg->flags & MD_FLAG_REGION_ALIGNED) || cfg->quant_threshold > 0.0f))) ? 0 : 1;
     dm.norm_attn = (cfg->flags & MD_FLAG_NORM_ATTENTION) ? 1 : 0;
+    dm.coop = (cfg->flags & MD_FLAG_COOPERATIVE) ? 1 : 0;
     dm.aligned = (cfg->flags & MD_FLAG_REGION_ALIGNED) ? 1 : 0;
     dm.quant = cfg->quant_threshold > 0.0f ? 1 : 0;
     dm.quant_thr = cfg->quant_threshold;
@@ -306,8 +308,9 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
         dm.n_wg = dm.U_cap = dm.wg_per_cu = dm.lane_cap = 0;
     }
     // The fused kernel's workgroups wait for each other, so all of them must
-    // be resident together: check it on the device, and step the grid down
-    // one workgroup per CU at a time until every workgroup arrives.
+    // be resident together: check it on the device, with the launch kind the
+    // step uses, and step the grid down one workgroup per CU at a time until
+    // every workgroup arrives.
     if (dm.fused) {
         int32_t* probe = static_cast<int32_t*>(static_base);   // the static scratch is free until carved
         if (!use_static && hipMalloc(&probe, 2 * sizeof(int32_t)) != hipSuccess) return MD_E_NOMEM;

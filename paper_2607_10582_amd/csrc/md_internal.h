@@ -35,6 +35,7 @@ struct Dims {
     int L, Hq, Hkv, G, P, Pshift, S, MP, NP, R, LHkv, n_regions, max_chunks;
     int W;         // window: decode queries per observation (R = L * Hq * W)
     int fused;     // 1: sessions that fit one pass run on k_attend
+    int coop;      // 1: k_attend is a cooperative launch (MD_FLAG_COOPERATIVE)
     int spill;     // 1: some session may not fit a pass (the spill kernels run)
     int multi;     // 1: the multi-kernel path runs at some step (its scratch exists)
     int norm_attn; // 1: the attention term of Eq. 4 is alpha * |K_t| * a_i

@@ -53,6 +53,19 @@ def test_small_workload_free_run(fused):
     assert st.evicted_pages > 10
 
 
+@pytest.mark.parametrize("name", ["small", "qwen3_32x1700"])
+def test_cooperative_launch(name):
+    # MD_FLAG_COOPERATIVE: the fused kernel as a cooperative launch (the
+    # default is an ordinary one); same results
+    w = C.get(name)
+    if name != "small":
+        w = C.with_overrides(w, S=8, steps=12)
+    p = Pair(w, fused=True, cooperative=True, oracle_sessions=[0, w.S - 1])
+    assert p.md.kernel_config()["fused"]
+    st = run_pair(p, w.steps, f"cooperative-{name}")
+    assert st.evicted_pages > 10
+
+
 def test_small_workload_planted_refresh():
     # Planted keys along a per-(layer, KV head) direction and queries that
     # lean on it: those tokens take mass >= tau and refresh their clocks.
