@@ -18,9 +18,12 @@ long-horizon batch (16 sessions x 32,768 tokens, 1.5B shape, 25 % budget,
 For every workload, step 1 runs three times on a copy of the state first
 (so the code objects are loaded), then one trajectory from the fresh cache:
 step 1 (the bulk eviction down to the budget) and the warm-up steps, then
-the timed steps, then the rest of the workload's steps.  Every step is bracketed by an event
-pair on the library's stream, so the record holds the first step, the timed
-steady steps and the mean over the workload's whole run.
+the timed steps, then the rest of the workload's steps.  Every step outside
+the timed region is bracketed by an event pair on the library's stream, and
+the timed region by one pair around all of its steps (an event between two
+steps costs the stream a few microseconds), so the record holds the first
+step, the timed steps' mean, the median of the untimed steady steps and the
+mean over the workload's whole run.
 
 Printed on stdout: one JSON line.  value = tokens scored per second over the
 timed steps (the sum over sessions and timed steps of the cached tokens
@@ -263,10 +266,16 @@ def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0, offload_
         q, nk, reg = inputs[k - 1]
         md.step(k, q, nk, reg, page_scores=False)
 
-    # warm-up, every step event-timed
+    # warm-up, every step event-timed; the tokens of step 1 (the bulk
+    # eviction) are counted on their own
+    c_start = md.counters()
+    first_end = torch.cuda.Event(enable_timing=True)
     for k in range(1, W + 1):
         ev[k - 1].record(stream)
         run(k)
+        if k == 1:
+            first_end.record(stream)
+            c_first = md.counters()
     ev[W].record(stream)
     torch.cuda.synchronize(dev)
     c0 = md.counters()
@@ -280,11 +289,12 @@ def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0, offload_
         abar = torch.zeros(cache.n_phys * w.P, dtype=torch.float32, device=dev)
         stats = [torch.zeros((w.S, 7, n_buckets), dtype=torch.int64, device=dev) for _ in range(3)]
         cal_ev = []
+    timed_ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
     torch.cuda.synchronize(dev)
     t0 = time.perf_counter()
+    timed_ev[0].record(stream)
     for k in range(W + 1, W + K + 1):
         q, nk, reg = inputs[k - 1]
-        ev[k - 1].record(stream)
         if calibrate and q is not None:
             # a calibration pass: the step's masses go to the lifetime bins
             md.observe(k, q, nk, reg, abar_out=abar)
@@ -298,7 +308,7 @@ def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0, offload_
             md.compact()
         else:
             run(k)
-    ev[W + K].record(stream)
+    timed_ev[1].record(stream)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0
     hot_ms, launches = md.profile_read(hot)
@@ -311,7 +321,10 @@ def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0, offload_
         run(k)
     ev[total].record(stream)
     torch.cuda.synchronize(dev)
-    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(total)]
+    warm_ms = [ev[0].elapsed_time(first_end)] + [ev[i].elapsed_time(ev[i + 1]) for i in range(1, W)]
+    timed_ms = timed_ev[0].elapsed_time(timed_ev[1])
+    rest_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(W + K, total)]
+    untimed_steady = warm_ms[1:] + rest_ms
     status = md.device_status()
     if status != 0:
         log(f"device status {status:#x}")
@@ -347,7 +360,10 @@ def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0, offload_
     # whole step: K + per-token state (region 1, a 4+4, t_ref 4+4) + per-page
     # score and page-table entry + the queries
     step_bytes = scored * (kb + 17) + scored // w.P * 8 + K * q_bytes - q_saved
-    timed = step_ms[W:W + K]
+    # the first observation (step 1) on the same terms
+    scored1 = c_first[0] - c_start[0]
+    first_bytes = scored1 * (kb + 17) + scored1 // w.P * 8 + (w.S * w.L * w.Hq * w.d * 4 * w.window
+                                                              if g.observes(w, 1) else 0)
     rec = {
         "value": scored / wall,
         "unit": "tokens/s",
@@ -363,10 +379,13 @@ def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0, offload_
         "tokens_evicted_per_step": (c1[3] - c0[3]) / K,
         "quantised_tokens_per_step": q_tok,
         "pages_evicted": c1[2] - c0[2],
-        "first_step_ms": step_ms[0],
-        "steady_step_ms_mean": float(np.mean(timed)),
-        "step_ms_median": float(np.median(timed)),
-        "run_mean_ms": float(np.mean(step_ms)),
+        "first_step_ms": warm_ms[0],
+        "first_step_tokens": scored1,
+        "first_step_algorithmic_bytes": first_bytes,
+        "first_step_frac_of_peak": first_bytes / (warm_ms[0] / 1e3) / 1e9 / PEAK_HBM_GBS,
+        "steady_step_ms_mean": timed_ms / K,
+        "step_ms_median": float(np.median(untimed_steady)) if untimed_steady else timed_ms / K,
+        "run_mean_ms": (sum(warm_ms) + timed_ms + sum(rest_ms)) / total,
         "run_steps": total,
         "calib_us_per_observation": (sum(a.elapsed_time(b) for a, b in cal_ev) * 1e3 / len(cal_ev)
                                      if calibrate and cal_ev else None),
@@ -479,7 +498,8 @@ def main():
         "roofline": main_rec["roofline"],
     }
     for key in ("tokens_scored_per_step", "tokens_evicted_per_step", "quantised_tokens_per_step",
-                "pages_evicted", "first_step_ms", "steady_step_ms_mean", "step_ms_median", "run_mean_ms",
+                "pages_evicted", "first_step_ms", "first_step_tokens", "first_step_algorithmic_bytes",
+                "first_step_frac_of_peak", "steady_step_ms_mean", "step_ms_median", "run_mean_ms",
                 "run_steps", "calib_us_per_observation", "step_algorithmic_gbs", "step_frac_of_peak"):
         line[key] = main_rec[key]
     if "offload" in main_rec:

@@ -534,6 +534,7 @@ md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_cou
 md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* evict_count) {
     if (h == nullptr || ((evict_serial == nullptr) != (evict_count == nullptr))) return MD_E_INVALID;
     if (h->phase == kNone) return MD_E_STATE;
+    const int trusted = evict_serial == nullptr ? 1 : 0;
     if (evict_serial == nullptr) {   // the selection of this step
         if (h->sel_serial == nullptr || h->phase != kScored) return MD_E_STATE;
         evict_serial = h->sel_serial;
@@ -550,7 +551,7 @@ md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* ev
         md::launch_quant(h->dm, h->v, h->sc, evict_serial, evict_count, h->stream) != hipSuccess)
         return MD_E_HIP;
     if (timed_launch(h, MD_K_COMPACT, [&] {
-            return md::launch_compact(h->dm, h->v, h->sc, evict_serial, evict_count, h->stream); }) !=
+            return md::launch_compact(h->dm, h->v, h->sc, evict_serial, evict_count, trusted, h->stream); }) !=
         hipSuccess)
         return MD_E_HIP;
     h->phase = kCompacted;

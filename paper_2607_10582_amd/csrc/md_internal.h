@@ -112,6 +112,7 @@ struct Scratch {
     int32_t* status;       // [1] device status word
     int32_t* warn;         // [1] warning bits (1: some session's budget was infeasible)
     int32_t* done_compact; // [1] completion counter of the compaction kernel
+    unsigned long long* compact_acc;   // [1] the same for its trusted form: blocks done << 40 | gaps
     int32_t* opened;       // [1] pages the append kernel takes from the free list
     unsigned long long* counters;  // [8] tokens scored, steps, pages evicted, tokens evicted, pages
                                    // offloaded, recalled, dropped from host memory, observed there
@@ -157,8 +158,9 @@ hipError_t launch_select(const Dims& dm, const View& v, const Scratch& sc, int32
 hipError_t launch_calib(const Dims& dm, const View& v, const Scratch& sc, const float* abar, int bucket_steps,
                         int n_buckets, unsigned long long* mass_fx, unsigned long long* count,
                         unsigned long long* age_sum, hipStream_t st);
+// trusted: the lists are the library's own selection of this step
 hipError_t launch_compact(const Dims& dm, const View& v, const Scratch& sc,
-                          const int32_t* ev_serial, const int32_t* ev_count, hipStream_t st);
+                          const int32_t* ev_serial, const int32_t* ev_count, int trusted, hipStream_t st);
 // Quantised tier, before the compaction of the same eviction lists.
 hipError_t launch_quant(const Dims& dm, const View& v, const Scratch& sc,
                         const int32_t* ev_serial, const int32_t* ev_count, hipStream_t st);

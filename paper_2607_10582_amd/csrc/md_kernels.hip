@@ -96,28 +96,38 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             if (i < n_pieces) kr[c] = src[i];
         }
     }
-    // pages the sessions before this one take at this append
+    // Thread 0's own counters go out with the other sessions' below (the
+    // pages the sessions before this one take at this append), and the last
+    // page's table entry right behind them, so the chain to the slot is
+    // three round trips to memory rather than six.
+    int t0_clock = 0, np = 0, nt = 0, fc0 = 0, last_p = -1;
+    if (threadIdx.x == 0) {
+        t0_clock = v.clock[s];
+        np = v.n_pages[s];
+        nt = v.n_tokens[s];
+        fc0 = v.free_count[0];   // changes only in the last block
+    }
     if (threadIdx.x == 0) sh_rank = 0;
+    int rank_mine = 0;
+    if (new_k != nullptr)
+        for (int s2 = threadIdx.x; s2 < s; s2 += blockDim.x) rank_mine += opens_page(dm, v, s2, new_region) ? 1 : 0;
+    if (threadIdx.x == 0 && np > 0 && np <= dm.MP) last_p = v.page_table[(size_t)s * dm.MP + np - 1];
     __syncthreads();
     if (new_k != nullptr) {
-        int mine = 0;
-        for (int s2 = threadIdx.x; s2 < s; s2 += blockDim.x) mine += opens_page(dm, v, s2, new_region) ? 1 : 0;
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o);
-        if (lane_id() == 0 && mine > 0) atomicAdd(&sh_rank, mine);
+        for (int o = 32; o > 0; o >>= 1) rank_mine += __shfl_xor(rank_mine, o);
+        if (lane_id() == 0 && rank_mine > 0) atomicAdd(&sh_rank, rank_mine);
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        const int t = v.clock[s] + 1;
+        const int t = t0_clock + 1;
         v.clock[s] = t;
         int phys = -1, slot = 0;
-        int np = v.n_pages[s];
-        int nt = v.n_tokens[s];
         if (new_k != nullptr && counters_ok(np, nt, dm)) {
             const size_t row = (size_t)s * dm.MP;
             bool open = !(np > 0 && nt < np * dm.P);
             if (!open) {
-                const int p = v.page_table[row + np - 1];
+                const int p = last_p;
                 if (p >= 0 && p < dm.NP) {
                     phys = p;
                     slot = nt - (np - 1) * dm.P;
@@ -143,10 +153,8 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                 // the token joins the last page (or the page was corrupt)
             } else if (np < dm.MP) {
                 // the free list is a stack: this session takes the entry
-                // below the earlier sessions' ones (free_count changes only
-                // in the last block)
-                const int fc = v.free_count[0];
-                const int idx = min(fc, dm.NP) - 1 - sh_rank;
+                // below the earlier sessions' ones
+                const int idx = min(fc0, dm.NP) - 1 - sh_rank;
                 if (idx >= 0) {
                     const int p = v.free_list[idx];
                     if (p >= 0 && p < dm.NP) {
@@ -1010,7 +1018,8 @@ hipError_t launch_select(const Dims& dm, const View& v, const Scratch& sc, int32
 // Pages listed for eviction in a session whose step stands (0 otherwise):
 // the places the session's freed ids take on the free list.
 __device__ __forceinline__ int evict_listed(const Dims& dm, const Scratch& sc, const int32_t* ev_count, int s) {
-    return sc.valid[s] ? min(max(ev_count[s], 0), dm.MP) : 0;
+    const int valid = sc.valid[s], c = ev_count[s];   // both loads issued together
+    return valid ? min(max(c, 0), dm.MP) : 0;
 }
 
 // One block per session.  Freed physical ids go onto the free list in
@@ -1018,26 +1027,38 @@ __device__ __forceinline__ int evict_listed(const Dims& dm, const Scratch& sc, c
 // sessions before it, which reserve one place per listed serial; the last
 // block to finish sets the new count and, if some list named serials its
 // session does not hold, closes the gaps they left, keeping the order.
+//
+// trusted: the lists are this step's selection (md_compact without lists),
+// which names only pages the sessions hold.  Then no gaps can arise, and the
+// blocks hand the last one nothing but a count, folded into the completion
+// counter itself: no memory fence (a device-scope fence writes back the L2
+// of the block's XCD, about 3 us each).  Should a session's table have
+// changed since the selection after all, its unused places get -1 (an id
+// the append refuses, setting MD_DEV_CORRUPT) rather than stale ids.
 __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratch sc,
                                                          const int32_t* __restrict__ ev_serial,
-                                                         const int32_t* __restrict__ ev_count) {
+                                                         const int32_t* __restrict__ ev_count, int trusted) {
     const int s = blockIdx.x;
     __shared__ int lds[3 * 17];
     __shared__ int sh_last, sh_before;
     const int tid = threadIdx.x;
+    // Every load that depends on nothing else goes out at once: the
+    // session's list length and counters, the free count (it changes only in
+    // the last block, after every block has read it), and the list lengths of
+    // the sessions before this one (their places on the free list).
     const int cnt = evict_listed(dm, sc, ev_count, s);
     const int np = v.n_pages[s], nt = v.n_tokens[s];
+    const int fc = v.free_count[0];
+    int mine = 0;
+    for (int s2 = tid; s2 < s; s2 += blockDim.x) mine += evict_listed(dm, sc, ev_count, s2);
     if (tid == 0) sh_before = 0;
     __syncthreads();
     {
-        int mine = 0;
-        for (int s2 = tid; s2 < s; s2 += blockDim.x) mine += evict_listed(dm, sc, ev_count, s2);
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o);
         if (lane_id() == 0 && mine > 0) atomicAdd(&sh_before, mine);
     }
     __syncthreads();
-    const int fc = v.free_count[0];   // changes only in the last block
     int gone_total = 0;
     if (cnt > 0 && np == 0) {
         if (tid == 0) atomicOr(sc.status, MD_DEV_BAD_EVICT);
@@ -1113,6 +1134,32 @@ __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratc
         }
     }
     if (tid == 0) sc.freed[s] = gone_total;
+
+    if (trusted) {
+        const int base = fc + sh_before;
+        for (int i = gone_total + tid; i < cnt; i += blockDim.x)
+            if (base + i >= 0 && base + i < dm.NP) v.free_list[base + i] = -1;
+        __syncthreads();   // every thread is past its reads of the free count
+        if (tid == 0) {
+            const unsigned long long old =
+                atomicAdd(sc.compact_acc, (1ull << 40) | (unsigned long long)(cnt - gone_total));
+            sh_last = (int)(old >> 40) == (int)gridDim.x - 1;
+        }
+        __syncthreads();
+        if (!sh_last) return;
+        // the last block: every block has read the free count; the list grew
+        // by one place per listed page
+        int listed = 0;
+        for (int s2 = tid; s2 < dm.S; s2 += blockDim.x) listed += evict_listed(dm, sc, ev_count, s2);
+        const int m1[1] = {listed};
+        int ex1[1], tot1[1];
+        block_exclusive_scan_n<1>(m1, lds, ex1, tot1);
+        if (tid == 0) {
+            v.free_count[0] = min(max(fc, 0) + tot1[0], dm.NP);
+            *sc.compact_acc = 0;
+        }
+        return;
+    }
 
     // The last block to finish: the new free count; gaps left by listed
     // serials a session did not hold are closed session by session, each
@@ -1250,8 +1297,9 @@ hipError_t launch_quant(const Dims& dm, const View& v, const Scratch& sc, const 
 }
 
 hipError_t launch_compact(const Dims& dm, const View& v, const Scratch& sc,
-                          const int32_t* ev_serial, const int32_t* ev_count, hipStream_t st) {
-    hipLaunchKernelGGL(k_compact, dim3(dm.S), dim3(kSelThreads), 0, st, dm, v, sc, ev_serial, ev_count);
+                          const int32_t* ev_serial, const int32_t* ev_count, int trusted, hipStream_t st) {
+    hipLaunchKernelGGL(k_compact, dim3(dm.S), dim3(kSelThreads), 0, st, dm, v, sc, ev_serial, ev_count,
+                       trusted);
     return hipGetLastError();
 }
 
@@ -1337,7 +1385,7 @@ size_t scratch_bytes(const Dims& dm) {
     n += align256((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long));
     n += align256((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long));
     n += align256(5 * sizeof(int32_t));
-    n += align256(8 * sizeof(unsigned long long));
+    n += align256(9 * sizeof(unsigned long long));
     n += align256((size_t)dm.S * dm.H * sizeof(int32_t));
     n += align256((size_t)(dm.S + 1) * sizeof(int32_t));
     return n;
@@ -1377,7 +1425,8 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
     sc->warn = words + 2;
     sc->done_compact = words + 3;
     sc->opened = words + 4;
-    sc->counters = reinterpret_cast<unsigned long long*>(take(8 * sizeof(unsigned long long)));
+    sc->counters = reinterpret_cast<unsigned long long*>(take(9 * sizeof(unsigned long long)));
+    sc->compact_acc = sc->counters + 8;
     sc->recall = reinterpret_cast<int32_t*>(take((size_t)dm.S * dm.H * sizeof(int32_t)));
     sc->rcount = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
 }

@@ -4,9 +4,11 @@ Two uses:
 
 * ``trace``: per-kernel launch counts and durations from a
   ``rocprofv3 --kernel-trace --stats --output-format csv`` run, as a short
-  markdown table, with the steady-state average of the library's kernels
-  (their first ``--skip`` launches left out: md_init's residency check and
-  the warm-up steps).
+  markdown table.  The fused kernel's launches fall into three kinds, told
+  apart by size against the median launch: md_init's residency checks
+  (under a third of it), first observations of whole prompts, the bulk
+  eviction (over twice it), and steady steps; the table gives the steady
+  and the first-observation averages apart.
 * ``hits``: L2 (TCC) hit rate of one kernel's steady launches from a
   ``--pmc TCC_HIT_sum TCC_MISS_sum`` run.
 * ``pmc``: HBM bytes per launch of one kernel from two counter runs
@@ -51,8 +53,20 @@ def _one(pattern: str) -> str:
     return hits[0]
 
 
+def kinds(values):
+    """Indices of (steady, first-observation, residency-check) launches of the
+    fused kernel, by size against the median launch (steady launches are
+    most of any run)."""
+    med = statistics.median(values)
+    steady = [i for i, v in enumerate(values) if med / 3 <= v <= 2 * med]
+    bulk = [i for i, v in enumerate(values) if v > 2 * med]
+    check = [i for i, v in enumerate(values) if v < med / 3]
+    return steady, bulk, check
+
+
 def trace_table(trace_dir: str, skip: int):
-    """Rows (kernel, launches, avg us, total us, steady avg us) from a kernel trace."""
+    """Rows (kernel, launches, avg us, total us, steady avg us, launches, first-observation avg
+    us, launches) from a kernel trace."""
     rows = list(csv.DictReader(open(_one(os.path.join(trace_dir, "*kernel_trace.csv")))))
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
     durs = defaultdict(list)
@@ -60,9 +74,14 @@ def trace_table(trace_dir: str, skip: int):
         durs[r["Kernel_Name"]].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
     out = []
     for name, d in durs.items():
-        steady = d[skip:] if ("md::" in name and len(d) > skip) else d
+        bulk = []
+        if "k_attend" in name:
+            st, bk, _ = kinds(d)
+            steady, bulk = [d[i] for i in st], [d[i] for i in bk]
+        else:
+            steady = d[skip:] if ("md::" in name and len(d) > skip) else d
         out.append((short_name(name)[:60], len(d), sum(d) / len(d), sum(d), sum(steady) / len(steady),
-                    len(steady)))
+                    len(steady), (sum(bulk) / len(bulk)) if bulk else None, len(bulk)))
     out.sort(key=lambda x: -x[3])
     return out
 
@@ -110,14 +129,18 @@ def main():
     p.add_argument("--copy-mib", type=int, default=256)
     p.add_argument("--algorithmic-bytes", type=float, default=None,
                    help="algorithmic bytes per launch, for the ratio")
+    p.add_argument("--first-algorithmic-bytes", type=float, default=None,
+                   help="algorithmic bytes of a first-observation launch, for its ratio")
     p.add_argument("--json", required=True)
     a = ap.parse_args()
 
     if a.mode == "trace":
-        print("| kernel | launches | avg us | total us | steady avg us (launches) |")
-        print("|---|---:|---:|---:|---:|")
-        for name, n, avg, tot, st, ns in trace_table(a.trace_dir, a.skip)[:a.top]:
-            print(f"| `{name}` | {n} | {avg:.2f} | {tot:.1f} | {st:.2f} ({ns}) |")
+        print("| kernel | launches | avg us | total us | steady avg us (launches) | first observation avg us "
+              "(launches) |")
+        print("|---|---:|---:|---:|---:|---:|")
+        for name, n, avg, tot, st, ns, bk, nb in trace_table(a.trace_dir, a.skip)[:a.top]:
+            b = f"{bk:.2f} ({nb})" if bk is not None else ""
+            print(f"| `{name}` | {n} | {avg:.2f} | {tot:.1f} | {st:.2f} ({ns}) | {b} |")
         return
 
     if a.mode == "hits":
@@ -139,17 +162,28 @@ def main():
     key = [k for k in fetch if short_name(k).startswith(a.kernel)]
     if not key:
         raise RuntimeError(f"{a.kernel} not in {a.fetch_dir}")
-    kf = fetch[key[0]][a.skip:]
-    kw = write[[k for k in write if short_name(k).startswith(a.kernel)][0]][a.skip:]
+    allf = fetch[key[0]]
+    allw = write[[k for k in write if short_name(k).startswith(a.kernel)][0]]
+    # the two runs launch the same sequence; kinds are read off the reads
+    st, bk, _ = kinds(allf)
+    kf, kw = [allf[i] for i in st], [allw[i] for i in st]
     rd = statistics.mean(kf) * ff
     wr = statistics.mean(kw) * fw
     rec = {"kernel": a.kernel, "workload": a.workload, "kernel_source_sha256_16": source_hash(a.kernel),
            "launches": len(kf), "fetch_bytes_per_launch": rd, "write_bytes_per_launch": wr,
            "hbm_bytes_per_launch": rd + wr, "fetch_bytes_per_counter_unit": ff,
            "write_bytes_per_counter_unit": fw, "copy_bytes": nbytes}
+    if bk:
+        brd = statistics.mean([allf[i] for i in bk]) * ff
+        bwr = statistics.mean([allw[i] for i in bk]) * fw
+        rec.update({"first_observation_launches": len(bk), "first_observation_fetch_bytes": brd,
+                    "first_observation_write_bytes": bwr, "first_observation_hbm_bytes": brd + bwr})
     if a.algorithmic_bytes:
         rec["algorithmic_bytes_per_launch"] = a.algorithmic_bytes
         rec["traffic_over_algorithmic"] = (rd + wr) / a.algorithmic_bytes
+    if bk and a.first_algorithmic_bytes:
+        rec["first_observation_algorithmic_bytes"] = a.first_algorithmic_bytes
+        rec["first_observation_traffic_over_algorithmic"] = (brd + bwr) / a.first_algorithmic_bytes
     with open(a.json, "w") as f:
         json.dump(rec, f, indent=1)
     print(f"| {a.kernel} on {a.workload} | per launch (mean of {len(kf)} steady launches) |")
@@ -159,6 +193,15 @@ def main():
     if a.algorithmic_bytes:
         print(f"| algorithmic bytes | {a.algorithmic_bytes / 1e9:.4f} GB |")
         print(f"| traffic / algorithmic | {(rd + wr) / a.algorithmic_bytes:.3f} |")
+    if bk:
+        print()
+        print(f"| {a.kernel} on {a.workload}, first observation (bulk eviction) | per launch (mean of {len(bk)}) |")
+        print("|---|---:|")
+        print(f"| HBM read | {brd / 1e9:.4f} GB |")
+        print(f"| HBM write | {bwr / 1e9:.4f} GB |")
+        if a.first_algorithmic_bytes:
+            print(f"| algorithmic bytes | {a.first_algorithmic_bytes / 1e9:.4f} GB |")
+            print(f"| traffic / algorithmic | {(brd + bwr) / a.first_algorithmic_bytes:.3f} |")
 
 
 if __name__ == "__main__":

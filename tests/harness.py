@@ -105,7 +105,8 @@ class Pair:
                  pinned_mask=None, alpha=None, n_phys_extra: int = 0, max_pages=None,
                  steps=None, fused: Optional[bool] = True, priors=None, strict_ties: bool = False,
                  check_free_list: bool = False, static: bool = False, pool: int = 0,
-                 offload_pages: int = 0, drop_threshold: float = 0.0, cooperative: bool = False):
+                 offload_pages: int = 0, drop_threshold: float = 0.0, cooperative: bool = False,
+                 explicit_lists: bool = False):
         # pool > 0: the oracle sessions run in that many worker processes
         # (oracle.pool), all sessions of a step at once
         self.w = w
@@ -120,6 +121,9 @@ class Pair:
             (np.asarray(priors[0], np.float32), np.asarray(priors[1], np.float32))
         self.strict_ties = strict_ties
         self.check_free_list = check_free_list
+        # explicit_lists: md_compact always gets the lists (else without them
+        # whenever the device's selection is the oracle's)
+        self.explicit_lists = explicit_lists
         self.pinned_mask = w.pinned_mask if pinned_mask is None else pinned_mask
         self.alpha = w.alpha if alpha is None else alpha
         self.oracle_sessions = list(range(S)) if oracle_sessions is None else list(oracle_sessions)
@@ -263,6 +267,7 @@ class Pair:
         infeas = md.infeasible.cpu().numpy()
         final_ser = ev_ser.copy()
         final_cnt = ev_cnt.copy()
+        same_selection = True   # every compared session's selection equals the oracle's
         tref_fix = []
         quant_before = {s: {p.serial for p in self.oracles[s].pages if p.quant}
                         for s in self.oracle_sessions} if w.quant_threshold > 0 else {}
@@ -326,6 +331,7 @@ class Pair:
             if self.strict_ties:
                 assert g_ev.tolist() == rec.evicted.tolist(), (k, s, "evicted serials (exact ties)")
             if g_ev.tolist() != rec.evicted.tolist():
+                same_selection = False
                 diff = set(g_ev.tolist()) ^ set(rec.evicted.tolist())
                 thr = max((rec.page_score[i] for i in range(npg)
                            if rec.page_serial[i] in set(rec.evicted.tolist())), default=0.0)
@@ -346,7 +352,12 @@ class Pair:
                 torch.from_numpy(vals.astype(np.int32)).to(self.dev)
         if self.check_free_list:
             pre_compact = self.free_list_state()
-        md.compact(torch.from_numpy(final_ser).to(self.dev), torch.from_numpy(final_cnt).to(self.dev))
+        if same_selection and not self.explicit_lists:
+            # the device's own selection: md_compact without lists (the path
+            # a caller takes)
+            md.compact()
+        else:
+            md.compact(torch.from_numpy(final_ser).to(self.dev), torch.from_numpy(final_cnt).to(self.dev))
         torch.cuda.synchronize(self.dev)
         if self.check_free_list:
             self.check_pushes(pre_compact, final_ser, final_cnt, self.free_list_state())

@@ -545,13 +545,15 @@ def test_region_aligned_closed_page_stays_closed(fused):
 # ---------------------------------------------------------------- free list
 
 @pytest.mark.parametrize("fused", [True, False])
-def test_free_list_order(fused):
+@pytest.mark.parametrize("explicit", [False, True])
+def test_free_list_order(fused, explicit):
     # 12 sessions: each append takes pages off the top of the free list in
     # session order, and each compaction pushes the freed ids in (session,
-    # serial) order; the harness checks both at every step.
+    # serial) order; the harness checks both at every step, for md_compact
+    # without lists (this step's selection) and with the same lists given
     w = C.with_overrides(C.get("qwen3_32x1700"), L=2, S=12, steps=24)
-    p = Pair(w, oracle_sessions=[0, 7], check_free_list=True, fused=fused)
-    run_pair(p, 24, f"free-list-order-fused{int(fused)}")
+    p = Pair(w, oracle_sessions=[0, 7], check_free_list=True, fused=fused, explicit_lists=explicit)
+    run_pair(p, 24, f"free-list-order-fused{int(fused)}-explicit{int(explicit)}")
 
 
 def test_physical_pages_are_reproducible():
