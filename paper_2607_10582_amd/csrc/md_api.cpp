@@ -92,8 +92,11 @@ hipError_t timed_launch(md_handle_s* h, int id, F&& fn) {
         t = h->spare.back();
         h->spare.pop_back();
     } else {
-        if (hipEventCreate(&t.start) != hipSuccess) return hipErrorOutOfMemory;
-        if (hipEventCreate(&t.stop) != hipSuccess) {
+        // timing only: no system-scope fence (cache writeback and
+        // invalidation) when the event is recorded, which would slow the
+        // work after it and inflate the figure
+        if (hipEventCreateWithFlags(&t.start, hipEventDisableSystemFence) != hipSuccess) return hipErrorOutOfMemory;
+        if (hipEventCreateWithFlags(&t.stop, hipEventDisableSystemFence) != hipSuccess) {
             (void)hipEventDestroy(t.start);
             return hipErrorOutOfMemory;
         }
