@@ -389,9 +389,12 @@ enum {
     MD_K_SCORE = 4, MD_K_SELECT = 5, MD_K_COMPACT = 6, MD_K_ATTEND = 7, MD_K_COUNT = 8
 };
 
-/* Diagnostics.  md_profile_enable: from now on, bracket every launch of the
+/* Diagnostics.  md_profile_enable: from now on, time every launch of the
  * kernels whose bit (1 << id) is set in kernel_mask with a pair of hipEvents
- * on the handle's stream (0 turns timing off).  md_profile_read: synchronise,
+ * on the handle's stream (0 turns timing off): the fused observation kernel
+ * (ordinary launch) records the pair with its own dispatch, so the pair
+ * holds the kernel alone; the others are bracketed by the pair.
+ * md_profile_read: synchronise,
  * return the summed duration in milliseconds and the number of timed launches
  * of kernel `kernel` since the last read, and reset them. */
 md_status md_profile_enable(md_handle h, uint32_t kernel_mask);

@@ -83,10 +83,14 @@ void give_back(md_handle_s* h) {
     g_static_taken[i].store(false);
 }
 
-// Launch through `fn`, bracketed by an event pair when kernel `id` is timed.
+// Launch through `fn(start, stop)`, timed by an event pair when kernel `id`
+// is timed.  With `inside` the launch records the pair itself
+// (hipExtLaunchKernel: the events take the kernel's own start and end, with
+// no packets of their own in the stream); otherwise fn gets (NULL, NULL)
+// and the pair is recorded around it.
 template <typename F>
-hipError_t timed_launch(md_handle_s* h, int id, F&& fn) {
-    if (!(h->profile_mask & (1u << id))) return fn();
+hipError_t timed_launch_ev(md_handle_s* h, int id, bool inside, F&& fn) {
+    if (!(h->profile_mask & (1u << id))) return fn(nullptr, nullptr);
     Timed t;
     if (!h->spare.empty()) {
         t = h->spare.back();
@@ -101,11 +105,21 @@ hipError_t timed_launch(md_handle_s* h, int id, F&& fn) {
             return hipErrorOutOfMemory;
         }
     }
-    hipError_t e = hipEventRecord(t.start, h->stream);
-    if (e == hipSuccess) e = fn();
-    if (e == hipSuccess) e = hipEventRecord(t.stop, h->stream);
+    hipError_t e;
+    if (inside) {
+        e = fn(t.start, t.stop);
+    } else {
+        e = hipEventRecord(t.start, h->stream);
+        if (e == hipSuccess) e = fn(nullptr, nullptr);
+        if (e == hipSuccess) e = hipEventRecord(t.stop, h->stream);
+    }
     if (e == hipSuccess) h->pending[id].push_back(t); else h->spare.push_back(t);
     return e;
+}
+
+template <typename F>
+hipError_t timed_launch(md_handle_s* h, int id, F&& fn) {
+    return timed_launch_ev(h, id, false, [&](hipEvent_t, hipEvent_t) { return fn(); });
 }
 
 void release_events(md_handle_s* h) {
@@ -481,8 +495,9 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     // tokens) take the three-kernel path with the logits in HBM, which on
     // the other steps observes every session.
     const bool multi = !fused || h->dm.spill;
-    if (e == hipSuccess && fused) e = timed_launch(h, MD_K_ATTEND, [&] {
-        return md::launch_attend(h->dm, h->v, h->sc, q, abar_out, h->stream); });
+    if (e == hipSuccess && fused)
+        e = timed_launch_ev(h, MD_K_ATTEND, !h->dm.coop, [&](hipEvent_t t0, hipEvent_t t1) {
+            return md::launch_attend(h->dm, h->v, h->sc, q, abar_out, h->stream, t0, t1); });
     if (e == hipSuccess && multi) e = timed_launch(h, MD_K_LOGITS, [&] {
         return md::launch_logits(h->dm, h->v, h->sc, q, h->logits_blocks, h->stream); });
     if (e == hipSuccess && multi) e = timed_launch(h, MD_K_ROWSTATS, [&] {

@@ -41,6 +41,8 @@
 // bounded; a wait that runs out sets MD_DEV_TIMEOUT, and the wave stops
 // waiting for the rest of the step, so the grid always drains.
 
+#include <hip/hip_ext.h>
+
 #include "md_device.h"
 
 namespace md {
@@ -977,16 +979,20 @@ const void* attend_kernel(int G, int aligned, int quant, int window) {
 // The grid as one launch: cooperative (the runtime keeps the device to it)
 // with MD_FLAG_COOPERATIVE, an ordinary one otherwise (measured 15-20 us
 // less per step; residency is checked at init with the same launch kind).
-static hipError_t launch_grid(const Dims& dm, int n_wg, void** args, hipStream_t st) {
+// With an event pair (t0, t1), an ordinary launch records the events with
+// the kernel's dispatch itself.
+static hipError_t launch_grid(const Dims& dm, int n_wg, void** args, hipStream_t st, hipEvent_t t0 = nullptr,
+                              hipEvent_t t1 = nullptr) {
     const void* fn = attend_kernel(dm.G * dm.W, dm.aligned, dm.quant, dm.W);
     const dim3 grid(n_wg), block(attend_threads(dm.G * dm.W));
     const unsigned lds = (unsigned)attend_lds_bytes(dm.G * dm.W);
-    return dm.coop ? hipLaunchCooperativeKernel(fn, grid, block, args, lds, st)
-                   : hipLaunchKernel(fn, grid, block, args, lds, st);
+    if (dm.coop) return hipLaunchCooperativeKernel(fn, grid, block, args, lds, st);
+    if (t0 != nullptr && t1 != nullptr) return hipExtLaunchKernel(fn, grid, block, args, lds, st, t0, t1, 0);
+    return hipLaunchKernel(fn, grid, block, args, lds, st);
 }
 
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q, float* abar_out,
-                         hipStream_t st) {
+                         hipStream_t st, hipEvent_t t0, hipEvent_t t1) {
     AttendDims ad{dm.L, dm.Hq, dm.Hkv, dm.G * dm.W, dm.P, dm.Pshift, dm.MP, dm.NP, dm.R, dm.LHkv,
                   dm.wg_per_cu, dm.n_wg / dm.wg_per_cu, dm.S, dm.n_regions, dm.norm_attn, dm.pin_mask,
                   dm.rho, dm.tau_scale, dm.alpha, dm.aligned, dm.G, dm.W};
@@ -994,7 +1000,7 @@ hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const
                   sc.pscore, q, abar_out, sc.ustart, sc.plan, sc.epoch, sc.claim, sc.lane_box, sc.ustat,
                   sc.unorm, sc.status, nullptr, v.n_live, v.page_format, v.t_ins, sc.valid};
     void* args[] = {&ad, &aa};
-    return launch_grid(dm, dm.n_wg, args, st);
+    return launch_grid(dm, dm.n_wg, args, st, t0, t1);
 }
 
 hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, hipStream_t st) {

@@ -140,8 +140,10 @@ hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
 hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q,
                          int n_blocks, hipStream_t st);
 hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st);
+// t0, t1: when not NULL (ordinary launches only), an event pair recorded by
+// the kernel's dispatch itself
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q,
-                         float* abar_out, hipStream_t st);
+                         float* abar_out, hipStream_t st, hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 size_t attend_lds_bytes(int G);
 // the instantiation for G MFMA columns (heads per KV head x window), layout, tier, window
 const void* attend_kernel(int G, int aligned, int quant, int window);
