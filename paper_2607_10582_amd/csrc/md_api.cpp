@@ -49,6 +49,7 @@ struct md_handle_s {
     std::vector<Timed> pending[MD_K_COUNT];   // launches not yet read back
     std::vector<Timed> spare;                  // recycled event pairs
     int static_slot;     // md_init_static: index in the static handles; -1 otherwise
+    uint32_t append_tag; // launches of the append kernel (their tag)
 };
 
 namespace {
@@ -120,6 +121,13 @@ hipError_t timed_launch_ev(md_handle_s* h, int id, bool inside, F&& fn) {
 template <typename F>
 hipError_t timed_launch(md_handle_s* h, int id, F&& fn) {
     return timed_launch_ev(h, id, false, [&](hipEvent_t, hipEvent_t) { return fn(); });
+}
+
+// Tag of the next append launch: never 0 (the scratch starts zeroed) and
+// never the previous one.
+uint32_t next_append_tag(md_handle_s* h) {
+    h->append_tag = (h->append_tag % md::kAppendTagMask) + 1;
+    return h->append_tag;
 }
 
 void release_events(md_handle_s* h) {
@@ -450,6 +458,7 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     h->fused_steady = fused_steady;
     h->fused_last = false;
     h->observed = 0;
+    h->append_tag = 0;
     h->phase = kNone;
     h->sel_serial = nullptr;
     h->sel_count = nullptr;
@@ -478,7 +487,8 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     if (q == nullptr) {
         // a decode step without an observation: the append and the clock only
         if (timed_launch(h, MD_K_APPEND, [&] {
-                return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, 0, 0, h->stream); }) !=
+                return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, 0, 0, next_append_tag(h),
+                                         h->stream); }) !=
             hipSuccess)
             return MD_E_HIP;
         h->have_step = true;
@@ -489,7 +499,8 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     }
     const bool fused = h->observed == 0 ? h->fused_first : h->fused_steady;
     hipError_t e = timed_launch(h, MD_K_APPEND, [&] {
-        return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, fused ? 1 : 0, 1, h->stream); });
+        return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, fused ? 1 : 0, 1, next_append_tag(h),
+                                 h->stream); });
     // On a fused step, sessions that fit one pass of the fused kernel run
     // there; the others (only possible when a session may outgrow n_wg * T
     // tokens) take the three-kernel path with the logits in HBM, which on

@@ -113,6 +113,7 @@ struct Scratch {
     int32_t* warn;         // [1] warning bits (1: some session's budget was infeasible)
     int32_t* done_compact; // [1] completion counter of the compaction kernel
     unsigned long long* compact_acc;   // [1] the same for its trusted form: blocks done << 40 | gaps
+    unsigned long long* app_word;      // [S] append kernel: each session's new counts, tagged
     int32_t* opened;       // [1] pages the append kernel takes from the free list
     unsigned long long* counters;  // [8] tokens scored, steps, pages evicted, tokens evicted, pages
                                    // offloaded, recalled, dropped from host memory, observed there
@@ -134,9 +135,11 @@ hipError_t static_scratch(void** ptr);
 // fused: this step observes on the fused kernel (sessions that fit a pass)
 // or, when 0, every session on the multi-kernel path.  observe: 0 for a
 // decode step without an observation (no work lists, no scored tokens).
+// tag: differs from the previous launch's (27 bits used)
+constexpr uint32_t kAppendTagMask = (1u << 27) - 1;
 hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
                          const uint16_t* new_k, const uint8_t* new_region, int fused, int observe,
-                         hipStream_t st);
+                         uint32_t tag, hipStream_t st);
 hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q,
                          int n_blocks, hipStream_t st);
 hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st);

@@ -73,10 +73,23 @@ __device__ bool opens_page(const Dims& dm, const View& v, int s2, const uint8_t*
 // No block changes a session's page or token count before the last block
 // (each block leaves its session's new counts in sc.freed / sc.chunks), so
 // every block judges the earlier sessions on the counts before the append.
+//
+// Each block hands its session's new counts to the last block as one 64-bit
+// word stored at device scope and tagged with the launch (`tag`, different
+// for consecutive launches), so the hand-off needs no memory fence: the last
+// block reads the words and waits, bounded, for any that still carries an
+// older tag.  (A device-scope fence writes back the L2 of the block's XCD.)
+__device__ __forceinline__ unsigned long long append_word(uint32_t tag, bool bad, bool opened, bool appended,
+                                                          int np, int nt) {
+    return ((unsigned long long)(tag & kAppendTagMask) << 37) | ((unsigned long long)bad << 36) |
+           ((unsigned long long)opened << 35) | ((unsigned long long)appended << 34) |
+           ((unsigned long long)(np & 0x3FFF) << 20) | (unsigned long long)(nt & 0xFFFFF);
+}
+
 __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                                                 const uint16_t* __restrict__ new_k,
                                                 const uint8_t* __restrict__ new_region, int fused,
-                                                int observe) {
+                                                int observe, uint32_t tag) {
     const int s = blockIdx.x;
     __shared__ int sh_phys, sh_slot, sh_last, sh_rank;
     __shared__ int lds[5 * 17];
@@ -123,6 +136,8 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         const int t = t0_clock + 1;
         v.clock[s] = t;
         int phys = -1, slot = 0;
+        bool opened = false, appended = false;
+        const bool bad = !counters_ok(np, nt, dm);
         if (new_k != nullptr && counters_ok(np, nt, dm)) {
             const size_t row = (size_t)s * dm.MP;
             bool open = !(np > 0 && nt < np * dm.P);
@@ -165,7 +180,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                         if (dm.quant) v.page_format[p] = 0;   // a reused page holds bf16 keys again
                         v.next_serial[s] += 1;
                         np += 1;
-                        atomicAdd(sc.opened, 1);
+                        opened = true;
                     } else {
                         atomicOr(sc.status, kDevCorrupt);
                     }
@@ -177,7 +192,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             }
             if (phys >= 0) {
                 nt += 1;
-                if (dm.aligned) v.n_live[s] += 1;
+                appended = true;
                 const size_t si = (size_t)phys * dm.P + slot;
                 v.region[si] = new_region[s];
                 v.t_ins[si] = t;
@@ -188,8 +203,8 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         sh_phys = phys;
         sh_slot = slot;
         // the session's counts after the append, applied by the last block
-        sc.freed[s] = np;
-        sc.chunks[s] = nt;
+        __hip_atomic_store(sc.app_word + s, append_word(tag, bad, opened, appended, np, nt), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
     const int phys = sh_phys;
@@ -212,31 +227,46 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         }
     }
 
-    // The last block to finish lays out the step's work lists.
-    __threadfence();
+    // The last block to finish lays out the step's work lists.  Every block
+    // has read all it reads of the counters before its increment.
     __syncthreads();
     if (threadIdx.x == 0) sh_last = (atomicAdd(sc.done, 1) == (int)gridDim.x - 1);
     __syncthreads();
     if (!sh_last) return;
-    __threadfence();
     __shared__ int s_n[kMaxSessions];      // live tokens (0 for a skipped session)
     __shared__ int s_pass[kMaxSessions];   // fused pass of the session, -1 on the spill path
-    if (threadIdx.x == 0) {
-        // pages taken from the free list by this append
-        const int fc = v.free_count[0];
-        v.free_count[0] = max(min(fc, dm.NP) - load_agent(sc.opened), 0);
-        *sc.opened = 0;
-    }
+    __shared__ int sh_opened;              // pages taken from the free list by this append
+    if (threadIdx.x == 0) sh_opened = 0;
+    __syncthreads();
+    int opened_mine = 0;
     for (int s2 = threadIdx.x; s2 < dm.S; s2 += blockDim.x) {
-        const int np = load_agent(sc.freed + s2);
-        const int nt = load_agent(sc.chunks + s2);
-        v.n_pages[s2] = np;
-        v.n_tokens[s2] = nt;
-        const bool ok = counters_ok(np, nt, dm);
-        if (!ok) atomicOr(sc.status, kDevCorrupt);
+        unsigned long long wd = __hip_atomic_load(sc.app_word + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        bool stale = (uint32_t)(wd >> 37) != (tag & kAppendTagMask);
+        while (stale && __builtin_amdgcn_s_memrealtime() - t0 < 100000ull) {   // 1 ms
+            __builtin_amdgcn_s_sleep(2);
+            wd = __hip_atomic_load(sc.app_word + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            stale = (uint32_t)(wd >> 37) != (tag & kAppendTagMask);
+        }
+        const int np = (int)((wd >> 20) & 0x3FFF), nt = (int)(wd & 0xFFFFF);
+        const bool ok = !stale && !((wd >> 36) & 1ull) && counters_ok(np, nt, dm);
+        if (ok) {
+            v.n_pages[s2] = np;
+            v.n_tokens[s2] = nt;
+            opened_mine += (int)((wd >> 35) & 1ull);
+            if (dm.aligned && ((wd >> 34) & 1ull)) v.n_live[s2] += 1;
+        } else {
+            atomicOr(sc.status, kDevCorrupt);
+        }
         sc.valid[s2] = ok ? 1 : 0;
         s_n[s2] = ok ? nt : 0;
         s_pass[s2] = -1;
+    }
+    if (opened_mine > 0) atomicAdd(&sh_opened, opened_mine);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int fc = v.free_count[0];
+        v.free_count[0] = max(min(fc, dm.NP) - sh_opened, 0);
     }
     // Lane mode when every fused session fits half a lane (one workgroup
     // per CU): each lane then claims whole sessions as it goes (see
@@ -323,7 +353,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             it[k] = ch * dm.LHkv;
             ti[k] = spill ? (nt + kTile - 1) / kTile : 0;
             si[k] = (nt + kTile - 1) / kTile;
-            my_tokens += (dm.aligned && nt > 0) ? load_agent(v.n_live + s2) : nt;
+            my_tokens += (dm.aligned && nt > 0) ? v.n_live[s2] : nt;
         }
         my_units += uu[k];
         my_items += it[k];
@@ -368,8 +398,8 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
 
 hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
                          const uint16_t* new_k, const uint8_t* new_region, int fused, int observe,
-                         hipStream_t st) {
-    hipLaunchKernelGGL(k_append, dim3(dm.S), dim3(256), 0, st, dm, v, sc, new_k, new_region, fused, observe);
+                         uint32_t tag, hipStream_t st) {
+    hipLaunchKernelGGL(k_append, dim3(dm.S), dim3(256), 0, st, dm, v, sc, new_k, new_region, fused, observe, tag);
     return hipGetLastError();
 }
 
@@ -1388,6 +1418,7 @@ size_t scratch_bytes(const Dims& dm) {
     n += align256(9 * sizeof(unsigned long long));
     n += align256((size_t)dm.S * dm.H * sizeof(int32_t));
     n += align256((size_t)(dm.S + 1) * sizeof(int32_t));
+    n += align256((size_t)dm.S * sizeof(unsigned long long));
     return n;
 }
 
@@ -1427,6 +1458,7 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
     sc->opened = words + 4;
     sc->counters = reinterpret_cast<unsigned long long*>(take(9 * sizeof(unsigned long long)));
     sc->compact_acc = sc->counters + 8;
+    sc->app_word = reinterpret_cast<unsigned long long*>(take((size_t)dm.S * sizeof(unsigned long long)));
     sc->recall = reinterpret_cast<int32_t*>(take((size_t)dm.S * dm.H * sizeof(int32_t)));
     sc->rcount = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
 }

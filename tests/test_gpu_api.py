@@ -201,3 +201,27 @@ def test_state_lives_in_caller_buffers():
         m = int(p.cache.n_pages[0].item())
         assert torch.equal(p.md.page_score[0, :m].view(torch.int32), first[i].view(torch.int32))
     p.close()
+
+
+@pytest.mark.parametrize("cooperative", [False, True])
+def test_kernel_timing(cooperative):
+    # md_profile_enable / md_profile_read: every launch of a timed kernel is
+    # counted once with a positive, finite duration (the fused kernel's
+    # events come with its own dispatch on an ordinary launch, around it on
+    # a cooperative one); a read resets the counts, and timing off stops them
+    p = small_pair(oracle_sessions=[], fused=True, cooperative=cooperative)
+    md = p.md
+    md.profile(("append", "attend", "select", "compact"))
+    for k in range(1, 5):
+        p.step(compare=False)
+    torch.cuda.synchronize()
+    for name in ("append", "attend", "select", "compact"):
+        ms, n = md.profile_read(name)
+        assert n == 4, (name, n)
+        assert np.isfinite(ms) and 0.0 < ms < 4 * 1000.0, (name, ms)
+        assert md.profile_read(name) == (0.0, 0)
+    md.profile(())
+    p.step(compare=False)
+    assert md.profile_read("attend") == (0.0, 0)
+    assert md.device_status() == 0
+    p.close()
