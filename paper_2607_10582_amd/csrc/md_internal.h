@@ -108,13 +108,12 @@ struct Scratch {
                            // consistent, its query finite and no wait of the fused
                            // kernel ran out; 0 leaves it out of selection and compaction
     int32_t* freed;        // [S + 1] pages each session's compaction frees
-    int32_t* done;         // [1] completion counter of the append kernel
     int32_t* status;       // [1] device status word
     int32_t* warn;         // [1] warning bits (1: some session's budget was infeasible)
-    int32_t* done_compact; // [1] completion counter of the compaction kernel
+    int32_t* done_compact; // [1] completion counter of the compaction and recall kernels
     unsigned long long* compact_acc;   // [1] the same for its trusted form: blocks done << 40 | gaps
     unsigned long long* app_word;      // [S] append kernel: each session's new counts, tagged
-    int32_t* opened;       // [1] pages the append kernel takes from the free list
+    int32_t* opened;       // [1] pages the recall kernel takes from the free list
     unsigned long long* counters;  // [8] tokens scored, steps, pages evicted, tokens evicted, pages
                                    // offloaded, recalled, dropped from host memory, observed there
     int32_t* recall;       // [S][H] offload tier: the listed page is recalled at this step

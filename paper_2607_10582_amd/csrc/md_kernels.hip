@@ -3,7 +3,7 @@
 // One step over a batch of sessions runs seven kernels on the caller's stream:
 //   k_append    one block per session: clock, append into the tail page or a
 //               page popped from the free list, copy of the new key rows; the
-//               last block to finish builds the step's work lists.
+//               last block builds the step's work lists.
 //   k_logits    HOT: every cached token's logits q.k/sqrt(d) for all query heads
 //               (Sec. III-C), one 128-token chunk of one (layer, KV head) per
 //               wave, on MFMA; chunk softmax statistics; logits spilled for
@@ -66,13 +66,13 @@ __device__ bool opens_page(const Dims& dm, const View& v, int s2, const uint8_t*
     return v.region[(size_t)p * dm.P + slot - 1] != new_region[s2];
 }
 
-// One block per session: the append.  The last block to finish lays out the
-// step's work lists.
+// One block per session: the append.  The last block (highest index) also
+// lays out the step's work lists.
 // Pages leave the free list in session order: session s takes the entry
 // below those of the sessions before it that open a page at this append.
-// No block changes a session's page or token count before the last block
-// (each block leaves its session's new counts in sc.freed / sc.chunks), so
-// every block judges the earlier sessions on the counts before the append.
+// No block but the last changes a session's page or token count (each block
+// hands its session's new counts to the last one), so every block judges
+// the earlier sessions on the counts before the append.
 //
 // Each block hands its session's new counts to the last block as one 64-bit
 // word stored at device scope and tagged with the launch (`tag`, different
@@ -91,7 +91,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                                                 const uint8_t* __restrict__ new_region, int fused,
                                                 int observe, uint32_t tag) {
     const int s = blockIdx.x;
-    __shared__ int sh_phys, sh_slot, sh_last, sh_rank;
+    __shared__ int sh_phys, sh_slot, sh_rank;
     __shared__ int lds[5 * 17];
     // The step's key rows (16 pieces of 16 bytes per (layer, KV head) row)
     // do not depend on the slot: waves 1.. read their first kPre pieces now
@@ -113,12 +113,13 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     // pages the sessions before this one take at this append), and the last
     // page's table entry right behind them, so the chain to the slot is
     // three round trips to memory rather than six.
-    int t0_clock = 0, np = 0, nt = 0, fc0 = 0, last_p = -1;
+    int t0_clock = 0, np = 0, nt = 0, fc0 = 0, ep0 = 0, last_p = -1;
     if (threadIdx.x == 0) {
         t0_clock = v.clock[s];
         np = v.n_pages[s];
         nt = v.n_tokens[s];
-        fc0 = v.free_count[0];   // changes only in the last block
+        fc0 = v.free_count[0];   // the free count and the epoch change only in the last block
+        ep0 = *sc.epoch;
     }
     if (threadIdx.x == 0) sh_rank = 0;
     int rank_mine = 0;
@@ -227,12 +228,13 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         }
     }
 
-    // The last block to finish lays out the step's work lists.  Every block
-    // has read all it reads of the counters before its increment.
-    __syncthreads();
-    if (threadIdx.x == 0) sh_last = (atomicAdd(sc.done, 1) == (int)gridDim.x - 1);
-    __syncthreads();
-    if (!sh_last) return;
+    // The last block (the highest index: blocks are dispatched in index
+    // order, so every other block has started before it) lays out the step's
+    // work lists once every session's word carries this launch's tag.  A
+    // block stores its word after all its reads of the counters have
+    // returned (the word is computed from them), so no block reads a count
+    // the last block has already changed.
+    if (s != (int)gridDim.x - 1) return;
     __shared__ int s_n[kMaxSessions];      // live tokens (0 for a skipped session)
     __shared__ int s_pass[kMaxSessions];   // fused pass of the session, -1 on the spill path
     __shared__ int sh_opened;              // pages taken from the free list by this append
@@ -264,10 +266,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     }
     if (opened_mine > 0) atomicAdd(&sh_opened, opened_mine);
     __syncthreads();
-    if (threadIdx.x == 0) {
-        const int fc = v.free_count[0];
-        v.free_count[0] = max(min(fc, dm.NP) - sh_opened, 0);
-    }
+    if (threadIdx.x == 0) v.free_count[0] = max(min(fc0, dm.NP) - sh_opened, 0);
     // Lane mode when every fused session fits half a lane (one workgroup
     // per CU): each lane then claims whole sessions as it goes (see
     // k_attend), at least two per pass.  A larger session would leave the
@@ -293,7 +292,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         // within one workgroup per CU and at most blockDim.x sessions (what
         // the kernel's own claims take); the rest stays to be claimed.
         sc.plan[0] = -1;
-        const int ep = *sc.epoch + 1;
+        const int ep = ep0 + 1;
         *sc.epoch = ep;
         auto units = [&](int s2) { return (s_n[s2] + dm.T - 1) / dm.T; };
         int f0 = 0, used = 0;
@@ -332,7 +331,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             s0 = e;
         }
         sc.plan[0] = np;
-        *sc.epoch += 1;
+        *sc.epoch = ep0 + 1;
     }
     __syncthreads();
     // Work lists: fused units; attention items, chunks and mass tiles of the
@@ -388,7 +387,6 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         sc.item_prefix[dm.S] = tot_i;
         sc.tile_prefix[dm.S] = tot_t;
         sc.score_prefix[dm.S] = tot_s;
-        *sc.done = 0;
         if (observe) {
             atomicAdd(&sc.counters[0], (unsigned long long)tot_n);
             atomicAdd(&sc.counters[1], 1ull);
@@ -913,14 +911,40 @@ __device__ int page_tokens(const Dims& dm, const View& v, int phys, int i, int n
 // with key == T go in serial order until the need is met.  Pinned pages
 // (+inf) never enter.  Each thread owns a contiguous run of page indices, so
 // per-thread runs in thread order are the serial order.
+// When the pages holding the smallest key already weigh at least the need
+// (the usual decode step: one token over the budget), T is that key and the
+// radix passes are skipped.
 __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch sc,
                                                         int32_t* ev_serial, int32_t* ev_count,
                                                         uint8_t* infeasible) {
     const int s = blockIdx.x;
     __shared__ int lds[17];
+    __shared__ uint32_t s_min[16];
     __shared__ int hist[256];
     __shared__ int sh_digit, sh_before;
     const int tid = threadIdx.x;
+    const uint32_t kInf = 0x7F800000u;
+    const float* ps = sc.pscore + (size_t)s * dm.MP;
+    const int* ser = v.page_serial + (size_t)s * dm.MP;
+    const int* ptab = v.page_table + (size_t)s * dm.MP;
+    // The runs split the page-table capacity, not the session's pages, so
+    // the scores (and, for region-aligned pages, the table entries) go out
+    // with the counters rather than after them; entries past the session's
+    // pages are read but not used.
+    const int per = (dm.MP + kSelThreads - 1) / kSelThreads;
+    const int i0 = min(dm.MP, tid * per), ie = min(dm.MP, i0 + per);
+    float sv[kPerThread];
+    int pv[kPerThread], sr[kPerThread];
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+        sv[k] = 0.0f;
+        pv[k] = sr[k] = 0;
+        if (i0 + k < ie) {
+            sv[k] = ps[i0 + k];
+            sr[k] = ser[i0 + k];
+            if (dm.aligned) pv[k] = ptab[i0 + k];
+        }
+    }
     const int np = v.n_pages[s], nt = v.n_tokens[s], B = v.budget[s];
     const int need = v.n_live[s] - B;
     if (!sc.valid[s] || need <= 0 || np == 0) {
@@ -930,32 +954,40 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
         }
         return;
     }
-    const uint32_t kInf = 0x7F800000u;
-    const float* ps = sc.pscore + (size_t)s * dm.MP;
-    const int* ser = v.page_serial + (size_t)s * dm.MP;
-    const int* ptab = v.page_table + (size_t)s * dm.MP;
-    const int per = (np + kSelThreads - 1) / kSelThreads;
-    const int i0 = min(np, tid * per), i1 = min(np, i0 + per);
+    const int i1 = min(np, ie);
     uint32_t key[kPerThread];
     int wt[kPerThread];
     int wsum = 0;
+    uint32_t kmin = kInf;
 #pragma unroll
     for (int k = 0; k < kPerThread; ++k) {
         const int i = i0 + k;
         key[k] = kInf;
         wt[k] = 0;
         if (i < i1) {
-            key[k] = __float_as_uint(ps[i]);
-            wt[k] = page_tokens(dm, v, dm.aligned ? ptab[i] : 0, i, np, nt);
+            key[k] = __float_as_uint(sv[k]);
+            wt[k] = page_tokens(dm, v, pv[k], i, np, nt);
             if (key[k] < kInf) wsum += wt[k];
+            kmin = min(kmin, key[k]);
         }
     }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o));
+    if (lane_id() == 0) s_min[tid >> 6] = kmin;
     int total;
-    block_exclusive_scan(wsum, lds, &total);
+    block_exclusive_scan(wsum, lds, &total);   // its barriers publish s_min too
     const bool infeas = total < need;
-    uint32_t T = 0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) kmin = min(kmin, s_min[w]);
+    // the smallest key's weight, and each thread's share of it before its run
+    int teq = 0;
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k)
+        if (key[k] == kmin && key[k] < kInf) teq += wt[k];
+    int at_min;
+    int run = block_exclusive_scan(teq, lds, &at_min);
+    uint32_t T = kmin;
     int rem = need;
-    if (!infeas) {
+    if (!infeas && at_min < need) {
         uint32_t prefix = 0, pmask = 0;
         for (int shift = 24; shift >= 0; shift -= 8) {
             if (tid < 256) hist[tid] = 0;
@@ -997,14 +1029,14 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
             __syncthreads();
         }
         T = prefix;
-    }
-    // weights of the key == T pages before this thread's run
-    int teq = 0;
+        // weights of the key == T pages before this thread's run
+        teq = 0;
 #pragma unroll
-    for (int k = 0; k < kPerThread; ++k)
-        if (!infeas && key[k] == T) teq += wt[k];
-    int dummy;
-    int run = block_exclusive_scan(teq, lds, &dummy);
+        for (int k = 0; k < kPerThread; ++k)
+            if (key[k] == T) teq += wt[k];
+        int dummy;
+        run = block_exclusive_scan(teq, lds, &dummy);
+    }
     bool ev[kPerThread];
     int my_ev = 0;
 #pragma unroll
@@ -1028,7 +1060,7 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
     int32_t* out = ev_serial + (size_t)s * dm.MP;
 #pragma unroll
     for (int k = 0; k < kPerThread; ++k)
-        if (ev[k]) out[pos++] = ser[i0 + k];
+        if (ev[k]) out[pos++] = sr[k];
     if (tid == 0) {
         ev_count[s] = n_ev;
         infeasible[s] = infeas ? 1 : 0;
@@ -1070,51 +1102,70 @@ __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratc
                                                          const int32_t* __restrict__ ev_count, int trusted) {
     const int s = blockIdx.x;
     __shared__ int lds[3 * 17];
-    __shared__ int sh_last, sh_before;
+    __shared__ int sh_last, sh_before, sh_listed;
+    __shared__ int s_evs[kMaxPages];   // the session's list, searched in LDS
     const int tid = threadIdx.x;
     // Every load that depends on nothing else goes out at once: the
     // session's list length and counters, the free count (it changes only in
-    // the last block, after every block has read it), and the list lengths of
-    // the sessions before this one (their places on the free list).
+    // the last block, after every block has read it), the list lengths of
+    // all sessions (those before this one give its places on the free list,
+    // all of them the growth of the list), and the thread's run of the table
+    // and of the list.  The runs split the page-table capacity, so they need
+    // no count first; entries past the session's pages or list are not used.
     const int cnt = evict_listed(dm, sc, ev_count, s);
     const int np = v.n_pages[s], nt = v.n_tokens[s];
     const int fc = v.free_count[0];
-    int mine = 0;
-    for (int s2 = tid; s2 < s; s2 += blockDim.x) mine += evict_listed(dm, sc, ev_count, s2);
-    if (tid == 0) sh_before = 0;
+    const int* evs = ev_serial + (size_t)s * dm.MP;
+    int* ptab = v.page_table + (size_t)s * dm.MP;
+    int* pser = v.page_serial + (size_t)s * dm.MP;
+    const int per = (dm.MP + kSelThreads - 1) / kSelThreads;
+    const int i0 = min(dm.MP, tid * per), ie = min(dm.MP, i0 + per);
+    int ph[kPerThread], se[kPerThread];
+#pragma unroll
+    for (int k = 0; k < kPerThread; ++k) {
+        ph[k] = se[k] = 0;
+        if (i0 + k < ie) {
+            ph[k] = ptab[i0 + k];
+            se[k] = pser[i0 + k];
+            s_evs[i0 + k] = evs[i0 + k];
+        }
+    }
+    int mine = 0, all = 0;
+    for (int s2 = tid; s2 < dm.S; s2 += blockDim.x) {
+        const int c = evict_listed(dm, sc, ev_count, s2);
+        mine += s2 < s ? c : 0;
+        all += c;
+    }
+    if (tid == 0) sh_before = sh_listed = 0;
     __syncthreads();
     {
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o);
+        for (int o = 32; o > 0; o >>= 1) {
+            mine += __shfl_xor(mine, o);
+            all += __shfl_xor(all, o);
+        }
         if (lane_id() == 0 && mine > 0) atomicAdd(&sh_before, mine);
+        if (lane_id() == 0 && all > 0) atomicAdd(&sh_listed, all);
     }
     __syncthreads();
     int gone_total = 0;
     if (cnt > 0 && np == 0) {
         if (tid == 0) atomicOr(sc.status, MD_DEV_BAD_EVICT);
     } else if (cnt > 0) {
-        const int* evs = ev_serial + (size_t)s * dm.MP;
-        int* ptab = v.page_table + (size_t)s * dm.MP;
-        int* pser = v.page_serial + (size_t)s * dm.MP;
-        const int per = (np + kSelThreads - 1) / kSelThreads;
-        const int i0 = min(np, tid * per), i1 = min(np, i0 + per);
-        int ph[kPerThread], se[kPerThread];
+        const int i1 = min(np, ie);
         bool keep[kPerThread];
         int n_keep = 0, n_gone = 0, live_gone = 0;
 #pragma unroll
         for (int k = 0; k < kPerThread; ++k) {
             const int i = i0 + k;
             keep[k] = false;
-            ph[k] = se[k] = 0;
             if (i < i1) {
-                ph[k] = ptab[i];
-                se[k] = pser[i];
-                int lo = 0, hi = min(cnt, dm.MP);
+                int lo = 0, hi = cnt;
                 while (lo < hi) {  // serials in the list ascend
                     const int mid = (lo + hi) >> 1;
-                    if (evs[mid] < se[k]) lo = mid + 1; else hi = mid;
+                    if (s_evs[mid] < se[k]) lo = mid + 1; else hi = mid;
                 }
-                const bool gone = lo < min(cnt, dm.MP) && evs[lo] == se[k];
+                const bool gone = lo < cnt && s_evs[lo] == se[k];
                 keep[k] = !gone;
                 n_keep += gone ? 0 : 1;
                 n_gone += gone ? 1 : 0;
@@ -1179,13 +1230,8 @@ __global__ void __launch_bounds__(kSelThreads) k_compact(Dims dm, View v, Scratc
         if (!sh_last) return;
         // the last block: every block has read the free count; the list grew
         // by one place per listed page
-        int listed = 0;
-        for (int s2 = tid; s2 < dm.S; s2 += blockDim.x) listed += evict_listed(dm, sc, ev_count, s2);
-        const int m1[1] = {listed};
-        int ex1[1], tot1[1];
-        block_exclusive_scan_n<1>(m1, lds, ex1, tot1);
         if (tid == 0) {
-            v.free_count[0] = min(max(fc, 0) + tot1[0], dm.NP);
+            v.free_count[0] = min(max(fc, 0) + sh_listed, dm.NP);
             *sc.compact_acc = 0;
         }
         return;
@@ -1450,12 +1496,11 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
         take((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long)));
     sc->unorm = reinterpret_cast<unsigned long long*>(
         take((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long)));
-    int32_t* words = reinterpret_cast<int32_t*>(take(5 * sizeof(int32_t)));
-    sc->done = words;
-    sc->status = words + 1;
-    sc->warn = words + 2;
-    sc->done_compact = words + 3;
-    sc->opened = words + 4;
+    int32_t* words = reinterpret_cast<int32_t*>(take(4 * sizeof(int32_t)));
+    sc->status = words;      // the warning word follows the status word (read together)
+    sc->warn = words + 1;
+    sc->done_compact = words + 2;
+    sc->opened = words + 3;
     sc->counters = reinterpret_cast<unsigned long long*>(take(9 * sizeof(unsigned long long)));
     sc->compact_acc = sc->counters + 8;
     sc->app_word = reinterpret_cast<unsigned long long*>(take((size_t)dm.S * sizeof(unsigned long long)));
