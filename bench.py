@@ -37,7 +37,6 @@ the host's cores, on a sample of the same workload.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -50,8 +49,6 @@ sys.path.insert(0, ROOT)
 
 METRIC = "cached tokens scored+evicted per second per decode step; achieved HBM GB/s vs peak"
 PEAK_HBM_GBS = 8000.0
-CSRC = os.path.join(ROOT, "paper_2607_10582_amd", "csrc")
-KERNEL_SRC = {"logits": os.path.join(CSRC, "md_kernels.hip"), "attend": os.path.join(CSRC, "md_attend.hip")}
 DEFAULT_WORKLOAD = "ragged_p16"
 DEFAULT_ALSO = "ragged_p64,long32k"
 
@@ -61,8 +58,8 @@ def log(*a):
 
 
 def kernel_source_hash(kernel: str) -> str:
-    with open(KERNEL_SRC[kernel], "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    from paper_2607_10582_amd.rocprof_summary import source_hash
+    return source_hash("k_" + kernel)
 
 
 def describe(w, n0s) -> str:

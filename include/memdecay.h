@@ -14,6 +14,8 @@
  *
  *     md_observe_step  ->  md_score_pages  ->  md_select_evict  ->  md_compact
  *
+ * (the last two also as one call, md_select_compact)
+ *
  * over a batch of independent sessions whose keys live in a paged bf16 pool.
  *
  * Conventions for every entry point
@@ -75,7 +77,7 @@
 extern "C" {
 #endif
 
-#define MD_ABI_VERSION 8
+#define MD_ABI_VERSION 9
 
 typedef int32_t md_status;
 
@@ -376,6 +378,18 @@ md_status md_select_evict(md_handle h, int32_t* evict_serial, int32_t* evict_cou
  */
 md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* evict_count);
 
+/*
+ * md_select_compact — md_select_evict followed by md_compact(h, NULL, NULL)
+ * (Alg. 1's eviction loop and its application, Sec. III-D and III-E) as one
+ * call: the same lists, infeasible flags, page tables, counts and free list
+ * as the two calls.  Without a tier (offload_pages = 0, quant_threshold = 0)
+ * it is one launch, each session's block selecting and compacting its own
+ * pages; with a tier it enqueues the two calls' launches.  For callers that
+ * apply the library's own selection without looking at it in between.
+ * Arguments, layout and requirements as for md_select_evict.
+ */
+md_status md_select_compact(md_handle h, int32_t* evict_serial, int32_t* evict_count, uint8_t* infeasible);
+
 /* Synchronise the stream and copy the device status word to *host_out, then
  * clear it.  Returns MD_W_BUDGET_INFEASIBLE when a selection since the last
  * read found a session whose pinned tokens exceed its budget (the
@@ -386,7 +400,9 @@ md_status md_read_device_status(md_handle h, int32_t* host_out);
 /* Kernel ids for md_profile_enable / md_profile_read. */
 enum {
     MD_K_APPEND = 0, MD_K_LOGITS = 1, MD_K_ROWSTATS = 2, MD_K_MASS = 3,
-    MD_K_SCORE = 4, MD_K_SELECT = 5, MD_K_COMPACT = 6, MD_K_ATTEND = 7, MD_K_COUNT = 8
+    MD_K_SCORE = 4, MD_K_SELECT = 5, MD_K_COMPACT = 6, MD_K_ATTEND = 7,
+    MD_K_EVICT = 8,   /* md_select_compact's one-launch form */
+    MD_K_COUNT = 9
 };
 
 /* Diagnostics.  md_profile_enable: from now on, time every launch of the

@@ -35,15 +35,15 @@ MD_FLAG_COOPERATIVE = 0x10
 MD_REGION_HOLE = 0xFF
 
 EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_init_static", "md_observe_step",
-           "md_score_pages", "md_select_evict", "md_compact", "md_read_device_status",
+           "md_score_pages", "md_select_evict", "md_compact", "md_select_compact", "md_read_device_status",
            "md_profile_enable", "md_profile_read", "md_read_counters", "md_kernel_config",
            "md_calib_accumulate", "md_calib_fit",
            "md_destroy")
 
 # kernel ids of md_profile_enable / md_profile_read
-KERNELS = ("append", "logits", "rowstats", "mass", "score", "select", "compact", "attend")
+KERNELS = ("append", "logits", "rowstats", "mass", "score", "select", "compact", "attend", "evict")
 (MD_K_APPEND, MD_K_LOGITS, MD_K_ROWSTATS, MD_K_MASS, MD_K_SCORE, MD_K_SELECT, MD_K_COMPACT,
- MD_K_ATTEND) = range(8)
+ MD_K_ATTEND, MD_K_EVICT) = range(9)
 
 
 class md_config(ctypes.Structure):
@@ -131,6 +131,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.md_select_evict.argtypes = [vp, vp, vp, vp]
     lib.md_compact.restype = i32
     lib.md_compact.argtypes = [vp, vp, vp]
+    lib.md_select_compact.restype = i32
+    lib.md_select_compact.argtypes = [vp, vp, vp, vp]
     lib.md_read_device_status.restype = i32
     lib.md_read_device_status.argtypes = [vp, ctypes.POINTER(i32)]
     lib.md_profile_enable.restype = i32
@@ -207,6 +209,11 @@ def md_select_evict(h: int, evict_serial: int, evict_count: int, infeasible: int
 def md_compact(h: int, evict_serial: int | None = None, evict_count: int | None = None) -> int:
     """Both lists None: apply this step's selection."""
     return _check("md_compact", load_library().md_compact(h, evict_serial or None, evict_count or None))
+
+
+def md_select_compact(h: int, evict_serial: int, evict_count: int, infeasible: int) -> int:
+    return _check("md_select_compact", load_library().md_select_compact(
+        h, evict_serial, evict_count, infeasible))
 
 
 def md_read_device_status(h: int, with_warning: bool = False):

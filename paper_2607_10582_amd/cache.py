@@ -237,15 +237,21 @@ class MemDecay:
         else:
             B.md_compact(self.handle, _ptr(evict_serial, torch.int32), _ptr(evict_count, torch.int32))
 
+    def select_compact(self):
+        """select() then compact() with this step's selection, as one call
+        (one launch when no tier is configured)."""
+        B.md_select_compact(self.handle, self.evict_serial.data_ptr(), self.evict_count.data_ptr(),
+                            self.infeasible.data_ptr())
+
     def step(self, step: int, q, new_k=None, new_region=None, page_scores: bool = True):
         """One decode step; page_scores=False leaves self.page_score untouched
-        (the library still scores every page for its own selection)."""
+        (the library still scores every page for its own selection).  The
+        step's selection is applied as it stands (select_compact)."""
         self.observe(step, q, new_k, new_region)
         if q is None:   # a decode step without an observation only appends
             return
         self.score(page_score=page_scores)
-        self.select()
-        self.compact()
+        self.select_compact()
 
     def calib_accumulate(self, abar: torch.Tensor, bucket_steps: int, stats) -> None:
         """Add this observation to stats = (mass_fx, count, age_sum), int64

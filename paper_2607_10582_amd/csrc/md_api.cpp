@@ -49,7 +49,7 @@ struct md_handle_s {
     std::vector<Timed> pending[MD_K_COUNT];   // launches not yet read back
     std::vector<Timed> spare;                  // recycled event pairs
     int static_slot;     // md_init_static: index in the static handles; -1 otherwise
-    uint32_t append_tag; // launches of the append kernel (their tag)
+    uint32_t word_tag; // tag of the last launch handing counts between blocks through tagged words
 };
 
 namespace {
@@ -123,11 +123,12 @@ hipError_t timed_launch(md_handle_s* h, int id, F&& fn) {
     return timed_launch_ev(h, id, false, [&](hipEvent_t, hipEvent_t) { return fn(); });
 }
 
-// Tag of the next append launch: never 0 (the scratch starts zeroed) and
-// never the previous one.
-uint32_t next_append_tag(md_handle_s* h) {
-    h->append_tag = (h->append_tag % md::kAppendTagMask) + 1;
-    return h->append_tag;
+// Tag of the next launch that hands counts between its blocks through
+// tagged words (the append, the one-launch select-and-compact): never 0 (the
+// scratch starts zeroed) and never the previous one.
+uint32_t next_word_tag(md_handle_s* h) {
+    h->word_tag = (h->word_tag % md::kWordTagMask) + 1;
+    return h->word_tag;
 }
 
 void release_events(md_handle_s* h) {
@@ -458,7 +459,7 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     h->fused_steady = fused_steady;
     h->fused_last = false;
     h->observed = 0;
-    h->append_tag = 0;
+    h->word_tag = 0;
     h->phase = kNone;
     h->sel_serial = nullptr;
     h->sel_count = nullptr;
@@ -487,7 +488,7 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     if (q == nullptr) {
         // a decode step without an observation: the append and the clock only
         if (timed_launch(h, MD_K_APPEND, [&] {
-                return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, 0, 0, next_append_tag(h),
+                return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, 0, 0, next_word_tag(h),
                                          h->stream); }) !=
             hipSuccess)
             return MD_E_HIP;
@@ -499,7 +500,7 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     }
     const bool fused = h->observed == 0 ? h->fused_first : h->fused_steady;
     hipError_t e = timed_launch(h, MD_K_APPEND, [&] {
-        return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, fused ? 1 : 0, 1, next_append_tag(h),
+        return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, fused ? 1 : 0, 1, next_word_tag(h),
                                  h->stream); });
     // On a fused step, sessions that fit one pass of the fused kernel run
     // there; the others (only possible when a session may outgrow n_wg * T
@@ -582,6 +583,26 @@ md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* ev
     if (timed_launch(h, MD_K_COMPACT, [&] {
             return md::launch_compact(h->dm, h->v, h->sc, evict_serial, evict_count, trusted, h->stream); }) !=
         hipSuccess)
+        return MD_E_HIP;
+    h->phase = kCompacted;
+    h->sel_serial = h->sel_count = nullptr;
+    return MD_OK;
+}
+
+md_status md_select_compact(md_handle h, int32_t* evict_serial, int32_t* evict_count, uint8_t* infeasible) {
+    if (h == nullptr || evict_serial == nullptr || evict_count == nullptr || infeasible == nullptr)
+        return MD_E_INVALID;
+    if (!aligned(evict_serial, 4) || !aligned(evict_count, 4)) return MD_E_INVALID;
+    if (h->phase != kScored) return MD_E_STATE;
+    if (h->dm.quant || h->dm.H > 0) {   // the tiers run between the selection and the compaction
+        const md_status st = md_select_evict(h, evict_serial, evict_count, infeasible);
+        return st != MD_OK ? st : md_compact(h, nullptr, nullptr);
+    }
+    if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
+    const uint32_t tag = next_word_tag(h);
+    if (timed_launch(h, MD_K_EVICT, [&] {
+            return md::launch_evict(h->dm, h->v, h->sc, evict_serial, evict_count, infeasible, tag,
+                                    h->stream); }) != hipSuccess)
         return MD_E_HIP;
     h->phase = kCompacted;
     h->sel_serial = h->sel_count = nullptr;

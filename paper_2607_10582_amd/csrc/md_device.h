@@ -38,70 +38,73 @@ __device__ __forceinline__ int load_agent(const int32_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Exclusive prefix of one int per thread across the whole block (any multiple
-// of 64 threads up to 1024).  lds needs 17 ints.  Contains __syncthreads.
-// N exclusive block-wide scans side by side, with one pair of barriers
-// (lds: 17 N ints).
+// Inclusive prefix sum over the 64 lanes of a wave with DPP moves: shifts
+// by 1, 2, 4 and 8 lanes inside each row of 16, then the last lane of each
+// row added to the rows after it (row broadcasts of lanes 15 and 31).  A
+// lane whose source lies outside its row, or whose row the mask leaves out,
+// adds the identity.
+__device__ __forceinline__ int wave_incl_sum(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);   // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);   // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);   // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);   // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);   // row_bcast:15 into rows 1, 3
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);   // row_bcast:31 into rows 2, 3
+    return v;
+}
+
+// Minimum over the 64 lanes of a wave (the same DPP steps; the last lane
+// ends with the minimum of all, read back to every lane).
+template <int Ctrl, int RowMask>
+__device__ __forceinline__ uint32_t dpp_min_step(uint32_t v) {
+    // -1 = 0xFFFFFFFF, the identity of the unsigned minimum
+    const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(-1, (int)v, Ctrl, RowMask, 0xf, false);
+    return v < o ? v : o;
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+    v = dpp_min_step<0x111, 0xf>(v);
+    v = dpp_min_step<0x112, 0xf>(v);
+    v = dpp_min_step<0x114, 0xf>(v);
+    v = dpp_min_step<0x118, 0xf>(v);
+    v = dpp_min_step<0x142, 0xa>(v);
+    v = dpp_min_step<0x143, 0xc>(v);
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// N exclusive block-wide scans side by side (any multiple of 64 threads up
+// to 1024; lds: 17 N ints).  Each wave scans its lanes (DPP) and publishes
+// its total; after one barrier every wave scans the (at most 16) wave totals
+// itself, so no thread walks them serially.  Ends with a barrier, after
+// which lds may be reused.
 template <int N>
 __device__ inline void block_exclusive_scan_n(const int (&v)[N], int* lds, int (&ex)[N], int (&total)[N]) {
     const int lane = lane_id(), wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
     int incl[N];
 #pragma unroll
-    for (int k = 0; k < N; ++k) incl[k] = v[k];
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1)
-#pragma unroll
-        for (int k = 0; k < N; ++k) {
-            const int t = __shfl_up(incl[k], o);
-            if (lane >= o) incl[k] += t;
-        }
+    for (int k = 0; k < N; ++k) incl[k] = wave_incl_sum(v[k]);
     if (lane == 63)
 #pragma unroll
         for (int k = 0; k < N; ++k) lds[17 * k + wid] = incl[k];
     __syncthreads();
-    if ((int)threadIdx.x < N) {
-        int* l = lds + 17 * threadIdx.x;
-        int acc = 0;
-        for (int w = 0; w < nw; ++w) {
-            const int t = l[w];
-            l[w] = acc;
-            acc += t;
-        }
-        l[16] = acc;
-    }
-    __syncthreads();
 #pragma unroll
     for (int k = 0; k < N; ++k) {
-        ex[k] = lds[17 * k + wid] + incl[k] - v[k];
-        total[k] = lds[17 * k + 16];
+        const int t = wave_incl_sum(lane < nw ? lds[17 * k + lane] : 0);
+        const int before = __builtin_amdgcn_readlane(t, wid > 0 ? wid - 1 : 0);
+        ex[k] = (wid > 0 ? before : 0) + incl[k] - v[k];
+        total[k] = __builtin_amdgcn_readlane(t, nw - 1);
     }
     __syncthreads();
 }
 
+// Exclusive prefix of one int per thread across the whole block; *total is
+// the block's sum.  lds needs 17 ints.  Ends with a barrier.
 __device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
-    const int lane = lane_id(), wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    int incl = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int t = __shfl_up(incl, o);
-        if (lane >= o) incl += t;
-    }
-    if (lane == 63) lds[wid] = incl;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int acc = 0;
-        for (int w = 0; w < nw; ++w) {
-            const int t = lds[w];
-            lds[w] = acc;
-            acc += t;
-        }
-        lds[16] = acc;
-    }
-    __syncthreads();
-    const int res = lds[wid] + incl - v;
-    *total = lds[16];
-    __syncthreads();
-    return res;
+    const int m[1] = {v};
+    int ex[1], tot[1];
+    block_exclusive_scan_n<1>(m, lds, ex, tot);
+    *total = tot[0];
+    return ex[0];
 }
 
 // Largest s in [0, S) with pref[s] <= x, given pref[0] <= x < pref[S].

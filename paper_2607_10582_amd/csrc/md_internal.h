@@ -113,6 +113,7 @@ struct Scratch {
     int32_t* done_compact; // [1] completion counter of the compaction and recall kernels
     unsigned long long* compact_acc;   // [1] the same for its trusted form: blocks done << 40 | gaps
     unsigned long long* app_word;      // [S] append kernel: each session's new counts, tagged
+    unsigned long long* ev_word;       // [S] select-and-compact kernel: each session's eviction count, tagged
     int32_t* opened;       // [1] pages the recall kernel takes from the free list
     unsigned long long* counters;  // [8] tokens scored, steps, pages evicted, tokens evicted, pages
                                    // offloaded, recalled, dropped from host memory, observed there
@@ -135,7 +136,7 @@ hipError_t static_scratch(void** ptr);
 // or, when 0, every session on the multi-kernel path.  observe: 0 for a
 // decode step without an observation (no work lists, no scored tokens).
 // tag: differs from the previous launch's (27 bits used)
-constexpr uint32_t kAppendTagMask = (1u << 27) - 1;
+constexpr uint32_t kWordTagMask = (1u << 27) - 1;
 hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
                          const uint16_t* new_k, const uint8_t* new_region, int fused, int observe,
                          uint32_t tag, hipStream_t st);
@@ -163,6 +164,8 @@ hipError_t launch_calib(const Dims& dm, const View& v, const Scratch& sc, const 
                         int n_buckets, unsigned long long* mass_fx, unsigned long long* count,
                         unsigned long long* age_sum, hipStream_t st);
 // trusted: the lists are the library's own selection of this step
+hipError_t launch_evict(const Dims& dm, const View& v, const Scratch& sc, int32_t* ev_serial,
+                        int32_t* ev_count, uint8_t* infeasible, uint32_t tag, hipStream_t st);
 hipError_t launch_compact(const Dims& dm, const View& v, const Scratch& sc,
                           const int32_t* ev_serial, const int32_t* ev_count, int trusted, hipStream_t st);
 // Quantised tier, before the compaction of the same eviction lists.

@@ -81,7 +81,7 @@ __device__ bool opens_page(const Dims& dm, const View& v, int s2, const uint8_t*
 // older tag.  (A device-scope fence writes back the L2 of the block's XCD.)
 __device__ __forceinline__ unsigned long long append_word(uint32_t tag, bool bad, bool opened, bool appended,
                                                           int np, int nt) {
-    return ((unsigned long long)(tag & kAppendTagMask) << 37) | ((unsigned long long)bad << 36) |
+    return ((unsigned long long)(tag & kWordTagMask) << 37) | ((unsigned long long)bad << 36) |
            ((unsigned long long)opened << 35) | ((unsigned long long)appended << 34) |
            ((unsigned long long)(np & 0x3FFF) << 20) | (unsigned long long)(nt & 0xFFFFF);
 }
@@ -113,13 +113,16 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     // pages the sessions before this one take at this append), and the last
     // page's table entry right behind them, so the chain to the slot is
     // three round trips to memory rather than six.
-    int t0_clock = 0, np = 0, nt = 0, fc0 = 0, ep0 = 0, last_p = -1;
+    int t0_clock = 0, np = 0, nt = 0, fc0 = 0, ep0 = 0, ns0 = 0, last_p = -1;
+    uint8_t rg_new = 0;
     if (threadIdx.x == 0) {
         t0_clock = v.clock[s];
         np = v.n_pages[s];
         nt = v.n_tokens[s];
         fc0 = v.free_count[0];   // the free count and the epoch change only in the last block
         ep0 = *sc.epoch;
+        ns0 = v.next_serial[s];
+        if (new_k != nullptr) rg_new = new_region[s];
     }
     if (threadIdx.x == 0) sh_rank = 0;
     int rank_mine = 0;
@@ -134,30 +137,23 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     }
     __syncthreads();
     if (threadIdx.x == 0) {
+        // Every load first, then the stores: a wait for a load also waits
+        // for the stores issued before it.
         const int t = t0_clock + 1;
-        v.clock[s] = t;
-        int phys = -1, slot = 0;
+        const size_t row = (size_t)s * dm.MP;
+        int phys = -1, slot = 0, new_p = -1, close_from = -1;
         bool opened = false, appended = false;
         const bool bad = !counters_ok(np, nt, dm);
-        if (new_k != nullptr && counters_ok(np, nt, dm)) {
-            const size_t row = (size_t)s * dm.MP;
+        if (new_k != nullptr && !bad) {
             bool open = !(np > 0 && nt < np * dm.P);
             if (!open) {
-                const int p = last_p;
-                if (p >= 0 && p < dm.NP) {
-                    phys = p;
+                if (last_p >= 0 && last_p < dm.NP) {
+                    phys = last_p;
                     slot = nt - (np - 1) * dm.P;
-                    const size_t s0 = (size_t)p * dm.P;
                     // region-aligned pages: a new region closes the last
                     // page, its unused slots becoming holes
-                    if (dm.aligned && slot > 0 && v.region[s0 + slot - 1] != new_region[s]) {
-                        for (int o = slot; o < dm.P; ++o) {
-                            v.region[s0 + o] = (uint8_t)kHole;
-                            v.t_ins[s0 + o] = 0;
-                            v.t_ref[s0 + o] = 0;
-                            v.imp[s0 + o] = 0.0f;
-                        }
-                        nt = np * dm.P;
+                    if (dm.aligned && slot > 0 && v.region[(size_t)last_p * dm.P + slot - 1] != rg_new) {
+                        close_from = slot;
                         phys = -1;
                         open = true;
                     }
@@ -174,14 +170,8 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                 if (idx >= 0) {
                     const int p = v.free_list[idx];
                     if (p >= 0 && p < dm.NP) {
-                        phys = p;
+                        new_p = phys = p;
                         slot = 0;
-                        v.page_table[row + np] = p;
-                        v.page_serial[row + np] = v.next_serial[s];
-                        if (dm.quant) v.page_format[p] = 0;   // a reused page holds bf16 keys again
-                        v.next_serial[s] += 1;
-                        np += 1;
-                        opened = true;
                     } else {
                         atomicOr(sc.status, kDevCorrupt);
                     }
@@ -191,15 +181,34 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             } else {
                 atomicOr(sc.status, MD_DEV_CAPACITY);
             }
-            if (phys >= 0) {
-                nt += 1;
-                appended = true;
-                const size_t si = (size_t)phys * dm.P + slot;
-                v.region[si] = new_region[s];
-                v.t_ins[si] = t;
-                v.t_ref[si] = t;
-                v.imp[si] = 0.0f;
+        }
+        v.clock[s] = t;
+        if (close_from >= 0) {
+            const size_t s0 = (size_t)last_p * dm.P;
+            for (int o = close_from; o < dm.P; ++o) {
+                v.region[s0 + o] = (uint8_t)kHole;
+                v.t_ins[s0 + o] = 0;
+                v.t_ref[s0 + o] = 0;
+                v.imp[s0 + o] = 0.0f;
             }
+            nt = np * dm.P;
+        }
+        if (new_p >= 0) {
+            v.page_table[row + np] = new_p;
+            v.page_serial[row + np] = ns0;
+            if (dm.quant) v.page_format[new_p] = 0;   // a reused page holds bf16 keys again
+            v.next_serial[s] = ns0 + 1;
+            np += 1;
+            opened = true;
+        }
+        if (phys >= 0) {
+            nt += 1;
+            appended = true;
+            const size_t si = (size_t)phys * dm.P + slot;
+            v.region[si] = rg_new;
+            v.t_ins[si] = t;
+            v.t_ref[si] = t;
+            v.imp[si] = 0.0f;
         }
         sh_phys = phys;
         sh_slot = slot;
@@ -235,33 +244,41 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     // returned (the word is computed from them), so no block reads a count
     // the last block has already changed.
     if (s != (int)gridDim.x - 1) return;
-    __shared__ int s_n[kMaxSessions];      // live tokens (0 for a skipped session)
+    __shared__ int s_n[kMaxSessions];      // token slots in use (0 for a skipped session)
+    __shared__ int s_live[kMaxSessions];   // live tokens (with region-aligned pages, holes left out)
     __shared__ int s_pass[kMaxSessions];   // fused pass of the session, -1 on the spill path
     __shared__ int sh_opened;              // pages taken from the free list by this append
     if (threadIdx.x == 0) sh_opened = 0;
     __syncthreads();
     int opened_mine = 0;
     for (int s2 = threadIdx.x; s2 < dm.S; s2 += blockDim.x) {
+        // loads before the stores (a wait for a load also waits for them)
+        const int live0 = dm.aligned ? v.n_live[s2] : 0;
         unsigned long long wd = __hip_atomic_load(sc.app_word + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-        bool stale = (uint32_t)(wd >> 37) != (tag & kAppendTagMask);
+        bool stale = (uint32_t)(wd >> 37) != (tag & kWordTagMask);
         while (stale && __builtin_amdgcn_s_memrealtime() - t0 < 100000ull) {   // 1 ms
             __builtin_amdgcn_s_sleep(2);
             wd = __hip_atomic_load(sc.app_word + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            stale = (uint32_t)(wd >> 37) != (tag & kAppendTagMask);
+            stale = (uint32_t)(wd >> 37) != (tag & kWordTagMask);
         }
         const int np = (int)((wd >> 20) & 0x3FFF), nt = (int)(wd & 0xFFFFF);
         const bool ok = !stale && !((wd >> 36) & 1ull) && counters_ok(np, nt, dm);
+        int live = nt;
         if (ok) {
             v.n_pages[s2] = np;
             v.n_tokens[s2] = nt;
             opened_mine += (int)((wd >> 35) & 1ull);
-            if (dm.aligned && ((wd >> 34) & 1ull)) v.n_live[s2] += 1;
+            if (dm.aligned) {
+                live = live0 + (int)((wd >> 34) & 1ull);
+                v.n_live[s2] = live;
+            }
         } else {
             atomicOr(sc.status, kDevCorrupt);
         }
         sc.valid[s2] = ok ? 1 : 0;
         s_n[s2] = ok ? nt : 0;
+        s_live[s2] = (ok && nt > 0) ? live : 0;
         s_pass[s2] = -1;
     }
     if (opened_mine > 0) atomicAdd(&sh_opened, opened_mine);
@@ -286,29 +303,18 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         }
     }
     __syncthreads();
-    if (threadIdx.x == 0 && fused && s_lane_ok) {
-        // The first pass of each lane, claimed here: lane 0 the longest
-        // prefix of sessions, lane 1 the longest suffix of the rest, each
-        // within one workgroup per CU and at most blockDim.x sessions (what
-        // the kernel's own claims take); the rest stays to be claimed.
-        sc.plan[0] = -1;
-        const int ep = ep0 + 1;
-        *sc.epoch = ep;
-        auto units = [&](int s2) { return (s_n[s2] + dm.T - 1) / dm.T; };
-        int f0 = 0, used = 0;
-        while (f0 < dm.S && f0 < (int)blockDim.x && used + units(f0) <= dm.lane_cap) used += units(f0++);
-        int e1 = dm.S;
-        used = 0;
-        while (e1 > f0 && dm.S - e1 < (int)blockDim.x && used + units(e1 - 1) <= dm.lane_cap) used += units(--e1);
-        const unsigned long long tag = (unsigned long long)(uint32_t)ep << 32;
-        sc.lane_box[0] = tag | ((unsigned long long)0 << 16) | (unsigned long long)f0;
-        sc.lane_box[dm.S + 1] = tag | ((unsigned long long)e1 << 16) | (unsigned long long)dm.S;
-        *sc.claim = ((unsigned long long)(uint32_t)f0 << 32) | (uint32_t)e1;
-    } else if (threadIdx.x == 0 && fused) {
-        // Sessions in order, packed greedily into passes of at most n_wg
-        // units (a session's units wait for each other row by row, so all of
-        // them run in the same pass).  A session larger than a whole pass
-        // takes the spill path.
+    const bool lane_mode = fused && s_lane_ok;
+    __shared__ int sh_f0, sh_e1;
+    if (threadIdx.x == 0) {
+        sh_f0 = min(dm.S, (int)blockDim.x);
+        sh_e1 = max(0, dm.S - (int)blockDim.x);
+    }
+    if (threadIdx.x == 0 && fused && !lane_mode) {
+        // Pass mode: sessions in order, packed greedily into passes of at
+        // most n_wg units (a session's units wait for each other row by row,
+        // so all of them run in the same pass).  A session larger than a
+        // whole pass takes the spill path.  (The lane plan follows the work
+        // lists below.)
         for (int s2 = 0; s2 < dm.S; ++s2) s_pass[s2] = -1;
         int np = 0, s0 = 0;
         while (s0 < dm.S) {
@@ -352,7 +358,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             it[k] = ch * dm.LHkv;
             ti[k] = spill ? (nt + kTile - 1) / kTile : 0;
             si[k] = (nt + kTile - 1) / kTile;
-            my_tokens += (dm.aligned && nt > 0) ? v.n_live[s2] : nt;
+            my_tokens += s_live[s2];
         }
         my_units += uu[k];
         my_items += it[k];
@@ -364,6 +370,15 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     block_exclusive_scan_n<5>(mine, lds, ex, tot);
     int ex_u = ex[0], ex_i = ex[1], ex_t = ex[2], ex_s = ex[3];
     const int tot_u = tot[0], tot_i = tot[1], tot_t = tot[2], tot_s = tot[3], tot_n = tot[4];
+    // Lane mode: the first pass of each lane, claimed here: lane 0 the
+    // longest prefix of sessions, lane 1 the longest suffix of the rest, each
+    // within one workgroup per CU (lane_cap units) and at most blockDim.x
+    // sessions (what the kernel's own claims take); the rest stays to be
+    // claimed.  The prefix ends at the first session whose inclusive unit
+    // count exceeds lane_cap, the suffix starts after the last session whose
+    // suffix count does (both counts are monotone), each found by the one
+    // thread that sees the crossing.
+    const int cap = dm.lane_cap;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int s2 = threadIdx.x * 4 + k;
@@ -372,13 +387,29 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             sc.item_prefix[s2] = ex_i;
             sc.tile_prefix[s2] = ex_t;
             sc.score_prefix[s2] = ex_s;
+            if (lane_mode) {
+                const int incl = ex_u + uu[k];
+                if (s2 < (int)blockDim.x && ex_u <= cap && cap < incl) atomicMin(&sh_f0, s2);
+                if (tot_u - ex_u > cap && tot_u - incl <= cap) atomicMax(&sh_e1, s2 + 1);
+            }
         }
         ex_u += uu[k];
         ex_i += it[k];
         ex_t += ti[k];
         ex_s += si[k];
     }
+    if (lane_mode) __syncthreads();
     if (threadIdx.x == 0) {
+        if (lane_mode) {
+            const int f0 = sh_f0, e1 = max(sh_e1, f0);
+            const int ep = ep0 + 1;
+            sc.plan[0] = -1;
+            *sc.epoch = ep;
+            const unsigned long long tag = (unsigned long long)(uint32_t)ep << 32;
+            sc.lane_box[0] = tag | ((unsigned long long)0 << 16) | (unsigned long long)f0;
+            sc.lane_box[dm.S + 1] = tag | ((unsigned long long)e1 << 16) | (unsigned long long)dm.S;
+            *sc.claim = ((unsigned long long)(uint32_t)f0 << 32) | (uint32_t)e1;
+        }
         if (tot_u > dm.U_cap) {            // cannot happen for consistent counters
             atomicOr(sc.status, kDevCorrupt);
             sc.plan[0] = 0;
@@ -914,23 +945,33 @@ __device__ int page_tokens(const Dims& dm, const View& v, int phys, int i, int n
 // When the pages holding the smallest key already weigh at least the need
 // (the usual decode step: one token over the budget), T is that key and the
 // radix passes are skipped.
-__global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch sc,
-                                                        int32_t* ev_serial, int32_t* ev_count,
-                                                        uint8_t* infeasible) {
+//
+// Apply: the selection is also carried out by the same block (k_evict, the
+// compaction of k_compact for this step's own selection).  Freed ids go
+// onto the free list in (session, serial) order: each block publishes its
+// count as a 64-bit word tagged with the launch (`tag`) and adds up the
+// words of the sessions before it (a look-back; blocks are dispatched in
+// index order, so every block it waits for has started), bounded in time.
+// The last block (highest index) then knows the total and sets the free
+// count; every block has read the free count before publishing its word
+// (the word is computed from it), so none reads the new value.
+template <bool Apply>
+__device__ __forceinline__ void select_session(const Dims& dm, const View& v, const Scratch& sc,
+                                               int32_t* ev_serial, int32_t* ev_count, uint8_t* infeasible,
+                                               uint32_t tag) {
     const int s = blockIdx.x;
-    __shared__ int lds[17];
+    __shared__ int lds[2 * 17];
     __shared__ uint32_t s_min[16];
     __shared__ int hist[256];
-    __shared__ int sh_digit, sh_before;
+    __shared__ int sh_digit, sh_before, sh_fc, sh_prior, sh_bad;
     const int tid = threadIdx.x;
     const uint32_t kInf = 0x7F800000u;
     const float* ps = sc.pscore + (size_t)s * dm.MP;
-    const int* ser = v.page_serial + (size_t)s * dm.MP;
-    const int* ptab = v.page_table + (size_t)s * dm.MP;
+    int* ser = v.page_serial + (size_t)s * dm.MP;
+    int* ptab = v.page_table + (size_t)s * dm.MP;
     // The runs split the page-table capacity, not the session's pages, so
-    // the scores (and, for region-aligned pages, the table entries) go out
-    // with the counters rather than after them; entries past the session's
-    // pages are read but not used.
+    // the scores, serials and table entries go out with the counters rather
+    // than after them; entries past the session's pages are read but not used.
     const int per = (dm.MP + kSelThreads - 1) / kSelThreads;
     const int i0 = min(dm.MP, tid * per), ie = min(dm.MP, i0 + per);
     float sv[kPerThread];
@@ -942,19 +983,21 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
         if (i0 + k < ie) {
             sv[k] = ps[i0 + k];
             sr[k] = ser[i0 + k];
-            if (dm.aligned) pv[k] = ptab[i0 + k];
+            if (Apply || dm.aligned) pv[k] = ptab[i0 + k];
         }
     }
+    if (Apply && tid == 0) sh_fc = v.free_count[0];
     const int np = v.n_pages[s], nt = v.n_tokens[s], B = v.budget[s];
     const int need = v.n_live[s] - B;
-    if (!sc.valid[s] || need <= 0 || np == 0) {
+    const bool active = sc.valid[s] && need > 0 && np > 0;
+    if (!Apply && !active) {
         if (tid == 0) {
             ev_count[s] = 0;
             infeasible[s] = 0;
         }
         return;
     }
-    const int i1 = min(np, ie);
+    const int i1 = active ? min(np, ie) : i0;
     uint32_t key[kPerThread];
     int wt[kPerThread];
     int wsum = 0;
@@ -971,12 +1014,11 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
             kmin = min(kmin, key[k]);
         }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o));
+    kmin = wave_min_u32(kmin);
     if (lane_id() == 0) s_min[tid >> 6] = kmin;
     int total;
     block_exclusive_scan(wsum, lds, &total);   // its barriers publish s_min too
-    const bool infeas = total < need;
+    const bool infeas = active && total < need;
     for (int w = 0; w < (int)(blockDim.x >> 6); ++w) kmin = min(kmin, s_min[w]);
     // the smallest key's weight, and each thread's share of it before its run
     int teq = 0;
@@ -987,7 +1029,7 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
     int run = block_exclusive_scan(teq, lds, &at_min);
     uint32_t T = kmin;
     int rem = need;
-    if (!infeas && at_min < need) {
+    if (active && !infeas && at_min < need) {
         uint32_t prefix = 0, pmask = 0;
         for (int shift = 24; shift >= 0; shift -= 8) {
             if (tid < 256) hist[tid] = 0;
@@ -1038,7 +1080,7 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
         run = block_exclusive_scan(teq, lds, &dummy);
     }
     bool ev[kPerThread];
-    int my_ev = 0;
+    int my_ev = 0, my_live = 0;
 #pragma unroll
     for (int k = 0; k < kPerThread; ++k) {
         bool e = false;
@@ -1054,9 +1096,15 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
         }
         ev[k] = e;
         my_ev += e ? 1 : 0;
+        my_live += e ? wt[k] : 0;
     }
-    int n_ev;
-    int pos = block_exclusive_scan(my_ev, lds, &n_ev);
+    int ex[2], tot[2];
+    {
+        const int m[2] = {my_ev, my_live};
+        block_exclusive_scan_n<2>(m, lds, ex, tot);
+    }
+    const int n_ev = tot[0];
+    int pos = ex[0];
     int32_t* out = ev_serial + (size_t)s * dm.MP;
 #pragma unroll
     for (int k = 0; k < kPerThread; ++k)
@@ -1066,12 +1114,108 @@ __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch
         infeasible[s] = infeas ? 1 : 0;
         if (infeas) atomicOr(sc.warn, 1);
     }
+    if (!Apply) return;
+
+    // ---- the compaction of this session, and the free list
+    const int fc = sh_fc;   // read by thread 0 before the barriers of the scans
+    const int last = (int)gridDim.x - 1;
+    if (tid == 0) {
+        sh_prior = 0;
+        sh_bad = 0;
+        __hip_atomic_store(sc.ev_word + s,
+                           ((unsigned long long)(tag & kWordTagMask) << 32) |
+                               ((unsigned long long)(fc < 0 ? 1 : 0) << 31) | (unsigned long long)n_ev,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    // look-back: the counts of the sessions before this one (all of them for
+    // the last block)
+    int prior = 0, bad = 0;
+    for (int s2 = tid; s2 < s; s2 += blockDim.x) {
+        unsigned long long wd = __hip_atomic_load(sc.ev_word + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        bool stale = (uint32_t)(wd >> 32) != (tag & kWordTagMask);
+        while (stale && __builtin_amdgcn_s_memrealtime() - t0 < 100000ull) {   // 1 ms
+            __builtin_amdgcn_s_sleep(1);
+            wd = __hip_atomic_load(sc.ev_word + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            stale = (uint32_t)(wd >> 32) != (tag & kWordTagMask);
+        }
+        if (stale || ((wd >> 31) & 1ull)) bad = 1;
+        prior += (int)(wd & 0x7FFFFFFFull);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        prior += __shfl_xor(prior, o);
+        bad |= __shfl_xor(bad, o);
+    }
+    if (lane_id() == 0 && prior > 0) atomicAdd(&sh_prior, prior);
+    if (lane_id() == 0 && bad) sh_bad = 1;
+    __syncthreads();
+    const bool ok = !sh_bad && fc >= 0;
+    const int base = fc + sh_prior;
+    if (tid == 0) {
+        if (!ok) atomicOr(sc.status, kDevCorrupt);
+        else if (base + n_ev > dm.NP) atomicOr(sc.status, kDevCorrupt);
+        sc.freed[s] = n_ev;
+    }
+    if (n_ev > 0) {
+        // kept pages move down in order; the evicted ones' ids go onto the
+        // free list at the session's places.  Every table entry was read
+        // before the scans' barriers.
+        int kpos = min(i0, np) - ex[0], gpos = ex[0];
+#pragma unroll
+        for (int k = 0; k < kPerThread; ++k) {
+            if (i0 + k < i1) {
+                if (!ev[k]) {
+                    ptab[kpos] = pv[k];
+                    ser[kpos] = sr[k];
+                    ++kpos;
+                } else {
+                    if (ok && base + gpos >= 0 && base + gpos < dm.NP) v.free_list[base + gpos] = pv[k];
+                    ++gpos;
+                }
+            }
+        }
+        // the thread owning the last page knows whether it survived; all
+        // pages but the last are full
+        if (i1 == np && i1 > i0) {
+            const int k_last = np - 1 - i0;
+            bool last_kept = false;
+#pragma unroll
+            for (int k = 0; k < kPerThread; ++k)
+                if (k == k_last) last_kept = !ev[k];
+            const int kept = np - n_ev;
+            v.n_pages[s] = kept;
+            v.n_tokens[s] = last_kept ? nt - n_ev * dm.P : kept * dm.P;
+            if (dm.aligned) v.n_live[s] -= tot[1];
+            atomicAdd(&sc.counters[2], (unsigned long long)n_ev);
+            atomicAdd(&sc.counters[3], (unsigned long long)tot[1]);
+        }
+    }
+    if (s == last && tid == 0 && ok) v.free_count[0] = min(base + n_ev, dm.NP);
+}
+
+__global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch sc, int32_t* ev_serial,
+                                                        int32_t* ev_count, uint8_t* infeasible) {
+    select_session<false>(dm, v, sc, ev_serial, ev_count, infeasible, 0);
+}
+
+__global__ void __launch_bounds__(kSelThreads) k_evict(Dims dm, View v, Scratch sc, int32_t* ev_serial,
+                                                       int32_t* ev_count, uint8_t* infeasible, uint32_t tag) {
+    select_session<true>(dm, v, sc, ev_serial, ev_count, infeasible, tag);
 }
 
 hipError_t launch_select(const Dims& dm, const View& v, const Scratch& sc, int32_t* ev_serial,
                          int32_t* ev_count, uint8_t* infeasible, hipStream_t st) {
     hipLaunchKernelGGL(k_select, dim3(dm.S), dim3(kSelThreads), 0, st, dm, v, sc, ev_serial,
                        ev_count, infeasible);
+    return hipGetLastError();
+}
+
+hipError_t launch_evict(const Dims& dm, const View& v, const Scratch& sc, int32_t* ev_serial,
+                        int32_t* ev_count, uint8_t* infeasible, uint32_t tag, hipStream_t st) {
+    hipLaunchKernelGGL(k_evict, dim3(dm.S), dim3(kSelThreads), 0, st, dm, v, sc, ev_serial,
+                       ev_count, infeasible, tag);
     return hipGetLastError();
 }
 
@@ -1460,11 +1604,11 @@ size_t scratch_bytes(const Dims& dm) {
     n += align256((1 + (size_t)kAttendPerCu * (dm.S + 1)) * sizeof(unsigned long long));
     n += align256((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long));
     n += align256((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long));
-    n += align256(5 * sizeof(int32_t));
+    n += align256(4 * sizeof(int32_t));
     n += align256(9 * sizeof(unsigned long long));
+    n += 2 * align256((size_t)dm.S * sizeof(unsigned long long));
     n += align256((size_t)dm.S * dm.H * sizeof(int32_t));
     n += align256((size_t)(dm.S + 1) * sizeof(int32_t));
-    n += align256((size_t)dm.S * sizeof(unsigned long long));
     return n;
 }
 
@@ -1504,6 +1648,7 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
     sc->counters = reinterpret_cast<unsigned long long*>(take(9 * sizeof(unsigned long long)));
     sc->compact_acc = sc->counters + 8;
     sc->app_word = reinterpret_cast<unsigned long long*>(take((size_t)dm.S * sizeof(unsigned long long)));
+    sc->ev_word = reinterpret_cast<unsigned long long*>(take((size_t)dm.S * sizeof(unsigned long long)));
     sc->recall = reinterpret_cast<int32_t*>(take((size_t)dm.S * dm.H * sizeof(int32_t)));
     sc->rcount = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
 }

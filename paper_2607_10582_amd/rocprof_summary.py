@@ -31,11 +31,17 @@ from collections import defaultdict
 PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 KERNEL_SOURCES = {"k_attend": "md_attend.hip", "k_logits": "md_kernels.hip"}
+HEADERS = ("md_internal.h", "md_device.h")   # included by both sources
 
 
 def source_hash(kernel: str) -> str:
-    with open(os.path.join(CSRC, KERNEL_SOURCES[kernel]), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the kernel's source file and the headers it includes: a
+    counter profile holds for the code it was taken on."""
+    h = hashlib.sha256()
+    for name in (KERNEL_SOURCES[kernel],) + HEADERS:
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def short_name(name: str) -> str:

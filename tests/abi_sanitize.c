@@ -219,6 +219,7 @@ static void handle_cases(void) {
     EXPECT(md_score_pages(NULL, NULL, NULL), MD_E_INVALID);
     EXPECT(md_select_evict(NULL, i32, i32, u8), MD_E_INVALID);
     EXPECT(md_compact(NULL, NULL, NULL), MD_E_INVALID);
+    EXPECT(md_select_compact(NULL, i32, i32, u8), MD_E_INVALID);
     EXPECT(md_read_device_status(NULL, i32), MD_E_INVALID);
     EXPECT(md_profile_enable(NULL, 1u), MD_E_INVALID);
     EXPECT(md_profile_read(NULL, 0, &ms, i64), MD_E_INVALID);

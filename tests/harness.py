@@ -106,7 +106,7 @@ class Pair:
                  steps=None, fused: Optional[bool] = True, priors=None, strict_ties: bool = False,
                  check_free_list: bool = False, static: bool = False, pool: int = 0,
                  offload_pages: int = 0, drop_threshold: float = 0.0, cooperative: bool = False,
-                 explicit_lists: bool = False):
+                 explicit_lists: bool = False, select_compact: bool = False):
         # pool > 0: the oracle sessions run in that many worker processes
         # (oracle.pool), all sessions of a step at once
         self.w = w
@@ -124,6 +124,11 @@ class Pair:
         # explicit_lists: md_compact always gets the lists (else without them
         # whenever the device's selection is the oracle's)
         self.explicit_lists = explicit_lists
+        # select_compact: the selection and its application as one call
+        # (md_select_compact); the device's selection must then equal the
+        # oracle's at every step, since it is applied before the comparison
+        self.select_compact = select_compact
+        assert not (select_compact and explicit_lists)
         self.pinned_mask = w.pinned_mask if pinned_mask is None else pinned_mask
         self.alpha = w.alpha if alpha is None else alpha
         self.oracle_sessions = list(range(S)) if oracle_sessions is None else list(oracle_sessions)
@@ -249,16 +254,30 @@ class Pair:
             torch.cuda.synchronize(self.dev)
             self.check_pops(before, self.free_list_state())
         md.score(token_score=self.tscore)
-        md.select()
+        c = self.cache
+
+        def snapshot():
+            h = {name: getattr(c, name).cpu().numpy() for name in
+                 ("page_table", "page_serial", "n_pages", "n_tokens", "importance", "t_ref", "region")}
+            h["n_live"] = self.live_counts()
+            return h
+
+        if self.select_compact:
+            # the tables as the selection sees them, then both in one call
+            torch.cuda.synchronize(self.dev)
+            host = snapshot()
+            if self.check_free_list:
+                pre_compact = self.free_list_state()
+            md.select_compact()
+        else:
+            md.select()
         torch.cuda.synchronize(self.dev)
         rc, dev_status = md.device_status(with_warning=True)
         self.warned |= rc == B.MD_W_BUDGET_INFEASIBLE
         self.status_seen |= dev_status
         assert dev_status == 0, f"step {k}: device status {dev_status:#x}"
-        c = self.cache
-        host = {name: getattr(c, name).cpu().numpy() for name in
-                ("page_table", "page_serial", "n_pages", "n_tokens", "importance", "t_ref", "region")}
-        host["n_live"] = self.live_counts()
+        if not self.select_compact:
+            host = snapshot()
         abar = self.abar.cpu().numpy()
         tsc = self.tscore.cpu().numpy()
         psc = md.page_score.cpu().numpy()
@@ -350,9 +369,13 @@ class Pair:
         for slots_, vals in tref_fix:
             c.t_ref.view(-1)[torch.from_numpy(slots_).to(self.dev)] = \
                 torch.from_numpy(vals.astype(np.int32)).to(self.dev)
-        if self.check_free_list:
+        if self.select_compact:
+            assert same_selection, (k, "the one-call form applied a selection other than the oracle's")
+        elif self.check_free_list:
             pre_compact = self.free_list_state()
-        if same_selection and not self.explicit_lists:
+        if self.select_compact:
+            pass   # applied already
+        elif same_selection and not self.explicit_lists:
             # the device's own selection: md_compact without lists (the path
             # a caller takes)
             md.compact()

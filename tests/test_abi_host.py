@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert B.md_abi_version() == 8
+    assert B.md_abi_version() == 9
     for st in (0, -1, -2, -3, -4, -5, -6):
         assert B.md_status_str(st)
     assert B.md_status_str(12345) == "unknown status"
@@ -184,6 +184,7 @@ def test_calls_reject_a_null_handle(lib):
     assert L.md_score_pages(None, None, None) == B.MD_E_INVALID
     assert L.md_select_evict(None, 0x1000, 0x1000, 0x1000) == B.MD_E_INVALID
     assert L.md_compact(None, 0x1000, 0x1000) == B.MD_E_INVALID
+    assert L.md_select_compact(None, 0x1000, 0x1000, 0x1000) == B.MD_E_INVALID
     assert L.md_destroy(None) == B.MD_E_INVALID
     out = ctypes.c_int32()
     assert L.md_read_device_status(None, ctypes.byref(out)) == B.MD_E_INVALID

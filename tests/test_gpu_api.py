@@ -82,8 +82,9 @@ def test_nonfinite_query_sets_status():
     p.close()
 
 
+@pytest.mark.parametrize("one_call", [False, True])
 @pytest.mark.parametrize("fused", [True, False])
-def test_nonfinite_query_voids_the_sessions_step(fused):
+def test_nonfinite_query_voids_the_sessions_step(fused, one_call):
     # Two sessions of 450 tokens with a budget of 225: the first observation
     # would evict about half of each.  Session 0's query holds a NaN: its step
     # is void (nothing selected, compacted or quantised; importance and
@@ -100,8 +101,11 @@ def test_nonfinite_query_voids_the_sessions_step(fused):
     q[0, 0, 0, 3, 17] = float("nan")
     p.md.observe(1, q, nk, reg)
     p.md.score()
-    p.md.select()
-    p.md.compact()
+    if one_call:
+        p.md.select_compact()
+    else:
+        p.md.select()
+        p.md.compact()
     torch.cuda.synchronize()
     assert p.md.device_status() == B.MD_DEV_NONFINITE
     cnt = p.md.evict_count.cpu().tolist()
@@ -114,11 +118,44 @@ def test_nonfinite_query_voids_the_sessions_step(fused):
     q, nk, reg, *_ = p.inputs(2)
     p.md.observe(2, q, nk, reg)
     p.md.score()
-    p.md.select()
-    p.md.compact()
+    if one_call:
+        p.md.select_compact()
+    else:
+        p.md.select()
+        p.md.compact()
     torch.cuda.synchronize()
     assert p.md.device_status() == 0
     assert p.md.evict_count.cpu().tolist()[0] > 0 and int(c.n_tokens[0]) <= 225
+    p.close()
+
+
+def test_select_compact_order_of_calls():
+    # md_select_compact needs md_score_pages since the observation, and
+    # applies the selection: md_compact without lists then has nothing to
+    # apply.  Its launch is timed under its own kernel id.
+    p = small_pair(oracle_sessions=[], n0s=[450], budgets=[225])
+    md = p.md
+    md.profile(("evict",))
+    q, nk, reg, *_ = p.inputs(1)
+    md.observe(1, q, nk, reg)
+    with pytest.raises(B.MemDecayError) as e:
+        md.select_compact()
+    assert e.value.status == B.MD_E_STATE
+    md.score()
+    md.select_compact()
+    with pytest.raises(B.MemDecayError) as e:
+        md.compact()
+    assert e.value.status == B.MD_E_STATE
+    with pytest.raises(B.MemDecayError) as e:
+        md.select_compact()
+    assert e.value.status == B.MD_E_STATE
+    torch.cuda.synchronize()
+    cnt = int(md.evict_count[0])
+    assert cnt > 0 and 225 - 16 < int(p.cache.n_tokens[0]) <= 225
+    assert int(p.cache.n_pages[0]) == 29 - cnt           # 451 tokens in 29 pages before
+    ms, launches = md.profile_read("evict")
+    assert launches == 1 and ms > 0
+    assert md.device_status() == 0
     p.close()
 
 

@@ -556,6 +556,62 @@ def test_free_list_order(fused, explicit):
     run_pair(p, 24, f"free-list-order-fused{int(fused)}-explicit{int(explicit)}")
 
 
+# ---------------------------------------------------------------- one-call selection and compaction
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_select_compact_free_list_order(fused):
+    # md_select_compact (one launch: each session's block selects and
+    # compacts, the blocks find their free-list places by a look-back over
+    # tagged counts): the same pops and (session, serial) pushes as the two
+    # calls, and the oracle's selection at every step
+    w = C.with_overrides(C.get("qwen3_32x1700"), L=2, S=12, steps=24)
+    p = Pair(w, oracle_sessions=[0, 7], check_free_list=True, fused=fused, select_compact=True)
+    run_pair(p, 24, f"select-compact-free-list-fused{int(fused)}")
+
+
+@pytest.mark.parametrize("P", [16, 64])
+def test_select_compact_exact_ties(P):
+    # the exact-tie batch (every unpinned page scores 0.5; more pages than
+    # the block's threads), selected and compacted in one launch
+    w = C.with_overrides(C.get("small"), S=3, n0=None, n0_range=(1, 2), P=P, system_len=64,
+                         mean_span=512.0, steps=6, append_cycle=C.APPEND_CYCLE)
+    b, lam = flat_priors(w, {r: 0.5 for r in range(1, 7)} | {0: 1.0})
+    p = Pair(w, n0s=[20000, 17001, 3000], budgets=[10000, 4000, 2999], priors=(b, lam), alpha=0.0,
+             strict_ties=True, check_free_list=True, select_compact=True)
+    st = run_pair(p, 6, f"select-compact-exact-ties-P{P}")
+    assert st.evicted_pages > 500 // (P // 16) and st.tie_excused == 0
+
+
+def test_select_compact_region_aligned_and_infeasible():
+    # region-aligned pages (live counts from the region codes) with exact
+    # ties, and a session whose pinned tokens exceed its budget
+    w = C.with_overrides(C.get("small"), S=3, n0=None, n0_range=(1, 2), system_len=64, mean_span=300.0,
+                         steps=6, append_cycle=C.APPEND_CYCLE, region_aligned=True, append_run=2)
+    b, lam = flat_priors(w, {0: 1.0, 1: 0.25, 2: 0.5, 3: 0.25, 4: 0.5, 5: 0.25, 6: 0.5})
+    p = Pair(w, n0s=[18000, 9000, 500], budgets=[5000, 4500, 32], priors=(b, lam), alpha=0.0,
+             strict_ties=True, check_free_list=True, select_compact=True)
+    st = run_pair(p, 6, "select-compact-aligned")
+    assert st.evicted_pages > 500 and st.tie_excused == 0 and p.warned
+
+
+def test_select_compact_with_the_quantised_tier():
+    # with a tier the call makes the two calls' launches (the tier runs
+    # between the selection and the compaction)
+    w = C.with_overrides(C.get("small"), quant_threshold=0.35, steps=12)
+    p = Pair(w, select_compact=True)
+    run_pair(p, 12, "select-compact-quant")
+
+
+def test_select_compact_long32k_sampled_sessions():
+    # the 32k batch as the benchmark runs it (fused observation, one-call
+    # selection and compaction): the bulk eviction, then steady steps
+    w = C.with_overrides(C.get("long32k"), steps=20)
+    p = Pair(w, backend="torch", oracle_sessions=[0, 11], fused=None, check_free_list=True,
+             select_compact=True)
+    st = run_pair(p, 20, "select-compact-long32k")
+    assert st.evicted_pages > 2 * (32768 - 8192) // 16
+
+
 def test_physical_pages_are_reproducible():
     # Two runs of the same batch hand out the same physical pages.
     w = C.with_overrides(C.get("qwen3_32x1700"), L=2, S=10, steps=20)
