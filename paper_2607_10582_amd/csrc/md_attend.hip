@@ -717,43 +717,62 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         if (threadIdx.x == 0) a.valid[un.s] = 0;
         return;
     }
+    // Every load first, then the stores: a wait for a load also waits for
+    // the stores issued before it.  The session's region priors are read
+    // once per wave (lane r holds region r's) and picked by shuffles.
     const int t_now = a.clock[un.s];
     const size_t rbase = (size_t)un.s * dm.n_regions;
+    const float b_l = lane < dm.n_regions ? a.b[rbase + lane] : 0.0f;
+    const float lam_l = lane < dm.n_regions ? a.lam[rbase + lane] : 0.0f;
     const int n_tok = AL ? un.nl_s : un.nt_s;   // |K_t|
     const float aw = attention_weight(dm.alpha, dm.norm_attn, n_tok);
+    bool live[kTok];
+    size_t si[kTok];
+    float a_old[kTok];
+    int tr_old[kTok], reg[kTok];
 #pragma unroll
     for (int k = 0; k < kTok; ++k) {
         const int lt = lane + 64 * k;   // wave-local token
         const int tile = lt >> 4;
         const int slot0 = __shfl(myslot, tile);
         // holes hold no token
-        const bool live = wtok0 + lt < un.ntok && ((vmask >> tile) & 1ull) &&
-                          (!AL || (lt & 15) < (int)((lims >> (8 * tile)) & 0xffu));
+        live[k] = wtok0 + lt < un.ntok && ((vmask >> tile) & 1ull) &&
+                  (!AL || (lt & 15) < (int)((lims >> (8 * tile)) & 0xffu));
+        si[k] = (size_t)slot0 + (lt & 15);
+        a_old[k] = 0.0f;
+        tr_old[k] = reg[k] = 0;
+        if (live[k]) {
+            a_old[k] = a.imp[si[k]];
+            tr_old[k] = a.t_ref[si[k]];
+            reg[k] = a.region[si[k]];
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < kTok; ++k) {
+        const int lt = lane + 64 * k;
+        int r = reg[k];
+        if (live[k] && r >= dm.n_regions) {
+            atomicOr(a.status, kDevCorrupt);
+            r = dm.n_regions - 1;
+        }
+        const float br = __shfl(b_l, r), lamr = __shfl(lam_l, r);
         float sc = 0.0f;
         bool pin = false;
-        if (live) {
+        if (live[k]) {
             const float abar = acc[k] / (float)dm.R;
-            const size_t si = (size_t)slot0 + (lt & 15);
-            const float an = fmaf(dm.rho, a.imp[si], (1.0f - dm.rho) * abar);
-            a.imp[si] = an;
-            int tr;
+            const float an = fmaf(dm.rho, a_old[k], (1.0f - dm.rho) * abar);
+            a.imp[si[k]] = an;
+            int tr = tr_old[k];
             if (abar >= dm.tau_scale / (float)n_tok) {
                 tr = t_now;
-                a.t_ref[si] = tr;
-            } else {
-                tr = a.t_ref[si];
+                a.t_ref[si[k]] = tr;
             }
-            if (a.abar_out != nullptr) a.abar_out[si] = abar;
-            int r = a.region[si];
-            if (r >= dm.n_regions) {
-                atomicOr(a.status, kDevCorrupt);
-                r = dm.n_regions - 1;
-            }
+            if (a.abar_out != nullptr) a.abar_out[si[k]] = abar;
             pin = (dm.pin_mask >> r) & 1u;
-            sc = pin ? INFINITY : retention_score(a.b[rbase + r], a.lam[rbase + r], t_now, tr, aw, an);
+            sc = pin ? INFINITY : retention_score(br, lamr, t_now, tr, aw, an);
         }
         float ps;
-        const bool has = page_score_of(sc, live, pin, dm.P, &ps);
+        const bool has = page_score_of(sc, live[k], pin, dm.P, &ps);
         const int tok = un.j * kT + wtok0 + lt;
         if ((lt & (dm.P - 1)) == 0 && has) a.pscore[(size_t)un.s * dm.MP + (tok >> dm.Pshift)] = ps;
     }

@@ -162,14 +162,13 @@ __device__ __forceinline__ bool page_score_of(float score, bool live, bool pinne
 }
 
 // Eight FP8 E4M3 key codes (bytes 8 half .. 8 half + 7 of v) as eight bf16
-// values in the MFMA operand order.  The hardware widens two codes at a time
-// to float32 (exactly); E4M3 values have four significant bits, so their
-// bf16 halves are exact too, and the product with the query stays exact.
+// values in the MFMA operand order.  One instruction widens two codes to a
+// pair of bf16 values (scale 1): E4M3 values have four significant bits and
+// exponents inside bf16's range, so the conversion is exact, and the
+// product with the query stays exact.
 template <bool HIGH>
 __device__ __forceinline__ uint32_t codes_pair_to_bf16(uint32_t x) {
-    typedef float f32x2 __attribute__((ext_vector_type(2)));
-    const f32x2 f = __builtin_amdgcn_cvt_pk_f32_fp8((int)x, HIGH);
-    return (__float_as_uint(f[0]) >> 16) | (__float_as_uint(f[1]) & 0xffff0000u);
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x, 1.0f, HIGH));
 }
 template <int HALF>
 __device__ __forceinline__ u32x4 codes_to_bf16(u32x4 v) {
