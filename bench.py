@@ -37,6 +37,7 @@ the host's cores, on a sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -469,6 +470,10 @@ def main():
                                offload_pages=args.offload_pages, drop_threshold=args.drop_threshold)
     subs = {}
     for name in also:
+        # each workload starts from device memory as a fresh process has it:
+        # the previous workload's buffers go back to the driver first
+        gc.collect()
+        torch.cuda.empty_cache()
         rec, _, _ = measure(C.get(name), W, K, dev, multi_kernel=args.multi_kernel)
         subs[name] = rec
         log(f"{name}: {rec['value']:.4g} tokens/s, k_{rec['roofline']['kernel'][2:]} "

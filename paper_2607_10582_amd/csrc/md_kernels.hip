@@ -1,6 +1,8 @@
 // gfx950 kernels of the MemDecay observation step.
 //
-// One step over a batch of sessions runs seven kernels on the caller's stream:
+// A step over a batch of sessions runs these kernels on the caller's stream (the
+// fused observation kernel of md_attend.hip replaces k_logits, k_rowstats,
+// k_mass and, for the library's own page scores, k_score):
 //   k_append    one block per session: clock, append into the tail page or a
 //               page popped from the free list, copy of the new key rows; the
 //               last block builds the step's work lists.
@@ -15,6 +17,8 @@
 //   k_select    one block per session: weighted radix select of the pages to
 //               evict (Sec. III-D, Alg. 1).
 //   k_compact   one block per session: page-table compaction, free-list push.
+//   k_evict     k_select and the compaction of its selection in one launch
+//               (md_select_compact without a tier).
 // Every reduction is in a fixed order; no float atomics are used.
 
 #include <mutex>
