@@ -129,23 +129,39 @@ def test_qwen15_single_session_full_run():
     assert st.evicted_pages > 60
 
 
-def test_max_pages_per_session():
-    # 8191 pages of 16 tokens in one session: every select thread holds 8 pages.
+@pytest.mark.parametrize("one_call", [False, True])
+def test_max_pages_per_session(one_call):
+    # 8191 pages of 16 tokens in one session: every select thread holds 8
+    # pages (with md_select_compact, the compaction's threads too).
     w = C.with_overrides(C.get("small"), L=1, n0=131050, steps=4, system_len=1024,
                          mean_span=512.0, budget_frac=0.25)
-    p = Pair(w, max_pages=8192)
+    kw = {}
+    if one_call:
+        # scores exact on both sides (every unpinned page 0.5), so the
+        # device's selection is the oracle's and can be applied at once
+        b, lam = flat_priors(w, {r: 0.5 for r in range(1, 7)} | {0: 1.0})
+        kw = dict(priors=(b, lam), alpha=0.0, strict_ties=True)
+    p = Pair(w, max_pages=8192, select_compact=one_call, check_free_list=one_call, **kw)
     assert p.cache.max_pages == 8192
-    run_pair(p, 4, "max-pages")
+    run_pair(p, 4, f"max-pages-one-call{int(one_call)}")
 
 
-@pytest.mark.parametrize("fused", [True, False])
-def test_max_sessions(fused):
+@pytest.mark.parametrize("fused,one_call", [(True, False), (False, False), (True, True)])
+def test_max_sessions(fused, one_call):
     # 1,024 sessions (the most a handle takes) of 1 to 400 tokens: the work
     # lists, lane claims and passes at their largest; a sample of sessions
-    # checked token by token, among them the first and the last.
+    # checked token by token, among them the first and the last.  With
+    # md_select_compact, 1,024 blocks find their free-list places by the
+    # look-back (more blocks than are resident at once) and the pushes are
+    # checked in (session, serial) order.
     w = C.with_overrides(C.get("small"), S=1024, n0=None, n0_range=(1, 400), steps=4, system_len=30)
-    p = Pair(w, oracle_sessions=[0, 1, 255, 256, 511, 700, 1022, 1023], fused=fused)
-    run_pair(p, 4, f"max-sessions-fused{int(fused)}")
+    kw = {}
+    if one_call:   # exact scores on both sides, as in test_max_pages_per_session
+        b, lam = flat_priors(w, {r: 0.5 for r in range(1, 7)} | {0: 1.0})
+        kw = dict(priors=(b, lam), alpha=0.0, strict_ties=True)
+    p = Pair(w, oracle_sessions=[0, 1, 255, 256, 511, 700, 1022, 1023], fused=fused,
+             select_compact=one_call, check_free_list=one_call, **kw)
+    run_pair(p, 4, f"max-sessions-fused{int(fused)}-one-call{int(one_call)}")
 
 
 def test_long32k_sampled_sessions_multikernel_path():
