@@ -386,7 +386,12 @@ md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* ev
  * it is one launch, each session's block selecting and compacting its own
  * pages; with a tier it enqueues the two calls' launches.  For callers that
  * apply the library's own selection without looking at it in between.
- * Arguments, layout and requirements as for md_select_evict.
+ * Arguments, layout and requirements as for md_select_evict.  In the one
+ * launch each block finds its session's places on the free list from the
+ * counts of the sessions before it, with bounded waits (1 ms); a wait that
+ * runs out, possible only while other work holds the compute units, sets
+ * MD_DEV_CORRUPT, and that session's freed ids (and, if it is the last
+ * block's, the new free count) are not written.
  */
 md_status md_select_compact(md_handle h, int32_t* evict_serial, int32_t* evict_count, uint8_t* infeasible);
 
