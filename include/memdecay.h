@@ -390,8 +390,10 @@ md_status md_compact(md_handle h, const int32_t* evict_serial, const int32_t* ev
  * launch each block finds its session's places on the free list from the
  * counts of the sessions before it, with bounded waits (1 ms); a wait that
  * runs out, possible only while other work holds the compute units, sets
- * MD_DEV_CORRUPT, and that session's freed ids (and, if it is the last
- * block's, the new free count) are not written.
+ * MD_DEV_CORRUPT: that session is left as it was (its lists are still
+ * written), and the free count is then not updated, so no page can be
+ * handed out twice (the pages the other sessions freed are lost to the
+ * free list).
  */
 md_status md_select_compact(md_handle h, int32_t* evict_serial, int32_t* evict_count, uint8_t* infeasible);
 

@@ -114,6 +114,7 @@ struct Scratch {
     unsigned long long* compact_acc;   // [1] the same for its trusted form: blocks done << 40 | gaps
     unsigned long long* app_word;      // [S] append kernel: each session's new counts, tagged
     unsigned long long* ev_word;       // [S] select-and-compact kernel: each session's eviction count, tagged
+    unsigned long long* ev_done;       // [S] the same kernel: whether each block applied its selection, tagged
     int32_t* opened;       // [1] pages the recall kernel takes from the free list
     unsigned long long* counters;  // [8] tokens scored, steps, pages evicted, tokens evicted, pages
                                    // offloaded, recalled, dropped from host memory, observed there

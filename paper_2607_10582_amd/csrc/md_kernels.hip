@@ -956,9 +956,12 @@ __device__ int page_tokens(const Dims& dm, const View& v, int phys, int i, int n
 // count as a 64-bit word tagged with the launch (`tag`) and adds up the
 // words of the sessions before it (a look-back; blocks are dispatched in
 // index order, so every block it waits for has started), bounded in time.
-// The last block (highest index) then knows the total and sets the free
-// count; every block has read the free count before publishing its word
-// (the word is computed from it), so none reads the new value.
+// Each block then tells the last one (highest index) whether it applied its
+// selection; the last block sets the free count only if all did, so a
+// block that gave up waiting (its session left as it was, MD_DEV_CORRUPT)
+// never has unwritten places counted.  Every block has read the free count
+// before publishing its word (the word is computed from it), so none reads
+// the new value.
 template <bool Apply>
 __device__ __forceinline__ void select_session(const Dims& dm, const View& v, const Scratch& sc,
                                                int32_t* ev_serial, int32_t* ev_count, uint8_t* infeasible,
@@ -1155,14 +1158,19 @@ __device__ __forceinline__ void select_session(const Dims& dm, const View& v, co
     if (lane_id() == 0 && prior > 0) atomicAdd(&sh_prior, prior);
     if (lane_id() == 0 && bad) sh_bad = 1;
     __syncthreads();
-    const bool ok = !sh_bad && fc >= 0;
     const int base = fc + sh_prior;
+    const bool ok = !sh_bad && fc >= 0 && base + n_ev <= dm.NP;
+    // Whether this block applies its selection, told to the last block
+    // (which commits the free count only if every block does: a block that
+    // gave up waiting leaves its session as it was and its places unwritten,
+    // and the count must not cover them).
     if (tid == 0) {
+        __hip_atomic_store(sc.ev_done + s, ((unsigned long long)(tag & kWordTagMask) << 32) | (ok ? 1ull : 0ull),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (!ok) atomicOr(sc.status, kDevCorrupt);
-        else if (base + n_ev > dm.NP) atomicOr(sc.status, kDevCorrupt);
-        sc.freed[s] = n_ev;
+        sc.freed[s] = ok ? n_ev : 0;
     }
-    if (n_ev > 0) {
+    if (ok && n_ev > 0) {
         // kept pages move down in order; the evicted ones' ids go onto the
         // free list at the session's places.  Every table entry was read
         // before the scans' barriers.
@@ -1196,7 +1204,26 @@ __device__ __forceinline__ void select_session(const Dims& dm, const View& v, co
             atomicAdd(&sc.counters[3], (unsigned long long)tot[1]);
         }
     }
-    if (s == last && tid == 0 && ok) v.free_count[0] = min(base + n_ev, dm.NP);
+    if (s != last) return;
+    // the last block: every block applied its selection, so the list grew
+    // by the sum of the counts
+    int all_ok = ok ? 1 : 0;
+    for (int s2 = tid; s2 < s; s2 += blockDim.x) {
+        unsigned long long wd = __hip_atomic_load(sc.ev_done + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        bool stale = (uint32_t)(wd >> 32) != (tag & kWordTagMask);
+        while (stale && __builtin_amdgcn_s_memrealtime() - t0 < 100000ull) {   // 1 ms
+            __builtin_amdgcn_s_sleep(1);
+            wd = __hip_atomic_load(sc.ev_done + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            stale = (uint32_t)(wd >> 32) != (tag & kWordTagMask);
+        }
+        if (stale || !(wd & 1ull)) all_ok = 0;
+    }
+    all_ok = __syncthreads_and(all_ok);
+    if (tid == 0) {
+        if (all_ok) v.free_count[0] = base + n_ev;
+        else atomicOr(sc.status, kDevCorrupt);
+    }
 }
 
 __global__ void __launch_bounds__(kSelThreads) k_select(Dims dm, View v, Scratch sc, int32_t* ev_serial,
@@ -1610,7 +1637,7 @@ size_t scratch_bytes(const Dims& dm) {
     n += align256((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long));
     n += align256(4 * sizeof(int32_t));
     n += align256(9 * sizeof(unsigned long long));
-    n += 2 * align256((size_t)dm.S * sizeof(unsigned long long));
+    n += 3 * align256((size_t)dm.S * sizeof(unsigned long long));
     n += align256((size_t)dm.S * dm.H * sizeof(int32_t));
     n += align256((size_t)(dm.S + 1) * sizeof(int32_t));
     return n;
@@ -1653,6 +1680,7 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
     sc->compact_acc = sc->counters + 8;
     sc->app_word = reinterpret_cast<unsigned long long*>(take((size_t)dm.S * sizeof(unsigned long long)));
     sc->ev_word = reinterpret_cast<unsigned long long*>(take((size_t)dm.S * sizeof(unsigned long long)));
+    sc->ev_done = reinterpret_cast<unsigned long long*>(take((size_t)dm.S * sizeof(unsigned long long)));
     sc->recall = reinterpret_cast<int32_t*>(take((size_t)dm.S * dm.H * sizeof(int32_t)));
     sc->rcount = reinterpret_cast<int32_t*>(take((size_t)(dm.S + 1) * sizeof(int32_t)));
 }
