@@ -138,6 +138,9 @@ hipError_t static_scratch(void** ptr);
 // decode step without an observation (no work lists, no scored tokens).
 // tag: differs from the previous launch's (27 bits used)
 constexpr uint32_t kWordTagMask = (1u << 27) - 1;
+// Bound of a wait for another block's tagged word (s_memrealtime ticks of
+// 10 ns): 50 ms, far beyond any scheduling delay of a running kernel.
+constexpr uint64_t kWordWaitTicks = 5000000ull;
 hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
                          const uint16_t* new_k, const uint8_t* new_region, int fused, int observe,
                          uint32_t tag, hipStream_t st);

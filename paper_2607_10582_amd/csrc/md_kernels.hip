@@ -83,11 +83,10 @@ __device__ bool opens_page(const Dims& dm, const View& v, int s2, const uint8_t*
 // for consecutive launches), so the hand-off needs no memory fence: the last
 // block reads the words and waits, bounded, for any that still carries an
 // older tag.  (A device-scope fence writes back the L2 of the block's XCD.)
-__device__ __forceinline__ unsigned long long append_word(uint32_t tag, bool bad, bool opened, bool appended,
-                                                          int np, int nt) {
+__device__ __forceinline__ unsigned long long append_word(uint32_t tag, bool bad, bool appended, int np, int nt) {
     return ((unsigned long long)(tag & kWordTagMask) << 37) | ((unsigned long long)bad << 36) |
-           ((unsigned long long)opened << 35) | ((unsigned long long)appended << 34) |
-           ((unsigned long long)(np & 0x3FFF) << 20) | (unsigned long long)(nt & 0xFFFFF);
+           ((unsigned long long)appended << 34) | ((unsigned long long)(np & 0x3FFF) << 20) |
+           (unsigned long long)(nt & 0xFFFFF);
 }
 
 __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
@@ -117,7 +116,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     // pages the sessions before this one take at this append), and the last
     // page's table entry right behind them, so the chain to the slot is
     // three round trips to memory rather than six.
-    int t0_clock = 0, np = 0, nt = 0, fc0 = 0, ep0 = 0, ns0 = 0, last_p = -1;
+    int t0_clock = 0, np = 0, nt = 0, fc0 = 0, ep0 = 0, ns0 = 0, last_p = -1, wants_page = 0;
     uint8_t rg_new = 0;
     if (threadIdx.x == 0) {
         t0_clock = v.clock[s];
@@ -146,7 +145,8 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         const int t = t0_clock + 1;
         const size_t row = (size_t)s * dm.MP;
         int phys = -1, slot = 0, new_p = -1, close_from = -1;
-        bool opened = false, appended = false;
+        bool appended = false;
+        wants_page = 0;
         const bool bad = !counters_ok(np, nt, dm);
         if (new_k != nullptr && !bad) {
             bool open = !(np > 0 && nt < np * dm.P);
@@ -170,6 +170,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             } else if (np < dm.MP) {
                 // the free list is a stack: this session takes the entry
                 // below the earlier sessions' ones
+                wants_page = 1;
                 const int idx = min(fc0, dm.NP) - 1 - sh_rank;
                 if (idx >= 0) {
                     const int p = v.free_list[idx];
@@ -203,7 +204,6 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             if (dm.quant) v.page_format[new_p] = 0;   // a reused page holds bf16 keys again
             v.next_serial[s] = ns0 + 1;
             np += 1;
-            opened = true;
         }
         if (phys >= 0) {
             nt += 1;
@@ -217,7 +217,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         sh_phys = phys;
         sh_slot = slot;
         // the session's counts after the append, applied by the last block
-        __hip_atomic_store(sc.app_word + s, append_word(tag, bad, opened, appended, np, nt), __ATOMIC_RELAXED,
+        __hip_atomic_store(sc.app_word + s, append_word(tag, bad, appended, np, nt), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
@@ -251,17 +251,14 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     __shared__ int s_n[kMaxSessions];      // token slots in use (0 for a skipped session)
     __shared__ int s_live[kMaxSessions];   // live tokens (with region-aligned pages, holes left out)
     __shared__ int s_pass[kMaxSessions];   // fused pass of the session, -1 on the spill path
-    __shared__ int sh_opened;              // pages taken from the free list by this append
-    if (threadIdx.x == 0) sh_opened = 0;
     __syncthreads();
-    int opened_mine = 0;
     for (int s2 = threadIdx.x; s2 < dm.S; s2 += blockDim.x) {
         // loads before the stores (a wait for a load also waits for them)
         const int live0 = dm.aligned ? v.n_live[s2] : 0;
         unsigned long long wd = __hip_atomic_load(sc.app_word + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
         bool stale = (uint32_t)(wd >> 37) != (tag & kWordTagMask);
-        while (stale && __builtin_amdgcn_s_memrealtime() - t0 < 100000ull) {   // 1 ms
+        while (stale && __builtin_amdgcn_s_memrealtime() - t0 < kWordWaitTicks) {
             __builtin_amdgcn_s_sleep(2);
             wd = __hip_atomic_load(sc.app_word + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             stale = (uint32_t)(wd >> 37) != (tag & kWordTagMask);
@@ -272,7 +269,6 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         if (ok) {
             v.n_pages[s2] = np;
             v.n_tokens[s2] = nt;
-            opened_mine += (int)((wd >> 35) & 1ull);
             if (dm.aligned) {
                 live = live0 + (int)((wd >> 34) & 1ull);
                 v.n_live[s2] = live;
@@ -285,9 +281,13 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         s_live[s2] = (ok && nt > 0) ? live : 0;
         s_pass[s2] = -1;
     }
-    if (opened_mine > 0) atomicAdd(&sh_opened, opened_mine);
     __syncthreads();
-    if (threadIdx.x == 0) v.free_count[0] = max(min(fc0, dm.NP) - sh_opened, 0);
+    // Entries off the free list: one per session that wants a page, as every
+    // block ranked them from the counts before the append (sh_rank counts
+    // the other sessions here), whether or not its word arrived in time; a
+    // session whose word did not keeps its old counts, and its page, if it
+    // took one, is lost to the list rather than handed out twice.
+    if (threadIdx.x == 0) v.free_count[0] = max(min(fc0, dm.NP) - (sh_rank + wants_page), 0);
     // Lane mode when every fused session fits half a lane (one workgroup
     // per CU): each lane then claims whole sessions as it goes (see
     // k_attend), at least two per pass.  A larger session would leave the
@@ -1142,7 +1142,7 @@ __device__ __forceinline__ void select_session(const Dims& dm, const View& v, co
         unsigned long long wd = __hip_atomic_load(sc.ev_word + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
         bool stale = (uint32_t)(wd >> 32) != (tag & kWordTagMask);
-        while (stale && __builtin_amdgcn_s_memrealtime() - t0 < 100000ull) {   // 1 ms
+        while (stale && __builtin_amdgcn_s_memrealtime() - t0 < kWordWaitTicks) {
             __builtin_amdgcn_s_sleep(1);
             wd = __hip_atomic_load(sc.ev_word + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             stale = (uint32_t)(wd >> 32) != (tag & kWordTagMask);
@@ -1212,7 +1212,7 @@ __device__ __forceinline__ void select_session(const Dims& dm, const View& v, co
         unsigned long long wd = __hip_atomic_load(sc.ev_done + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
         bool stale = (uint32_t)(wd >> 32) != (tag & kWordTagMask);
-        while (stale && __builtin_amdgcn_s_memrealtime() - t0 < 100000ull) {   // 1 ms
+        while (stale && __builtin_amdgcn_s_memrealtime() - t0 < kWordWaitTicks) {
             __builtin_amdgcn_s_sleep(1);
             wd = __hip_atomic_load(sc.ev_done + s2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             stale = (uint32_t)(wd >> 32) != (tag & kWordTagMask);
