@@ -64,11 +64,14 @@ def test_qwen3_batch_all_sessions_all_steps():
 
 
 def test_long32k_all_sessions_all_steps():
-    # 16 sessions x 32,768 tokens (1.5B shape), all 128 steps, on the fused
-    # kernel as the benchmark runs it: the bulk eviction at step 1, page
-    # openings every 16 steps, and the late steady state
+    # 16 sessions x 32,768 tokens (1.5B shape), all 128 steps, as the
+    # benchmark runs them (fused kernel, selection and compaction in one
+    # call): the bulk eviction at step 1, page openings every 16 steps, and
+    # the late steady state.  The one call applies the device's selection
+    # at once, so it must equal the oracle's at every step (no tie band is
+    # met on this trajectory).
     w = C.get("long32k")
-    p = Pair(w, backend="torch", pool=WORKERS, fused=None)
+    p = Pair(w, backend="torch", pool=WORKERS, fused=None, select_compact=True)
     cfg = p.md.kernel_config()
     assert cfg["first_fused"] and cfg["steady_fused"] and not cfg["spill"]
     st = run_full(p, w.steps, "long32k-full")
@@ -78,10 +81,11 @@ def test_long32k_all_sessions_all_steps():
 @pytest.mark.parametrize("name", ["ragged_p16", "ragged_p64"])
 def test_ragged_batch_all_sessions_all_steps(name):
     # 64 sessions of U[2,048, 65,536] tokens (3B shape), all 64 steps, on the
-    # fused kernel as the benchmark runs it; sessions below 5,120 tokens have
-    # more pinned tokens than budget (the infeasible path)
+    # fused kernel; sessions below 5,120 tokens have more pinned tokens than
+    # budget (the infeasible path).  Pages of 16 as the benchmark runs them
+    # (selection and compaction in one call), pages of 64 with the two calls.
     w = C.get(name)
-    p = Pair(w, backend="torch", pool=WORKERS, fused=None)
+    p = Pair(w, backend="torch", pool=WORKERS, fused=None, select_compact=name == "ragged_p16")
     cfg = p.md.kernel_config()
     assert cfg["first_fused"] and cfg["steady_fused"]
     st = run_full(p, w.steps, f"{name}-full")
