@@ -251,6 +251,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     __shared__ int s_n[kMaxSessions];      // token slots in use (0 for a skipped session)
     __shared__ int s_live[kMaxSessions];   // live tokens (with region-aligned pages, holes left out)
     __shared__ int s_pass[kMaxSessions];   // fused pass of the session, -1 on the spill path
+    __shared__ int s_pb[kMaxSessions], s_pe[kMaxSessions], s_pl[kMaxSessions];   // pass mode: sessions, units
     __syncthreads();
     for (int s2 = threadIdx.x; s2 < dm.S; s2 += blockDim.x) {
         // loads before the stores (a wait for a load also waits for them)
@@ -319,26 +320,49 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         // so all of them run in the same pass).  A session larger than a
         // whole pass takes the spill path.  (The lane plan follows the work
         // lists below.)
+        // Then neighbouring passes are evened out from the back: greedy
+        // packing can leave the last pass nearly empty (16 sessions of 129
+        // units give five passes of three and one of one), and a pass of few
+        // units streams at a fraction of the bandwidth (a quarter of the grid
+        // reads at about 2.5 TB/s, half of it at about 6.4), so the previous
+        // pass's last sessions move into the next one while that lowers the
+        // larger of the two passes' units.
+        auto units = [&](int s2) { return (s_n[s2] + dm.T - 1) / dm.T; };
         for (int s2 = 0; s2 < dm.S; ++s2) s_pass[s2] = -1;
         int np = 0, s0 = 0;
         while (s0 < dm.S) {
             int used = 0, e = s0;
             while (e < dm.S) {
-                const int u = (s_n[e] + dm.T - 1) / dm.T;
+                const int u = units(e);
                 if (used + u > dm.n_wg) break;
                 used += u;
-                s_pass[e] = np;
                 ++e;
             }
             if (e == s0) {   // too large for any pass
                 ++s0;
                 continue;
             }
-            sc.plan[1 + 3 * np] = dm.T;
-            sc.plan[2 + 3 * np] = s0;
-            sc.plan[3 + 3 * np] = e;
+            s_pb[np] = s0;
+            s_pe[np] = e;
+            s_pl[np] = used;
             ++np;
             s0 = e;
+        }
+        for (int p = np - 1; p >= 1; --p) {
+            while (s_pe[p - 1] == s_pb[p] && s_pe[p - 1] - s_pb[p - 1] > 1) {
+                const int u = units(s_pe[p - 1] - 1);
+                if (s_pl[p] + u > dm.n_wg || s_pl[p] + u >= s_pl[p - 1]) break;
+                s_pl[p - 1] -= u;
+                s_pl[p] += u;
+                s_pe[p - 1] -= 1;
+                s_pb[p] -= 1;
+            }
+        }
+        for (int p = 0; p < np; ++p) {
+            for (int s2 = s_pb[p]; s2 < s_pe[p]; ++s2) s_pass[s2] = p;
+            sc.plan[1 + 3 * p] = dm.T;
+            sc.plan[2 + 3 * p] = s_pb[p];
+            sc.plan[3 + 3 * p] = s_pe[p];
         }
         sc.plan[0] = np;
         *sc.epoch = ep0 + 1;
