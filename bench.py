@@ -70,7 +70,7 @@ def describe(w, n0s) -> str:
             f"budget {int(w.budget_frac * 100)}%, {w.steps} decode steps")
 
 
-def setup(w, steps_total, dev, fused=None, offload_pages=0, drop_threshold=0.0):
+def setup(w, steps_total, dev, fused=None, offload_pages=0, drop_threshold=0.0, row_groups=True):
     import torch
     from paper_2607_10582_amd.cache import MemDecay, PagedCache
     from synth import configs as C
@@ -104,7 +104,8 @@ def setup(w, steps_total, dev, fused=None, offload_pages=0, drop_threshold=0.0):
         return MemDecay(cache, torch.from_numpy(b), torch.from_numpy(lam), rho=w.rho, alpha=w.alpha,
                         tau_scale=w.tau_scale, pinned_mask=w.pinned_mask, fused=fused,
                         region_aligned=w.region_aligned, quant_threshold=w.quant_threshold,
-                        attention_norm=w.attention_norm, window=w.window, drop_threshold=drop_threshold)
+                        attention_norm=w.attention_norm, window=w.window, drop_threshold=drop_threshold,
+                        row_groups=row_groups)
 
     inputs = []
     for k in range(1, steps_total + 1):
@@ -244,7 +245,8 @@ def calibrate_copy(mib: int):
     log(f"copied {n} bytes 5 times")
 
 
-def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0, offload_pages=0, drop_threshold=0.0):
+def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0, offload_pages=0, drop_threshold=0.0,
+            row_groups=True):
     """One trajectory of workload w from a fresh cache: steps 1..W (warm-up;
     step 1 the bulk eviction), W+1..W+K timed, then on to the workload's
     last step.  Returns the record (value, roofline, step times)."""
@@ -254,7 +256,7 @@ def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0, offload_
 
     total = max(w.steps, W + K)
     t_setup = time.perf_counter()
-    n0s, B, cache, md, inputs = setup(w, total, dev, fused=False if multi_kernel else None,
+    n0s, B, cache, md, inputs = setup(w, total, dev, fused=False if multi_kernel else None, row_groups=row_groups,
                                       offload_pages=offload_pages, drop_threshold=drop_threshold)
     log(f"setup {time.perf_counter() - t_setup:.1f} s: {describe(w, n0s)}")
     stream = md.stream
@@ -389,6 +391,10 @@ def measure(w, W: int, K: int, dev, *, multi_kernel=False, calibrate=0, offload_
                                      if calibrate and cal_ev else None),
         "step_algorithmic_gbs": step_bytes / wall / 1e9,
         "step_frac_of_peak": step_bytes / wall / 1e9 / PEAK_HBM_GBS,
+        "observe_path": {"first": "fused" if kcfg["first_fused"] else "multi-kernel",
+                         "first_row_groups": kcfg["first_row_groups"],
+                         "steady": "fused" if kcfg["steady_fused"] else "multi-kernel",
+                         "steady_row_groups": kcfg["steady_row_groups"]},
     }
     if offload_pages > 0:
         # offload tier: pages moved over the host link in the timed steps,
@@ -423,6 +429,10 @@ def main():
     ap.add_argument("--multi-kernel", action="store_true",
                     help="observe on the multi-kernel path (logits in HBM) at every step instead of "
                          "letting the library pick")
+    ap.add_argument("--no-row-groups", action="store_true",
+                    help="keep every fused unit on all (layer, KV head) rows: without row groups, "
+                         "batches whose units fill less than half of the fused grid take the "
+                         "multi-kernel path")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB")
     ap.add_argument("--calibrate", type=int, default=0, metavar="BUCKET_STEPS",
@@ -467,14 +477,16 @@ def main():
         W = 1
 
     main_rec, n0s, B = measure(w, W, K, dev, multi_kernel=args.multi_kernel, calibrate=args.calibrate,
-                               offload_pages=args.offload_pages, drop_threshold=args.drop_threshold)
+                               offload_pages=args.offload_pages, drop_threshold=args.drop_threshold,
+                               row_groups=not args.no_row_groups)
     subs = {}
     for name in also:
         # each workload starts from device memory as a fresh process has it:
         # the previous workload's buffers go back to the driver first
         gc.collect()
         torch.cuda.empty_cache()
-        rec, _, _ = measure(C.get(name), W, K, dev, multi_kernel=args.multi_kernel)
+        rec, _, _ = measure(C.get(name), W, K, dev, multi_kernel=args.multi_kernel,
+                            row_groups=not args.no_row_groups)
         subs[name] = rec
         log(f"{name}: {rec['value']:.4g} tokens/s, k_{rec['roofline']['kernel'][2:]} "
             f"{rec['roofline']['frac']:.3f} of peak")
@@ -502,7 +514,8 @@ def main():
     for key in ("tokens_scored_per_step", "tokens_evicted_per_step", "quantised_tokens_per_step",
                 "pages_evicted", "first_step_ms", "first_step_tokens", "first_step_algorithmic_bytes",
                 "first_step_frac_of_peak", "steady_step_ms_mean", "step_ms_median", "run_mean_ms",
-                "run_steps", "calib_us_per_observation", "step_algorithmic_gbs", "step_frac_of_peak"):
+                "run_steps", "calib_us_per_observation", "step_algorithmic_gbs", "step_frac_of_peak",
+                "observe_path"):
         line[key] = main_rec[key]
     if "offload" in main_rec:
         line["offload"] = main_rec["offload"]

@@ -77,7 +77,7 @@
 extern "C" {
 #endif
 
-#define MD_ABI_VERSION 9
+#define MD_ABI_VERSION 10
 
 typedef int32_t md_status;
 
@@ -150,6 +150,15 @@ enum {
                                 /* the layers in order, so for small caches the */
                                 /* multi-kernel path, parallel over layers, is  */
                                 /* faster                                       */
+#define MD_FLAG_NO_ROW_GROUPS 0x20 /* keep every fused unit on all L Hkv rows. */
+                                /* By default, on plain pages with one query   */
+                                /* per observation, a step whose units would   */
+                                /* fill less than half of the fused kernel's   */
+                                /* grid splits each unit's rows into up to 16  */
+                                /* groups of at least 8 rows, one workgroup    */
+                                /* each, whose partial masses (over disjoint   */
+                                /* rows of Sec. III-C's mean) are added in a   */
+                                /* fixed order; results agree to rounding      */
 
 typedef struct md_config {
     int32_t n_layers;           /* L                                              */
@@ -431,13 +440,14 @@ md_status md_profile_read(md_handle h, int32_t kernel, double* total_ms, int64_t
  * once over the host link per observation). */
 md_status md_read_counters(md_handle h, int64_t* out);
 
-/* How md_init laid out the observation step on this device (out: 6 ints):
+/* How md_init laid out the observation step on this device (out: 8 ints):
  * out[0] 1 when the fused observation kernel is available, out[1] 1 when a
  * session could outgrow one pass of it (those sessions always take the
  * multi-kernel path), out[2] the largest fused unit in tokens, out[3] the
  * fused kernel's workgroups (all resident at once), out[4] 1 when the first
- * md_observe_step runs the fused kernel, out[5] 1 when the later ones do.
- * Host-only, no device work. */
+ * md_observe_step runs the fused kernel, out[5] 1 when the later ones do,
+ * out[6] and out[7] the row groups of their fused units (1: none; see
+ * MD_FLAG_NO_ROW_GROUPS).  Host-only, no device work. */
 md_status md_kernel_config(md_handle h, int32_t* out);
 
 /*

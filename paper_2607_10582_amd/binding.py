@@ -32,6 +32,7 @@ MD_FLAG_FUSED = 0x2
 MD_FLAG_NORM_ATTENTION = 0x4
 MD_FLAG_REGION_ALIGNED = 0x8
 MD_FLAG_COOPERATIVE = 0x10
+MD_FLAG_NO_ROW_GROUPS = 0x20
 MD_REGION_HOLE = 0xFF
 
 EXPORTS = ("md_abi_version", "md_status_str", "md_init", "md_init_static", "md_observe_step",
@@ -270,11 +271,13 @@ def md_read_counters(h: int):
 def md_kernel_config(h: int) -> dict:
     """How md_init laid out the observation step (fused kernel available,
     sessions that may outgrow it, largest fused unit in tokens, fused
-    workgroups, path of the first and of the later observes)."""
-    out = (ctypes.c_int32 * 6)()
+    workgroups, path of the first and of the later observes, and their row
+    groups)."""
+    out = (ctypes.c_int32 * 8)()
     _check("md_kernel_config", load_library().md_kernel_config(h, out))
     return {"fused": bool(out[0]), "spill": bool(out[1]), "unit_max": int(out[2]), "workgroups": int(out[3]),
-            "first_fused": bool(out[4]), "steady_fused": bool(out[5])}
+            "first_fused": bool(out[4]), "steady_fused": bool(out[5]), "first_row_groups": int(out[6]),
+            "steady_row_groups": int(out[7])}
 
 
 def md_destroy(h: int) -> int:

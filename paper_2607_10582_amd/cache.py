@@ -181,11 +181,12 @@ class MemDecay:
                  n_regions: int = 7, stream: Optional[torch.cuda.Stream] = None,
                  fused: Optional[bool] = None, attention_norm: bool = False, window: int = 1,
                  region_aligned: bool = False, quant_threshold: float = 0.0, static: bool = False,
-                 drop_threshold: float = 0.0, cooperative: bool = False):
+                 drop_threshold: float = 0.0, cooperative: bool = False, row_groups: bool = True):
         # fused: True = always the fused kernel, False = always the
         # multi-kernel path, None = the library picks from the cache's sizes;
         # cooperative: the fused kernel as a cooperative launch (for a GPU
-        # shared with other streams)
+        # shared with other streams); row_groups: False keeps every fused
+        # unit on all rows
         self.cache = cache
         dev = cache.device
         self.b = base_priority.to(dev, torch.float32).contiguous()
@@ -198,7 +199,8 @@ class MemDecay:
                           flags=(0 if fused is None else (B.MD_FLAG_FUSED if fused else B.MD_FLAG_NO_FUSED))
                           | (B.MD_FLAG_NORM_ATTENTION if attention_norm else 0)
                           | (B.MD_FLAG_REGION_ALIGNED if region_aligned else 0)
-                          | (B.MD_FLAG_COOPERATIVE if cooperative else 0),
+                          | (B.MD_FLAG_COOPERATIVE if cooperative else 0)
+                          | (0 if row_groups else B.MD_FLAG_NO_ROW_GROUPS),
                           window=window, quant_threshold=quant_threshold,
                           offload_pages=cache.offload_pages, drop_threshold=drop_threshold)
         rp = B.md_region_params(base_priority=self.b.data_ptr(), decay_rate=self.lam.data_ptr())

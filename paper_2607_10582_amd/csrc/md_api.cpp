@@ -40,6 +40,8 @@ struct md_handle_s {
     int32_t last_step;
     bool fused_first;    // the first observe runs the fused kernel
     bool fused_steady;   // later observes run the fused kernel
+    int rg_first;        // row groups of the fused units on the first observe
+    int rg_steady;       // and on later ones (1: every unit walks every row)
     bool fused_last;     // the last observe ran it
     int64_t observed;    // observes enqueued
     Phase phase;
@@ -170,7 +172,7 @@ const char* md_status_str(md_status s) {
 static md_status validate_config(const md_config* c) {
     if (c == nullptr) return MD_E_INVALID;
     if ((c->flags & ~(MD_FLAG_NO_FUSED | MD_FLAG_FUSED | MD_FLAG_NORM_ATTENTION | MD_FLAG_REGION_ALIGNED |
-                      MD_FLAG_COOPERATIVE)) != 0)
+                      MD_FLAG_COOPERATIVE | MD_FLAG_NO_ROW_GROUPS)) != 0)
         return MD_E_INVALID;
     if ((c->flags & MD_FLAG_NO_FUSED) && (c->flags & MD_FLAG_FUSED)) return MD_E_INVALID;
     if (c->offload_pages < 0 || c->offload_pages > md::kMaxOffload) return MD_E_INVALID;
@@ -313,18 +315,28 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     const int n_cu = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
     int occ = 0;
     dm.T = md::attend_unit_tokens(dm.G);
+    // Row groups (plain pages, one query per observation): their own
+    // instantiation, used only if it is as resident as the plain one.
+    bool rows_ok = dm.fused && !dm.aligned && !dm.quant && dm.W == 1 && !(cfg->flags & MD_FLAG_NO_ROW_GROUPS) &&
+                   dm.LHkv >= 2 * md::kMinGroupRows;
     if (dm.fused) {
         const size_t lds = md::attend_lds_bytes(dm.G * dm.W);
-        if (hipFuncSetAttribute(md::attend_kernel(dm.G * dm.W, dm.aligned, dm.quant, dm.W), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)lds) !=
-            hipSuccess) {
-            (void)hipGetLastError();
-        } else if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, md::attend_kernel(dm.G * dm.W, dm.aligned, dm.quant, dm.W),
-                                                                md::attend_threads(dm.G * dm.W),
-                                                                lds) != hipSuccess) {
-            return MD_E_HIP;
-        }
+        auto occupancy = [&](int rg, int* o) {
+            const void* fn = md::attend_kernel(dm.G * dm.W, dm.aligned, dm.quant, dm.W, rg);
+            *o = 0;
+            if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
+                (void)hipGetLastError();
+                return hipSuccess;
+            }
+            return hipOccupancyMaxActiveBlocksPerMultiprocessor(o, fn, md::attend_threads(dm.G * dm.W), lds);
+        };
+        if (occupancy(1, &occ) != hipSuccess) return MD_E_HIP;
         if (occ > md::kAttendPerCu) occ = md::kAttendPerCu;
+        if (rows_ok) {
+            int occ_rg = 0;
+            if (occupancy(2, &occ_rg) != hipSuccess) return MD_E_HIP;
+            rows_ok = occ_rg >= occ;
+        }
         dm.n_wg = occ * n_cu;
         dm.fused = occ >= 1;
     }
@@ -343,13 +355,25 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
         int verified = 0;
         for (int o = occ; o >= 1 && verified == 0; --o) {
             int32_t seen[2] = {0, 0};
-            if (md::launch_attend_check(dm, probe, o * n_cu, hs) != hipSuccess ||
+            if (md::launch_attend_check(dm, probe, o * n_cu, 1, hs) != hipSuccess ||
                 hipMemcpyAsync(seen, probe, sizeof(seen), hipMemcpyDeviceToHost, hs) != hipSuccess ||
                 hipStreamSynchronize(hs) != hipSuccess) {
                 (void)hipGetLastError();
                 continue;
             }
             if (seen[1] >= o * n_cu) verified = o * n_cu;
+        }
+        // the row-group instantiation must hold the same grid
+        if (rows_ok && verified > 0) {
+            int32_t seen[2] = {0, 0};
+            if (md::launch_attend_check(dm, probe, verified, 2, hs) != hipSuccess ||
+                hipMemcpyAsync(seen, probe, sizeof(seen), hipMemcpyDeviceToHost, hs) != hipSuccess ||
+                hipStreamSynchronize(hs) != hipSuccess) {
+                (void)hipGetLastError();
+                rows_ok = false;
+            } else {
+                rows_ok = seen[1] >= verified;
+            }
         }
         if (!use_static) (void)hipFree(probe);
         dm.n_wg = verified;
@@ -367,8 +391,14 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     // from the cache's sizes now (first observe) and with each session at
     // most one token over its budget (later observes, once evictions hold
     // the budget).
+    // Row groups: when a step's units fill less than half of the grid, each
+    // unit covers one of rg ranges of at least kMinGroupRows rows, rg as
+    // large as the grid takes (sessions of the page table's capacity still
+    // fit one pass); the fused kernel then runs for steps whose units, times
+    // rg, fill half the grid.
     bool fused_first = dm.fused, fused_steady = dm.fused;
-    if (dm.fused && !(cfg->flags & MD_FLAG_FUSED)) {
+    int rg_first = 1, rg_steady = 1;
+    if (dm.fused) {
         int32_t hn[md::kMaxSessions], hbud[md::kMaxSessions];
         if (hipMemcpyAsync(hn, cv->n_tokens, dm.S * sizeof(int32_t), hipMemcpyDeviceToHost, hs) != hipSuccess ||
             hipMemcpyAsync(hbud, cv->budget, dm.S * sizeof(int32_t), hipMemcpyDeviceToHost, hs) !=
@@ -382,9 +412,25 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
             first += (n + dm.T - 1) / dm.T;
             steady += (std::min(n, b) + dm.T - 1) / dm.T;
         }
-        fused_first = 2 * first >= dm.n_wg;
-        fused_steady = 2 * steady >= dm.n_wg;
+        const int64_t cap_units = ((int64_t)dm.MP * dm.P + dm.T - 1) / dm.T;
+        const int64_t rg_allow = rows_ok ? std::min<int64_t>({md::kMaxRowGroups, dm.LHkv / md::kMinGroupRows,
+                                                              dm.n_wg / std::max<int64_t>(cap_units, 1)})
+                                         : 1;
+        auto pick = [&](int64_t u) -> int {
+            if (u <= 0 || 2 * u >= dm.n_wg) return 1;
+            return (int)std::max<int64_t>(1, std::min<int64_t>(rg_allow, dm.n_wg / u));
+        };
+        rg_first = pick(first);
+        rg_steady = pick(steady);
+        if (!(cfg->flags & MD_FLAG_FUSED)) {
+            fused_first = 2 * first * rg_first >= dm.n_wg;
+            fused_steady = 2 * steady * rg_steady >= dm.n_wg;
+        }
+        if (!fused_first) rg_first = 1;
+        if (!fused_steady) rg_steady = 1;
     }
+    dm.rg_max = std::max(rg_first, rg_steady);
+    if (dm.fused) dm.U_cap *= dm.rg_max;
     dm.multi = dm.spill || !fused_first || !fused_steady;
 
     const size_t bytes = md::scratch_bytes(dm);
@@ -457,6 +503,8 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     h->last_step = 0;
     h->fused_first = fused_first;
     h->fused_steady = fused_steady;
+    h->rg_first = rg_first;
+    h->rg_steady = rg_steady;
     h->fused_last = false;
     h->observed = 0;
     h->word_tag = 0;
@@ -488,7 +536,7 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     if (q == nullptr) {
         // a decode step without an observation: the append and the clock only
         if (timed_launch(h, MD_K_APPEND, [&] {
-                return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, 0, 0, next_word_tag(h),
+                return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, 0, 0, 1, next_word_tag(h),
                                          h->stream); }) !=
             hipSuccess)
             return MD_E_HIP;
@@ -499,8 +547,9 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
         return MD_OK;
     }
     const bool fused = h->observed == 0 ? h->fused_first : h->fused_steady;
+    const int rg = fused ? (h->observed == 0 ? h->rg_first : h->rg_steady) : 1;
     hipError_t e = timed_launch(h, MD_K_APPEND, [&] {
-        return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, fused ? 1 : 0, 1, next_word_tag(h),
+        return md::launch_append(h->dm, h->v, h->sc, new_k, new_region, fused ? 1 : 0, 1, rg, next_word_tag(h),
                                  h->stream); });
     // On a fused step, sessions that fit one pass of the fused kernel run
     // there; the others (only possible when a session may outgrow n_wg * T
@@ -509,7 +558,7 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
     const bool multi = !fused || h->dm.spill;
     if (e == hipSuccess && fused)
         e = timed_launch_ev(h, MD_K_ATTEND, !h->dm.coop, [&](hipEvent_t t0, hipEvent_t t1) {
-            return md::launch_attend(h->dm, h->v, h->sc, q, abar_out, h->stream, t0, t1); });
+            return md::launch_attend(h->dm, h->v, h->sc, q, abar_out, rg, h->stream, t0, t1); });
     if (e == hipSuccess && multi) e = timed_launch(h, MD_K_LOGITS, [&] {
         return md::launch_logits(h->dm, h->v, h->sc, q, h->logits_blocks, h->stream); });
     if (e == hipSuccess && multi) e = timed_launch(h, MD_K_ROWSTATS, [&] {
@@ -730,6 +779,8 @@ md_status md_kernel_config(md_handle h, int32_t* out) {
     out[3] = h->dm.n_wg;
     out[4] = h->fused_first ? 1 : 0;
     out[5] = h->fused_steady ? 1 : 0;
+    out[6] = h->rg_first;
+    out[7] = h->rg_steady;
     return MD_OK;
 }
 

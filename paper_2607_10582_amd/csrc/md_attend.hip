@@ -57,6 +57,8 @@ struct AttendDims {
     int aligned;
     int Gq, Wn;   // window (WN instantiations): query heads per KV head and window
                   // queries; G above counts the MFMA columns, Gq * Wn
+    int rg;       // row groups (RS instantiations): a unit covers one of rg
+                  // consecutive ranges of the L * Hkv rows; 1 = every row
 };
 
 struct AttendArgs {
@@ -85,6 +87,7 @@ struct AttendArgs {
     const uint8_t* page_format;   // quantised tier: 1 = the page holds E4M3 codes
     const int32_t* t_ins;         // window: insertion steps, for the causal mask
     int32_t* valid;               // [S] cleared for a session whose step is void
+    unsigned long long* upart;    // row groups: [units][T] tagged partial masses
 };
 
 // LDS row stride (floats) of a head's values: W waves of KT tiles
@@ -190,6 +193,10 @@ struct Unit {
     int s, j, ntok, nt_s, nu, us;
     uint64_t deadline;   // real-time tick after which the unit stops waiting
     int nl_s;            // region-aligned pages: the session's tokens |K_t| (nt_s counts holes too)
+    // row groups (RS): the unit covers rows [r0, r1) of group grp of rg; nu,
+    // j and us count the units of that group, ubase is the session's first
+    // unit (group 0)
+    int r0, r1, grp, rg, ubase;
 };
 
 __device__ void claim_sessions(const AttendArgs& a, int* xs, int lane_no, int cap);
@@ -205,10 +212,13 @@ __device__ __forceinline__ int qrow0(const AttendDims& dm, int r) { return r * d
 // decode queries (column c of a row is window query c / Gq, head c % Gq, and
 // a causal mask keeps each query to the tokens inserted by its step);
 // separate instantiations keep the plain kernel's register budget.
+// RS = row groups: the unit walks only its group's rows, and the groups'
+// partial masses meet in the unit of group 0, which alone finishes the
+// tokens (the plain instantiations walk every row).
 // next_box (lane mode, the lane's first workgroup; else NULL): the lane's
 // next pass is claimed with claim_lane and cap once the unit's rows are
 // done, and published there.
-template <int W, int NH, int KT, bool AL, bool QT, bool WN>
+template <int W, int NH, int KT, bool AL, bool QT, bool WN, bool RS>
 __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendArgs& a, const Lds& sm,
                                             const Unit& un, int wv, int lane, uint32_t tag, int claim_lane,
                                             int cap, unsigned long long* next_box) {
@@ -223,6 +233,9 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     constexpr int kTok = KT / 4;          // tokens per lane
     const int wtok0 = wv * 16 * KT;       // unit-local token of this wave's first tile
     bool dead = false;                    // a wait of this wave ran out: stop waiting
+    // the unit's rows [r_beg, r_end)
+    const int r_beg = RS ? un.r0 : 0;
+    const int r_end = RS ? un.r1 : dm.LHkv;
 
     // lane i < KT: slot (physical page * P + offset) of tile i's first token
     int myslot = 0;
@@ -288,7 +301,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // tokens, or past the last row, reads the pool's first tile (its logits
     // are masked), so loads never branch.
     auto load_tile = [&](u32x4 (&rg)[4], int r, int u) {
-        const bool ok = r < dm.LHkv && ((vmask >> u) & 1ull);
+        const bool ok = r < r_end && ((vmask >> u) & 1ull);
         const int slot = __builtin_amdgcn_readlane(myslot, u);
         const size_t e = ok ? ((size_t)(slot >> dm.Pshift) * dm.LHkv + r) * dm.P + (slot & (dm.P - 1)) : 0;
         gbytes base = uni_ptr(a.k_pool + e * kHeadDim);
@@ -359,7 +372,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // (row, query head); the leader of row x (unit x mod nu of the session)
     // gathers them into the row's normaliser words (M, 1 / Lambda), which
     // every unit reads.  Wave wv looks after heads wv + W i (i < NH).
-    const int last = dm.LHkv - 1;
+    const int last = r_end - 1;
     const unsigned long long tag_hi = (unsigned long long)tag << 32;
     auto tag_ok = [&](unsigned long long v) { return (uint32_t)(v >> 32) == tag; };
     auto stat_word = [&](int x, int k, int hd) {
@@ -371,7 +384,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // Rows this unit leads are j, j + nu, j + 2 nu, ...: lead_next is the
     // next one to request, lead_now says whether the previous request was
     // this unit's (both advance once per iteration).
-    int lead_next = un.j;
+    int lead_next = RS ? r_beg + ((un.j - r_beg) % un.nu + un.nu) % un.nu : un.j;
     bool lead_now = false;
     // Re-read until every active lane's words carry the step's tag (bounded).
     auto await_tags = [&](auto&& ready, auto&& reload) {
@@ -534,11 +547,11 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     // in issue order).
     auto use_loads = [&](int r) {   // steps of iteration r that use iteration r - 1's loads
         const int xa = r - 6;
-        if (xa >= 0 && xa <= last && (xa & (W - 1)) == wv) check_norm(xa);
+        if (xa >= r_beg && xa <= last && (xa & (W - 1)) == wv) check_norm(xa);
         if (lead_now) lead(r - 4);
     };
     auto issue_loads = [&](int r) {
-        if (((r - 5) & (W - 1)) == wv) load_norm(min(max(r - 5, 0), last));
+        if (((r - 5) & (W - 1)) == wv) load_norm(min(max(r - 5, r_beg), last));
         const int xd = r - 3;
         lead_now = xd == lead_next && xd <= last;
         if (lead_now) {
@@ -547,27 +560,27 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         }
     };
     auto after_tiles = [&](int r) {   // publish row r - 1, normalise row r - 7
-        if (r >= 1 && r - 1 <= last) publish(r - 1);
+        if (r - 1 >= r_beg && r - 1 <= last) publish(r - 1);
         const int xf = r - kConsumeLag;
-        if (xf >= 0 && xf <= last) consume(xf);
+        if (xf >= r_beg && xf <= last) consume(xf);
     };
 
     // ---- prologue: query row 0 staged; then the loads in the order every
     // iteration issues them: row 0's tiles, the requests and row 1's query,
     // row 1's tiles
-    load_q(0);
-    store_q(0);
+    load_q(r_beg);
+    store_q(r_beg);
     lds_sync();
     // Two rings of four tiles: row r's tiles sit in ring r & 1, and the
     // loads of row r + 2 go out as soon as row r's tiles have been through
     // MFMA, so two rows of loads are in flight while a wave works on a row.
     u32x4 ringA[KT][4], ringB[KT][4];
 #pragma unroll
-    for (int u = 0; u < KT; ++u) load_tile(ringA[u], 0, u);
-    if (((0 - 5) & (W - 1)) == wv) load_norm(0);
-    load_q(min(1, last));
+    for (int u = 0; u < KT; ++u) load_tile(ringA[u], r_beg, u);
+    if (((r_beg - 5) & (W - 1)) == wv) load_norm(r_beg);
+    load_q(min(r_beg + 1, last));
 #pragma unroll
-    for (int u = 0; u < KT; ++u) load_tile(ringB[u], min(1, last + 2), u);
+    for (int u = 0; u < KT; ++u) load_tile(ringB[u], min(r_beg + 1, last + 2), u);
 
     // Row r:
     //   1. logits of the four tiles on MFMA, k-chunk by k-chunk (the chunk's
@@ -630,7 +643,7 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         load_tile(ring[0], row + 2, 0);
         use_loads(row);
         load_tile(ring[1], row + 2, 1);
-        if (row + 1 < dm.LHkv) store_q(row + 1);
+        if (row + 1 < r_end) store_q(row + 1);
         issue_loads(row);
         load_q(min(row + 2, last));
         load_tile(ring[2], row + 2, 2);
@@ -678,12 +691,12 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         if (g == 0 && h < G) sm.wstat[((row & 1) * W + wv) * 16 + h] = make_float2(mx, ls);
         lds_sync();
     };
-    int row = 0;
-    for (; row + 1 < dm.LHkv; row += 2) {
+    int row = r_beg;
+    for (; row + 1 < r_end; row += 2) {
         do_row(ringA, row);
         do_row(ringB, row + 1);
     }
-    if (row < dm.LHkv) do_row(ringA, row);
+    if (row < r_end) do_row(ringA, row);
 
     // ---- lane mode: the lane's next pass, claimed before this unit's
     // drain, so that the lane's other workgroups find it published as they
@@ -699,11 +712,68 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
     }
 
     // ---- iterations without tiles, until the last row is normalised
-    for (int r = dm.LHkv; r < dm.LHkv + kConsumeLag; ++r) {
+    for (int r = r_end; r < r_end + kConsumeLag; ++r) {
         use_loads(r);
         issue_loads(r);
         after_tiles(r);
         lds_sync();
+    }
+
+    // ---- row groups: every group but the first hands its tokens' partial
+    // masses to the unit of group 0 (same tokens) as tagged words, a NaN
+    // payload marking a void step; that unit adds them in group order and
+    // finishes the tokens alone.
+    if constexpr (RS) {
+        if (un.rg > 1) {
+            const bool void_here = *sm.vflag != 0;
+            unsigned long long* pbase = a.upart + (size_t)(un.ubase + un.j) * kT + wtok0 + lane;
+            const size_t gstride = (size_t)un.nu * kT;   // the words of one group's units
+            if (un.grp != 0) {
+#pragma unroll
+                for (int k = 0; k < kTok; ++k)
+                    __hip_atomic_store(pbase + un.grp * gstride + 64 * k,
+                                       tag_hi | (void_here ? 0x7fc00000u : __float_as_uint(acc[k])),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (void_here && threadIdx.x == 0) a.valid[un.s] = 0;
+                return;
+            }
+            if (!void_here) {
+                unsigned long long pw[kMaxRowGroups - 1][kTok];
+                auto load_parts = [&] {
+#pragma unroll
+                    for (int g2 = 1; g2 < kMaxRowGroups; ++g2)
+#pragma unroll
+                        for (int k = 0; k < kTok; ++k)
+                            pw[g2 - 1][k] = g2 < un.rg ? __hip_atomic_load(pbase + g2 * gstride + 64 * k, __ATOMIC_RELAXED,
+                                                                           __HIP_MEMORY_SCOPE_AGENT)
+                                                       : tag_hi;
+                };
+                load_parts();
+                await_tags(
+                    [&] {
+                        bool ok = true;
+#pragma unroll
+                        for (int g2 = 1; g2 < kMaxRowGroups; ++g2)
+#pragma unroll
+                            for (int k = 0; k < kTok; ++k) ok &= tag_ok(pw[g2 - 1][k]);
+                        return ok;
+                    },
+                    load_parts);
+                bool bad = false;
+#pragma unroll
+                for (int g2 = 1; g2 < kMaxRowGroups; ++g2)
+#pragma unroll
+                    for (int k = 0; k < kTok; ++k) {
+                        if (g2 < un.rg) {
+                            const float pv = __uint_as_float((uint32_t)pw[g2 - 1][k]);
+                            bad |= pv != pv;
+                            acc[k] += pv;
+                        }
+                    }
+                if (bad) *sm.vflag = 1;
+            }
+            lds_sync();   // every wave sees the unit's void flag
+        }
     }
 
     // ---- Eq. 2 and Eq. 3 for this wave's tokens, then their retention
@@ -860,7 +930,7 @@ __device__ void claim_sessions(const AttendArgs& a, int* xs, int lane_no, int ca
 // the whole register file.  (Workgroups that take a whole CU, with eight
 // waves or with eight tiles per wave, measured slower: the two workgroups'
 // row barriers fall at different times and fill each other's gaps.)
-template <int W, int NH, int KT, bool AL, bool QT, bool WN>
+template <int W, int NH, int KT, bool AL, bool QT, bool WN, bool RS>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(NH == 4 ? 1 : 2)))
 k_attend(AttendDims dm, AttendArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -955,6 +1025,21 @@ k_attend(AttendDims dm, AttendArgs a) {
         un.us = a.ustart[s];
         un.nu = a.ustart[s + 1] - un.us;
         un.j = u0 + w - un.us;
+        if constexpr (RS) {
+            // the session's units are rg groups of nu / rg units, group g
+            // covering rows [g L Hkv / rg, (g + 1) L Hkv / rg)
+            const int rg = min(max(dm.rg, 1), kMaxRowGroups);
+            const int nut = max(un.nu / rg, 1);
+            if (un.nu != nut * rg && threadIdx.x == 0) atomicOr(a.status, kDevCorrupt);
+            un.rg = rg;
+            un.ubase = un.us;
+            un.grp = min(un.j / nut, rg - 1);
+            un.j -= un.grp * nut;
+            un.nu = nut;
+            un.us += un.grp * nut;
+            un.r0 = un.grp * dm.LHkv / rg;
+            un.r1 = (un.grp + 1) * dm.LHkv / rg;
+        }
         un.nt_s = a.n_tokens[s];
         un.nl_s = AL ? a.n_live[s] : 0;
         constexpr int kT = 16 * W * KT;
@@ -966,7 +1051,7 @@ k_attend(AttendDims dm, AttendArgs a) {
         asm volatile("" : "+v"(lane));
         unsigned long long* next_box =
             (lanes && w == 0) ? a.lane_box + (size_t)lane_no * (dm.S + 1) + ps + 1 : nullptr;
-        attend_wave<W, NH, KT, AL, QT, WN>(dm, a, sm, un, wv, lane, tag, lane_no, cap, next_box);
+        attend_wave<W, NH, KT, AL, QT, WN, RS>(dm, a, sm, un, wv, lane, tag, lane_no, cap, next_box);
     }
 }
 
@@ -979,20 +1064,21 @@ size_t attend_lds_bytes(int G) {
 }
 
 namespace {
-template <bool AL, bool QT, bool WN>
+template <bool AL, bool QT, bool WN, bool RS = false>
 const void* attend_for(int G) {
-    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<4, 1, 4, AL, QT, WN>);
-    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<4, 2, 4, AL, QT, WN>);
-    return reinterpret_cast<const void*>(&k_attend<4, 4, 4, AL, QT, WN>);
+    if (G <= 4) return reinterpret_cast<const void*>(&k_attend<4, 1, 4, AL, QT, WN, RS>);
+    if (G <= 8) return reinterpret_cast<const void*>(&k_attend<4, 2, 4, AL, QT, WN, RS>);
+    return reinterpret_cast<const void*>(&k_attend<4, 4, 4, AL, QT, WN, RS>);
 }
 }  // namespace
 
 // G: MFMA columns (query heads per KV head times window queries).  The
-// window runs only on plain pages in full precision.
-const void* attend_kernel(int G, int aligned, int quant, int window) {
+// window runs only on plain pages in full precision, and so do row groups.
+const void* attend_kernel(int G, int aligned, int quant, int window, int row_groups) {
     if (window > 1) return attend_for<false, false, true>(G);
     if (aligned) return quant ? attend_for<true, true, false>(G) : attend_for<true, false, false>(G);
-    return quant ? attend_for<false, true, false>(G) : attend_for<false, false, false>(G);
+    if (quant) return attend_for<false, true, false>(G);
+    return row_groups > 1 ? attend_for<false, false, false, true>(G) : attend_for<false, false, false>(G);
 }
 
 // The grid as one launch: cooperative (the runtime keeps the device to it)
@@ -1000,9 +1086,9 @@ const void* attend_kernel(int G, int aligned, int quant, int window) {
 // less per step; residency is checked at init with the same launch kind).
 // With an event pair (t0, t1), an ordinary launch records the events with
 // the kernel's dispatch itself.
-static hipError_t launch_grid(const Dims& dm, int n_wg, void** args, hipStream_t st, hipEvent_t t0 = nullptr,
+static hipError_t launch_grid(const Dims& dm, int n_wg, int rg, void** args, hipStream_t st, hipEvent_t t0 = nullptr,
                               hipEvent_t t1 = nullptr) {
-    const void* fn = attend_kernel(dm.G * dm.W, dm.aligned, dm.quant, dm.W);
+    const void* fn = attend_kernel(dm.G * dm.W, dm.aligned, dm.quant, dm.W, rg);
     const dim3 grid(n_wg), block(attend_threads(dm.G * dm.W));
     const unsigned lds = (unsigned)attend_lds_bytes(dm.G * dm.W);
     if (dm.coop) return hipLaunchCooperativeKernel(fn, grid, block, args, lds, st);
@@ -1011,18 +1097,18 @@ static hipError_t launch_grid(const Dims& dm, int n_wg, void** args, hipStream_t
 }
 
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q, float* abar_out,
-                         hipStream_t st, hipEvent_t t0, hipEvent_t t1) {
+                         int rg, hipStream_t st, hipEvent_t t0, hipEvent_t t1) {
     AttendDims ad{dm.L, dm.Hq, dm.Hkv, dm.G * dm.W, dm.P, dm.Pshift, dm.MP, dm.NP, dm.R, dm.LHkv,
                   dm.wg_per_cu, dm.n_wg / dm.wg_per_cu, dm.S, dm.n_regions, dm.norm_attn, dm.pin_mask,
-                  dm.rho, dm.tau_scale, dm.alpha, dm.aligned, dm.G, dm.W};
+                  dm.rho, dm.tau_scale, dm.alpha, dm.aligned, dm.G, dm.W, rg};
     AttendArgs aa{v.k_pool, v.page_table, v.n_tokens, v.clock, v.region, v.b, v.lam, v.imp, v.t_ref,
                   sc.pscore, q, abar_out, sc.ustart, sc.plan, sc.epoch, sc.claim, sc.lane_box, sc.ustat,
-                  sc.unorm, sc.status, nullptr, v.n_live, v.page_format, v.t_ins, sc.valid};
+                  sc.unorm, sc.status, nullptr, v.n_live, v.page_format, v.t_ins, sc.valid, sc.upart};
     void* args[] = {&ad, &aa};
-    return launch_grid(dm, dm.n_wg, args, st, t0, t1);
+    return launch_grid(dm, dm.n_wg, rg, args, st, t0, t1);
 }
 
-hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, hipStream_t st) {
+hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, int rg, hipStream_t st) {
     AttendDims ad{};
     AttendArgs aa{};
     aa.probe = probe;
@@ -1030,7 +1116,7 @@ hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, hipStre
     if (e == hipSuccess) e = hipMemsetD32Async(reinterpret_cast<hipDeviceptr_t>(probe + 1), 1 << 30, 1, st);
     if (e != hipSuccess) return e;
     void* args[] = {&ad, &aa};
-    return launch_grid(dm, n_wg, args, st);
+    return launch_grid(dm, n_wg, rg, args, st);
 }
 
 }  // namespace md

@@ -24,6 +24,12 @@ constexpr int kAttendPerCu = 2;   // at most two workgroups per CU
 inline int attend_threads(int) { return 256; }
 inline int attend_unit_tokens(int) { return 256; }
 constexpr int kConsumeLag = 7;   // rows a unit runs ahead of the row it normalises
+// Row groups: when a step's units fill less than half of the fused grid, each
+// unit may cover one of up to kMaxRowGroups ranges of the L * Hkv rows
+// (at least kMinGroupRows rows each), the groups' partial masses meeting in
+// the unit of the first group.
+constexpr int kMaxRowGroups = 16;
+constexpr int kMinGroupRows = 8;
 constexpr int kRowBufs = kConsumeLag + 1;       // rows of logits held in LDS
 
 constexpr int kMaxOffload = 64;     // host-tier pages per session at most (one 64-bit slot mask)
@@ -50,6 +56,7 @@ struct Dims {
     int lane_cap;  // units one lane of k_attend workgroups holds (one workgroup per CU)
     int T;         // tokens per fused unit (attend_unit_tokens(G))
     int U_cap;     // capacity of the per-step fused unit list
+    int rg_max;    // most row groups any step uses (1: none; sizes the partial masses)
     uint32_t pin_mask;
     float rho, alpha, tau_scale;
 };
@@ -103,6 +110,7 @@ struct Scratch {
     unsigned long long* lane_box;  // [kAttendPerCu][S + 1] lane mode: tagged session range of each lane pass
     unsigned long long* ustat;  // [U_cap][R][2] tagged (max, sum) of each fused unit's rows
     unsigned long long* unorm;  // [S][R][2] tagged row normalisers (M, 1 / Lambda) of the fused sessions
+    unsigned long long* upart;  // [U_cap][T] row groups: tagged partial masses of each unit's tokens
     int32_t* chunks;       // [S] chunks per session (0 for a skipped session)
     int32_t* valid;        // [S] 1 while the session's step stands: its counters are
                            // consistent, its query finite and no wait of the fused
@@ -141,23 +149,28 @@ constexpr uint32_t kWordTagMask = (1u << 27) - 1;
 // Bound of a wait for another block's tagged word (s_memrealtime ticks of
 // 10 ns): 50 ms, far beyond any scheduling delay of a running kernel.
 constexpr uint64_t kWordWaitTicks = 5000000ull;
+// rg: row groups of the step's fused units (1: none)
 hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
                          const uint16_t* new_k, const uint8_t* new_region, int fused, int observe,
-                         uint32_t tag, hipStream_t st);
+                         int rg, uint32_t tag, hipStream_t st);
 hipError_t launch_logits(const Dims& dm, const View& v, const Scratch& sc, const float* q,
                          int n_blocks, hipStream_t st);
 hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st);
-// t0, t1: when not NULL (ordinary launches only), an event pair recorded by
-// the kernel's dispatch itself
+// rg: row groups, as given to the step's append.  t0, t1: when not NULL
+// (ordinary launches only), an event pair recorded by the kernel's dispatch
+// itself
 hipError_t launch_attend(const Dims& dm, const View& v, const Scratch& sc, const float* q,
-                         float* abar_out, hipStream_t st, hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
+                         float* abar_out, int rg, hipStream_t st, hipEvent_t t0 = nullptr,
+                         hipEvent_t t1 = nullptr);
 size_t attend_lds_bytes(int G);
-// the instantiation for G MFMA columns (heads per KV head x window), layout, tier, window
-const void* attend_kernel(int G, int aligned, int quant, int window);
-// Launch the fused kernel in check mode with n_wg workgroups: every wave
-// waits (bounded, ~20 ms) until all workgroups have arrived; probe[1]
-// receives the fewest arrivals any workgroup saw (probe: 2 device ints).
-hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, hipStream_t st);
+// the instantiation for G MFMA columns (heads per KV head x window), layout,
+// tier, window and row groups (> 1: the row-group instantiation)
+const void* attend_kernel(int G, int aligned, int quant, int window, int row_groups);
+// Launch the fused kernel (the instantiation for rg row groups) in check
+// mode with n_wg workgroups: every wave waits (bounded, ~20 ms) until all
+// workgroups have arrived; probe[1] receives the fewest arrivals any
+// workgroup saw (probe: 2 device ints).
+hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, int rg, hipStream_t st);
 hipError_t launch_mass(const Dims& dm, const View& v, const Scratch& sc, float* abar_out,
                        int n_blocks, hipStream_t st);
 hipError_t launch_score(const Dims& dm, const View& v, const Scratch& sc, float* page_score,

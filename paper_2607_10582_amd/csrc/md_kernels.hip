@@ -92,7 +92,7 @@ __device__ __forceinline__ unsigned long long append_word(uint32_t tag, bool bad
 __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
                                                 const uint16_t* __restrict__ new_k,
                                                 const uint8_t* __restrict__ new_region, int fused,
-                                                int observe, uint32_t tag) {
+                                                int observe, int rg, uint32_t tag) {
     const int s = blockIdx.x;
     __shared__ int sh_phys, sh_slot, sh_rank;
     __shared__ int lds[5 * 17];
@@ -300,9 +300,10 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
     __shared__ int s_lane_ok;
     if (threadIdx.x == 0) s_lane_ok = fused && dm.wg_per_cu >= 2;
     __syncthreads();
+    // With row groups a session's units are rg groups of its token units.
     if (fused) {
         for (int s2 = threadIdx.x; s2 < dm.S; s2 += blockDim.x) {
-            const int u = (s_n[s2] + dm.T - 1) / dm.T;
+            const int u = (s_n[s2] + dm.T - 1) / dm.T * rg;
             if (2 * u > dm.lane_cap) atomicExch(&s_lane_ok, 0);
             if (u <= dm.n_wg) s_pass[s2] = 0;
         }
@@ -327,7 +328,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
         // reads at about 2.5 TB/s, half of it at about 6.4), so the previous
         // pass's last sessions move into the next one while that lowers the
         // larger of the two passes' units.
-        auto units = [&](int s2) { return (s_n[s2] + dm.T - 1) / dm.T; };
+        auto units = [&](int s2) { return (s_n[s2] + dm.T - 1) / dm.T * rg; };
         for (int s2 = 0; s2 < dm.S; ++s2) s_pass[s2] = -1;
         int np = 0, s0 = 0;
         while (s0 < dm.S) {
@@ -382,7 +383,7 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
             const bool spill = ps < 0;
             const int ch = spill ? (nt + kChunk - 1) / kChunk : 0;
             sc.chunks[s2] = ch;
-            uu[k] = spill ? 0 : (nt + dm.T - 1) / dm.T;
+            uu[k] = spill ? 0 : (nt + dm.T - 1) / dm.T * rg;
             it[k] = ch * dm.LHkv;
             ti[k] = spill ? (nt + kTile - 1) / kTile : 0;
             si[k] = (nt + kTile - 1) / kTile;
@@ -455,8 +456,9 @@ __global__ void __launch_bounds__(256) k_append(Dims dm, View v, Scratch sc,
 
 hipError_t launch_append(const Dims& dm, const View& v, const Scratch& sc,
                          const uint16_t* new_k, const uint8_t* new_region, int fused, int observe,
-                         uint32_t tag, hipStream_t st) {
-    hipLaunchKernelGGL(k_append, dim3(dm.S), dim3(256), 0, st, dm, v, sc, new_k, new_region, fused, observe, tag);
+                         int rg, uint32_t tag, hipStream_t st) {
+    hipLaunchKernelGGL(k_append, dim3(dm.S), dim3(256), 0, st, dm, v, sc, new_k, new_region, fused, observe,
+                       max(rg, 1), tag);
     return hipGetLastError();
 }
 
@@ -1659,6 +1661,7 @@ size_t scratch_bytes(const Dims& dm) {
     n += align256((1 + (size_t)kAttendPerCu * (dm.S + 1)) * sizeof(unsigned long long));
     n += align256((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long));
     n += align256((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long));
+    n += align256((dm.rg_max > 1 ? (size_t)dm.U_cap * dm.T : 0) * sizeof(unsigned long long));
     n += align256(4 * sizeof(int32_t));
     n += align256(9 * sizeof(unsigned long long));
     n += 3 * align256((size_t)dm.S * sizeof(unsigned long long));
@@ -1695,6 +1698,8 @@ void scratch_carve(const Dims& dm, void* base, Scratch* sc) {
         take((size_t)dm.R * dm.U_cap * 2 * sizeof(unsigned long long)));
     sc->unorm = reinterpret_cast<unsigned long long*>(
         take((dm.fused ? (size_t)dm.S * dm.R : 0) * 2 * sizeof(unsigned long long)));
+    sc->upart = reinterpret_cast<unsigned long long*>(
+        take((dm.rg_max > 1 ? (size_t)dm.U_cap * dm.T : 0) * sizeof(unsigned long long)));
     int32_t* words = reinterpret_cast<int32_t*>(take(4 * sizeof(int32_t)));
     sc->status = words;      // the warning word follows the status word (read together)
     sc->warn = words + 1;

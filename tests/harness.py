@@ -106,7 +106,7 @@ class Pair:
                  steps=None, fused: Optional[bool] = True, priors=None, strict_ties: bool = False,
                  check_free_list: bool = False, static: bool = False, pool: int = 0,
                  offload_pages: int = 0, drop_threshold: float = 0.0, cooperative: bool = False,
-                 explicit_lists: bool = False, select_compact: bool = False):
+                 explicit_lists: bool = False, select_compact: bool = False, row_groups: bool = True):
         # pool > 0: the oracle sessions run in that many worker processes
         # (oracle.pool), all sessions of a step at once
         self.w = w
@@ -190,7 +190,8 @@ class Pair:
                            rho=f32(w.rho), alpha=f32(self.alpha), tau_scale=f32(w.tau_scale),
                            pinned_mask=self.pinned_mask, fused=fused, attention_norm=w.attention_norm,
                            window=w.window, region_aligned=al, quant_threshold=w.quant_threshold,
-                           static=static, drop_threshold=f32(drop_threshold), cooperative=cooperative)
+                           static=static, drop_threshold=f32(drop_threshold), cooperative=cooperative,
+                           row_groups=row_groups)
         n_slots = n_phys * P
         self.abar = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)
         self.tscore = torch.zeros(n_slots, dtype=torch.float32, device=self.dev)

@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert B.md_abi_version() == 9
+    assert B.md_abi_version() == 10
     for st in (0, -1, -2, -3, -4, -5, -6):
         assert B.md_status_str(st)
     assert B.md_status_str(12345) == "unknown status"
@@ -121,7 +121,7 @@ def fake_rp():
     (dict(alpha=-1.0), B.MD_E_INVALID),
     (dict(alpha=float("inf")), B.MD_E_INVALID),
     (dict(tau_scale=-2.0), B.MD_E_INVALID),
-    (dict(flags=32), B.MD_E_INVALID),
+    (dict(flags=64), B.MD_E_INVALID),
     (dict(window=0), B.MD_E_INVALID),
     (dict(quant_threshold=-1.0), B.MD_E_INVALID),
     (dict(quant_threshold=float("nan")), B.MD_E_INVALID),

@@ -265,11 +265,11 @@ def test_selection_on_scores_of_the_fused_kernel():
         assert np.array_equal(x, y)
 
 
-@pytest.mark.parametrize("name,steady_fused", [("qwen15_1700", False), ("long32k", True)])
+@pytest.mark.parametrize("name,steady_fused", [("qwen15_1700", False), ("long32k", True), ("qwen3_32x1700", True)])
 def test_library_picks_the_path(name, steady_fused):
     # Without a path flag the library runs the multi-kernel path for small
-    # caches and the fused kernel for large ones; either way the steps match
-    # the oracle.
+    # caches and the fused kernel for large ones (for a batch of small ones
+    # with row groups); either way the steps match the oracle.
     w = C.get(name)
     big = w.name == "long32k"
     p = Pair(w, fused=None, backend="torch" if big else "numpy",
