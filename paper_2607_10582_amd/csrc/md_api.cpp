@@ -349,8 +349,13 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     // be resident together: check it on the device, with the launch kind the
     // step uses, and step the grid down one workgroup per CU at a time until
     // every workgroup arrives.
+    int32_t* probe = nullptr;   // kept for the row-group instantiation's check below
+    auto free_probe = [&] {
+        if (!use_static && probe != nullptr) (void)hipFree(probe);
+        probe = nullptr;
+    };
     if (dm.fused) {
-        int32_t* probe = static_cast<int32_t*>(static_base);   // the static scratch is free until carved
+        probe = static_cast<int32_t*>(static_base);   // the static scratch is free until carved
         if (!use_static && hipMalloc(&probe, 2 * sizeof(int32_t)) != hipSuccess) return MD_E_NOMEM;
         int verified = 0;
         for (int o = occ; o >= 1 && verified == 0; --o) {
@@ -363,19 +368,6 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
             }
             if (seen[1] >= o * n_cu) verified = o * n_cu;
         }
-        // the row-group instantiation must hold the same grid
-        if (rows_ok && verified > 0) {
-            int32_t seen[2] = {0, 0};
-            if (md::launch_attend_check(dm, probe, verified, 2, hs) != hipSuccess ||
-                hipMemcpyAsync(seen, probe, sizeof(seen), hipMemcpyDeviceToHost, hs) != hipSuccess ||
-                hipStreamSynchronize(hs) != hipSuccess) {
-                (void)hipGetLastError();
-                rows_ok = false;
-            } else {
-                rows_ok = seen[1] >= verified;
-            }
-        }
-        if (!use_static) (void)hipFree(probe);
         dm.n_wg = verified;
         dm.wg_per_cu = verified / n_cu;
         dm.lane_cap = n_cu;
@@ -403,8 +395,10 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
         if (hipMemcpyAsync(hn, cv->n_tokens, dm.S * sizeof(int32_t), hipMemcpyDeviceToHost, hs) != hipSuccess ||
             hipMemcpyAsync(hbud, cv->budget, dm.S * sizeof(int32_t), hipMemcpyDeviceToHost, hs) !=
                 hipSuccess ||
-            hipStreamSynchronize(hs) != hipSuccess)
+            hipStreamSynchronize(hs) != hipSuccess) {
+            free_probe();
             return MD_E_HIP;
+        }
         int64_t first = 0, steady = 0;
         for (int s = 0; s < dm.S; ++s) {
             const int64_t n = hn[s] > 0 ? hn[s] : 0;
@@ -422,6 +416,20 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
         };
         rg_first = pick(first);
         rg_steady = pick(steady);
+        // the row-group instantiation, when a step will use it, must hold
+        // the same grid as the plain one
+        if (std::max(rg_first, rg_steady) > 1) {
+            int32_t seen[2] = {0, 0};
+            bool held = false;
+            if (md::launch_attend_check(dm, probe, dm.n_wg, 2, hs) != hipSuccess ||
+                hipMemcpyAsync(seen, probe, sizeof(seen), hipMemcpyDeviceToHost, hs) != hipSuccess ||
+                hipStreamSynchronize(hs) != hipSuccess) {
+                (void)hipGetLastError();
+            } else {
+                held = seen[1] >= dm.n_wg;
+            }
+            if (!held) rg_first = rg_steady = 1;
+        }
         if (!(cfg->flags & MD_FLAG_FUSED)) {
             fused_first = 2 * first * rg_first >= dm.n_wg;
             fused_steady = 2 * steady * rg_steady >= dm.n_wg;
@@ -429,6 +437,7 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
         if (!fused_first) rg_first = 1;
         if (!fused_steady) rg_steady = 1;
     }
+    free_probe();
     dm.rg_max = std::max(rg_first, rg_steady);
     if (dm.fused) dm.U_cap *= dm.rg_max;
     dm.multi = dm.spill || !fused_first || !fused_steady;

@@ -152,12 +152,25 @@ def main():
     if a.mode == "hits":
         hit = counter_values(a.pmc_dir, "TCC_HIT_sum")
         miss = counter_values(a.pmc_dir, "TCC_MISS_sum")
-        k = [n for n in hit if short_name(n).startswith(a.kernel)][0]
-        hs, ms = hit[k][a.skip:], miss[k][a.skip:]
-        rate = sum(hs) / max(sum(hs) + sum(ms), 1.0)
-        print(f"| {a.kernel} | steady launches | TCC hits per launch | TCC misses per launch | hit rate |")
+        names = [n for n in hit if short_name(n).startswith(a.kernel)]
+        if not names:
+            raise RuntimeError(f"{a.kernel} not in {a.pmc_dir}")
+        # every instantiation of the kernel, by dispatch order; the fused
+        # kernel's launch kinds are told apart by their accesses
+        hs_all = [v for n in names for v in hit[n]]
+        ms_all = [v for n in names for v in miss[n]]
+        groups = [("steady", list(range(a.skip, len(hs_all))))]
+        if a.kernel == "k_attend":
+            st, bk, _ = kinds([h + m for h, m in zip(hs_all, ms_all)])
+            groups = [("steady", st), ("first observation", bk)]
+        print(f"| {a.kernel} launches | count | L2 (TCC) hits per launch | misses per launch | hit rate |")
         print("|---|---:|---:|---:|---:|")
-        print(f"| | {len(hs)} | {statistics.mean(hs):.4g} | {statistics.mean(ms):.4g} | {100 * rate:.1f} % |")
+        for label, idx in groups:
+            if not idx:
+                continue
+            hs, ms = [hs_all[i] for i in idx], [ms_all[i] for i in idx]
+            rate = sum(hs) / max(sum(hs) + sum(ms), 1.0)
+            print(f"| {label} | {len(idx)} | {statistics.mean(hs):.4g} | {statistics.mean(ms):.4g} | {100 * rate:.1f} % |")
         return
 
     nbytes = a.copy_mib << 20
