@@ -335,9 +335,9 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q,
  * is pinned and scores +INFINITY.
  * page_score:  optional float32 [S][MP], logical page order.
  * token_score: optional float32 [NP][P] at each live slot.
- * The library keeps its own copy of the page scores for md_select_evict.
- * When md_observe_step ran on the fused kernel, that copy is already
- * complete, and a call with both outputs NULL enqueues nothing.
+ * The library keeps its own copy of the page scores for md_select_evict;
+ * md_observe_step completes it on either observation path, so a call with
+ * both outputs NULL enqueues nothing.
  * Requires md_observe_step since the last md_compact (MD_E_STATE otherwise).
  */
 md_status md_score_pages(md_handle h, float* page_score, float* token_score);

@@ -42,7 +42,6 @@ struct md_handle_s {
     bool fused_steady;   // later observes run the fused kernel
     int rg_first;        // row groups of the fused units on the first observe
     int rg_steady;       // and on later ones (1: every unit walks every row)
-    bool fused_last;     // the last observe ran it
     int64_t observed;    // observes enqueued
     Phase phase;
     const int32_t* sel_serial;   // md_select_evict's lists since the last observe
@@ -514,7 +513,6 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     h->fused_steady = fused_steady;
     h->rg_first = rg_first;
     h->rg_steady = rg_steady;
-    h->fused_last = false;
     h->observed = 0;
     h->word_tag = 0;
     h->phase = kNone;
@@ -570,13 +568,16 @@ md_status md_observe_step(md_handle h, int32_t step, const float* q, const uint1
             return md::launch_attend(h->dm, h->v, h->sc, q, abar_out, rg, h->stream, t0, t1); });
     if (e == hipSuccess && multi) e = timed_launch(h, MD_K_LOGITS, [&] {
         return md::launch_logits(h->dm, h->v, h->sc, q, h->logits_blocks, h->stream); });
-    if (e == hipSuccess && multi) e = timed_launch(h, MD_K_ROWSTATS, [&] {
+    // Sessions of at most kFoldChunks chunks: the mass kernel works out the
+    // row statistics itself (the offload tier reads them, so it keeps the
+    // separate kernel).
+    const bool fold = h->dm.max_chunks <= md::kFoldChunks && h->dm.H == 0;
+    if (e == hipSuccess && multi && !fold) e = timed_launch(h, MD_K_ROWSTATS, [&] {
         return md::launch_rowstats(h->dm, h->sc, h->stream); });
     if (e == hipSuccess && multi) e = timed_launch(h, MD_K_MASS, [&] {
-        return md::launch_mass(h->dm, h->v, h->sc, abar_out, h->mass_blocks, h->stream); });
+        return md::launch_mass(h->dm, h->v, h->sc, abar_out, h->mass_blocks, fold, h->stream); });
     if (e == hipSuccess && h->dm.H > 0) e = md::launch_recall(h->dm, h->v, h->sc, q, abar_out, h->stream);
     if (e != hipSuccess) return MD_E_HIP;
-    h->fused_last = fused && !h->dm.spill;
     h->observed += 1;
     h->have_step = true;
     h->last_step = step;
@@ -592,10 +593,10 @@ md_status md_score_pages(md_handle h, float* page_score, float* token_score) {
         return MD_E_INVALID;
     if (h->phase != kObserved && h->phase != kScored) return MD_E_STATE;
     if (hipSetDevice(h->device) != hipSuccess) return MD_E_HIP;
-    // The fused observation kernel already left every session's page scores
-    // in the library's copy; the scoring kernel runs again only to fill the
-    // caller's outputs, or for sessions of the multi-kernel path.
-    const bool needed = page_score != nullptr || token_score != nullptr || !h->fused_last;
+    // The observation (the fused kernel, or the multi-kernel path's mass
+    // kernel) already left every session's page scores in the library's
+    // copy; the scoring kernel runs again only to fill the caller's outputs.
+    const bool needed = page_score != nullptr || token_score != nullptr;
     if (needed && timed_launch(h, MD_K_SCORE, [&] {
             return md::launch_score(h->dm, h->v, h->sc, page_score, token_score, h->score_blocks,
                                     h->stream); }) != hipSuccess)

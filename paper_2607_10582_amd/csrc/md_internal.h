@@ -32,6 +32,7 @@ constexpr int kMaxRowGroups = 16;
 constexpr int kMinGroupRows = 8;
 constexpr int kRowBufs = kConsumeLag + 1;       // rows of logits held in LDS
 
+constexpr int kFoldChunks = 16;    // multi-kernel path: sessions of at most 2,048 tokens fold their row statistics into the mass kernel
 constexpr int kMaxOffload = 64;     // host-tier pages per session at most (one 64-bit slot mask)
 
 constexpr int kDevCorrupt = MD_DEV_CORRUPT;
@@ -171,8 +172,11 @@ const void* attend_kernel(int G, int aligned, int quant, int window, int row_gro
 // workgroups have arrived; probe[1] receives the fewest arrivals any
 // workgroup saw (probe: 2 device ints).
 hipError_t launch_attend_check(const Dims& dm, int32_t* probe, int n_wg, int rg, hipStream_t st);
+// fold: the mass kernel works out the row statistics itself (no
+// launch_rowstats before it; sessions of at most kFoldChunks chunks).  It
+// also writes the page scores of the sessions it observes.
 hipError_t launch_mass(const Dims& dm, const View& v, const Scratch& sc, float* abar_out,
-                       int n_blocks, hipStream_t st);
+                       int n_blocks, bool fold, hipStream_t st);
 hipError_t launch_score(const Dims& dm, const View& v, const Scratch& sc, float* page_score,
                         float* token_score, int n_blocks, hipStream_t st);
 hipError_t launch_select(const Dims& dm, const View& v, const Scratch& sc, int32_t* ev_serial,

@@ -815,7 +815,15 @@ hipError_t launch_rowstats(const Dims& dm, const Scratch& sc, hipStream_t st) {
 
 // One block per 64-token tile at a time: 4 row groups x 64 tokens; each
 // thread sums its rows' softmax weights 2^(x - M) / Lambda, the four partials
-// add in a fixed order.
+// add in a fixed order; then wave 0 applies Eq. 2 and Eq. 3 to the tile's
+// tokens and scores them and their pages (Eq. 4, Eq. 5: the scoring
+// kernel's work, with the same device functions and reduction, so the
+// selection reads the page scores the scoring kernel would have written).
+// FOLD: each block works its session's row statistics (M, 1 / Lambda) out
+// from the chunk statistics itself, in a fixed order (sessions of at most
+// kFoldChunks chunks: a few KB read per block), instead of a separate
+// row-statistics kernel.
+template <bool FOLD>
 __global__ void __launch_bounds__(256) k_mass(Dims dm, View v, Scratch sc, float* abar_out) {
     __shared__ int s_pref[kMaxSessions + 1];
     __shared__ float2 s_rs[kMaxRows];
@@ -831,7 +839,30 @@ __global__ void __launch_bounds__(256) k_mass(Dims dm, View v, Scratch sc, float
         const int s = find_session(s_pref, S, tile);
         if (s != cur) {
             __syncthreads();
-            for (int i = threadIdx.x; i < dm.R; i += blockDim.x) s_rs[i] = sc.rstats[(size_t)s * dm.R + i];
+            if constexpr (FOLD) {
+                // the session's rows: max over its chunks, then the sum of
+                // their sums rescaled to it, chunk by chunk
+                const int nch = min(sc.chunks[s], kFoldChunks);
+                for (int i = threadIdx.x; i < dm.R; i += blockDim.x) {
+                    const float2* cs = sc.cstats + ((size_t)s * dm.R + i) * dm.max_chunks;
+                    float2 st[kFoldChunks];
+                    float m = -INFINITY;
+#pragma unroll
+                    for (int c = 0; c < kFoldChunks; ++c) {
+                        st[c] = c < nch ? cs[c] : make_float2(-INFINITY, 0.0f);
+                        m = fmaxf(m, st[c].x);
+                    }
+                    float l = 0.0f;
+#pragma unroll
+                    for (int c = 0; c < kFoldChunks; ++c)
+                        if (c < nch) l += st[c].y * hw_exp2(st[c].x - m);
+                    // a window query that sees none of the session's tokens
+                    // gives them no weight (its row has no live logit)
+                    s_rs[i] = m == -INFINITY ? make_float2(0.0f, 0.0f) : make_float2(m, 1.0f / l);
+                }
+            } else {
+                for (int i = threadIdx.x; i < dm.R; i += blockDim.x) s_rs[i] = sc.rstats[(size_t)s * dm.R + i];
+            }
             __syncthreads();
             cur = s;
         }
@@ -851,7 +882,7 @@ __global__ void __launch_bounds__(256) k_mass(Dims dm, View v, Scratch sc, float
                 valid = false;   // a hole holds no token
             } else {
                 const float* lp = sc.logits + (size_t)phys * dm.R * dm.P + slot;
-#pragma unroll 8
+#pragma unroll 16
                 for (int row = rg; row < dm.R; row += 4) {
                     const float2 rs = s_rs[row];
                     acc += hw_exp2(lp[(size_t)row * dm.P] - rs.x) * rs.y;
@@ -860,22 +891,51 @@ __global__ void __launch_bounds__(256) k_mass(Dims dm, View v, Scratch sc, float
         }
         s_part[rg][tl] = acc;
         __syncthreads();
-        if (rg == 0 && valid && sc.valid[s]) {   // a void step writes nothing
-            const float abar =
-                (((s_part[0][tl] + s_part[1][tl]) + s_part[2][tl]) + s_part[3][tl]) / (float)dm.R;
+        if (rg == 0) {
+            // every load before the stores (a wait for a load also waits for them)
             const size_t si = (size_t)phys * dm.P + slot;
-            const float a = v.imp[si];
-            v.imp[si] = fmaf(dm.rho, a, one_m_rho * abar);
-            if (abar >= dm.tau_scale / (float)v.n_live[s]) v.t_ref[si] = v.clock[s];
-            if (abar_out != nullptr) abar_out[si] = abar;
+            const bool keep = sc.valid[s] != 0;   // a void step writes nothing
+            const int t = v.clock[s];
+            const int n_live = v.n_live[s];
+            float a = 0.0f;
+            int tr = 0, r = 0;
+            if (valid) {
+                a = v.imp[si];
+                tr = v.t_ref[si];
+                r = v.region[si];
+            }
+            if (valid && r >= dm.n_regions) {
+                atomicOr(sc.status, kDevCorrupt);
+                r = dm.n_regions - 1;
+            }
+            const size_t ri = (size_t)s * dm.n_regions + r;
+            const float br = valid ? v.b[ri] : 0.0f, lamr = valid ? v.lam[ri] : 0.0f;
+            if (valid && keep) {
+                const float abar =
+                    (((s_part[0][tl] + s_part[1][tl]) + s_part[2][tl]) + s_part[3][tl]) / (float)dm.R;
+                a = fmaf(dm.rho, a, one_m_rho * abar);
+                v.imp[si] = a;
+                if (abar >= dm.tau_scale / (float)n_live) {
+                    tr = t;
+                    v.t_ref[si] = tr;
+                }
+                if (abar_out != nullptr) abar_out[si] = abar;
+            }
+            const bool pin = valid && ((dm.pin_mask >> r) & 1u);
+            const float sc_i = pin ? INFINITY
+                                   : (valid ? retention_score(br, lamr, t, tr, attention_weight(dm.alpha, dm.norm_attn, n_live), a)
+                                            : 0.0f);
+            float ps;
+            const bool has = page_score_of(sc_i, valid, pin, dm.P, &ps);
+            if ((tl & (dm.P - 1)) == 0 && has) sc.pscore[(size_t)s * dm.MP + (tok >> dm.Pshift)] = ps;
         }
         __syncthreads();
     }
 }
 
 hipError_t launch_mass(const Dims& dm, const View& v, const Scratch& sc, float* abar_out,
-                       int n_blocks, hipStream_t st) {
-    hipLaunchKernelGGL(k_mass, dim3(n_blocks), dim3(256), 0, st, dm, v, sc, abar_out);
+                       int n_blocks, bool fold, hipStream_t st) {
+    hipLaunchKernelGGL(fold ? k_mass<true> : k_mass<false>, dim3(n_blocks), dim3(256), 0, st, dm, v, sc, abar_out);
     return hipGetLastError();
 }
 
