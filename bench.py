@@ -11,9 +11,11 @@ appended keys) are resident in HBM before timing starts.
 The default workload is the ragged batch: 64 agent sessions of U[2,048,
 65,536] cached tokens with Qwen2.5-3B's attention shape (36 layers, 16 query
 / 2 KV heads, d = 128), 16-token pages and a 20 % budget, 64 decode steps.
-The same run also measures the ragged batch with 64-token pages and the
+The same run also measures the ragged batch with 64-token pages, the
 long-horizon batch (16 sessions x 32,768 tokens, 1.5B shape, 25 % budget,
-128 steps) as sub-records.
+128 steps) and the batch of short sessions (32 x 1,700 tokens, 3B shape,
+30 % budget, 256 steps, on the fused kernel with row groups) as
+sub-records.
 
 For every workload, step 1 runs three times on a copy of the state first
 (so the code objects are loaded), then one trajectory from the fresh cache:
@@ -51,7 +53,7 @@ sys.path.insert(0, ROOT)
 METRIC = "cached tokens scored+evicted per second per decode step; achieved HBM GB/s vs peak"
 PEAK_HBM_GBS = 8000.0
 DEFAULT_WORKLOAD = "ragged_p16"
-DEFAULT_ALSO = "ragged_p64,long32k"
+DEFAULT_ALSO = "ragged_p64,long32k,qwen3_32x1700"
 
 
 def log(*a):
