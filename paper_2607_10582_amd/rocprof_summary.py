@@ -178,11 +178,14 @@ def main():
     fw = copy_factor(a.cal_write_dir, "WRITE_SIZE", nbytes)
     fetch = counter_values(a.fetch_dir, "FETCH_SIZE")
     write = counter_values(a.write_dir, "WRITE_SIZE")
+    # the kernel's instantiation that moved the most bytes (another one may
+    # have run only md_init's residency checks)
     key = [k for k in fetch if short_name(k).startswith(a.kernel)]
     if not key:
         raise RuntimeError(f"{a.kernel} not in {a.fetch_dir}")
-    allf = fetch[key[0]]
-    allw = write[[k for k in write if short_name(k).startswith(a.kernel)][0]]
+    name = max(key, key=lambda k: sum(fetch[k]))
+    allf = fetch[name]
+    allw = write[name]
     # the two runs launch the same sequence; kinds are read off the reads
     st, bk, _ = kinds(allf)
     kf, kw = [allf[i] for i in st], [allw[i] for i in st]
