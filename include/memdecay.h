@@ -176,8 +176,9 @@ typedef struct md_config {
     float tau_scale;            /* tau = tau_scale / |K_t| (Eq. 3's scaled form)  */
     int32_t flags;              /* MD_FLAG_* bits; other bits must be 0           */
     int32_t window;             /* W >= 1 decode queries per observation, with    */
-                                /* (Hq/Hkv) W <= 16 and L Hq W <= 1024; W > 1     */
-                                /* runs on the multi-kernel path (Sec. III-C)     */
+                                /* (Hq/Hkv) W <= 16 and L Hq W <= 1024 (Sec.      */
+                                /* III-C); both observation paths take W > 1 on   */
+                                /* every page layout and tier                     */
     float quant_threshold;      /* quantised tier (Sec. III-E): md_compact turns  */
                                 /* pages scoring below it into 8-bit codes; 0 =   */
                                 /* off, +INFINITY = every eligible page           */

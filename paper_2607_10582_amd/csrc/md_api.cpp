@@ -188,10 +188,6 @@ static md_status validate_config(const md_config* c) {
     if (!(c->tau_scale >= 0.0f) || !isfinite(c->tau_scale)) return MD_E_INVALID;
     if (c->window < 1) return MD_E_INVALID;
     if (!(c->quant_threshold >= 0.0f)) return MD_E_INVALID;   // NaN too
-    // the fused kernel takes a window only on plain pages in full precision
-    if ((c->flags & MD_FLAG_FUSED) && c->window > 1 &&
-        ((c->flags & MD_FLAG_REGION_ALIGNED) || c->quant_threshold > 0.0f))
-        return MD_E_UNSUPPORTED;
     if (c->head_dim != md::kHeadDim) return MD_E_UNSUPPORTED;
     if ((int64_t)(c->n_q_heads / c->n_kv_heads) * c->window > 16) return MD_E_UNSUPPORTED;
     if ((int64_t)c->n_layers * c->n_q_heads * c->window > md::kMaxRows) return MD_E_UNSUPPORTED;
@@ -268,8 +264,7 @@ static md_status init_handle(const md_config* cfg, const md_region_params* rp, c
     dm.rho = cfg->rho;
     dm.alpha = cfg->alpha;
     dm.tau_scale = cfg->tau_scale;
-    dm.fused = ((cfg->flags & MD_FLAG_NO_FUSED) ||
-                (dm.W > 1 && ((cfg->flags & MD_FLAG_REGION_ALIGNED) || cfg->quant_threshold > 0.0f))) ? 0 : 1;
+    dm.fused = (cfg->flags & MD_FLAG_NO_FUSED) ? 0 : 1;
     dm.norm_attn = (cfg->flags & MD_FLAG_NORM_ATTENTION) ? 1 : 0;
     dm.coop = (cfg->flags & MD_FLAG_COOPERATIVE) ? 1 : 0;
     dm.aligned = (cfg->flags & MD_FLAG_REGION_ALIGNED) ? 1 : 0;

@@ -1072,10 +1072,13 @@ const void* attend_for(int G) {
 }
 }  // namespace
 
-// G: MFMA columns (query heads per KV head times window queries).  The
-// window runs only on plain pages in full precision, and so do row groups.
+// G: MFMA columns (query heads per KV head times window queries).  Row
+// groups run only on plain pages in full precision with one query.
 const void* attend_kernel(int G, int aligned, int quant, int window, int row_groups) {
-    if (window > 1) return attend_for<false, false, true>(G);
+    if (window > 1) {
+        if (aligned) return quant ? attend_for<true, true, true>(G) : attend_for<true, false, true>(G);
+        return quant ? attend_for<false, true, true>(G) : attend_for<false, false, true>(G);
+    }
     if (aligned) return quant ? attend_for<true, true, false>(G) : attend_for<true, false, false>(G);
     if (quant) return attend_for<false, true, false>(G);
     return row_groups > 1 ? attend_for<false, false, false, true>(G) : attend_for<false, false, false>(G);

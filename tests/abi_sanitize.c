@@ -148,7 +148,6 @@ static void config_cases(void) {
     CONFIG_CASE(c_.tau_scale = NAN, MD_E_INVALID);
     CONFIG_CASE(c_.window = 0, MD_E_INVALID);
     CONFIG_CASE(c_.quant_threshold = NAN, MD_E_INVALID);
-    CONFIG_CASE((c_.flags = MD_FLAG_FUSED, c_.window = 2, c_.quant_threshold = 0.5f), MD_E_UNSUPPORTED);
     CONFIG_CASE(c_.head_dim = 64, MD_E_UNSUPPORTED);
     CONFIG_CASE(c_.window = 3, MD_E_UNSUPPORTED);            /* G W = 18 > 16 */
     CONFIG_CASE(c_.n_layers = 100, MD_E_UNSUPPORTED);        /* L Hq = 1200 rows */

@@ -126,8 +126,6 @@ def fake_rp():
     (dict(quant_threshold=-1.0), B.MD_E_INVALID),
     (dict(quant_threshold=float("nan")), B.MD_E_INVALID),
     (dict(window=3), B.MD_E_UNSUPPORTED),            # G = 6: 18 MFMA columns
-    (dict(window=2, flags=2 | 8), B.MD_E_UNSUPPORTED),   # fused with a window: plain pages only
-    (dict(window=2, flags=2, quant_threshold=0.5), B.MD_E_UNSUPPORTED),
     (dict(flags=3), B.MD_E_INVALID),
     (dict(offload_pages=-1), B.MD_E_INVALID),
     (dict(offload_pages=65), B.MD_E_INVALID),

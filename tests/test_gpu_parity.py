@@ -437,12 +437,14 @@ def test_region_aligned_ragged_batch(P):
     run_pair(p, 12, f"aligned-ragged-P{P}")
 
 
-def test_region_aligned_window():
-    # W = 2 window queries every other step on the multi-kernel path: the
-    # causal mask and the hole mask together.
+@pytest.mark.parametrize("fused", [True, False])
+def test_region_aligned_window(fused):
+    # W = 2 window queries every other step on both paths: the causal mask
+    # and the hole mask together.
     w = C.with_overrides(C.get("small_aligned"), window=2, obs_interval=2, steps=24)
-    p = Pair(w, fused=None, planted=24, planted_strength=2.5, query_gain=0.7)
-    run_pair(p, 24, "aligned-window2")
+    p = Pair(w, fused=fused, planted=24, planted_strength=2.5, query_gain=0.7)
+    assert p.md.kernel_config()["fused"] == fused
+    run_pair(p, 24, f"aligned-window2-fused{int(fused)}")
 
 
 # ---------------------------------------------------------------- quantised tier
@@ -480,10 +482,16 @@ def test_quantised_tier_3b_shape_pages_of_64_region_aligned(fused):
     assert run_quant(p, 20, f"quant-3b-p64-aligned-fused{int(fused)}") > 0
 
 
-def test_quantised_tier_with_a_window():
-    w = C.with_overrides(C.get("small"), L=2, window=2, obs_interval=2, quant_threshold=0.35, steps=24)
-    p = Pair(w, fused=None, planted=24, planted_strength=2.5, query_gain=0.7)
-    assert run_quant(p, 24, "quant-window2") > 0
+@pytest.mark.parametrize("aligned", [False, True])
+@pytest.mark.parametrize("fused", [True, False])
+def test_quantised_tier_with_a_window(fused, aligned):
+    # quantised tiles under a window of two queries, on plain and on
+    # region-aligned pages, on both observation paths
+    w = C.with_overrides(C.get("small_aligned" if aligned else "small"), L=2, window=2, obs_interval=2,
+                         quant_threshold=0.35, steps=24)
+    p = Pair(w, fused=fused, planted=24, planted_strength=2.5, query_gain=0.7)
+    assert p.md.kernel_config()["fused"] == fused
+    assert run_quant(p, 24, f"quant-window2-aligned{int(aligned)}-fused{int(fused)}") > 0
 
 
 def test_quantised_tier_long32k_sampled_sessions():
