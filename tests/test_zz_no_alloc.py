@@ -40,6 +40,7 @@ def _need_gpu():
 
 def trajectory(w, static: bool, steps: int, **kw):
     p = Pair(w, static=static, **kw)
+    cfg = p.md.kernel_config()
     out = []
     for _ in range(steps):
         p.step()
@@ -55,7 +56,7 @@ def trajectory(w, static: bool, steps: int, **kw):
     assert p.device_status() == 0
     assert p.free_pages_consistent()
     p.close()
-    return out
+    return out, cfg
 
 
 def same_bits(a: np.ndarray, b: np.ndarray) -> bool:
@@ -64,16 +65,23 @@ def same_bits(a: np.ndarray, b: np.ndarray) -> bool:
 
 @pytest.mark.parametrize("fused", [True, False])
 def test_static_handles_match_md_init_twice(fused):
-    # first a batch of three sessions (one over the budget from the start,
-    # one infeasible), then one smaller session: each md_init_static handle
+    # first two sessions of eight layers (on the fused kernel: two row
+    # groups, whose partial masses sit in the static scratch too), then a
+    # batch of three sessions (one over the budget from the start, one
+    # infeasible), then one smaller session: each md_init_static handle
     # reuses the static array the previous one left behind
+    rows = C.with_overrides(C.get("small"), L=8, S=2, n0=None, n0_range=(1, 2), steps=6)
     big = C.with_overrides(C.get("small"), L=2, S=3, n0=None, n0_range=(1, 2), steps=10)
     small = C.with_overrides(C.get("small"), L=2, n0=200, steps=8)
-    cases = [(big, dict(n0s=[450, 1200, 90], budgets=[225, 400, 50])), (small, dict())]
+    cases = [(rows, dict(n0s=[450, 700], budgets=[225, 300])),
+             (big, dict(n0s=[450, 1200, 90], budgets=[225, 400, 50])), (small, dict())]
     for w, kw in cases:
         say(f"[no-alloc] S={w.S} steps={w.steps} fused={fused}")
-        ref = trajectory(w, False, w.steps, fused=fused, **kw)
-        got = trajectory(w, True, w.steps, fused=fused, **kw)
+        ref, cfg_ref = trajectory(w, False, w.steps, fused=fused, **kw)
+        got, cfg_got = trajectory(w, True, w.steps, fused=fused, **kw)
+        assert cfg_ref == cfg_got
+        if w is rows and fused:
+            assert cfg_got["first_row_groups"] == 2 and cfg_got["steady_row_groups"] == 2
         for k, (a, b) in enumerate(zip(ref, got)):
             for name in a:
                 assert same_bits(a[name], b[name]), (k + 1, name)
