@@ -54,7 +54,8 @@ def test_library_splits_rows_for_a_small_batch():
     # observation and 64 later, against 512 workgroups; the library picks the
     # fused kernel with two row groups for the first and eight (of nine rows)
     # for the later ones.  With 8 sessions (16 units, 144 with nine groups)
-    # the grid stays under half full and the multi-kernel path runs.
+    # row groups still fill a quarter of the grid and take both; with 4 (8
+    # units, 72) the later observes take the multi-kernel path.
     w = C.with_overrides(C.get("qwen3_32x1700"), steps=16)
     p = Pair(w, fused=None, select_compact=True, oracle_sessions=[0, 13, 31])
     cfg = p.md.kernel_config()
@@ -62,10 +63,15 @@ def test_library_splits_rows_for_a_small_batch():
     assert cfg["first_row_groups"] == 2 and cfg["steady_row_groups"] == 8
     st = run_pair(p, 16, "rows-auto-qwen3-32")
     assert st.evicted_pages > 3 * 60
-    p8 = Pair(C.with_overrides(w, S=8), fused=None, oracle_sessions=[])
+    p8 = Pair(C.with_overrides(w, S=8), fused=None, oracle_sessions=[0, 7])
     cfg8 = p8.md.kernel_config()
-    assert cfg8["first_fused"] and cfg8["first_row_groups"] == 9 and not cfg8["steady_fused"]
-    p8.close()
+    assert cfg8["first_fused"] and cfg8["first_row_groups"] == 9
+    assert cfg8["steady_fused"] and cfg8["steady_row_groups"] == 9
+    run_pair(p8, 16, "rows-auto-qwen3-8")
+    p4 = Pair(C.with_overrides(w, S=4), fused=None, oracle_sessions=[])
+    cfg4 = p4.md.kernel_config()
+    assert cfg4["first_fused"] and not cfg4["steady_fused"]
+    p4.close()
 
 
 @pytest.mark.parametrize("L,Hq,Hkv,groups", [(13, 16, 2, 3), (8, 16, 2, 2), (28, 8, 1, 3), (36, 16, 2, 9)])
