@@ -148,3 +148,18 @@ def test_row_groups_cooperative_launch():
     p = Pair(w, fused=True, cooperative=True, oracle_sessions=[0, 5])
     assert p.md.kernel_config()["steady_row_groups"] > 1
     run_pair(p, 10, "rows-cooperative")
+
+
+@pytest.mark.parametrize("P", [16, 64])
+def test_row_groups_on_empty_and_short_sessions(P):
+    # empty, single-token, exact-page, page+1, partial-tail and longer
+    # sessions in one batch with row groups (16 layers x 2 KV heads = 32
+    # rows in four groups); budgets below, at and above the pinned span
+    w = C.with_overrides(C.get("small"), L=16, Hq=8, Hkv=2, S=7, n0=None, P=P,
+                         n0_range=(1, 2), steps=24, system_len=20)
+    n0s = [0, 1, 15, 16, 17, 130, 700]
+    budgets = [0, 0, 5, 16, 10, 100, 200]
+    p = Pair(w, n0s=n0s, budgets=budgets, fused=True)
+    cfg = p.md.kernel_config()
+    assert cfg["first_row_groups"] == 4 and cfg["steady_row_groups"] == 4
+    run_pair(p, 24, f"rows-edges-P{P}")
