@@ -163,3 +163,19 @@ def test_row_groups_on_empty_and_short_sessions(P):
     cfg = p.md.kernel_config()
     assert cfg["first_row_groups"] == 4 and cfg["steady_row_groups"] == 4
     run_pair(p, 24, f"rows-edges-P{P}")
+
+
+def test_row_groups_with_the_offload_tier():
+    # The offload tier observes its host-memory pages with the rows'
+    # normalisers of the step, which the leaders of every row group publish:
+    # three sessions of eight layers (16 rows, two groups), keys planted so
+    # that pages leave for host memory and come back; every step compared
+    # with the oracle, host-memory state included.
+    from test_gpu_parity import run_offload
+    w = C.with_overrides(C.get("small"), L=8, S=3, n0=None, n0_range=(1, 2), steps=40, system_len=60)
+    p = Pair(w, n0s=[450, 700, 300], budgets=[225, 300, 200], planted=24, planted_strength=2.5, query_gain=0.7,
+             fused=True, offload_pages=8, drop_threshold=1e-3)
+    cfg = p.md.kernel_config()
+    assert cfg["first_row_groups"] == 2 and cfg["steady_row_groups"] == 2
+    st = run_offload(p, 40, "rows-offload")
+    assert st.offloaded > 20 and st.recalled > 10
