@@ -307,12 +307,15 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
         gbytes base = uni_ptr(a.k_pool + e * kHeadDim);
         if constexpr (QT) {
             // a quantised block: codes in its first 2 KiB (rg[0], rg[1]), the
-            // scale at byte 2048 (rg[2], rg[3] the same)
+            // scale at byte 2048 (rg[2]); rg[3] takes the next 16 bytes of
+            // the same line, which the widening overwrites.  Two loads of
+            // one address would be merged into one and a register copy,
+            // and the copy of a load in flight waits for every load.
             const bool qt = (qmask >> u) & 1u;
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 rg[j] = __builtin_nontemporal_load(
-                    reinterpret_cast<gvec>(base + ((qt && j >= 2) ? 2048u : voff + 1024u * j)));
+                    reinterpret_cast<gvec>(base + ((qt && j >= 2) ? 2048u + 16u * (j - 2) : voff + 1024u * j)));
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
@@ -608,11 +611,12 @@ __device__ __forceinline__ void attend_wave(const AttendDims& dm, const AttendAr
                 qsc[u] = 1.0f;
                 if ((qmask >> u) & 1u) {
                     qsc[u] = __uint_as_float(__builtin_amdgcn_readfirstlane(ring[u][2][0]));
-                    const u32x4 c0 = ring[u][0], c1 = ring[u][1];
-                    ring[u][0] = codes_to_bf16<0>(c0);
-                    ring[u][1] = codes_to_bf16<1>(c0);
-                    ring[u][2] = codes_to_bf16<0>(c1);
-                    ring[u][3] = codes_to_bf16<1>(c1);
+                    // last slot first: each widened slot takes the place of
+                    // one whose contents are no longer needed
+                    ring[u][3] = codes_to_bf16<1>(ring[u][1]);
+                    ring[u][2] = codes_to_bf16<0>(ring[u][1]);
+                    ring[u][1] = codes_to_bf16<1>(ring[u][0]);
+                    ring[u][0] = codes_to_bf16<0>(ring[u][0]);
                 }
             }
         }
