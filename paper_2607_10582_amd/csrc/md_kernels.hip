@@ -595,12 +595,14 @@ __device__ __forceinline__ void load_tile(u32x4 (&a)[4], const LogitsDims& dm,
     gbytes base = uni_ptr(k_pool + tile * kHeadDim);
     if constexpr (QT) {
         // a quantised block: codes in its first 2 KiB (a[0], a[1]), the
-        // scale at byte 2048 (a[2], a[3] the same)
+        // scale at byte 2048 (a[2]; a[3] the next 16 bytes of that line:
+        // one address loaded twice becomes one load and a copy, and the copy
+        // waits for every load in flight)
         const bool qt = it.qmask & (1u << t);
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             a[j] = __builtin_nontemporal_load(
-                reinterpret_cast<gvec>(base + ((qt && j >= 2) ? 2048u : voff + 1024u * j)));
+                reinterpret_cast<gvec>(base + ((qt && j >= 2) ? 2048u + 16u * (j - 2) : voff + 1024u * j)));
     } else {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
